@@ -1,0 +1,516 @@
+"""Pins for the CPU oracle: each test checks it against something other than
+itself -- schoolbook arithmetic, closed forms, invariants, big-integer
+identities, float64 plaintext results -- so that a dropped term, a wrong sign
+or index, or a transposed operand anywhere in the oracle fails one of them.
+
+CPU only (no GPU marker)."""
+import numpy as np
+import pytest
+
+from oracle import ckks
+from paper_2608_21131_amd import gen
+
+
+# ----------------------------------------------------------------------------
+# helpers that are NOT the oracle's code: schoolbook / big-int definitions
+# ----------------------------------------------------------------------------
+def schoolbook_negacyclic(a, b, q):
+    """c = a*b mod (X^N + 1, q) by the O(N^2) definition with Python ints."""
+    n = len(a)
+    c = [0] * n
+    for i in range(n):
+        ai = int(a[i])
+        if ai == 0:
+            continue
+        for j in range(n):
+            k = i + j
+            v = ai * int(b[j])
+            if k < n:
+                c[k] += v
+            else:
+                c[k - n] -= v
+    return np.array([x % q for x in c], dtype=np.uint64)
+
+
+def small_primes_upto(m):
+    sieve = np.ones(m + 1, dtype=bool)
+    sieve[:2] = False
+    for i in range(2, int(m ** 0.5) + 1):
+        if sieve[i]:
+            sieve[i * i::i] = False
+    return np.nonzero(sieve)[0].astype(np.int64)
+
+
+_SMALL = None
+
+
+def trial_division_prime(p):
+    """Primality by trial division up to sqrt(p) (independent of Miller-Rabin)."""
+    global _SMALL
+    if _SMALL is None:
+        _SMALL = small_primes_upto(1 << 25)
+    lim = int(p ** 0.5) + 1
+    ds = _SMALL[_SMALL <= lim]
+    return not np.any(np.int64(p) % ds == 0)
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    """A tiny ring for schoolbook checks (N = 32)."""
+    par = ckks.Params(logn=5, L=3, K=1)
+    return par, ckks.Oracle(par)
+
+
+@pytest.fixture(scope="module")
+def small():
+    """A small ring for end-to-end checks (N = 1024, 3 + 1 primes)."""
+    par = ckks.Params(logn=10, L=3, K=1)
+    return par, ckks.Oracle(par)
+
+
+@pytest.fixture(scope="module")
+def small4():
+    """N = 2048 with 4 + 2 primes: two primes per digit."""
+    par = ckks.Params(logn=11, L=4, K=2)
+    return par, ckks.Oracle(par)
+
+
+def keyset(orc, s, steps, wid=0):
+    par = orc.par
+    keys = {}
+    for r in steps:
+        a = gen.uniform_residues(gen.rng(wid, gen.STREAM_KEY_A, r), par.primes, par.dnum, par.n)
+        e = gen.rounded_gaussian(gen.rng(wid, gen.STREAM_KEY_E, r), (par.dnum, par.n))
+        keys[r] = orc.keygen(s, r, a, e)
+    return keys
+
+
+def enc(orc, v, s, log_scale=40, wid=0):
+    par = orc.par
+    m = ckks.encode(v, par.n, log_scale)
+    a = gen.uniform_residues(gen.rng(wid, gen.STREAM_ENC_A), par.q, 1, par.n)[0]
+    e = gen.rounded_gaussian(gen.rng(wid, gen.STREAM_ENC_E), par.n)
+    return orc.encrypt(m, a, e, s)
+
+
+def dec(orc, ct, s, log_scale):
+    return ckks.decode_residues(orc.decrypt(ct, s), orc.par, log_scale)
+
+
+# ----------------------------------------------------------------------------
+# primes
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("logn,count", [(13, 4), (15, 10), (16, 15)])
+def test_primes_are_the_largest_ntt_primes_below_2_50(logn, count):
+    ps = ckks.find_primes(logn, count)
+    m = 2 << logn
+    assert ps == sorted(ps, reverse=True)
+    for p in ps:
+        assert p < (1 << 50) and p.bit_length() == 50
+        assert p % m == 1
+        assert trial_division_prime(p)
+    # nothing was skipped: every candidate 1 mod 2N above the smallest is either listed or composite
+    c = ((1 << 50) - 2) // m * m + 1
+    while c >= ps[-1]:
+        if c not in ps:
+            assert not trial_division_prime(c), c
+        c -= m
+
+
+def test_golden_primes_file():
+    """tests/golden/primes.txt (written by tests/golden/make_golden.py) matches."""
+    import os
+    path = os.path.join(os.path.dirname(__file__), "golden", "primes.txt")
+    rows = [ln.split() for ln in open(path) if ln.strip() and not ln.startswith("#")]
+    for row in rows:
+        logn, L, K = int(row[0]), int(row[1]), int(row[2])
+        ps = [int(x, 16) for x in row[3:]]
+        assert ps == ckks.find_primes(logn, L + K)
+
+
+# ----------------------------------------------------------------------------
+# ring arithmetic
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("logn", [3, 4, 5, 6])
+def test_ring_product_equals_schoolbook_negacyclic(logn):
+    par = ckks.Params(logn=logn, L=2, K=1)
+    orc = ckks.Oracle(par)
+    g = np.random.default_rng(logn)
+    for limb in range(3):
+        q = par.primes[limb]
+        a = g.integers(0, q, par.n, dtype=np.uint64)
+        b = g.integers(0, q, par.n, dtype=np.uint64)
+        assert np.array_equal(orc.polymul(limb, a, b), schoolbook_negacyclic(a, b, q))
+    # small signed polynomials: the RNS product, lifted by CRT, is the integer product
+    a = g.integers(-1000, 1000, par.n)
+    b = g.integers(-1000, 1000, par.n)
+    prod = [orc.polymul(t, np.mod(a, par.primes[t]).astype(np.uint64),
+                        np.mod(b, par.primes[t]).astype(np.uint64)) for t in range(2)]
+    lifted = ckks.crt_centered(np.stack(prod), par.primes[:2])
+    exact = np.zeros(par.n, dtype=object)
+    for i in range(par.n):
+        for j in range(par.n):
+            k = i + j
+            if k < par.n:
+                exact[k] += int(a[i]) * int(b[j])
+            else:
+                exact[k - par.n] -= int(a[i]) * int(b[j])
+    assert [int(x) for x in exact] == lifted
+
+
+def test_transform_is_evaluation_at_odd_powers(tiny):
+    par, orc = tiny
+    n = par.n
+    for limb in range(par.L + par.K):
+        q = par.primes[limb]
+        x = np.zeros(n, dtype=np.uint64)
+        x[1] = 1
+        A = orc.ntt(limb, x)  # A[j] = psi^{2j+1}
+        psi = int(A[0])
+        assert pow(psi, n, q) == q - 1  # primitive 2N-th root
+        for k in (0, 1, 3, n - 1):
+            mono = np.zeros(n, dtype=np.uint64)
+            mono[k] = 1
+            Ak = orc.ntt(limb, mono)
+            assert all(int(Ak[j]) == pow(psi, k * (2 * j + 1), q) for j in range(n))
+        r = np.random.default_rng(limb).integers(0, q, n, dtype=np.uint64)
+        assert np.array_equal(orc.intt(limb, orc.ntt(limb, r)), r)
+
+
+# ----------------------------------------------------------------------------
+# automorphisms
+# ----------------------------------------------------------------------------
+def test_automorphism_definition_and_homomorphism(tiny):
+    par, orc = tiny
+    n, q = par.n, par.primes[0]
+    g = np.random.default_rng(5)
+    a = g.integers(0, q, n, dtype=np.uint64)
+    b = g.integers(0, q, n, dtype=np.uint64)
+    for gal in (5, 25, 2 * n - 1, 3):
+        sa = orc.automorph(gal, a[None], [0])[0]
+        # definition: a(X^gal) reduced mod X^N + 1, written out with Python ints
+        ref = [0] * n
+        for j in range(n):
+            t = gal * j % (2 * n)
+            if t < n:
+                ref[t] = (ref[t] + int(a[j])) % q
+            else:
+                ref[t - n] = (ref[t - n] - int(a[j])) % q
+        assert [int(x) for x in sa] == ref
+        sb = orc.automorph(gal, b[None], [0])[0]
+        ab = schoolbook_negacyclic(a, b, q)
+        assert np.array_equal(orc.automorph(gal, ab[None], [0])[0], schoolbook_negacyclic(sa, sb, q))
+    # composition and the order of 5
+    s5 = orc.automorph(5, a[None], [0])
+    s25 = orc.automorph(25, a[None], [0])
+    assert np.array_equal(orc.automorph(5, s5, [0]), s25)
+    assert pow(5, n // 2, 2 * n) == 1
+    assert np.array_equal(orc.automorph(pow(5, n // 2, 2 * n), a[None], [0])[0], a)
+
+
+# ----------------------------------------------------------------------------
+# encoding
+# ----------------------------------------------------------------------------
+def test_encode_constant_vector_is_constant_polynomial():
+    n = 256
+    for c in (0.25, -0.7, 1.0):
+        m = ckks.encode(np.full(n // 2, c), n, 40)
+        assert m[0] == np.rint(c * 2 ** 40)
+        assert np.all(m[1:] == 0)
+
+
+@pytest.mark.parametrize("n", [16, 64, 512])
+def test_encode_fft_matches_defining_sum(n):
+    v = np.random.default_rng(n).standard_normal(n // 2)
+    fast = ckks.encode_real(v, n, 2.0 ** 40)
+    direct = ckks.encode_real_direct(v, n, 2.0 ** 40)
+    assert np.max(np.abs(fast - direct)) < 1e-3  # values are ~2^40: relative 1e-15
+
+
+def test_slot_product_is_ring_product():
+    """decode(encode(u) * encode(v)) / scale^2 = u * v  (canonical embedding is a ring map)."""
+    n = 64
+    g = np.random.default_rng(7)
+    u, v = g.standard_normal(n // 2), g.standard_normal(n // 2)
+    mu, mv = ckks.encode(u, n, 30), ckks.encode(v, n, 30)
+    prod = np.zeros(n, dtype=object)
+    for i in range(n):
+        for j in range(n):
+            k = i + j
+            t = int(mu[i]) * int(mv[j])
+            if k < n:
+                prod[k] += t
+            else:
+                prod[k - n] -= t
+    z = ckks.decode_coeffs(np.array([float(x) for x in prod]) / 2.0 ** 60, n)
+    assert np.max(np.abs(z.real - u * v)) < 1e-6
+    assert np.max(np.abs(z.imag)) < 1e-6
+
+
+def test_rotation_is_automorphism_by_power_of_5(small):
+    par, orc = small
+    n = par.n
+    v = np.random.default_rng(3).standard_normal(n // 2)
+    m = ckks.encode(v, n, 40)
+    res = ckks.to_residues(m, par.q)
+    for r in (1, 7, n // 4):
+        gal = ckks.galois_element(n, r)
+        rot = orc.automorph(gal, res, list(range(par.L)))
+        z = ckks.decode_residues(rot, par, 40)
+        assert np.max(np.abs(z - np.roll(v, -r))) < 1e-9
+
+
+def test_decode_encode_roundtrip():
+    n = 4096
+    v = np.random.default_rng(11).uniform(-1, 1, n // 2)
+    z = ckks.decode_coeffs(ckks.encode(v, n, 40).astype(np.float64) / 2.0 ** 40, n)
+    assert np.max(np.abs(z.real - v)) < n * 2.0 ** -41
+
+
+# ----------------------------------------------------------------------------
+# basis conversion
+# ----------------------------------------------------------------------------
+def test_modup_conv_is_lift_plus_small_multiple(small4):
+    """Conv_{D_i -> t}(x) = x + u * D_i (mod t) with one integer 0 <= u < |D_i| for all t."""
+    par, orc = small4
+    g = np.random.default_rng(17)
+    c1 = np.stack([g.integers(0, q, par.n, dtype=np.uint64) for q in par.q])
+    for i in range(par.dnum):
+        ext = orc.modup_digit(i, c1)
+        dig = par.digit(i)
+        D = 1
+        for t in dig:
+            D *= par.primes[t]
+        xs = ckks.crt_centered(c1[dig], [par.primes[t] for t in dig])
+        xs = [x % D for x in xs]  # canonical lift in [0, D)
+        for t in dig:
+            assert np.array_equal(ext[t], c1[t])
+        others = [t for t in range(par.L + par.K) if t not in dig]
+        for k in range(0, par.n, 97):
+            us = None
+            for t in others:
+                cand = {u for u in range(len(dig)) if (xs[k] + u * D) % par.primes[t] == int(ext[t, k])}
+                us = cand if us is None else us & cand
+            assert us, (i, k)
+
+
+def test_moddown_inverts_multiplication_by_P(small4):
+    par, orc = small4
+    g = np.random.default_rng(19)
+    x = np.stack([g.integers(0, q, par.n, dtype=np.uint64) for q in par.q])
+    P = par.P
+    y = np.stack([(x[t].astype(object) * P % par.primes[t]).astype(np.uint64) if t < par.L
+                  else np.zeros(par.n, dtype=np.uint64) for t in range(par.L + par.K)])
+    assert np.array_equal(orc.moddown(y), x)
+    # y = P x + e with 0 <= e < P  ->  ModDown(y) = x - u, 0 <= u < K
+    Q = par.Q
+    xi = ckks.crt_centered(x, par.q)
+    es = [int(v) for v in g.integers(0, 2 ** 62, par.n)]
+    es = [(e * 7919 + 12345) % P for e in es]
+    y = np.stack([np.array([(P * xi[k] + es[k]) % par.primes[t] for k in range(par.n)], dtype=np.uint64)
+                  for t in range(par.L + par.K)])
+    out = ckks.crt_centered(orc.moddown(y), par.q)
+    for k in range(par.n):
+        assert (xi[k] - out[k]) % Q in range(par.K), k
+
+
+# ----------------------------------------------------------------------------
+# encryption, key switching
+# ----------------------------------------------------------------------------
+def test_encrypt_decrypt_roundtrip(small):
+    par, orc = small
+    s = gen.ternary_secret(gen.rng(1, gen.STREAM_SECRET), par.n)
+    v = np.random.default_rng(2).uniform(-1, 1, par.slots)
+    ct = enc(orc, v, s, wid=1)
+    assert np.max(np.abs(dec(orc, ct, s, 40) - v)) < 1e-6
+    # decryption with the wrong key is garbage
+    s2 = gen.ternary_secret(gen.rng(2, gen.STREAM_SECRET), par.n)
+    assert np.max(np.abs(dec(orc, ct, s2, 40) - v)) > 1.0
+
+
+@pytest.mark.parametrize("which", ["small", "small4"])
+def test_rotation_decrypts_to_rolled_slots(which, request):
+    par, orc = request.getfixturevalue(which)
+    s = gen.ternary_secret(gen.rng(3, gen.STREAM_SECRET), par.n)
+    v = np.random.default_rng(4).uniform(-1, 1, par.slots)
+    ct = enc(orc, v, s, wid=3)
+    steps = [1, 2, 5, par.slots // 2]
+    keys = keyset(orc, s, steps, wid=3)
+    for r in steps:
+        z = dec(orc, orc.rotate(ct, r, keys[r]), s, 40)
+        assert np.max(np.abs(z - np.roll(v, -r))) < 1e-6, r
+    # composition
+    z = dec(orc, orc.rotate(orc.rotate(ct, 1, keys[1]), 5, keys[5]), s, 40)
+    assert np.max(np.abs(z - np.roll(v, -6))) < 1e-6
+    # rotation by the slot count is the identity automorphism
+    kS = keyset(orc, s, [par.slots], wid=3)
+    z = dec(orc, orc.rotate(ct, par.slots, kS[par.slots]), s, 40)
+    assert np.max(np.abs(z - v)) < 1e-6
+
+
+def test_key_inner_product_carries_P_times_rotated_c1(small4):
+    """u0 + u1*s = P * sigma(c1) * sigma(s) + sum_i sigma(ext_i) e_i   (mod P*Q),
+
+    where c1 is lifted to [0, Q) and the last term is bounded by
+    N * 19 * alpha * max(Q_i) * dnum; a wrong gadget, basis conversion or key
+    term leaves a residue of size ~P*Q instead."""
+    par, orc = small4
+    n = par.n
+    s = gen.ternary_secret(gen.rng(5, gen.STREAM_SECRET), n)
+    keys = keyset(orc, s, [3], wid=5)
+    g = np.random.default_rng(23)
+    c1 = np.stack([g.integers(0, q, n, dtype=np.uint64) for q in par.q])
+    u = orc.ks_inner(c1, 3, keys[3])
+    gal = ckks.galois_element(n, 3)
+    allp = list(range(par.L + par.K))
+    s_res = ckks.to_residues(s, par.primes)
+    ss = orc.automorph(gal, s_res, allp)
+    lhs = [(u[0, t].astype(object) + orc.polymul(t, u[1, t], s_res[t]).astype(object)) % par.primes[t]
+           for t in allp]
+    c1_int = [x % par.Q for x in ckks.crt_centered(c1, par.q)]
+    c1_res = np.stack([np.array([x % par.primes[t] for x in c1_int], dtype=np.uint64) for t in allp])
+    sc1 = orc.automorph(gal, c1_res, allp)
+    rhs = [(orc.polymul(t, sc1[t], ss[t]).astype(object) * (par.P % par.primes[t])) % par.primes[t]
+           for t in allp]
+    diff = np.stack([((lhs[t] - rhs[t]) % par.primes[t]).astype(np.uint64) for t in allp])
+    d_int = ckks.crt_centered(diff, par.primes)
+    qi_max = max(ckks._prod(par.primes[t] for t in par.digit(i)) for i in range(par.dnum))
+    bound = n * 19 * par.alpha * qi_max * par.dnum
+    assert max(abs(x) for x in d_int) < bound
+    assert max(abs(x) for x in d_int) > 0
+
+
+# ----------------------------------------------------------------------------
+# plaintext identities of the packings (float64, no encryption)
+# ----------------------------------------------------------------------------
+def test_layout_b_plaintext_identity():
+    S, d, B = 256, 32, 8
+    g = np.random.default_rng(29)
+    X = g.standard_normal((200, d))
+    q = g.standard_normal(d)
+    diags = ckks.diagonals(X, S, d)
+    pre = ckks.prerotate(diags, B)
+    qs = ckks.replicate(q, S)
+    out = np.zeros(S)
+    for gg in range(d // B):
+        acc = sum(pre[gg, b] * np.roll(qs, -b) for b in range(B))
+        out += np.roll(acc, -gg * B)
+    assert np.allclose(out[:200], X @ q, atol=1e-12)
+    assert np.allclose(out[200:], 0, atol=1e-12)
+
+
+def test_layout_a_plaintext_identity():
+    S, d = 256, 16
+    g = np.random.default_rng(31)
+    X = g.standard_normal((40, d))
+    q = g.standard_normal(d)
+    pts = ckks.pack_rows(X, S, d)
+    qs = ckks.replicate(q, S)
+    scores = []
+    for w in range(pts.shape[0]):
+        z = pts[w] * qs
+        for k in range(int(np.log2(d))):
+            z = z + np.roll(z, -(1 << k))
+        scores.extend(z[:: d])
+    assert np.allclose(np.array(scores)[:40], X @ q, atol=1e-12)
+
+
+def test_projection_plaintext_identity():
+    S, d_in, R, B = 2048, 64, 16, 4
+    g = np.random.default_rng(37)
+    W = g.standard_normal((d_in, R))
+    q = g.standard_normal(d_in)
+    e = ckks.projection_diagonals(W, S)
+    pre = ckks.prerotate(e, B)
+    qs = ckks.replicate(q, S)
+    z = np.zeros(S)
+    for gg in range(R // B):
+        acc = sum(pre[gg, b] * np.roll(qs, -b) for b in range(B))
+        z += np.roll(acc, -gg * B)
+    for k in range(int(np.log2(d_in // R))):
+        z = z + np.roll(z, -(R << k))
+    assert np.allclose(z, np.tile(W.T @ q, S // R), atol=1e-10)
+
+
+# ----------------------------------------------------------------------------
+# end to end: decrypted scores against float64 inner products
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("B", [1, 4, 16])
+def test_layout_b_scores_match_float64(small, B):
+    par, orc = small
+    d, rows = 16, 300
+    s = gen.ternary_secret(gen.rng(6, gen.STREAM_SECRET), par.n)
+    X = gen.gaussian_unit_rows(gen.rng(6, gen.STREAM_DB), rows, d)
+    q = gen.gaussian_unit_rows(gen.rng(6, gen.STREAM_QUERY), 1, d)[0]
+    ct = enc(orc, ckks.replicate(q, par.slots), s, wid=6)
+    keys = keyset(orc, s, ckks.steps_for_bsgs(d, B), wid=6)
+    qrot = orc.baby_rotations(ct, B, keys)
+    out = orc.bsgs_block(qrot, ckks.layout_b_pts(X, par, d, B), B, d // B, keys)
+    z = dec(orc, out, s, 80)
+    assert np.max(np.abs(z[:rows] - X @ q)) < 1e-4
+    assert np.max(np.abs(z[rows:])) < 1e-4
+
+
+def test_layout_b_zero_padding_is_exact_cosine(small):
+    """96-d vectors zero-padded to 128: the score is the 96-d cosine."""
+    par, orc = small
+    rows = 40
+    s = gen.ternary_secret(gen.rng(7, gen.STREAM_SECRET), par.n)
+    X = gen.gaussian_unit_rows(gen.rng(7, gen.STREAM_DB), rows, 96)
+    q = gen.gaussian_unit_rows(gen.rng(7, gen.STREAM_QUERY), 1, 96)[0]
+    qp = np.zeros(128)
+    qp[:96] = q
+    ct = enc(orc, ckks.replicate(qp, par.slots), s, wid=7)
+    B = 16
+    keys = keyset(orc, s, ckks.steps_for_bsgs(128, B), wid=7)
+    out = orc.bsgs_block(orc.baby_rotations(ct, B, keys), ckks.layout_b_pts(X, par, 128, B), B, 128 // B, keys)
+    z = dec(orc, out, s, 80)
+    cos = X @ q / (np.linalg.norm(X, axis=1) * np.linalg.norm(q))
+    assert np.max(np.abs(z[:rows] - cos)) < 1e-4
+
+
+def test_layout_a_scores_match_float64(small):
+    par, orc = small
+    d = 16
+    rows = 2 * par.slots // d + 5  # three plaintexts, last one ragged
+    s = gen.ternary_secret(gen.rng(8, gen.STREAM_SECRET), par.n)
+    X = gen.gaussian_unit_rows(gen.rng(8, gen.STREAM_DB), rows, d)
+    q = gen.gaussian_unit_rows(gen.rng(8, gen.STREAM_QUERY), 1, d)[0]
+    ct = enc(orc, ckks.replicate(q, par.slots), s, wid=8)
+    steps = [1 << k for k in range(4)]
+    keys = keyset(orc, s, steps, wid=8)
+    pts = ckks.pack_rows(X, par.slots, d)
+    scores = []
+    for w in range(pts.shape[0]):
+        pt = ckks.encode_residues(pts[w], par)
+        z = orc.rotate_sum(orc.mul_plain(ct, pt), 1, 4, keys)
+        scores.extend(dec(orc, z, s, 80)[::d])
+    assert np.max(np.abs(np.array(scores)[:rows] - X @ q)) < 1e-4
+
+
+def test_projection_then_scoring_with_norm_correction():
+    par = ckks.Params(logn=11, L=4, K=2)
+    orc = ckks.Oracle(par)
+    d_in, R, B, rows = 64, 16, 4, 100
+    s = gen.ternary_secret(gen.rng(9, gen.STREAM_SECRET), par.n)
+    W = gen.projection_matrix(gen.rng(9, gen.STREAM_W), d_in, R, var=1.0 / R)
+    q = gen.gaussian_unit_rows(gen.rng(9, gen.STREAM_QUERY), 1, d_in)[0]
+    Xr = gen.normalize_rows(gen.gaussian_unit_rows(gen.rng(9, gen.STREAM_DB), rows, d_in) @ W)
+    ct = enc(orc, ckks.replicate(q, par.slots), s, wid=9)
+    c = d_in // R
+    steps = sorted(set(ckks.steps_for_bsgs(R, B) + [R << k for k in range(int(np.log2(c)))]))
+    keys = keyset(orc, s, steps, wid=9)
+    # projection: hybrid diagonals, BSGS, one final fold
+    e = ckks.projection_diagonals(W, par.slots)
+    pre = ckks.prerotate(e, B)
+    wpts = np.stack([[ckks.encode_residues(pre[g, b], par) for b in range(B)] for g in range(R // B)])
+    z = orc.bsgs_block(orc.baby_rotations(ct, B, keys), wpts, B, R // B, keys)
+    z = orc.rotate_sum(z, R, int(np.log2(c)), keys)
+    qR = W.T @ q
+    assert np.max(np.abs(dec(orc, z, s, 80) - np.tile(qR, par.slots // R))) < 1e-4
+    # scoring the projected query (scale 2^120), then the client's norm correction
+    out = orc.bsgs_block(orc.baby_rotations(z, B, keys), ckks.layout_b_pts(Xr, par, R, B), B, R // B, keys)
+    raw = dec(orc, out, s, 120)[:rows]
+    assert np.max(np.abs(raw - Xr @ qR)) < 1e-4
+    cos = raw / np.linalg.norm(qR)
+    assert np.max(np.abs(cos - Xr @ qR / np.linalg.norm(qR))) < 1e-4
