@@ -1,0 +1,199 @@
+/*
+ * fa.h -- C ABI of libfa: encrypted nearest-neighbour scoring under RNS-CKKS
+ * on one AMD Instinct MI355X (gfx950).
+ *
+ * What it computes (paper: "Billion-Scale Nearest-Neighbor Search under Fully
+ * Homomorphic Encryption on a Single GPU, Balancing Leakage and Cost"):
+ *   - the server-side scorer: one slot-packed encrypted query against blocks
+ *     of up to N/2 plaintext candidate rows, each block stored as d diagonals
+ *     pre-rotated by their giant step (Section 2, "Measured prototype vs.
+ *     deployment" and "Reproducing this"; Section 3.1, "Detail");
+ *   - the encrypted rank reduction Enc(W^T q) by the diagonal method with one
+ *     final fold (Section 3.1, "How" and "Detail");
+ *   - the rotate-and-sum fold and the row-packed variant;
+ *   - client-side helpers for tests and benchmarks: key generation, secret-key
+ *     encryption, decryption, encoding and decoding (Section 2, "Setting").
+ *
+ * Scheme and conventions (shared with the documentation of every call):
+ *   N = 2^log_n ring degree, S = N/2 slots, L ciphertext primes, K special
+ *   primes, all 50-bit and congruent to 1 mod 2N: the L+K largest such primes
+ *   below 2^50, in descending order.  Hybrid key switching uses alpha = K
+ *   primes per digit and dnum = ceil(L/K) digits.  Slot j is the evaluation
+ *   at zeta^(5^j mod 2N), zeta = exp(i*pi/N); rotating by r rolls the slots
+ *   left by r (automorphism X -> X^(5^r)).  There is no rescaling: the scale
+ *   of a product is the product of the scales.
+ *
+ * Memory.  Ciphertext, plaintext and workspace buffers are caller-owned
+ * DEVICE memory (for example torch tensors), 8-byte words, 256-byte aligned:
+ *   ciphertext  2*L*N words  [c0 | c1], each [L][N]
+ *   plaintext     L*N words  [L][N]
+ * The word format and coefficient order inside the device buffers are private
+ * to the library (NTT form); fa_export_coeffs() returns the canonical form:
+ * coefficient order, residues in [0, q_i) as uint64.  Host arrays are marked
+ * "host".  The context owns its tables and rotation keys (device memory it
+ * allocates at fa_ctx_create / fa_keygen and frees at fa_ctx_destroy); the
+ * scoring calls allocate nothing.
+ *
+ * Streams.  Calls that take `stream` (a hipStream_t) only enqueue work on it
+ * and return; the caller synchronises.  Calls without `stream` are
+ * synchronous.
+ *
+ * Errors.  Every call returns FA_OK (0) or a negative FA_E_* code; all
+ * argument checks happen on the host before any launch, so a failed call has
+ * enqueued nothing.  fa_last_error() returns a message for the calling
+ * thread's most recent failure.  No C++ exception crosses this interface.
+ */
+#ifndef FA_H_
+#define FA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  FA_OK = 0,
+  FA_E_INVAL = -1, /* bad argument value (null pointer, out-of-range size)   */
+  FA_E_SHAPE = -2, /* sizes inconsistent with the context or with each other */
+  FA_E_NOKEY = -3, /* a rotation key the operation needs was never generated */
+  FA_E_NOMEM = -4, /* workspace too small, or a setup-time allocation failed */
+  FA_E_HIP = -5    /* HIP runtime / launch error                             */
+};
+
+enum { FA_LAYOUT_ROW = 0, FA_LAYOUT_DIAG = 1 };
+enum { FA_OP_SCORE = 0, FA_OP_PROJECT = 1, FA_OP_ROTATE_SUM = 2, FA_OP_ROTATE = 3 };
+
+typedef struct fa_ctx fa_ctx;
+
+typedef struct {
+  uint32_t log_n;     /* 10..16 */
+  uint32_t L;         /* ciphertext primes, 1..16 */
+  uint32_t K;         /* special primes, 1..4 (= primes per key-switch digit) */
+  uint32_t log_scale; /* default scale 2^log_scale used by fa_encode_db_block */
+} fa_params;
+
+/* ---- context ------------------------------------------------------------ */
+
+/* Create a context on the current HIP device: selects the primes, builds
+ * twiddle and basis-conversion tables on the device.  Returns FA_E_INVAL for
+ * parameters outside the ranges above, FA_E_NOMEM / FA_E_HIP on device
+ * failure.  *out is set only on success. */
+int fa_ctx_create(const fa_params* params, fa_ctx** out);
+void fa_ctx_destroy(fa_ctx* ctx);
+
+/* The L+K primes (host out[L+K]): q_0..q_{L-1}, then p_0..p_{K-1}. */
+int fa_ctx_primes(const fa_ctx* ctx, uint64_t* out);
+size_t fa_ct_words(const fa_ctx* ctx); /* 2*L*N */
+size_t fa_pt_words(const fa_ctx* ctx); /* L*N   */
+size_t fa_key_bytes(const fa_ctx* ctx); /* device bytes per rotation key */
+const char* fa_last_error(void);
+
+/* ---- keys and client-side operations (tests, benchmark set-up) ---------- */
+
+/* Rotation keys for left rotations by steps[0..n_steps-1] (1 <= step < S),
+ * switching from the automorphed secret sigma_{5^r}(s) back to s, with all
+ * randomness supplied by the caller (host arrays):
+ *   s  [N]                        ternary secret, entries in {-1, 0, 1}
+ *   a  [n_steps][dnum][L+K][N]    uniform residues, a[..][t][..] < prime t
+ *   e  [n_steps][dnum][N]         small noise integers
+ * Key digit i of step r: b_i = -a_i*s + e_i + (P*Qhat_i*[Qhat_i^-1]_{Q_i})*sigma(s)
+ * over every prime of Q u P.  Keys already present for a step are replaced.
+ * Synchronous; allocates the keys' device memory. */
+int fa_keygen(fa_ctx* ctx, const int64_t* s, const int32_t* steps, int n_steps, const uint64_t* a,
+              const int64_t* e);
+/* 1 if a key for left rotation by `step` exists, else 0. */
+int fa_has_key(const fa_ctx* ctx, int step);
+
+/* Secret-key encryption (the query is encrypted by its owner): host inputs
+ *   m [N] integer plaintext coefficients (|m| < 2^62), a [L][N] uniform
+ *   residues, e [N] noise; s is the secret given to fa_keygen (or set by
+ *   fa_set_secret).  Writes c1 = a, c0 = -a*s + e + m  into ct (device). */
+int fa_set_secret(fa_ctx* ctx, const int64_t* s);
+int fa_encrypt(fa_ctx* ctx, const int64_t* m, const uint64_t* a, const int64_t* e, void* ct, void* stream);
+/* m' = c0 + c1*s, coefficient form, host out [L][N] residues in [0, q_i).
+ * Synchronous with respect to `stream`. */
+int fa_decrypt(fa_ctx* ctx, const void* ct, uint64_t* out, void* stream);
+/* Canonical form of n_polys consecutive [L][N] polynomials of a device
+ * buffer (2 for a ciphertext, 1 for a plaintext): host out [n_polys][L][N]. */
+int fa_export_coeffs(fa_ctx* ctx, const void* buf, int n_polys, uint64_t* out, void* stream);
+/* Encode a real slot vector (host, n_slots <= S values, rest zero) to integer
+ * coefficients m_k = rint(2^log_scale * (2/N) * sum_j v_j cos(pi k 5^j / N))
+ * (round half to even, float64): host out [N]. */
+int fa_encode(const fa_ctx* ctx, const double* slots, int n_slots, int log_scale, int64_t* out);
+/* Decode decrypted residues (host [L][N], e.g. from fa_decrypt) at scale
+ * 2^log_scale into n_slots real slot values (host). */
+int fa_decode(const fa_ctx* ctx, const uint64_t* res, int log_scale, double* out, int n_slots);
+
+/* ---- server: enrollment ------------------------------------------------- */
+
+/* Encode a block of candidate rows (host float32 [n_rows][dim], dim <= d,
+ * zero-padded to d) into device plaintexts at scale 2^log_scale:
+ *   FA_LAYOUT_DIAG: n_rows <= S; d diagonals diag_j[i] = X[i][(i+j) mod d],
+ *     diagonal gB+b pre-rotated right by gB, stored g-major: pts[g*B+b];
+ *     d % baby_step == 0, d | S.  Writes d plaintexts.
+ *   FA_LAYOUT_ROW: rows packed S/d per plaintext, slot t*d+u = X[w*S/d+t][u];
+ *     writes ceil(n_rows / (S/d)) plaintexts (baby_step ignored).
+ * pts must hold that many plaintexts (L*N words each). */
+int fa_encode_db_block(fa_ctx* ctx, const float* rows, int n_rows, int dim, int d, int layout, int baby_step,
+                       void* pts, void* stream);
+/* Plaintexts from integer coefficients (host [n_pts][N], |c| < 2^62). */
+int fa_encode_db_block_int(fa_ctx* ctx, const int64_t* coeffs, int n_pts, void* pts, void* stream);
+
+/* ---- server: scoring ---------------------------------------------------- */
+
+/* Device workspace needed by an operation (bytes).  op = FA_OP_SCORE with
+ * layout FA_LAYOUT_DIAG: n_blocks, d, baby_step as passed to fa_score_block;
+ * FA_OP_PROJECT: n_blocks = 1, d = r; FA_OP_ROTATE_SUM / FA_OP_ROTATE: n_blocks
+ * = number of ciphertexts. */
+size_t fa_workspace_bytes(const fa_ctx* ctx, int op, int n_blocks, int d, int baby_step);
+
+/* Score one encrypted query q (device ciphertext, slot s = query[s mod d])
+ * against n_blocks resident blocks (device pointers blocks[0..n_blocks-1]).
+ *   FA_LAYOUT_DIAG (Section 3.1 diagonal method, baby step B = baby_step,
+ *   G = d/B giant steps): each block holds d pre-rotated plaintexts from
+ *   fa_encode_db_block; out receives n_blocks ciphertexts; slot i of output
+ *   b is <X_i, q> at the product scale.  Sequence: qrot_b = Rotate(q, b)
+ *   (b < B, one shared decomposition); acc_g = sum_b pt[g*B+b] * qrot_b;
+ *   out = acc_0 + sum_{g>=1} Rotate(acc_g, gB) with the key-switch products
+ *   of all g >= 1 summed over Q u P before one division by P per block.
+ *   Needs keys for steps 1..B-1 and g*B, 1 <= g < G.
+ *   FA_LAYOUT_ROW: n_blocks row-packed plaintexts; out[w] = q * pt_w (no
+ *   rotation; follow with fa_rotate_sum(first_shift=1, n_steps=log2 d)).
+ * ws: device workspace of ws_bytes >= fa_workspace_bytes(...). */
+int fa_score_block(fa_ctx* ctx, const void* q, const void* const* blocks, int n_blocks, int d, int layout,
+                   int baby_step, void* out, void* ws, size_t ws_bytes, void* stream);
+
+/* Encrypted projection q_R = W^T q (Section 3.1): q holds a d_in-periodic
+ * query, w_pts the r plaintexts of W's hybrid diagonals
+ * e_j[s] = W[(s+j) mod d_in][s mod r] (j < r), encoded by the caller as a
+ * FA_LAYOUT_DIAG block (pre-rotated, g-major, baby step B).  Runs the same
+ * baby-step/giant-step product, then folds: z += Rotate(z, r*2^k) for
+ * k < log2(d_in/r).  Output slot s = (W^T q)[s mod r].  Needs keys 1..B-1,
+ * g*B, and r*2^k. */
+int fa_project_ct(fa_ctx* ctx, const void* q, const void* w_pts, int d_in, int r, int baby_step, void* q_r,
+                  void* ws, size_t ws_bytes, void* stream);
+
+/* In place, for each of n_cts consecutive ciphertexts in cts:
+ * ct <- ct + Rotate(ct, first_shift * 2^k) for k = 0..n_steps-1. */
+int fa_rotate_sum(fa_ctx* ctx, void* cts, int n_cts, int first_shift, int n_steps, void* ws, size_t ws_bytes,
+                  void* stream);
+
+/* out = Rotate(ct, step) (one full key switch). */
+int fa_rotate(fa_ctx* ctx, const void* ct, int step, void* out, void* ws, size_t ws_bytes, void* stream);
+
+/* ---- measurement -------------------------------------------------------- */
+
+/* Phase timing of subsequent diagonal-layout fa_score_block calls with HIP
+ * events recorded on the call's stream (enable != 0 turns it on; adds no
+ * synchronisation).  fa_profile_read waits for the last profiled call and
+ * writes ms[0] baby rotations, ms[1] multiply-accumulate stream,
+ * ms[2] giant steps, ms[3] whole call; FA_E_INVAL if nothing was profiled. */
+int fa_profile(fa_ctx* ctx, int enable);
+int fa_profile_read(fa_ctx* ctx, double* ms);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FA_H_ */

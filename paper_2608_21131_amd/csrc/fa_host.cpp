@@ -1,0 +1,1053 @@
+// Host side of libfa: parameter set-up, the C ABI entry points and the
+// orchestration of the encrypted scoring path on the caller's stream.
+//
+// Paper: Section 2 ("Measured prototype vs. deployment", "Reproducing this")
+// for the block-of-n/2-rows-as-d-diagonals scorer; Section 3.1 ("How",
+// "Detail") for the diagonal matrix-vector method, baby-step/giant-step with
+// plaintext pre-rotation of the database, and the single final fold.
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <complex>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <thread>
+#include <vector>
+
+#include "fa_internal.h"
+
+using u64 = uint64_t;
+using u128 = unsigned __int128;
+
+// ---------------------------------------------------------------------------
+// errors
+// ---------------------------------------------------------------------------
+static thread_local std::string g_err;
+
+static int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+#define HIPCHK(x)                                                                  \
+  do {                                                                             \
+    hipError_t e_ = (x);                                                           \
+    if (e_ != hipSuccess) return fail(FA_E_HIP, "%s: %s", #x, hipGetErrorString(e_)); \
+  } while (0)
+
+static int check_launch(const char* what) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(FA_E_HIP, "%s: launch failed: %s", what, hipGetErrorString(e));
+  return FA_OK;
+}
+
+// ---------------------------------------------------------------------------
+// modular arithmetic on the host (table construction)
+// ---------------------------------------------------------------------------
+static u64 mulmod(u64 a, u64 b, u64 m) { return (u64)((u128)a * b % m); }
+static u64 powmod(u64 b, u64 e, u64 m) {
+  u64 r = 1 % m;
+  b %= m;
+  while (e) {
+    if (e & 1) r = mulmod(r, b, m);
+    b = mulmod(b, b, m);
+    e >>= 1;
+  }
+  return r;
+}
+static u64 invmod(u64 a, u64 p) { return powmod(a % p, p - 2, p); }  // p prime
+
+static bool is_prime(u64 n) {
+  if (n < 2) return false;
+  static const u64 bases[] = {2, 3, 5, 7, 11, 13, 17, 19, 23, 29, 31, 37};
+  for (u64 p : bases)
+    if (n % p == 0) return n == p;
+  u64 d = n - 1;
+  int r = 0;
+  while ((d & 1) == 0) {
+    d >>= 1;
+    ++r;
+  }
+  for (u64 a : bases) {
+    u64 x = powmod(a, d, n);
+    if (x == 1 || x == n - 1) continue;
+    bool comp = true;
+    for (int i = 1; i < r; ++i) {
+      x = mulmod(x, x, n);
+      if (x == n - 1) {
+        comp = false;
+        break;
+      }
+    }
+    if (comp) return false;
+  }
+  return true;
+}
+
+// The `count` largest primes below 2^50 that are 1 mod 2N, descending.
+static std::vector<u64> select_primes(int logn, int count) {
+  const u64 m = 2ull << logn;
+  u64 c = (((1ull << 50) - 2) / m) * m + 1;
+  std::vector<u64> out;
+  while ((int)out.size() < count && c > m) {
+    if (is_prime(c)) out.push_back(c);
+    c -= m;
+  }
+  return out;
+}
+
+// A primitive 2N-th root of unity mod q: x^((q-1)/2N) for the first odd x
+// giving an element whose N-th power is -1.
+static u64 primitive_root_2n(u64 q, int logn) {
+  const u64 n = 1ull << logn;
+  for (u64 x = 3;; x += 2) {
+    u64 y = powmod(x, (q - 1) / (2 * n), q);
+    if (powmod(y, n, q) == q - 1) return y;
+  }
+}
+
+static uint32_t bitrev(uint32_t x, int bits) {
+  uint32_t r = 0;
+  for (int i = 0; i < bits; ++i) {
+    r = (r << 1) | (x & 1);
+    x >>= 1;
+  }
+  return r;
+}
+
+static uint32_t galois(int n, long step) {
+  const long slots = n / 2;
+  long r = ((step % slots) + slots) % slots;
+  return (uint32_t)powmod(5, (u64)r, 2ull * n);
+}
+
+// ---------------------------------------------------------------------------
+// float64 encoding / decoding on the host (client and enrollment side)
+// ---------------------------------------------------------------------------
+namespace {
+using cplx = std::complex<double>;
+
+// in-place radix-2 FFT of length n; sign = -1: sum x_t e^{-2 pi i k t / n}, +1: e^{+...}
+void fft(std::vector<cplx>& a, int sign) {
+  const size_t n = a.size();
+  for (size_t i = 1, j = 0; i < n; ++i) {
+    size_t bit = n >> 1;
+    for (; j & bit; bit >>= 1) j ^= bit;
+    j ^= bit;
+    if (i < j) std::swap(a[i], a[j]);
+  }
+  std::vector<cplx> root(n / 2);
+  for (size_t k = 0; k < n / 2; ++k) {
+    const double ang = 2.0 * M_PI * (double)k / (double)n;
+    root[k] = cplx(std::cos(ang), sign * std::sin(ang));
+  }
+  for (size_t len = 2; len <= n; len <<= 1) {
+    const size_t step = n / len;
+    for (size_t s = 0; s < n; s += len)
+      for (size_t j = 0; j < len / 2; ++j) {
+        const cplx u = a[s + j], v = a[s + j + len / 2] * root[j * step];
+        a[s + j] = u + v;
+        a[s + j + len / 2] = u - v;
+      }
+  }
+}
+
+std::vector<u64> slot_exps(int n) {
+  std::vector<u64> e(n / 2);
+  u64 x = 1;
+  for (int j = 0; j < n / 2; ++j) {
+    e[j] = x;
+    x = x * 5 % (2ull * n);
+  }
+  return e;
+}
+
+// m_k = rint(scale * (2/N) sum_j v_j cos(pi k e_j / N)) via one length-N FFT:
+// sum_j v_j (w^{-k e_j} + w^{k e_j}) = w^{-k} sum_t Z_t e^{-2 pi i k t / N},
+// w = e^{i pi / N}, Z_t = v_j at t = (e_j - 1)/2 and t = (2N - e_j - 1)/2.
+void encode_one(int n, const std::vector<u64>& e, const double* v, int nv, double scale, int64_t* out) {
+  std::vector<cplx> z(n, cplx(0, 0));
+  for (int j = 0; j < nv; ++j) {
+    z[(e[j] - 1) / 2] = v[j];
+    z[(2 * (u64)n - e[j] - 1) / 2] = v[j];
+  }
+  fft(z, -1);
+  for (int k = 0; k < n; ++k) {
+    const double ang = -M_PI * (double)k / (double)n;
+    const double re = z[k].real() * std::cos(ang) - z[k].imag() * std::sin(ang);
+    out[k] = (int64_t)std::nearbyint(scale * re / (double)n);
+  }
+}
+
+template <class F>
+void parallel_for(int count, F f) {
+  int nt = (int)std::thread::hardware_concurrency();
+  nt = std::max(1, std::min(nt, 16));
+  nt = std::min(nt, count);
+  if (nt <= 1) {
+    for (int i = 0; i < count; ++i) f(i);
+    return;
+  }
+  std::vector<std::thread> th;
+  for (int w = 0; w < nt; ++w)
+    th.emplace_back([&, w]() {
+      for (int i = w; i < count; i += nt) f(i);
+    });
+  for (auto& t : th) t.join();
+}
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// context
+// ---------------------------------------------------------------------------
+template <class T>
+static int dev_alloc(T** p, size_t count) {
+  hipError_t e = hipMalloc((void**)p, count * sizeof(T));
+  if (e != hipSuccess) {
+    *p = nullptr;
+    return fail(FA_E_NOMEM, "hipMalloc(%zu bytes): %s", count * sizeof(T), hipGetErrorString(e));
+  }
+  return FA_OK;
+}
+
+extern "C" {
+
+const char* fa_last_error(void) { return g_err.c_str(); }
+
+void fa_ctx_destroy(fa_ctx* c) {
+  if (!c) return;
+  (void)hipFree(c->d_pr);
+  (void)hipFree(c->d_tw_fwd);
+  (void)hipFree(c->d_tw_inv);
+  (void)hipFree(c->d_mu_inv);
+  (void)hipFree(c->d_mu_hat);
+  (void)hipFree(c->d_md_inv);
+  (void)hipFree(c->d_md_hat);
+  (void)hipFree(c->d_s);
+  for (auto& kv : c->keys) (void)hipFree(kv.second);
+  for (auto& e : c->ev)
+    if (e) (void)hipEventDestroy(e);
+  delete c;
+}
+
+int fa_ctx_create(const fa_params* prm, fa_ctx** out) {
+  if (!prm || !out) return fail(FA_E_INVAL, "fa_ctx_create: null argument");
+  if (prm->log_n < 10 || prm->log_n > 16) return fail(FA_E_INVAL, "log_n must be in [10, 16], got %u", prm->log_n);
+  if (prm->L < 1 || prm->L > 16) return fail(FA_E_INVAL, "L must be in [1, 16], got %u", prm->L);
+  if (prm->K < 1 || prm->K > 4) return fail(FA_E_INVAL, "K must be in [1, 4], got %u", prm->K);
+  if (prm->log_scale < 1 || prm->log_scale > 60) return fail(FA_E_INVAL, "log_scale must be in [1, 60]");
+  fa_ctx* c = new (std::nothrow) fa_ctx();
+  if (!c) return fail(FA_E_NOMEM, "out of host memory");
+  c->logn = (int)prm->log_n;
+  c->n = 1 << c->logn;
+  c->L = (int)prm->L;
+  c->K = (int)prm->K;
+  c->np = c->L + c->K;
+  c->alpha = c->K;
+  c->dnum = (c->L + c->K - 1) / c->K;
+  c->log_scale = (int)prm->log_scale;
+  (void)hipGetDevice(&c->device);
+  c->primes = select_primes(c->logn, c->np);
+  if ((int)c->primes.size() != c->np) {
+    delete c;
+    return fail(FA_E_INVAL, "not enough 50-bit NTT primes");
+  }
+  const int n = c->n, np = c->np, L = c->L, K = c->K;
+  // P mod q_t, P^-1 mod q_t
+  c->p_mod_q.assign(L, 0);
+  std::vector<DevPrime> hp(np);
+  for (int t = 0; t < np; ++t) {
+    const u64 q = c->primes[t];
+    hp[t].q = (double)q;
+    hp[t].qinv = 1.0 / (double)q;
+    hp[t].ninv = (double)invmod((u64)n, q);
+    hp[t].pinv = 0.0;
+    hp[t].pmod = 0.0;
+    if (t < L) {
+      u64 pm = 1;
+      for (int k = 0; k < K; ++k) pm = mulmod(pm, c->primes[L + k] % q, q);
+      c->p_mod_q[t] = pm;
+      hp[t].pmod = (double)pm;
+      hp[t].pinv = (double)invmod(pm, q);
+    }
+  }
+  // twiddles psi^{brev(k)} and their inverses
+  std::vector<double> twf((size_t)np * n), twi((size_t)np * n);
+  c->psi.resize(np);
+  for (int t = 0; t < np; ++t) {
+    const u64 q = c->primes[t];
+    const u64 psi = primitive_root_2n(q, c->logn);
+    const u64 ipsi = invmod(psi, q);
+    c->psi[t] = psi;
+    std::vector<u64> pw(n), ipw(n);
+    u64 x = 1, y = 1;
+    for (int j = 0; j < n; ++j) {
+      pw[j] = x;
+      ipw[j] = y;
+      x = mulmod(x, psi, q);
+      y = mulmod(y, ipsi, q);
+    }
+    for (int k = 0; k < n; ++k) {
+      const uint32_t r = bitrev((uint32_t)k, c->logn);
+      twf[(size_t)t * n + k] = (double)pw[r];
+      twi[(size_t)t * n + k] = (double)ipw[r];
+    }
+  }
+  // basis-conversion constants: products of primes reduced prime by prime
+  std::vector<double> mu_inv((size_t)c->dnum * c->alpha, 0.0), mu_hat((size_t)c->dnum * c->alpha * np, 0.0);
+  for (int i = 0; i < c->dnum; ++i) {
+    const int lo = i * c->alpha, hi = std::min(lo + c->alpha, L);
+    for (int j = lo; j < hi; ++j) {
+      // (D_i / d_j) mod every prime t, and its inverse mod d_j
+      for (int t = 0; t < np; ++t) {
+        u64 v = 1;
+        for (int jj = lo; jj < hi; ++jj)
+          if (jj != j) v = mulmod(v, c->primes[jj] % c->primes[t], c->primes[t]);
+        mu_hat[((size_t)i * c->alpha + (j - lo)) * np + t] = (double)v;
+      }
+      u64 v = 1;
+      for (int jj = lo; jj < hi; ++jj)
+        if (jj != j) v = mulmod(v, c->primes[jj] % c->primes[j], c->primes[j]);
+      mu_inv[(size_t)i * c->alpha + (j - lo)] = (double)invmod(v, c->primes[j]);
+    }
+  }
+  std::vector<double> md_inv(K), md_hat((size_t)K * L);
+  for (int k = 0; k < K; ++k) {
+    const u64 pk = c->primes[L + k];
+    u64 v = 1;
+    for (int kk = 0; kk < K; ++kk)
+      if (kk != k) v = mulmod(v, c->primes[L + kk] % pk, pk);
+    md_inv[k] = (double)invmod(v, pk);
+    for (int t = 0; t < L; ++t) {
+      const u64 q = c->primes[t];
+      u64 w = 1;
+      for (int kk = 0; kk < K; ++kk)
+        if (kk != k) w = mulmod(w, c->primes[L + kk] % q, q);
+      md_hat[(size_t)k * L + t] = (double)w;
+    }
+  }
+  int rc;
+  if ((rc = dev_alloc(&c->d_pr, np)) || (rc = dev_alloc(&c->d_tw_fwd, (size_t)np * n)) ||
+      (rc = dev_alloc(&c->d_tw_inv, (size_t)np * n)) || (rc = dev_alloc(&c->d_mu_inv, mu_inv.size())) ||
+      (rc = dev_alloc(&c->d_mu_hat, mu_hat.size())) || (rc = dev_alloc(&c->d_md_inv, md_inv.size())) ||
+      (rc = dev_alloc(&c->d_md_hat, md_hat.size())) || (rc = dev_alloc(&c->d_s, (size_t)np * n))) {
+    fa_ctx_destroy(c);
+    return rc;
+  }
+  hipError_t e = hipSuccess;
+  e = e ? e : hipMemcpy(c->d_pr, hp.data(), np * sizeof(DevPrime), hipMemcpyHostToDevice);
+  e = e ? e : hipMemcpy(c->d_tw_fwd, twf.data(), twf.size() * 8, hipMemcpyHostToDevice);
+  e = e ? e : hipMemcpy(c->d_tw_inv, twi.data(), twi.size() * 8, hipMemcpyHostToDevice);
+  e = e ? e : hipMemcpy(c->d_mu_inv, mu_inv.data(), mu_inv.size() * 8, hipMemcpyHostToDevice);
+  e = e ? e : hipMemcpy(c->d_mu_hat, mu_hat.data(), mu_hat.size() * 8, hipMemcpyHostToDevice);
+  e = e ? e : hipMemcpy(c->d_md_inv, md_inv.data(), md_inv.size() * 8, hipMemcpyHostToDevice);
+  e = e ? e : hipMemcpy(c->d_md_hat, md_hat.data(), md_hat.size() * 8, hipMemcpyHostToDevice);
+  e = e ? e : hipMemset(c->d_s, 0, (size_t)np * n * 8);
+  if (e != hipSuccess) {
+    fa_ctx_destroy(c);
+    return fail(FA_E_HIP, "fa_ctx_create: %s", hipGetErrorString(e));
+  }
+  *out = c;
+  return FA_OK;
+}
+
+int fa_ctx_primes(const fa_ctx* c, uint64_t* out) {
+  if (!c || !out) return fail(FA_E_INVAL, "fa_ctx_primes: null argument");
+  std::copy(c->primes.begin(), c->primes.end(), out);
+  return FA_OK;
+}
+size_t fa_ct_words(const fa_ctx* c) { return c ? (size_t)2 * c->L * c->n : 0; }
+size_t fa_pt_words(const fa_ctx* c) { return c ? (size_t)c->L * c->n : 0; }
+size_t fa_key_bytes(const fa_ctx* c) { return c ? (size_t)c->dnum * 2 * c->np * c->n * 8 : 0; }
+
+// ---------------------------------------------------------------------------
+// secret, keys, encryption
+// ---------------------------------------------------------------------------
+int fa_set_secret(fa_ctx* c, const int64_t* s) {
+  if (!c || !s) return fail(FA_E_INVAL, "fa_set_secret: null argument");
+  for (int k = 0; k < c->n; ++k)
+    if (s[k] < -1 || s[k] > 1) return fail(FA_E_INVAL, "secret coefficient %d is not ternary", k);
+  int64_t* ds = nullptr;
+  int rc = dev_alloc(&ds, c->n);
+  if (rc) return rc;
+  HIPCHK(hipMemcpy(ds, s, (size_t)c->n * 8, hipMemcpyHostToDevice));
+  fa::int_to_res(c, ds, 1, c->np, c->d_s, 0);
+  fa::ntt_fwd_strided(c, c->d_s, c->n, c->np, c->np, 0, 0);
+  if ((rc = check_launch("fa_set_secret"))) return rc;
+  HIPCHK(hipDeviceSynchronize());
+  (void)hipFree(ds);
+  return FA_OK;
+}
+
+int fa_keygen(fa_ctx* c, const int64_t* s, const int32_t* steps, int n_steps, const uint64_t* a, const int64_t* e) {
+  if (!c || !s || (!steps && n_steps) || (!a && n_steps) || (!e && n_steps) || n_steps < 0)
+    return fail(FA_E_INVAL, "fa_keygen: bad argument");
+  for (int i = 0; i < n_steps; ++i)
+    if (steps[i] < 1 || steps[i] >= c->n / 2) return fail(FA_E_INVAL, "rotation step %d out of [1, N/2)", steps[i]);
+  int rc = fa_set_secret(c, s);
+  if (rc) return rc;
+  const size_t n = c->n, np = c->np, dnum = c->dnum;
+  const size_t key_words = dnum * 2 * np * n;
+  uint64_t* du = nullptr;
+  int64_t* de = nullptr;
+  double* den = nullptr;
+  if ((rc = dev_alloc(&du, dnum * np * n)) || (rc = dev_alloc(&de, dnum * n)) ||
+      (rc = dev_alloc(&den, dnum * np * n))) {
+    (void)hipFree(du);
+    (void)hipFree(de);
+    return rc;
+  }
+  for (int r = 0; r < n_steps; ++r) {
+    double* key = nullptr;
+    auto it = c->keys.find(steps[r]);
+    if (it != c->keys.end()) {
+      key = it->second;
+    } else {
+      if ((rc = dev_alloc(&key, key_words))) break;
+      c->keys[steps[r]] = key;
+    }
+    const uint64_t* ar = a + (size_t)r * dnum * np * n;
+    const int64_t* er = e + (size_t)r * dnum * n;
+    hipError_t he = hipMemcpy(du, ar, dnum * np * n * 8, hipMemcpyHostToDevice);
+    if (he == hipSuccess) he = hipMemcpy(de, er, dnum * n * 8, hipMemcpyHostToDevice);
+    if (he != hipSuccess) {
+      rc = fail(FA_E_HIP, "fa_keygen upload: %s", hipGetErrorString(he));
+      break;
+    }
+    // a part (digit i, slot 1) <- NTT(a_i); e residues -> NTT
+    for (size_t i = 0; i < dnum; ++i)
+      fa::u64_to_res(du + i * np * n, np * n, key + (i * 2 + 1) * np * n, 0);
+    for (size_t i = 0; i < dnum; ++i) fa::ntt_fwd_strided(c, key + (i * 2 + 1) * np * n, n, (int)np, (int)np, 0, 0);
+    fa::int_to_res(c, de, (int)dnum, (int)np, den, 0);
+    fa::ntt_fwd_strided(c, den, n, (int)(dnum * np), (int)np, 0, 0);
+    fa::keygen_combine(c, key, den, galois(c->n, steps[r]), 0);
+    if ((rc = check_launch("fa_keygen"))) break;
+    he = hipDeviceSynchronize();
+    if (he != hipSuccess) {
+      rc = fail(FA_E_HIP, "fa_keygen: %s", hipGetErrorString(he));
+      break;
+    }
+  }
+  (void)hipFree(du);
+  (void)hipFree(de);
+  (void)hipFree(den);
+  return rc;
+}
+
+int fa_has_key(const fa_ctx* c, int step) { return c && c->keys.count(step) ? 1 : 0; }
+
+int fa_encrypt(fa_ctx* c, const int64_t* m, const uint64_t* a, const int64_t* e, void* ct, void* stream) {
+  if (!c || !m || !a || !e || !ct) return fail(FA_E_INVAL, "fa_encrypt: null argument");
+  hipStream_t s = (hipStream_t)stream;
+  const size_t n = c->n, L = c->L;
+  for (size_t k = 0; k < n; ++k)
+    if (m[k] > (INT64_C(1) << 62) || m[k] < -(INT64_C(1) << 62) || e[k] > 1024 || e[k] < -1024)
+      return fail(FA_E_INVAL, "fa_encrypt: coefficient %zu out of range", k);
+  std::vector<int64_t> me(n);
+  for (size_t k = 0; k < n; ++k) me[k] = m[k] + e[k];
+  uint64_t* du = nullptr;
+  int64_t* dm = nullptr;
+  double* dv = nullptr;
+  int rc;
+  if ((rc = dev_alloc(&du, L * n)) || (rc = dev_alloc(&dm, n)) || (rc = dev_alloc(&dv, L * n))) {
+    (void)hipFree(du);
+    (void)hipFree(dm);
+    return rc;
+  }
+  double* dct = (double*)ct;
+  HIPCHK(hipMemcpyAsync(du, a, L * n * 8, hipMemcpyHostToDevice, s));
+  HIPCHK(hipMemcpyAsync(dm, me.data(), n * 8, hipMemcpyHostToDevice, s));
+  fa::u64_to_res(du, L * n, dct + L * n, s);
+  fa::ntt_fwd_strided(c, dct + L * n, n, (int)L, (int)L, 0, s);
+  fa::int_to_res(c, dm, 1, (int)L, dv, s);
+  fa::ntt_fwd_strided(c, dv, n, (int)L, (int)L, 0, s);
+  fa::enc_combine(c, dct, dv, s);
+  if ((rc = check_launch("fa_encrypt"))) return rc;
+  HIPCHK(hipStreamSynchronize(s));
+  (void)hipFree(du);
+  (void)hipFree(dm);
+  (void)hipFree(dv);
+  return FA_OK;
+}
+
+static int export_polys(fa_ctx* c, const double* src, int n_polys, uint64_t* out, hipStream_t s, bool decrypt) {
+  const size_t n = c->n, L = c->L;
+  const size_t words = (size_t)n_polys * L * n;
+  double* tmp = nullptr;
+  uint64_t* du = nullptr;
+  int rc;
+  if ((rc = dev_alloc(&tmp, words)) || (rc = dev_alloc(&du, words))) {
+    (void)hipFree(tmp);
+    return rc;
+  }
+  if (decrypt) {
+    fa::dec_combine(c, src, tmp, s);
+  } else {
+    HIPCHK(hipMemcpyAsync(tmp, src, words * 8, hipMemcpyDeviceToDevice, s));
+  }
+  fa::ntt_inv_strided(c, tmp, n, (int)(n_polys * L), (int)L, 0, s);
+  fa::res_to_u64(tmp, words, du, s);
+  if ((rc = check_launch("export"))) return rc;
+  HIPCHK(hipMemcpyAsync(out, du, words * 8, hipMemcpyDeviceToHost, s));
+  HIPCHK(hipStreamSynchronize(s));
+  (void)hipFree(tmp);
+  (void)hipFree(du);
+  return FA_OK;
+}
+
+int fa_decrypt(fa_ctx* c, const void* ct, uint64_t* out, void* stream) {
+  if (!c || !ct || !out) return fail(FA_E_INVAL, "fa_decrypt: null argument");
+  return export_polys(c, (const double*)ct, 1, out, (hipStream_t)stream, true);
+}
+
+int fa_export_coeffs(fa_ctx* c, const void* buf, int n_polys, uint64_t* out, void* stream) {
+  if (!c || !buf || !out || n_polys < 1) return fail(FA_E_INVAL, "fa_export_coeffs: bad argument");
+  return export_polys(c, (const double*)buf, n_polys, out, (hipStream_t)stream, false);
+}
+
+// ---------------------------------------------------------------------------
+// encoding
+// ---------------------------------------------------------------------------
+int fa_encode(const fa_ctx* c, const double* slots, int n_slots, int log_scale, int64_t* out) {
+  if (!c || !slots || !out) return fail(FA_E_INVAL, "fa_encode: null argument");
+  if (n_slots < 0 || n_slots > c->n / 2) return fail(FA_E_SHAPE, "fa_encode: n_slots %d > N/2", n_slots);
+  if (log_scale < 0 || log_scale > 61) return fail(FA_E_INVAL, "fa_encode: log_scale out of range");
+  std::vector<u64> e = slot_exps(c->n);
+  encode_one(c->n, e, slots, n_slots, std::ldexp(1.0, log_scale), out);
+  return FA_OK;
+}
+
+}  // extern "C"
+
+// centred CRT of L residues -> double, multi-word arithmetic (little endian)
+namespace {
+struct Crt {
+  int L, W;
+  std::vector<u64> Q, halfQ;             // [W]
+  std::vector<std::vector<u64>> qhat;    // [L][W]
+  std::vector<u64> qhat_inv;             // [L]
+  std::vector<u64> q;
+};
+int cmp(const u64* a, const u64* b, int W) {
+  for (int i = W - 1; i >= 0; --i)
+    if (a[i] != b[i]) return a[i] < b[i] ? -1 : 1;
+  return 0;
+}
+void sub_inplace(u64* a, const u64* b, int W) {
+  u64 borrow = 0;
+  for (int i = 0; i < W; ++i) {
+    const u128 d = (u128)a[i] - b[i] - borrow;
+    a[i] = (u64)d;
+    borrow = (u64)(d >> 64) ? 1 : 0;
+  }
+}
+void mul_small(std::vector<u64>& a, u64 m) {
+  u64 carry = 0;
+  for (auto& w : a) {
+    const u128 p = (u128)w * m + carry;
+    w = (u64)p;
+    carry = (u64)(p >> 64);
+  }
+  if (carry) a.push_back(carry);
+}
+Crt make_crt(const fa_ctx* c) {
+  Crt r;
+  r.L = c->L;
+  r.q.assign(c->primes.begin(), c->primes.begin() + c->L);
+  std::vector<u64> Q{1};
+  for (int t = 0; t < c->L; ++t) mul_small(Q, r.q[t]);
+  r.W = (int)Q.size() + 1;
+  Q.resize(r.W, 0);
+  r.Q = Q;
+  r.halfQ = Q;
+  u64 carry = 0;
+  for (int i = r.W - 1; i >= 0; --i) {
+    const u64 w = r.halfQ[i];
+    r.halfQ[i] = (w >> 1) | (carry << 63);
+    carry = w & 1;
+  }
+  r.qhat.resize(c->L);
+  r.qhat_inv.resize(c->L);
+  for (int t = 0; t < c->L; ++t) {
+    std::vector<u64> h{1};
+    u64 hm = 1;
+    for (int j = 0; j < c->L; ++j)
+      if (j != t) {
+        mul_small(h, r.q[j]);
+        hm = mulmod(hm, r.q[j] % r.q[t], r.q[t]);
+      }
+    h.resize(r.W, 0);
+    r.qhat[t] = h;
+    r.qhat_inv[t] = invmod(hm, r.q[t]);
+  }
+  return r;
+}
+double crt_to_double(const Crt& r, const uint64_t* res, size_t stride) {
+  std::vector<u64> acc(r.W + 1, 0);
+  for (int t = 0; t < r.L; ++t) {
+    const u64 y = mulmod(res[t * stride] % r.q[t], r.qhat_inv[t], r.q[t]);
+    u64 carry = 0;
+    for (int i = 0; i < r.W; ++i) {
+      const u128 p = (u128)r.qhat[t][i] * y + acc[i] + carry;
+      acc[i] = (u64)p;
+      carry = (u64)(p >> 64);
+    }
+    acc[r.W] += carry;
+  }
+  // reduce mod Q: acc < L * Q
+  while (acc[r.W] != 0 || cmp(acc.data(), r.Q.data(), r.W) >= 0) {
+    u64 borrow = 0;
+    for (int i = 0; i < r.W; ++i) {
+      const u128 d = (u128)acc[i] - r.Q[i] - borrow;
+      acc[i] = (u64)d;
+      borrow = (u64)(d >> 64) ? 1 : 0;
+    }
+    acc[r.W] -= borrow;
+  }
+  double sign = 1.0;
+  if (cmp(acc.data(), r.halfQ.data(), r.W) > 0) {
+    std::vector<u64> t = r.Q;
+    sub_inplace(t.data(), acc.data(), r.W);
+    std::copy(t.begin(), t.end(), acc.begin());
+    sign = -1.0;
+  }
+  double v = 0.0;
+  for (int i = r.W - 1; i >= 0; --i) v = v * 18446744073709551616.0 + (double)acc[i];
+  return sign * v;
+}
+}  // namespace
+
+extern "C" {
+
+int fa_decode(const fa_ctx* c, const uint64_t* res, int log_scale, double* out, int n_slots) {
+  if (!c || !res || !out) return fail(FA_E_INVAL, "fa_decode: null argument");
+  if (n_slots < 0 || n_slots > c->n / 2) return fail(FA_E_SHAPE, "fa_decode: n_slots %d > N/2", n_slots);
+  const int n = c->n;
+  Crt r = make_crt(c);
+  std::vector<double> m(n);
+  parallel_for(16, [&](int w) {
+    for (int k = w; k < n; k += 16) m[k] = crt_to_double(r, res + k, (size_t)n);
+  });
+  // z(2t+1) = sum_k m_k w^k e^{+2 pi i k t / N}
+  std::vector<cplx> y(n);
+  for (int k = 0; k < n; ++k) {
+    const double ang = M_PI * (double)k / (double)n;
+    y[k] = cplx(m[k] * std::cos(ang), m[k] * std::sin(ang));
+  }
+  fft(y, +1);
+  std::vector<u64> e = slot_exps(n);
+  const double inv_scale = std::ldexp(1.0, -log_scale);
+  for (int j = 0; j < n_slots; ++j) out[j] = y[(e[j] - 1) / 2].real() * inv_scale;
+  return FA_OK;
+}
+
+// Plaintexts from integer coefficients: residues then forward NTT.
+static int upload_int_pts(fa_ctx* c, const int64_t* coeffs, int n_pts, double* pts, hipStream_t s) {
+  const size_t n = c->n, L = c->L;
+  const int chunk = 64;
+  int64_t* dm = nullptr;
+  int rc = dev_alloc(&dm, (size_t)chunk * n);
+  if (rc) return rc;
+  for (int p0 = 0; p0 < n_pts; p0 += chunk) {
+    const int m = std::min(chunk, n_pts - p0);
+    HIPCHK(hipMemcpyAsync(dm, coeffs + (size_t)p0 * n, (size_t)m * n * 8, hipMemcpyHostToDevice, s));
+    double* dst = pts + (size_t)p0 * L * n;
+    fa::int_to_res(c, dm, m, (int)L, dst, s);
+    fa::ntt_fwd_strided(c, dst, n, m * (int)L, (int)L, 0, s);
+    if ((rc = check_launch("encode"))) break;
+    HIPCHK(hipStreamSynchronize(s));
+  }
+  (void)hipFree(dm);
+  return rc;
+}
+
+int fa_encode_db_block_int(fa_ctx* c, const int64_t* coeffs, int n_pts, void* pts, void* stream) {
+  if (!c || !coeffs || !pts || n_pts < 1) return fail(FA_E_INVAL, "fa_encode_db_block_int: bad argument");
+  for (size_t i = 0; i < (size_t)n_pts * c->n; ++i)
+    if (coeffs[i] > (INT64_C(1) << 62) || coeffs[i] < -(INT64_C(1) << 62))
+      return fail(FA_E_INVAL, "fa_encode_db_block_int: coefficient out of range");
+  return upload_int_pts(c, coeffs, n_pts, (double*)pts, (hipStream_t)stream);
+}
+
+int fa_encode_db_block(fa_ctx* c, const float* rows, int n_rows, int dim, int d, int layout, int baby_step,
+                       void* pts, void* stream) {
+  if (!c || !rows || !pts) return fail(FA_E_INVAL, "fa_encode_db_block: null argument");
+  const int S = c->n / 2;
+  if (d < 1 || (d & (d - 1)) || d > S) return fail(FA_E_SHAPE, "d=%d must be a power of two <= N/2", d);
+  if (dim < 1 || dim > d) return fail(FA_E_SHAPE, "dim=%d must be in [1, d=%d]", dim, d);
+  if (n_rows < 1) return fail(FA_E_SHAPE, "n_rows must be positive");
+  std::vector<u64> e = slot_exps(c->n);
+  const double scale = std::ldexp(1.0, c->log_scale);
+  std::vector<int64_t> coeffs;
+  int n_pts;
+  if (layout == FA_LAYOUT_DIAG) {
+    if (n_rows > S) return fail(FA_E_SHAPE, "a diagonal block holds at most N/2=%d rows, got %d", S, n_rows);
+    if (baby_step < 1 || d % baby_step) return fail(FA_E_INVAL, "baby_step %d must divide d=%d", baby_step, d);
+    n_pts = d;
+    coeffs.assign((size_t)n_pts * c->n, 0);
+    parallel_for(n_pts, [&](int j) {
+      const int g = j / baby_step;
+      const int shift = g * baby_step;  // pre-rotation right by gB
+      std::vector<double> v(S, 0.0);
+      for (int i = 0; i < n_rows; ++i) {
+        const int col = (i + j) % d;
+        const double x = col < dim ? (double)rows[(size_t)i * dim + col] : 0.0;
+        v[(i + shift) % S] = x;
+      }
+      encode_one(c->n, e, v.data(), S, scale, coeffs.data() + (size_t)j * c->n);
+    });
+  } else if (layout == FA_LAYOUT_ROW) {
+    const int per = S / d;
+    n_pts = (n_rows + per - 1) / per;
+    coeffs.assign((size_t)n_pts * c->n, 0);
+    parallel_for(n_pts, [&](int w) {
+      std::vector<double> v(S, 0.0);
+      for (int t = 0; t < per; ++t) {
+        const int row = w * per + t;
+        if (row >= n_rows) break;
+        for (int u = 0; u < dim; ++u) v[(size_t)t * d + u] = rows[(size_t)row * dim + u];
+      }
+      encode_one(c->n, e, v.data(), S, scale, coeffs.data() + (size_t)w * c->n);
+    });
+  } else {
+    return fail(FA_E_INVAL, "unknown layout %d", layout);
+  }
+  return upload_int_pts(c, coeffs.data(), n_pts, (double*)pts, (hipStream_t)stream);
+}
+
+// ---------------------------------------------------------------------------
+// workspace carving
+// ---------------------------------------------------------------------------
+}  // extern "C"
+
+namespace {
+constexpr int kRotBatch = 8;  // rotations key-switched per launch group
+
+struct Arena {
+  char* base;
+  size_t cap, used;
+  double* take(size_t words) {
+    const size_t bytes = (words * 8 + 255) & ~(size_t)255;
+    if (used + bytes > cap) return nullptr;
+    double* p = (double*)(base + used);
+    used += bytes;
+    return p;
+  }
+};
+size_t rup(size_t words) { return (words * 8 + 255) & ~(size_t)255; }
+
+// workspace of a batch of `nb` full rotations (own ModUp each)
+size_t rotate_ws(const fa_ctx* c, int nb) {
+  const size_t n = c->n;
+  return (size_t)nb * (rup(c->L * n) + rup((size_t)c->dnum * c->np * n) + rup(2 * (size_t)c->np * n) +
+                       rup(2 * (size_t)c->L * n));
+}
+
+size_t score_ws(const fa_ctx* c, int nb, int d, int B) {
+  const size_t n = c->n, L = c->L, np = c->np, dn = c->dnum;
+  const int G = d / B;
+  const int rb = std::max(1, std::min(kRotBatch, B - 1));
+  size_t w = 0;
+  w += rup(L * n);                         // c1 in coefficient form
+  w += rup(dn * np * n);                   // extended digits of q
+  w += (size_t)rb * rup(2 * np * n);       // key-switch products
+  w += (size_t)rb * rup(2 * L * n);        // ModDown conversions
+  w += (size_t)B * rup(2 * L * n);         // baby rotations
+  w += (size_t)nb * G * rup(2 * L * n);    // accumulators
+  w += (size_t)nb * rup(dn * np * n);      // giant-step extended digits
+  w += (size_t)nb * rup(2 * np * n);       // giant-step key-switch sums
+  w += (size_t)nb * rup(2 * L * n);        // giant-step ModDown conversions
+  return w;
+}
+}  // namespace
+
+// Hoisted rotations of one ciphertext q by steps[0..m-1]: one decomposition of
+// c1 shared by all, each rotation with its own key switch and ModDown.
+// ext must already hold the extended digits of q.c1 (NTT form).
+static int rotations_from_ext(fa_ctx* c, const double* q, const double* ext, const int* steps, int m,
+                              double* const* outs, double* u, double* conv, hipStream_t s) {
+  const size_t n = c->n, L = c->L, np = c->np, K = c->K;
+  for (int r0 = 0; r0 < m; r0 += kRotBatch) {
+    const int rb = std::min(kRotBatch, m - r0);
+    fa::KsItem ks[kRotBatch];
+    fa::FinishItem fin[kRotBatch];
+    for (int j = 0; j < rb; ++j) {
+      auto it = c->keys.find(steps[r0 + j]);
+      if (it == c->keys.end()) return fail(FA_E_NOKEY, "no rotation key for step %d", steps[r0 + j]);
+      ks[j] = {ext, it->second, u + (size_t)j * 2 * np * n, galois(c->n, steps[r0 + j])};
+      fin[j] = {u + (size_t)j * 2 * np * n, conv + (size_t)j * 2 * L * n, q, nullptr, outs[r0 + j], ks[j].gal};
+    }
+    fa::ks_inner(c, ks, rb, false, s);
+    // ModDown: special-prime limbs to coefficient form, convert, back to NTT
+    for (int j = 0; j < rb; ++j)
+      for (int h = 0; h < 2; ++h)
+        fa::ntt_inv_strided(c, u + ((size_t)j * 2 + h) * np * n + L * n, n, (int)K, (int)K, (int)L, s);
+    fa::conv_moddown(c, u + L * n, np * n, conv, L * n, 2 * rb, s);
+    fa::ntt_fwd_strided(c, conv, n, (int)(2 * rb * L), (int)L, 0, s);
+    fa::moddown_finish(c, fin, rb, s);
+  }
+  return check_launch("rotation");
+}
+
+// extended digits (NTT form) of the c1 of `batch` ciphertexts cts + b * ct_stride
+static void modup(fa_ctx* c, const double* cts, size_t ct_stride, int batch, double* c1c, size_t c1c_stride,
+                  double* ext, size_t ext_stride, hipStream_t s) {
+  const size_t n = c->n, L = c->L;
+  for (int b = 0; b < batch; ++b)
+    (void)hipMemcpyAsync(c1c + (size_t)b * c1c_stride, cts + (size_t)b * ct_stride + L * n, L * n * 8,
+                   hipMemcpyDeviceToDevice, s);
+  fa::scatter_own(c, cts + L * n, ct_stride, ext, ext_stride, batch, s);
+  for (int b = 0; b < batch; ++b) fa::ntt_inv_strided(c, c1c + (size_t)b * c1c_stride, n, (int)L, (int)L, 0, s);
+  fa::conv_modup(c, c1c, c1c_stride, ext, ext_stride, batch, s);
+  fa::ntt_fwd_ext(c, ext, ext_stride, batch, s);
+}
+
+// Full rotation of `nb` ciphertexts by the same step: outs[b] = Rotate(cts[b], step).
+static int rotate_batch(fa_ctx* c, const double* cts, int nb, int step, double* outs, Arena& ar, hipStream_t s) {
+  const size_t n = c->n, L = c->L, np = c->np, dn = c->dnum;
+  auto it = c->keys.find(step);
+  if (it == c->keys.end()) return fail(FA_E_NOKEY, "no rotation key for step %d", step);
+  const size_t mark = ar.used;
+  double* c1c = ar.take((size_t)nb * L * n);
+  double* ext = ar.take((size_t)nb * dn * np * n);
+  double* u = ar.take((size_t)nb * 2 * np * n);
+  double* conv = ar.take((size_t)nb * 2 * L * n);
+  if (!c1c || !ext || !u || !conv) return fail(FA_E_NOMEM, "workspace too small for rotation");
+  const size_t ctw = 2 * L * n;
+  modup(c, cts, ctw, nb, c1c, L * n, ext, dn * np * n, s);
+  std::vector<fa::KsItem> ks(nb);
+  std::vector<fa::FinishItem> fin(nb);
+  const uint32_t gal = galois(c->n, step);
+  for (int b = 0; b < nb; ++b) {
+    ks[b] = {ext + (size_t)b * dn * np * n, it->second, u + (size_t)b * 2 * np * n, gal};
+    fin[b] = {u + (size_t)b * 2 * np * n, conv + (size_t)b * 2 * L * n, cts + (size_t)b * ctw, nullptr,
+              outs + (size_t)b * ctw, gal};
+  }
+  fa::ks_inner(c, ks.data(), nb, false, s);
+  for (int b = 0; b < nb; ++b)
+    for (int h = 0; h < 2; ++h)
+      fa::ntt_inv_strided(c, u + ((size_t)b * 2 + h) * np * n + L * n, n, c->K, c->K, (int)L, s);
+  fa::conv_moddown(c, u + L * n, np * n, conv, L * n, 2 * nb, s);
+  fa::ntt_fwd_strided(c, conv, n, (int)(2 * nb * L), (int)L, 0, s);
+  fa::moddown_finish(c, fin.data(), nb, s);
+  ar.used = mark;
+  return check_launch("rotate_batch");
+}
+
+// Diagonal-layout scoring (baby-step / giant-step) of q against nb blocks.
+static int score_diag(fa_ctx* c, const double* q, const double* const* blocks, int nb, int d, int B, double* out,
+                      Arena& ar, hipStream_t s) {
+  const size_t n = c->n, L = c->L, np = c->np, dn = c->dnum;
+  const int G = d / B;
+  const size_t ctw = 2 * L * n;
+  const int rb = std::max(1, std::min(kRotBatch, B - 1));
+  double* c1c = ar.take(L * n);
+  double* ext = ar.take(dn * np * n);
+  double* u = ar.take((size_t)rb * 2 * np * n);
+  double* conv = ar.take((size_t)rb * 2 * L * n);
+  double* qrot = ar.take((size_t)B * ctw);
+  double* acc = ar.take((size_t)nb * G * ctw);
+  double* gext = ar.take((size_t)nb * dn * np * n);
+  double* usum = ar.take((size_t)nb * 2 * np * n);
+  double* gconv = ar.take((size_t)nb * 2 * L * n);
+  if (!gconv) return fail(FA_E_NOMEM, "workspace too small for score_block");
+  for (int b = 1; b < B; ++b)
+    if (!c->keys.count(b)) return fail(FA_E_NOKEY, "no rotation key for baby step %d", b);
+  for (int g = 1; g < G; ++g)
+    if (!c->keys.count(g * B)) return fail(FA_E_NOKEY, "no rotation key for giant step %d", g * B);
+
+  if (c->prof) HIPCHK(hipEventRecord(c->ev[0], s));
+  // 1. baby rotations of the query, one shared decomposition
+  HIPCHK(hipMemcpyAsync(qrot, q, ctw * 8, hipMemcpyDeviceToDevice, s));
+  if (B > 1) {
+    modup(c, q, ctw, 1, c1c, L * n, ext, dn * np * n, s);
+    std::vector<int> steps(B - 1);
+    std::vector<double*> outs(B - 1);
+    for (int b = 1; b < B; ++b) {
+      steps[b - 1] = b;
+      outs[b - 1] = qrot + (size_t)b * ctw;
+    }
+    int rc = rotations_from_ext(c, q, ext, steps.data(), B - 1, outs.data(), u, conv, s);
+    if (rc) return rc;
+  }
+  if (c->prof) HIPCHK(hipEventRecord(c->ev[1], s));
+  // 2. multiply-accumulate against the resident plaintexts
+  fa::mac_diag(c, qrot, blocks, nb, B, G, acc, s);
+  if (c->prof) HIPCHK(hipEventRecord(c->ev[2], s));
+  // 3. giant steps: Rotate(acc_g, gB) summed over Q u P, one ModDown per block
+  for (int blk = 0; blk < nb; ++blk)
+    HIPCHK(hipMemcpyAsync(out + (size_t)blk * ctw, acc + (size_t)blk * G * ctw, ctw * 8, hipMemcpyDeviceToDevice, s));
+  if (G > 1) {
+    const size_t astride = (size_t)G * ctw;
+    for (int g = 1; g < G; ++g) {
+      const double* accg = acc + (size_t)g * ctw;
+      // decompose acc_g.c1 of every block (in place: acc_g.c1 is not needed afterwards)
+      fa::scatter_own(c, accg + L * n, astride, gext, dn * np * n, nb, s);
+      for (int blk = 0; blk < nb; ++blk)
+        fa::ntt_inv_strided(c, (double*)accg + (size_t)blk * astride + L * n, n, (int)L, (int)L, 0, s);
+      fa::conv_modup(c, accg + L * n, astride, gext, dn * np * n, nb, s);
+      fa::ntt_fwd_ext(c, gext, dn * np * n, nb, s);
+      std::vector<fa::KsItem> ks(nb);
+      const uint32_t gal = galois(c->n, g * B);
+      for (int blk = 0; blk < nb; ++blk)
+        ks[blk] = {gext + (size_t)blk * dn * np * n, c->keys[g * B], usum + (size_t)blk * 2 * np * n, gal};
+      fa::ks_inner(c, ks.data(), nb, g > 1, s);
+      for (int blk = 0; blk < nb; ++blk)
+        fa::add_automorph(c, out + (size_t)blk * ctw, accg + (size_t)blk * astride, 1, gal, s);
+    }
+    for (int blk = 0; blk < nb; ++blk)
+      for (int h = 0; h < 2; ++h)
+        fa::ntt_inv_strided(c, usum + ((size_t)blk * 2 + h) * np * n + L * n, n, c->K, c->K, (int)L, s);
+    fa::conv_moddown(c, usum + L * n, np * n, gconv, L * n, 2 * nb, s);
+    fa::ntt_fwd_strided(c, gconv, n, (int)(2 * nb * L), (int)L, 0, s);
+    std::vector<fa::FinishItem> fin(nb);
+    for (int blk = 0; blk < nb; ++blk) {
+      double* o = out + (size_t)blk * ctw;
+      fin[blk] = {usum + (size_t)blk * 2 * np * n, gconv + (size_t)blk * 2 * L * n, o,
+                  acc + (size_t)blk * G * ctw + L * n, o, 1u};
+    }
+    fa::moddown_finish(c, fin.data(), nb, s);
+  }
+  if (c->prof) {
+    HIPCHK(hipEventRecord(c->ev[3], s));
+    c->prof_done = true;
+  }
+  return check_launch("score_block");
+}
+
+extern "C" {
+
+size_t fa_workspace_bytes(const fa_ctx* c, int op, int n_blocks, int d, int baby_step) {
+  if (!c) return 0;
+  switch (op) {
+    case FA_OP_SCORE:
+      if (baby_step < 1 || d < baby_step) return 0;
+      return score_ws(c, std::max(1, n_blocks), d, baby_step);
+    case FA_OP_PROJECT:
+      if (baby_step < 1 || d < baby_step) return 0;
+      return std::max(score_ws(c, 1, d, baby_step), rotate_ws(c, 1));
+    case FA_OP_ROTATE_SUM:
+    case FA_OP_ROTATE:
+      return rotate_ws(c, std::min(std::max(1, n_blocks), kRotBatch)) + rup(fa_ct_words(c) * kRotBatch);
+    default:
+      return 0;
+  }
+}
+
+int fa_score_block(fa_ctx* c, const void* q, const void* const* blocks, int n_blocks, int d, int layout,
+                   int baby_step, void* out, void* ws, size_t ws_bytes, void* stream) {
+  if (!c || !q || !blocks || !out) return fail(FA_E_INVAL, "fa_score_block: null argument");
+  if (n_blocks < 1) return fail(FA_E_SHAPE, "n_blocks must be positive");
+  for (int i = 0; i < n_blocks; ++i)
+    if (!blocks[i]) return fail(FA_E_INVAL, "block %d is null", i);
+  hipStream_t s = (hipStream_t)stream;
+  if (layout == FA_LAYOUT_ROW) {
+    fa::mul_plain(c, (const double*)q, (const double* const*)blocks, n_blocks, (double*)out, s);
+    return check_launch("fa_score_block(row)");
+  }
+  if (layout != FA_LAYOUT_DIAG) return fail(FA_E_INVAL, "unknown layout %d", layout);
+  const int S = c->n / 2;
+  if (d < 1 || (d & (d - 1)) || d > S) return fail(FA_E_SHAPE, "d=%d must be a power of two <= N/2", d);
+  if (baby_step < 1 || d % baby_step) return fail(FA_E_INVAL, "baby_step %d must divide d=%d", baby_step, d);
+  const size_t need = score_ws(c, n_blocks, d, baby_step);
+  if (!ws || ws_bytes < need) return fail(FA_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
+  Arena ar{(char*)ws, ws_bytes, 0};
+  return score_diag(c, (const double*)q, (const double* const*)blocks, n_blocks, d, baby_step, (double*)out, ar, s);
+}
+
+int fa_rotate(fa_ctx* c, const void* ct, int step, void* out, void* ws, size_t ws_bytes, void* stream) {
+  if (!c || !ct || !out) return fail(FA_E_INVAL, "fa_rotate: null argument");
+  if (step < 1 || step >= c->n / 2) return fail(FA_E_INVAL, "step %d out of [1, N/2)", step);
+  if (!c->keys.count(step)) return fail(FA_E_NOKEY, "no rotation key for step %d", step);
+  if (!ws || ws_bytes < rotate_ws(c, 1)) return fail(FA_E_NOMEM, "workspace too small for rotation");
+  Arena ar{(char*)ws, ws_bytes, 0};
+  return rotate_batch(c, (const double*)ct, 1, step, (double*)out, ar, (hipStream_t)stream);
+}
+
+int fa_rotate_sum(fa_ctx* c, void* cts, int n_cts, int first_shift, int n_steps, void* ws, size_t ws_bytes,
+                  void* stream) {
+  if (!c || !cts) return fail(FA_E_INVAL, "fa_rotate_sum: null argument");
+  if (n_cts < 1 || n_steps < 0 || first_shift < 1) return fail(FA_E_INVAL, "fa_rotate_sum: bad sizes");
+  for (int k = 0; k < n_steps; ++k) {
+    const long r = (long)first_shift << k;
+    if (r >= c->n / 2) return fail(FA_E_INVAL, "rotation %ld out of [1, N/2)", r);
+    if (!c->keys.count((int)r)) return fail(FA_E_NOKEY, "no rotation key for step %ld", r);
+  }
+  const size_t need = fa_workspace_bytes(c, FA_OP_ROTATE_SUM, n_cts, 0, 1);
+  if (!ws || ws_bytes < need) return fail(FA_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
+  hipStream_t s = (hipStream_t)stream;
+  const size_t ctw = fa_ct_words(c);
+  Arena ar{(char*)ws, ws_bytes, 0};
+  double* tmp = ar.take(ctw * kRotBatch);
+  double* base = (double*)cts;
+  for (int c0 = 0; c0 < n_cts; c0 += kRotBatch) {
+    const int nb = std::min(kRotBatch, n_cts - c0);
+    double* cur = base + (size_t)c0 * ctw;
+    for (int k = 0; k < n_steps; ++k) {
+      int rc = rotate_batch(c, cur, nb, first_shift << k, tmp, ar, s);
+      if (rc) return rc;
+      fa::add_automorph(c, cur, tmp, 2 * nb, 1u, s);
+    }
+  }
+  return check_launch("fa_rotate_sum");
+}
+
+int fa_profile(fa_ctx* c, int enable) {
+  if (!c) return fail(FA_E_INVAL, "fa_profile: null context");
+  if (enable && !c->ev[0])
+    for (auto& e : c->ev) HIPCHK(hipEventCreate(&e));
+  c->prof = enable != 0;
+  return FA_OK;
+}
+
+int fa_profile_read(fa_ctx* c, double* ms) {
+  if (!c || !ms) return fail(FA_E_INVAL, "fa_profile_read: null argument");
+  if (!c->prof_done) return fail(FA_E_INVAL, "fa_profile_read: no profiled call");
+  HIPCHK(hipEventSynchronize(c->ev[3]));
+  float t[4];
+  HIPCHK(hipEventElapsedTime(&t[0], c->ev[0], c->ev[1]));
+  HIPCHK(hipEventElapsedTime(&t[1], c->ev[1], c->ev[2]));
+  HIPCHK(hipEventElapsedTime(&t[2], c->ev[2], c->ev[3]));
+  HIPCHK(hipEventElapsedTime(&t[3], c->ev[0], c->ev[3]));
+  for (int i = 0; i < 4; ++i) ms[i] = t[i];
+  return FA_OK;
+}
+
+int fa_project_ct(fa_ctx* c, const void* q, const void* w_pts, int d_in, int r, int baby_step, void* q_r, void* ws,
+                  size_t ws_bytes, void* stream) {
+  if (!c || !q || !w_pts || !q_r) return fail(FA_E_INVAL, "fa_project_ct: null argument");
+  if (r < 1 || (r & (r - 1)) || d_in < r || d_in % r || ((d_in / r) & (d_in / r - 1)) || d_in > c->n / 2)
+    return fail(FA_E_SHAPE, "d_in=%d, r=%d: both powers of two with r <= d_in <= N/2", d_in, r);
+  if (baby_step < 1 || r % baby_step) return fail(FA_E_INVAL, "baby_step %d must divide r=%d", baby_step, r);
+  const size_t need = fa_workspace_bytes(c, FA_OP_PROJECT, 1, r, baby_step);
+  if (!ws || ws_bytes < need) return fail(FA_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
+  int steps = 0;
+  while ((r << steps) < d_in) ++steps;
+  for (int k = 0; k < steps; ++k)
+    if (!c->keys.count(r << k)) return fail(FA_E_NOKEY, "no rotation key for fold step %d", r << k);
+  hipStream_t s = (hipStream_t)stream;
+  Arena ar{(char*)ws, ws_bytes, 0};
+  const void* blocks[1] = {w_pts};
+  int rc = score_diag(c, (const double*)q, (const double* const*)blocks, 1, r, baby_step, (double*)q_r, ar, s);
+  if (rc) return rc;
+  for (int k = 0; k < steps; ++k) {
+    Arena ar2{(char*)ws, ws_bytes, 0};
+    double* tmp = ar2.take(fa_ct_words(c));
+    rc = rotate_batch(c, (const double*)q_r, 1, r << k, tmp, ar2, s);
+    if (rc) return rc;
+    fa::add_automorph(c, (double*)q_r, tmp, 2, 1u, s);
+  }
+  return check_launch("fa_project_ct");
+}
+
+}  // extern "C"

@@ -1,0 +1,274 @@
+"""Thin Python binding of libfa (the C ABI in include/fa.h).
+
+Argument marshalling only: every step of the encrypted scoring path runs in
+the library's HIP kernels.  PyTorch provides device memory (8-byte-word
+tensors) and the current HIP stream.  There is no fallback: if libfa.so is
+missing or no GPU is present, the calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+import torch  # noqa: F401  (load torch's HIP runtime before libfa so both share it)
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libfa.so")
+
+FA_OK, FA_E_INVAL, FA_E_SHAPE, FA_E_NOKEY, FA_E_NOMEM, FA_E_HIP = 0, -1, -2, -3, -4, -5
+LAYOUT_ROW, LAYOUT_DIAG = 0, 1
+OP_SCORE, OP_PROJECT, OP_ROTATE_SUM, OP_ROTATE = 0, 1, 2, 3
+
+_ERR_NAMES = {FA_E_INVAL: "FA_E_INVAL", FA_E_SHAPE: "FA_E_SHAPE", FA_E_NOKEY: "FA_E_NOKEY",
+              FA_E_NOMEM: "FA_E_NOMEM", FA_E_HIP: "FA_E_HIP"}
+
+
+class FaError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{_ERR_NAMES.get(code, code)}: {msg}")
+        self.code = code
+
+
+class _Params(ctypes.Structure):
+    _fields_ = [("log_n", ctypes.c_uint32), ("L", ctypes.c_uint32), ("K", ctypes.c_uint32),
+                ("log_scale", ctypes.c_uint32)]
+
+
+_vp = ctypes.c_void_p
+_u64p = ctypes.POINTER(ctypes.c_uint64)
+_i64p = ctypes.POINTER(ctypes.c_int64)
+_i32p = ctypes.POINTER(ctypes.c_int32)
+_f64p = ctypes.POINTER(ctypes.c_double)
+_f32p = ctypes.POINTER(ctypes.c_float)
+
+# name -> (restype, argtypes); mirrors include/fa.h
+SIGNATURES = {
+    "fa_ctx_create": (ctypes.c_int, [ctypes.POINTER(_Params), ctypes.POINTER(_vp)]),
+    "fa_ctx_destroy": (None, [_vp]),
+    "fa_ctx_primes": (ctypes.c_int, [_vp, _u64p]),
+    "fa_ct_words": (ctypes.c_size_t, [_vp]),
+    "fa_pt_words": (ctypes.c_size_t, [_vp]),
+    "fa_key_bytes": (ctypes.c_size_t, [_vp]),
+    "fa_last_error": (ctypes.c_char_p, []),
+    "fa_keygen": (ctypes.c_int, [_vp, _i64p, _i32p, ctypes.c_int, _u64p, _i64p]),
+    "fa_has_key": (ctypes.c_int, [_vp, ctypes.c_int]),
+    "fa_set_secret": (ctypes.c_int, [_vp, _i64p]),
+    "fa_encrypt": (ctypes.c_int, [_vp, _i64p, _u64p, _i64p, _vp, _vp]),
+    "fa_decrypt": (ctypes.c_int, [_vp, _vp, _u64p, _vp]),
+    "fa_export_coeffs": (ctypes.c_int, [_vp, _vp, ctypes.c_int, _u64p, _vp]),
+    "fa_encode": (ctypes.c_int, [_vp, _f64p, ctypes.c_int, ctypes.c_int, _i64p]),
+    "fa_decode": (ctypes.c_int, [_vp, _u64p, ctypes.c_int, _f64p, ctypes.c_int]),
+    "fa_encode_db_block": (ctypes.c_int, [_vp, _f32p, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                          ctypes.c_int, _vp, _vp]),
+    "fa_encode_db_block_int": (ctypes.c_int, [_vp, _i64p, ctypes.c_int, _vp, _vp]),
+    "fa_workspace_bytes": (ctypes.c_size_t, [_vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int]),
+    "fa_score_block": (ctypes.c_int, [_vp, _vp, ctypes.POINTER(_vp), ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                      ctypes.c_int, _vp, _vp, ctypes.c_size_t, _vp]),
+    "fa_project_ct": (ctypes.c_int, [_vp, _vp, _vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, _vp, _vp,
+                                     ctypes.c_size_t, _vp]),
+    "fa_rotate_sum": (ctypes.c_int, [_vp, _vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, _vp, ctypes.c_size_t,
+                                     _vp]),
+    "fa_rotate": (ctypes.c_int, [_vp, _vp, ctypes.c_int, _vp, _vp, ctypes.c_size_t, _vp]),
+    "fa_profile": (ctypes.c_int, [_vp, ctypes.c_int]),
+    "fa_profile_read": (ctypes.c_int, [_vp, _f64p]),
+}
+
+_LIB = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libfa.so and declare its signatures (raises if it was never built)."""
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    if not os.path.exists(path):
+        raise RuntimeError(f"libfa.so not built ({path}); run __graft_entry__.build()")
+    lib = ctypes.CDLL(path)
+    for name, (res, args) in SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _LIB = lib
+    return lib
+
+
+def _check(rc: int):
+    if rc != FA_OK:
+        raise FaError(rc, _LIB.fa_last_error().decode())
+
+
+def _np(a, dtype):
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def _ptr(a: np.ndarray, kind):
+    return a.ctypes.data_as(kind)
+
+
+def _stream(stream=None):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dev(t: torch.Tensor):
+    assert t.is_cuda and t.is_contiguous() and t.element_size() == 8
+    return ctypes.c_void_p(t.data_ptr())
+
+
+class Context:
+    """One parameter set (ring degree, primes, tables, rotation keys) on the current GPU."""
+
+    def __init__(self, log_n: int, L: int, K: int, log_scale: int = 40):
+        if not torch.cuda.is_available():
+            raise RuntimeError("libfa needs a HIP GPU; none is visible")
+        self.lib = load_library()
+        self.log_n, self.L, self.K, self.log_scale = log_n, L, K, log_scale
+        self.n = 1 << log_n
+        self.slots = self.n // 2
+        self.dnum = -(-L // K)
+        prm = _Params(log_n, L, K, log_scale)
+        h = _vp()
+        _check(self.lib.fa_ctx_create(ctypes.byref(prm), ctypes.byref(h)))
+        self.h = h
+        pr = np.zeros(L + K, dtype=np.uint64)
+        _check(self.lib.fa_ctx_primes(self.h, _ptr(pr, _u64p)))
+        self.primes = [int(x) for x in pr]
+        self.ct_words = int(self.lib.fa_ct_words(self.h))
+        self.pt_words = int(self.lib.fa_pt_words(self.h))
+
+    def close(self):
+        if getattr(self, "h", None):
+            self.lib.fa_ctx_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # ---- buffers ----
+    def new_ct(self, count: int = 1) -> torch.Tensor:
+        return torch.empty(count * self.ct_words, dtype=torch.float64, device="cuda")
+
+    def new_pt(self, count: int = 1) -> torch.Tensor:
+        return torch.empty(count * self.pt_words, dtype=torch.float64, device="cuda")
+
+    def workspace(self, op: int, n_blocks: int = 1, d: int = 1, baby_step: int = 1) -> torch.Tensor:
+        nbytes = int(self.lib.fa_workspace_bytes(self.h, op, n_blocks, d, baby_step))
+        return torch.empty(max(1, nbytes // 8 + 32), dtype=torch.float64, device="cuda")
+
+    def workspace_bytes(self, op: int, n_blocks: int = 1, d: int = 1, baby_step: int = 1) -> int:
+        return int(self.lib.fa_workspace_bytes(self.h, op, n_blocks, d, baby_step))
+
+    # ---- keys / client ----
+    def keygen(self, s, steps, a, e):
+        s = _np(s, np.int64)
+        steps = _np(steps, np.int32)
+        a = _np(a, np.uint64)
+        e = _np(e, np.int64)
+        assert a.size == len(steps) * self.dnum * (self.L + self.K) * self.n
+        assert e.size == len(steps) * self.dnum * self.n
+        _check(self.lib.fa_keygen(self.h, _ptr(s, _i64p), _ptr(steps, _i32p), len(steps), _ptr(a, _u64p),
+                                  _ptr(e, _i64p)))
+
+    def has_key(self, step: int) -> bool:
+        return bool(self.lib.fa_has_key(self.h, step))
+
+    def set_secret(self, s):
+        s = _np(s, np.int64)
+        _check(self.lib.fa_set_secret(self.h, _ptr(s, _i64p)))
+
+    def encrypt(self, m, a, e, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+        out = self.new_ct() if out is None else out
+        m, a, e = _np(m, np.int64), _np(a, np.uint64), _np(e, np.int64)
+        _check(self.lib.fa_encrypt(self.h, _ptr(m, _i64p), _ptr(a, _u64p), _ptr(e, _i64p), _dev(out),
+                                   _stream(stream)))
+        return out
+
+    def decrypt(self, ct: torch.Tensor, stream=None) -> np.ndarray:
+        out = np.empty((self.L, self.n), dtype=np.uint64)
+        _check(self.lib.fa_decrypt(self.h, _dev(ct), _ptr(out, _u64p), _stream(stream)))
+        return out
+
+    def export(self, buf: torch.Tensor, n_polys: int, stream=None) -> np.ndarray:
+        out = np.empty((n_polys, self.L, self.n), dtype=np.uint64)
+        _check(self.lib.fa_export_coeffs(self.h, _dev(buf), n_polys, _ptr(out, _u64p), _stream(stream)))
+        return out
+
+    def encode(self, slots, log_scale: int | None = None) -> np.ndarray:
+        v = _np(slots, np.float64)
+        out = np.empty(self.n, dtype=np.int64)
+        ls = self.log_scale if log_scale is None else log_scale
+        _check(self.lib.fa_encode(self.h, _ptr(v, _f64p), v.size, ls, _ptr(out, _i64p)))
+        return out
+
+    def decode(self, res, log_scale: int, n_slots: int | None = None) -> np.ndarray:
+        r = _np(res, np.uint64)
+        k = self.slots if n_slots is None else n_slots
+        out = np.empty(k, dtype=np.float64)
+        _check(self.lib.fa_decode(self.h, _ptr(r, _u64p), log_scale, _ptr(out, _f64p), k))
+        return out
+
+    # ---- enrollment ----
+    def encode_db_block(self, rows, d: int, layout: int, baby_step: int = 1,
+                        out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+        rows = _np(rows, np.float32)
+        n_rows, dim = rows.shape
+        n_pts = d if layout == LAYOUT_DIAG else -(-n_rows // (self.slots // d))
+        out = self.new_pt(n_pts) if out is None else out
+        _check(self.lib.fa_encode_db_block(self.h, _ptr(rows, _f32p), n_rows, dim, d, layout, baby_step,
+                                           _dev(out), _stream(stream)))
+        return out
+
+    def encode_db_block_int(self, coeffs, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+        c = _np(coeffs, np.int64).reshape(-1, self.n)
+        out = self.new_pt(c.shape[0]) if out is None else out
+        _check(self.lib.fa_encode_db_block_int(self.h, _ptr(c, _i64p), c.shape[0], _dev(out), _stream(stream)))
+        return out
+
+    # ---- scoring ----
+    def score_block(self, q: torch.Tensor, blocks, d: int, layout: int, baby_step: int = 1,
+                    out: torch.Tensor | None = None, ws: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+        blocks = list(blocks)
+        nb = len(blocks)
+        out = self.new_ct(nb) if out is None else out
+        if ws is None and layout == LAYOUT_DIAG:
+            ws = self.workspace(OP_SCORE, nb, d, baby_step)
+        arr = (_vp * nb)(*[ctypes.c_void_p(b.data_ptr()) for b in blocks])
+        ws_p, ws_b = (_dev(ws), ws.numel() * 8) if ws is not None else (ctypes.c_void_p(0), 0)
+        _check(self.lib.fa_score_block(self.h, _dev(q), arr, nb, d, layout, baby_step, _dev(out), ws_p, ws_b,
+                                       _stream(stream)))
+        return out
+
+    def project_ct(self, q: torch.Tensor, w_pts: torch.Tensor, d_in: int, r: int, baby_step: int,
+                   out: torch.Tensor | None = None, ws: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+        out = self.new_ct() if out is None else out
+        ws = self.workspace(OP_PROJECT, 1, r, baby_step) if ws is None else ws
+        _check(self.lib.fa_project_ct(self.h, _dev(q), _dev(w_pts), d_in, r, baby_step, _dev(out), _dev(ws),
+                                      ws.numel() * 8, _stream(stream)))
+        return out
+
+    def rotate_sum(self, cts: torch.Tensor, n_cts: int, first_shift: int, n_steps: int,
+                   ws: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+        ws = self.workspace(OP_ROTATE_SUM, n_cts) if ws is None else ws
+        _check(self.lib.fa_rotate_sum(self.h, _dev(cts), n_cts, first_shift, n_steps, _dev(ws), ws.numel() * 8,
+                                      _stream(stream)))
+        return cts
+
+    def profile(self, enable: bool = True):
+        _check(self.lib.fa_profile(self.h, 1 if enable else 0))
+
+    def profile_read(self) -> dict:
+        ms = np.zeros(4, dtype=np.float64)
+        _check(self.lib.fa_profile_read(self.h, _ptr(ms, _f64p)))
+        return {"baby_ms": ms[0], "mac_ms": ms[1], "giant_ms": ms[2], "total_ms": ms[3]}
+
+    def rotate(self, ct: torch.Tensor, step: int, out: torch.Tensor | None = None,
+               ws: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+        out = self.new_ct() if out is None else out
+        ws = self.workspace(OP_ROTATE, 1) if ws is None else ws
+        _check(self.lib.fa_rotate(self.h, _dev(ct), step, _dev(out), _dev(ws), ws.numel() * 8, _stream(stream)))
+        return out

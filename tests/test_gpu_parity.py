@@ -1,0 +1,248 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Ciphertexts are compared word for word in canonical coefficient form
+(bit-exact); decrypted scores against float64 inner products (<= 1e-4)."""
+import numpy as np
+import pytest
+
+from oracle import ckks
+from paper_2608_21131_amd import gen
+
+from common import Pair, say
+
+pytestmark = pytest.mark.gpu
+
+_PAIRS = {}
+
+
+def pair(name, wid=0):
+    key = (name, wid)
+    if key not in _PAIRS:
+        say(f"[setup] context {name} wid={wid}")
+        _PAIRS[key] = Pair(name, wid)
+    return _PAIRS[key]
+
+
+def rand_coeffs(g, n, count, bits=62):
+    return g.integers(-(1 << bits), 1 << bits, size=(count, n), dtype=np.int64)
+
+
+@pytest.mark.parametrize("name", ["tiny", "p1", "p2", "p4"])
+def test_ntt_roundtrip_and_residues(name):
+    p = pair(name)
+    g = np.random.default_rng(1)
+    c = rand_coeffs(g, p.n, 3)
+    say(f"[ntt] {name} encode_db_block_int + export")
+    pts = p.ctx.encode_db_block_int(c)
+    got = p.ctx.export(pts, 3)
+    for i in range(3):
+        assert np.array_equal(got[i], ckks.to_residues(c[i], p.par.q)), i
+
+
+@pytest.mark.parametrize("name", ["tiny", "p1", "p2", "p4"])
+def test_encrypt_decrypt_parity(name):
+    p = pair(name)
+    v = np.random.default_rng(2).uniform(-1, 1, p.par.slots)
+    m = ckks.encode(v, p.n, 40)
+    say(f"[enc] {name}")
+    ct_dev, ct_orc = p.encrypt_both(m)
+    assert np.array_equal(p.export_ct(ct_dev)[0], ct_orc)
+    res = p.ctx.decrypt(ct_dev)
+    assert np.array_equal(res, p.orc.decrypt(ct_orc, p.s))
+    z = p.ctx.decode(res, 40)
+    assert np.max(np.abs(z - v)) < 1e-6
+
+
+@pytest.mark.parametrize("name,steps", [("tiny", [1, 3, 100]), ("small", [1, 7]), ("p1", [1, 64]),
+                                        ("p2", [5]), ("p4", [1])])
+def test_rotation_parity(name, steps):
+    p = pair(name)
+    v = np.random.default_rng(3).uniform(-1, 1, p.par.slots)
+    ct_dev, ct_orc = p.encrypt_both(ckks.encode(v, p.n, 40), tag=3)
+    keys = p.keys(steps)
+    for r in steps:
+        say(f"[rot] {name} step {r}")
+        got = p.export_ct(p.ctx.rotate(ct_dev, r))[0]
+        ref = p.orc.rotate(ct_orc, r, keys[r])
+        assert np.array_equal(got, ref), r
+        # key-switch noise grows with N (the extended digits are not centred):
+        # about 1e-6 at N = 2^13 and 3e-5 at N = 2^16, identical in the oracle
+        z = p.ctx.decode(p.ctx.decrypt(p.ctx.rotate(ct_dev, r)), 40)
+        assert np.max(np.abs(z - np.roll(v, -r))) < 1e-4
+
+
+@pytest.mark.parametrize("name,d,rows", [("tiny", 16, 500), ("p1", 128, 1024)])
+def test_row_layout_then_rotate_sum(name, d, rows):
+    """Row-packed scoring: ct x pt per plaintext, then log2(d) rotate-and-sum steps."""
+    p = pair(name, wid=4)
+    X = gen.gaussian_unit_rows(gen.rng(4, gen.STREAM_DB), rows, d)
+    q = gen.gaussian_unit_rows(gen.rng(4, gen.STREAM_QUERY), 1, d)[0]
+    S = p.par.slots
+    ct_dev, ct_orc = p.encrypt_both(ckks.encode(ckks.replicate(q, S), p.n, 40), tag=4)
+    slot_pts = ckks.pack_rows(X, S, d)
+    coeffs = np.stack([ckks.encode(v, p.n, 40) for v in slot_pts])
+    steps = int(np.log2(d))
+    keys = p.keys([1 << k for k in range(steps)])
+    say(f"[rowA] {name} d={d} rows={rows} pts={len(coeffs)}")
+    pts = p.ctx.encode_db_block_int(coeffs)
+    W = p.ctx.pt_words
+    blocks = [pts[w * W:(w + 1) * W] for w in range(len(coeffs))]
+    out = p.ctx.score_block(ct_dev, blocks, d, 0)
+    p.ctx.rotate_sum(out, len(coeffs), 1, steps)
+    got = p.export_ct(out, len(coeffs))
+    scores = []
+    for w in range(len(coeffs)):
+        pt_res = ckks.to_residues(coeffs[w], p.par.q)
+        ref = p.orc.rotate_sum(p.orc.mul_plain(ct_orc, pt_res), 1, steps, keys)
+        assert np.array_equal(got[w], ref), w
+        z = p.ctx.decode(p.ctx.decrypt(out[w * p.ctx.ct_words:(w + 1) * p.ctx.ct_words]), 80)
+        scores.extend(z[::d])
+    assert np.max(np.abs(np.array(scores)[:rows] - X @ q)) < 1e-4
+
+
+@pytest.mark.parametrize("name,d,B,rows_list", [
+    ("tiny", 16, 4, [300, 512, 17]),
+    ("tiny", 16, 1, [100]),
+    ("tiny", 16, 16, [100]),
+    ("p1", 128, 16, [4096, 1000]),
+    ("p2", 128, 16, [3000]),
+])
+def test_diag_score_parity(name, d, B, rows_list):
+    p = pair(name, wid=5)
+    S = p.par.slots
+    G = d // B
+    g = gen.rng(5, gen.STREAM_DB, d, B)
+    Xs = [gen.gaussian_unit_rows(g, r, d) for r in rows_list]
+    q = gen.gaussian_unit_rows(gen.rng(5, gen.STREAM_QUERY), 1, d)[0]
+    ct_dev, ct_orc = p.encrypt_both(ckks.encode(ckks.replicate(q, S), p.n, 40), tag=5)
+    keys = p.keys(ckks.steps_for_bsgs(d, B))
+    blocks = []
+    coeffs = []
+    for X in Xs:
+        c = ckks.layout_b_coeffs(X, p.par, d, B)
+        coeffs.append(c)
+        blocks.append(p.ctx.encode_db_block_int(c))
+    say(f"[diag] {name} d={d} B={B} blocks={rows_list}")
+    out = p.ctx.score_block(ct_dev, blocks, d, 1, B)
+    got = p.export_ct(out, len(Xs))
+    qrot = p.orc.baby_rotations(ct_orc, B, keys)
+    for i, (X, c) in enumerate(zip(Xs, coeffs)):
+        pts = np.stack([ckks.to_residues(ci, p.par.q) for ci in c]).reshape(G, B, p.par.L, p.n)
+        ref = p.orc.bsgs_block(qrot, pts, B, G, keys)
+        assert np.array_equal(got[i], ref), i
+        z = p.ctx.decode(p.ctx.decrypt(out[i * p.ctx.ct_words:(i + 1) * p.ctx.ct_words]), 80)
+        assert np.max(np.abs(z[:len(X)] - X @ q)) < 1e-4
+        if len(X) < S:
+            assert np.max(np.abs(z[len(X):])) < 1e-4
+
+
+@pytest.mark.parametrize("name,d_in,R,B,rows", [("small", 64, 16, 4, 100), ("p2", 512, 128, 16, 2000)])
+def test_projection_parity(name, d_in, R, B, rows):
+    p = pair(name, wid=6)
+    S = p.par.slots
+    W = gen.projection_matrix(gen.rng(6, gen.STREAM_W), d_in, R, var=1.0 / R)
+    q = gen.gaussian_unit_rows(gen.rng(6, gen.STREAM_QUERY), 1, d_in)[0]
+    ct_dev, ct_orc = p.encrypt_both(ckks.encode(ckks.replicate(q, S), p.n, 40), tag=6)
+    c = d_in // R
+    fold = [R << k for k in range(int(np.log2(c)))]
+    keys = p.keys(ckks.steps_for_bsgs(R, B) + fold)
+    pre = ckks.prerotate(ckks.projection_diagonals(W, S), B)
+    wco = np.stack([ckks.encode(pre[g, b], p.n, 40) for g in range(R // B) for b in range(B)])
+    wpts = p.ctx.encode_db_block_int(wco)
+    say(f"[proj] {name} d_in={d_in} R={R} B={B}")
+    qr = p.ctx.project_ct(ct_dev, wpts, d_in, R, B)
+    got = p.export_ct(qr)[0]
+    wres = np.stack([ckks.to_residues(x, p.par.q) for x in wco]).reshape(R // B, B, p.par.L, p.n)
+    z = p.orc.bsgs_block(p.orc.baby_rotations(ct_orc, B, keys), wres, B, R // B, keys)
+    z = p.orc.rotate_sum(z, R, len(fold), keys)
+    assert np.array_equal(got, z)
+    qR = W.T @ q
+    zz = p.ctx.decode(p.ctx.decrypt(qr), 80)
+    assert np.max(np.abs(zz - np.tile(qR, S // R))) < 1e-4
+    # score the projected query (scale 2^120) against normalised projected rows
+    Xr = gen.normalize_rows(gen.gaussian_unit_rows(gen.rng(6, gen.STREAM_DB), rows, d_in) @ W)
+    blk = p.ctx.encode_db_block(Xr.astype(np.float32), R, 1, B)
+    out = p.ctx.score_block(qr, [blk], R, 1, B)
+    raw = p.ctx.decode(p.ctx.decrypt(out), 120)[:rows]
+    cos = raw / np.linalg.norm(qR)
+    ref = Xr.astype(np.float32).astype(np.float64) @ qR / np.linalg.norm(qR)
+    assert np.max(np.abs(cos - ref)) < 1e-4
+
+
+@pytest.mark.parametrize("name", ["tiny", "p4"])
+def test_float_encode_matches_oracle(name):
+    p = pair(name)
+    v = np.random.default_rng(7).standard_normal(p.par.slots) * 0.1
+    mine = p.ctx.encode(v, 40)
+    ref = ckks.encode(v, p.n, 40)
+    diff = np.abs(mine - ref)
+    assert diff.max() <= 1
+    assert np.count_nonzero(diff) <= max(2, p.n // 1000)
+
+
+def test_encode_db_block_float_vs_oracle():
+    p = pair("p1", wid=8)
+    d, B = 128, 16
+    X = gen.gaussian_unit_rows(gen.rng(8, gen.STREAM_DB), 3000, d).astype(np.float32)
+    say("[encode_db_block] p1")
+    pts = p.ctx.encode_db_block(X, d, 1, B)
+    got = p.ctx.export(pts, d)
+    ref = ckks.layout_b_coeffs(X.astype(np.float64), p.par, d, B)
+    mism = 0
+    for j in range(d):
+        r = ckks.to_residues(ref[j], p.par.q)
+        dif = (got[j].astype(np.int64) - r.astype(np.int64))
+        qs = np.array(p.par.q, dtype=np.int64)[:, None]
+        dif = np.where(dif > qs // 2, dif - qs, np.where(dif < -(qs // 2), dif + qs, dif))
+        assert np.abs(dif).max() <= 1
+        mism += int(np.count_nonzero(dif[0]))
+    assert mism <= d * p.n // 1000
+    say(f"[encode_db_block] coefficient mismatches (|dm| = 1): {mism} of {d * p.n}")
+
+
+def test_error_paths():
+    from paper_2608_21131_amd import fa
+    p = pair("tiny", wid=9)
+    ct = p.ctx.new_ct()
+    ct.zero_()
+    # missing rotation key
+    with pytest.raises(fa.FaError) as ei:
+        p.ctx.rotate(ct, 77)
+    assert ei.value.code == fa.FA_E_NOKEY
+    # workspace too small
+    blk = p.ctx.new_pt(16)
+    p.keys(ckks.steps_for_bsgs(16, 4), oracle=False)
+    small = p.ctx.new_pt(1)
+    with pytest.raises(fa.FaError) as ei:
+        p.ctx.score_block(ct, [blk], 16, 1, 4, ws=small)
+    assert ei.value.code == fa.FA_E_NOMEM
+    # d not a power of two / baby step not dividing d
+    with pytest.raises(fa.FaError) as ei:
+        p.ctx.score_block(ct, [blk], 12, 1, 4)
+    assert ei.value.code == fa.FA_E_SHAPE
+    with pytest.raises(fa.FaError) as ei:
+        p.ctx.score_block(ct, [blk], 16, 1, 3)
+    assert ei.value.code == fa.FA_E_INVAL
+    # too many rows for one diagonal block
+    with pytest.raises(fa.FaError) as ei:
+        p.ctx.encode_db_block(np.zeros((p.par.slots + 1, 16), np.float32), 16, 1, 4)
+    assert ei.value.code == fa.FA_E_SHAPE
+    # fold key missing for a projection
+    with pytest.raises(fa.FaError) as ei:
+        p.ctx.project_ct(ct, blk, 64, 16, 4)
+    assert ei.value.code == fa.FA_E_NOKEY
+
+
+def test_deterministic_repeat():
+    """Two runs of the same scoring call give identical words (no races)."""
+    p = pair("p1", wid=10)
+    d, B = 128, 16
+    X = gen.gaussian_unit_rows(gen.rng(10, gen.STREAM_DB), 4096, d)
+    q = gen.gaussian_unit_rows(gen.rng(10, gen.STREAM_QUERY), 1, d)[0]
+    ct_dev, _ = p.encrypt_both(ckks.encode(ckks.replicate(q, p.par.slots), p.n, 40), tag=10)
+    p.keys(ckks.steps_for_bsgs(d, B), oracle=False)
+    blk = p.ctx.encode_db_block(X.astype(np.float32), d, 1, B)
+    a = p.export_ct(p.ctx.score_block(ct_dev, [blk, blk], d, 1, B), 2)
+    b = p.export_ct(p.ctx.score_block(ct_dev, [blk, blk], d, 1, B), 2)
+    assert np.array_equal(a, b)
+    assert np.array_equal(a[0], a[1])
