@@ -13,6 +13,7 @@
 #include <complex>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <string>
@@ -227,11 +228,13 @@ const char* fa_last_error(void) { return g_err.c_str(); }
 void fa_ctx_destroy(fa_ctx* c) {
   if (!c) return;
   (void)hipFree(c->d_pr);
-  (void)hipFree(c->d_tw_fwd);
-  (void)hipFree(c->d_tw_inv);
-  (void)hipFree(c->d_mu_inv);
+  (void)hipFree(c->d_twa_fwd);
+  (void)hipFree(c->d_twa_inv);
+  (void)hipFree(c->d_twt_fwd);
+  (void)hipFree(c->d_twt_inv);
+  (void)hipFree(c->d_twr_fwd);
+  (void)hipFree(c->d_twr_inv);
   (void)hipFree(c->d_mu_hat);
-  (void)hipFree(c->d_md_inv);
   (void)hipFree(c->d_md_hat);
   (void)hipFree(c->d_s);
   for (auto& kv : c->keys) (void)hipFree(kv.second);
@@ -281,30 +284,45 @@ int fa_ctx_create(const fa_params* prm, fa_ctx** out) {
       hp[t].pinv = (double)invmod(pm, q);
     }
   }
-  // twiddles psi^{brev(k)} and their inverses
-  std::vector<double> twf((size_t)np * n), twi((size_t)np * n);
+  // twiddles: first-pass table psi^{brev(k)} (k < 256), second-pass table T and
+  // per-row factors F (see fa_kernels.hip), each also for psi^-1
+  const int SA = c->logn - 8, H = 1 << SA;
+  std::vector<double> twa_f((size_t)np * 256), twa_i((size_t)np * 256), twt_f((size_t)np * 256),
+      twt_i((size_t)np * 256), twr_f((size_t)np * H * 8), twr_i((size_t)np * H * 8);
   c->psi.resize(np);
+  c->h_ninv.resize(np);
   for (int t = 0; t < np; ++t) {
     const u64 q = c->primes[t];
     const u64 psi = primitive_root_2n(q, c->logn);
     const u64 ipsi = invmod(psi, q);
     c->psi[t] = psi;
-    std::vector<u64> pw(n), ipw(n);
-    u64 x = 1, y = 1;
-    for (int j = 0; j < n; ++j) {
-      pw[j] = x;
-      ipw[j] = y;
-      x = mulmod(x, psi, q);
-      y = mulmod(y, ipsi, q);
+    c->h_ninv[t] = hp[t].ninv;
+    for (int k = 0; k < 256; ++k) {
+      const u64 e = bitrev((uint32_t)k, c->logn);
+      twa_f[(size_t)t * 256 + k] = (double)powmod(psi, e, q);
+      twa_i[(size_t)t * 256 + k] = (double)powmod(ipsi, e, q);
     }
-    for (int k = 0; k < n; ++k) {
-      const uint32_t r = bitrev((uint32_t)k, c->logn);
-      twf[(size_t)t * n + k] = (double)pw[r];
-      twi[(size_t)t * n + k] = (double)ipw[r];
+    twt_f[(size_t)t * 256] = 1.0;
+    twt_i[(size_t)t * 256] = 1.0;
+    for (int s1 = 0; s1 < 8; ++s1)
+      for (int i1 = 0; i1 < (1 << s1); ++i1) {
+        const u64 e = (u64)bitrev((uint32_t)i1, s1) * (u64)(n >> s1);
+        twt_f[(size_t)t * 256 + (1 << s1) + i1] = (double)powmod(psi, e, q);
+        twt_i[(size_t)t * 256 + (1 << s1) + i1] = (double)powmod(ipsi, e, q);
+      }
+    for (int r = 0; r < H; ++r) {
+      const u64 e0 = 2 * (u64)bitrev((uint32_t)r, SA) + 1;
+      for (int s1 = 0; s1 < 8; ++s1) {
+        const u64 e = e0 << (7 - s1);
+        twr_f[((size_t)t * H + r) * 8 + s1] = (double)powmod(psi, e, q);
+        twr_i[((size_t)t * H + r) * 8 + s1] = (double)powmod(ipsi, e, q);
+      }
     }
   }
-  // basis-conversion constants: products of primes reduced prime by prime
-  std::vector<double> mu_inv((size_t)c->dnum * c->alpha, 0.0), mu_hat((size_t)c->dnum * c->alpha * np, 0.0);
+  // basis-conversion constants: products of primes reduced prime by prime;
+  // the inverse factors are folded into the scaling of the inverse transforms
+  std::vector<double> mu_hat((size_t)c->dnum * c->alpha * np, 0.0);
+  c->h_mu_scale.assign(L, 0.0);
   for (int i = 0; i < c->dnum; ++i) {
     const int lo = i * c->alpha, hi = std::min(lo + c->alpha, L);
     for (int j = lo; j < hi; ++j) {
@@ -318,16 +336,18 @@ int fa_ctx_create(const fa_params* prm, fa_ctx** out) {
       u64 v = 1;
       for (int jj = lo; jj < hi; ++jj)
         if (jj != j) v = mulmod(v, c->primes[jj] % c->primes[j], c->primes[j]);
-      mu_inv[(size_t)i * c->alpha + (j - lo)] = (double)invmod(v, c->primes[j]);
+      const u64 q = c->primes[j];
+      c->h_mu_scale[j] = (double)mulmod(invmod(v, q), invmod((u64)n, q), q);
     }
   }
-  std::vector<double> md_inv(K), md_hat((size_t)K * L);
+  std::vector<double> md_hat((size_t)K * L);
+  c->h_md_scale.assign(K, 0.0);
   for (int k = 0; k < K; ++k) {
     const u64 pk = c->primes[L + k];
     u64 v = 1;
     for (int kk = 0; kk < K; ++kk)
       if (kk != k) v = mulmod(v, c->primes[L + kk] % pk, pk);
-    md_inv[k] = (double)invmod(v, pk);
+    c->h_md_scale[k] = (double)mulmod(invmod(v, pk), invmod((u64)n, pk), pk);
     for (int t = 0; t < L; ++t) {
       const u64 q = c->primes[t];
       u64 w = 1;
@@ -337,22 +357,28 @@ int fa_ctx_create(const fa_params* prm, fa_ctx** out) {
     }
   }
   int rc;
-  if ((rc = dev_alloc(&c->d_pr, np)) || (rc = dev_alloc(&c->d_tw_fwd, (size_t)np * n)) ||
-      (rc = dev_alloc(&c->d_tw_inv, (size_t)np * n)) || (rc = dev_alloc(&c->d_mu_inv, mu_inv.size())) ||
-      (rc = dev_alloc(&c->d_mu_hat, mu_hat.size())) || (rc = dev_alloc(&c->d_md_inv, md_inv.size())) ||
+  if ((rc = dev_alloc(&c->d_pr, np)) || (rc = dev_alloc(&c->d_twa_fwd, twa_f.size())) ||
+      (rc = dev_alloc(&c->d_twa_inv, twa_i.size())) || (rc = dev_alloc(&c->d_twt_fwd, twt_f.size())) ||
+      (rc = dev_alloc(&c->d_twt_inv, twt_i.size())) || (rc = dev_alloc(&c->d_twr_fwd, twr_f.size())) ||
+      (rc = dev_alloc(&c->d_twr_inv, twr_i.size())) || (rc = dev_alloc(&c->d_mu_hat, mu_hat.size())) ||
       (rc = dev_alloc(&c->d_md_hat, md_hat.size())) || (rc = dev_alloc(&c->d_s, (size_t)np * n))) {
     fa_ctx_destroy(c);
     return rc;
   }
   hipError_t e = hipSuccess;
-  e = e ? e : hipMemcpy(c->d_pr, hp.data(), np * sizeof(DevPrime), hipMemcpyHostToDevice);
-  e = e ? e : hipMemcpy(c->d_tw_fwd, twf.data(), twf.size() * 8, hipMemcpyHostToDevice);
-  e = e ? e : hipMemcpy(c->d_tw_inv, twi.data(), twi.size() * 8, hipMemcpyHostToDevice);
-  e = e ? e : hipMemcpy(c->d_mu_inv, mu_inv.data(), mu_inv.size() * 8, hipMemcpyHostToDevice);
-  e = e ? e : hipMemcpy(c->d_mu_hat, mu_hat.data(), mu_hat.size() * 8, hipMemcpyHostToDevice);
-  e = e ? e : hipMemcpy(c->d_md_inv, md_inv.data(), md_inv.size() * 8, hipMemcpyHostToDevice);
-  e = e ? e : hipMemcpy(c->d_md_hat, md_hat.data(), md_hat.size() * 8, hipMemcpyHostToDevice);
-  e = e ? e : hipMemset(c->d_s, 0, (size_t)np * n * 8);
+  auto up = [&](double* d, const std::vector<double>& h) {
+    if (e == hipSuccess) e = hipMemcpy(d, h.data(), h.size() * 8, hipMemcpyHostToDevice);
+  };
+  if (e == hipSuccess) e = hipMemcpy(c->d_pr, hp.data(), np * sizeof(DevPrime), hipMemcpyHostToDevice);
+  up(c->d_twa_fwd, twa_f);
+  up(c->d_twa_inv, twa_i);
+  up(c->d_twt_fwd, twt_f);
+  up(c->d_twt_inv, twt_i);
+  up(c->d_twr_fwd, twr_f);
+  up(c->d_twr_inv, twr_i);
+  up(c->d_mu_hat, mu_hat);
+  up(c->d_md_hat, md_hat);
+  if (e == hipSuccess) e = hipMemset(c->d_s, 0, (size_t)np * n * 8);
   if (e != hipSuccess) {
     fa_ctx_destroy(c);
     return fail(FA_E_HIP, "fa_ctx_create: %s", hipGetErrorString(e));
@@ -731,7 +757,19 @@ int fa_encode_db_block(fa_ctx* c, const float* rows, int n_rows, int dim, int d,
 }  // extern "C"
 
 namespace {
-constexpr int kRotBatch = 8;  // rotations key-switched per launch group
+constexpr int kRotBatch = 16;  // most rotations key-switched per launch group
+
+// Rotations per launch group actually used (<= kRotBatch; FA_ROT_BATCH tunes it):
+// smaller groups keep the key-switch products resident in the last-level cache.
+int rot_batch() {
+  static int v = -1;
+  if (v < 0) {
+    const char* e = getenv("FA_ROT_BATCH");
+    v = e ? atoi(e) : kRotBatch;
+    if (v < 1 || v > kRotBatch) v = kRotBatch;
+  }
+  return v;
+}
 
 struct Arena {
   char* base;
@@ -749,67 +787,95 @@ size_t rup(size_t words) { return (words * 8 + 255) & ~(size_t)255; }
 // workspace of a batch of `nb` full rotations (own ModUp each)
 size_t rotate_ws(const fa_ctx* c, int nb) {
   const size_t n = c->n;
-  return (size_t)nb * (rup(c->L * n) + rup((size_t)c->dnum * c->np * n) + rup(2 * (size_t)c->np * n) +
-                       rup(2 * (size_t)c->L * n));
+  return rup((size_t)nb * c->L * n) + rup((size_t)nb * c->dnum * c->np * n) + rup((size_t)nb * 2 * c->np * n) +
+         rup((size_t)nb * 2 * c->L * n);
 }
 
 size_t score_ws(const fa_ctx* c, int nb, int d, int B) {
   const size_t n = c->n, L = c->L, np = c->np, dn = c->dnum;
-  const int G = d / B;
-  const int rb = std::max(1, std::min(kRotBatch, B - 1));
+  const size_t G = d / B;
+  const size_t rb = std::max(1, std::min(kRotBatch, B - 1));
   size_t w = 0;
-  w += rup(L * n);                         // c1 in coefficient form
-  w += rup(dn * np * n);                   // extended digits of q
-  w += (size_t)rb * rup(2 * np * n);       // key-switch products
-  w += (size_t)rb * rup(2 * L * n);        // ModDown conversions
-  w += (size_t)B * rup(2 * L * n);         // baby rotations
-  w += (size_t)nb * G * rup(2 * L * n);    // accumulators
-  w += (size_t)nb * rup(dn * np * n);      // giant-step extended digits
-  w += (size_t)nb * rup(2 * np * n);       // giant-step key-switch sums
-  w += (size_t)nb * rup(2 * L * n);        // giant-step ModDown conversions
+  w += rup(L * n);                            // scaled coefficients of q.c1
+  w += rup(dn * np * n);                      // extended digits of q
+  w += rup(rb * 2 * np * n);                  // key-switch products
+  w += rup(rb * 2 * L * n);                   // ModDown conversions
+  w += rup((size_t)(B - 1) * 2 * L * n + 1);  // baby rotations 1..B-1
+  w += rup(nb * G * 2 * L * n);               // accumulators
+  w += rup(nb * L * n);                       // giant-step scaled coefficients
+  w += rup(nb * dn * np * n);                 // giant-step extended digits
+  w += rup(nb * 2 * np * n);                  // giant-step key-switch sums
+  w += rup(nb * 2 * L * n);                   // giant-step ModDown conversions
   return w;
 }
 }  // namespace
+
+// Extended digits (NTT form) of the c1 of `batch` ciphertexts cts + b * ct_stride.
+// y (per item [L][N]) receives c1's coefficients times (D_i/q_t)^-1; ext receives
+// every converted limb.  The ciphertexts are only read.
+static void modup(fa_ctx* c, const double* cts, size_t ct_stride, int batch, double* y, size_t y_stride,
+                  double* ext, size_t ext_stride, hipStream_t s) {
+  const size_t n = c->n, L = c->L;
+  {
+    fa::LimbBatch inv(c, s, false);
+    for (int b = 0; b < batch; ++b)
+      for (size_t t = 0; t < L; ++t)
+        inv.add(y + (size_t)b * y_stride + t * n, (int)t, cts + (size_t)b * ct_stride + (L + t) * n,
+                c->h_mu_scale[t]);
+  }
+  std::vector<fa::MuItem> it(batch);
+  for (int b = 0; b < batch; ++b) it[b] = {y + (size_t)b * y_stride, ext + (size_t)b * ext_stride};
+  fa::modup_ntt(c, it.data(), batch, s);
+}
+
+// ModDown of `count` polynomials u_i = u + i * np * N over Q u P (NTT form):
+// out_i = bases_i[pi_gal_i] + (u_i,Q - Conv_{P->Q}(u_i,P)) * P^-1.  The special-
+// prime limbs of u are overwritten (scaled coefficients); conv is scratch.
+static void moddown_polys(fa_ctx* c, double* u, int count, double* conv, const double* const* bases,
+                          double* const* outs, const uint32_t* gals, hipStream_t s) {
+  const size_t n = c->n, L = c->L, np = c->np;
+  {
+    fa::LimbBatch inv(c, s, false);
+    for (int i = 0; i < count; ++i)
+      for (int k = 0; k < c->K; ++k)
+        inv.add(u + (size_t)i * np * n + (L + k) * n, (int)L + k, nullptr, c->h_md_scale[k]);
+  }
+  std::vector<fa::MdItem> it(count);
+  for (int i = 0; i < count; ++i) {
+    double* ui = u + (size_t)i * np * n;
+    it[i] = {ui + L * n, conv + (size_t)i * L * n, ui, bases[i], outs[i], gals[i]};
+  }
+  fa::moddown(c, it.data(), count, s);
+}
 
 // Hoisted rotations of one ciphertext q by steps[0..m-1]: one decomposition of
 // c1 shared by all, each rotation with its own key switch and ModDown.
 // ext must already hold the extended digits of q.c1 (NTT form).
 static int rotations_from_ext(fa_ctx* c, const double* q, const double* ext, const int* steps, int m,
                               double* const* outs, double* u, double* conv, hipStream_t s) {
-  const size_t n = c->n, L = c->L, np = c->np, K = c->K;
-  for (int r0 = 0; r0 < m; r0 += kRotBatch) {
-    const int rb = std::min(kRotBatch, m - r0);
+  const size_t n = c->n, L = c->L, np = c->np;
+  const int rbmax = rot_batch();
+  for (int r0 = 0; r0 < m; r0 += rbmax) {
+    const int rb = std::min(rbmax, m - r0);
     fa::KsItem ks[kRotBatch];
-    fa::FinishItem fin[kRotBatch];
+    const double* bases[2 * kRotBatch];
+    double* douts[2 * kRotBatch];
+    uint32_t gals[2 * kRotBatch];
     for (int j = 0; j < rb; ++j) {
       auto it = c->keys.find(steps[r0 + j]);
       if (it == c->keys.end()) return fail(FA_E_NOKEY, "no rotation key for step %d", steps[r0 + j]);
-      ks[j] = {ext, it->second, u + (size_t)j * 2 * np * n, galois(c->n, steps[r0 + j])};
-      fin[j] = {u + (size_t)j * 2 * np * n, conv + (size_t)j * 2 * L * n, q, nullptr, outs[r0 + j], ks[j].gal};
+      const uint32_t gal = galois(c->n, steps[r0 + j]);
+      ks[j] = {ext, q + L * n, it->second, u + (size_t)j * 2 * np * n, nullptr, gal};
+      bases[2 * j] = q;
+      bases[2 * j + 1] = nullptr;
+      douts[2 * j] = outs[r0 + j];
+      douts[2 * j + 1] = outs[r0 + j] + L * n;
+      gals[2 * j] = gals[2 * j + 1] = gal;
     }
     fa::ks_inner(c, ks, rb, false, s);
-    // ModDown: special-prime limbs to coefficient form, convert, back to NTT
-    for (int j = 0; j < rb; ++j)
-      for (int h = 0; h < 2; ++h)
-        fa::ntt_inv_strided(c, u + ((size_t)j * 2 + h) * np * n + L * n, n, (int)K, (int)K, (int)L, s);
-    fa::conv_moddown(c, u + L * n, np * n, conv, L * n, 2 * rb, s);
-    fa::ntt_fwd_strided(c, conv, n, (int)(2 * rb * L), (int)L, 0, s);
-    fa::moddown_finish(c, fin, rb, s);
+    moddown_polys(c, u, 2 * rb, conv, bases, douts, gals, s);
   }
   return check_launch("rotation");
-}
-
-// extended digits (NTT form) of the c1 of `batch` ciphertexts cts + b * ct_stride
-static void modup(fa_ctx* c, const double* cts, size_t ct_stride, int batch, double* c1c, size_t c1c_stride,
-                  double* ext, size_t ext_stride, hipStream_t s) {
-  const size_t n = c->n, L = c->L;
-  for (int b = 0; b < batch; ++b)
-    (void)hipMemcpyAsync(c1c + (size_t)b * c1c_stride, cts + (size_t)b * ct_stride + L * n, L * n * 8,
-                   hipMemcpyDeviceToDevice, s);
-  fa::scatter_own(c, cts + L * n, ct_stride, ext, ext_stride, batch, s);
-  for (int b = 0; b < batch; ++b) fa::ntt_inv_strided(c, c1c + (size_t)b * c1c_stride, n, (int)L, (int)L, 0, s);
-  fa::conv_modup(c, c1c, c1c_stride, ext, ext_stride, batch, s);
-  fa::ntt_fwd_ext(c, ext, ext_stride, batch, s);
 }
 
 // Full rotation of `nb` ciphertexts by the same step: outs[b] = Rotate(cts[b], step).
@@ -818,28 +884,27 @@ static int rotate_batch(fa_ctx* c, const double* cts, int nb, int step, double* 
   auto it = c->keys.find(step);
   if (it == c->keys.end()) return fail(FA_E_NOKEY, "no rotation key for step %d", step);
   const size_t mark = ar.used;
-  double* c1c = ar.take((size_t)nb * L * n);
+  double* y = ar.take((size_t)nb * L * n);
   double* ext = ar.take((size_t)nb * dn * np * n);
   double* u = ar.take((size_t)nb * 2 * np * n);
   double* conv = ar.take((size_t)nb * 2 * L * n);
-  if (!c1c || !ext || !u || !conv) return fail(FA_E_NOMEM, "workspace too small for rotation");
+  if (!y || !ext || !u || !conv) return fail(FA_E_NOMEM, "workspace too small for rotation");
   const size_t ctw = 2 * L * n;
-  modup(c, cts, ctw, nb, c1c, L * n, ext, dn * np * n, s);
+  modup(c, cts, ctw, nb, y, L * n, ext, dn * np * n, s);
   std::vector<fa::KsItem> ks(nb);
-  std::vector<fa::FinishItem> fin(nb);
-  const uint32_t gal = galois(c->n, step);
+  std::vector<const double*> bases(2 * nb);
+  std::vector<double*> douts(2 * nb);
+  std::vector<uint32_t> gals(2 * nb, galois(c->n, step));
   for (int b = 0; b < nb; ++b) {
-    ks[b] = {ext + (size_t)b * dn * np * n, it->second, u + (size_t)b * 2 * np * n, gal};
-    fin[b] = {u + (size_t)b * 2 * np * n, conv + (size_t)b * 2 * L * n, cts + (size_t)b * ctw, nullptr,
-              outs + (size_t)b * ctw, gal};
+    const double* ct = cts + (size_t)b * ctw;
+    ks[b] = {ext + (size_t)b * dn * np * n, ct + L * n, it->second, u + (size_t)b * 2 * np * n, nullptr, gals[0]};
+    bases[2 * b] = ct;
+    bases[2 * b + 1] = nullptr;
+    douts[2 * b] = outs + (size_t)b * ctw;
+    douts[2 * b + 1] = outs + (size_t)b * ctw + L * n;
   }
   fa::ks_inner(c, ks.data(), nb, false, s);
-  for (int b = 0; b < nb; ++b)
-    for (int h = 0; h < 2; ++h)
-      fa::ntt_inv_strided(c, u + ((size_t)b * 2 + h) * np * n + L * n, n, c->K, c->K, (int)L, s);
-  fa::conv_moddown(c, u + L * n, np * n, conv, L * n, 2 * nb, s);
-  fa::ntt_fwd_strided(c, conv, n, (int)(2 * nb * L), (int)L, 0, s);
-  fa::moddown_finish(c, fin.data(), nb, s);
+  moddown_polys(c, u, 2 * nb, conv, bases.data(), douts.data(), gals.data(), s);
   ar.used = mark;
   return check_launch("rotate_batch");
 }
@@ -851,16 +916,18 @@ static int score_diag(fa_ctx* c, const double* q, const double* const* blocks, i
   const int G = d / B;
   const size_t ctw = 2 * L * n;
   const int rb = std::max(1, std::min(kRotBatch, B - 1));
-  double* c1c = ar.take(L * n);
+  double* y = ar.take(L * n);
   double* ext = ar.take(dn * np * n);
   double* u = ar.take((size_t)rb * 2 * np * n);
   double* conv = ar.take((size_t)rb * 2 * L * n);
-  double* qrot = ar.take((size_t)B * ctw);
+  double* qrot = ar.take((size_t)(B - 1) * ctw + 1);
   double* acc = ar.take((size_t)nb * G * ctw);
+  double* gy = ar.take((size_t)nb * L * n);
   double* gext = ar.take((size_t)nb * dn * np * n);
   double* usum = ar.take((size_t)nb * 2 * np * n);
   double* gconv = ar.take((size_t)nb * 2 * L * n);
-  if (!gconv) return fail(FA_E_NOMEM, "workspace too small for score_block");
+  if (!y || !ext || !u || !conv || !qrot || !acc || !gy || !gext || !usum || !gconv)
+    return fail(FA_E_NOMEM, "workspace too small for score_block");
   for (int b = 1; b < B; ++b)
     if (!c->keys.count(b)) return fail(FA_E_NOKEY, "no rotation key for baby step %d", b);
   for (int g = 1; g < G; ++g)
@@ -868,55 +935,51 @@ static int score_diag(fa_ctx* c, const double* q, const double* const* blocks, i
 
   if (c->prof) HIPCHK(hipEventRecord(c->ev[0], s));
   // 1. baby rotations of the query, one shared decomposition
-  HIPCHK(hipMemcpyAsync(qrot, q, ctw * 8, hipMemcpyDeviceToDevice, s));
   if (B > 1) {
-    modup(c, q, ctw, 1, c1c, L * n, ext, dn * np * n, s);
+    modup(c, q, ctw, 1, y, L * n, ext, dn * np * n, s);
     std::vector<int> steps(B - 1);
     std::vector<double*> outs(B - 1);
     for (int b = 1; b < B; ++b) {
       steps[b - 1] = b;
-      outs[b - 1] = qrot + (size_t)b * ctw;
+      outs[b - 1] = qrot + (size_t)(b - 1) * ctw;
     }
     int rc = rotations_from_ext(c, q, ext, steps.data(), B - 1, outs.data(), u, conv, s);
     if (rc) return rc;
   }
   if (c->prof) HIPCHK(hipEventRecord(c->ev[1], s));
   // 2. multiply-accumulate against the resident plaintexts
-  fa::mac_diag(c, qrot, blocks, nb, B, G, acc, s);
+  fa::mac_diag(c, q, qrot, blocks, nb, B, G, acc, s);
   if (c->prof) HIPCHK(hipEventRecord(c->ev[2], s));
-  // 3. giant steps: Rotate(acc_g, gB) summed over Q u P, one ModDown per block
-  for (int blk = 0; blk < nb; ++blk)
-    HIPCHK(hipMemcpyAsync(out + (size_t)blk * ctw, acc + (size_t)blk * G * ctw, ctw * 8, hipMemcpyDeviceToDevice, s));
-  if (G > 1) {
-    const size_t astride = (size_t)G * ctw;
+  // 3. giant steps: Rotate(acc_g, gB) summed over Q u P, one ModDown per block;
+  //    sigma(acc_g.c0) rides in the key-switch sum multiplied by P
+  const size_t astride = (size_t)G * ctw;
+  if (G == 1) {
+    for (int blk = 0; blk < nb; ++blk)
+      HIPCHK(hipMemcpyAsync(out + (size_t)blk * ctw, acc + (size_t)blk * ctw, ctw * 8, hipMemcpyDeviceToDevice, s));
+  } else {
     for (int g = 1; g < G; ++g) {
       const double* accg = acc + (size_t)g * ctw;
-      // decompose acc_g.c1 of every block (in place: acc_g.c1 is not needed afterwards)
-      fa::scatter_own(c, accg + L * n, astride, gext, dn * np * n, nb, s);
-      for (int blk = 0; blk < nb; ++blk)
-        fa::ntt_inv_strided(c, (double*)accg + (size_t)blk * astride + L * n, n, (int)L, (int)L, 0, s);
-      fa::conv_modup(c, accg + L * n, astride, gext, dn * np * n, nb, s);
-      fa::ntt_fwd_ext(c, gext, dn * np * n, nb, s);
+      modup(c, accg, astride, nb, gy, L * n, gext, dn * np * n, s);
       std::vector<fa::KsItem> ks(nb);
       const uint32_t gal = galois(c->n, g * B);
-      for (int blk = 0; blk < nb; ++blk)
-        ks[blk] = {gext + (size_t)blk * dn * np * n, c->keys[g * B], usum + (size_t)blk * 2 * np * n, gal};
+      for (int blk = 0; blk < nb; ++blk) {
+        const double* a = accg + (size_t)blk * astride;
+        ks[blk] = {gext + (size_t)blk * dn * np * n, a + L * n, c->keys[g * B], usum + (size_t)blk * 2 * np * n, a,
+                   gal};
+      }
       fa::ks_inner(c, ks.data(), nb, g > 1, s);
-      for (int blk = 0; blk < nb; ++blk)
-        fa::add_automorph(c, out + (size_t)blk * ctw, accg + (size_t)blk * astride, 1, gal, s);
     }
-    for (int blk = 0; blk < nb; ++blk)
-      for (int h = 0; h < 2; ++h)
-        fa::ntt_inv_strided(c, usum + ((size_t)blk * 2 + h) * np * n + L * n, n, c->K, c->K, (int)L, s);
-    fa::conv_moddown(c, usum + L * n, np * n, gconv, L * n, 2 * nb, s);
-    fa::ntt_fwd_strided(c, gconv, n, (int)(2 * nb * L), (int)L, 0, s);
-    std::vector<fa::FinishItem> fin(nb);
+    std::vector<const double*> bases(2 * nb);
+    std::vector<double*> douts(2 * nb);
+    std::vector<uint32_t> gals(2 * nb, 1u);
     for (int blk = 0; blk < nb; ++blk) {
-      double* o = out + (size_t)blk * ctw;
-      fin[blk] = {usum + (size_t)blk * 2 * np * n, gconv + (size_t)blk * 2 * L * n, o,
-                  acc + (size_t)blk * G * ctw + L * n, o, 1u};
+      const double* acc0 = acc + (size_t)blk * astride;
+      bases[2 * blk] = acc0;
+      bases[2 * blk + 1] = acc0 + L * n;
+      douts[2 * blk] = out + (size_t)blk * ctw;
+      douts[2 * blk + 1] = out + (size_t)blk * ctw + L * n;
     }
-    fa::moddown_finish(c, fin.data(), nb, s);
+    moddown_polys(c, usum, 2 * nb, gconv, bases.data(), douts.data(), gals.data(), s);
   }
   if (c->prof) {
     HIPCHK(hipEventRecord(c->ev[3], s));

@@ -24,10 +24,15 @@ struct DevPrime {
 
 // Up to FA_MAXL limbs (polynomials over one prime) processed by one launch.
 #define FA_MAXL 64
+// Each limb is transformed from src[i] into ptr[i] (src[i] == ptr[i]: in place);
+// the inverse transform ends with a multiply by scale[i] (N^-1, possibly times a
+// basis-conversion constant).
 struct LimbList {
   int n;
   int prime[FA_MAXL];
   double* ptr[FA_MAXL];
+  const double* src[FA_MAXL];
+  double scale[FA_MAXL];
 };
 
 struct fa_ctx {
@@ -36,12 +41,21 @@ struct fa_ctx {
   std::vector<uint64_t> psi;      // chosen primitive 2N-th roots
   // device tables
   DevPrime* d_pr = nullptr;       // [np]
-  double* d_tw_fwd = nullptr;     // [np][N]  psi^{brev(k)}
-  double* d_tw_inv = nullptr;     // [np][N]  psi^{-brev(k)}
-  double* d_mu_inv = nullptr;     // [dnum][alpha]       (D_i/d_j)^-1 mod d_j
+  // twiddles (see the transform in fa_kernels.hip): psi^{brev(k)} for k < 256,
+  // the 256-entry table T and the per-row factors F of the second pass, and
+  // the same three for psi^-1
+  double* d_twa_fwd = nullptr;    // [np][256]
+  double* d_twa_inv = nullptr;
+  double* d_twt_fwd = nullptr;    // [np][256]
+  double* d_twt_inv = nullptr;
+  double* d_twr_fwd = nullptr;    // [np][N/256][8]
+  double* d_twr_inv = nullptr;
   double* d_mu_hat = nullptr;     // [dnum][alpha][np]   (D_i/d_j) mod prime t
-  double* d_md_inv = nullptr;     // [K]                 (P/p_k)^-1 mod p_k
   double* d_md_hat = nullptr;     // [K][L]              (P/p_k) mod q_t
+  // host copies used to build per-limb constants
+  std::vector<double> h_ninv;     // [np] N^-1 mod prime
+  std::vector<double> h_mu_scale; // [L] N^-1 (D_i/q_t)^-1 mod q_t, t in digit i
+  std::vector<double> h_md_scale; // [K] N^-1 (P/p_k)^-1 mod p_k
   // secret (NTT form over every prime), keys
   double* d_s = nullptr;          // [np][N]
   std::map<int, double*> keys;    // step -> [dnum][2][np][N] (b, a), NTT form
@@ -67,50 +81,48 @@ void ntt_fwd_strided(const fa_ctx* c, double* base, size_t stride, int count, in
 void ntt_inv_strided(const fa_ctx* c, double* base, size_t stride, int count, int period, int prime_off,
                      hipStream_t s);
 
-// ModUp basis conversion for `batch` ciphertext c1's in coefficient form:
-// src[b] = c1c + b * src_stride ([L][N]); dst[b] = ext + b * dst_stride
-// ([dnum][np][N]); writes every (digit i, prime t not in digit i) limb.
-void conv_modup(const fa_ctx* c, const double* c1c, size_t src_stride, double* ext, size_t dst_stride, int batch,
-                hipStream_t s);
-// ModDown basis conversion P -> Q for `count` polynomials:
-// src[i] = up + i * src_stride points at the K special-prime limbs (coefficient
-// form, [K][N]); dst[i] = out + i * dst_stride ([L][N]).
-void conv_moddown(const fa_ctx* c, const double* up, size_t src_stride, double* out, size_t dst_stride, int count,
-                  hipStream_t s);
+// ModUp: for each item, ext[i][t] = NTT(Conv_{digit i -> t}(y)) for every digit
+// i and prime t outside the digit, where y ([L][N]) holds the coefficients of
+// c1 already multiplied by (D_i/q_t)^-1 (canonical).  Own-digit limbs of ext
+// are not written: the key-switch kernel reads them from c1.
+#define FA_MAXMU 16
+struct MuItem {
+  const double* y;  // [L][N]
+  double* ext;      // [dnum][np][N]
+};
+void modup_ntt(const fa_ctx* c, const MuItem* items, int count, hipStream_t s);
 
-// ext[b][i][t][k] = c1[b][t][k] for every ciphertext prime t of digit i = t / alpha
-// (the digit's own limbs, copied in NTT form), b < batch.
-void scatter_own(const fa_ctx* c, const double* c1, size_t src_stride, double* ext, size_t dst_stride, int batch,
-                 hipStream_t s);
-// Forward NTT of every limb (digit i, prime t not in digit i) of `batch`
-// extended digit sets ext + b * stride ([dnum][np][N]).
-void ntt_fwd_ext(const fa_ctx* c, double* ext, size_t stride, int batch, hipStream_t s);
+// ModDown with its finish: out = base[pi_gal] + (uQ - NTT(Conv_{P->Q}(yP))) * P^-1,
+// where yP ([K][N]) holds the special-prime coefficients of the key-switch
+// product already multiplied by (P/p_k)^-1 (canonical); conv is scratch.
+#define FA_MAXMD 32
+struct MdItem {
+  const double* yP;    // [K][N]
+  double* conv;        // [L][N] scratch
+  const double* uQ;    // [L][N] NTT form
+  const double* base;  // [L][N] or null
+  double* out;         // [L][N]
+  uint32_t gal;        // permutation of base (1 = none)
+};
+void moddown(const fa_ctx* c, const MdItem* items, int count, hipStream_t s);
 
 // Key-switch inner product with the automorphism folded in:
 // u[j] (+)= sum_i sigma_{g_j}(ext[j or 0]_i) * key_j[i]  over all np primes.
 struct KsItem {
   const double* ext;  // [dnum][np][N]
+  const double* c1;   // [L][N] NTT form: the digits' own limbs
   const double* key;  // [dnum][2][np][N]
   double* u;          // [2][np][N]
+  const double* c0;   // [L][N] or null: adds P * sigma(c0) to u0 on the ciphertext primes
   uint32_t gal;       // Galois element
 };
 void ks_inner(const fa_ctx* c, const KsItem* items, int count, bool accumulate, hipStream_t s);
 
-// out[h][t][k] = base_h[t][pi_g(k)] + (u[h][t][k] - conv[h][t][k]) * P^-1   (canonical)
-// for h = 0, 1; base_h may be null (treated as 0).
-struct FinishItem {
-  const double* u;      // [2][np][N]
-  const double* conv;   // [2][L][N]
-  const double* base0;  // [L][N] or null
-  const double* base1;  // [L][N] or null
-  double* out;          // [2][L][N]
-  uint32_t gal;         // permutation applied to base0/base1 (1 = none)
-};
-void moddown_finish(const fa_ctx* c, const FinishItem* items, int count, hipStream_t s);
 
-// acc[blk][g][2][L][N] = sum_b pts[blk][(g*B+b)][L][N] * qrot[b][2][L][N]
-void mac_diag(const fa_ctx* c, const double* qrot, const double* const* blocks, int n_blocks, int B, int G,
-              double* acc, hipStream_t s);
+// acc[blk][g][2][L][N] = sum_b pts[blk][(g*B+b)][L][N] * rot_b[2][L][N]
+// with rot_0 = q and rot_b = qrot[b-1] for b >= 1.
+void mac_diag(const fa_ctx* c, const double* q, const double* qrot, const double* const* blocks, int n_blocks,
+              int B, int G, double* acc, hipStream_t s);
 
 // out[w] = ct * pt[w] (both polys), w < count
 void mul_plain(const fa_ctx* c, const double* ct, const double* const* pts, int count, double* out, hipStream_t s);
@@ -128,5 +140,30 @@ void keygen_combine(const fa_ctx* c, double* key, const double* e_ntt, uint32_t 
 void enc_combine(const fa_ctx* c, double* ct, const double* v, hipStream_t s);
 // decryption: out[t] = c0[t] + c1[t]*s[t]
 void dec_combine(const fa_ctx* c, const double* ct, double* out, hipStream_t s);
+
+// Collects limbs for batched transforms; launches every FA_MAXL limbs and on flush.
+struct LimbBatch {
+  const fa_ctx* c;
+  hipStream_t s;
+  bool fwd;
+  LimbList l;
+  LimbBatch(const fa_ctx* c_, hipStream_t s_, bool fwd_) : c(c_), s(s_), fwd(fwd_) { l.n = 0; }
+  // scale < 0: N^-1 of the prime
+  void add(double* dst, int prime, const double* src = nullptr, double scale = -1.0) {
+    l.ptr[l.n] = dst;
+    l.src[l.n] = src ? src : dst;
+    l.prime[l.n] = prime;
+    l.scale[l.n] = scale < 0.0 ? c->h_ninv[prime] : scale;
+    if (++l.n == FA_MAXL) flush();
+  }
+  void flush() {
+    if (l.n) {
+      if (fwd) ntt_fwd(c, l, s);
+      else ntt_inv(c, l, s);
+      l.n = 0;
+    }
+  }
+  ~LimbBatch() { flush(); }
+};
 
 }  // namespace fa

@@ -18,6 +18,8 @@
 
 #include <hip/hip_runtime.h>
 
+#include <cstdlib>
+
 #include "fa_internal.h"
 
 namespace {
@@ -74,10 +76,16 @@ __device__ __forceinline__ void gs_bfly(double& x, double& y, double winv, doubl
 
 // ---------------------------------------------------------------------------
 // Negacyclic NTT, N = 2^logn = 2^SA * 256, natural order in, bit-reversed out.
-// Stage s pairs elements j and j + N/2^(s+1) with twiddle psi_rev[2^s + (j >> (logn - s))].
-// Pass A runs stages 0..SA-1 on columns (j mod 256 fixed), pass B stages
-// SA..logn-1 on contiguous rows of 256.  Each pass keeps a unit of elements
-// in registers for half its stages, exchanges through LDS, then finishes.
+// Stage s pairs elements j and j + N/2^(s+1) with twiddle
+//   w(s, j) = psi^brev(2^s + (j >> (logn - s)))       (brev over logn bits).
+// Pass A runs stages 0..SA-1 on columns (j mod 256 fixed): its twiddles are
+// the first 2^SA table entries.  Pass B runs stages SA..SA+7 on contiguous
+// rows of 256; for row r and stage SA + s' the twiddle factors as
+//   w = f[r][s'] * T[2^s' + i'],  f[r][s'] = psi^((2 brev_SA(r) + 1) 2^(7-s')),
+//   T[2^s' + i'] = psi^(brev_s'(i') N / 2^s'),
+// so pass B reads 8 row factors and a 256-entry table instead of N entries.
+// Each pass keeps a unit of elements in registers for half its stages,
+// exchanges through LDS, then finishes.
 // ---------------------------------------------------------------------------
 template <int SA>
 struct PassA {
@@ -90,22 +98,35 @@ struct PassA {
   static constexpr int TILE = COLS * H;
 };
 
-template <int SA>
-__global__ __launch_bounds__(256) void k_ntt_fwd_a(LimbList ll, const DevPrime* __restrict__ pr,
-                                                   const double* __restrict__ tw, int logn) {
+// loaders for the first pass of the forward transform
+struct PlainLd {
+  const double* src;
+  __device__ double operator()(size_t i) const { return src[i]; }
+};
+// fast basis conversion of NS canonical inputs y_j = [x_j (S/s_j)^-1]_{s_j}
+// into the target prime: sum_j y_j * ((S/s_j) mod q)   (lazily reduced)
+template <int NS>
+struct ConvLd {
+  const double* y[NS];
+  double h[NS], hp[NS];
+  double q, qinv;
+  __device__ double operator()(size_t i) const {
+    double acc = 0.0;
+#pragma unroll
+    for (int j = 0; j < NS; ++j) acc += mulc(y[j][i], h[j], hp[j], q);
+    return reduce(acc, q, qinv);
+  }
+};
+
+template <int SA, class Ld>
+__device__ __forceinline__ void fwd_a_body(const Ld& ld, double* a, const double* __restrict__ w, double q,
+                                           double qinv, int col0, double* sm) {
   using P = PassA<SA>;
-  __shared__ double sm[P::TILE];
-  const int n = 1 << logn;
-  const int pi = ll.prime[blockIdx.y];
-  double* __restrict__ a = ll.ptr[blockIdx.y];
-  const double q = pr[pi].q, qinv = pr[pi].qinv;
-  const double* __restrict__ w = tw + (size_t)pi * n;
-  const int col0 = blockIdx.x * P::COLS;
   for (int u = threadIdx.x; u < P::TILE / P::E1; u += 256) {
     const int c = u % P::COLS, hl = u / P::COLS;
     double x[P::E1];
 #pragma unroll
-    for (int m = 0; m < P::E1; ++m) x[m] = a[((size_t)(hl + (m << P::S2)) << 8) + col0 + c];
+    for (int m = 0; m < P::E1; ++m) x[m] = ld(((size_t)(hl + (m << P::S2)) << 8) + col0 + c);
 #pragma unroll
     for (int s = 0; s < P::S1; ++s) {
       const int half = P::E1 >> (s + 1);
@@ -139,15 +160,88 @@ __global__ __launch_bounds__(256) void k_ntt_fwd_a(LimbList ll, const DevPrime* 
 }
 
 template <int SA>
-__global__ __launch_bounds__(256) void k_ntt_inv_a(LimbList ll, const DevPrime* __restrict__ pr,
-                                                   const double* __restrict__ tw, int logn) {
+__global__ __launch_bounds__(256) void k_ntt_fwd_a(LimbList ll, const DevPrime* __restrict__ pr,
+                                                   const double* __restrict__ twa) {
   using P = PassA<SA>;
   __shared__ double sm[P::TILE];
+  const int pi = ll.prime[blockIdx.y];
+  const double q = pr[pi].q, qinv = pr[pi].qinv;
+  fwd_a_body<SA>(PlainLd{ll.src[blockIdx.y]}, ll.ptr[blockIdx.y], twa + (size_t)pi * 256, q, qinv,
+                 blockIdx.x * P::COLS, sm);
+}
+
+// ModUp, first pass: ext[i][t] = pass A of Conv_{digit i -> t}(y), for every
+// digit i and prime t outside the digit; y holds the digit-scaled
+// coefficients of c1 (inverse transform with the conversion constant folded
+// into its final scaling).
+struct MuArgs {
+  fa::MuItem it[FA_MAXMU];
+};
+
+template <int SA, int ALPHA>
+__global__ __launch_bounds__(256) void k_modup_a(MuArgs args, const DevPrime* __restrict__ pr,
+                                                 const double* __restrict__ twa, const double* __restrict__ hat,
+                                                 int logn, int L, int np) {
+  using P = PassA<SA>;
+  __shared__ double sm[P::TILE];
+  const int i = blockIdx.y / np, t = blockIdx.y % np;
+  const int lo = i * ALPHA;
+  if (t >= lo && t < lo + ALPHA && t < L) return;  // own limbs: read from c1 directly
+  const fa::MuItem& it = args.it[blockIdx.z];
   const int n = 1 << logn;
+  ConvLd<ALPHA> ld;
+  ld.q = pr[t].q;
+  ld.qinv = pr[t].qinv;
+#pragma unroll
+  for (int j = 0; j < ALPHA; ++j) {
+    const bool ok = lo + j < L;  // a short last digit converts fewer primes
+    ld.y[j] = it.y + (size_t)(ok ? lo + j : lo) * n;
+    ld.h[j] = ok ? hat[((size_t)i * ALPHA + j) * np + t] : 0.0;
+    ld.hp[j] = ld.h[j] * ld.qinv;
+  }
+  fwd_a_body<SA>(ld, it.ext + ((size_t)i * np + t) * n, twa + (size_t)t * 256, ld.q, ld.qinv, blockIdx.x * P::COLS,
+                 sm);
+}
+
+// ModDown, first pass: conv[t] = pass A of Conv_{P -> q_t}(y_P), where y_P
+// holds the scaled special-prime coefficients of the key-switch product.
+struct MdArgs {
+  fa::MdItem it[FA_MAXMD];
+};
+
+template <int SA, int KP>
+__global__ __launch_bounds__(256) void k_moddown_a(MdArgs args, const DevPrime* __restrict__ pr,
+                                                   const double* __restrict__ twa, const double* __restrict__ hat,
+                                                   int logn, int L) {
+  using P = PassA<SA>;
+  __shared__ double sm[P::TILE];
+  const int t = blockIdx.y;
+  const fa::MdItem& it = args.it[blockIdx.z];
+  const int n = 1 << logn;
+  ConvLd<KP> ld;
+  ld.q = pr[t].q;
+  ld.qinv = pr[t].qinv;
+#pragma unroll
+  for (int k = 0; k < KP; ++k) {
+    ld.y[k] = it.yP + (size_t)k * n;
+    ld.h[k] = hat[(size_t)k * L + t];
+    ld.hp[k] = ld.h[k] * ld.qinv;
+  }
+  fwd_a_body<SA>(ld, it.conv + (size_t)t * n, twa + (size_t)t * 256, ld.q, ld.qinv, blockIdx.x * P::COLS, sm);
+}
+
+// inverse pass A (the last pass of the inverse transform): columns; the final
+// multiply uses a per-limb constant (N^-1, or N^-1 times a basis-conversion
+// factor) and leaves canonical residues.
+template <int SA>
+__global__ __launch_bounds__(256) void k_ntt_inv_a(LimbList ll, const DevPrime* __restrict__ pr,
+                                                   const double* __restrict__ twa) {
+  using P = PassA<SA>;
+  __shared__ double sm[P::TILE];
   const int pi = ll.prime[blockIdx.y];
   double* __restrict__ a = ll.ptr[blockIdx.y];
   const double q = pr[pi].q, qinv = pr[pi].qinv;
-  const double* __restrict__ w = tw + (size_t)pi * n;
+  const double* __restrict__ w = twa + (size_t)pi * 256;
   const int col0 = blockIdx.x * P::COLS;
   for (int u = threadIdx.x; u < P::TILE / P::E2; u += 256) {
     const int c = u % P::COLS, hh = u / P::COLS;
@@ -167,7 +261,7 @@ __global__ __launch_bounds__(256) void k_ntt_inv_a(LimbList ll, const DevPrime* 
     for (int m = 0; m < P::E2; ++m) sm[((hh << P::S2) + m) * P::COLS + c] = x[m];
   }
   __syncthreads();
-  const double ninv = pr[pi].ninv, ninvp = ninv * qinv;
+  const double sc = ll.scale[blockIdx.y], scp = sc * qinv;
   for (int u = threadIdx.x; u < P::TILE / P::E1; u += 256) {
     const int c = u % P::COLS, hl = u / P::COLS;
     double x[P::E1];
@@ -184,26 +278,63 @@ __global__ __launch_bounds__(256) void k_ntt_inv_a(LimbList ll, const DevPrime* 
     }
 #pragma unroll
     for (int m = 0; m < P::E1; ++m)
-      a[((size_t)(hl + (m << P::S2)) << 8) + col0 + c] = canon_full(mulc(x[m], ninv, ninvp, q), q, qinv);
+      a[((size_t)(hl + (m << P::S2)) << 8) + col0 + c] = canon_full(mulc(x[m], sc, scp, q), q, qinv);
   }
 }
 
-// Pass B: rows of 256 contiguous elements, stages SA..SA+7.  Row stride in
-// LDS is 272 words (one pad word per 16) so that both access patterns spread
-// over all banks.
+// Pass B: rows of 256 contiguous elements.  Row stride in LDS is 272 words
+// (one pad word per 16) so that both access patterns spread over all banks.
 #define ROWW 272
 __device__ __forceinline__ int lds_row(int rl, int lo) { return rl * ROWW + lo + (lo >> 4); }
 
-__global__ __launch_bounds__(256) void k_ntt_fwd_b(LimbList ll, const DevPrime* __restrict__ pr,
-                                                   const double* __restrict__ tw, int logn) {
-  __shared__ double sm[16 * ROWW];
-  const int n = 1 << logn, SA = logn - 8;
+// twiddle of pass B for stage SA+s', row r, index i' (see the header above)
+__device__ __forceinline__ double twb(const double* __restrict__ T, double f, int s1, int i1, double q, double qinv) {
+  const double t = T[(1 << s1) + i1];
+  return mulc(t, f, f * qinv, q);
+}
+
+// stores for the last pass of the forward transform (16 consecutive elements)
+struct CanonSt {
+  double* a;
+  double q, qinv;
+  __device__ void operator()(size_t i0, const double (&x)[16]) const {
+    double2* dst = reinterpret_cast<double2*>(a + i0);
+#pragma unroll
+    for (int m = 0; m < 8; ++m) dst[m] = make_double2(canon_full(x[2 * m], q, qinv), canon_full(x[2 * m + 1], q, qinv));
+  }
+};
+// ModDown finish: out[k] = base[pi(k)] + (u_Q[k] - conv^[k]) * P^-1
+struct FinishSt {
+  const double* uQ;
+  const double* base;
+  double* out;
+  uint32_t gal;
+  int logn;
+  double q, qinv, pv, pvp;
+  __device__ void operator()(size_t i0, const double (&x)[16]) const {
+    double r[16];
+#pragma unroll
+    for (int m = 0; m < 16; ++m) r[m] = mulc(uQ[i0 + m] - x[m], pv, pvp, q);
+    if (base) {
+#pragma unroll
+      for (int m = 0; m < 16; ++m) {
+        const uint32_t k = (uint32_t)(i0 + m);
+        r[m] += base[gal == 1u ? k : perm(k, gal, logn)];
+      }
+    }
+    double2* dst = reinterpret_cast<double2*>(out + i0);
+#pragma unroll
+    for (int m = 0; m < 8; ++m) dst[m] = make_double2(canon_full(r[2 * m], q, qinv), canon_full(r[2 * m + 1], q, qinv));
+  }
+};
+
+template <class St>
+__device__ __forceinline__ void fwd_b_body(double* a, const St& st, const double* __restrict__ T,
+                                           const double* __restrict__ F, double q, double qinv, int logn,
+                                           double* sm) {
+  const int n = 1 << logn;
   const int rows = (n >> 8) < 16 ? (n >> 8) : 16;
   const int row0 = blockIdx.x * rows;
-  const int pi = ll.prime[blockIdx.y];
-  double* __restrict__ a = ll.ptr[blockIdx.y];
-  const double q = pr[pi].q, qinv = pr[pi].qinv;
-  const double* __restrict__ w = tw + (size_t)pi * n;
   for (int u = threadIdx.x; u < rows * 16; u += 256) {
     const int l0 = u & 15, rl = u >> 4, r = row0 + rl;
     double x[16];
@@ -212,10 +343,11 @@ __global__ __launch_bounds__(256) void k_ntt_fwd_b(LimbList ll, const DevPrime* 
 #pragma unroll
     for (int s1 = 0; s1 < 4; ++s1) {
       const int half = 8 >> s1;
+      const double f = F[r * 8 + s1];
 #pragma unroll
       for (int m = 0; m < 16; ++m) {
         if (m & half) continue;
-        ct_bfly(x[m], x[m + half], w[(1 << (SA + s1)) + (r << s1) + (m >> (4 - s1))], q, qinv);
+        ct_bfly(x[m], x[m + half], twb(T, f, s1, m >> (4 - s1), q, qinv), q, qinv);
       }
     }
 #pragma unroll
@@ -230,33 +362,59 @@ __global__ __launch_bounds__(256) void k_ntt_fwd_b(LimbList ll, const DevPrime* 
 #pragma unroll
     for (int s1 = 4; s1 < 8; ++s1) {
       const int half = 8 >> (s1 - 4);
+      const double f = F[r * 8 + s1];
 #pragma unroll
       for (int m = 0; m < 16; ++m) {
         if (m & half) continue;
-        ct_bfly(x[m], x[m + half], w[(1 << (SA + s1)) + (r << s1) + (lh << (s1 - 4)) + (m >> (8 - s1))], q, qinv);
+        ct_bfly(x[m], x[m + half], twb(T, f, s1, (lh << (s1 - 4)) + (m >> (8 - s1)), q, qinv), q, qinv);
       }
     }
-    double2* dst = reinterpret_cast<double2*>(a + (size_t)r * 256 + 16 * lh);
-#pragma unroll
-    for (int m = 0; m < 8; ++m)
-      dst[m] = make_double2(canon_full(x[2 * m], q, qinv), canon_full(x[2 * m + 1], q, qinv));
+    st((size_t)r * 256 + 16 * lh, x);
   }
 }
 
-__global__ __launch_bounds__(256) void k_ntt_inv_b(LimbList ll, const DevPrime* __restrict__ pr,
-                                                   const double* __restrict__ tw, int logn) {
+__global__ __launch_bounds__(256) void k_ntt_fwd_b(LimbList ll, const DevPrime* __restrict__ pr,
+                                                   const double* __restrict__ twt, const double* __restrict__ twr,
+                                                   int logn) {
   __shared__ double sm[16 * ROWW];
-  const int n = 1 << logn, SA = logn - 8;
+  const int pi = ll.prime[blockIdx.y];
+  double* a = ll.ptr[blockIdx.y];
+  const double q = pr[pi].q, qinv = pr[pi].qinv;
+  const int H = 1 << (logn - 8);
+  fwd_b_body(a, CanonSt{a, q, qinv}, twt + (size_t)pi * 256, twr + (size_t)pi * H * 8, q, qinv, logn, sm);
+}
+
+__global__ __launch_bounds__(256) void k_moddown_b(MdArgs args, const DevPrime* __restrict__ pr,
+                                                   const double* __restrict__ twt, const double* __restrict__ twr,
+                                                   int logn) {
+  __shared__ double sm[16 * ROWW];
+  const int t = blockIdx.y;
+  const fa::MdItem& it = args.it[blockIdx.z];
+  const int n = 1 << logn;
+  const double q = pr[t].q, qinv = pr[t].qinv, pv = pr[t].pinv;
+  const size_t o = (size_t)t * n;
+  FinishSt st{it.uQ + o, it.base ? it.base + o : nullptr, it.out + o, it.gal, logn, q, qinv, pv, pv * qinv};
+  const int H = 1 << (logn - 8);
+  fwd_b_body(it.conv + o, st, twt + (size_t)t * 256, twr + (size_t)t * H * 8, q, qinv, logn, sm);
+}
+
+// inverse pass B (the first pass of the inverse transform), src -> ptr
+__global__ __launch_bounds__(256) void k_ntt_inv_b(LimbList ll, const DevPrime* __restrict__ pr,
+                                                   const double* __restrict__ twt, const double* __restrict__ twr,
+                                                   int logn) {
+  __shared__ double sm[16 * ROWW];
+  const int n = 1 << logn;
   const int rows = (n >> 8) < 16 ? (n >> 8) : 16;
   const int row0 = blockIdx.x * rows;
   const int pi = ll.prime[blockIdx.y];
-  double* __restrict__ a = ll.ptr[blockIdx.y];
+  double* a = ll.ptr[blockIdx.y];
   const double q = pr[pi].q, qinv = pr[pi].qinv;
-  const double* __restrict__ w = tw + (size_t)pi * n;
+  const double* __restrict__ T = twt + (size_t)pi * 256;
+  const double* __restrict__ F = twr + (size_t)pi * (n >> 8) * 8;
   for (int u = threadIdx.x; u < rows * 16; u += 256) {
     const int lh = u & 15, rl = u >> 4, r = row0 + rl;
     double x[16];
-    const double2* src = reinterpret_cast<const double2*>(a + (size_t)r * 256 + 16 * lh);
+    const double2* src = reinterpret_cast<const double2*>(ll.src[blockIdx.y] + (size_t)r * 256 + 16 * lh);
 #pragma unroll
     for (int m = 0; m < 8; ++m) {
       const double2 v = src[m];
@@ -266,10 +424,11 @@ __global__ __launch_bounds__(256) void k_ntt_inv_b(LimbList ll, const DevPrime* 
 #pragma unroll
     for (int s1 = 7; s1 >= 4; --s1) {
       const int half = 8 >> (s1 - 4);
+      const double f = F[r * 8 + s1];
 #pragma unroll
       for (int m = 0; m < 16; ++m) {
         if (m & half) continue;
-        gs_bfly(x[m], x[m + half], w[(1 << (SA + s1)) + (r << s1) + (lh << (s1 - 4)) + (m >> (8 - s1))], q, qinv);
+        gs_bfly(x[m], x[m + half], twb(T, f, s1, (lh << (s1 - 4)) + (m >> (8 - s1)), q, qinv), q, qinv);
       }
     }
 #pragma unroll
@@ -284,10 +443,11 @@ __global__ __launch_bounds__(256) void k_ntt_inv_b(LimbList ll, const DevPrime* 
 #pragma unroll
     for (int s1 = 3; s1 >= 0; --s1) {
       const int half = 8 >> s1;
+      const double f = F[r * 8 + s1];
 #pragma unroll
       for (int m = 0; m < 16; ++m) {
         if (m & half) continue;
-        gs_bfly(x[m], x[m + half], w[(1 << (SA + s1)) + (r << s1) + (m >> (4 - s1))], q, qinv);
+        gs_bfly(x[m], x[m + half], twb(T, f, s1, m >> (4 - s1), q, qinv), q, qinv);
       }
     }
 #pragma unroll
@@ -296,118 +456,41 @@ __global__ __launch_bounds__(256) void k_ntt_inv_b(LimbList ll, const DevPrime* 
 }
 
 // ---------------------------------------------------------------------------
-// fast basis conversion (no correction term):
-//   Conv_{S->t}(x) = sum_j [x_j * (S/s_j)^-1]_{s_j} * ((S/s_j) mod t)  mod t
-// The bracket is taken canonical in [0, s_j), as the definition requires.
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_conv_modup(const double* __restrict__ c1c, size_t src_stride,
-                                                    double* __restrict__ ext, size_t dst_stride,
-                                                    const DevPrime* __restrict__ pr,
-                                                    const double* __restrict__ inv, const double* __restrict__ hat,
-                                                    int logn, int L, int np, int alpha) {
-  const int n = 1 << logn;
-  const int k = blockIdx.x * 256 + threadIdx.x;
-  const int i = blockIdx.y;
-  const int b = blockIdx.z;
-  const int lo = i * alpha;
-  const int hi = min(lo + alpha, L);
-  const double* __restrict__ src = c1c + (size_t)b * src_stride;
-  double* __restrict__ dst = ext + (size_t)b * dst_stride + (size_t)i * np * n;
-  double y[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    if (lo + j < hi) {
-      const double q = pr[lo + j].q, qinv = pr[lo + j].qinv, iv = inv[i * alpha + j];
-      y[j] = canon(mulc(src[(size_t)(lo + j) * n + k], iv, iv * qinv, q), q);
-    } else {
-      y[j] = 0.0;
-    }
-  }
-  for (int t = 0; t < np; ++t) {
-    if (t >= lo && t < hi) continue;
-    const double q = pr[t].q, qinv = pr[t].qinv;
-    double acc = 0.0;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      if (lo + j < hi) {
-        const double hv = hat[((size_t)i * alpha + j) * np + t];
-        acc += mulc(y[j], hv, hv * qinv, q);
-      }
-    }
-    dst[(size_t)t * n + k] = reduce(acc, q, qinv);
-  }
-}
-
-__global__ __launch_bounds__(256) void k_conv_moddown(const double* __restrict__ up, size_t src_stride,
-                                                      double* __restrict__ out, size_t dst_stride,
-                                                      const DevPrime* __restrict__ pr,
-                                                      const double* __restrict__ inv,
-                                                      const double* __restrict__ hat, int logn, int L, int K) {
-  const int n = 1 << logn;
-  const int k = blockIdx.x * 256 + threadIdx.x;
-  const int b = blockIdx.y;
-  const double* __restrict__ src = up + (size_t)b * src_stride;
-  double* __restrict__ dst = out + (size_t)b * dst_stride;
-  double y[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    if (j < K) {
-      const double q = pr[L + j].q, qinv = pr[L + j].qinv, iv = inv[j];
-      y[j] = canon(mulc(src[(size_t)j * n + k], iv, iv * qinv, q), q);
-    } else {
-      y[j] = 0.0;
-    }
-  }
-  for (int t = 0; t < L; ++t) {
-    const double q = pr[t].q, qinv = pr[t].qinv;
-    double acc = 0.0;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      if (j < K) {
-        const double hv = hat[(size_t)j * L + t];
-        acc += mulc(y[j], hv, hv * qinv, q);
-      }
-    }
-    dst[(size_t)t * n + k] = reduce(acc, q, qinv);
-  }
-}
-
-__global__ __launch_bounds__(256) void k_scatter_own(const double* __restrict__ c1, size_t src_stride,
-                                                     double* __restrict__ ext, size_t dst_stride, int logn,
-                                                     int L, int np, int alpha) {
-  const int n = 1 << logn;
-  const int k = blockIdx.x * 256 + threadIdx.x;
-  const int t = blockIdx.y;
-  const int b = blockIdx.z;
-  const int i = t / alpha;
-  ext[(size_t)b * dst_stride + ((size_t)i * np + t) * n + k] = c1[(size_t)b * src_stride + (size_t)t * n + k];
-}
-
-// ---------------------------------------------------------------------------
-// key-switch inner product with the automorphism folded into the read of ext
+// key-switch inner product with the automorphism folded into the read of the
+// extended digits; a digit's own limbs are read from c1 itself
 // ---------------------------------------------------------------------------
 #define FA_MAXKS 32
 struct KsArgs {
-  int count;
   fa::KsItem it[FA_MAXKS];
 };
 
-__global__ __launch_bounds__(256) void k_ks_inner(KsArgs args, const DevPrime* __restrict__ pr, int logn, int np,
-                                                  int dnum, int accumulate) {
+template <int DNUM>
+__global__ __launch_bounds__(256) void k_ks_inner(KsArgs args, const DevPrime* __restrict__ pr, int logn, int L,
+                                                  int np, int alpha, int accumulate) {
   const int n = 1 << logn;
   const int k = blockIdx.x * 256 + threadIdx.x;
   const int t = blockIdx.y;
   const fa::KsItem& it = args.it[blockIdx.z];
   const double q = pr[t].q, qinv = pr[t].qinv;
   const uint32_t kk = perm((uint32_t)k, it.gal, logn);
-  double acc0 = 0.0, acc1 = 0.0;
-  for (int i = 0; i < dnum; ++i) {
-    const double x = it.ext[((size_t)i * np + t) * n + kk];
-    const double kb = it.key[(((size_t)i * 2 + 0) * np + t) * n + k];
-    const double ka = it.key[(((size_t)i * 2 + 1) * np + t) * n + k];
-    acc0 += mul(x, kb, q, qinv);
-    acc1 += mul(x, ka, q, qinv);
+  const int own = t < L ? t / alpha : -1;
+  double x[DNUM], kb[DNUM], ka[DNUM];
+#pragma unroll
+  for (int i = 0; i < DNUM; ++i) {
+    const double* src = i == own ? it.c1 + (size_t)t * n : it.ext + ((size_t)i * np + t) * n;
+    x[i] = src[kk];
+    kb[i] = __builtin_nontemporal_load(it.key + (((size_t)i * 2 + 0) * np + t) * n + k);
+    ka[i] = __builtin_nontemporal_load(it.key + (((size_t)i * 2 + 1) * np + t) * n + k);
   }
+  double acc0 = 0.0, acc1 = 0.0;
+#pragma unroll
+  for (int i = 0; i < DNUM; ++i) {
+    acc0 += mul(x[i], kb[i], q, qinv);
+    acc1 += mul(x[i], ka[i], q, qinv);
+  }
+  // P * sigma(c0) on the ciphertext primes: ModDown of the sum then returns
+  // ModDown(sum u0) + sigma(c0) exactly, so the giant-step c0 terms ride along.
+  if (it.c0 && t < L) acc0 += mul(it.c0[(size_t)t * n + kk], pr[t].pmod, q, qinv);
   double* u0 = it.u + (size_t)t * n + k;
   double* u1 = it.u + ((size_t)np + t) * n + k;
   if (accumulate) {
@@ -416,30 +499,6 @@ __global__ __launch_bounds__(256) void k_ks_inner(KsArgs args, const DevPrime* _
   }
   *u0 = canon_full(acc0, q, qinv);
   *u1 = canon_full(acc1, q, qinv);
-}
-
-#define FA_MAXFIN 32
-struct FinArgs {
-  int count;
-  fa::FinishItem it[FA_MAXFIN];
-};
-
-__global__ __launch_bounds__(256) void k_moddown_finish(FinArgs args, const DevPrime* __restrict__ pr, int logn,
-                                                        int L, int np) {
-  const int n = 1 << logn;
-  const int k = blockIdx.x * 256 + threadIdx.x;
-  const int t = blockIdx.y;
-  const fa::FinishItem& it = args.it[blockIdx.z];
-  const double q = pr[t].q, qinv = pr[t].qinv, pv = pr[t].pinv, pvp = pv * qinv;
-  const uint32_t kk = it.gal == 1u ? (uint32_t)k : perm((uint32_t)k, it.gal, logn);
-  const size_t o = (size_t)t * n + k;
-  for (int h = 0; h < 2; ++h) {
-    const double* base = h == 0 ? it.base0 : it.base1;
-    const double v = it.u[(size_t)h * np * n + o] - it.conv[(size_t)h * L * n + o];
-    double r = mulc(v, pv, pvp, q);
-    if (base) r += base[(size_t)t * n + kk];
-    it.out[(size_t)h * L * n + o] = canon_full(r, q, qinv);
-  }
 }
 
 // ---------------------------------------------------------------------------
@@ -451,10 +510,11 @@ __global__ __launch_bounds__(256) void k_moddown_finish(FinArgs args, const DevP
 // ---------------------------------------------------------------------------
 #define FA_MAXBLK 32
 struct MacArgs {
-  const double* qrot;
+  const double* q0;    // rotation 0: the query
+  const double* qrot;  // rotations 1..B-1: [B-1][2][L][N]
   const double* blk[FA_MAXBLK];
   double* acc;
-  int n_pairs, pair0, B, G, L;
+  int n_pairs, pair0, B, logG, L;
 };
 
 template <int NACC>
@@ -464,32 +524,32 @@ __global__ __launch_bounds__(256) void k_mac_diag(MacArgs args, const DevPrime* 
   const size_t f = (size_t)blockIdx.x * 256 + threadIdx.x;
   const int t = (int)(f >> logn);
   const double q = pr[t].q, qinv = pr[t].qinv;
-  const int cnt = min(NACC, args.n_pairs - args.pair0);
-  const double* __restrict__ pbase[NACC];
-#pragma unroll
-  for (int i = 0; i < NACC; ++i) {
-    const int pair = args.pair0 + (i < cnt ? i : 0);
-    const int blk = pair / args.G, g = pair % args.G;
-    pbase[i] = args.blk[blk] + (size_t)g * args.B * ln + f;
-  }
+  const int last = args.n_pairs - 1;
+  const int G = 1 << args.logG;
   double a0[NACC], a1[NACC];
 #pragma unroll
   for (int i = 0; i < NACC; ++i) {
     a0[i] = 0.0;
     a1[i] = 0.0;
   }
-  const double* __restrict__ qr = args.qrot + f;
   for (int b = 0; b < args.B; ++b) {
-    const double x0 = qr[(size_t)(2 * b) * ln];
-    const double x1 = qr[(size_t)(2 * b + 1) * ln];
+    const double* __restrict__ qb = b == 0 ? args.q0 : args.qrot + (size_t)(b - 1) * 2 * ln;
+    const double x0 = qb[f];
+    const double x1 = qb[ln + f];
+    // every load of this step is issued before any arithmetic; pairs past the
+    // end re-read the last pair (in bounds) and are never stored
+    double p[NACC];
+#pragma unroll
+    for (int i = 0; i < NACC; ++i) {
+      const int pair = min(args.pair0 + i, last);
+      const double* base = args.blk[pair >> args.logG];
+      p[i] = __builtin_nontemporal_load(base + (size_t)((pair & (G - 1)) * args.B + b) * ln + f);
+    }
     const double x0p = x0 * qinv, x1p = x1 * qinv;
 #pragma unroll
     for (int i = 0; i < NACC; ++i) {
-      if (i < cnt) {
-        const double p = pbase[i][(size_t)b * ln];
-        a0[i] += mulc(p, x0, x0p, q);
-        a1[i] += mulc(p, x1, x1p, q);
-      }
+      a0[i] += mulc(p[i], x0, x0p, q);
+      a1[i] += mulc(p[i], x1, x1p, q);
     }
     if ((b & 7) == 7) {
 #pragma unroll
@@ -499,6 +559,7 @@ __global__ __launch_bounds__(256) void k_mac_diag(MacArgs args, const DevPrime* 
       }
     }
   }
+  const int cnt = min(NACC, args.n_pairs - args.pair0);
 #pragma unroll
   for (int i = 0; i < NACC; ++i) {
     if (i < cnt) {
@@ -621,10 +682,10 @@ template <int SA>
 static void launch_fwd(const fa_ctx* c, const LimbList& l, hipStream_t s) {
   using P = PassA<SA>;
   dim3 ga(c->n / P::TILE, l.n);
-  hipLaunchKernelGGL(k_ntt_fwd_a<SA>, ga, dim3(256), 0, s, l, c->d_pr, c->d_tw_fwd, c->logn);
+  hipLaunchKernelGGL(k_ntt_fwd_a<SA>, ga, dim3(256), 0, s, l, c->d_pr, c->d_twa_fwd);
   const int rows = (c->n >> 8) < 16 ? (c->n >> 8) : 16;
   dim3 gb((c->n >> 8) / rows, l.n);
-  hipLaunchKernelGGL(k_ntt_fwd_b, gb, dim3(256), 0, s, l, c->d_pr, c->d_tw_fwd, c->logn);
+  hipLaunchKernelGGL(k_ntt_fwd_b, gb, dim3(256), 0, s, l, c->d_pr, c->d_twt_fwd, c->d_twr_fwd, c->logn);
 }
 
 template <int SA>
@@ -632,52 +693,37 @@ static void launch_inv(const fa_ctx* c, const LimbList& l, hipStream_t s) {
   using P = PassA<SA>;
   const int rows = (c->n >> 8) < 16 ? (c->n >> 8) : 16;
   dim3 gb((c->n >> 8) / rows, l.n);
-  hipLaunchKernelGGL(k_ntt_inv_b, gb, dim3(256), 0, s, l, c->d_pr, c->d_tw_inv, c->logn);
+  hipLaunchKernelGGL(k_ntt_inv_b, gb, dim3(256), 0, s, l, c->d_pr, c->d_twt_inv, c->d_twr_inv, c->logn);
   dim3 ga(c->n / P::TILE, l.n);
-  hipLaunchKernelGGL(k_ntt_inv_a<SA>, ga, dim3(256), 0, s, l, c->d_pr, c->d_tw_inv, c->logn);
+  hipLaunchKernelGGL(k_ntt_inv_a<SA>, ga, dim3(256), 0, s, l, c->d_pr, c->d_twa_inv);
 }
+
+#define FA_SA_SWITCH(fn, ...)            \
+  switch (c->logn - 8) {                  \
+    case 2: fn<2>(__VA_ARGS__); break;    \
+    case 3: fn<3>(__VA_ARGS__); break;    \
+    case 4: fn<4>(__VA_ARGS__); break;    \
+    case 5: fn<5>(__VA_ARGS__); break;    \
+    case 6: fn<6>(__VA_ARGS__); break;    \
+    case 7: fn<7>(__VA_ARGS__); break;    \
+    case 8: fn<8>(__VA_ARGS__); break;    \
+    default: break;                       \
+  }
 
 void ntt_fwd(const fa_ctx* c, const LimbList& l, hipStream_t s) {
   if (l.n == 0) return;
-  switch (c->logn - 8) {
-    case 2: launch_fwd<2>(c, l, s); break;
-    case 3: launch_fwd<3>(c, l, s); break;
-    case 4: launch_fwd<4>(c, l, s); break;
-    case 5: launch_fwd<5>(c, l, s); break;
-    case 6: launch_fwd<6>(c, l, s); break;
-    case 7: launch_fwd<7>(c, l, s); break;
-    case 8: launch_fwd<8>(c, l, s); break;
-    default: break;
-  }
+  FA_SA_SWITCH(launch_fwd, c, l, s)
 }
 
 void ntt_inv(const fa_ctx* c, const LimbList& l, hipStream_t s) {
   if (l.n == 0) return;
-  switch (c->logn - 8) {
-    case 2: launch_inv<2>(c, l, s); break;
-    case 3: launch_inv<3>(c, l, s); break;
-    case 4: launch_inv<4>(c, l, s); break;
-    case 5: launch_inv<5>(c, l, s); break;
-    case 6: launch_inv<6>(c, l, s); break;
-    case 7: launch_inv<7>(c, l, s); break;
-    case 8: launch_inv<8>(c, l, s); break;
-    default: break;
-  }
+  FA_SA_SWITCH(launch_inv, c, l, s)
 }
 
 static void strided(const fa_ctx* c, double* base, size_t stride, int count, int period, int prime_off,
                     hipStream_t s, bool fwd) {
-  LimbList l;
-  l.n = 0;
-  for (int i = 0; i < count; ++i) {
-    l.ptr[l.n] = base + (size_t)i * stride;
-    l.prime[l.n] = i % period + prime_off;
-    if (++l.n == FA_MAXL) {
-      fwd ? ntt_fwd(c, l, s) : ntt_inv(c, l, s);
-      l.n = 0;
-    }
-  }
-  if (l.n) fwd ? ntt_fwd(c, l, s) : ntt_inv(c, l, s);
+  LimbBatch b(c, s, fwd);
+  for (int i = 0; i < count; ++i) b.add(base + (size_t)i * stride, i % period + prime_off);
 }
 
 void ntt_fwd_strided(const fa_ctx* c, double* base, size_t stride, int count, int period, int prime_off,
@@ -689,86 +735,151 @@ void ntt_inv_strided(const fa_ctx* c, double* base, size_t stride, int count, in
   strided(c, base, stride, count, period, prime_off, s, false);
 }
 
-void ntt_fwd_ext(const fa_ctx* c, double* ext, size_t stride, int batch, hipStream_t s) {
+template <int SA, int ALPHA>
+static void launch_modup_a(const fa_ctx* c, const MuArgs& a, int count, hipStream_t s) {
+  using P = PassA<SA>;
+  dim3 g(c->n / P::TILE, c->dnum * c->np, count);
+  hipLaunchKernelGGL((k_modup_a<SA, ALPHA>), g, dim3(256), 0, s, a, c->d_pr, c->d_twa_fwd, c->d_mu_hat, c->logn,
+                     c->L, c->np);
+}
+template <int SA>
+static void launch_modup_a_sa(const fa_ctx* c, const MuArgs& a, int count, hipStream_t s) {
+  switch (c->alpha) {
+    case 1: launch_modup_a<SA, 1>(c, a, count, s); break;
+    case 2: launch_modup_a<SA, 2>(c, a, count, s); break;
+    case 3: launch_modup_a<SA, 3>(c, a, count, s); break;
+    case 4: launch_modup_a<SA, 4>(c, a, count, s); break;
+    default: break;
+  }
+}
+
+void modup_ntt(const fa_ctx* c, const MuItem* items, int count, hipStream_t s) {
+  for (int off = 0; off < count; off += FA_MAXMU) {
+    const int m = count - off < FA_MAXMU ? count - off : FA_MAXMU;
+    MuArgs a;
+    for (int i = 0; i < m; ++i) a.it[i] = items[off + i];
+    FA_SA_SWITCH(launch_modup_a_sa, c, a, m, s)
+  }
+  // second pass over every converted limb
   LimbList l;
   l.n = 0;
-  const size_t n = c->n;
-  for (int b = 0; b < batch; ++b)
+  const int rows = (c->n >> 8) < 16 ? (c->n >> 8) : 16;
+  dim3 gb((c->n >> 8) / rows, 0);
+  auto flush = [&]() {
+    if (!l.n) return;
+    gb.y = l.n;
+    hipLaunchKernelGGL(k_ntt_fwd_b, gb, dim3(256), 0, s, l, c->d_pr, c->d_twt_fwd, c->d_twr_fwd, c->logn);
+    l.n = 0;
+  };
+  for (int b = 0; b < count; ++b)
     for (int i = 0; i < c->dnum; ++i) {
       const int lo = i * c->alpha, hi = lo + c->alpha < c->L ? lo + c->alpha : c->L;
       for (int t = 0; t < c->np; ++t) {
         if (t >= lo && t < hi) continue;
-        l.ptr[l.n] = ext + (size_t)b * stride + ((size_t)i * c->np + t) * n;
+        l.ptr[l.n] = items[b].ext + ((size_t)i * c->np + t) * c->n;
+        l.src[l.n] = l.ptr[l.n];
         l.prime[l.n] = t;
-        if (++l.n == FA_MAXL) {
-          ntt_fwd(c, l, s);
-          l.n = 0;
-        }
+        l.scale[l.n] = 0.0;
+        if (++l.n == FA_MAXL) flush();
       }
     }
-  if (l.n) ntt_fwd(c, l, s);
+  flush();
 }
 
-void conv_modup(const fa_ctx* c, const double* c1c, size_t src_stride, double* ext, size_t dst_stride, int batch,
-                hipStream_t s) {
-  dim3 g(c->n / 256, c->dnum, batch);
-  hipLaunchKernelGGL(k_conv_modup, g, dim3(256), 0, s, c1c, src_stride, ext, dst_stride, c->d_pr, c->d_mu_inv,
-                     c->d_mu_hat, c->logn, c->L, c->np, c->alpha);
+template <int SA, int KP>
+static void launch_moddown_a(const fa_ctx* c, const MdArgs& a, int count, hipStream_t s) {
+  using P = PassA<SA>;
+  dim3 g(c->n / P::TILE, c->L, count);
+  hipLaunchKernelGGL((k_moddown_a<SA, KP>), g, dim3(256), 0, s, a, c->d_pr, c->d_twa_fwd, c->d_md_hat, c->logn,
+                     c->L);
+}
+template <int SA>
+static void launch_moddown_a_sa(const fa_ctx* c, const MdArgs& a, int count, hipStream_t s) {
+  switch (c->K) {
+    case 1: launch_moddown_a<SA, 1>(c, a, count, s); break;
+    case 2: launch_moddown_a<SA, 2>(c, a, count, s); break;
+    case 3: launch_moddown_a<SA, 3>(c, a, count, s); break;
+    case 4: launch_moddown_a<SA, 4>(c, a, count, s); break;
+    default: break;
+  }
 }
 
-void conv_moddown(const fa_ctx* c, const double* up, size_t src_stride, double* out, size_t dst_stride, int count,
-                  hipStream_t s) {
-  dim3 g(c->n / 256, count);
-  hipLaunchKernelGGL(k_conv_moddown, g, dim3(256), 0, s, up, src_stride, out, dst_stride, c->d_pr, c->d_md_inv,
-                     c->d_md_hat, c->logn, c->L, c->K);
+void moddown(const fa_ctx* c, const MdItem* items, int count, hipStream_t s) {
+  const int rows = (c->n >> 8) < 16 ? (c->n >> 8) : 16;
+  for (int off = 0; off < count; off += FA_MAXMD) {
+    const int m = count - off < FA_MAXMD ? count - off : FA_MAXMD;
+    MdArgs a;
+    for (int i = 0; i < m; ++i) a.it[i] = items[off + i];
+    FA_SA_SWITCH(launch_moddown_a_sa, c, a, m, s)
+    dim3 gb((c->n >> 8) / rows, c->L, m);
+    hipLaunchKernelGGL(k_moddown_b, gb, dim3(256), 0, s, a, c->d_pr, c->d_twt_fwd, c->d_twr_fwd, c->logn);
+  }
 }
 
-void scatter_own(const fa_ctx* c, const double* c1, size_t src_stride, double* ext, size_t dst_stride, int batch,
-                 hipStream_t s) {
-  dim3 g(c->n / 256, c->L, batch);
-  hipLaunchKernelGGL(k_scatter_own, g, dim3(256), 0, s, c1, src_stride, ext, dst_stride, c->logn, c->L, c->np,
-                     c->alpha);
+template <int DNUM>
+static void launch_ks(const fa_ctx* c, const KsArgs& a, int m, bool accumulate, hipStream_t s) {
+  dim3 g(c->n / 256, c->np, m);
+  hipLaunchKernelGGL(k_ks_inner<DNUM>, g, dim3(256), 0, s, a, c->d_pr, c->logn, c->L, c->np, c->alpha,
+                     accumulate ? 1 : 0);
 }
 
 void ks_inner(const fa_ctx* c, const KsItem* items, int count, bool accumulate, hipStream_t s) {
   for (int off = 0; off < count; off += FA_MAXKS) {
     KsArgs a;
-    a.count = count - off < FA_MAXKS ? count - off : FA_MAXKS;
-    for (int i = 0; i < a.count; ++i) a.it[i] = items[off + i];
-    dim3 g(c->n / 256, c->np, a.count);
-    hipLaunchKernelGGL(k_ks_inner, g, dim3(256), 0, s, a, c->d_pr, c->logn, c->np, c->dnum, accumulate ? 1 : 0);
+    const int m = count - off < FA_MAXKS ? count - off : FA_MAXKS;
+    for (int i = 0; i < m; ++i) a.it[i] = items[off + i];
+    switch (c->dnum) {
+      case 1: launch_ks<1>(c, a, m, accumulate, s); break;
+      case 2: launch_ks<2>(c, a, m, accumulate, s); break;
+      case 3: launch_ks<3>(c, a, m, accumulate, s); break;
+      case 4: launch_ks<4>(c, a, m, accumulate, s); break;
+      case 5: launch_ks<5>(c, a, m, accumulate, s); break;
+      case 6: launch_ks<6>(c, a, m, accumulate, s); break;
+      case 7: launch_ks<7>(c, a, m, accumulate, s); break;
+      case 8: launch_ks<8>(c, a, m, accumulate, s); break;
+      default: break;
+    }
   }
 }
 
-void moddown_finish(const fa_ctx* c, const FinishItem* items, int count, hipStream_t s) {
-  for (int off = 0; off < count; off += FA_MAXFIN) {
-    FinArgs a;
-    a.count = count - off < FA_MAXFIN ? count - off : FA_MAXFIN;
-    for (int i = 0; i < a.count; ++i) a.it[i] = items[off + i];
-    dim3 g(c->n / 256, c->L, a.count);
-    hipLaunchKernelGGL(k_moddown_finish, g, dim3(256), 0, s, a, c->d_pr, c->logn, c->L, c->np);
+// Most (block, giant) accumulator pairs one pass keeps in registers: 32 (default),
+// 16 or 8; FA_MAC_PAIRS overrides it for tuning.
+static int mac_pairs_max() {
+  static int v = -1;
+  if (v < 0) {
+    const char* e = getenv("FA_MAC_PAIRS");
+    v = e ? atoi(e) : 32;
+    if (v != 8 && v != 16) v = 32;
   }
+  return v;
 }
 
-void mac_diag(const fa_ctx* c, const double* qrot, const double* const* blocks, int n_blocks, int B, int G,
-              double* acc, hipStream_t s) {
+void mac_diag(const fa_ctx* c, const double* q, const double* qrot, const double* const* blocks, int n_blocks,
+              int B, int G, double* acc, hipStream_t s) {
+  const int pmax = mac_pairs_max();
+  int logG = 0;
+  while ((1 << logG) < G) ++logG;
   for (int b0 = 0; b0 < n_blocks; b0 += FA_MAXBLK) {
     const int nb = n_blocks - b0 < FA_MAXBLK ? n_blocks - b0 : FA_MAXBLK;
     MacArgs a;
+    a.q0 = q;
     a.qrot = qrot;
     for (int i = 0; i < nb; ++i) a.blk[i] = blocks[b0 + i];
     a.acc = acc + (size_t)b0 * G * 2 * c->L * c->n;
     a.n_pairs = nb * G;
     a.B = B;
-    a.G = G;
+    a.logG = logG;
     a.L = c->L;
     dim3 g((unsigned)((size_t)c->L * c->n / 256));
     for (int p0 = 0; p0 < a.n_pairs;) {
       a.pair0 = p0;
       const int left = a.n_pairs - p0;
-      if (left > 8) {
+      if (left > 16 && pmax >= 32) {
         hipLaunchKernelGGL(k_mac_diag<32>, g, dim3(256), 0, s, a, c->d_pr, c->logn);
         p0 += 32;
+      } else if (left > 8 && pmax >= 16) {
+        hipLaunchKernelGGL(k_mac_diag<16>, g, dim3(256), 0, s, a, c->d_pr, c->logn);
+        p0 += 16;
       } else {
         hipLaunchKernelGGL(k_mac_diag<8>, g, dim3(256), 0, s, a, c->d_pr, c->logn);
         p0 += 8;
