@@ -1,15 +1,19 @@
-"""Benchmark: encrypted candidate scoring of one query level on one MI355X.
+"""Benchmark: encrypted candidate scoring on one MI355X.
 
-Default workload: the rerank level of the three-level search -- one
-slot-packed CKKS query ciphertext scored against 110,000 candidate rows of
-dimension 512 (4 diagonal blocks of up to 32,768 rows, 2,048 plaintexts),
-ring N = 2^16, 12 ciphertext primes + 3 special primes of 50 bits, scale
-2^40.  A step is one whole level: hoisted baby rotations of the query, the
-multiply-accumulate stream over every resident plaintext, the giant-step
-rotations and ModDown, ending with the block output ciphertexts in HBM.
+Default workload (``--workload rerank``): the rerank level of the three-level
+search -- one slot-packed CKKS query ciphertext scored against 110,000
+candidate rows of dimension 512 (4 diagonal blocks of up to 32,768 rows,
+2,048 plaintexts), ring N = 2^16, 12 ciphertext primes + 3 special primes of
+50 bits, scale 2^40.  A step is one whole level: hoisted baby rotations of the
+query, the multiply-accumulate stream over every resident plaintext, the
+giant-step rotations and ModDown, ending with the block output ciphertexts in
+HBM.  Other workloads: tiny (row layout + rotate-and-sum), fine (65,536 x 96-d
+at N=2^15), rank (encrypted 512->128 projection, then 16,384 candidates) and
+three_level (32 queries through coarse, fine and rerank levels with the
+client's decrypt and top-k between levels).
 
-Prints one JSON line (rank 0).  Inputs are synthetic (seeded Gaussian
-mixture with near-duplicates standing in for CLIP embeddings).
+Prints one JSON line.  Inputs are synthetic (seeded), see
+paper_2608_21131_amd/workloads.py.
 """
 from __future__ import annotations
 
@@ -25,15 +29,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-
-WORKLOADS = {
-    # name: (log_n, L, K, rows, dim, d, n_comp, dup_frac, default baby step)
-    "rerank": dict(log_n=16, L=12, K=3, rows=110_000, dim=512, d=512, n_comp=4096, dup=0.05, B=64, wid=4,
-                   desc="rerank level: 110,000 x 512-d candidates vs one encrypted query, CKKS N=2^16, "
-                        "12+3 primes of 50 bits, scale 2^40, diagonal blocks"),
-    "fine": dict(log_n=15, L=8, K=2, rows=65_536, dim=96, d=128, n_comp=1024, dup=0.0, B=16, wid=2,
-                 desc="fine level: 65,536 x 96-d (zero-padded to 128) candidates, CKKS N=2^15, 8+2 primes"),
-}
+METRIC = "encrypted candidate scores/sec + ms/level at 110k x 512-dim, one MI355X"
 
 
 def log(*a):
@@ -45,9 +41,12 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="rerank", choices=sorted(WORKLOADS))
+    ap.add_argument("--workload", default="rerank",
+                    choices=["tiny", "fine", "rank", "rerank", "three_level"])
     ap.add_argument("--baby-step", type=int, default=0)
+    ap.add_argument("--queries", type=int, default=0, help="three_level: queries per step (default 32)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-check", action="store_true", help="skip the decrypt-and-compare check")
     ap.add_argument("--copy-calib", action="store_true",
                     help="run one plain 1 GiB device copy before the timed region (HBM counter calibration)")
     ap.add_argument("--traffic", default=None,
@@ -55,172 +54,283 @@ def parse():
     return ap.parse_args()
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU only (the scoring level runs on one MI355X); --gpus {args.gpus} "
-              "is not supported", file=sys.stderr)
-        sys.exit(2)
-    import torch
-    from paper_2608_21131_amd import fa, gen
+class Bench:
+    def __init__(self, args):
+        import torch
+        from paper_2608_21131_amd import fa, workloads as wl
+        self.torch, self.fa, self.wl = torch, fa, wl
+        self.args = args
+        w = wl.WORKLOADS[args.workload]
+        if args.baby_step:
+            w.B = args.baby_step
+        self.w = w
+        torch.cuda.set_device(0)
+        t0 = time.time()
+        self.ctx = fa.Context(w.log_n, w.L, w.K, 40)
+        self.s = wl.secret(w)
+        steps = wl.rotation_steps(w)
+        for i in range(0, len(steps), 8):
+            chunk = steps[i:i + 8]
+            rand = [wl.key_randomness(w, r, self.ctx.primes, self.ctx.dnum) for r in chunk]
+            self.ctx.keygen(self.s, chunk, np.stack([x[0] for x in rand]), np.stack([x[1] for x in rand]))
+        log(f"[bench] {w.name}: keys for {len(steps)} rotations ({time.time() - t0:.1f}s)")
+        self.t0 = t0
 
-    wl = WORKLOADS[args.workload]
-    B = args.baby_step or wl["B"]
-    d = wl["d"]
-    G = d // B
-    log_n, L, K = wl["log_n"], wl["L"], wl["K"]
-    n = 1 << log_n
-    S = n // 2
-    wid = wl["wid"]
-    torch.cuda.set_device(0)
-    t0 = time.time()
-    ctx = fa.Context(log_n, L, K, 40)
-    dnum = ctx.dnum
-    primes = ctx.primes
+    def encrypt(self, v, tag=0):
+        w = self.w
+        a, e = self.wl.enc_randomness(w, self.ctx.primes[:w.L], tag)
+        return self.ctx.encrypt(self.ctx.encode(np.tile(v, w.slots // len(v)), 40), a, e)
 
-    # ---- keys (client side, set-up) ----
-    s = gen.ternary_secret(gen.rng(wid, gen.STREAM_SECRET), n)
-    steps = list(range(1, B)) + [g * B for g in range(1, G)]
-    for i in range(0, len(steps), 8):
-        chunk = steps[i:i + 8]
-        a = np.stack([gen.uniform_residues(gen.rng(wid, gen.STREAM_KEY_A, r), primes, dnum, n) for r in chunk])
-        e = np.stack([gen.rounded_gaussian(gen.rng(wid, gen.STREAM_KEY_E, r), (dnum, n)) for r in chunk])
-        ctx.keygen(s, chunk, a, e)
-    log(f"[bench] keys for {len(steps)} rotations ({time.time() - t0:.1f}s)")
+    def decode(self, ct, i, log_scale):
+        W = self.ctx.ct_words
+        return self.ctx.decode(self.ctx.decrypt(ct[i * W:(i + 1) * W]), log_scale)
 
-    # ---- database (enrollment, resident in HBM) ----
-    g = gen.rng(wid, gen.STREAM_DB)
-    centers = g.standard_normal((wl["n_comp"], wl["dim"]))
-    X = gen.mixture_rows(g, wl["rows"], wl["dim"], wl["n_comp"], sigma=0.3, dup_frac=wl["dup"], centers=centers)
-    n_blocks = -(-wl["rows"] // S)
-    blocks = []
-    for b in range(n_blocks):
-        rows = X[b * S:(b + 1) * S]
-        blocks.append(ctx.encode_db_block(rows, d, fa.LAYOUT_DIAG, B))
-    torch.cuda.synchronize()
-    log(f"[bench] encoded {n_blocks} blocks, {n_blocks * d} plaintexts ({time.time() - t0:.1f}s)")
+    def timed(self, step_fn, steps, warmup):
+        torch = self.torch
+        for _ in range(warmup):
+            step_fn()
+        torch.cuda.synchronize()
+        stream = torch.cuda.current_stream()
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ev0.record(stream)
+        for _ in range(steps):
+            step_fn()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        return ev0.elapsed_time(ev1) / steps
 
-    # ---- query (client encrypts) ----
-    qv = gen.mixture_queries(gen.rng(wid, gen.STREAM_QUERY), 1, wl["dim"], centers)[0]
-    qpad = np.zeros(d)
-    qpad[:wl["dim"]] = qv
-    m = ctx.encode(np.tile(qpad, S // d), 40)
-    ea = gen.uniform_residues(gen.rng(wid, gen.STREAM_ENC_A), primes[:L], 1, n)[0]
-    ee = gen.rounded_gaussian(gen.rng(wid, gen.STREAM_ENC_E), n)
-    q = ctx.encrypt(m, ea, ee)
-    out = ctx.new_ct(n_blocks)
-    ws = ctx.workspace(fa.OP_SCORE, n_blocks, d, B)
-    stream = torch.cuda.current_stream()
 
+def pad(v, d):
+    out = np.zeros(d)
+    out[:len(v)] = v
+    return out
+
+
+def run_diag_level(bn, args):
+    """fine / rerank: one diagonal-layout level over all blocks."""
+    w, ctx, fa = bn.w, bn.ctx, bn.fa
+    X, centers = bn.wl.candidate_rows(w)
+    S = w.slots
+    blocks = [ctx.encode_db_block(X[b * S:(b + 1) * S], w.d, fa.LAYOUT_DIAG, w.B) for b in range(w.n_blocks)]
+    bn.torch.cuda.synchronize()
+    log(f"[bench] encoded {w.n_blocks} blocks, {w.n_blocks * w.d} plaintexts ({time.time() - bn.t0:.1f}s)")
+    qv = bn.wl.query_vectors(w, 1, centers)[0]
+    q = bn.encrypt(pad(qv, w.d))
+    out = ctx.new_ct(w.n_blocks)
+    ws = ctx.workspace(fa.OP_SCORE, w.n_blocks, w.d, w.B)
     if args.copy_calib:
-        src = torch.empty(1 << 27, dtype=torch.float64, device="cuda")
-        dst = torch.empty_like(src)
+        src = bn.torch.empty(1 << 27, dtype=bn.torch.float64, device="cuda")
+        dst = bn.torch.empty_like(src)
         src.fill_(1.0)
         dst.copy_(src)
-        torch.cuda.synchronize()
+        bn.torch.cuda.synchronize()
         del src, dst
-
     ctx.profile(True)
-    for _ in range(args.warmup):
-        ctx.score_block(q, blocks, d, fa.LAYOUT_DIAG, B, out=out, ws=ws)
-    torch.cuda.synchronize()
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     phases = []
-    ev0.record(stream)
-    for _ in range(args.steps):
-        ctx.score_block(q, blocks, d, fa.LAYOUT_DIAG, B, out=out, ws=ws)
+
+    def step():
+        ctx.score_block(q, blocks, w.d, fa.LAYOUT_DIAG, w.B, out=out, ws=ws)
         phases.append(ctx.profile_read())
-    ev1.record(stream)
+
+    ms = bn.timed(step, args.steps, args.warmup)
+    ph = {k: float(np.mean([p[k] for p in phases[args.warmup:]])) for k in phases[0]}
+    err = None
+    if not args.no_check:
+        err = 0.0
+        for b in range(w.n_blocks):
+            rows = X[b * S:(b + 1) * S].astype(np.float64)
+            z = bn.decode(out, b, 80)
+            err = max(err, float(np.max(np.abs(z[:len(rows)] - rows @ qv))))
+    ptw = w.L * w.n
+    mac_bytes = 8 * (w.n_blocks * w.d * ptw + (w.B - 1) * 2 * ptw + 2 * ptw + w.n_blocks * w.G * 2 * ptw)
+    stream_bytes = 8 * w.n_blocks * w.d * ptw
+    return dict(ms=ms, scores=w.rows, phases=ph, err=err, mac_bytes=mac_bytes, stream_bytes=stream_bytes,
+                X=X, cpu=(lambda: cpu_baseline_diag(bn, X, qv)))
+
+
+def run_tiny(bn, args):
+    w, ctx, fa = bn.w, bn.ctx, bn.fa
+    X, _ = bn.wl.candidate_rows(w)
+    pts = ctx.encode_db_block(X, w.d, fa.LAYOUT_ROW)
+    per = w.slots // w.d
+    n_pts = -(-w.rows // per)
+    PW = ctx.pt_words
+    blocks = [pts[i * PW:(i + 1) * PW] for i in range(n_pts)]
+    qv = bn.wl.query_vectors(w)[0]
+    q = bn.encrypt(qv)
+    out = ctx.new_ct(n_pts)
+    ws = ctx.workspace(fa.OP_ROTATE_SUM, n_pts)
+    steps = int(np.log2(w.d))
+
+    def step():
+        ctx.score_block(q, blocks, w.d, fa.LAYOUT_ROW, 1, out=out)
+        ctx.rotate_sum(out, n_pts, 1, steps, ws=ws)
+
+    ms = bn.timed(step, args.steps, args.warmup)
+    err = None
+    if not args.no_check:
+        sc = np.concatenate([bn.decode(out, i, 80)[::w.d] for i in range(n_pts)])[:w.rows]
+        err = float(np.max(np.abs(sc - X.astype(np.float64) @ qv)))
+    return dict(ms=ms, scores=w.rows, phases={}, err=err, mac_bytes=None, stream_bytes=8 * n_pts * w.L * w.n,
+                cpu=None)
+
+
+def run_rank(bn, args):
+    w, ctx, fa = bn.w, bn.ctx, bn.fa
+    W32 = bn.wl.projection(w).astype(np.float32)
+    W = W32.astype(np.float64)
+    wpts = ctx.encode_projection(W32, w.B_proj)
+    Xr = bn.wl.projected_rows(w, W)
+    blk = ctx.encode_db_block(Xr.astype(np.float32), w.d, fa.LAYOUT_DIAG, w.B)
+    qv = bn.wl.query_vectors(w)[0]
+    q = bn.encrypt(qv)
+    qr = ctx.new_ct()
+    out = ctx.new_ct()
+    ws_p = ctx.workspace(fa.OP_PROJECT, 1, w.d, w.B_proj)
+    ws_s = ctx.workspace(fa.OP_SCORE, 1, w.d, w.B)
+    torch = bn.torch
+    stream = torch.cuda.current_stream()
+    marks = []
+
+    def step():
+        e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+        e0.record(stream)
+        ctx.project_ct(q, wpts, w.d_in, w.d, w.B_proj, out=qr, ws=ws_p)
+        e1.record(stream)
+        ctx.score_block(qr, [blk], w.d, fa.LAYOUT_DIAG, w.B, out=out, ws=ws_s)
+        e2.record(stream)
+        marks.append((e0, e1, e2))
+
+    ms = bn.timed(step, args.steps, args.warmup)
     torch.cuda.synchronize()
-    total_ms = ev0.elapsed_time(ev1)
-    ms_level = total_ms / args.steps
-    ph = {k: float(np.mean([p[k] for p in phases])) for k in phases[0]}
-    log(f"[bench] {args.steps} levels: {ms_level:.3f} ms/level; phases {ph}")
-
-    # ---- check: decrypt and compare with float64 inner products ----
-    err = 0.0
-    ctw = ctx.ct_words
-    for b in range(n_blocks):
-        z = ctx.decode(ctx.decrypt(out[b * ctw:(b + 1) * ctw]), 80)
-        rows = X[b * S:(b + 1) * S].astype(np.float64)
-        err = max(err, float(np.max(np.abs(z[:rows.shape[0]] - rows[:, :wl["dim"]] @ qv))))
-    log(f"[bench] max |decrypted score - float64| = {err:.2e}")
-
-    # ---- roofline of the multiply-accumulate stream (dominant kernel) ----
-    ptw = L * n
-    mac_bytes = 8 * (n_blocks * d * ptw + B * 2 * ptw + n_blocks * G * 2 * ptw)
-    mac_ms = ph["mac_ms"]
-    achieved = mac_bytes / (mac_ms * 1e-3) / 1e9
-    traffic = None
-    if args.traffic and os.path.exists(args.traffic):
-        traffic = json.load(open(args.traffic)).get("bytes_per_launch")
-    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                "kernel": "k_mac_diag", "algorithmic_bytes": mac_bytes, "avg_ms": round(mac_ms, 4)}
-
-    # ---- CPU baseline: the oracle on a bounded sample of the same level ----
-    cpu = None
-    if not args.no_cpu_baseline:
-        cpu = cpu_baseline(wl, B, G, n_blocks, X, s, m, ea, ee)
-
-    scores = wl["rows"]
-    value = scores / (ms_level * 1e-3)
-    floor_ms = 8 * n_blocks * d * ptw / (HBM_PEAK_GBS * 1e9) * 1e3
-    res = {
-        "metric": "encrypted candidate scores/sec + ms/level at 110k x 512-dim, one MI355X",
-        "value": round(value, 1),
-        "unit": "scores/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(ms_level, 4),
-        "ms_per_level": round(ms_level, 4),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "f64",
-        "data": "synthetic",
-        "config": {"workload": wl["desc"], "rows": wl["rows"], "dim": wl["dim"], "d": d, "blocks": n_blocks,
-                   "plaintexts": n_blocks * d, "baby_step": B, "giant_steps": G, "log_n": log_n, "L": L, "K": K,
-                   "log_scale": 40},
-        "phases_ms": {k: round(v, 4) for k, v in ph.items()},
-        "level_hbm_floor_ms": round(floor_ms, 4),
-        "level_frac_of_hbm_roofline": round(floor_ms / ms_level, 4),
-        "max_abs_score_err": err,
-        "roofline": roofline,
-        "cpu_baseline": cpu,
-    }
-    print(json.dumps(res), flush=True)
+    pj = float(np.mean([a.elapsed_time(b) for a, b, _ in marks[args.warmup:]]))
+    sc = float(np.mean([b.elapsed_time(c) for _, b, c in marks[args.warmup:]]))
+    err = None
+    if not args.no_check:
+        qR = W.T @ qv
+        raw = bn.decode(out, 0, 120)[:w.rows]
+        err = float(np.max(np.abs(raw / np.linalg.norm(qR) - Xr @ qR / np.linalg.norm(qR))))
+    return dict(ms=ms, scores=w.rows, phases={"projection_ms": pj, "scoring_ms": sc}, err=err, mac_bytes=None,
+                stream_bytes=8 * 2 * w.d * w.L * w.n, cpu=None)
 
 
-def cpu_baseline(wl, B, G, n_blocks, X, s, m, ea, ee):
+def run_three_level(bn, args):
+    """32 queries, each: coarse level (222,049 rows, 7 blocks) -> client decrypt, top-16 ->
+    fine level (2 of 4 fine-pool blocks) -> top-64 -> rerank level (4 of 8 rerank-pool
+    blocks, the last truncated to 11,696 rows) -> top-10.  Pool blocks are chosen by
+    hashing the kept ids (id mod pool size), deterministic and data-oblivious in cost."""
+    w, ctx, fa, torch = bn.w, bn.ctx, bn.fa, bn.torch
+    ex = w.extra
+    S = w.slots
+    nq = args.queries or ex["queries"]
+    g_coarse, centers = bn.wl.candidate_rows(w, ex["coarse"], stream_extra=1)
+    # the fine and rerank pools are drawn around the same cluster centres
+    pools = {"coarse": [], "fine": [], "rerank": []}
+    rows_of = {"coarse": [], "fine": [], "rerank": []}
+    for b in range(-(-ex["coarse"] // S)):
+        r = g_coarse[b * S:(b + 1) * S]
+        rows_of["coarse"].append(r)
+        pools["coarse"].append(ctx.encode_db_block(r, w.d, fa.LAYOUT_DIAG, w.B))
+    for name, nb, extra in (("fine", ex["fine_pool_blocks"], 2), ("rerank", ex["rerank_pool_blocks"], 3)):
+        X, _ = bn.wl.candidate_rows(w, nb * S, stream_extra=extra, centers=centers)
+        for b in range(nb):
+            r = X[b * S:(b + 1) * S]
+            rows_of[name].append(r)
+            pools[name].append(ctx.encode_db_block(r, w.d, fa.LAYOUT_DIAG, w.B))
+    torch.cuda.synchronize()
+    nblk = sum(len(v) for v in pools.values())
+    log(f"[bench] three_level: {nblk} resident blocks ({nblk * w.d * w.L * w.n * 8 / 1e9:.1f} GB), "
+        f"{time.time() - bn.t0:.1f}s")
+    queries = bn.wl.query_vectors(w, nq, centers)
+    qcts = [bn.encrypt(qv, tag=i) for i, qv in enumerate(queries)]
+    out = ctx.new_ct(7)
+    ws = ctx.workspace(fa.OP_SCORE, 7, w.d, w.B)
+    stream = torch.cuda.current_stream()
+    level_ms = []
+    errs = []
+
+    def top(ct, nb, k, rows_list, qv, n_rows_last=None):
+        scores = []
+        for b in range(nb):
+            z = bn.decode(ct, b, 80)
+            n_valid = len(rows_list[b]) if (b < nb - 1 or n_rows_last is None) else n_rows_last
+            scores.append(z[:n_valid])
+            if qv is not None:
+                ref = rows_list[b][:n_valid].astype(np.float64) @ qv
+                errs.append(float(np.max(np.abs(z[:n_valid] - ref))))
+        sc = np.concatenate(scores)
+        order = np.lexsort((np.arange(len(sc)), -sc))
+        return order[:k]
+
+    def one_query(i, check):
+        qv = queries[i] if check else None
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+        evs[0].record(stream)
+        ctx.score_block(qcts[i], pools["coarse"], w.d, fa.LAYOUT_DIAG, w.B, out=out, ws=ws)
+        evs[1].record(stream)
+        ids = top(out, len(pools["coarse"]), ex["top_coarse"], rows_of["coarse"], qv)
+        fsel = sorted(set(int(x) % ex["fine_pool_blocks"] for x in ids))
+        fsel = (fsel + [b for b in range(ex["fine_pool_blocks"]) if b not in fsel])[:ex["fine_blocks"]]
+        evs[2].record(stream)
+        ctx.score_block(qcts[i], [pools["fine"][b] for b in fsel], w.d, fa.LAYOUT_DIAG, w.B, out=out, ws=ws)
+        evs[3].record(stream)
+        ids = top(out, len(fsel), ex["top_fine"], [rows_of["fine"][b] for b in fsel], qv)
+        rsel = sorted(set(int(x) % ex["rerank_pool_blocks"] for x in ids))
+        rsel = (rsel + [b for b in range(ex["rerank_pool_blocks"]) if b not in rsel])[:ex["rerank_blocks"]]
+        evs[4].record(stream)
+        ctx.score_block(qcts[i], [pools["rerank"][b] for b in rsel], w.d, fa.LAYOUT_DIAG, w.B, out=out, ws=ws)
+        evs[5].record(stream)
+        top(out, len(rsel), 10, [rows_of["rerank"][b] for b in rsel], qv, n_rows_last=ex["rerank_last"])
+        torch.cuda.synchronize()
+        level_ms.append([evs[0].elapsed_time(evs[1]), evs[2].elapsed_time(evs[3]), evs[4].elapsed_time(evs[5])])
+
+    for i in range(min(2, nq)):  # warm-up queries (first one checked against float64)
+        one_query(i, check=(i == 0))
+    level_ms.clear()
+    t = time.time()
+    steps = max(1, args.steps)
+    for _ in range(steps):
+        for i in range(nq):
+            one_query(i, check=False)
+    wall = (time.time() - t) / (steps * nq)
+    lm = np.array(level_ms)
+    gpu_q = float(lm.sum(axis=1).mean())
+    n_scores = ex["coarse"] + ex["fine_blocks"] * S + (ex["rerank_blocks"] - 1) * S + ex["rerank_last"]
+    ph = {"coarse_ms": float(lm[:, 0].mean()), "fine_ms": float(lm[:, 1].mean()),
+          "rerank_ms": float(lm[:, 2].mean()), "query_gpu_ms": gpu_q, "query_wall_ms": wall * 1e3}
+    blocks_q = len(pools["coarse"]) + ex["fine_blocks"] + ex["rerank_blocks"]
+    return dict(ms=gpu_q, scores=n_scores, phases=ph, err=max(errs) if errs else None, mac_bytes=None,
+                stream_bytes=8 * blocks_q * w.d * w.L * w.n, cpu=None, queries=nq)
+
+
+def cpu_baseline_diag(bn, X, qv):
     """Time the oracle on a sample of the same level and scale to scores/s.
 
-    Sample: two hoisted-equivalent baby rotations of the query, and the
-    oracle's block product with G = 1 and G = 2 on the first B diagonals of
-    block 0.  Level estimate = (B-1) t_rot + n_blocks (t_G1 + (G-1)(t_G2 - t_G1)).
+    Sample: two rotations of the query, and the oracle's block product with
+    G = 1 and G = 2 on the first B diagonals of block 0.  Level estimate =
+    (B-1) t_rot + n_blocks (t_G1 + (G-1)(t_G2 - t_G1)).
     """
     from oracle import ckks
-    from paper_2608_21131_amd import gen
+    w = bn.w
+    B, G = w.B, w.G
     t_start = time.time()
-    par = ckks.Params(logn=wl["log_n"], L=wl["L"], K=wl["K"])
+    par = ckks.Params(logn=w.log_n, L=w.L, K=w.K)
     orc = ckks.Oracle(par)
-    wid = wl["wid"]
     keys = {}
     for r in (1, 2, B):
-        a = gen.uniform_residues(gen.rng(wid, gen.STREAM_KEY_A, r), par.primes, par.dnum, par.n)
-        e = gen.rounded_gaussian(gen.rng(wid, gen.STREAM_KEY_E, r), (par.dnum, par.n))
-        keys[r] = orc.keygen(s, r, a, e)
-    ct = orc.encrypt(m, ea, ee, s)
+        a, e = bn.wl.key_randomness(w, r, par.primes, par.dnum)
+        keys[r] = orc.keygen(bn.s, r, a, e)
+    ea, ee = bn.wl.enc_randomness(w, par.q)
+    m = ckks.encode(ckks.replicate(pad(qv, w.d), par.slots), par.n, 40)
+    ct = orc.encrypt(m, ea, ee, bn.s)
     t = time.time()
     orc.rotate(ct, 1, keys[1])
     orc.rotate(ct, 2, keys[2])
     t_rot = (time.time() - t) / 2
     S = par.slots
-    d = wl["d"]
-    rows = np.zeros((min(S, X.shape[0]), d))
-    rows[:, :wl["dim"]] = X[:S]
-    diags = ckks.diagonals(rows, S, d)
+    rows = np.zeros((min(S, X.shape[0]), w.d))
+    rows[:, :w.dim] = X[:S]
+    diags = ckks.diagonals(rows, S, w.d)
     pts = np.empty((2, B, par.L, par.n), dtype=np.uint64)
     for gg in range(2):
         for b in range(B):
@@ -232,14 +342,74 @@ def cpu_baseline(wl, B, G, n_blocks, X, s, m, ea, ee):
     t = time.time()
     orc.bsgs_block(qrot, pts, B, 2, keys)
     t_g2 = time.time() - t
-    est = (B - 1) * t_rot + n_blocks * (t_g1 + (G - 1) * max(t_g2 - t_g1, 0.0))
+    est = (B - 1) * t_rot + w.n_blocks * (t_g1 + (G - 1) * max(t_g2 - t_g1, 0.0))
     cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
     log(f"[bench] oracle sample: rot {t_rot:.2f}s, G1 {t_g1:.2f}s, G2 {t_g2:.2f}s -> level {est:.1f}s "
         f"({time.time() - t_start:.1f}s wall)")
-    return {"value": round(wl["rows"] / est, 2), "unit": "scores/s", "cores": cores, "kind": "oracle",
-            "sample": f"2 rotations + block product with 1 and 2 giant groups (B={B}) on block 0; level "
-                      f"extrapolated to {B - 1} baby rotations and {n_blocks} blocks x {G} groups",
+    return {"value": round(w.rows / est, 2), "unit": "scores/s", "cores": cores, "kind": "oracle",
+            "sample": f"2 rotations + block product with 1 and 2 giant groups (B={B}) on block 0 of the same "
+                      f"level; extrapolated to {B - 1} baby rotations and {w.n_blocks} blocks x {G} groups",
             "level_s_est": round(est, 2)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU (the scoring level runs on one MI355X); --gpus {args.gpus} is not "
+              "supported", file=sys.stderr)
+        sys.exit(2)
+    bn = Bench(args)
+    w = bn.w
+    runner = {"tiny": run_tiny, "fine": run_diag_level, "rerank": run_diag_level, "rank": run_rank,
+              "three_level": run_three_level}[w.name]
+    r = runner(bn, args)
+    ms = r["ms"]
+    value = r["scores"] / (ms * 1e-3)
+    log(f"[bench] {w.name}: {ms:.3f} ms/step, {value / 1e6:.2f} M scores/s, phases {r['phases']}, err {r['err']}")
+    roofline = None
+    if r["mac_bytes"]:
+        mac_ms = r["phases"]["mac_ms"]
+        achieved = r["mac_bytes"] / (mac_ms * 1e-3) / 1e9
+        traffic = None
+        if args.traffic and os.path.exists(args.traffic):
+            traffic = json.load(open(args.traffic)).get("bytes_per_launch")
+        roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic, "kernel": "k_mac_diag",
+                    "algorithmic_bytes": r["mac_bytes"], "avg_ms": round(mac_ms, 4)}
+    cpu = None
+    if not args.no_cpu_baseline and r.get("cpu"):
+        cpu = r["cpu"]()
+    floor_ms = r["stream_bytes"] / (HBM_PEAK_GBS * 1e9) * 1e3
+    cfg = {"workload": w.desc, "rows_scored_per_step": r["scores"], "d": w.d, "baby_step": w.B,
+           "giant_steps": w.G, "log_n": w.log_n, "L": w.L, "K": w.K, "log_scale": 40}
+    if r.get("queries"):
+        cfg["queries_per_step"] = r["queries"]
+    res = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "scores/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "ms_per_level": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": cfg,
+        "phases_ms": {k: round(v, 4) for k, v in r["phases"].items()},
+        "level_hbm_floor_ms": round(floor_ms, 4),
+        "level_frac_of_hbm_roofline": round(floor_ms / ms, 4),
+        "max_abs_score_err": r["err"],
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    if w.name == "three_level":
+        res["metric"] = "warm per-query latency (3 levels) + aggregate scores/s, 32 encrypted queries, one MI355X"
+        res["ms_per_level"] = None
+    print(json.dumps(res), flush=True)
 
 
 if __name__ == "__main__":

@@ -123,7 +123,9 @@ int fa_export_coeffs(fa_ctx* ctx, const void* buf, int n_polys, uint64_t* out, v
  * (round half to even, float64): host out [N]. */
 int fa_encode(const fa_ctx* ctx, const double* slots, int n_slots, int log_scale, int64_t* out);
 /* Decode decrypted residues (host [L][N], e.g. from fa_decrypt) at scale
- * 2^log_scale into n_slots real slot values (host). */
+ * 2^log_scale into n_slots real slot values (host).  The centred CRT uses
+ * the first primes whose product exceeds 2^(log_scale + 22), which is exact
+ * for slot values of magnitude below 2^12 (scores are cosines). */
 int fa_decode(const fa_ctx* ctx, const uint64_t* res, int log_scale, double* out, int n_slots);
 
 /* ---- server: enrollment ------------------------------------------------- */
@@ -138,6 +140,13 @@ int fa_decode(const fa_ctx* ctx, const uint64_t* res, int log_scale, double* out
  * pts must hold that many plaintexts (L*N words each). */
 int fa_encode_db_block(fa_ctx* ctx, const float* rows, int n_rows, int dim, int d, int layout, int baby_step,
                        void* pts, void* stream);
+/* Plaintexts of a projection W (host float32 [d_in][r], row-major) for
+ * fa_project_ct (Section 3.1 "How", "Detail"): the r hybrid diagonals
+ * e_j[s] = W[(s+j) mod d_in][s mod r] over all S slots, diagonal gB+b
+ * pre-rotated right by gB, stored g-major (pts[g*B+b]), at scale 2^log_scale.
+ * d_in and r powers of two, r | d_in, d_in | S, baby_step | r.  Writes r
+ * plaintexts. */
+int fa_encode_projection(fa_ctx* ctx, const float* W, int d_in, int r, int baby_step, void* pts, void* stream);
 /* Plaintexts from integer coefficients (host [n_pts][N], |c| < 2^62). */
 int fa_encode_db_block_int(fa_ctx* ctx, const int64_t* coeffs, int n_pts, void* pts, void* stream);
 

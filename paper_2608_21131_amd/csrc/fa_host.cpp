@@ -586,12 +586,12 @@ void mul_small(std::vector<u64>& a, u64 m) {
   }
   if (carry) a.push_back(carry);
 }
-Crt make_crt(const fa_ctx* c) {
+Crt make_crt(const fa_ctx* c, int nl) {
   Crt r;
-  r.L = c->L;
-  r.q.assign(c->primes.begin(), c->primes.begin() + c->L);
+  r.L = nl;
+  r.q.assign(c->primes.begin(), c->primes.begin() + nl);
   std::vector<u64> Q{1};
-  for (int t = 0; t < c->L; ++t) mul_small(Q, r.q[t]);
+  for (int t = 0; t < nl; ++t) mul_small(Q, r.q[t]);
   r.W = (int)Q.size() + 1;
   Q.resize(r.W, 0);
   r.Q = Q;
@@ -602,12 +602,12 @@ Crt make_crt(const fa_ctx* c) {
     r.halfQ[i] = (w >> 1) | (carry << 63);
     carry = w & 1;
   }
-  r.qhat.resize(c->L);
-  r.qhat_inv.resize(c->L);
-  for (int t = 0; t < c->L; ++t) {
+  r.qhat.resize(nl);
+  r.qhat_inv.resize(nl);
+  for (int t = 0; t < nl; ++t) {
     std::vector<u64> h{1};
     u64 hm = 1;
-    for (int j = 0; j < c->L; ++j)
+    for (int j = 0; j < nl; ++j)
       if (j != t) {
         mul_small(h, r.q[j]);
         hm = mulmod(hm, r.q[j] % r.q[t], r.q[t]);
@@ -659,7 +659,13 @@ int fa_decode(const fa_ctx* c, const uint64_t* res, int log_scale, double* out, 
   if (!c || !res || !out) return fail(FA_E_INVAL, "fa_decode: null argument");
   if (n_slots < 0 || n_slots > c->n / 2) return fail(FA_E_SHAPE, "fa_decode: n_slots %d > N/2", n_slots);
   const int n = c->n;
-  Crt r = make_crt(c);
+  // The decrypted value m' = m + e is far below the product of the first few
+  // primes: |m'| < 2^(log_scale + 20) for slot values below 2^12 in magnitude,
+  // so the centred CRT over just enough primes already returns it exactly.
+  int nl = 0;
+  double bits = 0.0;
+  while (nl < c->L && bits < log_scale + 22.0) bits += std::log2((double)c->primes[nl++]);
+  Crt r = make_crt(c, nl);
   std::vector<double> m(n);
   parallel_for(16, [&](int w) {
     for (int k = w; k < n; k += 16) m[k] = crt_to_double(r, res + k, (size_t)n);
@@ -749,6 +755,25 @@ int fa_encode_db_block(fa_ctx* c, const float* rows, int n_rows, int dim, int d,
     return fail(FA_E_INVAL, "unknown layout %d", layout);
   }
   return upload_int_pts(c, coeffs.data(), n_pts, (double*)pts, (hipStream_t)stream);
+}
+
+int fa_encode_projection(fa_ctx* c, const float* W, int d_in, int r, int baby_step, void* pts, void* stream) {
+  if (!c || !W || !pts) return fail(FA_E_INVAL, "fa_encode_projection: null argument");
+  const int S = c->n / 2;
+  if (r < 1 || (r & (r - 1)) || d_in < r || d_in % r || (d_in & (d_in - 1)) || d_in > S)
+    return fail(FA_E_SHAPE, "d_in=%d, r=%d: powers of two with r | d_in and d_in <= N/2", d_in, r);
+  if (baby_step < 1 || r % baby_step) return fail(FA_E_INVAL, "baby_step %d must divide r=%d", baby_step, r);
+  std::vector<u64> e = slot_exps(c->n);
+  const double scale = std::ldexp(1.0, c->log_scale);
+  std::vector<int64_t> coeffs((size_t)r * c->n);
+  parallel_for(r, [&](int j) {
+    const int shift = (j / baby_step) * baby_step;  // pre-rotation right by gB
+    std::vector<double> v(S);
+    for (int s = 0; s < S; ++s)
+      v[(s + shift) % S] = (double)W[(size_t)((s + j) % d_in) * r + (s % r)];
+    encode_one(c->n, e, v.data(), S, scale, coeffs.data() + (size_t)j * c->n);
+  });
+  return upload_int_pts(c, coeffs.data(), r, (double*)pts, (hipStream_t)stream);
 }
 
 // ---------------------------------------------------------------------------

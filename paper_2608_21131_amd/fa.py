@@ -63,6 +63,7 @@ SIGNATURES = {
     "fa_encode_db_block": (ctypes.c_int, [_vp, _f32p, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                           ctypes.c_int, _vp, _vp]),
     "fa_encode_db_block_int": (ctypes.c_int, [_vp, _i64p, ctypes.c_int, _vp, _vp]),
+    "fa_encode_projection": (ctypes.c_int, [_vp, _f32p, ctypes.c_int, ctypes.c_int, ctypes.c_int, _vp, _vp]),
     "fa_workspace_bytes": (ctypes.c_size_t, [_vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int]),
     "fa_score_block": (ctypes.c_int, [_vp, _vp, ctypes.POINTER(_vp), ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                       ctypes.c_int, _vp, _vp, ctypes.c_size_t, _vp]),
@@ -221,6 +222,13 @@ class Context:
         out = self.new_pt(n_pts) if out is None else out
         _check(self.lib.fa_encode_db_block(self.h, _ptr(rows, _f32p), n_rows, dim, d, layout, baby_step,
                                            _dev(out), _stream(stream)))
+        return out
+
+    def encode_projection(self, W, baby_step: int, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+        W = _np(W, np.float32)
+        d_in, r = W.shape
+        out = self.new_pt(r) if out is None else out
+        _check(self.lib.fa_encode_projection(self.h, _ptr(W, _f32p), d_in, r, baby_step, _dev(out), _stream(stream)))
         return out
 
     def encode_db_block_int(self, coeffs, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:

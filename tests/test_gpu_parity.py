@@ -246,3 +246,20 @@ def test_deterministic_repeat():
     b = p.export_ct(p.ctx.score_block(ct_dev, [blk, blk], d, 1, B), 2)
     assert np.array_equal(a, b)
     assert np.array_equal(a[0], a[1])
+
+
+def test_encode_projection_vs_oracle():
+    """fa_encode_projection packs W's hybrid diagonals, pre-rotated, like the oracle (|dm| <= 1)."""
+    p = pair("small", wid=11)
+    d_in, R, B = 64, 16, 4
+    W = gen.projection_matrix(gen.rng(11, gen.STREAM_W), d_in, R, var=1.0 / R).astype(np.float32)
+    say("[encode_projection] small")
+    pts = p.ctx.encode_projection(W, B)
+    got = p.ctx.export(pts, R)
+    pre = ckks.prerotate(ckks.projection_diagonals(W.astype(np.float64), p.par.slots), B)
+    for j in range(R):
+        ref = ckks.to_residues(ckks.encode(pre[j // B, j % B], p.n, 40), p.par.q)
+        dif = got[j][0].astype(np.int64) - ref[0].astype(np.int64)
+        q0 = np.int64(p.par.q[0])
+        dif = np.where(dif > q0 // 2, dif - q0, np.where(dif < -(q0 // 2), dif + q0, dif))
+        assert np.abs(dif).max() <= 1, j

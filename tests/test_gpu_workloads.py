@@ -1,0 +1,173 @@
+"""Parity at the workloads' full sizes, in the launch configuration bench.py
+times: every GPU output ciphertext the oracle can afford is compared word for
+word (the last, partial block of the multi-block levels), and every decrypted
+score against float64 inner products (<= 1e-4)."""
+import numpy as np
+import pytest
+
+from oracle import ckks
+from paper_2608_21131_amd import workloads as wl
+
+from common import say
+
+pytestmark = pytest.mark.gpu
+
+
+class Setup:
+    """Library context + oracle with the workload's secret and keys."""
+
+    def __init__(self, w: wl.Workload, oracle_steps=None):
+        from paper_2608_21131_amd import fa
+        self.w = w
+        self.par = ckks.Params(logn=w.log_n, L=w.L, K=w.K)
+        self.orc = ckks.Oracle(self.par)
+        self.ctx = fa.Context(w.log_n, w.L, w.K, 40)
+        assert self.ctx.primes == self.par.primes
+        self.s = wl.secret(w)
+        steps = wl.rotation_steps(w)
+        say(f"[setup] {w.name}: {len(steps)} rotation keys")
+        for i in range(0, len(steps), 8):
+            chunk = steps[i:i + 8]
+            rand = [wl.key_randomness(w, r, self.par.primes, self.par.dnum) for r in chunk]
+            self.ctx.keygen(self.s, chunk, np.stack([x[0] for x in rand]), np.stack([x[1] for x in rand]))
+        self.keys = {}
+        for r in (steps if oracle_steps is None else oracle_steps):
+            a, e = wl.key_randomness(w, r, self.par.primes, self.par.dnum)
+            self.keys[r] = self.orc.keygen(self.s, r, a, e)
+
+    def encrypt_query(self, v):
+        a, e = wl.enc_randomness(self.w, self.par.q)
+        m = ckks.encode(ckks.replicate(v, self.par.slots), self.par.n, 40)
+        return self.ctx.encrypt(m, a, e), self.orc.encrypt(m, a, e, self.s)
+
+    def decode(self, ct_tensor, i, log_scale):
+        W = self.ctx.ct_words
+        return self.ctx.decode(self.ctx.decrypt(ct_tensor[i * W:(i + 1) * W]), log_scale)
+
+    def export(self, t, count):
+        return self.ctx.export(t, 2 * count).reshape(count, 2, self.par.L, self.par.n)
+
+
+def padded(X, d):
+    Xp = np.zeros((X.shape[0], d))
+    Xp[:, :X.shape[1]] = X
+    return Xp
+
+
+def test_tiny_rows_fullsize():
+    """1,024 x 128-d at N=2^13: row layout, ct x pt then 7 rotate-and-sum steps
+    (all 32 outputs bit-exact), and one diagonal block as a cross-check."""
+    w = wl.WORKLOADS["tiny"]
+    st = Setup(w, oracle_steps=sorted(set(wl.rotation_steps(w) + ckks.steps_for_bsgs(w.d, w.B))))
+    extra = [r for r in ckks.steps_for_bsgs(w.d, w.B) if not st.ctx.has_key(r)]
+    rand = [wl.key_randomness(w, r, st.par.primes, st.par.dnum) for r in extra]
+    st.ctx.keygen(st.s, extra, np.stack([x[0] for x in rand]), np.stack([x[1] for x in rand]))
+    X, _ = wl.candidate_rows(w)
+    q = wl.query_vectors(w)[0]
+    ct, ct_o = st.encrypt_query(q)
+    S = st.par.slots
+    slot_pts = ckks.pack_rows(X.astype(np.float64), S, w.d)
+    coeffs = np.stack([ckks.encode(v, st.par.n, 40) for v in slot_pts])
+    say(f"[tiny] row layout, {len(coeffs)} plaintexts")
+    pts = st.ctx.encode_db_block_int(coeffs)
+    PW = st.ctx.pt_words
+    out = st.ctx.score_block(ct, [pts[i * PW:(i + 1) * PW] for i in range(len(coeffs))], w.d, 0)
+    st.ctx.rotate_sum(out, len(coeffs), 1, int(np.log2(w.d)))
+    got = st.export(out, len(coeffs))
+    scores = []
+    for i in range(len(coeffs)):
+        ref = st.orc.rotate_sum(st.orc.mul_plain(ct_o, ckks.to_residues(coeffs[i], st.par.q)), 1,
+                                int(np.log2(w.d)), st.keys)
+        assert np.array_equal(got[i], ref), i
+        scores.extend(st.decode(out, i, 80)[::w.d])
+    Xd = X.astype(np.float64)
+    assert np.max(np.abs(np.array(scores)[:w.rows] - Xd @ q)) < 1e-4
+    # diagonal layout on the same rows
+    say("[tiny] diagonal cross-check")
+    c = ckks.layout_b_coeffs(Xd, st.par, w.d, w.B)
+    blk = st.ctx.encode_db_block_int(c)
+    o2 = st.ctx.score_block(ct, [blk], w.d, 1, w.B)
+    pts_o = np.stack([ckks.to_residues(x, st.par.q) for x in c]).reshape(w.G, w.B, st.par.L, st.par.n)
+    ref = st.orc.bsgs_block(st.orc.baby_rotations(ct_o, w.B, st.keys), pts_o, w.B, w.G, st.keys)
+    assert np.array_equal(st.export(o2, 1)[0], ref)
+    assert np.max(np.abs(st.decode(o2, 0, 80)[:w.rows] - Xd @ q)) < 1e-4
+
+
+def _multi_block(w, check_block):
+    st = Setup(w)
+    X, centers = wl.candidate_rows(w)
+    q = wl.query_vectors(w, 1, centers)[0]
+    qp = np.zeros(w.d)
+    qp[:len(q)] = q
+    ct, ct_o = st.encrypt_query(qp)
+    S = st.par.slots
+    blocks, ref_coeffs = [], None
+    for b in range(w.n_blocks):
+        rows = X[b * S:(b + 1) * S]
+        if b == check_block:
+            ref_coeffs = ckks.layout_b_coeffs(padded(rows.astype(np.float64), w.d), st.par, w.d, w.B)
+            blocks.append(st.ctx.encode_db_block_int(ref_coeffs))
+        else:
+            blocks.append(st.ctx.encode_db_block(rows, w.d, 1, w.B))
+    say(f"[{w.name}] scoring {w.n_blocks} blocks (B={w.B}, G={w.G}) on the GPU")
+    out = st.ctx.score_block(ct, blocks, w.d, 1, w.B)
+    got = st.export(out, w.n_blocks)[check_block]
+    say(f"[{w.name}] oracle: {w.B - 1} baby rotations + block {check_block}")
+    qrot = st.orc.baby_rotations(ct_o, w.B, st.keys)
+    pts_o = np.stack([ckks.to_residues(x, st.par.q) for x in ref_coeffs]).reshape(w.G, w.B, st.par.L, st.par.n)
+    ref = st.orc.bsgs_block(qrot, pts_o, w.B, w.G, st.keys)
+    assert np.array_equal(got, ref)
+    err = 0.0
+    for b in range(w.n_blocks):
+        rows = X[b * S:(b + 1) * S].astype(np.float64)
+        z = st.decode(out, b, 80)
+        err = max(err, float(np.max(np.abs(z[:len(rows)] - rows @ q))))
+        if len(rows) < S:
+            err = max(err, float(np.max(np.abs(z[len(rows):]))))
+    say(f"[{w.name}] max |score - float64| = {err:.2e}")
+    assert err < 1e-4
+
+
+def test_fine_level_fullsize():
+    """65,536 x 96-d (zero-padded to 128) at N=2^15: 4 diagonal blocks; block 3 bit-exact;
+    every score is the exact 96-d cosine."""
+    _multi_block(wl.WORKLOADS["fine"], check_block=3)
+
+
+def test_rerank_level_fullsize():
+    """110,000 x 512-d at N=2^16, B=64: 4 blocks as bench.py times them; the partial last
+    block (11,696 rows) bit-exact; all 110,000 scores within 1e-4 of float64."""
+    _multi_block(wl.WORKLOADS["rerank"], check_block=3)
+
+
+def test_rank_reduction_fullsize():
+    """Encrypted 512 -> 128 projection (hybrid diagonals, BSGS, one fold) then 16,384
+    candidates at d=128; both ciphertexts bit-exact; norm-corrected cosines vs float64."""
+    w = wl.WORKLOADS["rank"]
+    st = Setup(w)
+    W = wl.projection(w)
+    q = wl.query_vectors(w)[0]
+    ct, ct_o = st.encrypt_query(q)
+    S = st.par.slots
+    R, Bp = w.d, w.B_proj
+    pre = ckks.prerotate(ckks.projection_diagonals(W, S), Bp)
+    wco = np.stack([ckks.encode(pre[g, b], st.par.n, 40) for g in range(R // Bp) for b in range(Bp)])
+    wpts = st.ctx.encode_db_block_int(wco)
+    say("[rank] projection on the GPU")
+    qr = st.ctx.project_ct(ct, wpts, w.d_in, R, Bp)
+    Xr = wl.projected_rows(w, W)
+    c = ckks.layout_b_coeffs(Xr, st.par, R, w.B)
+    blk = st.ctx.encode_db_block_int(c)
+    out = st.ctx.score_block(qr, [blk], R, 1, w.B)
+    say("[rank] oracle projection + fold + scoring")
+    wres = np.stack([ckks.to_residues(x, st.par.q) for x in wco]).reshape(R // Bp, Bp, st.par.L, st.par.n)
+    z = st.orc.bsgs_block(st.orc.baby_rotations(ct_o, Bp, st.keys), wres, Bp, R // Bp, st.keys)
+    z = st.orc.rotate_sum(z, R, int(np.log2(w.d_in // R)), st.keys)
+    assert np.array_equal(st.export(qr, 1)[0], z)
+    pts_o = np.stack([ckks.to_residues(x, st.par.q) for x in c]).reshape(w.G, w.B, st.par.L, st.par.n)
+    ref = st.orc.bsgs_block(st.orc.baby_rotations(z, w.B, st.keys), pts_o, w.B, w.G, st.keys)
+    assert np.array_equal(st.export(out, 1)[0], ref)
+    qR = W.T @ q
+    raw = st.decode(out, 0, 120)[:w.rows]
+    cos = raw / np.linalg.norm(qR)
+    assert np.max(np.abs(cos - Xr @ qR / np.linalg.norm(qR))) < 1e-4
