@@ -49,8 +49,9 @@ def parse():
     ap.add_argument("--no-check", action="store_true", help="skip the decrypt-and-compare check")
     ap.add_argument("--copy-calib", action="store_true",
                     help="run one plain 1 GiB device copy before the timed region (HBM counter calibration)")
-    ap.add_argument("--traffic", default=None,
-                    help="JSON file with measured per-launch HBM bytes of the multiply-accumulate kernel")
+    ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "k_mac_diag_rerank110k_traffic.md"),
+                    help="rocprofv3 counter summary with the measured per-launch HBM bytes of the "
+                         "multiply-accumulate kernel (used only while that kernel's source is unchanged)")
     return ap.parse_args()
 
 
@@ -303,6 +304,26 @@ def run_three_level(bn, args):
                 stream_bytes=8 * blocks_q * w.d * w.L * w.n, cpu=None, queries=nq)
 
 
+def measured_traffic(path):
+    """HBM bytes per launch of k_mac_diag from the committed counter summary, or None
+    when the summary is missing or the kernel source changed since it was taken."""
+    import hashlib
+    import re
+    if not path or not os.path.exists(path):
+        return None
+    txt = open(path).read()
+    mb = re.search(r"bytes_per_launch: (\d+)", txt)
+    mh = re.search(r"kernel_source_sha256: ([0-9a-f]+)", txt)
+    if not mb or not mh:
+        return None
+    src = open(os.path.join(ROOT, "paper_2608_21131_amd", "csrc", "fa_kernels.hip")).read()
+    a = src.index("template <int NACC>\n__global__ __launch_bounds__(256) void k_mac_diag(")
+    b = src.index("\n}\n", a) + 3
+    if hashlib.sha256(src[a:b].encode()).hexdigest() != mh.group(1):
+        return None
+    return int(mb.group(1))
+
+
 def cpu_baseline_diag(bn, X, qv):
     """Time the oracle on a sample of the same level and scale to scores/s.
 
@@ -370,9 +391,7 @@ def main():
     if r["mac_bytes"]:
         mac_ms = r["phases"]["mac_ms"]
         achieved = r["mac_bytes"] / (mac_ms * 1e-3) / 1e9
-        traffic = None
-        if args.traffic and os.path.exists(args.traffic):
-            traffic = json.load(open(args.traffic)).get("bytes_per_launch")
+        traffic = measured_traffic(args.traffic) if (w.name == "rerank" and w.B == 64) else None
         roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic, "kernel": "k_mac_diag",
                     "algorithmic_bytes": r["mac_bytes"], "avg_ms": round(mac_ms, 4)}

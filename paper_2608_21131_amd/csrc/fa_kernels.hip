@@ -293,15 +293,13 @@ __device__ __forceinline__ double twb(const double* __restrict__ T, double f, in
   return mulc(t, f, f * qinv, q);
 }
 
-// stores for the last pass of the forward transform (16 consecutive elements)
+// stores for the last pass of the forward transform, one element at a time
+// (global index i, lazily reduced value x); the pass hands them out so that
+// consecutive threads touch consecutive words.
 struct CanonSt {
   double* a;
   double q, qinv;
-  __device__ void operator()(size_t i0, const double (&x)[16]) const {
-    double2* dst = reinterpret_cast<double2*>(a + i0);
-#pragma unroll
-    for (int m = 0; m < 8; ++m) dst[m] = make_double2(canon_full(x[2 * m], q, qinv), canon_full(x[2 * m + 1], q, qinv));
-  }
+  __device__ void operator()(size_t i, double x) const { a[i] = canon_full(x, q, qinv); }
 };
 // ModDown finish: out[k] = base[pi(k)] + (u_Q[k] - conv^[k]) * P^-1
 struct FinishSt {
@@ -311,20 +309,10 @@ struct FinishSt {
   uint32_t gal;
   int logn;
   double q, qinv, pv, pvp;
-  __device__ void operator()(size_t i0, const double (&x)[16]) const {
-    double r[16];
-#pragma unroll
-    for (int m = 0; m < 16; ++m) r[m] = mulc(uQ[i0 + m] - x[m], pv, pvp, q);
-    if (base) {
-#pragma unroll
-      for (int m = 0; m < 16; ++m) {
-        const uint32_t k = (uint32_t)(i0 + m);
-        r[m] += base[gal == 1u ? k : perm(k, gal, logn)];
-      }
-    }
-    double2* dst = reinterpret_cast<double2*>(out + i0);
-#pragma unroll
-    for (int m = 0; m < 8; ++m) dst[m] = make_double2(canon_full(r[2 * m], q, qinv), canon_full(r[2 * m + 1], q, qinv));
+  __device__ void operator()(size_t i, double x) const {
+    double r = mulc(uQ[i] - x, pv, pvp, q);
+    if (base) r += base[gal == 1u ? (uint32_t)i : perm((uint32_t)i, gal, logn)];
+    out[i] = canon_full(r, q, qinv);
   }
 };
 
@@ -369,8 +357,13 @@ __device__ __forceinline__ void fwd_b_body(double* a, const St& st, const double
         ct_bfly(x[m], x[m + half], twb(T, f, s1, (lh << (s1 - 4)) + (m >> (8 - s1)), q, qinv), q, qinv);
       }
     }
-    st((size_t)r * 256 + 16 * lh, x);
+    // back to LDS (each thread rewrites the words it read) ...
+#pragma unroll
+    for (int m = 0; m < 16; ++m) sm[lds_row(rl, 16 * lh + m)] = x[m];
   }
+  __syncthreads();
+  // ... and out with consecutive threads on consecutive words
+  for (int e = threadIdx.x; e < rows * 256; e += 256) st((size_t)row0 * 256 + e, sm[lds_row(e >> 8, e & 255)]);
 }
 
 __global__ __launch_bounds__(256) void k_ntt_fwd_b(LimbList ll, const DevPrime* __restrict__ pr,
@@ -853,7 +846,6 @@ static int mac_pairs_max() {
   }
   return v;
 }
-
 void mac_diag(const fa_ctx* c, const double* q, const double* qrot, const double* const* blocks, int n_blocks,
               int B, int G, double* acc, hipStream_t s) {
   const int pmax = mac_pairs_max();
