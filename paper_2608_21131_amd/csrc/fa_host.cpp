@@ -240,6 +240,11 @@ void fa_ctx_destroy(fa_ctx* c) {
   for (auto& kv : c->keys) (void)hipFree(kv.second);
   for (auto& e : c->ev)
     if (e) (void)hipEventDestroy(e);
+  for (int i = 0; i < c->n_aux; ++i) {
+    (void)hipStreamDestroy(c->aux[i]);
+    (void)hipEventDestroy(c->join_ev[i]);
+  }
+  if (c->fork_ev) (void)hipEventDestroy(c->fork_ev);
   delete c;
 }
 
@@ -816,20 +821,34 @@ size_t rotate_ws(const fa_ctx* c, int nb) {
          rup((size_t)nb * 2 * c->L * n);
 }
 
+// Lanes (the caller's stream plus auxiliary streams) that independent
+// key-switch batches of one scoring call are spread over; FA_STREAMS tunes it.
+int lanes_wanted() {
+  static int v = -1;
+  if (v < 0) {
+    const char* e = getenv("FA_STREAMS");
+    v = e ? atoi(e) : 3;
+    if (v < 1) v = 1;
+    if (v > FA_MAXAUX + 1) v = FA_MAXAUX + 1;
+  }
+  return v;
+}
+
 size_t score_ws(const fa_ctx* c, int nb, int d, int B) {
   const size_t n = c->n, L = c->L, np = c->np, dn = c->dnum;
   const size_t G = d / B;
-  const size_t rb = std::max(1, std::min(kRotBatch, B - 1));
+  const size_t rb = std::max(1, std::min(rot_batch(), B - 1));
+  const size_t lanes = lanes_wanted();
   size_t w = 0;
   w += rup(L * n);                            // scaled coefficients of q.c1
   w += rup(dn * np * n);                      // extended digits of q
-  w += rup(rb * 2 * np * n);                  // key-switch products
-  w += rup(rb * 2 * L * n);                   // ModDown conversions
+  w += lanes * rup(rb * 2 * np * n);          // key-switch products, per lane
+  w += lanes * rup(rb * 2 * L * n);           // ModDown conversions, per lane
   w += rup((size_t)(B - 1) * 2 * L * n + 1);  // baby rotations 1..B-1
   w += rup(nb * G * 2 * L * n);               // accumulators
-  w += rup(nb * L * n);                       // giant-step scaled coefficients
-  w += rup(nb * dn * np * n);                 // giant-step extended digits
-  w += rup(nb * 2 * np * n);                  // giant-step key-switch sums
+  w += lanes * rup(nb * L * n);               // giant-step scaled coefficients, per lane
+  w += lanes * rup(nb * dn * np * n);         // giant-step extended digits, per lane
+  w += lanes * rup(nb * 2 * np * n);          // giant-step key-switch sums, per lane
   w += rup(nb * 2 * L * n);                   // giant-step ModDown conversions
   return w;
 }
@@ -873,15 +892,47 @@ static void moddown_polys(fa_ctx* c, double* u, int count, double* conv, const d
   fa::moddown(c, it.data(), count, s);
 }
 
+// Auxiliary streams for `lanes` lanes (lane 0 is the caller's stream).
+static int ensure_lanes(fa_ctx* c, int lanes) {
+  if (!c->fork_ev) HIPCHK(hipEventCreateWithFlags(&c->fork_ev, hipEventDisableTiming));
+  while (c->n_aux < lanes - 1) {
+    const int i = c->n_aux;
+    HIPCHK(hipStreamCreateWithFlags(&c->aux[i], hipStreamNonBlocking));
+    HIPCHK(hipEventCreateWithFlags(&c->join_ev[i], hipEventDisableTiming));
+    c->n_aux++;
+  }
+  return FA_OK;
+}
+static hipStream_t lane_stream(fa_ctx* c, hipStream_t s, int lane) { return lane == 0 ? s : c->aux[lane - 1]; }
+static int fork_lanes(fa_ctx* c, hipStream_t s, int lanes) {
+  if (lanes < 2) return FA_OK;
+  HIPCHK(hipEventRecord(c->fork_ev, s));
+  for (int i = 0; i < lanes - 1; ++i) HIPCHK(hipStreamWaitEvent(c->aux[i], c->fork_ev, 0));
+  return FA_OK;
+}
+static int join_lanes(fa_ctx* c, hipStream_t s, int lanes) {
+  for (int i = 0; i < lanes - 1; ++i) {
+    HIPCHK(hipEventRecord(c->join_ev[i], c->aux[i]));
+    HIPCHK(hipStreamWaitEvent(s, c->join_ev[i], 0));
+  }
+  return FA_OK;
+}
+
 // Hoisted rotations of one ciphertext q by steps[0..m-1]: one decomposition of
 // c1 shared by all, each rotation with its own key switch and ModDown.
-// ext must already hold the extended digits of q.c1 (NTT form).
+// ext must already hold the extended digits of q.c1 (NTT form).  Batches of
+// rotations go round-robin to `lanes` lanes, lane l using scratch u/conv +
+// l * (per-lane size).
 static int rotations_from_ext(fa_ctx* c, const double* q, const double* ext, const int* steps, int m,
-                              double* const* outs, double* u, double* conv, hipStream_t s) {
+                              double* const* outs, double* u, double* conv, hipStream_t s, int lanes, int rbmax,
+                              size_t u_lane, size_t c_lane) {
   const size_t n = c->n, L = c->L, np = c->np;
-  const int rbmax = rot_batch();
-  for (int r0 = 0; r0 < m; r0 += rbmax) {
+  for (int r0 = 0, j0 = 0; r0 < m; r0 += rbmax, ++j0) {
     const int rb = std::min(rbmax, m - r0);
+    const int lane = j0 % lanes;
+    hipStream_t ls = lane_stream(c, s, lane);
+    double* ul = u + lane * u_lane;
+    double* cl = conv + lane * c_lane;
     fa::KsItem ks[kRotBatch];
     const double* bases[2 * kRotBatch];
     double* douts[2 * kRotBatch];
@@ -890,15 +941,15 @@ static int rotations_from_ext(fa_ctx* c, const double* q, const double* ext, con
       auto it = c->keys.find(steps[r0 + j]);
       if (it == c->keys.end()) return fail(FA_E_NOKEY, "no rotation key for step %d", steps[r0 + j]);
       const uint32_t gal = galois(c->n, steps[r0 + j]);
-      ks[j] = {ext, q + L * n, it->second, u + (size_t)j * 2 * np * n, nullptr, gal};
+      ks[j] = {ext, q + L * n, it->second, ul + (size_t)j * 2 * np * n, nullptr, gal};
       bases[2 * j] = q;
       bases[2 * j + 1] = nullptr;
       douts[2 * j] = outs[r0 + j];
       douts[2 * j + 1] = outs[r0 + j] + L * n;
       gals[2 * j] = gals[2 * j + 1] = gal;
     }
-    fa::ks_inner(c, ks, rb, false, s);
-    moddown_polys(c, u, 2 * rb, conv, bases, douts, gals, s);
+    fa::ks_inner(c, ks, rb, false, ls);
+    moddown_polys(c, ul, 2 * rb, cl, bases, douts, gals, ls);
   }
   return check_launch("rotation");
 }
@@ -940,16 +991,19 @@ static int score_diag(fa_ctx* c, const double* q, const double* const* blocks, i
   const size_t n = c->n, L = c->L, np = c->np, dn = c->dnum;
   const int G = d / B;
   const size_t ctw = 2 * L * n;
-  const int rb = std::max(1, std::min(kRotBatch, B - 1));
+  const int rb = std::max(1, std::min(rot_batch(), B - 1));
+  const int lanes = lanes_wanted();
   double* y = ar.take(L * n);
   double* ext = ar.take(dn * np * n);
-  double* u = ar.take((size_t)rb * 2 * np * n);
-  double* conv = ar.take((size_t)rb * 2 * L * n);
+  double* u = ar.take((size_t)lanes * (rup((size_t)rb * 2 * np * n) / 8));
+  double* conv = ar.take((size_t)lanes * (rup((size_t)rb * 2 * L * n) / 8));
   double* qrot = ar.take((size_t)(B - 1) * ctw + 1);
   double* acc = ar.take((size_t)nb * G * ctw);
-  double* gy = ar.take((size_t)nb * L * n);
-  double* gext = ar.take((size_t)nb * dn * np * n);
-  double* usum = ar.take((size_t)nb * 2 * np * n);
+  const size_t gy_l = rup((size_t)nb * L * n) / 8, gext_l = rup((size_t)nb * dn * np * n) / 8,
+               us_l = rup((size_t)nb * 2 * np * n) / 8;
+  double* gy = ar.take(lanes * gy_l);
+  double* gext = ar.take(lanes * gext_l);
+  double* usum = ar.take(lanes * us_l);
   double* gconv = ar.take((size_t)nb * 2 * L * n);
   if (!y || !ext || !u || !conv || !qrot || !acc || !gy || !gext || !usum || !gconv)
     return fail(FA_E_NOMEM, "workspace too small for score_block");
@@ -957,9 +1011,11 @@ static int score_diag(fa_ctx* c, const double* q, const double* const* blocks, i
     if (!c->keys.count(b)) return fail(FA_E_NOKEY, "no rotation key for baby step %d", b);
   for (int g = 1; g < G; ++g)
     if (!c->keys.count(g * B)) return fail(FA_E_NOKEY, "no rotation key for giant step %d", g * B);
+  int rc = ensure_lanes(c, lanes);
+  if (rc) return rc;
 
   if (c->prof) HIPCHK(hipEventRecord(c->ev[0], s));
-  // 1. baby rotations of the query, one shared decomposition
+  // 1. baby rotations of the query, one shared decomposition; batches spread over lanes
   if (B > 1) {
     modup(c, q, ctw, 1, y, L * n, ext, dn * np * n, s);
     std::vector<int> steps(B - 1);
@@ -968,32 +1024,47 @@ static int score_diag(fa_ctx* c, const double* q, const double* const* blocks, i
       steps[b - 1] = b;
       outs[b - 1] = qrot + (size_t)(b - 1) * ctw;
     }
-    int rc = rotations_from_ext(c, q, ext, steps.data(), B - 1, outs.data(), u, conv, s);
+    const int nbatch = (B - 1 + rb - 1) / rb;
+    const int bl = std::min(lanes, nbatch);
+    if ((rc = fork_lanes(c, s, bl))) return rc;
+    rc = rotations_from_ext(c, q, ext, steps.data(), B - 1, outs.data(), u, conv, s, bl, rb,
+                            rup((size_t)rb * 2 * np * n) / 8, rup((size_t)rb * 2 * L * n) / 8);
     if (rc) return rc;
+    if ((rc = join_lanes(c, s, bl))) return rc;
   }
   if (c->prof) HIPCHK(hipEventRecord(c->ev[1], s));
   // 2. multiply-accumulate against the resident plaintexts
   fa::mac_diag(c, q, qrot, blocks, nb, B, G, acc, s);
   if (c->prof) HIPCHK(hipEventRecord(c->ev[2], s));
   // 3. giant steps: Rotate(acc_g, gB) summed over Q u P, one ModDown per block;
-  //    sigma(acc_g.c0) rides in the key-switch sum multiplied by P
+  //    sigma(acc_g.c0) rides in the key-switch sum multiplied by P.  Giant
+  //    indices go round-robin to lanes, each lane summing into its own buffer.
   const size_t astride = (size_t)G * ctw;
   if (G == 1) {
     for (int blk = 0; blk < nb; ++blk)
       HIPCHK(hipMemcpyAsync(out + (size_t)blk * ctw, acc + (size_t)blk * ctw, ctw * 8, hipMemcpyDeviceToDevice, s));
   } else {
+    const int gl = std::min(lanes, G - 1);
+    if ((rc = fork_lanes(c, s, gl))) return rc;
     for (int g = 1; g < G; ++g) {
+      const int lane = (g - 1) % gl;
+      hipStream_t ls = lane_stream(c, s, lane);
       const double* accg = acc + (size_t)g * ctw;
-      modup(c, accg, astride, nb, gy, L * n, gext, dn * np * n, s);
+      double* gyl = gy + lane * gy_l;
+      double* gextl = gext + lane * gext_l;
+      double* usl = usum + lane * us_l;
+      modup(c, accg, astride, nb, gyl, L * n, gextl, dn * np * n, ls);
       std::vector<fa::KsItem> ks(nb);
       const uint32_t gal = galois(c->n, g * B);
       for (int blk = 0; blk < nb; ++blk) {
         const double* a = accg + (size_t)blk * astride;
-        ks[blk] = {gext + (size_t)blk * dn * np * n, a + L * n, c->keys[g * B], usum + (size_t)blk * 2 * np * n, a,
+        ks[blk] = {gextl + (size_t)blk * dn * np * n, a + L * n, c->keys[g * B], usl + (size_t)blk * 2 * np * n, a,
                    gal};
       }
-      fa::ks_inner(c, ks.data(), nb, g > 1, s);
+      fa::ks_inner(c, ks.data(), nb, g > lane + 1, ls);
     }
+    if ((rc = join_lanes(c, s, gl))) return rc;
+    for (int lane = 1; lane < gl; ++lane) fa::add_limbs(c, usum, usum + lane * us_l, nb * 2 * (int)np, (int)np, s);
     std::vector<const double*> bases(2 * nb);
     std::vector<double*> douts(2 * nb);
     std::vector<uint32_t> gals(2 * nb, 1u);

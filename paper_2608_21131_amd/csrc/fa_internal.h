@@ -35,6 +35,8 @@ struct LimbList {
   double scale[FA_MAXL];
 };
 
+#define FA_MAXAUX 3
+
 struct fa_ctx {
   int logn, n, L, K, np, alpha, dnum, log_scale, device;
   std::vector<uint64_t> primes;   // [np] q_0..q_{L-1}, p_0..p_{K-1}
@@ -63,6 +65,12 @@ struct fa_ctx {
   // phase timing (fa_profile)
   bool prof = false, prof_done = false;
   hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
+  // auxiliary streams (default priority) that independent key-switch batches
+  // run on, forked from and joined back to the caller's stream with events
+  int n_aux = 0;
+  hipStream_t aux[FA_MAXAUX] = {};
+  hipEvent_t fork_ev = nullptr;
+  hipEvent_t join_ev[FA_MAXAUX] = {};
 };
 
 // --------------------------------------------------------------------------
@@ -126,6 +134,8 @@ void mac_diag(const fa_ctx* c, const double* q, const double* qrot, const double
 
 // out[w] = ct * pt[w] (both polys), w < count
 void mul_plain(const fa_ctx* c, const double* ct, const double* const* pts, int count, double* out, hipStream_t s);
+// dst[r] += src[r] for n_limbs limbs of N words, limb r over prime r % period
+void add_limbs(const fa_ctx* c, double* dst, const double* src, int n_limbs, int period, hipStream_t s);
 // dst[i] = dst[i] + sigma_g(src[i]) over `words` words of [.][L][N] data; g = 1 -> plain add
 void add_automorph(const fa_ctx* c, double* dst, const double* src, int n_polys, uint32_t gal, hipStream_t s);
 // residues of signed integers: dst[p][t][k] = src[p][k] mod prime t (t < nprimes)

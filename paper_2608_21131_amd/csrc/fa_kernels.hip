@@ -598,6 +598,16 @@ __global__ __launch_bounds__(256) void k_add_automorph(double* __restrict__ dst,
   dst[o + k] = canon(dst[o + k] + src[o + kk], q);
 }
 
+__global__ __launch_bounds__(256) void k_add_limbs(double* __restrict__ dst, const double* __restrict__ src,
+                                                   const DevPrime* __restrict__ pr, int logn, int period) {
+  const int n = 1 << logn;
+  const int k = blockIdx.x * 256 + threadIdx.x;
+  const int row = blockIdx.y;
+  const double q = pr[row % period].q;
+  const size_t o = (size_t)row * n + k;
+  dst[o] = canon(dst[o] + src[o], q);
+}
+
 __global__ __launch_bounds__(256) void k_int_to_res(const int64_t* __restrict__ src, double* __restrict__ dst,
                                                     const DevPrime* __restrict__ pr, int logn, int nprimes) {
   const int n = 1 << logn;
@@ -894,6 +904,11 @@ void mul_plain(const fa_ctx* c, const double* ct, const double* const* pts, int 
 void add_automorph(const fa_ctx* c, double* dst, const double* src, int n_polys, uint32_t gal, hipStream_t s) {
   dim3 g(c->n / 256, n_polys * c->L);
   hipLaunchKernelGGL(k_add_automorph, g, dim3(256), 0, s, dst, src, c->d_pr, c->logn, c->L, gal);
+}
+
+void add_limbs(const fa_ctx* c, double* dst, const double* src, int n_limbs, int period, hipStream_t s) {
+  dim3 g(c->n / 256, n_limbs);
+  hipLaunchKernelGGL(k_add_limbs, g, dim3(256), 0, s, dst, src, c->d_pr, c->logn, period);
 }
 
 void int_to_res(const fa_ctx* c, const int64_t* src, int n_polys, int nprimes, double* dst, hipStream_t s) {
