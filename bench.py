@@ -44,7 +44,13 @@ def parse():
     ap.add_argument("--workload", default="rerank",
                     choices=["tiny", "fine", "rank", "rerank", "three_level"])
     ap.add_argument("--baby-step", type=int, default=0)
+    ap.add_argument("--level", type=int, default=0,
+                    help="fine/rerank: drop the query to this many ciphertext primes and score there, with the "
+                         "database enrolled at that level (0: score at all primes)")
     ap.add_argument("--queries", type=int, default=0, help="three_level: queries per step (default 32)")
+    ap.add_argument("--also-level", type=int, default=3,
+                    help="rerank: also time the level with the query dropped to this many primes and report it "
+                         "under level_drop (0: skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-check", action="store_true", help="skip the decrypt-and-compare check")
     ap.add_argument("--copy-calib", action="store_true",
@@ -108,15 +114,18 @@ def pad(v, d):
 
 
 def run_diag_level(bn, args):
-    """fine / rerank: one diagonal-layout level over all blocks."""
-    w, ctx, fa = bn.w, bn.ctx, bn.fa
+    """fine / rerank: one diagonal-layout level over all blocks (optionally after a level drop)."""
+    w, fa = bn.w, bn.fa
+    top = bn.ctx
+    ctx = top.at_level(args.level) if args.level and args.level < w.L else top
     X, centers = bn.wl.candidate_rows(w)
     S = w.slots
     blocks = [ctx.encode_db_block(X[b * S:(b + 1) * S], w.d, fa.LAYOUT_DIAG, w.B) for b in range(w.n_blocks)]
     bn.torch.cuda.synchronize()
     log(f"[bench] encoded {w.n_blocks} blocks, {w.n_blocks * w.d} plaintexts ({time.time() - bn.t0:.1f}s)")
     qv = bn.wl.query_vectors(w, 1, centers)[0]
-    q = bn.encrypt(pad(qv, w.d))
+    q_top = bn.encrypt(pad(qv, w.d))
+    q = ctx.new_ct() if ctx is not top else q_top
     out = ctx.new_ct(w.n_blocks)
     ws = ctx.workspace(fa.OP_SCORE, w.n_blocks, w.d, w.B)
     if args.copy_calib:
@@ -130,6 +139,8 @@ def run_diag_level(bn, args):
     phases = []
 
     def step():
+        if ctx is not top:
+            top.drop_level(ctx, q_top, out=q)
         ctx.score_block(q, blocks, w.d, fa.LAYOUT_DIAG, w.B, out=out, ws=ws)
         phases.append(ctx.profile_read())
 
@@ -138,11 +149,12 @@ def run_diag_level(bn, args):
     err = None
     if not args.no_check:
         err = 0.0
+        W_ = ctx.ct_words
         for b in range(w.n_blocks):
             rows = X[b * S:(b + 1) * S].astype(np.float64)
-            z = bn.decode(out, b, 80)
+            z = ctx.decode(ctx.decrypt(out[b * W_:(b + 1) * W_]), 80)
             err = max(err, float(np.max(np.abs(z[:len(rows)] - rows @ qv))))
-    ptw = w.L * w.n
+    ptw = ctx.L * w.n
     mac_bytes = 8 * (w.n_blocks * w.d * ptw + (w.B - 1) * 2 * ptw + 2 * ptw + w.n_blocks * w.G * 2 * ptw)
     stream_bytes = 8 * w.n_blocks * w.d * ptw
     return dict(ms=ms, scores=w.rows, phases=ph, err=err, mac_bytes=mac_bytes, stream_bytes=stream_bytes,
@@ -391,7 +403,7 @@ def main():
     if r["mac_bytes"]:
         mac_ms = r["phases"]["mac_ms"]
         achieved = r["mac_bytes"] / (mac_ms * 1e-3) / 1e9
-        traffic = measured_traffic(args.traffic) if (w.name == "rerank" and w.B == 64) else None
+        traffic = measured_traffic(args.traffic) if (w.name == "rerank" and w.B == 64 and not args.level) else None
         roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic, "kernel": "k_mac_diag",
                     "algorithmic_bytes": r["mac_bytes"], "avg_ms": round(mac_ms, 4)}
@@ -401,6 +413,10 @@ def main():
     floor_ms = r["stream_bytes"] / (HBM_PEAK_GBS * 1e9) * 1e3
     cfg = {"workload": w.desc, "rows_scored_per_step": r["scores"], "d": w.d, "baby_step": w.B,
            "giant_steps": w.G, "log_n": w.log_n, "L": w.L, "K": w.K, "log_scale": 40}
+    if args.level and args.level < w.L:
+        cfg["scoring_level_primes"] = args.level
+        cfg["workload"] += (f"; query dropped to {args.level} ciphertext primes and database enrolled at that "
+                            "level before scoring")
     if r.get("queries"):
         cfg["queries_per_step"] = r["queries"]
     res = {
@@ -428,6 +444,19 @@ def main():
     if w.name == "three_level":
         res["metric"] = "warm per-query latency (3 levels) + aggregate scores/s, 32 encrypted queries, one MI355X"
         res["ms_per_level"] = None
+    if w.name == "rerank" and args.also_level and not args.level and args.also_level < w.L:
+        import copy
+        a2 = copy.copy(args)
+        a2.level = args.also_level
+        a2.no_check = args.no_check
+        r2 = run_diag_level(bn, a2)
+        res["level_drop"] = {"scoring_level_primes": args.also_level, "ms_per_level": round(r2["ms"], 4),
+                             "value": round(r2["scores"] / (r2["ms"] * 1e-3), 1), "unit": "scores/s",
+                             "phases_ms": {k: round(v, 4) for k, v in r2["phases"].items()},
+                             "max_abs_score_err": r2["err"],
+                             "level_hbm_floor_ms": round(r2["stream_bytes"] / (HBM_PEAK_GBS * 1e9) * 1e3, 4),
+                             "mac_achieved_GBs": round(r2["mac_bytes"] / (r2["phases"]["mac_ms"] * 1e-3) / 1e9, 1)}
+        log(f"[bench] level drop to {args.also_level} primes: {r2['ms']:.3f} ms/level")
     print(json.dumps(res), flush=True)
 
 

@@ -83,6 +83,20 @@ typedef struct {
 int fa_ctx_create(const fa_params* params, fa_ctx** out);
 void fa_ctx_destroy(fa_ctx* ctx);
 
+/* A lower-level context over the first L_low ciphertext primes of `parent`
+ * and the same special primes (same N, K, scale).  Its secret and every
+ * rotation key are the parent's restricted to those primes: a key digit's
+ * gadget P*Qhat_i*[Qhat_i^-1]_{Q_i} is P on the digit's own primes and 0 on
+ * the others at every level, so the restriction is the lower-level key.  The
+ * database can then live at this shallow level (the paper stores it at the
+ * level its ranked product needs, Section 2 "Measured prototype vs.
+ * deployment").  Keys generated later on either context are not shared. */
+int fa_ctx_create_level(const fa_ctx* parent, uint32_t L_low, fa_ctx** out);
+/* Level drop of a ciphertext from `parent` to `child` (fa_ctx_create_level):
+ * keeps the first child->L limbs of c0 and c1.  Exact while the message plus
+ * noise stays below half the product of the kept primes. */
+int fa_drop_level(const fa_ctx* parent, const fa_ctx* child, const void* ct, void* out, void* stream);
+
 /* The L+K primes (host out[L+K]): q_0..q_{L-1}, then p_0..p_{K-1}. */
 int fa_ctx_primes(const fa_ctx* ctx, uint64_t* out);
 size_t fa_ct_words(const fa_ctx* ctx); /* 2*L*N */

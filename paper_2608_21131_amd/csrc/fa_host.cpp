@@ -248,12 +248,10 @@ void fa_ctx_destroy(fa_ctx* c) {
   delete c;
 }
 
-int fa_ctx_create(const fa_params* prm, fa_ctx** out) {
-  if (!prm || !out) return fail(FA_E_INVAL, "fa_ctx_create: null argument");
-  if (prm->log_n < 10 || prm->log_n > 16) return fail(FA_E_INVAL, "log_n must be in [10, 16], got %u", prm->log_n);
-  if (prm->L < 1 || prm->L > 16) return fail(FA_E_INVAL, "L must be in [1, 16], got %u", prm->L);
-  if (prm->K < 1 || prm->K > 4) return fail(FA_E_INVAL, "K must be in [1, 4], got %u", prm->K);
-  if (prm->log_scale < 1 || prm->log_scale > 60) return fail(FA_E_INVAL, "log_scale must be in [1, 60]");
+}  // extern "C"
+
+// Builds a context over an explicit prime list (L ciphertext primes, then K special primes).
+static int ctx_build(const fa_params* prm, const std::vector<u64>& primes, fa_ctx** out) {
   fa_ctx* c = new (std::nothrow) fa_ctx();
   if (!c) return fail(FA_E_NOMEM, "out of host memory");
   c->logn = (int)prm->log_n;
@@ -265,11 +263,7 @@ int fa_ctx_create(const fa_params* prm, fa_ctx** out) {
   c->dnum = (c->L + c->K - 1) / c->K;
   c->log_scale = (int)prm->log_scale;
   (void)hipGetDevice(&c->device);
-  c->primes = select_primes(c->logn, c->np);
-  if ((int)c->primes.size() != c->np) {
-    delete c;
-    return fail(FA_E_INVAL, "not enough 50-bit NTT primes");
-  }
+  c->primes = primes;
   const int n = c->n, np = c->np, L = c->L, K = c->K;
   // P mod q_t, P^-1 mod q_t
   c->p_mod_q.assign(L, 0);
@@ -389,6 +383,71 @@ int fa_ctx_create(const fa_params* prm, fa_ctx** out) {
     return fail(FA_E_HIP, "fa_ctx_create: %s", hipGetErrorString(e));
   }
   *out = c;
+  return FA_OK;
+}
+
+extern "C" {
+
+int fa_ctx_create(const fa_params* prm, fa_ctx** out) {
+  if (!prm || !out) return fail(FA_E_INVAL, "fa_ctx_create: null argument");
+  if (prm->log_n < 10 || prm->log_n > 16) return fail(FA_E_INVAL, "log_n must be in [10, 16], got %u", prm->log_n);
+  if (prm->L < 1 || prm->L > 16) return fail(FA_E_INVAL, "L must be in [1, 16], got %u", prm->L);
+  if (prm->K < 1 || prm->K > 4) return fail(FA_E_INVAL, "K must be in [1, 4], got %u", prm->K);
+  if (prm->log_scale < 1 || prm->log_scale > 60) return fail(FA_E_INVAL, "log_scale must be in [1, 60]");
+  std::vector<u64> primes = select_primes((int)prm->log_n, (int)(prm->L + prm->K));
+  if (primes.size() != prm->L + prm->K) return fail(FA_E_INVAL, "not enough 50-bit NTT primes");
+  return ctx_build(prm, primes, out);
+}
+
+int fa_ctx_create_level(const fa_ctx* parent, uint32_t L_low, fa_ctx** out) {
+  if (!parent || !out) return fail(FA_E_INVAL, "fa_ctx_create_level: null argument");
+  if (L_low < 1 || (int)L_low > parent->L) return fail(FA_E_INVAL, "L_low=%u must be in [1, %d]", L_low, parent->L);
+  const fa_params prm{(uint32_t)parent->logn, L_low, (uint32_t)parent->K, (uint32_t)parent->log_scale};
+  std::vector<u64> primes(parent->primes.begin(), parent->primes.begin() + L_low);
+  primes.insert(primes.end(), parent->primes.begin() + parent->L, parent->primes.end());
+  fa_ctx* c = nullptr;
+  int rc = ctx_build(&prm, primes, &c);
+  if (rc) return rc;
+  // restrict the parent's secret and rotation keys (NTT-form limbs per prime:
+  // both contexts use the same root per prime, so the limbs carry over)
+  const size_t n = c->n;
+  hipError_t e = hipSuccess;
+  auto limb_src = [&](int t) { return t < (int)L_low ? t : parent->L + (t - (int)L_low); };
+  for (int t = 0; t < c->np && e == hipSuccess; ++t)
+    e = hipMemcpy(c->d_s + (size_t)t * n, parent->d_s + (size_t)limb_src(t) * n, n * 8, hipMemcpyDeviceToDevice);
+  for (auto& kv : parent->keys) {
+    if (e != hipSuccess) break;
+    double* key = nullptr;
+    if ((rc = dev_alloc(&key, (size_t)c->dnum * 2 * c->np * n))) {
+      fa_ctx_destroy(c);
+      return rc;
+    }
+    c->keys[kv.first] = key;
+    for (int i = 0; i < c->dnum && e == hipSuccess; ++i)
+      for (int h = 0; h < 2 && e == hipSuccess; ++h)
+        for (int t = 0; t < c->np && e == hipSuccess; ++t)
+          e = hipMemcpy(key + (((size_t)i * 2 + h) * c->np + t) * n,
+                        kv.second + (((size_t)i * 2 + h) * parent->np + limb_src(t)) * n, n * 8,
+                        hipMemcpyDeviceToDevice);
+  }
+  if (e != hipSuccess) {
+    fa_ctx_destroy(c);
+    return fail(FA_E_HIP, "fa_ctx_create_level: %s", hipGetErrorString(e));
+  }
+  *out = c;
+  return FA_OK;
+}
+
+int fa_drop_level(const fa_ctx* parent, const fa_ctx* child, const void* ct, void* out, void* stream) {
+  if (!parent || !child || !ct || !out) return fail(FA_E_INVAL, "fa_drop_level: null argument");
+  if (child->n != parent->n || child->L > parent->L) return fail(FA_E_SHAPE, "fa_drop_level: not a lower level");
+  for (int t = 0; t < child->L; ++t)
+    if (child->primes[t] != parent->primes[t]) return fail(FA_E_SHAPE, "fa_drop_level: prime %d differs", t);
+  const size_t n = parent->n;
+  hipStream_t s = (hipStream_t)stream;
+  for (int h = 0; h < 2; ++h)
+    HIPCHK(hipMemcpyAsync((double*)out + (size_t)h * child->L * n, (const double*)ct + (size_t)h * parent->L * n,
+                          (size_t)child->L * n * 8, hipMemcpyDeviceToDevice, s));
   return FA_OK;
 }
 
@@ -827,7 +886,7 @@ int lanes_wanted() {
   static int v = -1;
   if (v < 0) {
     const char* e = getenv("FA_STREAMS");
-    v = e ? atoi(e) : 3;
+    v = e ? atoi(e) : 2;
     if (v < 1) v = 1;
     if (v > FA_MAXAUX + 1) v = FA_MAXAUX + 1;
   }

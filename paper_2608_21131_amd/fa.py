@@ -47,6 +47,8 @@ _f32p = ctypes.POINTER(ctypes.c_float)
 SIGNATURES = {
     "fa_ctx_create": (ctypes.c_int, [ctypes.POINTER(_Params), ctypes.POINTER(_vp)]),
     "fa_ctx_destroy": (None, [_vp]),
+    "fa_ctx_create_level": (ctypes.c_int, [_vp, ctypes.c_uint32, ctypes.POINTER(_vp)]),
+    "fa_drop_level": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp]),
     "fa_ctx_primes": (ctypes.c_int, [_vp, _u64p]),
     "fa_ct_words": (ctypes.c_size_t, [_vp]),
     "fa_pt_words": (ctypes.c_size_t, [_vp]),
@@ -121,7 +123,7 @@ def _dev(t: torch.Tensor):
 class Context:
     """One parameter set (ring degree, primes, tables, rotation keys) on the current GPU."""
 
-    def __init__(self, log_n: int, L: int, K: int, log_scale: int = 40):
+    def __init__(self, log_n: int, L: int, K: int, log_scale: int = 40, _parent: "Context | None" = None):
         if not torch.cuda.is_available():
             raise RuntimeError("libfa needs a HIP GPU; none is visible")
         self.lib = load_library()
@@ -129,15 +131,30 @@ class Context:
         self.n = 1 << log_n
         self.slots = self.n // 2
         self.dnum = -(-L // K)
-        prm = _Params(log_n, L, K, log_scale)
         h = _vp()
-        _check(self.lib.fa_ctx_create(ctypes.byref(prm), ctypes.byref(h)))
+        if _parent is None:
+            prm = _Params(log_n, L, K, log_scale)
+            _check(self.lib.fa_ctx_create(ctypes.byref(prm), ctypes.byref(h)))
+        else:
+            _check(self.lib.fa_ctx_create_level(_parent.h, L, ctypes.byref(h)))
         self.h = h
+        self.parent = _parent
         pr = np.zeros(L + K, dtype=np.uint64)
         _check(self.lib.fa_ctx_primes(self.h, _ptr(pr, _u64p)))
         self.primes = [int(x) for x in pr]
         self.ct_words = int(self.lib.fa_ct_words(self.h))
         self.pt_words = int(self.lib.fa_pt_words(self.h))
+
+    def at_level(self, L_low: int) -> "Context":
+        """Lower-level context: first L_low ciphertext primes, same special primes,
+        restricted secret and rotation keys."""
+        return Context(self.log_n, L_low, self.K, self.log_scale, _parent=self)
+
+    def drop_level(self, child: "Context", ct: torch.Tensor, out: torch.Tensor | None = None,
+                   stream=None) -> torch.Tensor:
+        out = child.new_ct() if out is None else out
+        _check(self.lib.fa_drop_level(self.h, child.h, _dev(ct), _dev(out), _stream(stream)))
+        return out
 
     def close(self):
         if getattr(self, "h", None):

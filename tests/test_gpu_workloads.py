@@ -171,3 +171,66 @@ def test_rank_reduction_fullsize():
     raw = st.decode(out, 0, 120)[:w.rows]
     cos = raw / np.linalg.norm(qR)
     assert np.max(np.abs(cos - Xr @ qR / np.linalg.norm(qR))) < 1e-4
+
+
+def test_rerank_level_at_three_primes_fullsize():
+    """Level drop: the query (encrypted at all 12 primes) is dropped to 3 ciphertext primes and
+    the 110,000 x 512 rerank level is scored there, with the database enrolled at that level and
+    the rotation keys restricted.  Dropped ciphertext, one rotation and the last block bit-exact
+    against the oracle at the lower level; all scores within 1e-4."""
+    from paper_2608_21131_amd import fa
+    w = wl.WORKLOADS["rerank"]
+    L_low = 3
+    par = ckks.Params(logn=w.log_n, L=w.L, K=w.K)
+    lp = ckks.Params(logn=w.log_n, L=L_low, K=w.K, primes=par.q[:L_low] + par.p)
+    ctx = fa.Context(w.log_n, w.L, w.K, 40)
+    s = wl.secret(w)
+    steps = wl.rotation_steps(w)
+    say(f"[low] keys for {len(steps)} rotations at 12 primes")
+    for i in range(0, len(steps), 8):
+        chunk = steps[i:i + 8]
+        rand = [wl.key_randomness(w, r, par.primes, par.dnum) for r in chunk]
+        ctx.keygen(s, chunk, np.stack([x[0] for x in rand]), np.stack([x[1] for x in rand]))
+    low = ctx.at_level(L_low)
+    assert low.primes == lp.primes
+    lo = ckks.Oracle(lp)
+    idx = list(range(L_low)) + list(range(par.L, par.L + par.K))
+    keys = {}
+    for r in steps:
+        a, e = wl.key_randomness(w, r, par.primes, par.dnum)
+        keys[r] = lo.keygen(s, r, a[:lp.dnum][:, idx], e[:lp.dnum])
+    X, centers = wl.candidate_rows(w)
+    q = wl.query_vectors(w, 1, centers)[0]
+    a, e = wl.enc_randomness(w, par.q)
+    m = ckks.encode(ckks.replicate(q, par.slots), par.n, 40)
+    ct = ctx.encrypt(m, a, e)
+    ct_low = ctx.drop_level(low, ct)
+    full_o = ckks.Oracle(par).encrypt(m, a, e, s)
+    ct_low_o = np.ascontiguousarray(full_o[:, :L_low])
+    assert np.array_equal(low.export(ct_low, 2).reshape(2, L_low, par.n), ct_low_o)
+    say("[low] one rotation at 3 primes")
+    assert np.array_equal(low.export(low.rotate(ct_low, 5), 2).reshape(2, L_low, par.n),
+                          lo.rotate(ct_low_o, 5, keys[5]))
+    S = par.slots
+    blocks, ref_coeffs = [], None
+    for b in range(w.n_blocks):
+        rows = X[b * S:(b + 1) * S]
+        if b == w.n_blocks - 1:
+            ref_coeffs = ckks.layout_b_coeffs(rows.astype(np.float64), lp, w.d, w.B)
+            blocks.append(low.encode_db_block_int(ref_coeffs))
+        else:
+            blocks.append(low.encode_db_block(rows, w.d, 1, w.B))
+    say("[low] scoring 4 blocks at 3 primes")
+    out = low.score_block(ct_low, blocks, w.d, 1, w.B)
+    got = low.export(out, 2 * w.n_blocks).reshape(w.n_blocks, 2, L_low, par.n)[-1]
+    qrot = lo.baby_rotations(ct_low_o, w.B, keys)
+    pts_o = np.stack([ckks.to_residues(x, lp.q) for x in ref_coeffs]).reshape(w.G, w.B, L_low, par.n)
+    assert np.array_equal(got, lo.bsgs_block(qrot, pts_o, w.B, w.G, keys))
+    err = 0.0
+    W_ = low.ct_words
+    for b in range(w.n_blocks):
+        rows = X[b * S:(b + 1) * S].astype(np.float64)
+        z = low.decode(low.decrypt(out[b * W_:(b + 1) * W_]), 80)
+        err = max(err, float(np.max(np.abs(z[:len(rows)] - rows @ q))))
+    say(f"[low] max |score - float64| = {err:.2e}")
+    assert err < 1e-4

@@ -514,3 +514,47 @@ def test_projection_then_scoring_with_norm_correction():
     assert np.max(np.abs(raw - Xr @ qR)) < 1e-4
     cos = raw / np.linalg.norm(qR)
     assert np.max(np.abs(cos - Xr @ qR / np.linalg.norm(qR))) < 1e-4
+
+
+# ----------------------------------------------------------------------------
+# lower levels: restricted keys and dropped ciphertexts
+# ----------------------------------------------------------------------------
+def low_params(par, L_low):
+    return ckks.Params(logn=par.logn, L=L_low, K=par.K, primes=par.q[:L_low] + par.p)
+
+
+def restrict(par, L_low, x):
+    """Limbs of a [..][L+K][N] array for the primes of the lower level."""
+    idx = list(range(L_low)) + list(range(par.L, par.L + par.K))
+    return x[..., idx, :]
+
+
+@pytest.mark.parametrize("L_low", [2, 3])
+def test_lower_level_key_is_restriction_of_full_key(small4, L_low):
+    """Key generated at the lower level from the restricted randomness == restricted full key."""
+    par, orc = small4
+    s = gen.ternary_secret(gen.rng(12, gen.STREAM_SECRET), par.n)
+    a = gen.uniform_residues(gen.rng(12, gen.STREAM_KEY_A, 3), par.primes, par.dnum, par.n)
+    e = gen.rounded_gaussian(gen.rng(12, gen.STREAM_KEY_E, 3), (par.dnum, par.n))
+    b_full, _ = orc.keygen(s, 3, a, e)
+    lp = low_params(par, L_low)
+    lo = ckks.Oracle(lp)
+    b_low, _ = lo.keygen(s, 3, restrict(par, L_low, a)[:lp.dnum], e[:lp.dnum])
+    assert np.array_equal(b_low, restrict(par, L_low, b_full)[:lp.dnum])
+
+
+def test_dropped_ciphertext_decrypts_and_rotates(small4):
+    par, orc = small4
+    L_low = 2
+    s = gen.ternary_secret(gen.rng(13, gen.STREAM_SECRET), par.n)
+    v = np.random.default_rng(13).uniform(-1, 1, par.slots)
+    ct = enc(orc, v, s, wid=13)
+    lp = low_params(par, L_low)
+    lo = ckks.Oracle(lp)
+    ct_low = np.ascontiguousarray(ct[:, :L_low])
+    assert np.max(np.abs(ckks.decode_residues(lo.decrypt(ct_low, s), lp, 40) - v)) < 1e-6
+    a = gen.uniform_residues(gen.rng(13, gen.STREAM_KEY_A, 5), par.primes, par.dnum, par.n)
+    e = gen.rounded_gaussian(gen.rng(13, gen.STREAM_KEY_E, 5), (par.dnum, par.n))
+    key = lo.keygen(s, 5, restrict(par, L_low, a)[:lp.dnum], e[:lp.dnum])
+    z = ckks.decode_residues(lo.decrypt(lo.rotate(ct_low, 5, key), s), lp, 40)
+    assert np.max(np.abs(z - np.roll(v, -5))) < 1e-6
