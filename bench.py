@@ -231,19 +231,24 @@ def run_three_level(bn, args):
     """32 queries, each: coarse level (222,049 rows, 7 blocks) -> client decrypt, top-16 ->
     fine level (2 of 4 fine-pool blocks) -> top-64 -> rerank level (4 of 8 rerank-pool
     blocks, the last truncated to 11,696 rows) -> top-10.  Pool blocks are chosen by
-    hashing the kept ids (id mod pool size), deterministic and data-oblivious in cost."""
-    w, ctx, fa, torch = bn.w, bn.ctx, bn.fa, bn.torch
+    hashing the kept ids (id mod pool size), deterministic and data-oblivious in cost.
+    Each query is dropped to --level primes (default 3) and its baby rotations are
+    computed once and reused by the three levels."""
+    w, fa, torch = bn.w, bn.fa, bn.torch
+    top_ctx = bn.ctx
+    level = args.level if args.level else 3
+    ctx = top_ctx.at_level(level) if level < w.L else top_ctx
     ex = w.extra
     S = w.slots
     nq = args.queries or ex["queries"]
     g_coarse, centers = bn.wl.candidate_rows(w, ex["coarse"], stream_extra=1)
-    # the fine and rerank pools are drawn around the same cluster centres
     pools = {"coarse": [], "fine": [], "rerank": []}
     rows_of = {"coarse": [], "fine": [], "rerank": []}
     for b in range(-(-ex["coarse"] // S)):
         r = g_coarse[b * S:(b + 1) * S]
         rows_of["coarse"].append(r)
         pools["coarse"].append(ctx.encode_db_block(r, w.d, fa.LAYOUT_DIAG, w.B))
+    # the fine and rerank pools are drawn around the same cluster centres
     for name, nb, extra in (("fine", ex["fine_pool_blocks"], 2), ("rerank", ex["rerank_pool_blocks"], 3)):
         X, _ = bn.wl.candidate_rows(w, nb * S, stream_extra=extra, centers=centers)
         for b in range(nb):
@@ -252,20 +257,27 @@ def run_three_level(bn, args):
             pools[name].append(ctx.encode_db_block(r, w.d, fa.LAYOUT_DIAG, w.B))
     torch.cuda.synchronize()
     nblk = sum(len(v) for v in pools.values())
-    log(f"[bench] three_level: {nblk} resident blocks ({nblk * w.d * w.L * w.n * 8 / 1e9:.1f} GB), "
-        f"{time.time() - bn.t0:.1f}s")
+    log(f"[bench] three_level: {nblk} resident blocks at {ctx.L} primes "
+        f"({nblk * w.d * ctx.L * w.n * 8 / 1e9:.1f} GB), {time.time() - bn.t0:.1f}s")
     queries = bn.wl.query_vectors(w, nq, centers)
     qcts = [bn.encrypt(qv, tag=i) for i, qv in enumerate(queries)]
+    q = ctx.new_ct()
+    prep = ctx.prepare_query(qcts[0] if ctx is top_ctx else top_ctx.drop_level(ctx, qcts[0]), w.B)
     out = ctx.new_ct(7)
-    ws = ctx.workspace(fa.OP_SCORE, 7, w.d, w.B)
+    ws_p = ctx.workspace(fa.OP_PREPARE, 1, w.B, w.B)
+    ws = ctx.workspace(fa.OP_SCORE_PREPARED, 7, w.d, w.B)
     stream = torch.cuda.current_stream()
     level_ms = []
     errs = []
 
+    def decode(ct, b):
+        W_ = ctx.ct_words
+        return ctx.decode(ctx.decrypt(ct[b * W_:(b + 1) * W_]), 80)
+
     def top(ct, nb, k, rows_list, qv, n_rows_last=None):
         scores = []
         for b in range(nb):
-            z = bn.decode(ct, b, 80)
+            z = decode(ct, b)
             n_valid = len(rows_list[b]) if (b < nb - 1 or n_rows_last is None) else n_rows_last
             scores.append(z[:n_valid])
             if qv is not None:
@@ -277,27 +289,35 @@ def run_three_level(bn, args):
 
     def one_query(i, check):
         qv = queries[i] if check else None
-        evs = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(7)]
         evs[0].record(stream)
-        ctx.score_block(qcts[i], pools["coarse"], w.d, fa.LAYOUT_DIAG, w.B, out=out, ws=ws)
+        if ctx is not top_ctx:
+            top_ctx.drop_level(ctx, qcts[i], out=q)
+            qi = q
+        else:
+            qi = qcts[i]
+        ctx.prepare_query(qi, w.B, out=prep, ws=ws_p)
         evs[1].record(stream)
+        ctx.score_prepared(qi, prep, pools["coarse"], w.d, w.B, out=out, ws=ws)
+        evs[2].record(stream)
         ids = top(out, len(pools["coarse"]), ex["top_coarse"], rows_of["coarse"], qv)
         fsel = sorted(set(int(x) % ex["fine_pool_blocks"] for x in ids))
         fsel = (fsel + [b for b in range(ex["fine_pool_blocks"]) if b not in fsel])[:ex["fine_blocks"]]
-        evs[2].record(stream)
-        ctx.score_block(qcts[i], [pools["fine"][b] for b in fsel], w.d, fa.LAYOUT_DIAG, w.B, out=out, ws=ws)
         evs[3].record(stream)
+        ctx.score_prepared(qi, prep, [pools["fine"][b] for b in fsel], w.d, w.B, out=out, ws=ws)
+        evs[4].record(stream)
         ids = top(out, len(fsel), ex["top_fine"], [rows_of["fine"][b] for b in fsel], qv)
         rsel = sorted(set(int(x) % ex["rerank_pool_blocks"] for x in ids))
         rsel = (rsel + [b for b in range(ex["rerank_pool_blocks"]) if b not in rsel])[:ex["rerank_blocks"]]
-        evs[4].record(stream)
-        ctx.score_block(qcts[i], [pools["rerank"][b] for b in rsel], w.d, fa.LAYOUT_DIAG, w.B, out=out, ws=ws)
         evs[5].record(stream)
+        ctx.score_prepared(qi, prep, [pools["rerank"][b] for b in rsel], w.d, w.B, out=out, ws=ws)
+        evs[6].record(stream)
         top(out, len(rsel), 10, [rows_of["rerank"][b] for b in rsel], qv, n_rows_last=ex["rerank_last"])
         torch.cuda.synchronize()
-        level_ms.append([evs[0].elapsed_time(evs[1]), evs[2].elapsed_time(evs[3]), evs[4].elapsed_time(evs[5])])
+        level_ms.append([evs[0].elapsed_time(evs[1]), evs[1].elapsed_time(evs[2]), evs[3].elapsed_time(evs[4]),
+                         evs[5].elapsed_time(evs[6])])
 
-    for i in range(min(2, nq)):  # warm-up queries (first one checked against float64)
+    for i in range(min(2, nq)):  # warm-up queries (the first one checked against float64)
         one_query(i, check=(i == 0))
     level_ms.clear()
     t = time.time()
@@ -309,11 +329,12 @@ def run_three_level(bn, args):
     lm = np.array(level_ms)
     gpu_q = float(lm.sum(axis=1).mean())
     n_scores = ex["coarse"] + ex["fine_blocks"] * S + (ex["rerank_blocks"] - 1) * S + ex["rerank_last"]
-    ph = {"coarse_ms": float(lm[:, 0].mean()), "fine_ms": float(lm[:, 1].mean()),
-          "rerank_ms": float(lm[:, 2].mean()), "query_gpu_ms": gpu_q, "query_wall_ms": wall * 1e3}
+    ph = {"prepare_ms": float(lm[:, 0].mean()), "coarse_ms": float(lm[:, 1].mean()),
+          "fine_ms": float(lm[:, 2].mean()), "rerank_ms": float(lm[:, 3].mean()), "query_gpu_ms": gpu_q,
+          "query_wall_ms": wall * 1e3}
     blocks_q = len(pools["coarse"]) + ex["fine_blocks"] + ex["rerank_blocks"]
     return dict(ms=gpu_q, scores=n_scores, phases=ph, err=max(errs) if errs else None, mac_bytes=None,
-                stream_bytes=8 * blocks_q * w.d * w.L * w.n, cpu=None, queries=nq)
+                stream_bytes=8 * blocks_q * w.d * ctx.L * w.n, cpu=None, queries=nq, level=ctx.L)
 
 
 def measured_traffic(path):
@@ -419,6 +440,8 @@ def main():
                             "level before scoring")
     if r.get("queries"):
         cfg["queries_per_step"] = r["queries"]
+    if r.get("level") and r["level"] < w.L:
+        cfg["scoring_level_primes"] = r["level"]
     res = {
         "metric": METRIC,
         "value": round(value, 1),

@@ -63,7 +63,14 @@ enum {
 };
 
 enum { FA_LAYOUT_ROW = 0, FA_LAYOUT_DIAG = 1 };
-enum { FA_OP_SCORE = 0, FA_OP_PROJECT = 1, FA_OP_ROTATE_SUM = 2, FA_OP_ROTATE = 3 };
+enum {
+  FA_OP_SCORE = 0,
+  FA_OP_PROJECT = 1,
+  FA_OP_ROTATE_SUM = 2,
+  FA_OP_ROTATE = 3,
+  FA_OP_PREPARE = 4,
+  FA_OP_SCORE_PREPARED = 5
+};
 
 typedef struct fa_ctx fa_ctx;
 
@@ -187,6 +194,21 @@ size_t fa_workspace_bytes(const fa_ctx* ctx, int op, int n_blocks, int d, int ba
  * ws: device workspace of ws_bytes >= fa_workspace_bytes(...). */
 int fa_score_block(fa_ctx* ctx, const void* q, const void* const* blocks, int n_blocks, int d, int layout,
                    int baby_step, void* out, void* ws, size_t ws_bytes, void* stream);
+
+/* The same diagonal-layout scoring split in two, so that one query's baby
+ * rotations serve several levels or batches (the paper projects the query
+ * once and reuses it across batches, Section 3.4):
+ *   fa_prepare_query writes Rotate(q, b), b = 1..baby_step-1, into prep
+ *     (device, fa_prepared_words(ctx, baby_step) words);
+ *   fa_score_prepared then scores q against n_blocks blocks exactly as
+ *     fa_score_block with FA_LAYOUT_DIAG does (bit-identical output).
+ * Workspace: FA_OP_PREPARE (baby_step) and FA_OP_SCORE_PREPARED (n_blocks,
+ * d, baby_step). */
+size_t fa_prepared_words(const fa_ctx* ctx, int baby_step);
+int fa_prepare_query(fa_ctx* ctx, const void* q, int baby_step, void* prep, void* ws, size_t ws_bytes,
+                     void* stream);
+int fa_score_prepared(fa_ctx* ctx, const void* q, const void* prep, const void* const* blocks, int n_blocks, int d,
+                      int baby_step, void* out, void* ws, size_t ws_bytes, void* stream);
 
 /* Encrypted projection q_R = W^T q (Section 3.1): q holds a d_in-periodic
  * query, w_pts the r plaintexts of W's hybrid diagonals

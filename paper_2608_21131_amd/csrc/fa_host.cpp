@@ -893,23 +893,24 @@ int lanes_wanted() {
   return v;
 }
 
-size_t score_ws(const fa_ctx* c, int nb, int d, int B) {
+// workspace of the baby rotations (qrot itself is separate)
+size_t baby_ws(const fa_ctx* c, int B) {
   const size_t n = c->n, L = c->L, np = c->np, dn = c->dnum;
-  const size_t G = d / B;
   const size_t rb = std::max(1, std::min(rot_batch(), B - 1));
   const size_t lanes = lanes_wanted();
-  size_t w = 0;
-  w += rup(L * n);                            // scaled coefficients of q.c1
-  w += rup(dn * np * n);                      // extended digits of q
-  w += lanes * rup(rb * 2 * np * n);          // key-switch products, per lane
-  w += lanes * rup(rb * 2 * L * n);           // ModDown conversions, per lane
-  w += rup((size_t)(B - 1) * 2 * L * n + 1);  // baby rotations 1..B-1
-  w += rup(nb * G * 2 * L * n);               // accumulators
-  w += lanes * rup(nb * L * n);               // giant-step scaled coefficients, per lane
-  w += lanes * rup(nb * dn * np * n);         // giant-step extended digits, per lane
-  w += lanes * rup(nb * 2 * np * n);          // giant-step key-switch sums, per lane
-  w += rup(nb * 2 * L * n);                   // giant-step ModDown conversions
-  return w;
+  return rup(L * n) + rup(dn * np * n) + lanes * rup(rb * 2 * np * n) + lanes * rup(rb * 2 * L * n);
+}
+// workspace of the multiply-accumulate and the giant steps
+size_t giant_ws(const fa_ctx* c, int nb, int d, int B) {
+  const size_t n = c->n, L = c->L, np = c->np, dn = c->dnum;
+  const size_t G = d / B;
+  const size_t lanes = lanes_wanted();
+  return rup(nb * G * 2 * L * n) + lanes * rup(nb * L * n) + lanes * rup(nb * dn * np * n) +
+         lanes * rup(nb * 2 * np * n) + rup(nb * 2 * L * n);
+}
+size_t qrot_words(const fa_ctx* c, int B) { return (size_t)(B - 1) * 2 * c->L * c->n + 1; }
+size_t score_ws(const fa_ctx* c, int nb, int d, int B) {
+  return baby_ws(c, B) + rup(qrot_words(c, B)) + giant_ws(c, nb, d, B);
 }
 }  // namespace
 
@@ -1044,19 +1045,54 @@ static int rotate_batch(fa_ctx* c, const double* cts, int nb, int step, double* 
   return check_launch("rotate_batch");
 }
 
-// Diagonal-layout scoring (baby-step / giant-step) of q against nb blocks.
-static int score_diag(fa_ctx* c, const double* q, const double* const* blocks, int nb, int d, int B, double* out,
-                      Arena& ar, hipStream_t s) {
+// Baby rotations qrot[b-1] = Rotate(q, b), b = 1..B-1: one shared decomposition
+// of q.c1, rotation batches spread over lanes.
+static int baby_phase(fa_ctx* c, const double* q, int B, double* qrot, Arena& ar, hipStream_t s) {
   const size_t n = c->n, L = c->L, np = c->np, dn = c->dnum;
-  const int G = d / B;
   const size_t ctw = 2 * L * n;
+  if (B < 2) return FA_OK;
+  for (int b = 1; b < B; ++b)
+    if (!c->keys.count(b)) return fail(FA_E_NOKEY, "no rotation key for baby step %d", b);
   const int rb = std::max(1, std::min(rot_batch(), B - 1));
   const int lanes = lanes_wanted();
+  const size_t mark = ar.used;
   double* y = ar.take(L * n);
   double* ext = ar.take(dn * np * n);
   double* u = ar.take((size_t)lanes * (rup((size_t)rb * 2 * np * n) / 8));
   double* conv = ar.take((size_t)lanes * (rup((size_t)rb * 2 * L * n) / 8));
-  double* qrot = ar.take((size_t)(B - 1) * ctw + 1);
+  if (!y || !ext || !u || !conv) return fail(FA_E_NOMEM, "workspace too small for the baby rotations");
+  int rc = ensure_lanes(c, lanes);
+  if (rc) return rc;
+  modup(c, q, ctw, 1, y, L * n, ext, dn * np * n, s);
+  std::vector<int> steps(B - 1);
+  std::vector<double*> outs(B - 1);
+  for (int b = 1; b < B; ++b) {
+    steps[b - 1] = b;
+    outs[b - 1] = qrot + (size_t)(b - 1) * ctw;
+  }
+  const int nbatch = (B - 1 + rb - 1) / rb;
+  const int bl = std::min(lanes, nbatch);
+  if ((rc = fork_lanes(c, s, bl))) return rc;
+  rc = rotations_from_ext(c, q, ext, steps.data(), B - 1, outs.data(), u, conv, s, bl, rb,
+                          rup((size_t)rb * 2 * np * n) / 8, rup((size_t)rb * 2 * L * n) / 8);
+  if (rc) return rc;
+  if ((rc = join_lanes(c, s, bl))) return rc;
+  ar.used = mark;
+  return FA_OK;
+}
+
+// Multiply-accumulate of q's baby rotations against nb blocks, then the giant
+// steps: Rotate(acc_g, gB) summed over Q u P with one ModDown per block;
+// sigma(acc_g.c0) rides in the key-switch sum multiplied by P.  Giant indices
+// go round-robin to lanes, each lane summing into its own buffer.
+static int mac_giant_phase(fa_ctx* c, const double* q, const double* qrot, const double* const* blocks, int nb,
+                           int d, int B, double* out, Arena& ar, hipStream_t s) {
+  const size_t n = c->n, L = c->L, np = c->np, dn = c->dnum;
+  const int G = d / B;
+  const size_t ctw = 2 * L * n;
+  for (int g = 1; g < G; ++g)
+    if (!c->keys.count(g * B)) return fail(FA_E_NOKEY, "no rotation key for giant step %d", g * B);
+  const int lanes = lanes_wanted();
   double* acc = ar.take((size_t)nb * G * ctw);
   const size_t gy_l = rup((size_t)nb * L * n) / 8, gext_l = rup((size_t)nb * dn * np * n) / 8,
                us_l = rup((size_t)nb * 2 * np * n) / 8;
@@ -1064,40 +1100,12 @@ static int score_diag(fa_ctx* c, const double* q, const double* const* blocks, i
   double* gext = ar.take(lanes * gext_l);
   double* usum = ar.take(lanes * us_l);
   double* gconv = ar.take((size_t)nb * 2 * L * n);
-  if (!y || !ext || !u || !conv || !qrot || !acc || !gy || !gext || !usum || !gconv)
-    return fail(FA_E_NOMEM, "workspace too small for score_block");
-  for (int b = 1; b < B; ++b)
-    if (!c->keys.count(b)) return fail(FA_E_NOKEY, "no rotation key for baby step %d", b);
-  for (int g = 1; g < G; ++g)
-    if (!c->keys.count(g * B)) return fail(FA_E_NOKEY, "no rotation key for giant step %d", g * B);
+  if (!acc || !gy || !gext || !usum || !gconv) return fail(FA_E_NOMEM, "workspace too small for score_block");
   int rc = ensure_lanes(c, lanes);
   if (rc) return rc;
-
-  if (c->prof) HIPCHK(hipEventRecord(c->ev[0], s));
-  // 1. baby rotations of the query, one shared decomposition; batches spread over lanes
-  if (B > 1) {
-    modup(c, q, ctw, 1, y, L * n, ext, dn * np * n, s);
-    std::vector<int> steps(B - 1);
-    std::vector<double*> outs(B - 1);
-    for (int b = 1; b < B; ++b) {
-      steps[b - 1] = b;
-      outs[b - 1] = qrot + (size_t)(b - 1) * ctw;
-    }
-    const int nbatch = (B - 1 + rb - 1) / rb;
-    const int bl = std::min(lanes, nbatch);
-    if ((rc = fork_lanes(c, s, bl))) return rc;
-    rc = rotations_from_ext(c, q, ext, steps.data(), B - 1, outs.data(), u, conv, s, bl, rb,
-                            rup((size_t)rb * 2 * np * n) / 8, rup((size_t)rb * 2 * L * n) / 8);
-    if (rc) return rc;
-    if ((rc = join_lanes(c, s, bl))) return rc;
-  }
   if (c->prof) HIPCHK(hipEventRecord(c->ev[1], s));
-  // 2. multiply-accumulate against the resident plaintexts
   fa::mac_diag(c, q, qrot, blocks, nb, B, G, acc, s);
   if (c->prof) HIPCHK(hipEventRecord(c->ev[2], s));
-  // 3. giant steps: Rotate(acc_g, gB) summed over Q u P, one ModDown per block;
-  //    sigma(acc_g.c0) rides in the key-switch sum multiplied by P.  Giant
-  //    indices go round-robin to lanes, each lane summing into its own buffer.
   const size_t astride = (size_t)G * ctw;
   if (G == 1) {
     for (int blk = 0; blk < nb; ++blk)
@@ -1143,6 +1151,19 @@ static int score_diag(fa_ctx* c, const double* q, const double* const* blocks, i
   return check_launch("score_block");
 }
 
+// Diagonal-layout scoring (baby-step / giant-step) of q against nb blocks.
+static int score_diag(fa_ctx* c, const double* q, const double* const* blocks, int nb, int d, int B, double* out,
+                      Arena& ar, hipStream_t s) {
+  double* qrot = ar.take(qrot_words(c, B));
+  if (!qrot) return fail(FA_E_NOMEM, "workspace too small for score_block");
+  for (int g = 1; g < d / B; ++g)
+    if (!c->keys.count(g * B)) return fail(FA_E_NOKEY, "no rotation key for giant step %d", g * B);
+  if (c->prof) HIPCHK(hipEventRecord(c->ev[0], s));
+  int rc = baby_phase(c, q, B, qrot, ar, s);
+  if (rc) return rc;
+  return mac_giant_phase(c, q, qrot, blocks, nb, d, B, out, ar, s);
+}
+
 extern "C" {
 
 size_t fa_workspace_bytes(const fa_ctx* c, int op, int n_blocks, int d, int baby_step) {
@@ -1157,9 +1178,47 @@ size_t fa_workspace_bytes(const fa_ctx* c, int op, int n_blocks, int d, int baby
     case FA_OP_ROTATE_SUM:
     case FA_OP_ROTATE:
       return rotate_ws(c, std::min(std::max(1, n_blocks), kRotBatch)) + rup(fa_ct_words(c) * kRotBatch);
+    case FA_OP_PREPARE:
+      if (baby_step < 1) return 0;
+      return baby_ws(c, baby_step);
+    case FA_OP_SCORE_PREPARED:
+      if (baby_step < 1 || d < baby_step) return 0;
+      return giant_ws(c, std::max(1, n_blocks), d, baby_step);
     default:
       return 0;
   }
+}
+
+size_t fa_prepared_words(const fa_ctx* c, int baby_step) {
+  return (c && baby_step >= 1) ? qrot_words(c, baby_step) : 0;
+}
+
+int fa_prepare_query(fa_ctx* c, const void* q, int baby_step, void* prep, void* ws, size_t ws_bytes, void* stream) {
+  if (!c || !q || !prep) return fail(FA_E_INVAL, "fa_prepare_query: null argument");
+  if (baby_step < 1 || baby_step > c->n / 2) return fail(FA_E_INVAL, "baby_step %d out of range", baby_step);
+  const size_t need = baby_ws(c, baby_step);
+  if (baby_step > 1 && (!ws || ws_bytes < need)) return fail(FA_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
+  Arena ar{(char*)ws, ws_bytes, 0};
+  int rc = baby_phase(c, (const double*)q, baby_step, (double*)prep, ar, (hipStream_t)stream);
+  return rc ? rc : check_launch("fa_prepare_query");
+}
+
+int fa_score_prepared(fa_ctx* c, const void* q, const void* prep, const void* const* blocks, int n_blocks, int d,
+                      int baby_step, void* out, void* ws, size_t ws_bytes, void* stream) {
+  if (!c || !q || !prep || !blocks || !out) return fail(FA_E_INVAL, "fa_score_prepared: null argument");
+  if (n_blocks < 1) return fail(FA_E_SHAPE, "n_blocks must be positive");
+  for (int i = 0; i < n_blocks; ++i)
+    if (!blocks[i]) return fail(FA_E_INVAL, "block %d is null", i);
+  const int S = c->n / 2;
+  if (d < 1 || (d & (d - 1)) || d > S) return fail(FA_E_SHAPE, "d=%d must be a power of two <= N/2", d);
+  if (baby_step < 1 || d % baby_step) return fail(FA_E_INVAL, "baby_step %d must divide d=%d", baby_step, d);
+  const size_t need = giant_ws(c, n_blocks, d, baby_step);
+  if (!ws || ws_bytes < need) return fail(FA_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
+  Arena ar{(char*)ws, ws_bytes, 0};
+  hipStream_t s = (hipStream_t)stream;
+  if (c->prof) HIPCHK(hipEventRecord(c->ev[0], s));
+  return mac_giant_phase(c, (const double*)q, (const double*)prep, (const double* const*)blocks, n_blocks, d,
+                         baby_step, (double*)out, ar, s);
 }
 
 int fa_score_block(fa_ctx* c, const void* q, const void* const* blocks, int n_blocks, int d, int layout,

@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libfa.so")
 
 FA_OK, FA_E_INVAL, FA_E_SHAPE, FA_E_NOKEY, FA_E_NOMEM, FA_E_HIP = 0, -1, -2, -3, -4, -5
 LAYOUT_ROW, LAYOUT_DIAG = 0, 1
-OP_SCORE, OP_PROJECT, OP_ROTATE_SUM, OP_ROTATE = 0, 1, 2, 3
+OP_SCORE, OP_PROJECT, OP_ROTATE_SUM, OP_ROTATE, OP_PREPARE, OP_SCORE_PREPARED = 0, 1, 2, 3, 4, 5
 
 _ERR_NAMES = {FA_E_INVAL: "FA_E_INVAL", FA_E_SHAPE: "FA_E_SHAPE", FA_E_NOKEY: "FA_E_NOKEY",
               FA_E_NOMEM: "FA_E_NOMEM", FA_E_HIP: "FA_E_HIP"}
@@ -74,6 +74,10 @@ SIGNATURES = {
     "fa_rotate_sum": (ctypes.c_int, [_vp, _vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, _vp, ctypes.c_size_t,
                                      _vp]),
     "fa_rotate": (ctypes.c_int, [_vp, _vp, ctypes.c_int, _vp, _vp, ctypes.c_size_t, _vp]),
+    "fa_prepared_words": (ctypes.c_size_t, [_vp, ctypes.c_int]),
+    "fa_prepare_query": (ctypes.c_int, [_vp, _vp, ctypes.c_int, _vp, _vp, ctypes.c_size_t, _vp]),
+    "fa_score_prepared": (ctypes.c_int, [_vp, _vp, _vp, ctypes.POINTER(_vp), ctypes.c_int, ctypes.c_int,
+                                         ctypes.c_int, _vp, _vp, ctypes.c_size_t, _vp]),
     "fa_profile": (ctypes.c_int, [_vp, ctypes.c_int]),
     "fa_profile_read": (ctypes.c_int, [_vp, _f64p]),
 }
@@ -266,6 +270,26 @@ class Context:
         ws_p, ws_b = (_dev(ws), ws.numel() * 8) if ws is not None else (ctypes.c_void_p(0), 0)
         _check(self.lib.fa_score_block(self.h, _dev(q), arr, nb, d, layout, baby_step, _dev(out), ws_p, ws_b,
                                        _stream(stream)))
+        return out
+
+    def prepare_query(self, q: torch.Tensor, baby_step: int, out: torch.Tensor | None = None,
+                      ws: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+        words = int(self.lib.fa_prepared_words(self.h, baby_step))
+        out = torch.empty(words, dtype=torch.float64, device="cuda") if out is None else out
+        ws = self.workspace(OP_PREPARE, 1, baby_step, baby_step) if ws is None else ws
+        _check(self.lib.fa_prepare_query(self.h, _dev(q), baby_step, _dev(out), _dev(ws), ws.numel() * 8,
+                                         _stream(stream)))
+        return out
+
+    def score_prepared(self, q: torch.Tensor, prep: torch.Tensor, blocks, d: int, baby_step: int,
+                       out: torch.Tensor | None = None, ws: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+        blocks = list(blocks)
+        nb = len(blocks)
+        out = self.new_ct(nb) if out is None else out
+        ws = self.workspace(OP_SCORE_PREPARED, nb, d, baby_step) if ws is None else ws
+        arr = (_vp * nb)(*[ctypes.c_void_p(b.data_ptr()) for b in blocks])
+        _check(self.lib.fa_score_prepared(self.h, _dev(q), _dev(prep), arr, nb, d, baby_step, _dev(out), _dev(ws),
+                                          ws.numel() * 8, _stream(stream)))
         return out
 
     def project_ct(self, q: torch.Tensor, w_pts: torch.Tensor, d_in: int, r: int, baby_step: int,

@@ -263,3 +263,22 @@ def test_encode_projection_vs_oracle():
         q0 = np.int64(p.par.q[0])
         dif = np.where(dif > q0 // 2, dif - q0, np.where(dif < -(q0 // 2), dif + q0, dif))
         assert np.abs(dif).max() <= 1, j
+
+
+@pytest.mark.parametrize("name,d,B", [("tiny", 16, 4), ("p1", 128, 16)])
+def test_prepared_query_scores_identically(name, d, B):
+    """fa_prepare_query + fa_score_prepared == fa_score_block, word for word, reused for two block sets."""
+    p = pair(name, wid=14)
+    S = p.par.slots
+    X = gen.gaussian_unit_rows(gen.rng(14, gen.STREAM_DB, d), 2 * S, d)
+    q = gen.gaussian_unit_rows(gen.rng(14, gen.STREAM_QUERY), 1, d)[0]
+    ct, _ = p.encrypt_both(ckks.encode(ckks.replicate(q, S), p.n, 40), tag=14)
+    p.keys(ckks.steps_for_bsgs(d, B), oracle=False)
+    b0 = p.ctx.encode_db_block(X[:S].astype(np.float32), d, 1, B)
+    b1 = p.ctx.encode_db_block(X[S:S + 1000].astype(np.float32), d, 1, B)
+    say(f"[prepared] {name}")
+    prep = p.ctx.prepare_query(ct, B)
+    for blocks in ([b0, b1], [b1]):
+        ref = p.export_ct(p.ctx.score_block(ct, blocks, d, 1, B), len(blocks))
+        got = p.export_ct(p.ctx.score_prepared(ct, prep, blocks, d, B), len(blocks))
+        assert np.array_equal(got, ref)
