@@ -900,13 +900,16 @@ size_t baby_ws(const fa_ctx* c, int B) {
   const size_t lanes = lanes_wanted();
   return rup(L * n) + rup(dn * np * n) + lanes * rup(rb * 2 * np * n) + lanes * rup(rb * 2 * L * n);
 }
+// blocks whose giant steps are processed together
+constexpr int kGiantChunk = 8;
 // workspace of the multiply-accumulate and the giant steps
 size_t giant_ws(const fa_ctx* c, int nb, int d, int B) {
   const size_t n = c->n, L = c->L, np = c->np, dn = c->dnum;
   const size_t G = d / B;
   const size_t lanes = lanes_wanted();
-  return rup(nb * G * 2 * L * n) + lanes * rup(nb * L * n) + lanes * rup(nb * dn * np * n) +
-         lanes * rup(nb * 2 * np * n) + rup(nb * 2 * L * n);
+  const size_t cb = std::min(nb, kGiantChunk);
+  return rup(nb * G * 2 * L * n) + lanes * rup(cb * L * n) + rup(cb * (G > 1 ? G - 1 : 1) * dn * np * n) +
+         rup(cb * 2 * np * n) + rup(cb * 2 * L * n);
 }
 size_t qrot_words(const fa_ctx* c, int B) { return (size_t)(B - 1) * 2 * c->L * c->n + 1; }
 size_t score_ws(const fa_ctx* c, int nb, int d, int B) {
@@ -918,7 +921,7 @@ size_t score_ws(const fa_ctx* c, int nb, int d, int B) {
 // y (per item [L][N]) receives c1's coefficients times (D_i/q_t)^-1; ext receives
 // every converted limb.  The ciphertexts are only read.
 static void modup(fa_ctx* c, const double* cts, size_t ct_stride, int batch, double* y, size_t y_stride,
-                  double* ext, size_t ext_stride, hipStream_t s) {
+                  double* ext, size_t ext_stride, hipStream_t s, bool pass_b = true) {
   const size_t n = c->n, L = c->L;
   {
     fa::LimbBatch inv(c, s, false);
@@ -929,7 +932,7 @@ static void modup(fa_ctx* c, const double* cts, size_t ct_stride, int batch, dou
   }
   std::vector<fa::MuItem> it(batch);
   for (int b = 0; b < batch; ++b) it[b] = {y + (size_t)b * y_stride, ext + (size_t)b * ext_stride};
-  fa::modup_ntt(c, it.data(), batch, s);
+  fa::modup_ntt(c, it.data(), batch, s, pass_b);
 }
 
 // ModDown of `count` polynomials u_i = u + i * np * N over Q u P (NTT form):
@@ -1083,8 +1086,9 @@ static int baby_phase(fa_ctx* c, const double* q, int B, double* qrot, Arena& ar
 
 // Multiply-accumulate of q's baby rotations against nb blocks, then the giant
 // steps: Rotate(acc_g, gB) summed over Q u P with one ModDown per block;
-// sigma(acc_g.c0) rides in the key-switch sum multiplied by P.  Giant indices
-// go round-robin to lanes, each lane summing into its own buffer.
+// sigma(acc_g.c0) rides in the key-switch sum multiplied by P.  The first pass
+// of every giant's ModUp runs on the lanes (round-robin over g); one fused
+// kernel then finishes the transforms and forms the key-switch sums.
 static int mac_giant_phase(fa_ctx* c, const double* q, const double* qrot, const double* const* blocks, int nb,
                            int d, int B, double* out, Arena& ar, hipStream_t s) {
   const size_t n = c->n, L = c->L, np = c->np, dn = c->dnum;
@@ -1093,13 +1097,15 @@ static int mac_giant_phase(fa_ctx* c, const double* q, const double* qrot, const
   for (int g = 1; g < G; ++g)
     if (!c->keys.count(g * B)) return fail(FA_E_NOKEY, "no rotation key for giant step %d", g * B);
   const int lanes = lanes_wanted();
+  const int cbm = std::min(nb, kGiantChunk);
+  const int ng = G > 1 ? G - 1 : 1;
   double* acc = ar.take((size_t)nb * G * ctw);
-  const size_t gy_l = rup((size_t)nb * L * n) / 8, gext_l = rup((size_t)nb * dn * np * n) / 8,
-               us_l = rup((size_t)nb * 2 * np * n) / 8;
+  const size_t gy_l = rup((size_t)cbm * L * n) / 8;
+  const size_t ext_w = dn * np * n;
   double* gy = ar.take(lanes * gy_l);
-  double* gext = ar.take(lanes * gext_l);
-  double* usum = ar.take(lanes * us_l);
-  double* gconv = ar.take((size_t)nb * 2 * L * n);
+  double* gext = ar.take((size_t)cbm * ng * ext_w);
+  double* usum = ar.take((size_t)cbm * 2 * np * n);
+  double* gconv = ar.take((size_t)cbm * 2 * L * n);
   if (!acc || !gy || !gext || !usum || !gconv) return fail(FA_E_NOMEM, "workspace too small for score_block");
   int rc = ensure_lanes(c, lanes);
   if (rc) return rc;
@@ -1111,38 +1117,36 @@ static int mac_giant_phase(fa_ctx* c, const double* q, const double* qrot, const
     for (int blk = 0; blk < nb; ++blk)
       HIPCHK(hipMemcpyAsync(out + (size_t)blk * ctw, acc + (size_t)blk * ctw, ctw * 8, hipMemcpyDeviceToDevice, s));
   } else {
-    const int gl = std::min(lanes, G - 1);
-    if ((rc = fork_lanes(c, s, gl))) return rc;
+    std::vector<const double*> keys(G - 1);
+    std::vector<uint32_t> ggal(G - 1);
     for (int g = 1; g < G; ++g) {
-      const int lane = (g - 1) % gl;
-      hipStream_t ls = lane_stream(c, s, lane);
-      const double* accg = acc + (size_t)g * ctw;
-      double* gyl = gy + lane * gy_l;
-      double* gextl = gext + lane * gext_l;
-      double* usl = usum + lane * us_l;
-      modup(c, accg, astride, nb, gyl, L * n, gextl, dn * np * n, ls);
-      std::vector<fa::KsItem> ks(nb);
-      const uint32_t gal = galois(c->n, g * B);
-      for (int blk = 0; blk < nb; ++blk) {
-        const double* a = accg + (size_t)blk * astride;
-        ks[blk] = {gextl + (size_t)blk * dn * np * n, a + L * n, c->keys[g * B], usl + (size_t)blk * 2 * np * n, a,
-                   gal};
+      keys[g - 1] = c->keys[g * B];
+      ggal[g - 1] = galois(c->n, g * B);
+    }
+    for (int b0 = 0; b0 < nb; b0 += cbm) {
+      const int cb = std::min(cbm, nb - b0);
+      const double* accb = acc + (size_t)b0 * astride;
+      const int gl = std::min(lanes, G - 1);
+      if ((rc = fork_lanes(c, s, gl))) return rc;
+      for (int g = 1; g < G; ++g) {
+        const int lane = (g - 1) % gl;
+        modup(c, accb + (size_t)g * ctw, astride, cb, gy + lane * gy_l, L * n, gext + (size_t)(g - 1) * ext_w,
+              (size_t)(G - 1) * ext_w, lane_stream(c, s, lane), false);
       }
-      fa::ks_inner(c, ks.data(), nb, g > lane + 1, ls);
+      if ((rc = join_lanes(c, s, gl))) return rc;
+      fa::giant_ks(c, gext, accb, astride, keys.data(), ggal.data(), cb, G - 1, usum, s);
+      std::vector<const double*> bases(2 * cb);
+      std::vector<double*> douts(2 * cb);
+      std::vector<uint32_t> gals(2 * cb, 1u);
+      for (int blk = 0; blk < cb; ++blk) {
+        const double* acc0 = accb + (size_t)blk * astride;
+        bases[2 * blk] = acc0;
+        bases[2 * blk + 1] = acc0 + L * n;
+        douts[2 * blk] = out + (size_t)(b0 + blk) * ctw;
+        douts[2 * blk + 1] = out + (size_t)(b0 + blk) * ctw + L * n;
+      }
+      moddown_polys(c, usum, 2 * cb, gconv, bases.data(), douts.data(), gals.data(), s);
     }
-    if ((rc = join_lanes(c, s, gl))) return rc;
-    for (int lane = 1; lane < gl; ++lane) fa::add_limbs(c, usum, usum + lane * us_l, nb * 2 * (int)np, (int)np, s);
-    std::vector<const double*> bases(2 * nb);
-    std::vector<double*> douts(2 * nb);
-    std::vector<uint32_t> gals(2 * nb, 1u);
-    for (int blk = 0; blk < nb; ++blk) {
-      const double* acc0 = acc + (size_t)blk * astride;
-      bases[2 * blk] = acc0;
-      bases[2 * blk + 1] = acc0 + L * n;
-      douts[2 * blk] = out + (size_t)blk * ctw;
-      douts[2 * blk + 1] = out + (size_t)blk * ctw + L * n;
-    }
-    moddown_polys(c, usum, 2 * nb, gconv, bases.data(), douts.data(), gals.data(), s);
   }
   if (c->prof) {
     HIPCHK(hipEventRecord(c->ev[3], s));

@@ -98,7 +98,8 @@ struct MuItem {
   const double* y;  // [L][N]
   double* ext;      // [dnum][np][N]
 };
-void modup_ntt(const fa_ctx* c, const MuItem* items, int count, hipStream_t s);
+// pass_b false: only the first forward pass (the giant-step kernel finishes it)
+void modup_ntt(const fa_ctx* c, const MuItem* items, int count, hipStream_t s, bool pass_b = true);
 
 // ModDown with its finish: out = base[pi_gal] + (uQ - NTT(Conv_{P->Q}(yP))) * P^-1,
 // where yP ([K][N]) holds the special-prime coefficients of the key-switch
@@ -125,6 +126,12 @@ struct KsItem {
   uint32_t gal;       // Galois element
 };
 void ks_inner(const fa_ctx* c, const KsItem* items, int count, bool accumulate, hipStream_t s);
+
+// Fused giant steps of nb blocks: u[blk] = sum_{g=1..ng} sum_i sigma_g(NTT(ext)_i) key_g[i]
+// + P sigma_g(acc_g.c0), with ext = [nb][ng][dnum][np][N] holding only the first
+// forward pass of the extended digits of acc_g.c1 (acc_g = acc + blk*astride + g*2LN).
+void giant_ks(const fa_ctx* c, const double* ext, const double* acc, size_t astride, const double* const* keys,
+              const uint32_t* gals, int nb, int ng, double* u, hipStream_t s);
 
 
 // acc[blk][g][2][L][N] = sum_b pts[blk][(g*B+b)][L][N] * rot_b[2][L][N]

@@ -316,13 +316,11 @@ struct FinishSt {
   }
 };
 
-template <class St>
-__device__ __forceinline__ void fwd_b_body(double* a, const St& st, const double* __restrict__ T,
-                                           const double* __restrict__ F, double q, double qinv, int logn,
-                                           double* sm) {
-  const int n = 1 << logn;
-  const int rows = (n >> 8) < 16 ? (n >> 8) : 16;
-  const int row0 = blockIdx.x * rows;
+// The eight stages of pass B over `rows` rows row0.. of a; the results are
+// left in LDS (lds_row layout) and the block is synchronised on return.
+__device__ __forceinline__ void fwd_b_lds(const double* __restrict__ a, int row0, int rows,
+                                          const double* __restrict__ T, const double* __restrict__ F, double q,
+                                          double qinv, double* sm) {
   for (int u = threadIdx.x; u < rows * 16; u += 256) {
     const int l0 = u & 15, rl = u >> 4, r = row0 + rl;
     double x[16];
@@ -357,12 +355,22 @@ __device__ __forceinline__ void fwd_b_body(double* a, const St& st, const double
         ct_bfly(x[m], x[m + half], twb(T, f, s1, (lh << (s1 - 4)) + (m >> (8 - s1)), q, qinv), q, qinv);
       }
     }
-    // back to LDS (each thread rewrites the words it read) ...
+    // back to LDS: each thread rewrites the words it read
 #pragma unroll
     for (int m = 0; m < 16; ++m) sm[lds_row(rl, 16 * lh + m)] = x[m];
   }
   __syncthreads();
-  // ... and out with consecutive threads on consecutive words
+}
+
+template <class St>
+__device__ __forceinline__ void fwd_b_body(double* a, const St& st, const double* __restrict__ T,
+                                           const double* __restrict__ F, double q, double qinv, int logn,
+                                           double* sm) {
+  const int n = 1 << logn;
+  const int rows = (n >> 8) < 16 ? (n >> 8) : 16;
+  const int row0 = blockIdx.x * rows;
+  fwd_b_lds(a, row0, rows, T, F, q, qinv, sm);
+  // out with consecutive threads on consecutive words
   for (int e = threadIdx.x; e < rows * 256; e += 256) st((size_t)row0 * 256 + e, sm[lds_row(e >> 8, e & 255)]);
 }
 
@@ -492,6 +500,114 @@ __global__ __launch_bounds__(256) void k_ks_inner(KsArgs args, const DevPrime* _
   }
   *u0 = canon_full(acc0, q, qinv);
   *u1 = canon_full(acc1, q, qinv);
+}
+
+// ---------------------------------------------------------------------------
+// Giant steps of the diagonal scoring, fused: for every block and every
+// ciphertext/special prime t,
+//   u[blk] = sum_{g=1}^{G-1} ( sum_i sigma_g(ext[blk][g]_i) * key_g[i]  +  P * sigma_g(acc_g.c0) )
+// where ext holds the first forward pass only of the extended digits of
+// acc_g.c1.  A workgroup owns one tile of rows*256 output words of one prime:
+// for each (g, digit) it runs the last eight NTT stages on the source tile
+// (the automorphism maps an aligned tile onto an aligned tile) in LDS, then
+// gathers through the permutation and multiplies by the key, so the digits in
+// NTT form never reach HBM.  The digit's own limbs come from acc_g.c1 itself.
+// Workgroup ids are decoded so that the nb blocks of one (tile, prime) land on
+// the same XCD one after the other and share the key rows in its L2.
+// ---------------------------------------------------------------------------
+#define FA_MAXG 32
+struct GiantArgs {
+  const double* ext;  // [nb][ng][dnum][np][N], first pass only
+  const double* acc;  // acc of block blk, giant g: acc + blk * astride + g * 2 L N
+  const double* key[FA_MAXG];
+  uint32_t gal[FA_MAXG];
+  double* u;          // [nb][2][np][N]
+  size_t astride;
+  int nb, ng, ngs, g0, accumulate;  // ng giants in this launch; ngs: the giant stride of ext
+};
+
+template <int DNUM, int ROWS>
+__global__ __launch_bounds__(256) void k_giant_ks(GiantArgs a, const DevPrime* __restrict__ pr,
+                                                  const double* __restrict__ twt, const double* __restrict__ twr,
+                                                  int logn, int L, int np, int alpha, int ntile) {
+  __shared__ double sm[ROWS * ROWW];
+  const unsigned W = blockIdx.x;
+  const unsigned j8 = W >> 3;
+  const int blk = (int)(j8 % (unsigned)a.nb);
+  const unsigned rest = (j8 / (unsigned)a.nb) * 8u + (W & 7u);
+  if (rest >= (unsigned)(ntile * np)) return;
+  const int t = (int)(rest / (unsigned)ntile), tile = (int)(rest % (unsigned)ntile);
+  const int n = 1 << logn;
+  constexpr uint32_t TW = ROWS * 256u;  // words of a tile; ROWS words per thread
+  const uint32_t k0 = (uint32_t)tile * TW;
+  const double q = pr[t].q, qinv = pr[t].qinv;
+  const double* __restrict__ T = twt + (size_t)t * 256;
+  const double* __restrict__ F = twr + (size_t)t * (n >> 8) * 8;
+  const int own = t < L ? t / alpha : -1;
+  const size_t ln = (size_t)L * n;
+  double acc0[ROWS], acc1[ROWS];
+#pragma unroll
+  for (int j = 0; j < ROWS; ++j) acc0[j] = acc1[j] = 0.0;
+#pragma unroll 1
+  for (int g = 0; g < a.ng; ++g) {
+    const uint32_t gal = a.gal[g];
+    const uint32_t sbase = perm(k0, gal, logn) & ~(TW - 1u);
+    const double* __restrict__ accg = a.acc + (size_t)blk * a.astride + (size_t)(a.g0 + g) * 2 * ln;
+    const double* __restrict__ key = a.key[g];
+#pragma unroll 1
+    for (int i = 0; i < DNUM; ++i) {
+      // opaque copies: recomputing the permutation per digit is cheaper than
+      // keeping it (and the twiddle loads) live across the loop
+      uint32_t galv = gal;
+      const double* Tv = T;
+      asm volatile("" : "+s"(galv), "+s"(Tv));
+      const double* __restrict__ kb = key + (((size_t)i * 2 + 0) * np + t) * n + k0 + threadIdx.x;
+      const double* __restrict__ ka = key + (((size_t)i * 2 + 1) * np + t) * n + k0 + threadIdx.x;
+      double x[ROWS];
+      if (i == own) {
+        const double* __restrict__ c1 = accg + ln + (size_t)t * n;
+#pragma unroll
+        for (int j = 0; j < ROWS; ++j) x[j] = c1[perm(k0 + threadIdx.x + 256u * j, galv, logn)];
+      } else {
+        const double* src = a.ext + ((((size_t)blk * a.ngs + g) * DNUM + i) * np + t) * n;
+        fwd_b_lds(src, (int)(sbase >> 8), ROWS, Tv, F, q, qinv, sm);
+#pragma unroll
+        for (int j = 0; j < ROWS; ++j) {
+          const uint32_t sk = perm(k0 + threadIdx.x + 256u * j, galv, logn) - sbase;
+          x[j] = sm[lds_row((int)(sk >> 8), (int)(sk & 255u))];
+        }
+        __syncthreads();  // the next digit's pass reuses the LDS tile
+      }
+#pragma unroll
+      for (int j = 0; j < ROWS; ++j) {
+        acc0[j] += mul(x[j], kb[256 * j], q, qinv);
+        acc1[j] += mul(x[j], ka[256 * j], q, qinv);
+      }
+    }
+    if (t < L) {
+      const double* __restrict__ c0 = accg + (size_t)t * n;
+      const double pm = pr[t].pmod;
+#pragma unroll
+      for (int j = 0; j < ROWS; ++j) acc0[j] += mul(c0[perm(k0 + threadIdx.x + 256u * j, gal, logn)], pm, q, qinv);
+    }
+#pragma unroll
+    for (int j = 0; j < ROWS; ++j) {
+      acc0[j] = reduce(acc0[j], q, qinv);
+      acc1[j] = reduce(acc1[j], q, qinv);
+    }
+  }
+  double* u0 = a.u + ((size_t)blk * 2 * np + t) * n + k0 + threadIdx.x;
+  double* u1 = u0 + (size_t)np * n;
+#pragma unroll
+  for (int j = 0; j < ROWS; ++j) {
+    double r0 = acc0[j], r1 = acc1[j];
+    if (a.accumulate) {
+      r0 += u0[256 * j];
+      r1 += u1[256 * j];
+    }
+    u0[256 * j] = canon_full(r0, q, qinv);
+    u1[256 * j] = canon_full(r1, q, qinv);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -756,13 +872,14 @@ static void launch_modup_a_sa(const fa_ctx* c, const MuArgs& a, int count, hipSt
   }
 }
 
-void modup_ntt(const fa_ctx* c, const MuItem* items, int count, hipStream_t s) {
+void modup_ntt(const fa_ctx* c, const MuItem* items, int count, hipStream_t s, bool pass_b) {
   for (int off = 0; off < count; off += FA_MAXMU) {
     const int m = count - off < FA_MAXMU ? count - off : FA_MAXMU;
     MuArgs a;
     for (int i = 0; i < m; ++i) a.it[i] = items[off + i];
     FA_SA_SWITCH(launch_modup_a_sa, c, a, m, s)
   }
+  if (!pass_b) return;
   // second pass over every converted limb
   LimbList l;
   l.n = 0;
@@ -840,6 +957,57 @@ void ks_inner(const fa_ctx* c, const KsItem* items, int count, bool accumulate, 
       case 6: launch_ks<6>(c, a, m, accumulate, s); break;
       case 7: launch_ks<7>(c, a, m, accumulate, s); break;
       case 8: launch_ks<8>(c, a, m, accumulate, s); break;
+      default: break;
+    }
+  }
+}
+
+template <int DNUM>
+static void launch_giant(const fa_ctx* c, const GiantArgs& a, hipStream_t s) {
+  const int rows = (c->n >> 8) < 16 ? (c->n >> 8) : 16;
+  const int ntile = (c->n >> 8) / rows;
+  const int rest8 = (ntile * c->np + 7) / 8;
+  dim3 g((unsigned)(8 * a.nb * rest8));
+  if (rows == 16)
+    hipLaunchKernelGGL((k_giant_ks<DNUM, 16>), g, dim3(256), 0, s, a, c->d_pr, c->d_twt_fwd, c->d_twr_fwd, c->logn,
+                       c->L, c->np, c->alpha, ntile);
+  else if (rows == 8)
+    hipLaunchKernelGGL((k_giant_ks<DNUM, 8>), g, dim3(256), 0, s, a, c->d_pr, c->d_twt_fwd, c->d_twr_fwd, c->logn,
+                       c->L, c->np, c->alpha, ntile);
+  else
+    hipLaunchKernelGGL((k_giant_ks<DNUM, 4>), g, dim3(256), 0, s, a, c->d_pr, c->d_twt_fwd, c->d_twr_fwd, c->logn,
+                       c->L, c->np, c->alpha, ntile);
+}
+
+void giant_ks(const fa_ctx* c, const double* ext, const double* acc, size_t astride, const double* const* keys,
+              const uint32_t* gals, int nb, int ng, double* u, hipStream_t s) {
+  const size_t ext_g = (size_t)c->dnum * c->np * c->n;
+  for (int g0 = 0; g0 < ng; g0 += FA_MAXG) {
+    GiantArgs a;
+    const int m = ng - g0 < FA_MAXG ? ng - g0 : FA_MAXG;
+    // chunks of giant indices: ext of chunk g0 is [nb][m] laid out inside [nb][ng]
+    a.ext = ext + (size_t)g0 * ext_g;
+    a.acc = acc;
+    for (int g = 0; g < m; ++g) {
+      a.key[g] = keys[g0 + g];
+      a.gal[g] = gals[g0 + g];
+    }
+    a.u = u;
+    a.astride = astride;
+    a.nb = nb;
+    a.ng = m;
+    a.ngs = ng;
+    a.g0 = 1 + g0;
+    a.accumulate = g0 > 0;
+    switch (c->dnum) {
+      case 1: launch_giant<1>(c, a, s); break;
+      case 2: launch_giant<2>(c, a, s); break;
+      case 3: launch_giant<3>(c, a, s); break;
+      case 4: launch_giant<4>(c, a, s); break;
+      case 5: launch_giant<5>(c, a, s); break;
+      case 6: launch_giant<6>(c, a, s); break;
+      case 7: launch_giant<7>(c, a, s); break;
+      case 8: launch_giant<8>(c, a, s); break;
       default: break;
     }
   }
