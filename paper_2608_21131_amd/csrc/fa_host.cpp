@@ -938,8 +938,10 @@ static void modup(fa_ctx* c, const double* cts, size_t ct_stride, int batch, dou
 // ModDown of `count` polynomials u_i = u + i * np * N over Q u P (NTT form):
 // out_i = bases_i[pi_gal_i] + (u_i,Q - Conv_{P->Q}(u_i,P)) * P^-1.  The special-
 // prime limbs of u are overwritten (scaled coefficients); conv is scratch.
+// With pass_b false only the special-prime inverse and the conversion's first
+// pass run (bases, outs and gals unused): moddown_ks finishes.
 static void moddown_polys(fa_ctx* c, double* u, int count, double* conv, const double* const* bases,
-                          double* const* outs, const uint32_t* gals, hipStream_t s) {
+                          double* const* outs, const uint32_t* gals, hipStream_t s, bool pass_b = true) {
   const size_t n = c->n, L = c->L, np = c->np;
   {
     fa::LimbBatch inv(c, s, false);
@@ -950,9 +952,25 @@ static void moddown_polys(fa_ctx* c, double* u, int count, double* conv, const d
   std::vector<fa::MdItem> it(count);
   for (int i = 0; i < count; ++i) {
     double* ui = u + (size_t)i * np * n;
-    it[i] = {ui + L * n, conv + (size_t)i * L * n, ui, bases[i], outs[i], gals[i]};
+    it[i] = {ui + L * n, conv + (size_t)i * L * n, ui, pass_b ? bases[i] : nullptr, pass_b ? outs[i] : nullptr,
+             pass_b ? gals[i] : 1u};
   }
-  fa::moddown(c, it.data(), count, s);
+  fa::moddown(c, it.data(), count, s, pass_b);
+}
+
+// Key switch and ModDown of `count` rotations: outs[j] = (c0s[j][pi] + ModDown(u_0),
+// ModDown(u_1)) with u = sum_i sigma(ext_i) key_i.  The special-prime part of u
+// goes through u (per rotation [2][np][N]); the ciphertext-prime part is formed
+// inside the finishing kernel.  conv: per rotation [2][L][N] scratch.
+static void ks_moddown(fa_ctx* c, const fa::KsItem* ks, int count, const double* const* c0s, double* const* outs,
+                       double* u, double* conv, hipStream_t s) {
+  const size_t n = c->n, L = c->L;
+  fa::ks_inner(c, ks, count, false, s, c->L);
+  moddown_polys(c, u, 2 * count, conv, nullptr, nullptr, nullptr, s, false);
+  std::vector<fa::MdKsItem> it(count);
+  for (int j = 0; j < count; ++j)
+    it[j] = {conv + (size_t)2 * j * L * n, ks[j].ext, ks[j].c1, ks[j].key, c0s[j], outs[j], ks[j].gal};
+  fa::moddown_ks(c, it.data(), count, s);
 }
 
 // Auxiliary streams for `lanes` lanes (lane 0 is the caller's stream).
@@ -997,22 +1015,15 @@ static int rotations_from_ext(fa_ctx* c, const double* q, const double* ext, con
     double* ul = u + lane * u_lane;
     double* cl = conv + lane * c_lane;
     fa::KsItem ks[kRotBatch];
-    const double* bases[2 * kRotBatch];
-    double* douts[2 * kRotBatch];
-    uint32_t gals[2 * kRotBatch];
+    const double* c0s[kRotBatch];
     for (int j = 0; j < rb; ++j) {
       auto it = c->keys.find(steps[r0 + j]);
       if (it == c->keys.end()) return fail(FA_E_NOKEY, "no rotation key for step %d", steps[r0 + j]);
       const uint32_t gal = galois(c->n, steps[r0 + j]);
       ks[j] = {ext, q + L * n, it->second, ul + (size_t)j * 2 * np * n, nullptr, gal};
-      bases[2 * j] = q;
-      bases[2 * j + 1] = nullptr;
-      douts[2 * j] = outs[r0 + j];
-      douts[2 * j + 1] = outs[r0 + j] + L * n;
-      gals[2 * j] = gals[2 * j + 1] = gal;
+      c0s[j] = q;
     }
-    fa::ks_inner(c, ks, rb, false, ls);
-    moddown_polys(c, ul, 2 * rb, cl, bases, douts, gals, ls);
+    ks_moddown(c, ks, rb, c0s, outs + r0, ul, cl, ls);
   }
   return check_launch("rotation");
 }
@@ -1031,19 +1042,16 @@ static int rotate_batch(fa_ctx* c, const double* cts, int nb, int step, double* 
   const size_t ctw = 2 * L * n;
   modup(c, cts, ctw, nb, y, L * n, ext, dn * np * n, s);
   std::vector<fa::KsItem> ks(nb);
-  std::vector<const double*> bases(2 * nb);
-  std::vector<double*> douts(2 * nb);
-  std::vector<uint32_t> gals(2 * nb, galois(c->n, step));
+  std::vector<const double*> c0s(nb);
+  std::vector<double*> douts(nb);
+  const uint32_t gal = galois(c->n, step);
   for (int b = 0; b < nb; ++b) {
     const double* ct = cts + (size_t)b * ctw;
-    ks[b] = {ext + (size_t)b * dn * np * n, ct + L * n, it->second, u + (size_t)b * 2 * np * n, nullptr, gals[0]};
-    bases[2 * b] = ct;
-    bases[2 * b + 1] = nullptr;
-    douts[2 * b] = outs + (size_t)b * ctw;
-    douts[2 * b + 1] = outs + (size_t)b * ctw + L * n;
+    ks[b] = {ext + (size_t)b * dn * np * n, ct + L * n, it->second, u + (size_t)b * 2 * np * n, nullptr, gal};
+    c0s[b] = ct;
+    douts[b] = outs + (size_t)b * ctw;
   }
-  fa::ks_inner(c, ks.data(), nb, false, s);
-  moddown_polys(c, u, 2 * nb, conv, bases.data(), douts.data(), gals.data(), s);
+  ks_moddown(c, ks.data(), nb, c0s.data(), douts.data(), u, conv, s);
   ar.used = mark;
   return check_launch("rotate_batch");
 }

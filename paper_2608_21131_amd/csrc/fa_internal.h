@@ -113,7 +113,24 @@ struct MdItem {
   double* out;         // [L][N]
   uint32_t gal;        // permutation of base (1 = none)
 };
-void moddown(const fa_ctx* c, const MdItem* items, int count, hipStream_t s);
+// pass_b false: conversion and first forward pass only (conv is left for moddown_ks)
+void moddown(const fa_ctx* c, const MdItem* items, int count, hipStream_t s, bool pass_b = true);
+
+// ModDown finish of rotations whose key-switch sum on the ciphertext primes is
+// formed in the same kernel (ks_inner then only covers the special primes):
+// out = (sigma(c0) + (u_Q,0 - conv0^) P^-1, (u_Q,1 - conv1^) P^-1) with
+// u_Q,h = sum_i sigma(ext_i) key[i][h] and conv (from moddown with pass_b false)
+// holding the first pass of Conv_{P->Q} of both polynomials.
+struct MdKsItem {
+  const double* conv;  // [2][L][N]
+  const double* ext;   // [dnum][np][N]
+  const double* c1;    // [L][N] the digits' own limbs
+  const double* key;   // [dnum][2][np][N]
+  const double* c0;    // [L][N]
+  double* out;         // [2][L][N]
+  uint32_t gal;
+};
+void moddown_ks(const fa_ctx* c, const MdKsItem* items, int count, hipStream_t s);
 
 // Key-switch inner product with the automorphism folded in:
 // u[j] (+)= sum_i sigma_{g_j}(ext[j or 0]_i) * key_j[i]  over all np primes.
@@ -125,7 +142,8 @@ struct KsItem {
   const double* c0;   // [L][N] or null: adds P * sigma(c0) to u0 on the ciphertext primes
   uint32_t gal;       // Galois element
 };
-void ks_inner(const fa_ctx* c, const KsItem* items, int count, bool accumulate, hipStream_t s);
+// t0 > 0: only primes t0..np-1 (the special primes when t0 = L)
+void ks_inner(const fa_ctx* c, const KsItem* items, int count, bool accumulate, hipStream_t s, int t0 = 0);
 
 // Fused giant steps of nb blocks: u[blk] = sum_{g=1..ng} sum_i sigma_g(NTT(ext)_i) key_g[i]
 // + P sigma_g(acc_g.c0), with ext = [nb][ng][dnum][np][N] holding only the first

@@ -399,6 +399,68 @@ __global__ __launch_bounds__(256) void k_moddown_b(MdArgs args, const DevPrime* 
   fwd_b_body(it.conv + o, st, twt + (size_t)t * 256, twr + (size_t)t * H * 8, q, qinv, logn, sm);
 }
 
+// ModDown finish of a rotation with its key-switch sum on the ciphertext
+// primes formed in place: for limb t < L and the tile's words k,
+//   u_h[k] = sum_i sigma(ext_i)[k] * key_i[h][t][k]   (h = 0, 1; own limbs from c1)
+//   out0[k] = c0[pi(k)] + (u_0[k] - conv0^[k]) * P^-1,  out1[k] = (u_1[k] - conv1^[k]) * P^-1
+// where conv_h^ is the forward transform of Conv_{P->Q} finished here (pass B).
+// The sums never reach HBM; both polynomials of the rotation share one gather.
+struct MdKsArgs {
+  fa::MdKsItem it[FA_MAXMD];
+};
+
+template <int DNUM, int ROWS>
+__global__ __launch_bounds__(256) void k_moddown_ks_b(MdKsArgs args, const DevPrime* __restrict__ pr,
+                                                      const double* __restrict__ twt, const double* __restrict__ twr,
+                                                      int logn, int L, int np, int alpha) {
+  __shared__ double sm[ROWS * ROWW];
+  const int t = blockIdx.y;
+  const fa::MdKsItem& it = args.it[blockIdx.z];
+  const int n = 1 << logn;
+  const int row0 = blockIdx.x * ROWS;
+  const uint32_t k0 = (uint32_t)row0 * 256u + threadIdx.x;  // this thread's words: k0 + 256 j, j < ROWS
+  const double q = pr[t].q, qinv = pr[t].qinv, pv = pr[t].pinv, pvp = pv * qinv;
+  const int own = t / alpha;
+  const double* __restrict__ T = twt + (size_t)t * 256;
+  const double* __restrict__ F = twr + (size_t)t * (n >> 8) * 8;
+  const size_t o = (size_t)t * n;
+  double u0[ROWS], u1[ROWS];
+#pragma unroll
+  for (int j = 0; j < ROWS; ++j) u0[j] = u1[j] = 0.0;
+#pragma unroll 1
+  for (int i = 0; i < DNUM; ++i) {
+    const double* __restrict__ src = i == own ? it.c1 + o : it.ext + ((size_t)i * np + t) * n;
+    const double* __restrict__ kb = it.key + (((size_t)i * 2 + 0) * np + t) * n + k0;
+    const double* __restrict__ ka = it.key + (((size_t)i * 2 + 1) * np + t) * n + k0;
+#pragma unroll
+    for (int j = 0; j < ROWS; ++j) {
+      const double x = src[perm(k0 + 256u * j, it.gal, logn)];
+      u0[j] += mul(x, kb[256 * j], q, qinv);
+      u1[j] += mul(x, ka[256 * j], q, qinv);
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < ROWS; ++j) {
+    u0[j] = reduce(u0[j], q, qinv);
+    u1[j] = reduce(u1[j], q, qinv);
+  }
+  fwd_b_lds(it.conv + o, row0, ROWS, T, F, q, qinv, sm);
+#pragma unroll
+  for (int j = 0; j < ROWS; ++j) {
+    const int e = threadIdx.x + 256 * j;
+    const double r = mulc(u0[j] - sm[lds_row(e >> 8, e & 255)], pv, pvp, q) + it.c0[o + perm(k0 + 256u * j, it.gal, logn)];
+    it.out[o + k0 + 256 * j] = canon_full(r, q, qinv);
+  }
+  __syncthreads();
+  fwd_b_lds(it.conv + (size_t)L * n + o, row0, ROWS, T, F, q, qinv, sm);
+#pragma unroll
+  for (int j = 0; j < ROWS; ++j) {
+    const int e = threadIdx.x + 256 * j;
+    const double r = mulc(u1[j] - sm[lds_row(e >> 8, e & 255)], pv, pvp, q);
+    it.out[(size_t)L * n + o + k0 + 256 * j] = canon_full(r, q, qinv);
+  }
+}
+
 // inverse pass B (the first pass of the inverse transform), src -> ptr
 __global__ __launch_bounds__(256) void k_ntt_inv_b(LimbList ll, const DevPrime* __restrict__ pr,
                                                    const double* __restrict__ twt, const double* __restrict__ twr,
@@ -467,10 +529,10 @@ struct KsArgs {
 
 template <int DNUM>
 __global__ __launch_bounds__(256) void k_ks_inner(KsArgs args, const DevPrime* __restrict__ pr, int logn, int L,
-                                                  int np, int alpha, int accumulate) {
+                                                  int np, int alpha, int accumulate, int t0) {
   const int n = 1 << logn;
   const int k = blockIdx.x * 256 + threadIdx.x;
-  const int t = blockIdx.y;
+  const int t = t0 + blockIdx.y;
   const fa::KsItem& it = args.it[blockIdx.z];
   const double q = pr[t].q, qinv = pr[t].qinv;
   const uint32_t kk = perm((uint32_t)k, it.gal, logn);
@@ -924,39 +986,74 @@ static void launch_moddown_a_sa(const fa_ctx* c, const MdArgs& a, int count, hip
   }
 }
 
-void moddown(const fa_ctx* c, const MdItem* items, int count, hipStream_t s) {
+void moddown(const fa_ctx* c, const MdItem* items, int count, hipStream_t s, bool pass_b) {
   const int rows = (c->n >> 8) < 16 ? (c->n >> 8) : 16;
   for (int off = 0; off < count; off += FA_MAXMD) {
     const int m = count - off < FA_MAXMD ? count - off : FA_MAXMD;
     MdArgs a;
     for (int i = 0; i < m; ++i) a.it[i] = items[off + i];
     FA_SA_SWITCH(launch_moddown_a_sa, c, a, m, s)
+    if (!pass_b) continue;
     dim3 gb((c->n >> 8) / rows, c->L, m);
     hipLaunchKernelGGL(k_moddown_b, gb, dim3(256), 0, s, a, c->d_pr, c->d_twt_fwd, c->d_twr_fwd, c->logn);
   }
 }
 
 template <int DNUM>
-static void launch_ks(const fa_ctx* c, const KsArgs& a, int m, bool accumulate, hipStream_t s) {
-  dim3 g(c->n / 256, c->np, m);
-  hipLaunchKernelGGL(k_ks_inner<DNUM>, g, dim3(256), 0, s, a, c->d_pr, c->logn, c->L, c->np, c->alpha,
-                     accumulate ? 1 : 0);
+static void launch_moddown_ks(const fa_ctx* c, const MdKsArgs& a, int m, hipStream_t s) {
+  const int rows = (c->n >> 8) < 16 ? (c->n >> 8) : 16;
+  dim3 gb((c->n >> 8) / rows, c->L, m);
+  if (rows == 16)
+    hipLaunchKernelGGL((k_moddown_ks_b<DNUM, 16>), gb, dim3(256), 0, s, a, c->d_pr, c->d_twt_fwd, c->d_twr_fwd,
+                       c->logn, c->L, c->np, c->alpha);
+  else if (rows == 8)
+    hipLaunchKernelGGL((k_moddown_ks_b<DNUM, 8>), gb, dim3(256), 0, s, a, c->d_pr, c->d_twt_fwd, c->d_twr_fwd,
+                       c->logn, c->L, c->np, c->alpha);
+  else
+    hipLaunchKernelGGL((k_moddown_ks_b<DNUM, 4>), gb, dim3(256), 0, s, a, c->d_pr, c->d_twt_fwd, c->d_twr_fwd,
+                       c->logn, c->L, c->np, c->alpha);
 }
 
-void ks_inner(const fa_ctx* c, const KsItem* items, int count, bool accumulate, hipStream_t s) {
+void moddown_ks(const fa_ctx* c, const MdKsItem* items, int count, hipStream_t s) {
+  for (int off = 0; off < count; off += FA_MAXMD) {
+    const int m = count - off < FA_MAXMD ? count - off : FA_MAXMD;
+    MdKsArgs a;
+    for (int i = 0; i < m; ++i) a.it[i] = items[off + i];
+    switch (c->dnum) {
+      case 1: launch_moddown_ks<1>(c, a, m, s); break;
+      case 2: launch_moddown_ks<2>(c, a, m, s); break;
+      case 3: launch_moddown_ks<3>(c, a, m, s); break;
+      case 4: launch_moddown_ks<4>(c, a, m, s); break;
+      case 5: launch_moddown_ks<5>(c, a, m, s); break;
+      case 6: launch_moddown_ks<6>(c, a, m, s); break;
+      case 7: launch_moddown_ks<7>(c, a, m, s); break;
+      case 8: launch_moddown_ks<8>(c, a, m, s); break;
+      default: break;
+    }
+  }
+}
+
+template <int DNUM>
+static void launch_ks(const fa_ctx* c, const KsArgs& a, int m, bool accumulate, hipStream_t s, int t0) {
+  dim3 g(c->n / 256, c->np - t0, m);
+  hipLaunchKernelGGL(k_ks_inner<DNUM>, g, dim3(256), 0, s, a, c->d_pr, c->logn, c->L, c->np, c->alpha,
+                     accumulate ? 1 : 0, t0);
+}
+
+void ks_inner(const fa_ctx* c, const KsItem* items, int count, bool accumulate, hipStream_t s, int t0) {
   for (int off = 0; off < count; off += FA_MAXKS) {
     KsArgs a;
     const int m = count - off < FA_MAXKS ? count - off : FA_MAXKS;
     for (int i = 0; i < m; ++i) a.it[i] = items[off + i];
     switch (c->dnum) {
-      case 1: launch_ks<1>(c, a, m, accumulate, s); break;
-      case 2: launch_ks<2>(c, a, m, accumulate, s); break;
-      case 3: launch_ks<3>(c, a, m, accumulate, s); break;
-      case 4: launch_ks<4>(c, a, m, accumulate, s); break;
-      case 5: launch_ks<5>(c, a, m, accumulate, s); break;
-      case 6: launch_ks<6>(c, a, m, accumulate, s); break;
-      case 7: launch_ks<7>(c, a, m, accumulate, s); break;
-      case 8: launch_ks<8>(c, a, m, accumulate, s); break;
+      case 1: launch_ks<1>(c, a, m, accumulate, s, t0); break;
+      case 2: launch_ks<2>(c, a, m, accumulate, s, t0); break;
+      case 3: launch_ks<3>(c, a, m, accumulate, s, t0); break;
+      case 4: launch_ks<4>(c, a, m, accumulate, s, t0); break;
+      case 5: launch_ks<5>(c, a, m, accumulate, s, t0); break;
+      case 6: launch_ks<6>(c, a, m, accumulate, s, t0); break;
+      case 7: launch_ks<7>(c, a, m, accumulate, s, t0); break;
+      case 8: launch_ks<8>(c, a, m, accumulate, s, t0); break;
       default: break;
     }
   }
