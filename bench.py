@@ -51,6 +51,10 @@ def parse():
     ap.add_argument("--also-level", type=int, default=3,
                     help="rerank: also time the level with the query dropped to this many primes and report it "
                          "under level_drop (0: skip)")
+    ap.add_argument("--batch", type=int, default=4,
+                    help="rerank: also time cross-query batching (this many queries per plaintext pass, each "
+                         "prepared once, all scored against the same blocks) and report it under query_batch "
+                         "(0: skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-check", action="store_true", help="skip the decrypt-and-compare check")
     ap.add_argument("--copy-calib", action="store_true",
@@ -158,7 +162,83 @@ def run_diag_level(bn, args):
     mac_bytes = 8 * (w.n_blocks * w.d * ptw + (w.B - 1) * 2 * ptw + 2 * ptw + w.n_blocks * w.G * 2 * ptw)
     stream_bytes = 8 * w.n_blocks * w.d * ptw
     return dict(ms=ms, scores=w.rows, phases=ph, err=err, mac_bytes=mac_bytes, stream_bytes=stream_bytes,
-                X=X, cpu=(lambda: cpu_baseline_diag(bn, X, qv)))
+                X=X, cpu=(lambda: cpu_baseline_diag(bn, X, qv)), ctx=ctx, blocks=blocks, centers=centers)
+
+
+def mac_batch_bytes(nq, n_pairs, B, ptw):
+    """Algorithmic bytes of the multiply-accumulate launches for nq queries, following the
+    launcher's grouping (4, then 2, then 1 queries per plaintext pass; the full chunks of a
+    group's pairs in one launch whose chunks share the rotated queries through L2, a narrower
+    launch for the rest): every plaintext once per group, each query's rotations once per
+    launch, the accumulators once."""
+    total, j = 0, 0
+    while j < nq:
+        m = 4 if nq - j >= 4 else 2 if nq - j >= 2 else 1
+        wide = 32 // m
+        p0 = launches = 0
+        while p0 < n_pairs:
+            left = n_pairs - p0
+            p0 += (left // wide) * wide if left >= wide else 16 if (wide > 16 and left > 8) else 8
+            launches += 1
+        total += n_pairs * B * ptw + launches * m * B * 2 * ptw + m * n_pairs * 2 * ptw
+        j += m
+    return 8 * total
+
+
+def run_batch_level(bn, args, r, nq):
+    """Cross-query batching on the level r was timed on (same context and resident blocks):
+    per step, nq fresh queries are (dropped and) prepared -- their baby rotations -- and then
+    scored together, every plaintext pass serving up to four of them."""
+    w, fa, torch = bn.w, bn.fa, bn.torch
+    top, ctx, blocks = bn.ctx, r["ctx"], r["blocks"]
+    X, S = r["X"], w.slots
+    qvs = bn.wl.query_vectors(w, nq + 1, r["centers"])[1:]
+    q_tops = [bn.encrypt(pad(v, w.d), tag=100 + j) for j, v in enumerate(qvs)]
+    qs = [ctx.new_ct() for _ in range(nq)] if ctx is not top else q_tops
+    preps = [torch.empty(int(ctx.lib.fa_prepared_words(ctx.h, w.B)), dtype=torch.float64, device="cuda")
+             for _ in range(nq)]
+    outs = [ctx.new_ct(w.n_blocks) for _ in range(nq)]
+    ws_p = ctx.workspace(fa.OP_PREPARE, 1, w.B, w.B)
+    ws_b = ctx.batch_workspace(nq, w.n_blocks, w.d, w.B)
+    stream = torch.cuda.current_stream()
+    marks, phases = [], []
+
+    def step():
+        e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+        e0.record(stream)
+        for j in range(nq):
+            if ctx is not top:
+                top.drop_level(ctx, q_tops[j], out=qs[j])
+            ctx.prepare_query(qs[j], w.B, out=preps[j], ws=ws_p)
+        e1.record(stream)
+        ctx.score_batch(qs, preps, blocks, w.d, w.B, outs=outs, ws=ws_b)
+        e2.record(stream)
+        marks.append((e0, e1, e2))
+        phases.append(ctx.profile_read())
+
+    ms = bn.timed(step, args.steps, args.warmup)
+    torch.cuda.synchronize()
+    prep_ms = float(np.mean([a.elapsed_time(b) for a, b, _ in marks[args.warmup:]]))
+    score_ms = float(np.mean([b.elapsed_time(c) for _, b, c in marks[args.warmup:]]))
+    mac_ms = float(np.mean([p["mac_ms"] for p in phases[args.warmup:]]))
+    giant_ms = float(np.mean([p["giant_ms"] for p in phases[args.warmup:]]))
+    err = None
+    if not args.no_check:
+        err = 0.0
+        W_ = ctx.ct_words
+        for j in range(nq):
+            for b in range(w.n_blocks):
+                rows = X[b * S:(b + 1) * S].astype(np.float64)
+                z = ctx.decode(ctx.decrypt(outs[j][b * W_:(b + 1) * W_]), 80)
+                err = max(err, float(np.max(np.abs(z[:len(rows)] - rows @ qvs[j]))))
+    ptw = ctx.L * w.n
+    mac_bytes = mac_batch_bytes(nq, w.n_blocks * w.G, w.B, ctx.L * w.n)
+    return {"queries": nq, "scoring_level_primes": ctx.L, "ms_per_step": round(ms, 4),
+            "ms_per_query_level": round(ms / nq, 4), "value": round(nq * w.rows / (ms * 1e-3), 1),
+            "unit": "scores/s", "phases_ms": {"prepare_ms": round(prep_ms, 4), "score_batch_ms": round(score_ms, 4),
+                                              "mac_ms": round(mac_ms, 4), "giant_ms": round(giant_ms, 4)},
+            "mac_achieved_GBs": round(mac_bytes / (mac_ms * 1e-3) / 1e9, 1), "mac_algorithmic_bytes": mac_bytes,
+            "max_abs_score_err": err}
 
 
 def run_tiny(bn, args):
@@ -349,12 +429,19 @@ def measured_traffic(path):
     mh = re.search(r"kernel_source_sha256: ([0-9a-f]+)", txt)
     if not mb or not mh:
         return None
-    src = open(os.path.join(ROOT, "paper_2608_21131_amd", "csrc", "fa_kernels.hip")).read()
-    a = src.index("template <int NACC>\n__global__ __launch_bounds__(256) void k_mac_diag(")
-    b = src.index("\n}\n", a) + 3
-    if hashlib.sha256(src[a:b].encode()).hexdigest() != mh.group(1):
+    if mac_source_sha256() != mh.group(1):
         return None
     return int(mb.group(1))
+
+
+def mac_source_sha256():
+    """sha256 of the multiply-accumulate kernel's source text (template line to closing brace)."""
+    import hashlib
+    src = open(os.path.join(ROOT, "paper_2608_21131_amd", "csrc", "fa_kernels.hip")).read()
+    a = src.index("void k_mac_diag(")
+    a = src.rindex("template <", 0, a)
+    b = src.index("\n}\n", a) + 3
+    return hashlib.sha256(src[a:b].encode()).hexdigest()
 
 
 def cpu_baseline_diag(bn, X, qv):
@@ -480,6 +567,11 @@ def main():
                              "level_hbm_floor_ms": round(r2["stream_bytes"] / (HBM_PEAK_GBS * 1e9) * 1e3, 4),
                              "mac_achieved_GBs": round(r2["mac_bytes"] / (r2["phases"]["mac_ms"] * 1e-3) / 1e9, 1)}
         log(f"[bench] level drop to {args.also_level} primes: {r2['ms']:.3f} ms/level")
+        if args.batch > 1:
+            res["query_batch"] = [run_batch_level(bn, args, r, args.batch), run_batch_level(bn, a2, r2, args.batch)]
+            for qb in res["query_batch"]:
+                log(f"[bench] batch of {qb['queries']} at {qb['scoring_level_primes']} primes: "
+                    f"{qb['ms_per_query_level']:.3f} ms per query level, {qb['value'] / 1e6:.1f} M scores/s")
     print(json.dumps(res), flush=True)
 
 

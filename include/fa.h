@@ -210,6 +210,22 @@ int fa_prepare_query(fa_ctx* ctx, const void* q, int baby_step, void* prep, void
 int fa_score_prepared(fa_ctx* ctx, const void* q, const void* prep, const void* const* blocks, int n_blocks, int d,
                       int baby_step, void* out, void* ws, size_t ws_bytes, void* stream);
 
+/* Cross-query batching against resident blocks (section "Conclusion and
+ * Future Work": score a batch of queries per loaded region so that the load
+ * is paid once per batch): n_q queries,
+ * each prepared with fa_prepare_query (qs[j] the query ciphertext, preps[j]
+ * its baby rotations), scored against the same n_blocks blocks.  Each pass
+ * over the plaintexts serves up to four queries, so the plaintext stream is
+ * read once per four queries instead of once per query.  outs[j] (device,
+ * n_blocks ciphertexts) is bit-identical to fa_score_prepared(qs[j],
+ * preps[j], ...).  Workspace: fa_batch_workspace_bytes(n_q, n_blocks, d,
+ * baby_step) bytes (the accumulators of all n_q queries plus one query's
+ * giant-step scratch).  Errors as fa_score_prepared; FA_E_SHAPE if n_q < 1. */
+size_t fa_batch_workspace_bytes(const fa_ctx* ctx, int n_q, int n_blocks, int d, int baby_step);
+int fa_score_batch(fa_ctx* ctx, const void* const* qs, const void* const* preps, int n_q,
+                   const void* const* blocks, int n_blocks, int d, int baby_step, void* const* outs, void* ws,
+                   size_t ws_bytes, void* stream);
+
 /* Encrypted projection q_R = W^T q (Section 3.1): q holds a d_in-periodic
  * query, w_pts the r plaintexts of W's hybrid diagonals
  * e_j[s] = W[(s+j) mod d_in][s mod r] (j < r), encoded by the caller as a

@@ -902,14 +902,19 @@ size_t baby_ws(const fa_ctx* c, int B) {
 }
 // blocks whose giant steps are processed together
 constexpr int kGiantChunk = 8;
-// workspace of the multiply-accumulate and the giant steps
-size_t giant_ws(const fa_ctx* c, int nb, int d, int B) {
+// scratch of the giant steps of one query (accumulators not included)
+size_t giant_scratch_ws(const fa_ctx* c, int nb, int d, int B) {
   const size_t n = c->n, L = c->L, np = c->np, dn = c->dnum;
   const size_t G = d / B;
+  if (G <= 1) return 0;
   const size_t lanes = lanes_wanted();
   const size_t cb = std::min(nb, kGiantChunk);
-  return rup(nb * G * 2 * L * n) + lanes * rup(cb * L * n) + rup(cb * (G > 1 ? G - 1 : 1) * dn * np * n) +
-         rup(cb * 2 * np * n) + rup(cb * 2 * L * n);
+  return lanes * rup(cb * L * n) + rup(cb * (G - 1) * dn * np * n) + rup(cb * 2 * np * n) + rup(cb * 2 * L * n);
+}
+// workspace of the multiply-accumulate and the giant steps of nq queries
+size_t giant_ws(const fa_ctx* c, int nb, int d, int B, int nq = 1) {
+  const size_t G = d / B;
+  return (size_t)nq * rup((size_t)nb * G * 2 * c->L * c->n) + giant_scratch_ws(c, nb, d, B);
 }
 size_t qrot_words(const fa_ctx* c, int B) { return (size_t)(B - 1) * 2 * c->L * c->n + 1; }
 size_t score_ws(const fa_ctx* c, int nb, int d, int B) {
@@ -1092,70 +1097,91 @@ static int baby_phase(fa_ctx* c, const double* q, int B, double* qrot, Arena& ar
   return FA_OK;
 }
 
-// Multiply-accumulate of q's baby rotations against nb blocks, then the giant
-// steps: Rotate(acc_g, gB) summed over Q u P with one ModDown per block;
-// sigma(acc_g.c0) rides in the key-switch sum multiplied by P.  The first pass
-// of every giant's ModUp runs on the lanes (round-robin over g); one fused
-// kernel then finishes the transforms and forms the key-switch sums.
-static int mac_giant_phase(fa_ctx* c, const double* q, const double* qrot, const double* const* blocks, int nb,
-                           int d, int B, double* out, Arena& ar, hipStream_t s) {
+// Giant steps of one query from its accumulators acc ([nb][G][2][L][N]):
+// out[blk] = acc_0 + Rotate(acc_g, gB) summed over g >= 1 in Q u P with one
+// ModDown per block; sigma(acc_g.c0) rides in the key-switch sum multiplied by
+// P.  The first pass of every giant's ModUp runs on the lanes (round-robin over
+// g); one fused kernel then finishes the transforms and forms the key-switch
+// sums.  Scratch comes from ar (giant_ws minus the accumulators).
+static int giant_phase(fa_ctx* c, const double* acc, int nb, int G, int B, double* out, Arena& ar, hipStream_t s) {
   const size_t n = c->n, L = c->L, np = c->np, dn = c->dnum;
-  const int G = d / B;
   const size_t ctw = 2 * L * n;
-  for (int g = 1; g < G; ++g)
-    if (!c->keys.count(g * B)) return fail(FA_E_NOKEY, "no rotation key for giant step %d", g * B);
-  const int lanes = lanes_wanted();
-  const int cbm = std::min(nb, kGiantChunk);
-  const int ng = G > 1 ? G - 1 : 1;
-  double* acc = ar.take((size_t)nb * G * ctw);
-  const size_t gy_l = rup((size_t)cbm * L * n) / 8;
-  const size_t ext_w = dn * np * n;
-  double* gy = ar.take(lanes * gy_l);
-  double* gext = ar.take((size_t)cbm * ng * ext_w);
-  double* usum = ar.take((size_t)cbm * 2 * np * n);
-  double* gconv = ar.take((size_t)cbm * 2 * L * n);
-  if (!acc || !gy || !gext || !usum || !gconv) return fail(FA_E_NOMEM, "workspace too small for score_block");
-  int rc = ensure_lanes(c, lanes);
-  if (rc) return rc;
-  if (c->prof) HIPCHK(hipEventRecord(c->ev[1], s));
-  fa::mac_diag(c, q, qrot, blocks, nb, B, G, acc, s);
-  if (c->prof) HIPCHK(hipEventRecord(c->ev[2], s));
   const size_t astride = (size_t)G * ctw;
   if (G == 1) {
     for (int blk = 0; blk < nb; ++blk)
       HIPCHK(hipMemcpyAsync(out + (size_t)blk * ctw, acc + (size_t)blk * ctw, ctw * 8, hipMemcpyDeviceToDevice, s));
-  } else {
-    std::vector<const double*> keys(G - 1);
-    std::vector<uint32_t> ggal(G - 1);
-    for (int g = 1; g < G; ++g) {
-      keys[g - 1] = c->keys[g * B];
-      ggal[g - 1] = galois(c->n, g * B);
-    }
-    for (int b0 = 0; b0 < nb; b0 += cbm) {
-      const int cb = std::min(cbm, nb - b0);
-      const double* accb = acc + (size_t)b0 * astride;
-      const int gl = std::min(lanes, G - 1);
-      if ((rc = fork_lanes(c, s, gl))) return rc;
-      for (int g = 1; g < G; ++g) {
-        const int lane = (g - 1) % gl;
-        modup(c, accb + (size_t)g * ctw, astride, cb, gy + lane * gy_l, L * n, gext + (size_t)(g - 1) * ext_w,
-              (size_t)(G - 1) * ext_w, lane_stream(c, s, lane), false);
-      }
-      if ((rc = join_lanes(c, s, gl))) return rc;
-      fa::giant_ks(c, gext, accb, astride, keys.data(), ggal.data(), cb, G - 1, usum, s);
-      std::vector<const double*> bases(2 * cb);
-      std::vector<double*> douts(2 * cb);
-      std::vector<uint32_t> gals(2 * cb, 1u);
-      for (int blk = 0; blk < cb; ++blk) {
-        const double* acc0 = accb + (size_t)blk * astride;
-        bases[2 * blk] = acc0;
-        bases[2 * blk + 1] = acc0 + L * n;
-        douts[2 * blk] = out + (size_t)(b0 + blk) * ctw;
-        douts[2 * blk + 1] = out + (size_t)(b0 + blk) * ctw + L * n;
-      }
-      moddown_polys(c, usum, 2 * cb, gconv, bases.data(), douts.data(), gals.data(), s);
-    }
+    return FA_OK;
   }
+  const int lanes = lanes_wanted();
+  const int cbm = std::min(nb, kGiantChunk);
+  const size_t gy_l = rup((size_t)cbm * L * n) / 8;
+  const size_t ext_w = dn * np * n;
+  const size_t mark = ar.used;
+  double* gy = ar.take(lanes * gy_l);
+  double* gext = ar.take((size_t)cbm * (G - 1) * ext_w);
+  double* usum = ar.take((size_t)cbm * 2 * np * n);
+  double* gconv = ar.take((size_t)cbm * 2 * L * n);
+  if (!gy || !gext || !usum || !gconv) return fail(FA_E_NOMEM, "workspace too small for the giant steps");
+  int rc = ensure_lanes(c, lanes);
+  if (rc) return rc;
+  std::vector<const double*> keys(G - 1);
+  std::vector<uint32_t> ggal(G - 1);
+  for (int g = 1; g < G; ++g) {
+    keys[g - 1] = c->keys[g * B];
+    ggal[g - 1] = galois(c->n, g * B);
+  }
+  for (int b0 = 0; b0 < nb; b0 += cbm) {
+    const int cb = std::min(cbm, nb - b0);
+    const double* accb = acc + (size_t)b0 * astride;
+    const int gl = std::min(lanes, G - 1);
+    if ((rc = fork_lanes(c, s, gl))) return rc;
+    for (int g = 1; g < G; ++g) {
+      const int lane = (g - 1) % gl;
+      modup(c, accb + (size_t)g * ctw, astride, cb, gy + lane * gy_l, L * n, gext + (size_t)(g - 1) * ext_w,
+            (size_t)(G - 1) * ext_w, lane_stream(c, s, lane), false);
+    }
+    if ((rc = join_lanes(c, s, gl))) return rc;
+    fa::giant_ks(c, gext, accb, astride, keys.data(), ggal.data(), cb, G - 1, usum, s);
+    std::vector<const double*> bases(2 * cb);
+    std::vector<double*> douts(2 * cb);
+    std::vector<uint32_t> gals(2 * cb, 1u);
+    for (int blk = 0; blk < cb; ++blk) {
+      const double* acc0 = accb + (size_t)blk * astride;
+      bases[2 * blk] = acc0;
+      bases[2 * blk + 1] = acc0 + L * n;
+      douts[2 * blk] = out + (size_t)(b0 + blk) * ctw;
+      douts[2 * blk + 1] = out + (size_t)(b0 + blk) * ctw + L * n;
+    }
+    moddown_polys(c, usum, 2 * cb, gconv, bases.data(), douts.data(), gals.data(), s);
+  }
+  ar.used = mark;
+  return FA_OK;
+}
+
+static int check_giant_keys(const fa_ctx* c, int d, int B) {
+  for (int g = 1; g < d / B; ++g)
+    if (!c->keys.count(g * B)) return fail(FA_E_NOKEY, "no rotation key for giant step %d", g * B);
+  return FA_OK;
+}
+
+// Multiply-accumulate of nq queries' baby rotations against nb blocks (one
+// pass over the plaintexts per group of up to FA_MAXQ queries), then each
+// query's giant steps into outs[j].
+static int mac_giant_phase(fa_ctx* c, const double* const* q, const double* const* qrot, int nq,
+                           const double* const* blocks, int nb, int d, int B, double* const* outs, Arena& ar,
+                           hipStream_t s) {
+  const size_t ctw = 2 * (size_t)c->L * c->n;
+  const int G = d / B;
+  int rc = check_giant_keys(c, d, B);
+  if (rc) return rc;
+  std::vector<double*> acc(nq);
+  for (int j = 0; j < nq; ++j)
+    if (!(acc[j] = ar.take((size_t)nb * G * ctw))) return fail(FA_E_NOMEM, "workspace too small for score_block");
+  if (c->prof) HIPCHK(hipEventRecord(c->ev[1], s));
+  fa::mac_diag(c, q, qrot, nq, blocks, nb, B, G, acc.data(), s);
+  if (c->prof) HIPCHK(hipEventRecord(c->ev[2], s));
+  for (int j = 0; j < nq; ++j)
+    if ((rc = giant_phase(c, acc[j], nb, G, B, outs[j], ar, s))) return rc;
   if (c->prof) {
     HIPCHK(hipEventRecord(c->ev[3], s));
     c->prof_done = true;
@@ -1173,7 +1199,8 @@ static int score_diag(fa_ctx* c, const double* q, const double* const* blocks, i
   if (c->prof) HIPCHK(hipEventRecord(c->ev[0], s));
   int rc = baby_phase(c, q, B, qrot, ar, s);
   if (rc) return rc;
-  return mac_giant_phase(c, q, qrot, blocks, nb, d, B, out, ar, s);
+  const double* qq = qrot;
+  return mac_giant_phase(c, &q, &qq, 1, blocks, nb, d, B, &out, ar, s);
 }
 
 extern "C" {
@@ -1229,8 +1256,36 @@ int fa_score_prepared(fa_ctx* c, const void* q, const void* prep, const void* co
   Arena ar{(char*)ws, ws_bytes, 0};
   hipStream_t s = (hipStream_t)stream;
   if (c->prof) HIPCHK(hipEventRecord(c->ev[0], s));
-  return mac_giant_phase(c, (const double*)q, (const double*)prep, (const double* const*)blocks, n_blocks, d,
-                         baby_step, (double*)out, ar, s);
+  const double* qp = (const double*)q;
+  const double* pp = (const double*)prep;
+  double* op = (double*)out;
+  return mac_giant_phase(c, &qp, &pp, 1, (const double* const*)blocks, n_blocks, d, baby_step, &op, ar, s);
+}
+
+size_t fa_batch_workspace_bytes(const fa_ctx* c, int n_q, int n_blocks, int d, int baby_step) {
+  if (!c || n_q < 1 || baby_step < 1 || d < baby_step) return 0;
+  return giant_ws(c, std::max(1, n_blocks), d, baby_step, n_q);
+}
+
+int fa_score_batch(fa_ctx* c, const void* const* qs, const void* const* preps, int n_q, const void* const* blocks,
+                   int n_blocks, int d, int baby_step, void* const* outs, void* ws, size_t ws_bytes, void* stream) {
+  if (!c || !qs || !preps || !blocks || !outs) return fail(FA_E_INVAL, "fa_score_batch: null argument");
+  if (n_q < 1) return fail(FA_E_SHAPE, "n_q must be positive");
+  for (int j = 0; j < n_q; ++j)
+    if (!qs[j] || !preps[j] || !outs[j]) return fail(FA_E_INVAL, "query %d: null argument", j);
+  if (n_blocks < 1) return fail(FA_E_SHAPE, "n_blocks must be positive");
+  for (int i = 0; i < n_blocks; ++i)
+    if (!blocks[i]) return fail(FA_E_INVAL, "block %d is null", i);
+  const int S = c->n / 2;
+  if (d < 1 || (d & (d - 1)) || d > S) return fail(FA_E_SHAPE, "d=%d must be a power of two <= N/2", d);
+  if (baby_step < 1 || d % baby_step) return fail(FA_E_INVAL, "baby_step %d must divide d=%d", baby_step, d);
+  const size_t need = giant_ws(c, n_blocks, d, baby_step, n_q);
+  if (!ws || ws_bytes < need) return fail(FA_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
+  Arena ar{(char*)ws, ws_bytes, 0};
+  hipStream_t s = (hipStream_t)stream;
+  if (c->prof) HIPCHK(hipEventRecord(c->ev[0], s));
+  return mac_giant_phase(c, (const double* const*)qs, (const double* const*)preps, n_q, (const double* const*)blocks,
+                         n_blocks, d, baby_step, (double* const*)outs, ar, s);
 }
 
 int fa_score_block(fa_ctx* c, const void* q, const void* const* blocks, int n_blocks, int d, int layout,

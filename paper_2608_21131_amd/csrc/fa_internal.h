@@ -152,10 +152,12 @@ void giant_ks(const fa_ctx* c, const double* ext, const double* acc, size_t astr
               const uint32_t* gals, int nb, int ng, double* u, hipStream_t s);
 
 
-// acc[blk][g][2][L][N] = sum_b pts[blk][(g*B+b)][L][N] * rot_b[2][L][N]
-// with rot_0 = q and rot_b = qrot[b-1] for b >= 1.
-void mac_diag(const fa_ctx* c, const double* q, const double* qrot, const double* const* blocks, int n_blocks,
-              int B, int G, double* acc, hipStream_t s);
+// For each query j < nq: acc[j][blk][g][2][L][N] = sum_b pts[blk][(g*B+b)][L][N] * rot_b[2][L][N]
+// with rot_0 = q[j] and rot_b = qrot[j][b-1] for b >= 1.  Up to FA_MAXQ queries
+// share each pass over the plaintexts.
+#define FA_MAXQ 4
+void mac_diag(const fa_ctx* c, const double* const* q, const double* const* qrot, int nq,
+              const double* const* blocks, int n_blocks, int B, int G, double* const* acc, hipStream_t s);
 
 // out[w] = ct * pt[w] (both polys), w < count
 void mul_plain(const fa_ctx* c, const double* ct, const double* const* pts, int count, double* out, hipStream_t s);

@@ -674,71 +674,96 @@ __global__ __launch_bounds__(256) void k_giant_ks(GiantArgs a, const DevPrime* _
 
 // ---------------------------------------------------------------------------
 // diagonal-layout multiply-accumulate: the HBM stream of the scoring path
-//   acc[blk][g][h][t][k] = sum_b pts[blk][g*B+b][t][k] * qrot[b][h][t][k]
-// One thread per coefficient (t, k); up to NACC (block, g) pairs per pass so
-// every baby rotation of the query is read once per pass; a reduction every
-// 8 products keeps the lazy sums below 2^53.
+//   acc_j[pair][h][t][k] = sum_b pts[blk][g*B+b][t][k] * qrot_j[b][h][t][k]
+// for NQ queries j at once, pair = (blk, g).  One thread per coefficient
+// (t, k); NACC pairs per chunk, so every plaintext word is read once per
+// group of NQ queries; a reduction every 8 products keeps the lazy sums below
+// 2^53.  With several chunks in one launch, workgroup ids are decoded so that
+// the chunks of one coefficient tile run on one XCD back to back: the baby
+// rotations they all read then come from that XCD's L2 after the first.
 // ---------------------------------------------------------------------------
 #define FA_MAXBLK 32
 struct MacArgs {
-  const double* q0;    // rotation 0: the query
-  const double* qrot;  // rotations 1..B-1: [B-1][2][L][N]
+  const double* q0[FA_MAXQ];    // per query: rotation 0 (the query itself)
+  const double* qrot[FA_MAXQ];  // per query: rotations 1..B-1, [B-1][2][L][N]
+  double* acc[FA_MAXQ];         // per query: [n_pairs][2][L][N]
   const double* blk[FA_MAXBLK];
-  double* acc;
   int n_pairs, pair0, B, logG, L;
+  int nchunk, ntile;            // chunks of NACC pairs from pair0; tiles of 256 words
 };
 
-template <int NACC>
+template <int NQ, int NACC>
 __global__ __launch_bounds__(256) void k_mac_diag(MacArgs args, const DevPrime* __restrict__ pr, int logn) {
   const int n = 1 << logn;
   const size_t ln = (size_t)args.L * n;
-  const size_t f = (size_t)blockIdx.x * 256 + threadIdx.x;
+  unsigned tile = blockIdx.x, chunk = 0;
+  if (args.nchunk > 1) {
+    const unsigned j = blockIdx.x >> 3;
+    chunk = j % (unsigned)args.nchunk;
+    tile = (j / (unsigned)args.nchunk) * 8u + (blockIdx.x & 7u);
+    if (tile >= (unsigned)args.ntile) return;
+  }
+  const int pair0 = args.pair0 + (int)chunk * NACC;
+  const size_t f = (size_t)tile * 256 + threadIdx.x;
   const int t = (int)(f >> logn);
   const double q = pr[t].q, qinv = pr[t].qinv;
   const int last = args.n_pairs - 1;
   const int G = 1 << args.logG;
-  double a0[NACC], a1[NACC];
+  double a0[NQ][NACC], a1[NQ][NACC];
 #pragma unroll
-  for (int i = 0; i < NACC; ++i) {
-    a0[i] = 0.0;
-    a1[i] = 0.0;
-  }
+  for (int j = 0; j < NQ; ++j)
+#pragma unroll
+    for (int i = 0; i < NACC; ++i) {
+      a0[j][i] = 0.0;
+      a1[j][i] = 0.0;
+    }
   for (int b = 0; b < args.B; ++b) {
-    const double* __restrict__ qb = b == 0 ? args.q0 : args.qrot + (size_t)(b - 1) * 2 * ln;
-    const double x0 = qb[f];
-    const double x1 = qb[ln + f];
+    double x0[NQ], x1[NQ];
+#pragma unroll
+    for (int j = 0; j < NQ; ++j) {
+      const double* __restrict__ qb = b == 0 ? args.q0[j] : args.qrot[j] + (size_t)(b - 1) * 2 * ln;
+      x0[j] = qb[f];
+      x1[j] = qb[ln + f];
+    }
     // every load of this step is issued before any arithmetic; pairs past the
     // end re-read the last pair (in bounds) and are never stored
     double p[NACC];
 #pragma unroll
     for (int i = 0; i < NACC; ++i) {
-      const int pair = min(args.pair0 + i, last);
+      const int pair = min(pair0 + i, last);
       const double* base = args.blk[pair >> args.logG];
       p[i] = __builtin_nontemporal_load(base + (size_t)((pair & (G - 1)) * args.B + b) * ln + f);
     }
-    const double x0p = x0 * qinv, x1p = x1 * qinv;
 #pragma unroll
-    for (int i = 0; i < NACC; ++i) {
-      a0[i] += mulc(p[i], x0, x0p, q);
-      a1[i] += mulc(p[i], x1, x1p, q);
+    for (int j = 0; j < NQ; ++j) {
+      const double x0p = x0[j] * qinv, x1p = x1[j] * qinv;
+#pragma unroll
+      for (int i = 0; i < NACC; ++i) {
+        a0[j][i] += mulc(p[i], x0[j], x0p, q);
+        a1[j][i] += mulc(p[i], x1[j], x1p, q);
+      }
     }
     if ((b & 7) == 7) {
 #pragma unroll
-      for (int i = 0; i < NACC; ++i) {
-        a0[i] = reduce(a0[i], q, qinv);
-        a1[i] = reduce(a1[i], q, qinv);
+      for (int j = 0; j < NQ; ++j)
+#pragma unroll
+        for (int i = 0; i < NACC; ++i) {
+          a0[j][i] = reduce(a0[j][i], q, qinv);
+          a1[j][i] = reduce(a1[j][i], q, qinv);
+        }
+    }
+  }
+  const int cnt = min(NACC, args.n_pairs - pair0);
+#pragma unroll
+  for (int j = 0; j < NQ; ++j)
+#pragma unroll
+    for (int i = 0; i < NACC; ++i) {
+      if (i < cnt) {
+        double* o = args.acc[j] + (size_t)(pair0 + i) * 2 * ln + f;
+        o[0] = canon_full(a0[j][i], q, qinv);
+        o[ln] = canon_full(a1[j][i], q, qinv);
       }
     }
-  }
-  const int cnt = min(NACC, args.n_pairs - args.pair0);
-#pragma unroll
-  for (int i = 0; i < NACC; ++i) {
-    if (i < cnt) {
-      double* o = args.acc + (size_t)(args.pair0 + i) * 2 * ln + f;
-      o[0] = canon_full(a0[i], q, qinv);
-      o[ln] = canon_full(a1[i], q, qinv);
-    }
-  }
 }
 
 // ---------------------------------------------------------------------------
@@ -1110,8 +1135,9 @@ void giant_ks(const fa_ctx* c, const double* ext, const double* acc, size_t astr
   }
 }
 
-// Most (block, giant) accumulator pairs one pass keeps in registers: 32 (default),
-// 16 or 8; FA_MAC_PAIRS overrides it for tuning.
+// Most (block, giant) accumulator pairs one pass keeps in registers for one
+// query: 32 (default), 16 or 8; FA_MAC_PAIRS overrides it for tuning.  With
+// NQ queries per pass the pairs per pass drop to 32 / NQ.
 static int mac_pairs_max() {
   static int v = -1;
   if (v < 0) {
@@ -1121,37 +1147,63 @@ static int mac_pairs_max() {
   }
   return v;
 }
-void mac_diag(const fa_ctx* c, const double* q, const double* qrot, const double* const* blocks, int n_blocks,
-              int B, int G, double* acc, hipStream_t s) {
+
+template <int NQ, int NACC>
+static void launch_mac(MacArgs a, int nchunk, const fa_ctx* c, hipStream_t s) {
+  a.ntile = (int)((size_t)c->L * c->n / 256);
+  a.nchunk = nchunk;
+  const unsigned grid = nchunk == 1 ? (unsigned)a.ntile : 8u * nchunk * ((a.ntile + 7) / 8);
+  hipLaunchKernelGGL((k_mac_diag<NQ, NACC>), dim3(grid), dim3(256), 0, s, a, c->d_pr, c->logn);
+}
+
+// pairs p0.. of the current query group: all full chunks of the group's widest
+// pass in one launch, then one narrower launch for the rest
+template <int NQ, int WIDE>
+static int mac_chunks(MacArgs& a, int p0, const fa_ctx* c, hipStream_t s) {
+  const int left = a.n_pairs - p0;
+  a.pair0 = p0;
+  if (left >= WIDE) {
+    launch_mac<NQ, WIDE>(a, left / WIDE, c, s);
+    return p0 + (left / WIDE) * WIDE;
+  }
+  if (WIDE > 16 && left > 8) {
+    launch_mac<NQ, (WIDE > 16 ? 16 : WIDE)>(a, 1, c, s);
+    return p0 + 16;
+  }
+  launch_mac<NQ, 8>(a, 1, c, s);
+  return p0 + 8;
+}
+
+void mac_diag(const fa_ctx* c, const double* const* q, const double* const* qrot, int nq,
+              const double* const* blocks, int n_blocks, int B, int G, double* const* acc, hipStream_t s) {
   const int pmax = mac_pairs_max();
   int logG = 0;
   while ((1 << logG) < G) ++logG;
-  for (int b0 = 0; b0 < n_blocks; b0 += FA_MAXBLK) {
-    const int nb = n_blocks - b0 < FA_MAXBLK ? n_blocks - b0 : FA_MAXBLK;
-    MacArgs a;
-    a.q0 = q;
-    a.qrot = qrot;
-    for (int i = 0; i < nb; ++i) a.blk[i] = blocks[b0 + i];
-    a.acc = acc + (size_t)b0 * G * 2 * c->L * c->n;
-    a.n_pairs = nb * G;
-    a.B = B;
-    a.logG = logG;
-    a.L = c->L;
-    dim3 g((unsigned)((size_t)c->L * c->n / 256));
-    for (int p0 = 0; p0 < a.n_pairs;) {
-      a.pair0 = p0;
-      const int left = a.n_pairs - p0;
-      if (left > 16 && pmax >= 32) {
-        hipLaunchKernelGGL(k_mac_diag<32>, g, dim3(256), 0, s, a, c->d_pr, c->logn);
-        p0 += 32;
-      } else if (left > 8 && pmax >= 16) {
-        hipLaunchKernelGGL(k_mac_diag<16>, g, dim3(256), 0, s, a, c->d_pr, c->logn);
-        p0 += 16;
-      } else {
-        hipLaunchKernelGGL(k_mac_diag<8>, g, dim3(256), 0, s, a, c->d_pr, c->logn);
-        p0 += 8;
+  const size_t ctw = (size_t)2 * c->L * c->n;
+  for (int j0 = 0; j0 < nq;) {
+    const int m = nq - j0 >= 4 ? 4 : nq - j0 >= 2 ? 2 : 1;  // queries sharing this plaintext pass
+    for (int b0 = 0; b0 < n_blocks; b0 += FA_MAXBLK) {
+      const int nb = n_blocks - b0 < FA_MAXBLK ? n_blocks - b0 : FA_MAXBLK;
+      MacArgs a;
+      for (int j = 0; j < m; ++j) {
+        a.q0[j] = q[j0 + j];
+        a.qrot[j] = qrot[j0 + j];
+        a.acc[j] = acc[j0 + j] + (size_t)b0 * G * ctw;
+      }
+      for (int i = 0; i < nb; ++i) a.blk[i] = blocks[b0 + i];
+      a.n_pairs = nb * G;
+      a.B = B;
+      a.logG = logG;
+      a.L = c->L;
+      for (int p0 = 0; p0 < a.n_pairs;) {
+        if (m == 4) p0 = mac_chunks<4, 8>(a, p0, c, s);
+        else if (m == 2) p0 = pmax >= 32 ? mac_chunks<2, 16>(a, p0, c, s) : mac_chunks<2, 8>(a, p0, c, s);
+        else if (pmax >= 32) p0 = mac_chunks<1, 32>(a, p0, c, s);
+        else if (pmax >= 16) p0 = mac_chunks<1, 16>(a, p0, c, s);
+        else p0 = mac_chunks<1, 8>(a, p0, c, s);
       }
     }
+    j0 += m;
   }
 }
 

@@ -78,6 +78,10 @@ SIGNATURES = {
     "fa_prepare_query": (ctypes.c_int, [_vp, _vp, ctypes.c_int, _vp, _vp, ctypes.c_size_t, _vp]),
     "fa_score_prepared": (ctypes.c_int, [_vp, _vp, _vp, ctypes.POINTER(_vp), ctypes.c_int, ctypes.c_int,
                                          ctypes.c_int, _vp, _vp, ctypes.c_size_t, _vp]),
+    "fa_batch_workspace_bytes": (ctypes.c_size_t, [_vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int]),
+    "fa_score_batch": (ctypes.c_int, [_vp, ctypes.POINTER(_vp), ctypes.POINTER(_vp), ctypes.c_int,
+                                      ctypes.POINTER(_vp), ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                      ctypes.POINTER(_vp), _vp, ctypes.c_size_t, _vp]),
     "fa_profile": (ctypes.c_int, [_vp, ctypes.c_int]),
     "fa_profile_read": (ctypes.c_int, [_vp, _f64p]),
 }
@@ -291,6 +295,28 @@ class Context:
         _check(self.lib.fa_score_prepared(self.h, _dev(q), _dev(prep), arr, nb, d, baby_step, _dev(out), _dev(ws),
                                           ws.numel() * 8, _stream(stream)))
         return out
+
+    def batch_workspace(self, n_q: int, n_blocks: int, d: int, baby_step: int) -> torch.Tensor:
+        nbytes = int(self.lib.fa_batch_workspace_bytes(self.h, n_q, n_blocks, d, baby_step))
+        return torch.empty(max(1, nbytes // 8 + 32), dtype=torch.float64, device="cuda")
+
+    def score_batch(self, qs, preps, blocks, d: int, baby_step: int, outs=None, ws: torch.Tensor | None = None,
+                    stream=None) -> list:
+        """Score several prepared queries against the same blocks, one plaintext pass per
+        group of up to four queries; outs[j] equals score_prepared(qs[j], preps[j], ...)."""
+        qs, preps, blocks = list(qs), list(preps), list(blocks)
+        nq, nb = len(qs), len(blocks)
+        if len(preps) != nq:
+            raise ValueError("one prepared rotation set per query")
+        outs = [self.new_ct(nb) for _ in range(nq)] if outs is None else list(outs)
+        ws = self.batch_workspace(nq, nb, d, baby_step) if ws is None else ws
+        qa = (_vp * nq)(*[ctypes.c_void_p(x.data_ptr()) for x in qs])
+        pa = (_vp * nq)(*[ctypes.c_void_p(x.data_ptr()) for x in preps])
+        oa = (_vp * nq)(*[ctypes.c_void_p(x.data_ptr()) for x in outs])
+        ba = (_vp * nb)(*[ctypes.c_void_p(b.data_ptr()) for b in blocks])
+        _check(self.lib.fa_score_batch(self.h, qa, pa, nq, ba, nb, d, baby_step, oa, _dev(ws), ws.numel() * 8,
+                                       _stream(stream)))
+        return outs
 
     def project_ct(self, q: torch.Tensor, w_pts: torch.Tensor, d_in: int, r: int, baby_step: int,
                    out: torch.Tensor | None = None, ws: torch.Tensor | None = None, stream=None) -> torch.Tensor:

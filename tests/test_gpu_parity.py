@@ -282,3 +282,59 @@ def test_prepared_query_scores_identically(name, d, B):
         ref = p.export_ct(p.ctx.score_block(ct, blocks, d, 1, B), len(blocks))
         got = p.export_ct(p.ctx.score_prepared(ct, prep, blocks, d, B), len(blocks))
         assert np.array_equal(got, ref)
+
+
+@pytest.mark.parametrize("name,d,B,nq,rows_list,oracle", [
+    ("tiny", 16, 4, 5, [300, 512], True),   # groups of 4 + 1 queries per plaintext pass
+    ("tiny", 16, 16, 3, [100], True),        # 2 + 1, G = 1 (no giant steps)
+    ("p1", 128, 16, 2, [4096, 1000], False),
+    ("p2", 128, 16, 4, [3000], False),
+])
+def test_batch_scores_match_oracle_and_single(name, d, B, nq, rows_list, oracle):
+    """fa_score_batch: each query's blocks equal fa_score_prepared's word for word and, at the
+    small size, the oracle's BSGS block; decrypted scores match float64 within 1e-4."""
+    p = pair(name, wid=15)
+    S = p.par.slots
+    G = d // B
+    g = gen.rng(15, gen.STREAM_DB, d, B)
+    Xs = [gen.gaussian_unit_rows(g, r, d) for r in rows_list]
+    Q = gen.gaussian_unit_rows(gen.rng(15, gen.STREAM_QUERY), nq, d)
+    keys = p.keys(ckks.steps_for_bsgs(d, B), oracle=oracle)
+    coeffs = [ckks.layout_b_coeffs(X, p.par, d, B) for X in Xs]
+    blocks = [p.ctx.encode_db_block_int(c) for c in coeffs]
+    cts = [p.encrypt_both(ckks.encode(ckks.replicate(Q[j], S), p.n, 40), tag=100 + j) for j in range(nq)]
+    preps = [p.ctx.prepare_query(ct[0], B) for ct in cts]
+    say(f"[batch] {name} d={d} B={B} nq={nq} blocks={rows_list}")
+    outs = p.ctx.score_batch([ct[0] for ct in cts], preps, blocks, d, B)
+    for j in range(nq):
+        got = p.export_ct(outs[j], len(Xs))
+        single = p.export_ct(p.ctx.score_prepared(cts[j][0], preps[j], blocks, d, B), len(Xs))
+        assert np.array_equal(got, single), j
+        if oracle:
+            qrot = p.orc.baby_rotations(cts[j][1], B, keys)
+            for i, c in enumerate(coeffs):
+                pts = np.stack([ckks.to_residues(ci, p.par.q) for ci in c]).reshape(G, B, p.par.L, p.n)
+                assert np.array_equal(got[i], p.orc.bsgs_block(qrot, pts, B, G, keys)), (j, i)
+        for i, X in enumerate(Xs):
+            W = p.ctx.ct_words
+            z = p.ctx.decode(p.ctx.decrypt(outs[j][i * W:(i + 1) * W]), 80)
+            assert np.max(np.abs(z[:len(X)] - X @ Q[j])) < 1e-4
+
+
+def test_batch_rejects_bad_arguments():
+    from paper_2608_21131_amd import fa
+    p = pair("tiny", wid=16)
+    S = p.par.slots
+    d, B = 16, 4
+    p.keys(ckks.steps_for_bsgs(d, B), oracle=False)
+    q = gen.gaussian_unit_rows(gen.rng(16, gen.STREAM_QUERY), 1, d)[0]
+    ct, _ = p.encrypt_both(ckks.encode(ckks.replicate(q, S), p.n, 40), tag=16)
+    prep = p.ctx.prepare_query(ct, B)
+    blk = p.ctx.encode_db_block(gen.gaussian_unit_rows(gen.rng(16, 0), 10, d).astype(np.float32), d, 1, B)
+    with pytest.raises(ValueError):
+        p.ctx.score_batch([ct, ct], [prep], [blk], d, B)       # one prepared set missing
+    with pytest.raises(fa.FaError):
+        p.ctx.score_batch([ct], [prep], [blk], d, 3)           # baby step does not divide d
+    small = p.ctx.batch_workspace(1, 1, d, B)[:16]
+    with pytest.raises(fa.FaError):
+        p.ctx.score_batch([ct], [prep], [blk], d, B, ws=small)  # workspace too small

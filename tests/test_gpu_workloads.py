@@ -234,3 +234,33 @@ def test_rerank_level_at_three_primes_fullsize():
         err = max(err, float(np.max(np.abs(z[:len(rows)] - rows @ q))))
     say(f"[low] max |score - float64| = {err:.2e}")
     assert err < 1e-4
+
+
+def test_rerank_query_batch_fullsize():
+    """Cross-query batching at the rerank level's full size: 5 queries (one plaintext pass for
+    the first four, one for the fifth) against the 4 resident blocks.  Every output ciphertext
+    equals the single-query path word for word (that path is checked against the oracle above)
+    and every decrypted score is within 1e-4 of float64."""
+    w = wl.WORKLOADS["rerank"]
+    st = Setup(w, oracle_steps=[])
+    X, centers = wl.candidate_rows(w)
+    Q = wl.query_vectors(w, 5, centers)
+    S = st.par.slots
+    blocks = [st.ctx.encode_db_block(X[b * S:(b + 1) * S], w.d, 1, w.B) for b in range(w.n_blocks)]
+    cts, preps = [], []
+    for j, v in enumerate(Q):
+        a, e = wl.enc_randomness(w, st.par.q, tag=j)
+        cts.append(st.ctx.encrypt(ckks.encode(ckks.replicate(v, S), st.par.n, 40), a, e))
+        preps.append(st.ctx.prepare_query(cts[-1], w.B))
+    say(f"[batch] {len(Q)} queries x {w.n_blocks} blocks")
+    outs = st.ctx.score_batch(cts, preps, blocks, w.d, w.B)
+    err = 0.0
+    for j in range(len(Q)):
+        single = st.ctx.score_prepared(cts[j], preps[j], blocks, w.d, w.B)
+        assert np.array_equal(st.export(outs[j], w.n_blocks), st.export(single, w.n_blocks)), j
+        for b in range(w.n_blocks):
+            rows = X[b * S:(b + 1) * S].astype(np.float64)
+            z = st.decode(outs[j], b, 80)
+            err = max(err, float(np.max(np.abs(z[:len(rows)] - rows @ Q[j]))))
+    say(f"[batch] max |score - float64| = {err:.2e}")
+    assert err < 1e-4
