@@ -19,6 +19,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdlib>
+#include <type_traits>
 
 #include "fa_internal.h"
 
@@ -675,12 +676,22 @@ __global__ __launch_bounds__(256) void k_giant_ks(GiantArgs a, const DevPrime* _
 // ---------------------------------------------------------------------------
 // diagonal-layout multiply-accumulate: the HBM stream of the scoring path
 //   acc_j[pair][h][t][k] = sum_b pts[blk][g*B+b][t][k] * qrot_j[b][h][t][k]
-// for NQ queries j at once, pair = (blk, g).  One thread per coefficient
-// (t, k); NACC pairs per chunk, so every plaintext word is read once per
-// group of NQ queries; a reduction every 8 products keeps the lazy sums below
-// 2^53.  With several chunks in one launch, workgroup ids are decoded so that
-// the chunks of one coefficient tile run on one XCD back to back: the baby
-// rotations they all read then come from that XCD's L2 after the first.
+// for NQ queries j at once, pair = (blk, g).  Each wave owns 64 consecutive
+// coefficients and keeps NACC pairs x NQ queries x 2 accumulators in
+// registers; every plaintext word is read once per group of NQ queries.
+//
+// The operands of a step (NACC plaintext words and each query's two rotated
+// words per coefficient) travel HBM -> LDS with direct-to-LDS loads into a
+// ring of S per-wave slots: while step b is multiplied out of LDS, steps
+// b+1..b+S-1 are in flight, and they occupy no registers.  A wave only reads
+// its own slots, so the vector-memory counter (loads complete in order) is
+// the only synchronisation: before step b, wait until at most the loads of
+// the later steps are outstanding.  A reduction every 8 products keeps the
+// lazy sums below 2^53.
+//
+// With several chunks of NACC pairs in one launch, workgroup ids are decoded
+// so that the chunks of one coefficient tile run on one XCD back to back and
+// read the rotated queries from that XCD's L2 after the first.
 // ---------------------------------------------------------------------------
 #define FA_MAXBLK 32
 struct MacArgs {
@@ -692,10 +703,21 @@ struct MacArgs {
   int nchunk, ntile;            // chunks of NACC pairs from pair0; tiles of 256 words
 };
 
-template <int NQ, int NACC>
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) const void gbl_void_t;
+
+// s_waitcnt immediate (gfx9 encoding): wait until at most n vector-memory
+// operations are outstanding; the LDS and export counters are not waited on
+#define FA_VMCNT(n) (0x0F70 | ((n) & 15) | (((n) >> 4) << 14))
+#define FA_LGKMCNT0 0xC07F
+
+template <int NQ, int NACC, int S>
 __global__ __launch_bounds__(256) void k_mac_diag(MacArgs args, const DevPrime* __restrict__ pr, int logn) {
-  const int n = 1 << logn;
-  const size_t ln = (size_t)args.L * n;
+  constexpr int ROWS = NACC + 2 * NQ;    // 64-word rows of one step: plaintexts, then x0/x1 per query
+  constexpr int GL = NACC / 2 + NQ;      // loads issued per step
+  static_assert(S == 2 || S == 3, "ring of two or three slots");
+  static_assert((S - 1) * GL <= 63, "vector-memory counter range");
+  __shared__ double slab[4][S][ROWS][64];
   unsigned tile = blockIdx.x, chunk = 0;
   if (args.nchunk > 1) {
     const unsigned j = blockIdx.x >> 3;
@@ -703,12 +725,52 @@ __global__ __launch_bounds__(256) void k_mac_diag(MacArgs args, const DevPrime* 
     tile = (j / (unsigned)args.nchunk) * 8u + (blockIdx.x & 7u);
     if (tile >= (unsigned)args.ntile) return;
   }
-  const int pair0 = args.pair0 + (int)chunk * NACC;
-  const size_t f = (size_t)tile * 256 + threadIdx.x;
-  const int t = (int)(f >> logn);
+  const int n = 1 << logn;
+  const size_t ln = (size_t)args.L * n;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const size_t c0 = (size_t)tile * 256 + (size_t)w * 64;  // first coefficient of this wave
+  const size_t f = c0 + lane;
+  const int t = (int)(c0 >> logn);
   const double q = pr[t].q, qinv = pr[t].qinv;
+  const int pair0 = args.pair0 + (int)chunk * NACC;
   const int last = args.n_pairs - 1;
   const int G = 1 << args.logG;
+  const int B = args.B;
+  const int hp = lane >> 5;                         // which of the two rows a lane's 16 bytes land in
+  const size_t lo = c0 + 2 * (size_t)(lane & 31);   // its two coefficients
+  // per-lane source of each load at step 0 (step b adds b * ln words): lanes
+  // 0-31 read pair 2i, lanes 32-63 pair 2i+1 (pairs past the end re-read the
+  // last pair, in bounds, and are never stored); the queries' x0 / x1 rows
+  const double* src[NACC / 2];
+#pragma unroll
+  for (int i = 0; i < NACC / 2; ++i) {
+    const int pa = min(pair0 + 2 * i, last), pb = min(pair0 + 2 * i + 1, last);
+    const double* xa = args.blk[pa >> args.logG] + (size_t)((pa & (G - 1)) * B) * ln;
+    const double* xb = args.blk[pb >> args.logG] + (size_t)((pb & (G - 1)) * B) * ln;
+    src[i] = (hp ? xb : xa) + lo;
+  }
+  const double* qs0[NQ];
+  const double* qsr[NQ];
+#pragma unroll
+  for (int j = 0; j < NQ; ++j) {
+    qs0[j] = args.q0[j] + (size_t)hp * ln + lo;
+    qsr[j] = args.qrot[j] + (size_t)hp * ln + lo;
+  }
+  // one step's loads into slot sl: row 2i gets pair 2i, row 2i+1 pair 2i+1
+  auto issue = [&](int sl, int b) {
+#pragma unroll
+    for (int i = 0; i < NACC / 2; ++i)
+      __builtin_amdgcn_global_load_lds((gbl_void_t*)(src[i] + (size_t)b * ln), (lds_void_t*)&slab[w][sl][2 * i][0],
+                                       16, 0, 0);
+#pragma unroll
+    for (int j = 0; j < NQ; ++j)
+      __builtin_amdgcn_global_load_lds((gbl_void_t*)(b == 0 ? qs0[j] : qsr[j] + (size_t)(b - 1) * 2 * ln),
+                                       (lds_void_t*)&slab[w][sl][NACC + 2 * j][0], 16, 0, 0);
+  };
+  double* accp[NQ];
+#pragma unroll
+  for (int j = 0; j < NQ; ++j) accp[j] = args.acc[j];
+  const int cnt = min(NACC, args.n_pairs - pair0);
   double a0[NQ][NACC], a1[NQ][NACC];
 #pragma unroll
   for (int j = 0; j < NQ; ++j)
@@ -717,31 +779,40 @@ __global__ __launch_bounds__(256) void k_mac_diag(MacArgs args, const DevPrime* 
       a0[j][i] = 0.0;
       a1[j][i] = 0.0;
     }
-  for (int b = 0; b < args.B; ++b) {
-    double x0[NQ], x1[NQ];
+#pragma unroll
+  for (int sl = 0; sl < S; ++sl)
+    if (sl < B) issue(sl, sl);
+  // one step out of slot SL (a compile-time slot index lets the compiler's
+  // tracking of pending direct-to-LDS loads tell the slots apart)
+  auto step = [&](auto slc, int b) {
+    constexpr int SL = decltype(slc)::value;
+    // steps b+1 .. min(b+S-1, B-1) were issued after step b
+    const int later = min(S - 1, B - 1 - b);
+    __builtin_amdgcn_sched_barrier(0);
+    if (later >= 2) __builtin_amdgcn_s_waitcnt(FA_VMCNT(2 * GL));
+    else if (later == 1) __builtin_amdgcn_s_waitcnt(FA_VMCNT(GL));
+    else __builtin_amdgcn_s_waitcnt(FA_VMCNT(0));
+    __builtin_amdgcn_sched_barrier(0);
+    double x0[NQ], x1[NQ], x0p[NQ], x1p[NQ];
 #pragma unroll
     for (int j = 0; j < NQ; ++j) {
-      const double* __restrict__ qb = b == 0 ? args.q0[j] : args.qrot[j] + (size_t)(b - 1) * 2 * ln;
-      x0[j] = qb[f];
-      x1[j] = qb[ln + f];
-    }
-    // every load of this step is issued before any arithmetic; pairs past the
-    // end re-read the last pair (in bounds) and are never stored
-    double p[NACC];
-#pragma unroll
-    for (int i = 0; i < NACC; ++i) {
-      const int pair = min(pair0 + i, last);
-      const double* base = args.blk[pair >> args.logG];
-      p[i] = __builtin_nontemporal_load(base + (size_t)((pair & (G - 1)) * args.B + b) * ln + f);
+      x0[j] = slab[w][SL][NACC + 2 * j][lane];
+      x1[j] = slab[w][SL][NACC + 2 * j + 1][lane];
+      x0p[j] = x0[j] * qinv;
+      x1p[j] = x1[j] * qinv;
     }
 #pragma unroll
-    for (int j = 0; j < NQ; ++j) {
-      const double x0p = x0[j] * qinv, x1p = x1[j] * qinv;
+    for (int i0 = 0; i0 < NACC; i0 += 8) {
+      double p[8];
 #pragma unroll
-      for (int i = 0; i < NACC; ++i) {
-        a0[j][i] += mulc(p[i], x0[j], x0p, q);
-        a1[j][i] += mulc(p[i], x1[j], x1p, q);
-      }
+      for (int i = 0; i < 8; ++i) p[i] = slab[w][SL][i0 + i][lane];
+#pragma unroll
+      for (int j = 0; j < NQ; ++j)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          a0[j][i0 + i] += mulc(p[i], x0[j], x0p[j], q);
+          a1[j][i0 + i] += mulc(p[i], x1[j], x1p[j], q);
+        }
     }
     if ((b & 7) == 7) {
 #pragma unroll
@@ -752,14 +823,23 @@ __global__ __launch_bounds__(256) void k_mac_diag(MacArgs args, const DevPrime* 
           a1[j][i] = reduce(a1[j][i], q, qinv);
         }
     }
+    // the slot is read out: refill it with step b+S
+    __builtin_amdgcn_s_waitcnt(FA_LGKMCNT0);
+    __builtin_amdgcn_sched_barrier(0);
+    if (b + S < B) issue(SL, b + S);
+  };
+  for (int b0 = 0; b0 < B; b0 += S) {
+    step(std::integral_constant<int, 0>{}, b0);
+    if (b0 + 1 < B) step(std::integral_constant<int, 1>{}, b0 + 1);
+    if constexpr (S > 2)
+      if (b0 + 2 < B) step(std::integral_constant<int, 2>{}, b0 + 2);
   }
-  const int cnt = min(NACC, args.n_pairs - pair0);
 #pragma unroll
   for (int j = 0; j < NQ; ++j)
 #pragma unroll
     for (int i = 0; i < NACC; ++i) {
       if (i < cnt) {
-        double* o = args.acc[j] + (size_t)(pair0 + i) * 2 * ln + f;
+        double* o = accp[j] + (size_t)(pair0 + i) * 2 * ln + f;
         o[0] = canon_full(a0[j][i], q, qinv);
         o[ln] = canon_full(a1[j][i], q, qinv);
       }
@@ -1148,12 +1228,21 @@ static int mac_pairs_max() {
   return v;
 }
 
+// ring depth of the staged loads: as many slots as fit beside the other
+// workgroup sharing a CU's 160 KB of LDS (two slots at one query x 32 pairs)
+template <int NQ, int NACC>
+struct MacStages {
+  static constexpr int BYTES = 4 * (NACC + 2 * NQ) * 64 * 8;
+  static constexpr int S = BYTES * 3 <= 80 * 1024 ? 3 : 2;
+};
+
 template <int NQ, int NACC>
 static void launch_mac(MacArgs a, int nchunk, const fa_ctx* c, hipStream_t s) {
   a.ntile = (int)((size_t)c->L * c->n / 256);
   a.nchunk = nchunk;
   const unsigned grid = nchunk == 1 ? (unsigned)a.ntile : 8u * nchunk * ((a.ntile + 7) / 8);
-  hipLaunchKernelGGL((k_mac_diag<NQ, NACC>), dim3(grid), dim3(256), 0, s, a, c->d_pr, c->logn);
+  hipLaunchKernelGGL((k_mac_diag<NQ, NACC, MacStages<NQ, NACC>::S>), dim3(grid), dim3(256), 0, s, a, c->d_pr,
+                     c->logn);
 }
 
 // pairs p0.. of the current query group: all full chunks of the group's widest
