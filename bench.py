@@ -307,6 +307,16 @@ def run_rank(bn, args):
                 stream_bytes=8 * 2 * w.d * w.L * w.n, cpu=None)
 
 
+def topk(sc, k):
+    """Ids of the k largest scores, ties to the lower id, in descending order."""
+    if k >= len(sc):
+        return np.lexsort((np.arange(len(sc)), -sc))
+    thr = sc[np.argpartition(-sc, k - 1)[:k]].min()
+    above = np.nonzero(sc > thr)[0]
+    sel = np.concatenate([above, np.nonzero(sc == thr)[0][:k - len(above)]])
+    return sel[np.lexsort((sel, -sc[sel]))]
+
+
 def run_three_level(bn, args):
     """32 queries, each: coarse level (222,049 rows, 7 blocks) -> client decrypt, top-16 ->
     fine level (2 of 4 fine-pool blocks) -> top-64 -> rerank level (4 of 8 rerank-pool
@@ -350,22 +360,23 @@ def run_three_level(bn, args):
     level_ms = []
     errs = []
 
-    def decode(ct, b):
-        W_ = ctx.ct_words
-        return ctx.decode(ctx.decrypt(ct[b * W_:(b + 1) * W_]), 80)
+    from concurrent.futures import ThreadPoolExecutor
+    pool = ThreadPoolExecutor(max_workers=8)
 
     def top(ct, nb, k, rows_list, qv, n_rows_last=None):
+        # client side: decrypt every block (device), then decode them on host threads
+        W_ = ctx.ct_words
+        res = [ctx.decrypt(ct[b * W_:(b + 1) * W_]) for b in range(nb)]
+        zs = list(pool.map(lambda r: ctx.decode(r, 80), res))
         scores = []
         for b in range(nb):
-            z = decode(ct, b)
+            z = zs[b]
             n_valid = len(rows_list[b]) if (b < nb - 1 or n_rows_last is None) else n_rows_last
             scores.append(z[:n_valid])
             if qv is not None:
                 ref = rows_list[b][:n_valid].astype(np.float64) @ qv
                 errs.append(float(np.max(np.abs(z[:n_valid] - ref))))
-        sc = np.concatenate(scores)
-        order = np.lexsort((np.arange(len(sc)), -sc))
-        return order[:k]
+        return topk(np.concatenate(scores), k)
 
     def one_query(i, check):
         qv = queries[i] if check else None

@@ -15,6 +15,9 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <map>
+#include <memory>
+#include <mutex>
 #include <new>
 #include <string>
 #include <thread>
@@ -138,19 +141,52 @@ static uint32_t galois(int n, long step) {
 namespace {
 using cplx = std::complex<double>;
 
-// in-place radix-2 FFT of length n; sign = -1: sum x_t e^{-2 pi i k t / n}, +1: e^{+...}
-void fft(std::vector<cplx>& a, int sign) {
+// Tables of the host transforms for ring degree n, built once per n and
+// shared by every context (they depend on n only).
+struct FftTables {
+  std::vector<cplx> root_fwd, root_inv;  // e^{-2 pi i k / n}, e^{+2 pi i k / n}, k < n/2
+  std::vector<cplx> twist;               // e^{i pi k / n}, k < n
+  std::vector<u64> e;                    // slot exponents 5^j mod 2n, j < n/2
+};
+const FftTables& fft_tables(int n) {
+  static std::mutex mu;
+  static std::map<int, std::unique_ptr<FftTables>> cache;
+  std::lock_guard<std::mutex> lock(mu);
+  auto& slot = cache[n];
+  if (!slot) {
+    auto t = std::make_unique<FftTables>();
+    t->root_fwd.resize(n / 2);
+    t->root_inv.resize(n / 2);
+    for (int k = 0; k < n / 2; ++k) {
+      const double ang = 2.0 * M_PI * (double)k / (double)n;
+      t->root_fwd[k] = cplx(std::cos(ang), -std::sin(ang));
+      t->root_inv[k] = cplx(std::cos(ang), std::sin(ang));
+    }
+    t->twist.resize(n);
+    for (int k = 0; k < n; ++k) {
+      const double ang = M_PI * (double)k / (double)n;
+      t->twist[k] = cplx(std::cos(ang), std::sin(ang));
+    }
+    t->e.resize(n / 2);
+    u64 x = 1;
+    for (int j = 0; j < n / 2; ++j) {
+      t->e[j] = x;
+      x = x * 5 % (2ull * n);
+    }
+    slot = std::move(t);
+  }
+  return *slot;
+}
+
+// in-place radix-2 FFT of length n with the root table of the wanted sign
+// (root_fwd: sum x_t e^{-2 pi i k t / n}; root_inv: e^{+...})
+void fft(std::vector<cplx>& a, const std::vector<cplx>& root) {
   const size_t n = a.size();
   for (size_t i = 1, j = 0; i < n; ++i) {
     size_t bit = n >> 1;
     for (; j & bit; bit >>= 1) j ^= bit;
     j ^= bit;
     if (i < j) std::swap(a[i], a[j]);
-  }
-  std::vector<cplx> root(n / 2);
-  for (size_t k = 0; k < n / 2; ++k) {
-    const double ang = 2.0 * M_PI * (double)k / (double)n;
-    root[k] = cplx(std::cos(ang), sign * std::sin(ang));
   }
   for (size_t len = 2; len <= n; len <<= 1) {
     const size_t step = n / len;
@@ -163,29 +199,22 @@ void fft(std::vector<cplx>& a, int sign) {
   }
 }
 
-std::vector<u64> slot_exps(int n) {
-  std::vector<u64> e(n / 2);
-  u64 x = 1;
-  for (int j = 0; j < n / 2; ++j) {
-    e[j] = x;
-    x = x * 5 % (2ull * n);
-  }
-  return e;
-}
+const std::vector<u64>& slot_exps(int n) { return fft_tables(n).e; }
 
 // m_k = rint(scale * (2/N) sum_j v_j cos(pi k e_j / N)) via one length-N FFT:
 // sum_j v_j (w^{-k e_j} + w^{k e_j}) = w^{-k} sum_t Z_t e^{-2 pi i k t / N},
 // w = e^{i pi / N}, Z_t = v_j at t = (e_j - 1)/2 and t = (2N - e_j - 1)/2.
 void encode_one(int n, const std::vector<u64>& e, const double* v, int nv, double scale, int64_t* out) {
+  const FftTables& tb = fft_tables(n);
   std::vector<cplx> z(n, cplx(0, 0));
   for (int j = 0; j < nv; ++j) {
     z[(e[j] - 1) / 2] = v[j];
     z[(2 * (u64)n - e[j] - 1) / 2] = v[j];
   }
-  fft(z, -1);
+  fft(z, tb.root_fwd);
   for (int k = 0; k < n; ++k) {
-    const double ang = -M_PI * (double)k / (double)n;
-    const double re = z[k].real() * std::cos(ang) - z[k].imag() * std::sin(ang);
+    // Re(z_k w^-k), w = e^{i pi / N}
+    const double re = z[k].real() * tb.twist[k].real() + z[k].imag() * tb.twist[k].imag();
     out[k] = (int64_t)std::nearbyint(scale * re / (double)n);
   }
 }
@@ -245,6 +274,7 @@ void fa_ctx_destroy(fa_ctx* c) {
     (void)hipEventDestroy(c->join_ev[i]);
   }
   if (c->fork_ev) (void)hipEventDestroy(c->fork_ev);
+  (void)hipFree(c->d_export);
   delete c;
 }
 
@@ -573,13 +603,20 @@ int fa_encrypt(fa_ctx* c, const int64_t* m, const uint64_t* a, const int64_t* e,
 static int export_polys(fa_ctx* c, const double* src, int n_polys, uint64_t* out, hipStream_t s, bool decrypt) {
   const size_t n = c->n, L = c->L;
   const size_t words = (size_t)n_polys * L * n;
-  double* tmp = nullptr;
-  uint64_t* du = nullptr;
-  int rc;
-  if ((rc = dev_alloc(&tmp, words)) || (rc = dev_alloc(&du, words))) {
-    (void)hipFree(tmp);
-    return rc;
+  std::lock_guard<std::mutex> lock(c->export_mu);
+  if (c->export_words < words) {
+    if (c->d_export) {
+      HIPCHK(hipStreamSynchronize(s));
+      (void)hipFree(c->d_export);
+      c->d_export = nullptr;
+      c->export_words = 0;
+    }
+    int rc = dev_alloc(&c->d_export, 2 * words);
+    if (rc) return rc;
+    c->export_words = words;
   }
+  double* tmp = c->d_export;
+  uint64_t* du = reinterpret_cast<uint64_t*>(c->d_export + c->export_words);
   if (decrypt) {
     fa::dec_combine(c, src, tmp, s);
   } else {
@@ -587,11 +624,10 @@ static int export_polys(fa_ctx* c, const double* src, int n_polys, uint64_t* out
   }
   fa::ntt_inv_strided(c, tmp, n, (int)(n_polys * L), (int)L, 0, s);
   fa::res_to_u64(tmp, words, du, s);
-  if ((rc = check_launch("export"))) return rc;
+  int rc = check_launch("export");
+  if (rc) return rc;
   HIPCHK(hipMemcpyAsync(out, du, words * 8, hipMemcpyDeviceToHost, s));
   HIPCHK(hipStreamSynchronize(s));
-  (void)hipFree(tmp);
-  (void)hipFree(du);
   return FA_OK;
 }
 
@@ -612,7 +648,7 @@ int fa_encode(const fa_ctx* c, const double* slots, int n_slots, int log_scale, 
   if (!c || !slots || !out) return fail(FA_E_INVAL, "fa_encode: null argument");
   if (n_slots < 0 || n_slots > c->n / 2) return fail(FA_E_SHAPE, "fa_encode: n_slots %d > N/2", n_slots);
   if (log_scale < 0 || log_scale > 61) return fail(FA_E_INVAL, "fa_encode: log_scale out of range");
-  std::vector<u64> e = slot_exps(c->n);
+  const std::vector<u64>& e = slot_exps(c->n);
   encode_one(c->n, e, slots, n_slots, std::ldexp(1.0, log_scale), out);
   return FA_OK;
 }
@@ -735,13 +771,11 @@ int fa_decode(const fa_ctx* c, const uint64_t* res, int log_scale, double* out, 
     for (int k = w; k < n; k += 16) m[k] = crt_to_double(r, res + k, (size_t)n);
   });
   // z(2t+1) = sum_k m_k w^k e^{+2 pi i k t / N}
+  const FftTables& tb = fft_tables(n);
   std::vector<cplx> y(n);
-  for (int k = 0; k < n; ++k) {
-    const double ang = M_PI * (double)k / (double)n;
-    y[k] = cplx(m[k] * std::cos(ang), m[k] * std::sin(ang));
-  }
-  fft(y, +1);
-  std::vector<u64> e = slot_exps(n);
+  for (int k = 0; k < n; ++k) y[k] = cplx(m[k] * tb.twist[k].real(), m[k] * tb.twist[k].imag());
+  fft(y, tb.root_inv);
+  const std::vector<u64>& e = tb.e;
   const double inv_scale = std::ldexp(1.0, -log_scale);
   for (int j = 0; j < n_slots; ++j) out[j] = y[(e[j] - 1) / 2].real() * inv_scale;
   return FA_OK;
@@ -782,7 +816,7 @@ int fa_encode_db_block(fa_ctx* c, const float* rows, int n_rows, int dim, int d,
   if (d < 1 || (d & (d - 1)) || d > S) return fail(FA_E_SHAPE, "d=%d must be a power of two <= N/2", d);
   if (dim < 1 || dim > d) return fail(FA_E_SHAPE, "dim=%d must be in [1, d=%d]", dim, d);
   if (n_rows < 1) return fail(FA_E_SHAPE, "n_rows must be positive");
-  std::vector<u64> e = slot_exps(c->n);
+  const std::vector<u64>& e = slot_exps(c->n);
   const double scale = std::ldexp(1.0, c->log_scale);
   std::vector<int64_t> coeffs;
   int n_pts;
@@ -827,7 +861,7 @@ int fa_encode_projection(fa_ctx* c, const float* W, int d_in, int r, int baby_st
   if (r < 1 || (r & (r - 1)) || d_in < r || d_in % r || (d_in & (d_in - 1)) || d_in > S)
     return fail(FA_E_SHAPE, "d_in=%d, r=%d: powers of two with r | d_in and d_in <= N/2", d_in, r);
   if (baby_step < 1 || r % baby_step) return fail(FA_E_INVAL, "baby_step %d must divide r=%d", baby_step, r);
-  std::vector<u64> e = slot_exps(c->n);
+  const std::vector<u64>& e = slot_exps(c->n);
   const double scale = std::ldexp(1.0, c->log_scale);
   std::vector<int64_t> coeffs((size_t)r * c->n);
   parallel_for(r, [&](int j) {

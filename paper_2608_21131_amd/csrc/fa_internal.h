@@ -6,6 +6,7 @@
 #include <cstddef>
 #include <cstdint>
 #include <map>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -71,6 +72,11 @@ struct fa_ctx {
   hipStream_t aux[FA_MAXAUX] = {};
   hipEvent_t fork_ev = nullptr;
   hipEvent_t join_ev[FA_MAXAUX] = {};
+  // device staging of fa_decrypt / fa_export_coeffs (client and test side),
+  // grown on demand and reused; the mutex serialises callers on other threads
+  std::mutex export_mu;
+  double* d_export = nullptr;     // [2][words]: coefficient transform, then u64 residues
+  size_t export_words = 0;
 };
 
 // --------------------------------------------------------------------------
