@@ -357,6 +357,11 @@ def _lib():
     lib.or_mul_plain.argtypes = [ctypes.c_void_p, _u64p, _u64p, _u64p]
     lib.or_bsgs_block.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int, _u64p, _u64p, _u64p,
                                   ctypes.POINTER(_u64p), ctypes.POINTER(_u64p), _u64p]
+    lib.or_keygen_relin.argtypes = [ctypes.c_void_p, _i64p, _u64p, _i64p, _u64p, _u64p]
+    lib.or_tensor.argtypes = [ctypes.c_void_p, _u64p, _u64p, _u64p]
+    lib.or_relin.argtypes = [ctypes.c_void_p, _u64p, _u64p, _u64p, _u64p]
+    lib.or_bsgs_block_ct.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int, _u64p, _u64p, _u64p,
+                                     ctypes.POINTER(_u64p), ctypes.POINTER(_u64p), _u64p, _u64p, _u64p]
     return lib
 
 
@@ -469,6 +474,62 @@ class Oracle:
     def mul_plain(self, ct: np.ndarray, pt: np.ndarray) -> np.ndarray:
         out = np.empty_like(_c(ct))
         self.lib.or_mul_plain(self.ctx, _p(_c(ct)), _p(_c(pt)), _p(out))
+        return out
+
+    # ---- encrypted database (ct x ct) ----
+    def keygen_relin(self, s: np.ndarray, a: np.ndarray, e: np.ndarray):
+        """Relinearisation key switching s^2 to s: (b, a), each [dnum][L+K][N],
+        b_i = -a_i s + e_i + gadget_i * s^2 (the rotation keys' form with s^2 in
+        place of sigma(s))."""
+        par = self.par
+        a = _c(a)
+        assert a.shape == (par.dnum, par.L + par.K, par.n)
+        b = np.empty_like(a)
+        self.lib.or_keygen_relin(self.ctx, _p(_c(s, np.int64), _i64p), _p(a), _p(_c(e, np.int64), _i64p),
+                                 _p(self.gadget), _p(b))
+        return b, a
+
+    def tensor(self, x: np.ndarray, y: np.ndarray) -> np.ndarray:
+        """(x0, x1) x (y0, y1) = (x0 y0, x0 y1 + x1 y0, x1 y1): [3][L][N], decrypts under (1, s, s^2)."""
+        out = np.empty((3, self.par.L, self.par.n), dtype=np.uint64)
+        self.lib.or_tensor(self.ctx, _p(_c(x)), _p(_c(y)), _p(out))
+        return out
+
+    def relin(self, d: np.ndarray, rlk) -> np.ndarray:
+        """(d0 + ModDown(u0), d1 + ModDown(u1)), (u0, u1) the key-switch inner product of d2."""
+        out = np.empty((2, self.par.L, self.par.n), dtype=np.uint64)
+        kb, ka = rlk
+        self.lib.or_relin(self.ctx, _p(_c(d)), _p(_c(kb)), _p(_c(ka)), _p(out))
+        return out
+
+    def decrypt3(self, d: np.ndarray, s: np.ndarray) -> np.ndarray:
+        """d0 + d1 s + d2 s^2 per ciphertext prime (coefficient form)."""
+        par = self.par
+        out = np.empty((par.L, par.n), dtype=np.uint64)
+        for t, q in enumerate(par.q):
+            st = to_residues(s, [q])[0]
+            s2 = self.polymul(t, st, st)
+            v = (d[0, t].astype(object) + self.polymul(t, d[1, t], st).astype(object)
+                 + self.polymul(t, d[2, t], s2).astype(object)) % q
+            out[t] = v.astype(np.uint64)
+        return out
+
+    def bsgs_block_ct(self, qrot: np.ndarray, cts: np.ndarray, B: int, G: int, keys: dict, rlk) -> np.ndarray:
+        """One block against encrypted pre-rotated diagonals cts [G][B][2][L][N]: per giant
+        index, the tensor sum over b, one relinearisation, then the giant sum of bsgs_block."""
+        par = self.par
+        cts = _c(cts)
+        assert cts.shape == (G, B, 2, par.L, par.n)
+        qrot = _c(qrot)
+        gs = _c([0] + [galois_element(par.n, g * B) for g in range(1, G)])
+        dummy = np.zeros(1, dtype=np.uint64)
+        kb = [dummy] + [_c(keys[g * B][0]) for g in range(1, G)]
+        ka = [dummy] + [_c(keys[g * B][1]) for g in range(1, G)]
+        kbp = (_u64p * G)(*[_p(x) for x in kb])
+        kap = (_u64p * G)(*[_p(x) for x in ka])
+        rkb, rka = _c(rlk[0]), _c(rlk[1])
+        out = np.empty((2, par.L, par.n), dtype=np.uint64)
+        self.lib.or_bsgs_block_ct(self.ctx, B, G, _p(qrot), _p(cts), _p(gs), kbp, kap, _p(rkb), _p(rka), _p(out))
         return out
 
     def baby_rotations(self, ct: np.ndarray, B: int, keys: dict) -> np.ndarray:

@@ -575,3 +575,178 @@ void or_bsgs_block(void* p, int B, int G, const u64* qrot, const u64* pts, const
   }
   free(acc); free(usum); free(u); free(tmp); free(qhat);
 }
+
+/* ------------------------------------------------------------------ */
+/* encrypted database: ct x ct products with lazy relinearisation       */
+/* ------------------------------------------------------------------ */
+
+/* Relinearisation key (switches s^2 to s): for every digit i and prime t of
+ * Q u P,  b_i = -a_i*s + e_i + gad[i][t] * s^2.  s^2 is the negacyclic square
+ * of s reduced mod the prime.  a: [dnum][L+K][N]; e: [dnum][N]; b: out. */
+void or_keygen_relin(void* p, const i64* s, const u64* a, const i64* e, const u64* gad, u64* b) {
+  octx* c = (octx*)p;
+  int n = c->n, np = c->L + c->K, dnum = c->dnum;
+#pragma omp parallel for collapse(2) schedule(dynamic)
+  for (int i = 0; i < dnum; ++i) {
+    for (int t = 0; t < np; ++t) {
+      u64 q = c->primes[t];
+      u64* sp = (u64*)malloc(sizeof(u64) * n);
+      u64* s2 = (u64*)malloc(sizeof(u64) * n);
+      u64* as = (u64*)malloc(sizeof(u64) * n);
+      for (int k = 0; k < n; ++k) sp[k] = from_signed(s[k], q);
+      or_polymul(c, t, sp, sp, s2);
+      const u64* ai = a + ((size_t)i * np + t) * n;
+      or_polymul(c, t, ai, sp, as);
+      u64* bi = b + ((size_t)i * np + t) * n;
+      u64 gt = gad[(size_t)i * np + t];
+      for (int k = 0; k < n; ++k) {
+        u64 v = negm(as[k], q);
+        v = addm(v, from_signed(e[(size_t)i * n + k], q), q);
+        v = addm(v, mulm(gt, s2[k], q), q);
+        bi[k] = v;
+      }
+      free(sp); free(s2); free(as);
+    }
+  }
+}
+
+/* Tensor product of two ciphertexts over Q: (a0, a1) x (b0, b1) =
+ * (a0 b0, a0 b1 + a1 b0, a1 b1), which decrypts under (1, s, s^2).
+ * x, y: [2][L][N]; out: [3][L][N]; all coefficient form. */
+void or_tensor(void* p, const u64* x, const u64* y, u64* out) {
+  octx* c = (octx*)p;
+  int n = c->n, L = c->L;
+#pragma omp parallel for schedule(dynamic)
+  for (int t = 0; t < L; ++t) {
+    u64 q = c->primes[t];
+    u64* m = (u64*)malloc(sizeof(u64) * n);
+    const u64 *x0 = x + (size_t)t * n, *x1 = x + ((size_t)L + t) * n;
+    const u64 *y0 = y + (size_t)t * n, *y1 = y + ((size_t)L + t) * n;
+    u64 *d0 = out + (size_t)t * n, *d1 = out + ((size_t)L + t) * n, *d2 = out + ((size_t)2 * L + t) * n;
+    or_polymul(c, t, x0, y0, d0);
+    or_polymul(c, t, x0, y1, d1);
+    or_polymul(c, t, x1, y0, m);
+    for (int k = 0; k < n; ++k) d1[k] = addm(d1[k], m[k], q);
+    or_polymul(c, t, x1, y1, d2);
+    free(m);
+  }
+}
+
+/* Relinearise a three-component ciphertext d = (d0, d1, d2) [3][L][N]:
+ * (u0, u1) = key-switch inner product of d2 with (kb, ka) (no automorphism);
+ * out = (d0 + ModDown(u0), d1 + ModDown(u1))  [2][L][N]. */
+void or_relin(void* p, const u64* d, const u64* kb, const u64* ka, u64* out) {
+  octx* c = (octx*)p;
+  int n = c->n, L = c->L, np = L + c->K;
+  size_t poly = (size_t)np * n, ptw = (size_t)L * n;
+  u64* u = (u64*)malloc(sizeof(u64) * 2 * poly);
+  u64* w = (u64*)malloc(sizeof(u64) * ptw);
+  or_ks_inner(c, d + 2 * ptw, 1, kb, ka, u);
+  for (int h = 0; h < 2; ++h) {
+    or_moddown(c, u + (size_t)h * poly, w);
+    for (int t = 0; t < L; ++t) {
+      u64 q = c->primes[t];
+      for (int k = 0; k < n; ++k) {
+        size_t o = (size_t)t * n + k;
+        out[(size_t)h * ptw + o] = addm(d[(size_t)h * ptw + o], w[o], q);
+      }
+    }
+  }
+  free(u); free(w);
+}
+
+/* acc = sum_{b<B} ct[b] x qrot[b] for one giant index g, three components.
+ * qrot_hat: [B][2][L][N] transform domain; cts_g: [B][2][L][N] coefficient
+ * form; out: [3][L][N] coefficient form.  Formed in the transform domain
+ * (exact: the transform is linear and multiplicative). */
+static void mac_group_ct(octx* c, int B, const u64* qrot_hat, const u64* cts_g, u64* out) {
+  int n = c->n, L = c->L;
+  size_t ctw = (size_t)2 * L * n;
+#pragma omp parallel for schedule(dynamic)
+  for (int t = 0; t < L; ++t) {
+    u64 q = c->primes[t];
+    u64* acc0 = (u64*)calloc(n, sizeof(u64));
+    u64* acc1 = (u64*)calloc(n, sizeof(u64));
+    u64* acc2 = (u64*)calloc(n, sizeof(u64));
+    u64* y0 = (u64*)malloc(sizeof(u64) * n);
+    u64* y1 = (u64*)malloc(sizeof(u64) * n);
+    for (int b = 0; b < B; ++b) {
+      memcpy(y0, cts_g + (size_t)b * ctw + (size_t)t * n, sizeof(u64) * n);
+      memcpy(y1, cts_g + (size_t)b * ctw + ((size_t)L + t) * n, sizeof(u64) * n);
+      or_ntt(c, t, y0);
+      or_ntt(c, t, y1);
+      const u64* x0 = qrot_hat + (size_t)b * ctw + (size_t)t * n;
+      const u64* x1 = qrot_hat + (size_t)b * ctw + ((size_t)L + t) * n;
+      for (int k = 0; k < n; ++k) {
+        acc0[k] = addm(acc0[k], mulm(y0[k], x0[k], q), q);
+        acc1[k] = addm(acc1[k], addm(mulm(y0[k], x1[k], q), mulm(y1[k], x0[k], q), q), q);
+        acc2[k] = addm(acc2[k], mulm(y1[k], x1[k], q), q);
+      }
+    }
+    or_intt(c, t, acc0);
+    or_intt(c, t, acc1);
+    or_intt(c, t, acc2);
+    memcpy(out + (size_t)t * n, acc0, sizeof(u64) * n);
+    memcpy(out + ((size_t)L + t) * n, acc1, sizeof(u64) * n);
+    memcpy(out + ((size_t)2 * L + t) * n, acc2, sizeof(u64) * n);
+    free(acc0); free(acc1); free(acc2); free(y0); free(y1);
+  }
+}
+
+/* One block of the diagonal product against an encrypted block:
+ *   cts [G][B][2][L][N]  the encrypted pre-rotated diagonals ct[g][b]
+ *   rel_g = Relin(sum_b ct[g][b] x qrot[b])    (one relinearisation per g)
+ * then the giant sum of or_bsgs_block on the rel_g:
+ *   c0 = rel_0.c0 + sum_{g>=1} sigma_{gB}(rel_g.c0) + ModDown(sum_{g>=1} u0_g)
+ *   c1 = rel_0.c1 + ModDown(sum_{g>=1} u1_g). */
+void or_bsgs_block_ct(void* p, int B, int G, const u64* qrot, const u64* cts, const u64* gs,
+                      const u64* const* kbs, const u64* const* kas, const u64* rkb, const u64* rka, u64* out) {
+  octx* c = (octx*)p;
+  int n = c->n, L = c->L, np = L + c->K;
+  size_t ctw = (size_t)2 * L * n, ptw = (size_t)L * n, poly = (size_t)np * n;
+  u64* acc3 = (u64*)malloc(sizeof(u64) * 3 * ptw);
+  u64* rel = (u64*)malloc(sizeof(u64) * ctw);
+  u64* usum = (u64*)calloc(2 * poly, sizeof(u64));
+  u64* u = (u64*)malloc(sizeof(u64) * 2 * poly);
+  u64* tmp = (u64*)malloc(sizeof(u64) * n);
+  u64* qhat = (u64*)malloc(sizeof(u64) * ctw * B);
+  memcpy(qhat, qrot, sizeof(u64) * ctw * B);
+#pragma omp parallel for collapse(2) schedule(dynamic)
+  for (int b = 0; b < B; ++b)
+    for (int t = 0; t < 2 * L; ++t) or_ntt(c, t % L, qhat + (size_t)b * ctw + (size_t)t * n);
+  mac_group_ct(c, B, qhat, cts, acc3);
+  or_relin(c, acc3, rkb, rka, out); /* g = 0: no rotation */
+  for (int g = 1; g < G; ++g) {
+    mac_group_ct(c, B, qhat, cts + (size_t)g * B * ctw, acc3);
+    or_relin(c, acc3, rkb, rka, rel);
+    or_ks_inner(c, rel + (size_t)L * n, gs[g], kbs[g], kas[g], u);
+    for (int t = 0; t < np; ++t) {
+      u64 q = c->primes[t];
+      for (int h = 0; h < 2; ++h)
+        for (int k = 0; k < n; ++k) {
+          size_t o = (size_t)h * poly + (size_t)t * n + k;
+          usum[o] = addm(usum[o], u[o], q);
+        }
+    }
+    for (int t = 0; t < L; ++t) {
+      u64 q = c->primes[t];
+      automorph_poly(n, gs[g], q, rel + (size_t)t * n, tmp);
+      for (int k = 0; k < n; ++k) out[(size_t)t * n + k] = addm(out[(size_t)t * n + k], tmp[k], q);
+    }
+  }
+  if (G > 1) {
+    u64* d = (u64*)malloc(sizeof(u64) * ptw);
+    for (int h = 0; h < 2; ++h) {
+      or_moddown(c, usum + (size_t)h * poly, d);
+      for (int t = 0; t < L; ++t) {
+        u64 q = c->primes[t];
+        for (int k = 0; k < n; ++k) {
+          size_t o = ((size_t)h * L + t) * n + k;
+          out[o] = addm(out[o], d[(size_t)t * n + k], q);
+        }
+      }
+    }
+    free(d);
+  }
+  free(acc3); free(rel); free(usum); free(u); free(tmp); free(qhat);
+}

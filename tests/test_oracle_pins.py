@@ -558,3 +558,113 @@ def test_dropped_ciphertext_decrypts_and_rotates(small4):
     key = lo.keygen(s, 5, restrict(par, L_low, a)[:lp.dnum], e[:lp.dnum])
     z = ckks.decode_residues(lo.decrypt(lo.rotate(ct_low, 5, key), s), lp, 40)
     assert np.max(np.abs(z - np.roll(v, -5))) < 1e-6
+
+
+# ----------------------------------------------------------------------------
+# encrypted database: tensor product, relinearisation key, relinearisation,
+# ct x ct diagonal scoring
+# ----------------------------------------------------------------------------
+def negacyclic_square_int(s):
+    """s^2 mod X^N + 1 over the integers (s small), by the definition."""
+    n = len(s)
+    full = np.convolve(s.astype(np.int64), s.astype(np.int64))  # degree 2N-2
+    out = full[:n].copy()
+    out[:n - 1] -= full[n:]
+    return out
+
+
+def relin_key(orc, s, wid):
+    par = orc.par
+    a = gen.uniform_residues(gen.rng(wid, gen.STREAM_KEY_A, 0), par.primes, par.dnum, par.n)
+    e = gen.rounded_gaussian(gen.rng(wid, gen.STREAM_KEY_E, 0), (par.dnum, par.n))
+    return orc.keygen_relin(s, a, e), e
+
+
+def test_tensor_decrypts_to_product_of_decryptions(small):
+    """(c0 + c1 s)(d0 + d1 s) = c0 d0 + (c0 d1 + c1 d0) s + c1 d1 s^2 exactly mod Q: the
+    tensor's three components decrypted under (1, s, s^2) equal the ring product of the two
+    decryptions (a dropped or misplaced cross term breaks the equality)."""
+    par, orc = small
+    s = gen.ternary_secret(gen.rng(30, gen.STREAM_SECRET), par.n)
+    g = np.random.default_rng(30)
+    x = np.stack([np.stack([g.integers(0, q, par.n, dtype=np.uint64) for q in par.q]) for _ in range(2)])
+    y = np.stack([np.stack([g.integers(0, q, par.n, dtype=np.uint64) for q in par.q]) for _ in range(2)])
+    d = orc.tensor(x, y)
+    lhs = orc.decrypt3(d, s)
+    mx, my = orc.decrypt(x, s), orc.decrypt(y, s)
+    for t, q in enumerate(par.q):
+        assert np.array_equal(lhs[t], orc.polymul(t, mx[t], my[t]))
+    # and the tensor's first component is the plain product c0 d0 (schoolbook at a tiny ring)
+    tp = ckks.Params(logn=5, L=2, K=1)
+    to = ckks.Oracle(tp)
+    xs = np.stack([np.stack([g.integers(0, q, tp.n, dtype=np.uint64) for q in tp.q]) for _ in range(2)])
+    ys = np.stack([np.stack([g.integers(0, q, tp.n, dtype=np.uint64) for q in tp.q]) for _ in range(2)])
+    ds = to.tensor(xs, ys)
+    for t, q in enumerate(tp.q):
+        assert np.array_equal(ds[0, t], schoolbook_negacyclic(xs[0, t], ys[0, t], q))
+        cross = (schoolbook_negacyclic(xs[0, t], ys[1, t], q).astype(object)
+                 + schoolbook_negacyclic(xs[1, t], ys[0, t], q).astype(object)) % q
+        assert np.array_equal(ds[1, t], cross.astype(np.uint64))
+        assert np.array_equal(ds[2, t], schoolbook_negacyclic(xs[1, t], ys[1, t], q))
+
+
+def test_relin_key_is_gadget_times_s_squared(small4):
+    """b_i + a_i s - gadget_i s^2 = e_i on every prime of Q u P, with s^2 formed here over
+    the integers (not by the oracle)."""
+    par, orc = small4
+    s = gen.ternary_secret(gen.rng(31, gen.STREAM_SECRET), par.n)
+    (b, a), e = relin_key(orc, s, 31)
+    s2 = negacyclic_square_int(s)
+    gad = ckks.gadget_table(par)
+    for i in range(par.dnum):
+        for t, q in enumerate(par.primes):
+            st = [int(v) % q for v in s]
+            sa = schoolbook_negacyclic(a[i, t], np.array(st, dtype=np.uint64), q) if par.n <= 64 else \
+                orc.polymul(t, a[i, t], np.array(st, dtype=np.uint64))
+            lhs = (b[i, t].astype(object) + sa.astype(object)
+                   - int(gad[i, t]) * np.array([int(v) % q for v in s2], dtype=object)) % q
+            assert np.array_equal(lhs, np.array([int(v) % q for v in e[i]], dtype=object)), (i, t)
+
+
+def test_relin_preserves_the_decryption(small4):
+    """decrypt(Relin(d)) = decrypt3(d) + small key-switch noise: the centred difference is far
+    below the product scale (a wrong key, sign or missing ModDown leaves ~Q)."""
+    par, orc = small4
+    s = gen.ternary_secret(gen.rng(32, gen.STREAM_SECRET), par.n)
+    rlk, _ = relin_key(orc, s, 32)
+    v1 = gen.gaussian_unit_rows(gen.rng(32, gen.STREAM_QUERY), 1, par.slots)[0]
+    v2 = gen.gaussian_unit_rows(gen.rng(32, gen.STREAM_DB), 1, par.slots)[0]
+    x = enc(orc, v1, s, wid=32)
+    y = enc(orc, v2, s, wid=33)
+    d = orc.tensor(x, y)
+    r = orc.relin(d, rlk)
+    diff = np.stack([((orc.decrypt(r, s)[t].astype(object) - orc.decrypt3(d, s)[t].astype(object)) % q)
+                     .astype(np.uint64) for t, q in enumerate(par.q)])
+    assert max(abs(v) for v in ckks.crt_centered(diff, par.q)) < 2 ** 40
+    z = ckks.decode_residues(orc.decrypt(r, s), par, 80)
+    assert np.max(np.abs(z - v1 * v2)) < 1e-6
+
+
+@pytest.mark.parametrize("B", [1, 4])
+def test_encrypted_block_scores_match_float64(small, B):
+    """Encrypted pre-rotated diagonals: per giant index the tensor sum, one relinearisation,
+    then the giant sum; decrypted scores are the float64 inner products."""
+    par, orc = small
+    d, rows = 16, 300
+    G = d // B
+    s = gen.ternary_secret(gen.rng(34, gen.STREAM_SECRET), par.n)
+    X = gen.gaussian_unit_rows(gen.rng(34, gen.STREAM_DB), rows, d)
+    q = gen.gaussian_unit_rows(gen.rng(34, gen.STREAM_QUERY), 1, d)[0]
+    ct = enc(orc, ckks.replicate(q, par.slots), s, wid=34)
+    keys = keyset(orc, s, ckks.steps_for_bsgs(d, B), wid=34)
+    rlk, _ = relin_key(orc, s, 34)
+    coeffs = ckks.layout_b_coeffs(X, par, d, B)
+    cts = np.empty((G, B, 2, par.L, par.n), dtype=np.uint64)
+    for j, m in enumerate(coeffs):
+        a = gen.uniform_residues(gen.rng(34, gen.STREAM_ENC_A, 1 + j), par.q, 1, par.n)[0]
+        e = gen.rounded_gaussian(gen.rng(34, gen.STREAM_ENC_E, 1 + j), par.n)
+        cts[j // B, j % B] = orc.encrypt(m, a, e, s)
+    out = orc.bsgs_block_ct(orc.baby_rotations(ct, B, keys), cts, B, G, keys, rlk)
+    z = dec(orc, out, s, 80)
+    assert np.max(np.abs(z[:rows] - X @ q)) < 1e-4
+    assert np.max(np.abs(z[rows:])) < 1e-4
