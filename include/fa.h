@@ -62,14 +62,15 @@ enum {
   FA_E_HIP = -5    /* HIP runtime / launch error                             */
 };
 
-enum { FA_LAYOUT_ROW = 0, FA_LAYOUT_DIAG = 1 };
+enum { FA_LAYOUT_ROW = 0, FA_LAYOUT_DIAG = 1, FA_LAYOUT_DIAG_ENC = 2 };
 enum {
   FA_OP_SCORE = 0,
   FA_OP_PROJECT = 1,
   FA_OP_ROTATE_SUM = 2,
   FA_OP_ROTATE = 3,
   FA_OP_PREPARE = 4,
-  FA_OP_SCORE_PREPARED = 5
+  FA_OP_SCORE_PREPARED = 5,
+  FA_OP_SCORE_ENC = 6
 };
 
 typedef struct fa_ctx fa_ctx;
@@ -127,12 +128,29 @@ int fa_keygen(fa_ctx* ctx, const int64_t* s, const int32_t* steps, int n_steps, 
 /* 1 if a key for left rotation by `step` exists, else 0. */
 int fa_has_key(const fa_ctx* ctx, int step);
 
+/* Relinearisation key for ct x ct products (the encrypted-database scoring of
+ * Section 2, "Measured prototype vs. deployment", where the stored rows are
+ * ciphertexts): the rotation-key form with s^2 in place of sigma(s),
+ *   b_i = -a_i*s + e_i + (P*Qhat_i*[Qhat_i^-1]_{Q_i}) * s^2  over Q u P,
+ * with the same host inputs as one step of fa_keygen (a [dnum][L+K][N],
+ * e [dnum][N]).  Replaces an existing relinearisation key; synchronous. */
+int fa_keygen_relin(fa_ctx* ctx, const int64_t* s, const uint64_t* a, const int64_t* e);
+/* 1 if the relinearisation key exists, else 0. */
+int fa_has_relin_key(const fa_ctx* ctx);
+
 /* Secret-key encryption (the query is encrypted by its owner): host inputs
  *   m [N] integer plaintext coefficients (|m| < 2^62), a [L][N] uniform
  *   residues, e [N] noise; s is the secret given to fa_keygen (or set by
  *   fa_set_secret).  Writes c1 = a, c0 = -a*s + e + m  into ct (device). */
 int fa_set_secret(fa_ctx* ctx, const int64_t* s);
 int fa_encrypt(fa_ctx* ctx, const int64_t* m, const uint64_t* a, const int64_t* e, void* ct, void* stream);
+/* Encrypts n_pts device plaintexts (as written by fa_encode_db_block /
+ * fa_encode_db_block_int, [n_pts][L][N]) into cts (device, [n_pts][2][L][N]):
+ * ct_j = (-a_j*s + e_j + pt_j, a_j) with host a [n_pts][L][N] residues and
+ * e [n_pts][N] noise (|e| <= 1024).  This is how a data owner enrolls an
+ * encrypted block (FA_LAYOUT_DIAG_ENC).  Synchronous on the stream. */
+int fa_encrypt_pts(fa_ctx* ctx, const void* pts, int n_pts, const uint64_t* a, const int64_t* e, void* cts,
+                   void* stream);
 /* m' = c0 + c1*s, coefficient form, host out [L][N] residues in [0, q_i).
  * Synchronous with respect to `stream`. */
 int fa_decrypt(fa_ctx* ctx, const void* ct, uint64_t* out, void* stream);
@@ -174,13 +192,19 @@ int fa_encode_db_block_int(fa_ctx* ctx, const int64_t* coeffs, int n_pts, void* 
 /* ---- server: scoring ---------------------------------------------------- */
 
 /* Device workspace needed by an operation (bytes).  op = FA_OP_SCORE with
- * layout FA_LAYOUT_DIAG: n_blocks, d, baby_step as passed to fa_score_block;
+ * layout FA_LAYOUT_DIAG (FA_OP_SCORE_ENC with FA_LAYOUT_DIAG_ENC): n_blocks,
+ * d, baby_step as passed to fa_score_block;
  * FA_OP_PROJECT: n_blocks = 1, d = r; FA_OP_ROTATE_SUM / FA_OP_ROTATE: n_blocks
  * = number of ciphertexts. */
 size_t fa_workspace_bytes(const fa_ctx* ctx, int op, int n_blocks, int d, int baby_step);
 
 /* Score one encrypted query q (device ciphertext, slot s = query[s mod d])
  * against n_blocks resident blocks (device pointers blocks[0..n_blocks-1]).
+ *   FA_LAYOUT_DIAG_ENC: as FA_LAYOUT_DIAG with every block holding d
+ *   ciphertexts ([d][2][L][N], fa_encrypt_pts of a diagonal block): acc_g is
+ *   the three-component tensor sum over b, relinearised once per (block, g)
+ *   (lazy relinearisation), before the same giant steps.  Needs the
+ *   relinearisation key as well.
  *   FA_LAYOUT_DIAG (Section 3.1 diagonal method, baby step B = baby_step,
  *   G = d/B giant steps): each block holds d pre-rotated plaintexts from
  *   fa_encode_db_block; out receives n_blocks ciphertexts; slot i of output

@@ -267,6 +267,7 @@ void fa_ctx_destroy(fa_ctx* c) {
   (void)hipFree(c->d_md_hat);
   (void)hipFree(c->d_s);
   for (auto& kv : c->keys) (void)hipFree(kv.second);
+  (void)hipFree(c->d_rlk);
   for (auto& e : c->ev)
     if (e) (void)hipEventDestroy(e);
   for (int i = 0; i < c->n_aux; ++i) {
@@ -445,19 +446,23 @@ int fa_ctx_create_level(const fa_ctx* parent, uint32_t L_low, fa_ctx** out) {
   auto limb_src = [&](int t) { return t < (int)L_low ? t : parent->L + (t - (int)L_low); };
   for (int t = 0; t < c->np && e == hipSuccess; ++t)
     e = hipMemcpy(c->d_s + (size_t)t * n, parent->d_s + (size_t)limb_src(t) * n, n * 8, hipMemcpyDeviceToDevice);
-  for (auto& kv : parent->keys) {
+  // every key (rotations and relinearisation) restricted the same way
+  std::vector<std::pair<const double*, double**>> todo;
+  for (auto& kv : parent->keys) todo.push_back({kv.second, &c->keys[kv.first]});
+  if (parent->d_rlk) todo.push_back({parent->d_rlk, &c->d_rlk});
+  for (auto& kt : todo) {
     if (e != hipSuccess) break;
     double* key = nullptr;
     if ((rc = dev_alloc(&key, (size_t)c->dnum * 2 * c->np * n))) {
       fa_ctx_destroy(c);
       return rc;
     }
-    c->keys[kv.first] = key;
+    *kt.second = key;
     for (int i = 0; i < c->dnum && e == hipSuccess; ++i)
       for (int h = 0; h < 2 && e == hipSuccess; ++h)
         for (int t = 0; t < c->np && e == hipSuccess; ++t)
           e = hipMemcpy(key + (((size_t)i * 2 + h) * c->np + t) * n,
-                        kv.second + (((size_t)i * 2 + h) * parent->np + limb_src(t)) * n, n * 8,
+                        kt.first + (((size_t)i * 2 + h) * parent->np + limb_src(t)) * n, n * 8,
                         hipMemcpyDeviceToDevice);
   }
   if (e != hipSuccess) {
@@ -566,6 +571,44 @@ int fa_keygen(fa_ctx* c, const int64_t* s, const int32_t* steps, int n_steps, co
 
 int fa_has_key(const fa_ctx* c, int step) { return c && c->keys.count(step) ? 1 : 0; }
 
+int fa_keygen_relin(fa_ctx* c, const int64_t* s, const uint64_t* a, const int64_t* e) {
+  if (!c || !s || !a || !e) return fail(FA_E_INVAL, "fa_keygen_relin: null argument");
+  int rc = fa_set_secret(c, s);
+  if (rc) return rc;
+  const size_t n = c->n, np = c->np, dnum = c->dnum;
+  if (!c->d_rlk && (rc = dev_alloc(&c->d_rlk, dnum * 2 * np * n))) return rc;
+  double* key = c->d_rlk;
+  uint64_t* du = nullptr;
+  int64_t* de = nullptr;
+  double* den = nullptr;
+  if ((rc = dev_alloc(&du, dnum * np * n)) || (rc = dev_alloc(&de, dnum * n)) ||
+      (rc = dev_alloc(&den, dnum * np * n))) {
+    (void)hipFree(du);
+    (void)hipFree(de);
+    return rc;
+  }
+  hipError_t he = hipMemcpy(du, a, dnum * np * n * 8, hipMemcpyHostToDevice);
+  if (he == hipSuccess) he = hipMemcpy(de, e, dnum * n * 8, hipMemcpyHostToDevice);
+  if (he != hipSuccess) {
+    rc = fail(FA_E_HIP, "fa_keygen_relin upload: %s", hipGetErrorString(he));
+  } else {
+    for (size_t i = 0; i < dnum; ++i) fa::u64_to_res(du + i * np * n, np * n, key + (i * 2 + 1) * np * n, 0);
+    for (size_t i = 0; i < dnum; ++i) fa::ntt_fwd_strided(c, key + (i * 2 + 1) * np * n, n, (int)np, (int)np, 0, 0);
+    fa::int_to_res(c, de, (int)dnum, (int)np, den, 0);
+    fa::ntt_fwd_strided(c, den, n, (int)(dnum * np), (int)np, 0, 0);
+    fa::keygen_combine(c, key, den, 0u, 0);  // gal 0: gadget times s^2
+    rc = check_launch("fa_keygen_relin");
+    if (!rc && (he = hipDeviceSynchronize()) != hipSuccess) rc = fail(FA_E_HIP, "fa_keygen_relin: %s", hipGetErrorString(he));
+  }
+  (void)hipFree(du);
+  (void)hipFree(de);
+  (void)hipFree(den);
+  return rc;
+}
+
+int fa_has_relin_key(const fa_ctx* c) { return c && c->d_rlk ? 1 : 0; }
+
+
 int fa_encrypt(fa_ctx* c, const int64_t* m, const uint64_t* a, const int64_t* e, void* ct, void* stream) {
   if (!c || !m || !a || !e || !ct) return fail(FA_E_INVAL, "fa_encrypt: null argument");
   hipStream_t s = (hipStream_t)stream;
@@ -598,6 +641,53 @@ int fa_encrypt(fa_ctx* c, const int64_t* m, const uint64_t* a, const int64_t* e,
   (void)hipFree(dm);
   (void)hipFree(dv);
   return FA_OK;
+}
+
+int fa_encrypt_pts(fa_ctx* c, const void* pts, int n_pts, const uint64_t* a, const int64_t* e, void* cts,
+                   void* stream) {
+  if (!c || !pts || !a || !e || !cts) return fail(FA_E_INVAL, "fa_encrypt_pts: null argument");
+  if (n_pts < 1) return fail(FA_E_SHAPE, "n_pts must be positive");
+  hipStream_t s = (hipStream_t)stream;
+  const size_t n = c->n, L = c->L;
+  for (size_t k = 0; k < (size_t)n_pts * n; ++k)
+    if (e[k] > 1024 || e[k] < -1024) return fail(FA_E_INVAL, "fa_encrypt_pts: noise coefficient %zu out of range", k);
+  const int chunk = 16;
+  uint64_t* du = nullptr;
+  int64_t* de = nullptr;
+  double* dv = nullptr;
+  int rc;
+  if ((rc = dev_alloc(&du, (size_t)chunk * L * n)) || (rc = dev_alloc(&de, (size_t)chunk * n)) ||
+      (rc = dev_alloc(&dv, (size_t)chunk * L * n))) {
+    (void)hipFree(du);
+    (void)hipFree(de);
+    return rc;
+  }
+  const double* dp = (const double*)pts;
+  double* dc = (double*)cts;
+  hipError_t he = hipSuccess;
+  for (int p0 = 0; p0 < n_pts && he == hipSuccess && !rc; p0 += chunk) {
+    const int m = std::min(chunk, n_pts - p0);
+    he = hipMemcpyAsync(du, a + (size_t)p0 * L * n, (size_t)m * L * n * 8, hipMemcpyHostToDevice, s);
+    if (he == hipSuccess) he = hipMemcpyAsync(de, e + (size_t)p0 * n, (size_t)m * n * 8, hipMemcpyHostToDevice, s);
+    if (he != hipSuccess) break;
+    // v = NTT(e) + m (the plaintexts are already in NTT form); c1 = NTT(a); c0 = -c1 s + v
+    fa::int_to_res(c, de, m, (int)L, dv, s);
+    fa::ntt_fwd_strided(c, dv, n, m * (int)L, (int)L, 0, s);
+    fa::add_limbs(c, dv, dp + (size_t)p0 * L * n, m * (int)L, (int)L, s);
+    for (int j = 0; j < m; ++j) {
+      double* ct = dc + (size_t)(p0 + j) * 2 * L * n;
+      fa::u64_to_res(du + (size_t)j * L * n, L * n, ct + L * n, s);
+      fa::ntt_fwd_strided(c, ct + L * n, n, (int)L, (int)L, 0, s);
+      fa::enc_combine(c, ct, dv + (size_t)j * L * n, s);
+    }
+    rc = check_launch("fa_encrypt_pts");
+    if (!rc) he = hipStreamSynchronize(s);
+  }
+  (void)hipFree(du);
+  (void)hipFree(de);
+  (void)hipFree(dv);
+  if (!rc && he != hipSuccess) rc = fail(FA_E_HIP, "fa_encrypt_pts: %s", hipGetErrorString(he));
+  return rc;
 }
 
 static int export_polys(fa_ctx* c, const double* src, int n_polys, uint64_t* out, hipStream_t s, bool decrypt) {
@@ -1002,13 +1092,14 @@ static void moddown_polys(fa_ctx* c, double* u, int count, double* conv, const d
 // goes through u (per rotation [2][np][N]); the ciphertext-prime part is formed
 // inside the finishing kernel.  conv: per rotation [2][L][N] scratch.
 static void ks_moddown(fa_ctx* c, const fa::KsItem* ks, int count, const double* const* c0s, double* const* outs,
-                       double* u, double* conv, hipStream_t s) {
+                       double* u, double* conv, hipStream_t s, const double* const* b1s = nullptr) {
   const size_t n = c->n, L = c->L;
   fa::ks_inner(c, ks, count, false, s, c->L);
   moddown_polys(c, u, 2 * count, conv, nullptr, nullptr, nullptr, s, false);
   std::vector<fa::MdKsItem> it(count);
   for (int j = 0; j < count; ++j)
-    it[j] = {conv + (size_t)2 * j * L * n, ks[j].ext, ks[j].c1, ks[j].key, c0s[j], outs[j], ks[j].gal};
+    it[j] = {conv + (size_t)2 * j * L * n, ks[j].ext, ks[j].c1, ks[j].key, c0s[j], b1s ? b1s[j] : nullptr, outs[j],
+             ks[j].gal};
   fa::moddown_ks(c, it.data(), count, s);
 }
 
@@ -1093,6 +1184,42 @@ static int rotate_batch(fa_ctx* c, const double* cts, int nb, int step, double* 
   ks_moddown(c, ks.data(), nb, c0s.data(), douts.data(), u, conv, s);
   ar.used = mark;
   return check_launch("rotate_batch");
+}
+
+// Relinearisation of `count` three-component ciphertexts d [count][3][L][N]:
+// out[j] = (d0 + ModDown(u0), d1 + ModDown(u1)) with (u0, u1) the key-switch
+// inner product of d2 with the relinearisation key (no automorphism), in
+// batches of up to kRotBatch; out [count][2][L][N].
+static size_t relin_ws(const fa_ctx* c) { return rotate_ws(c, kRotBatch); }
+static int relin_batch(fa_ctx* c, const double* d, int count, double* out, Arena& ar, hipStream_t s) {
+  const size_t n = c->n, L = c->L, np = c->np, dn = c->dnum;
+  if (!c->d_rlk) return fail(FA_E_NOKEY, "no relinearisation key (fa_keygen_relin)");
+  const size_t mark = ar.used;
+  const int nbm = std::min(count, kRotBatch);
+  double* y = ar.take((size_t)nbm * L * n);
+  double* ext = ar.take((size_t)nbm * dn * np * n);
+  double* u = ar.take((size_t)nbm * 2 * np * n);
+  double* conv = ar.take((size_t)nbm * 2 * L * n);
+  if (!y || !ext || !u || !conv) return fail(FA_E_NOMEM, "workspace too small for relinearisation");
+  const size_t d3 = 3 * L * n, ctw = 2 * L * n;
+  for (int j0 = 0; j0 < count; j0 += nbm) {
+    const int nb = std::min(nbm, count - j0);
+    // ModUp of the s^2 components: "ciphertexts" at d + 2LN with stride 3LN read as (., c1)
+    modup(c, d + (size_t)j0 * d3 + L * n, d3, nb, y, L * n, ext, dn * np * n, s);
+    std::vector<fa::KsItem> ks(nb);
+    std::vector<const double*> c0s(nb), b1s(nb);
+    std::vector<double*> outs(nb);
+    for (int j = 0; j < nb; ++j) {
+      const double* dj = d + (size_t)(j0 + j) * d3;
+      ks[j] = {ext + (size_t)j * dn * np * n, dj + 2 * L * n, c->d_rlk, u + (size_t)j * 2 * np * n, nullptr, 1u};
+      c0s[j] = dj;
+      b1s[j] = dj + L * n;
+      outs[j] = out + (size_t)(j0 + j) * ctw;
+    }
+    ks_moddown(c, ks.data(), nb, c0s.data(), outs.data(), u, conv, s, b1s.data());
+  }
+  ar.used = mark;
+  return check_launch("relinearise");
 }
 
 // Baby rotations qrot[b-1] = Rotate(q, b), b = 1..B-1: one shared decomposition
@@ -1237,6 +1364,39 @@ static int score_diag(fa_ctx* c, const double* q, const double* const* blocks, i
   return mac_giant_phase(c, &q, &qq, 1, blocks, nb, d, B, &out, ar, s);
 }
 
+// Encrypted blocks (ct x ct): baby rotations, the tensor multiply-accumulate
+// (three components per (block, giant)), one relinearisation per (block,
+// giant), then the giant steps of the plaintext path on the relinearised sums.
+static size_t score_enc_ws(const fa_ctx* c, int nb, int d, int B) {
+  const size_t G = d / B, ln = (size_t)c->L * c->n;
+  return baby_ws(c, B) + rup(qrot_words(c, B)) + rup((size_t)nb * G * 3 * ln) + giant_ws(c, nb, d, B) +
+         relin_ws(c);
+}
+static int score_diag_enc(fa_ctx* c, const double* q, const double* const* blocks, int nb, int d, int B,
+                          double* out, Arena& ar, hipStream_t s) {
+  const size_t ln = (size_t)c->L * c->n;
+  const int G = d / B;
+  if (!c->d_rlk) return fail(FA_E_NOKEY, "no relinearisation key (fa_keygen_relin)");
+  int rc = check_giant_keys(c, d, B);
+  if (rc) return rc;
+  double* qrot = ar.take(qrot_words(c, B));
+  double* acc3 = ar.take((size_t)nb * G * 3 * ln);
+  double* acc = ar.take((size_t)nb * G * 2 * ln);
+  if (!qrot || !acc3 || !acc) return fail(FA_E_NOMEM, "workspace too small for score_block");
+  if (c->prof) HIPCHK(hipEventRecord(c->ev[0], s));
+  if ((rc = baby_phase(c, q, B, qrot, ar, s))) return rc;
+  if (c->prof) HIPCHK(hipEventRecord(c->ev[1], s));
+  fa::mac_diag_ct(c, q, qrot, blocks, nb, B, G, acc3, s);
+  if (c->prof) HIPCHK(hipEventRecord(c->ev[2], s));
+  if ((rc = relin_batch(c, acc3, nb * G, acc, ar, s))) return rc;
+  if ((rc = giant_phase(c, acc, nb, G, B, out, ar, s))) return rc;
+  if (c->prof) {
+    HIPCHK(hipEventRecord(c->ev[3], s));
+    c->prof_done = true;
+  }
+  return check_launch("score_block(encrypted)");
+}
+
 extern "C" {
 
 size_t fa_workspace_bytes(const fa_ctx* c, int op, int n_blocks, int d, int baby_step) {
@@ -1257,6 +1417,9 @@ size_t fa_workspace_bytes(const fa_ctx* c, int op, int n_blocks, int d, int baby
     case FA_OP_SCORE_PREPARED:
       if (baby_step < 1 || d < baby_step) return 0;
       return giant_ws(c, std::max(1, n_blocks), d, baby_step);
+    case FA_OP_SCORE_ENC:
+      if (baby_step < 1 || d < baby_step) return 0;
+      return score_enc_ws(c, std::max(1, n_blocks), d, baby_step);
     default:
       return 0;
   }
@@ -1333,13 +1496,17 @@ int fa_score_block(fa_ctx* c, const void* q, const void* const* blocks, int n_bl
     fa::mul_plain(c, (const double*)q, (const double* const*)blocks, n_blocks, (double*)out, s);
     return check_launch("fa_score_block(row)");
   }
-  if (layout != FA_LAYOUT_DIAG) return fail(FA_E_INVAL, "unknown layout %d", layout);
+  if (layout != FA_LAYOUT_DIAG && layout != FA_LAYOUT_DIAG_ENC) return fail(FA_E_INVAL, "unknown layout %d", layout);
   const int S = c->n / 2;
   if (d < 1 || (d & (d - 1)) || d > S) return fail(FA_E_SHAPE, "d=%d must be a power of two <= N/2", d);
   if (baby_step < 1 || d % baby_step) return fail(FA_E_INVAL, "baby_step %d must divide d=%d", baby_step, d);
-  const size_t need = score_ws(c, n_blocks, d, baby_step);
+  const bool enc = layout == FA_LAYOUT_DIAG_ENC;
+  const size_t need = enc ? score_enc_ws(c, n_blocks, d, baby_step) : score_ws(c, n_blocks, d, baby_step);
   if (!ws || ws_bytes < need) return fail(FA_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
   Arena ar{(char*)ws, ws_bytes, 0};
+  if (enc)
+    return score_diag_enc(c, (const double*)q, (const double* const*)blocks, n_blocks, d, baby_step, (double*)out, ar,
+                          s);
   return score_diag(c, (const double*)q, (const double* const*)blocks, n_blocks, d, baby_step, (double*)out, ar, s);
 }
 

@@ -62,6 +62,7 @@ struct fa_ctx {
   // secret (NTT form over every prime), keys
   double* d_s = nullptr;          // [np][N]
   std::map<int, double*> keys;    // step -> [dnum][2][np][N] (b, a), NTT form
+  double* d_rlk = nullptr;        // relinearisation key (s^2 -> s), same layout
   std::vector<uint64_t> p_mod_q;  // [L] P mod q_t (gadget)
   // phase timing (fa_profile)
   bool prof = false, prof_done = false;
@@ -124,7 +125,7 @@ void moddown(const fa_ctx* c, const MdItem* items, int count, hipStream_t s, boo
 
 // ModDown finish of rotations whose key-switch sum on the ciphertext primes is
 // formed in the same kernel (ks_inner then only covers the special primes):
-// out = (sigma(c0) + (u_Q,0 - conv0^) P^-1, (u_Q,1 - conv1^) P^-1) with
+// out = (sigma(c0) + (u_Q,0 - conv0^) P^-1, b1 + (u_Q,1 - conv1^) P^-1) with
 // u_Q,h = sum_i sigma(ext_i) key[i][h] and conv (from moddown with pass_b false)
 // holding the first pass of Conv_{P->Q} of both polynomials.
 struct MdKsItem {
@@ -133,6 +134,7 @@ struct MdKsItem {
   const double* c1;    // [L][N] the digits' own limbs
   const double* key;   // [dnum][2][np][N]
   const double* c0;    // [L][N]
+  const double* b1;    // [L][N] or null: added to the second output polynomial
   double* out;         // [2][L][N]
   uint32_t gal;
 };
@@ -165,6 +167,11 @@ void giant_ks(const fa_ctx* c, const double* ext, const double* acc, size_t astr
 void mac_diag(const fa_ctx* c, const double* const* q, const double* const* qrot, int nq,
               const double* const* blocks, int n_blocks, int B, int G, double* const* acc, hipStream_t s);
 
+// Encrypted blocks: acc[pair][3][L][N] = sum_b ct[blk][(g*B+b)] (x) rot_b, the
+// three components of the tensor product (rot_0 = q, rot_b = qrot[b-1]).
+void mac_diag_ct(const fa_ctx* c, const double* q, const double* qrot, const double* const* blocks, int n_blocks,
+                 int B, int G, double* acc, hipStream_t s);
+
 // out[w] = ct * pt[w] (both polys), w < count
 void mul_plain(const fa_ctx* c, const double* ct, const double* const* pts, int count, double* out, hipStream_t s);
 // dst[r] += src[r] for n_limbs limbs of N words, limb r over prime r % period
@@ -178,6 +185,7 @@ void u64_to_res(const uint64_t* src, size_t words, double* dst, hipStream_t s);
 void res_to_u64(const double* src, size_t words, uint64_t* dst, hipStream_t s);
 // keygen combine: for each digit i and prime t:
 //   b = -a*s + e + gad[i][t] * s[pi_g(k)]   (all NTT form); a in place already NTT
+// gal = 0 selects the relinearisation key: s^2 in place of s[pi_g(k)]
 void keygen_combine(const fa_ctx* c, double* key, const double* e_ntt, uint32_t gal, hipStream_t s);
 // encryption combine: c0[t] = -c1[t]*s[t] + v[t]
 void enc_combine(const fa_ctx* c, double* ct, const double* v, hipStream_t s);

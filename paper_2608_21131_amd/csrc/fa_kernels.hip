@@ -403,7 +403,8 @@ __global__ __launch_bounds__(256) void k_moddown_b(MdArgs args, const DevPrime* 
 // ModDown finish of a rotation with its key-switch sum on the ciphertext
 // primes formed in place: for limb t < L and the tile's words k,
 //   u_h[k] = sum_i sigma(ext_i)[k] * key_i[h][t][k]   (h = 0, 1; own limbs from c1)
-//   out0[k] = c0[pi(k)] + (u_0[k] - conv0^[k]) * P^-1,  out1[k] = (u_1[k] - conv1^[k]) * P^-1
+//   out0[k] = c0[pi(k)] + (u_0[k] - conv0^[k]) * P^-1,
+//   out1[k] = b1[k] + (u_1[k] - conv1^[k]) * P^-1       (b1 = 0 for a rotation)
 // where conv_h^ is the forward transform of Conv_{P->Q} finished here (pass B).
 // The sums never reach HBM; both polynomials of the rotation share one gather.
 struct MdKsArgs {
@@ -457,7 +458,8 @@ __global__ __launch_bounds__(256) void k_moddown_ks_b(MdKsArgs args, const DevPr
 #pragma unroll
   for (int j = 0; j < ROWS; ++j) {
     const int e = threadIdx.x + 256 * j;
-    const double r = mulc(u1[j] - sm[lds_row(e >> 8, e & 255)], pv, pvp, q);
+    double r = mulc(u1[j] - sm[lds_row(e >> 8, e & 255)], pv, pvp, q);
+    if (it.b1) r += it.b1[o + k0 + 256 * j];
     it.out[(size_t)L * n + o + k0 + 256 * j] = canon_full(r, q, qinv);
   }
 }
@@ -847,6 +849,87 @@ __global__ __launch_bounds__(256) void k_mac_diag(MacArgs args, const DevPrime* 
 }
 
 // ---------------------------------------------------------------------------
+// multiply-accumulate against an encrypted block (ct x ct, three components)
+//   acc[pair][0] += c0 q0,  acc[pair][1] += c0 q1 + c1 q0,  acc[pair][2] += c1 q1
+// with (c0, c1) = ct[blk][g*B+b] and (q0, q1) = rot_b.  One thread per
+// coefficient, NACC pairs per chunk; several chunks in one launch share the
+// rotated query through one XCD's L2 as in k_mac_diag.  A reduction every 4
+// steps keeps the lazy sums below 2^53 (the middle component gains two
+// products per step).
+// ---------------------------------------------------------------------------
+struct MacCtArgs {
+  const double* q0;
+  const double* qrot;
+  double* acc;  // [n_pairs][3][L][N]
+  const double* blk[FA_MAXBLK];
+  int n_pairs, pair0, B, logG, L;
+  int nchunk, ntile;
+};
+
+template <int NACC>
+__global__ __launch_bounds__(256) void k_mac_diag_ct(MacCtArgs args, const DevPrime* __restrict__ pr, int logn) {
+  unsigned tile = blockIdx.x, chunk = 0;
+  if (args.nchunk > 1) {
+    const unsigned j = blockIdx.x >> 3;
+    chunk = j % (unsigned)args.nchunk;
+    tile = (j / (unsigned)args.nchunk) * 8u + (blockIdx.x & 7u);
+    if (tile >= (unsigned)args.ntile) return;
+  }
+  const int n = 1 << logn;
+  const size_t ln = (size_t)args.L * n;
+  const size_t f = (size_t)tile * 256 + threadIdx.x;
+  const int t = (int)(f >> logn);
+  const double q = pr[t].q, qinv = pr[t].qinv;
+  const int pair0 = args.pair0 + (int)chunk * NACC;
+  const int last = args.n_pairs - 1;
+  const int G = 1 << args.logG;
+  const double* src[NACC];
+#pragma unroll
+  for (int i = 0; i < NACC; ++i) {
+    const int pair = min(pair0 + i, last);
+    src[i] = args.blk[pair >> args.logG] + (size_t)((pair & (G - 1)) * args.B) * 2 * ln + f;
+  }
+  double a0[NACC], a1[NACC], a2[NACC];
+#pragma unroll
+  for (int i = 0; i < NACC; ++i) a0[i] = a1[i] = a2[i] = 0.0;
+  for (int b = 0; b < args.B; ++b) {
+    const double* __restrict__ qb = b == 0 ? args.q0 : args.qrot + (size_t)(b - 1) * 2 * ln;
+    const double x0 = qb[f], x1 = qb[ln + f];
+    double p0[NACC], p1[NACC];
+#pragma unroll
+    for (int i = 0; i < NACC; ++i) {
+      p0[i] = __builtin_nontemporal_load(src[i] + (size_t)b * 2 * ln);
+      p1[i] = __builtin_nontemporal_load(src[i] + (size_t)b * 2 * ln + ln);
+    }
+    const double x0p = x0 * qinv, x1p = x1 * qinv;
+#pragma unroll
+    for (int i = 0; i < NACC; ++i) {
+      a0[i] += mulc(p0[i], x0, x0p, q);
+      a1[i] += mulc(p0[i], x1, x1p, q) + mulc(p1[i], x0, x0p, q);
+      a2[i] += mulc(p1[i], x1, x1p, q);
+    }
+    if ((b & 3) == 3) {
+#pragma unroll
+      for (int i = 0; i < NACC; ++i) {
+        a0[i] = reduce(a0[i], q, qinv);
+        a1[i] = reduce(a1[i], q, qinv);
+        a2[i] = reduce(a2[i], q, qinv);
+      }
+    }
+  }
+  const int cnt = min(NACC, args.n_pairs - pair0);
+#pragma unroll
+  for (int i = 0; i < NACC; ++i) {
+    if (i < cnt) {
+      double* o = args.acc + (size_t)(pair0 + i) * 3 * ln + f;
+      o[0] = canon_full(a0[i], q, qinv);
+      o[ln] = canon_full(a1[i], q, qinv);
+      o[2 * ln] = canon_full(a2[i], q, qinv);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // small element-wise kernels
 // ---------------------------------------------------------------------------
 #define FA_MAXPT 32
@@ -928,7 +1011,7 @@ __global__ __launch_bounds__(256) void k_keygen_combine(double* __restrict__ key
   const double gad = (t >= lo && t < hi) ? pr[t].pmod : 0.0;
   const double a = key[(((size_t)i * 2 + 1) * np + t) * n + k];
   const double st = s[(size_t)t * n + k];
-  const double sg = s[(size_t)t * n + perm((uint32_t)k, gal, logn)];
+  const double sg = gal == 0u ? mul(st, st, q, qinv) : s[(size_t)t * n + perm((uint32_t)k, gal, logn)];
   const double ev = e[((size_t)i * np + t) * n + k];
   const double v = -mul(a, st, q, qinv) + ev + mul(gad, sg, q, qinv);
   key[(((size_t)i * 2 + 0) * np + t) * n + k] = canon_full(v, q, qinv);
@@ -1293,6 +1376,44 @@ void mac_diag(const fa_ctx* c, const double* const* q, const double* const* qrot
       }
     }
     j0 += m;
+  }
+}
+
+template <int NACC>
+static void launch_mac_ct(MacCtArgs a, int nchunk, const fa_ctx* c, hipStream_t s) {
+  a.ntile = (int)((size_t)c->L * c->n / 256);
+  a.nchunk = nchunk;
+  const unsigned grid = nchunk == 1 ? (unsigned)a.ntile : 8u * nchunk * ((a.ntile + 7) / 8);
+  hipLaunchKernelGGL((k_mac_diag_ct<NACC>), dim3(grid), dim3(256), 0, s, a, c->d_pr, c->logn);
+}
+
+void mac_diag_ct(const fa_ctx* c, const double* q, const double* qrot, const double* const* blocks, int n_blocks,
+                 int B, int G, double* acc, hipStream_t s) {
+  int logG = 0;
+  while ((1 << logG) < G) ++logG;
+  const size_t ln = (size_t)c->L * c->n;
+  for (int b0 = 0; b0 < n_blocks; b0 += FA_MAXBLK) {
+    const int nb = n_blocks - b0 < FA_MAXBLK ? n_blocks - b0 : FA_MAXBLK;
+    MacCtArgs a;
+    a.q0 = q;
+    a.qrot = qrot;
+    a.acc = acc + (size_t)b0 * G * 3 * ln;
+    for (int i = 0; i < nb; ++i) a.blk[i] = blocks[b0 + i];
+    a.n_pairs = nb * G;
+    a.B = B;
+    a.logG = logG;
+    a.L = c->L;
+    for (int p0 = 0; p0 < a.n_pairs;) {
+      const int left = a.n_pairs - p0;
+      a.pair0 = p0;
+      if (left >= 16) {
+        launch_mac_ct<16>(a, left / 16, c, s);
+        p0 += (left / 16) * 16;
+      } else {
+        launch_mac_ct<8>(a, 1, c, s);
+        p0 += 8;
+      }
+    }
   }
 }
 

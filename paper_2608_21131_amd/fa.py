@@ -18,8 +18,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libfa.so")
 
 FA_OK, FA_E_INVAL, FA_E_SHAPE, FA_E_NOKEY, FA_E_NOMEM, FA_E_HIP = 0, -1, -2, -3, -4, -5
-LAYOUT_ROW, LAYOUT_DIAG = 0, 1
-OP_SCORE, OP_PROJECT, OP_ROTATE_SUM, OP_ROTATE, OP_PREPARE, OP_SCORE_PREPARED = 0, 1, 2, 3, 4, 5
+LAYOUT_ROW, LAYOUT_DIAG, LAYOUT_DIAG_ENC = 0, 1, 2
+OP_SCORE, OP_PROJECT, OP_ROTATE_SUM, OP_ROTATE, OP_PREPARE, OP_SCORE_PREPARED, OP_SCORE_ENC = 0, 1, 2, 3, 4, 5, 6
 
 _ERR_NAMES = {FA_E_INVAL: "FA_E_INVAL", FA_E_SHAPE: "FA_E_SHAPE", FA_E_NOKEY: "FA_E_NOKEY",
               FA_E_NOMEM: "FA_E_NOMEM", FA_E_HIP: "FA_E_HIP"}
@@ -78,6 +78,9 @@ SIGNATURES = {
     "fa_prepare_query": (ctypes.c_int, [_vp, _vp, ctypes.c_int, _vp, _vp, ctypes.c_size_t, _vp]),
     "fa_score_prepared": (ctypes.c_int, [_vp, _vp, _vp, ctypes.POINTER(_vp), ctypes.c_int, ctypes.c_int,
                                          ctypes.c_int, _vp, _vp, ctypes.c_size_t, _vp]),
+    "fa_keygen_relin": (ctypes.c_int, [_vp, _i64p, _u64p, _i64p]),
+    "fa_has_relin_key": (ctypes.c_int, [_vp]),
+    "fa_encrypt_pts": (ctypes.c_int, [_vp, _vp, ctypes.c_int, _u64p, _i64p, _vp, _vp]),
     "fa_batch_workspace_bytes": (ctypes.c_size_t, [_vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int]),
     "fa_score_batch": (ctypes.c_int, [_vp, ctypes.POINTER(_vp), ctypes.POINTER(_vp), ctypes.c_int,
                                       ctypes.POINTER(_vp), ctypes.c_int, ctypes.c_int, ctypes.c_int,
@@ -203,6 +206,29 @@ class Context:
     def has_key(self, step: int) -> bool:
         return bool(self.lib.fa_has_key(self.h, step))
 
+    def keygen_relin(self, s, a, e):
+        """Relinearisation key (s^2 -> s) from host randomness a [dnum][L+K][N], e [dnum][N]."""
+        s = _np(s, np.int64)
+        a = _np(a, np.uint64)
+        e = _np(e, np.int64)
+        assert a.size == self.dnum * (self.L + self.K) * self.n and e.size == self.dnum * self.n
+        _check(self.lib.fa_keygen_relin(self.h, _ptr(s, _i64p), _ptr(a, _u64p), _ptr(e, _i64p)))
+
+    def has_relin_key(self) -> bool:
+        return bool(self.lib.fa_has_relin_key(self.h))
+
+    def encrypt_pts(self, pts: torch.Tensor, n_pts: int, a, e, out: torch.Tensor | None = None,
+                    stream=None) -> torch.Tensor:
+        """Encrypt n_pts device plaintexts with host randomness a [n_pts][L][N], e [n_pts][N];
+        returns [n_pts][2][L][N] ciphertexts (an encrypted diagonal block)."""
+        a = _np(a, np.uint64)
+        e = _np(e, np.int64)
+        assert a.size == n_pts * self.L * self.n and e.size == n_pts * self.n
+        out = self.new_ct(n_pts) if out is None else out
+        _check(self.lib.fa_encrypt_pts(self.h, _dev(pts), n_pts, _ptr(a, _u64p), _ptr(e, _i64p), _dev(out),
+                                       _stream(stream)))
+        return out
+
     def set_secret(self, s):
         s = _np(s, np.int64)
         _check(self.lib.fa_set_secret(self.h, _ptr(s, _i64p)))
@@ -270,6 +296,8 @@ class Context:
         out = self.new_ct(nb) if out is None else out
         if ws is None and layout == LAYOUT_DIAG:
             ws = self.workspace(OP_SCORE, nb, d, baby_step)
+        elif ws is None and layout == LAYOUT_DIAG_ENC:
+            ws = self.workspace(OP_SCORE_ENC, nb, d, baby_step)
         arr = (_vp * nb)(*[ctypes.c_void_p(b.data_ptr()) for b in blocks])
         ws_p, ws_b = (_dev(ws), ws.numel() * 8) if ws is not None else (ctypes.c_void_p(0), 0)
         _check(self.lib.fa_score_block(self.h, _dev(q), arr, nb, d, layout, baby_step, _dev(out), ws_p, ws_b,

@@ -137,3 +137,21 @@ def enc_randomness(w: Workload, primes_q, tag: int = 0):
     a = gen.uniform_residues(gen.rng(w.wid, gen.STREAM_ENC_A, tag), primes_q, 1, w.n)[0]
     e = gen.rounded_gaussian(gen.rng(w.wid, gen.STREAM_ENC_E, tag), w.n)
     return a, e
+
+
+def relin_randomness(w: Workload, primes, dnum: int):
+    """Randomness of the relinearisation key (key streams, tag 0: rotation steps start at 1)."""
+    return key_randomness(w, 0, primes, dnum)
+
+
+def db_enc_randomness(w: Workload, primes_q, first: int, count: int, block: int = 0):
+    """Encryption randomness of `count` database plaintexts starting at index `first` of
+    block `block` (one generator per ciphertext, so any slice is reproducible):
+    a [count][L][N] uniform residues, e [count][N] noise."""
+    a = np.empty((count, len(primes_q), w.n), dtype=np.uint64)
+    e = np.empty((count, w.n), dtype=np.int64)
+    for j in range(count):
+        tag = 1_000_000 + block * 100_000 + first + j
+        a[j] = gen.uniform_residues(gen.rng(w.wid, gen.STREAM_ENC_A, tag), primes_q, 1, w.n)[0]
+        e[j] = gen.rounded_gaussian(gen.rng(w.wid, gen.STREAM_ENC_E, tag), w.n)
+    return a, e

@@ -338,3 +338,65 @@ def test_batch_rejects_bad_arguments():
     small = p.ctx.batch_workspace(1, 1, d, B)[:16]
     with pytest.raises(fa.FaError):
         p.ctx.score_batch([ct], [prep], [blk], d, B, ws=small)  # workspace too small
+
+
+@pytest.mark.parametrize("name,d,B,rows_list", [
+    ("tiny", 16, 4, [300, 512]),
+    ("tiny", 16, 16, [100]),
+    ("p1", 128, 16, [4096, 1000]),
+])
+def test_encrypted_block_score_parity(name, d, B, rows_list):
+    """Encrypted database blocks (ct x ct, lazy relinearisation): the encrypted diagonals, and
+    every output ciphertext, equal the oracle's word for word; decrypted scores match float64."""
+    from paper_2608_21131_amd import fa
+    p = pair(name, wid=17)
+    S = p.par.slots
+    G = d // B
+    g = gen.rng(17, gen.STREAM_DB, d, B)
+    Xs = [gen.gaussian_unit_rows(g, r, d) for r in rows_list]
+    q = gen.gaussian_unit_rows(gen.rng(17, gen.STREAM_QUERY), 1, d)[0]
+    ct_dev, ct_orc = p.encrypt_both(ckks.encode(ckks.replicate(q, S), p.n, 40), tag=17)
+    keys = p.keys(ckks.steps_for_bsgs(d, B))
+    par = p.par
+    ra = gen.uniform_residues(gen.rng(17, gen.STREAM_KEY_A, 0), par.primes, par.dnum, par.n)
+    re = gen.rounded_gaussian(gen.rng(17, gen.STREAM_KEY_E, 0), (par.dnum, par.n))
+    p.ctx.keygen_relin(p.s, ra, re)
+    assert p.ctx.has_relin_key()
+    rlk = p.orc.keygen_relin(p.s, ra, re)
+    blocks, oblocks = [], []
+    for bi, X in enumerate(Xs):
+        c = ckks.layout_b_coeffs(X, par, d, B)
+        a = np.stack([gen.uniform_residues(gen.rng(17, gen.STREAM_ENC_A, 1000 * bi + 1 + j), par.q, 1, p.n)[0]
+                      for j in range(d)])
+        e = np.stack([gen.rounded_gaussian(gen.rng(17, gen.STREAM_ENC_E, 1000 * bi + 1 + j), p.n) for j in range(d)])
+        cts = p.ctx.encrypt_pts(p.ctx.encode_db_block_int(c), d, a, e)
+        ocs = np.stack([p.orc.encrypt(c[j], a[j], e[j], p.s) for j in range(d)])
+        assert np.array_equal(p.export_ct(cts, d), ocs)
+        blocks.append(cts)
+        oblocks.append(ocs.reshape(G, B, 2, par.L, p.n))
+    say(f"[enc] {name} d={d} B={B} blocks={rows_list}")
+    out = p.ctx.score_block(ct_dev, blocks, d, fa.LAYOUT_DIAG_ENC, B)
+    got = p.export_ct(out, len(Xs))
+    qrot = p.orc.baby_rotations(ct_orc, B, keys)
+    for i, X in enumerate(Xs):
+        assert np.array_equal(got[i], p.orc.bsgs_block_ct(qrot, oblocks[i], B, G, keys, rlk)), i
+        W = p.ctx.ct_words
+        z = p.ctx.decode(p.ctx.decrypt(out[i * W:(i + 1) * W]), 80)
+        assert np.max(np.abs(z[:len(X)] - X @ q)) < 1e-4
+
+
+def test_encrypted_block_needs_relin_key():
+    from paper_2608_21131_amd import fa
+    p = pair("tiny", wid=18)
+    S = p.par.slots
+    d, B = 16, 4
+    p.keys(ckks.steps_for_bsgs(d, B), oracle=False)
+    q = gen.gaussian_unit_rows(gen.rng(18, gen.STREAM_QUERY), 1, d)[0]
+    ct, _ = p.encrypt_both(ckks.encode(ckks.replicate(q, S), p.n, 40), tag=18)
+    c = ckks.layout_b_coeffs(gen.gaussian_unit_rows(gen.rng(18, 0), 10, d), p.par, d, B)
+    a = np.zeros((d, p.par.L, p.n), dtype=np.uint64)
+    e = np.zeros((d, p.n), dtype=np.int64)
+    cts = p.ctx.encrypt_pts(p.ctx.encode_db_block_int(c), d, a, e)
+    with pytest.raises(fa.FaError) as ei:
+        p.ctx.score_block(ct, [cts], d, fa.LAYOUT_DIAG_ENC, B)
+    assert ei.value.code == fa.FA_E_NOKEY
