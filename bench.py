@@ -55,6 +55,10 @@ def parse():
                     help="rerank: also time cross-query batching (this many queries per plaintext pass, each "
                          "prepared once, all scored against the same blocks) and report it under query_batch "
                          "(0: skip)")
+    ap.add_argument("--enc-level", type=int, default=3,
+                    help="rerank: also time the encrypted-database variant (ct x ct, database diagonals encrypted "
+                         "and enrolled at this many primes, lazy relinearisation) and report it under enc_db "
+                         "(0: skip; 12: all primes)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-check", action="store_true", help="skip the decrypt-and-compare check")
     ap.add_argument("--copy-calib", action="store_true",
@@ -84,7 +88,9 @@ class Bench:
             chunk = steps[i:i + 8]
             rand = [wl.key_randomness(w, r, self.ctx.primes, self.ctx.dnum) for r in chunk]
             self.ctx.keygen(self.s, chunk, np.stack([x[0] for x in rand]), np.stack([x[1] for x in rand]))
-        log(f"[bench] {w.name}: keys for {len(steps)} rotations ({time.time() - t0:.1f}s)")
+        ra, re_ = wl.relin_randomness(w, self.ctx.primes, self.ctx.dnum)
+        self.ctx.keygen_relin(self.s, ra, re_)
+        log(f"[bench] {w.name}: keys for {len(steps)} rotations + relinearisation ({time.time() - t0:.1f}s)")
         self.t0 = t0
 
     def encrypt(self, v, tag=0):
@@ -163,6 +169,66 @@ def run_diag_level(bn, args):
     stream_bytes = 8 * w.n_blocks * w.d * ptw
     return dict(ms=ms, scores=w.rows, phases=ph, err=err, mac_bytes=mac_bytes, stream_bytes=stream_bytes,
                 X=X, cpu=(lambda: cpu_baseline_diag(bn, X, qv)), ctx=ctx, blocks=blocks, centers=centers)
+
+
+def run_enc_level(bn, args, level):
+    """The rerank level against an encrypted database: every diagonal of every block is a
+    ciphertext (the paper's deployment stores encrypted rows), enrolled at `level` primes;
+    the query is dropped to that level and scored ct x ct with one relinearisation per
+    (block, giant step)."""
+    w, fa, torch = bn.w, bn.fa, bn.torch
+    top = bn.ctx
+    ctx = top.at_level(level) if level < w.L else top
+    X, centers = bn.wl.candidate_rows(w)
+    S = w.slots
+    t = time.time()
+    blocks = []
+    for b in range(w.n_blocks):
+        pts = ctx.encode_db_block(X[b * S:(b + 1) * S], w.d, fa.LAYOUT_DIAG, w.B)
+        a, e = bn.wl.db_enc_randomness(w, ctx.primes[:ctx.L], 0, w.d, block=b)
+        blocks.append(ctx.encrypt_pts(pts, w.d, a, e))
+        del pts, a, e
+    torch.cuda.synchronize()
+    log(f"[bench] encrypted {w.n_blocks} blocks, {w.n_blocks * w.d} ciphertexts at {ctx.L} primes "
+        f"({time.time() - t:.1f}s)")
+    qv = bn.wl.query_vectors(w, 1, centers)[0]
+    q_top = bn.encrypt(pad(qv, w.d))
+    q = ctx.new_ct() if ctx is not top else q_top
+    out = ctx.new_ct(w.n_blocks)
+    ws = ctx.workspace(fa.OP_SCORE_ENC, w.n_blocks, w.d, w.B)
+    ctx.profile(True)
+    phases = []
+
+    def step():
+        if ctx is not top:
+            top.drop_level(ctx, q_top, out=q)
+        ctx.score_block(q, blocks, w.d, fa.LAYOUT_DIAG_ENC, w.B, out=out, ws=ws)
+        phases.append(ctx.profile_read())
+
+    ms = bn.timed(step, args.steps, args.warmup)
+    ph = {k: float(np.mean([p[k] for p in phases[args.warmup:]])) for k in phases[0]}
+    err = None
+    if not args.no_check:
+        err = 0.0
+        W_ = ctx.ct_words
+        for b in range(w.n_blocks):
+            rows = X[b * S:(b + 1) * S].astype(np.float64)
+            z = ctx.decode(ctx.decrypt(out[b * W_:(b + 1) * W_]), 80)
+            err = max(err, float(np.max(np.abs(z[:len(rows)] - rows @ qv))))
+    ptw = ctx.L * w.n
+    stream_bytes = 8 * w.n_blocks * w.d * 2 * ptw
+    # the encrypted diagonals once, each baby rotation once (the pair chunks of a launch share it
+    # through L2), the three-component accumulators written once
+    mac_bytes = stream_bytes + 8 * (w.B * 2 * ptw + w.n_blocks * w.G * 3 * ptw)
+    res = {"scoring_level_primes": ctx.L, "ms_per_level": round(ms, 4), "value": round(w.rows / (ms * 1e-3), 1),
+           "unit": "scores/s", "phases_ms": {"baby_ms": round(ph["baby_ms"], 4),
+                                             "mac_ct_ms": round(ph["mac_ms"], 4),
+                                             "relin_and_giant_ms": round(ph["giant_ms"], 4)},
+           "database_bytes": stream_bytes, "level_hbm_floor_ms": round(stream_bytes / (HBM_PEAK_GBS * 1e9) * 1e3, 4),
+           "mac_achieved_GBs": round(mac_bytes / (ph["mac_ms"] * 1e-3) / 1e9, 1), "max_abs_score_err": err}
+    del blocks
+    torch.cuda.empty_cache()
+    return res
 
 
 def mac_batch_bytes(nq, n_pairs, B, ptw):
@@ -578,6 +644,10 @@ def main():
                              "level_hbm_floor_ms": round(r2["stream_bytes"] / (HBM_PEAK_GBS * 1e9) * 1e3, 4),
                              "mac_achieved_GBs": round(r2["mac_bytes"] / (r2["phases"]["mac_ms"] * 1e-3) / 1e9, 1)}
         log(f"[bench] level drop to {args.also_level} primes: {r2['ms']:.3f} ms/level")
+        if args.enc_level:
+            res["enc_db"] = run_enc_level(bn, args, args.enc_level)
+            log(f"[bench] encrypted database at {res['enc_db']['scoring_level_primes']} primes: "
+                f"{res['enc_db']['ms_per_level']:.3f} ms/level")
         if args.batch > 1:
             res["query_batch"] = [run_batch_level(bn, args, r, args.batch), run_batch_level(bn, a2, r2, args.batch)]
             for qb in res["query_batch"]:
