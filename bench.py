@@ -631,11 +631,12 @@ def main():
     if w.name == "three_level":
         res["metric"] = "warm per-query latency (3 levels) + aggregate scores/s, 32 encrypted queries, one MI355X"
         res["ms_per_level"] = None
-    if w.name == "rerank" and args.also_level and not args.level and args.also_level < w.L:
+    extra = w.name == "rerank" and not args.level
+    r2 = None
+    if extra and args.also_level and args.also_level < w.L:
         import copy
         a2 = copy.copy(args)
         a2.level = args.also_level
-        a2.no_check = args.no_check
         r2 = run_diag_level(bn, a2)
         res["level_drop"] = {"scoring_level_primes": args.also_level, "ms_per_level": round(r2["ms"], 4),
                              "value": round(r2["scores"] / (r2["ms"] * 1e-3), 1), "unit": "scores/s",
@@ -644,15 +645,17 @@ def main():
                              "level_hbm_floor_ms": round(r2["stream_bytes"] / (HBM_PEAK_GBS * 1e9) * 1e3, 4),
                              "mac_achieved_GBs": round(r2["mac_bytes"] / (r2["phases"]["mac_ms"] * 1e-3) / 1e9, 1)}
         log(f"[bench] level drop to {args.also_level} primes: {r2['ms']:.3f} ms/level")
-        if args.enc_level:
-            res["enc_db"] = run_enc_level(bn, args, args.enc_level)
-            log(f"[bench] encrypted database at {res['enc_db']['scoring_level_primes']} primes: "
-                f"{res['enc_db']['ms_per_level']:.3f} ms/level")
-        if args.batch > 1:
-            res["query_batch"] = [run_batch_level(bn, args, r, args.batch), run_batch_level(bn, a2, r2, args.batch)]
-            for qb in res["query_batch"]:
-                log(f"[bench] batch of {qb['queries']} at {qb['scoring_level_primes']} primes: "
-                    f"{qb['ms_per_query_level']:.3f} ms per query level, {qb['value'] / 1e6:.1f} M scores/s")
+    if extra and args.enc_level:
+        res["enc_db"] = run_enc_level(bn, args, min(args.enc_level, w.L))
+        log(f"[bench] encrypted database at {res['enc_db']['scoring_level_primes']} primes: "
+            f"{res['enc_db']['ms_per_level']:.3f} ms/level")
+    if extra and args.batch > 1:
+        res["query_batch"] = [run_batch_level(bn, args, r, args.batch)]
+        if r2 is not None:
+            res["query_batch"].append(run_batch_level(bn, a2, r2, args.batch))
+        for qb in res["query_batch"]:
+            log(f"[bench] batch of {qb['queries']} at {qb['scoring_level_primes']} primes: "
+                f"{qb['ms_per_query_level']:.3f} ms per query level, {qb['value'] / 1e6:.1f} M scores/s")
     print(json.dumps(res), flush=True)
 
 
