@@ -357,6 +357,8 @@ def _lib():
     lib.or_mul_plain.argtypes = [ctypes.c_void_p, _u64p, _u64p, _u64p]
     lib.or_bsgs_block.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int, _u64p, _u64p, _u64p,
                                   ctypes.POINTER(_u64p), ctypes.POINTER(_u64p), _u64p]
+    lib.or_rescale.argtypes = [ctypes.c_void_p, _u64p, ctypes.c_int, _u64p]
+    lib.or_mul_const.argtypes = [ctypes.c_void_p, _u64p, ctypes.c_int, _u64p, _u64p]
     lib.or_keygen_relin.argtypes = [ctypes.c_void_p, _i64p, _u64p, _i64p, _u64p, _u64p]
     lib.or_tensor.argtypes = [ctypes.c_void_p, _u64p, _u64p, _u64p]
     lib.or_relin.argtypes = [ctypes.c_void_p, _u64p, _u64p, _u64p, _u64p]
@@ -532,6 +534,43 @@ class Oracle:
         self.lib.or_bsgs_block_ct(self.ctx, B, G, _p(qrot), _p(cts), _p(gs), kbp, kap, _p(rkb), _p(rka), _p(out))
         return out
 
+    # ---- rescaling and constants (the membership path) ----
+    def rescale(self, ct: np.ndarray) -> np.ndarray:
+        """Divide by the last ciphertext prime with rounding and drop it: [h][L][N] -> [h][L-1][N]."""
+        ct = _c(ct)
+        h = ct.shape[0]
+        assert ct.shape[1:] == (self.par.L, self.par.n)
+        out = np.empty((h, self.par.L - 1, self.par.n), dtype=np.uint64)
+        self.lib.or_rescale(self.ctx, _p(ct), h, _p(out))
+        return out
+
+    def mul_const(self, ct: np.ndarray, c: int) -> np.ndarray:
+        """Every polynomial times the integer c (mod each ciphertext prime)."""
+        ct = _c(ct)
+        cres = _c([int(c) % q for q in self.par.q])
+        out = np.empty_like(ct)
+        self.lib.or_mul_const(self.ctx, _p(ct), ct.shape[0], _p(cres), _p(out))
+        return out
+
+    def add_const(self, ct: np.ndarray, c: int) -> np.ndarray:
+        """c0 + c (the integer c, mod each ciphertext prime, on the constant coefficient);
+        the constant polynomial c encodes the value c / scale in every slot."""
+        out = _c(ct).copy()
+        for t, q in enumerate(self.par.q):
+            out[0, t, 0] = np.uint64((int(out[0, t, 0]) + int(c)) % q)
+        return out
+
+    def add(self, x: np.ndarray, y: np.ndarray, sub: bool = False) -> np.ndarray:
+        out = np.empty_like(_c(x))
+        for t, q in enumerate(self.par.q):
+            a, b = x[:, t].astype(object), y[:, t].astype(object)
+            out[:, t] = ((a - b if sub else a + b) % q).astype(np.uint64)
+        return out
+
+    def mul(self, x: np.ndarray, y: np.ndarray, rlk) -> np.ndarray:
+        """ct x ct product relinearised (no rescale): Relin(x (x) y)."""
+        return self.relin(self.tensor(x, y), rlk)
+
     def baby_rotations(self, ct: np.ndarray, B: int, keys: dict) -> np.ndarray:
         """[B][2][L][N]: qrot[0] = ct, qrot[b] = Rotate(ct, b)."""
         out = np.empty((B,) + ct.shape, dtype=np.uint64)
@@ -587,3 +626,95 @@ def layout_b_coeffs(X: np.ndarray, par: Params, d: int, B: int) -> np.ndarray:
 
 def steps_for_bsgs(d: int, B: int) -> list[int]:
     return list(range(1, B)) + [g * B for g in range(1, d // B)]
+
+
+# ----------------------------------------------------------------------------
+# The membership (threshold) path: a chain of levels with rescaling, a
+# Chebyshev series by the direct (product-formula) evaluator, and an odd
+# polynomial iteration approximating the sign (the paper's face path:
+# sqrt(tau^2 |q_R|^2) by a low-degree Chebyshev polynomial, then the sign of
+# score - tau |q_R| after pre-scaling into [-1, 1]).
+#
+# A ciphertext travels with its level (number of ciphertext primes) and its
+# scale (a float); a product is relinearised and then rescaled by the last
+# prime of its level, so a scale s_a * s_b / q follows it.  Constants enter
+# only as integers: an added constant c at scale s is round(c * s) on the
+# constant coefficient, a real factor c costs a rescale as round(c * q).
+# ----------------------------------------------------------------------------
+class LevelChain:
+    """Oracles for every level L_top..2 of one prime chain, with the secret's keys
+    restricted to each level (the same restriction as the level drop)."""
+
+    def __init__(self, top: Params, s: np.ndarray, rlk_rand, rot_rand: dict, rot_levels=None):
+        self.top = top
+        self.s = s
+        self.orc, self.rlk, self.keys = {}, {}, {}
+        a_r, e_r = rlk_rand
+        for L in range(top.L, 1, -1):
+            par = top if L == top.L else Params(logn=top.logn, L=L, K=top.K, log_scale=top.log_scale,
+                                                 primes=top.q[:L] + top.p)
+            idx = list(range(L)) + list(range(top.L, top.L + top.K))
+            orc = Oracle(par)
+            self.orc[L] = orc
+            self.rlk[L] = orc.keygen_relin(s, a_r[:par.dnum][:, idx], e_r[:par.dnum])
+            self.keys[L] = {}
+            if rot_levels is None or L in rot_levels:
+                for r, (a, e) in rot_rand.items():
+                    self.keys[L][r] = orc.keygen(s, r, a[:par.dnum][:, idx], e[:par.dnum])
+
+    def q(self, L: int) -> int:
+        return self.top.q[L - 1]
+
+    @staticmethod
+    def drop(ct: np.ndarray, L: int) -> np.ndarray:
+        return np.ascontiguousarray(ct[:, :L])
+
+    def mul_rescale(self, x, Lx, sx, y, Ly, sy):
+        """Relinearised product of two ciphertexts at the lower of their levels, then rescaled."""
+        L = min(Lx, Ly)
+        p = self.orc[L].mul(self.drop(x, L), self.drop(y, L), self.rlk[L])
+        return self.orc[L].rescale(p), L - 1, sx * sy / float(self.q(L))
+
+
+def cheb_eval(ch: LevelChain, u: np.ndarray, Lu: int, su: float, coeffs) -> tuple:
+    """sum_k c_k T_k(u) for a ciphertext u (slots in [-1, 1]) by the direct evaluator:
+    T_{a+b} = 2 T_a T_b - T_{a-b} with a = b = k/2 (then T_0 = 1) for even k and
+    a = b + 1 for odd k (then T_1), T_2..T_d in order; then every T_k is brought to the
+    lowest level, multiplied by round(c_k * q) for the prime q the final rescale divides
+    out, summed with round(c_0 * s) and rescaled.  Returns (ct, level, scale)."""
+    d = len(coeffs) - 1
+    assert d >= 1
+    T = {1: (u, Lu, su)}
+    for k in range(2, d + 1):
+        a, b = (k // 2, k // 2) if k % 2 == 0 else (k // 2 + 1, k // 2)
+        p, L, sp = ch.mul_rescale(*T[a], *T[b])
+        orc = ch.orc[L]
+        p = orc.add(p, p)
+        if k % 2 == 0:
+            p = orc.add_const(p, -int(np.rint(1.0 * sp)))
+        else:
+            p = orc.add(p, ch.drop(T[1][0], L), sub=True)
+        T[k] = (p, L, sp)
+    Lmin = min(v[1] for v in T.values())
+    qn = ch.q(Lmin)
+    orc = ch.orc[Lmin]
+    acc = None
+    for k in range(1, d + 1):
+        term = orc.mul_const(ch.drop(T[k][0], Lmin), int(np.rint(coeffs[k] * float(qn))))
+        acc = term if acc is None else orc.add(acc, term)
+    s_acc = su * float(qn)
+    acc = orc.add_const(acc, int(np.rint(coeffs[0] * s_acc)))
+    return orc.rescale(acc), Lmin - 1, s_acc / float(qn)
+
+
+def sign_iter(ch: LevelChain, V: np.ndarray, L: int, s: float, m: int, iters: int) -> tuple:
+    """Odd iteration towards sign(x) for x = V/m in [-1, 1]: f(x) = (3x - x^3)/2, kept with
+    integer constants only -- V' = V (3 m^2 - V^2) stands for f(x) with multiplier
+    m' = 2 m^3.  Two levels per iteration.  Returns (ct, level, scale, multiplier)."""
+    for _ in range(iters):
+        z, Lz, sz = ch.mul_rescale(V, L, s, V, L, s)
+        orc = ch.orc[Lz]
+        w = orc.add_const(orc.mul_const(z, -1), int(np.rint(3.0 * float(m) * float(m) * sz)))
+        V, L, s = ch.mul_rescale(V, L, s, w, Lz, sz)
+        m = 2 * m ** 3
+    return V, L, s, m

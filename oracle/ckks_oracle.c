@@ -750,3 +750,48 @@ void or_bsgs_block_ct(void* p, int B, int G, const u64* qrot, const u64* cts, co
   }
   free(acc3); free(rel); free(usum); free(u); free(tmp); free(qhat);
 }
+
+/* ------------------------------------------------------------------ */
+/* rescaling and constants (the deep membership path)                   */
+/* ------------------------------------------------------------------ */
+
+/* Rescale: divide by the last ciphertext prime q_{L-1} with rounding and drop
+ * it.  ct [npolys][L][N] coefficient form -> out [npolys][L-1][N]:
+ *   out_t = (c_t - r) * q_{L-1}^{-1} mod q_t,
+ * r the centred residue of c mod q_{L-1} (in (-q_{L-1}/2, q_{L-1}/2]), so that
+ * out = round(c / q_{L-1}) coefficient-wise. */
+void or_rescale(void* p, const u64* ct, int npolys, u64* out) {
+  octx* c = (octx*)p;
+  int n = c->n, L = c->L;
+  u64 ql = c->primes[L - 1];
+  for (int h = 0; h < npolys; ++h) {
+    const u64* last = ct + ((size_t)h * L + L - 1) * n;
+#pragma omp parallel for schedule(static)
+    for (int t = 0; t < L - 1; ++t) {
+      u64 q = c->primes[t];
+      u64 inv = powm(ql % q, q - 2, q);
+      const u64* src = ct + ((size_t)h * L + t) * n;
+      u64* dst = out + ((size_t)h * (L - 1) + t) * n;
+      for (int k = 0; k < n; ++k) {
+        u64 x = last[k];
+        u64 r = x <= (ql - 1) / 2 ? x % q : negm((ql - x) % q, q);
+        dst[k] = mulm(subm(src[k], r, q), inv, q);
+      }
+    }
+  }
+}
+
+/* out[h][t] = x[h][t] * c_t mod q_t for npolys polynomials over the L
+ * ciphertext primes; c: [L] residues of an integer constant. */
+void or_mul_const(void* p, const u64* x, int npolys, const u64* cres, u64* out) {
+  octx* c = (octx*)p;
+  int n = c->n, L = c->L;
+  for (int h = 0; h < npolys; ++h)
+    for (int t = 0; t < L; ++t) {
+      u64 q = c->primes[t];
+      for (int k = 0; k < n; ++k) {
+        size_t o = ((size_t)h * L + t) * n + k;
+        out[o] = mulm(x[o], cres[t], q);
+      }
+    }
+}

@@ -668,3 +668,88 @@ def test_encrypted_block_scores_match_float64(small, B):
     z = dec(orc, out, s, 80)
     assert np.max(np.abs(z[:rows] - X @ q)) < 1e-4
     assert np.max(np.abs(z[rows:])) < 1e-4
+
+
+# ----------------------------------------------------------------------------
+# membership path: rescale, Chebyshev direct evaluator, sign iteration
+# ----------------------------------------------------------------------------
+def test_rescale_is_rounded_division_by_the_last_prime(small4):
+    """Coefficient-wise, rescale(c) = round(c / q_last) mod Q' for c lifted to [0, Q), with
+    the remainder taken in (-q_last/2, q_last/2] -- checked with big integers."""
+    par, orc = small4
+    g = np.random.default_rng(40)
+    ct = np.stack([np.stack([g.integers(0, q, par.n, dtype=np.uint64) for q in par.q]) for _ in range(2)])
+    out = orc.rescale(ct)
+    ql = par.q[-1]
+    for h in range(2):
+        big = ckks.crt_centered(ct[h], par.q)
+        for k in range(0, par.n, 97):
+            c = int(big[k]) % par.Q
+            r = c % ql
+            if r > (ql - 1) // 2:
+                r -= ql
+            v = (c - r) // ql
+            assert [int(out[h, t, k]) for t in range(par.L - 1)] == [v % q for q in par.q[:-1]], (h, k)
+
+
+def test_rescale_of_multiple_of_last_prime_is_exact(small4):
+    """c = q_last * x  ->  rescale(c) = x exactly, for a small signed polynomial x."""
+    par, orc = small4
+    x = np.random.default_rng(41).integers(-1000, 1000, par.n)
+    ql = par.q[-1]
+    c = np.stack([np.array([(ql * int(v)) % q for v in x], dtype=np.uint64) for q in par.q])[None]
+    out = orc.rescale(c)[0]
+    for t, q in enumerate(par.q[:-1]):
+        assert np.array_equal(out[t], np.array([int(v) % q for v in x], dtype=np.uint64))
+
+
+def _chain(logn, L, K, wid):
+    top = ckks.Params(logn=logn, L=L, K=K, log_scale=50)
+    s = gen.ternary_secret(gen.rng(wid, gen.STREAM_SECRET), top.n)
+    ra = gen.uniform_residues(gen.rng(wid, gen.STREAM_KEY_A, 0), top.primes, top.dnum, top.n)
+    re_ = gen.rounded_gaussian(gen.rng(wid, gen.STREAM_KEY_E, 0), (top.dnum, top.n))
+    return ckks.LevelChain(top, s, (ra, re_), {}, rot_levels=[]), s
+
+
+def _enc_at(ch, v, s, wid, tag, scale_bits=50):
+    top = ch.top
+    m = ckks.encode(v, top.n, scale_bits)
+    a = gen.uniform_residues(gen.rng(wid, gen.STREAM_ENC_A, tag), top.q, 1, top.n)[0]
+    e = gen.rounded_gaussian(gen.rng(wid, gen.STREAM_ENC_E, tag), top.n)
+    return ch.orc[top.L].encrypt(m, a, e, s)
+
+
+def _dec_at(ch, ct, L, scale, s):
+    orc = ch.orc[L]
+    return ckks.decode_residues(orc.decrypt(ct, s), orc.par, 0) / scale
+
+
+def test_chebyshev_direct_evaluator_matches_numpy():
+    """Degree-7 Chebyshev series of an encrypted u in [-1, 1] (levels 7 -> 3): decrypted
+    values equal numpy's chebval of the decrypted input within 1e-6."""
+    ch, s = _chain(10, 7, 2, 42)
+    top = ch.top
+    u = np.random.default_rng(42).uniform(-1, 1, top.slots)
+    coeffs = np.random.default_rng(43).uniform(-1, 1, 8)
+    ct = _enc_at(ch, u, s, 42, 1)
+    out, L, sc = ckks.cheb_eval(ch, ct, top.L, 2.0 ** 50, coeffs)
+    assert L == top.L - 4
+    z = _dec_at(ch, out, L, sc, s)
+    assert np.max(np.abs(z - np.polynomial.chebyshev.chebval(u, coeffs))) < 1e-6
+
+
+def test_sign_iteration_matches_the_odd_polynomial():
+    """Two iterations of f(x) = (3x - x^3)/2 on x = V/4 (integer constants, tracked
+    multiplier 4 -> 128 -> 2^22): decrypted V / m equals f(f(x)) within 1e-6 and has the
+    sign of x."""
+    ch, s = _chain(10, 6, 2, 44)
+    top = ch.top
+    x = np.random.default_rng(44).uniform(-0.5, 0.5, top.slots)
+    ct = _enc_at(ch, 4 * x, s, 44, 1)
+    V, L, sc, m = ckks.sign_iter(ch, ct, top.L, 2.0 ** 50, 4, 2)
+    assert (L, m) == (top.L - 4, 2 * 128 ** 3)
+    z = _dec_at(ch, V, L, sc, s) / m
+    f = lambda t: (3 * t - t ** 3) / 2
+    assert np.max(np.abs(z - f(f(x)))) < 1e-6
+    big = np.abs(x) > 1e-3
+    assert np.all(np.sign(z[big]) == np.sign(x[big]))
