@@ -268,6 +268,52 @@ int fa_rotate_sum(fa_ctx* ctx, void* cts, int n_cts, int first_shift, int n_step
 /* out = Rotate(ct, step) (one full key switch). */
 int fa_rotate(fa_ctx* ctx, const void* ct, int step, void* out, void* ws, size_t ws_bytes, void* stream);
 
+/* ---- the membership (threshold) path ------------------------------------
+ * Section 3.1 ("Membership search"): the server returns an encrypted yes/no
+ * for score >= tau |q_R| by approximating tau |q_R| = sqrt(tau^2 |q_R|^2)
+ * with a low-degree Chebyshev polynomial (direct evaluator) and then the
+ * sign of score - tau |q_R| after pre-scaling into [-1, 1].  These calls run
+ * on a chain of contexts, levels[0] with L primes and each next one the
+ * previous minus its last ciphertext prime (fa_ctx_create_level), every one
+ * holding the relinearisation key.  A ciphertext's level is its number of
+ * primes; its scale (a double) is tracked by the caller and returned by the
+ * polynomial calls.  Products are relinearised and rescaled by the last prime
+ * of their level (scale sa*sb/q); constants are integers. */
+
+/* Rescale n_polys polynomials of ct ([n_polys][L][N] at hi) by hi's last
+ * prime: out ([n_polys][L-1][N], lo's layout) = round(ct / q_last), the
+ * remainder centred in (-q_last/2, q_last/2].  lo must be hi minus that prime.
+ * ws: n_polys * L * N words. */
+int fa_rescale(const fa_ctx* hi, const fa_ctx* lo, const void* ct, int n_polys, void* out, void* ws,
+               size_t ws_bytes, void* stream);
+/* out = Relin(x (x) y) at one level (no rescale); needs the relinearisation
+ * key.  ws: fa_workspace_bytes is not used; pass fa_chain_workspace_bytes(ctx, 1). */
+int fa_mul_ct(fa_ctx* ctx, const void* x, const void* y, void* out, void* ws, size_t ws_bytes, void* stream);
+/* out = x + y (subtract = 0) or x - y; out = k * x; out = x + k (the constant
+ * k on every slot: k / scale) -- k an integer (for fa_ct_add_const an
+ * integer-valued double, any magnitude below 2^1000, as constants at a
+ * product's scale exceed 64 bits); out may alias x. */
+int fa_ct_add(fa_ctx* ctx, const void* x, const void* y, void* out, int subtract, void* stream);
+int fa_ct_mul_const(fa_ctx* ctx, const void* x, int64_t k, void* out, void* stream);
+int fa_ct_add_const(fa_ctx* ctx, const void* x, double k, void* out, void* stream);
+/* Workspace (bytes) of fa_cheb_eval of this degree and of fa_sign_iter
+ * (degree 3) on a chain whose first context is top. */
+size_t fa_chain_workspace_bytes(const fa_ctx* top, int degree);
+/* sum_{k<=degree} coeffs[k] T_k(u), u at level L_u and scale s_u with slots in
+ * [-1, 1]: T_{a+b} = 2 T_a T_b - T_{a-b} (a = b = k/2 with T_0 = 1 for even k,
+ * a = b + 1 with T_1 for odd k), T_2..T_degree in order; every T_k is then
+ * dropped to the lowest level, multiplied by round(c_k q) for that level's
+ * last prime q, summed with round(c_0 s_u q) and rescaled.  Writes the result
+ * to out (a ciphertext at *L_out primes, scale *s_out). */
+int fa_cheb_eval(fa_ctx* const* levels, int n_levels, const void* u, int L_u, double s_u, const double* coeffs,
+                 int degree, void* out, int* L_out, double* s_out, void* ws, size_t ws_bytes, void* stream);
+/* iters steps towards sign(x), x = V/m in [-1, 1] (m >= 1 an integer): with
+ * f(x) = (3x - x^3)/2, V <- V (3 m^2 - V^2) and m <- 2 m^3 each step (two
+ * levels per step, integer constants only).  out holds the last V (level
+ * *L_out, scale *s_out); its value divided by *m_out approximates f^iters(x). */
+int fa_sign_iter(fa_ctx* const* levels, int n_levels, const void* v, int L_v, double s_v, int64_t m, int iters,
+                 void* out, int* L_out, double* s_out, int64_t* m_out, void* ws, size_t ws_bytes, void* stream);
+
 /* ---- measurement -------------------------------------------------------- */
 
 /* Phase timing of subsequent diagonal-layout fa_score_block calls with HIP

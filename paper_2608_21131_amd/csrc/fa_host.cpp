@@ -1510,6 +1510,270 @@ int fa_score_block(fa_ctx* c, const void* q, const void* const* blocks, int n_bl
   return score_diag(c, (const double*)q, (const double* const*)blocks, n_blocks, d, baby_step, (double*)out, ar, s);
 }
 
+// ---- the membership path: rescale, ct x ct products, constants, polynomials ----
+
+static bool chain_ok(const fa_ctx* hi, const fa_ctx* lo) {
+  if (!hi || !lo || lo->L != hi->L - 1 || lo->K != hi->K || lo->n != hi->n) return false;
+  for (int t = 0; t < lo->L; ++t)
+    if (lo->primes[t] != hi->primes[t]) return false;
+  for (int k = 0; k < hi->K; ++k)
+    if (lo->primes[lo->L + k] != hi->primes[hi->L + k]) return false;
+  return true;
+}
+
+size_t fa_chain_workspace_bytes(const fa_ctx* top, int degree) {
+  if (!top || degree < 1) return 0;
+  const size_t ctw = 2 * (size_t)top->L * top->n;
+  return (size_t)(degree + 4) * rup(ctw) + 2 * rup(3 * (size_t)top->L * top->n) + relin_ws(top);
+}
+
+int fa_rescale(const fa_ctx* hi, const fa_ctx* lo, const void* ct, int n_polys, void* out, void* ws, size_t ws_bytes,
+               void* stream) {
+  if (!hi || !lo || !ct || !out) return fail(FA_E_INVAL, "fa_rescale: null argument");
+  if (!chain_ok(hi, lo)) return fail(FA_E_SHAPE, "fa_rescale: the second context must be the first minus its last prime");
+  if (n_polys < 1 || n_polys > 3) return fail(FA_E_SHAPE, "n_polys must be 1..3");
+  const size_t need = rup((size_t)n_polys * hi->L * hi->n);
+  if (!ws || ws_bytes < need) return fail(FA_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
+  fa::rescale(hi, (const double*)ct, n_polys, (double*)out, (double*)ws, (hipStream_t)stream);
+  return check_launch("fa_rescale");
+}
+
+// relinearised product at one level: out = Relin(x (x) y)
+static int mul_relin(fa_ctx* c, const double* x, const double* y, double* out, Arena& ar, hipStream_t s) {
+  const size_t mark = ar.used;
+  double* t3 = ar.take(3 * (size_t)c->L * c->n);
+  if (!t3) return fail(FA_E_NOMEM, "workspace too small for a ciphertext product");
+  fa::tensor(c, x, y, t3, s);
+  const int rc = relin_batch(c, t3, 1, out, ar, s);
+  ar.used = mark;
+  return rc;
+}
+
+int fa_mul_ct(fa_ctx* c, const void* x, const void* y, void* out, void* ws, size_t ws_bytes, void* stream) {
+  if (!c || !x || !y || !out) return fail(FA_E_INVAL, "fa_mul_ct: null argument");
+  const size_t need = rup(3 * (size_t)c->L * c->n) + relin_ws(c);
+  if (!ws || ws_bytes < need) return fail(FA_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
+  Arena ar{(char*)ws, ws_bytes, 0};
+  int rc = mul_relin(c, (const double*)x, (const double*)y, (double*)out, ar, (hipStream_t)stream);
+  return rc ? rc : check_launch("fa_mul_ct");
+}
+
+// Residues mod each ciphertext prime of an integer-valued double v (|v| up to
+// 2^1023): v = m * 2^e with m a 53-bit integer, so v mod q = (m mod q)(2^e mod q).
+static std::vector<uint64_t> const_residues(const fa_ctx* c, double v) {
+  std::vector<uint64_t> r(c->L);
+  const bool neg = v < 0;
+  const double a = std::fabs(v);
+  int e = 0;
+  const double fr = std::frexp(a, &e);  // a = fr * 2^e, fr in [0.5, 1)
+  u64 m = 0;
+  int sh = 0;
+  if (e <= 53) {
+    m = (u64)a;  // exact: a is an integer below 2^53
+  } else {
+    m = (u64)std::ldexp(fr, 53);  // 53-bit mantissa
+    sh = e - 53;
+  }
+  for (int t = 0; t < c->L; ++t) {
+    const u64 q = c->primes[t];
+    u64 x = m % q;
+    x = mulmod(x, powmod(2, (u64)sh, q), q);
+    r[t] = neg && x ? q - x : x;
+  }
+  return r;
+}
+static std::vector<uint64_t> const_residues(const fa_ctx* c, int64_t k) {
+  std::vector<uint64_t> r(c->L);
+  for (int t = 0; t < c->L; ++t) {
+    const int64_t q = (int64_t)c->primes[t];
+    const int64_t x = k % q;
+    r[t] = (uint64_t)(x < 0 ? x + q : x);
+  }
+  return r;
+}
+
+int fa_ct_add(fa_ctx* c, const void* x, const void* y, void* out, int subtract, void* stream) {
+  if (!c || !x || !y || !out) return fail(FA_E_INVAL, "fa_ct_add: null argument");
+  fa::ct_elem(c, (const double*)x, (const double*)y, (double*)out, 2, nullptr, subtract ? 3 : 2,
+              (hipStream_t)stream);
+  return check_launch("fa_ct_add");
+}
+
+int fa_ct_mul_const(fa_ctx* c, const void* x, int64_t k, void* out, void* stream) {
+  if (!c || !x || !out) return fail(FA_E_INVAL, "fa_ct_mul_const: null argument");
+  const auto r = const_residues(c, k);
+  fa::ct_elem(c, (const double*)x, nullptr, (double*)out, 2, r.data(), 0, (hipStream_t)stream);
+  return check_launch("fa_ct_mul_const");
+}
+
+int fa_ct_add_const(fa_ctx* c, const void* x, double k, void* out, void* stream) {
+  if (!c || !x || !out) return fail(FA_E_INVAL, "fa_ct_add_const: null argument");
+  if (!(std::fabs(k) < 0x1p1000) || k != std::nearbyint(k)) return fail(FA_E_INVAL, "k must be an integer value");
+  const auto r = const_residues(c, k);
+  fa::ct_elem(c, (const double*)x, nullptr, (double*)out, 2, r.data(), 1, (hipStream_t)stream);
+  return check_launch("fa_ct_add_const");
+}
+
+namespace {
+// A ciphertext in the chain: device words [2][L][N], its level and scale.
+struct CtRef {
+  double* p;
+  int L;
+  double s;
+};
+struct Chain {
+  std::vector<fa_ctx*> by_L;  // index L -> context with L ciphertext primes
+  fa_ctx* at(int L) const { return L >= 0 && L < (int)by_L.size() ? by_L[L] : nullptr; }
+};
+int make_chain(fa_ctx* const* levels, int n_levels, Chain& ch) {
+  if (!levels || n_levels < 2) return fail(FA_E_INVAL, "a chain needs at least two levels");
+  ch.by_L.assign(levels[0] ? levels[0]->L + 1 : 0, nullptr);
+  for (int i = 0; i < n_levels; ++i) {
+    if (!levels[i] || (i && !chain_ok(levels[i - 1], levels[i])))
+      return fail(FA_E_SHAPE, "levels[%d] must hold the primes of levels[%d] minus its last ciphertext prime", i, i - 1);
+    if (!levels[i]->d_rlk) return fail(FA_E_NOKEY, "level with %d primes has no relinearisation key", levels[i]->L);
+    ch.by_L[levels[i]->L] = levels[i];
+  }
+  return FA_OK;
+}
+// copy x ([2][Lx][N]) dropped to L primes into dst ([2][L][N])
+int drop_to(const Chain& ch, const CtRef& x, int L, double* dst, hipStream_t s) {
+  const size_t n = ch.at(L)->n;
+  for (int h = 0; h < 2; ++h)
+    HIPCHK(hipMemcpyAsync(dst + (size_t)h * L * n, x.p + (size_t)h * x.L * n, (size_t)L * n * 8,
+                          hipMemcpyDeviceToDevice, s));
+  return FA_OK;
+}
+}  // namespace
+
+// product of two chain ciphertexts at the lower of their levels, rescaled into
+// dst (level L-1, scale sa*sb/q_{L-1}); tmp: two [2][L][N] + scratch from ar
+static int chain_mul_rescale(const Chain& ch, const CtRef& a, const CtRef& b, double* dst, CtRef& out, Arena& ar,
+                             hipStream_t s) {
+  const int L = std::min(a.L, b.L);
+  fa_ctx* c = ch.at(L);
+  if (!c || !ch.at(L - 1)) return fail(FA_E_SHAPE, "the chain has no level %d", L - 1);
+  const size_t mark = ar.used, ctw = 2 * (size_t)L * c->n;
+  double* xa = ar.take(ctw);
+  double* xb = ar.take(ctw);
+  double* prod = ar.take(ctw);
+  double* scr = ar.take(2 * (size_t)L * c->n);
+  if (!xa || !xb || !prod || !scr) return fail(FA_E_NOMEM, "workspace too small for a chain product");
+  int rc;
+  if ((rc = drop_to(ch, a, L, xa, s)) || (rc = drop_to(ch, b, L, xb, s))) return rc;
+  if ((rc = mul_relin(c, xa, xb, prod, ar, s))) return rc;
+  fa::rescale(c, prod, 2, dst, scr, s);
+  out = {dst, L - 1, a.s * b.s / (double)c->primes[L - 1]};
+  ar.used = mark;
+  return FA_OK;
+}
+
+int fa_cheb_eval(fa_ctx* const* levels, int n_levels, const void* u, int L_u, double s_u, const double* coeffs,
+                 int degree, void* out, int* L_out, double* s_out, void* ws, size_t ws_bytes, void* stream) {
+  if (!u || !coeffs || !out || !L_out || !s_out) return fail(FA_E_INVAL, "fa_cheb_eval: null argument");
+  if (degree < 1 || degree > 64) return fail(FA_E_INVAL, "degree %d out of [1, 64]", degree);
+  Chain ch;
+  int rc = make_chain(levels, n_levels, ch);
+  if (rc) return rc;
+  fa_ctx* top = levels[0];
+  if (!ch.at(L_u)) return fail(FA_E_SHAPE, "no level %d in the chain", L_u);
+  const size_t need = fa_chain_workspace_bytes(top, degree);
+  if (!ws || ws_bytes < need) return fail(FA_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
+  Arena ar{(char*)ws, ws_bytes, 0};
+  hipStream_t s = (hipStream_t)stream;
+  const size_t ctw = 2 * (size_t)top->L * top->n;
+  std::vector<CtRef> T(degree + 1);
+  T[1] = {(double*)u, L_u, s_u};
+  for (int k = 2; k <= degree; ++k) {
+    const int a = k % 2 == 0 ? k / 2 : k / 2 + 1, b = k / 2;
+    double* dst = ar.take(ctw);
+    if (!dst) return fail(FA_E_NOMEM, "workspace too small for the Chebyshev terms");
+    CtRef p;
+    if ((rc = chain_mul_rescale(ch, T[a], T[b], dst, p, ar, s))) return rc;
+    fa_ctx* c = ch.at(p.L);
+    fa::ct_elem(c, p.p, p.p, p.p, 2, nullptr, 2, s);  // 2 T_a T_b
+    if (k % 2 == 0) {
+      const auto r = const_residues(c, -std::nearbyint(1.0 * p.s));
+      fa::ct_elem(c, p.p, nullptr, p.p, 2, r.data(), 1, s);
+    } else {
+      double* t1 = ar.take(ctw);
+      if (!t1) return fail(FA_E_NOMEM, "workspace too small for the Chebyshev terms");
+      if ((rc = drop_to(ch, T[1], p.L, t1, s))) return rc;
+      fa::ct_elem(c, p.p, t1, p.p, 2, nullptr, 3, s);
+      ar.used -= rup(ctw);  // t1 released
+    }
+    T[k] = p;
+  }
+  int Lmin = L_u;
+  for (int k = 1; k <= degree; ++k) Lmin = std::min(Lmin, T[k].L);
+  fa_ctx* c = ch.at(Lmin);
+  if (!ch.at(Lmin - 1)) return fail(FA_E_SHAPE, "the chain has no level %d", Lmin - 1);
+  const double qn = (double)c->primes[Lmin - 1];
+  const size_t cw = 2 * (size_t)Lmin * c->n;
+  double* acc = ar.take(cw);
+  double* term = ar.take(cw);
+  double* scr = ar.take(2 * (size_t)Lmin * c->n);
+  if (!acc || !term || !scr) return fail(FA_E_NOMEM, "workspace too small for the Chebyshev sum");
+  for (int k = 1; k <= degree; ++k) {
+    if ((rc = drop_to(ch, T[k], Lmin, term, s))) return rc;
+    const auto ck = const_residues(c, std::nearbyint(coeffs[k] * qn));
+    if (k == 1) {
+      fa::ct_elem(c, term, nullptr, acc, 2, ck.data(), 0, s);
+    } else {
+      fa::ct_elem(c, term, nullptr, term, 2, ck.data(), 0, s);
+      fa::ct_elem(c, acc, term, acc, 2, nullptr, 2, s);
+    }
+  }
+  const double s_acc = s_u * qn;
+  const auto c0 = const_residues(c, std::nearbyint(coeffs[0] * s_acc));
+  fa::ct_elem(c, acc, nullptr, acc, 2, c0.data(), 1, s);
+  fa::rescale(c, acc, 2, (double*)out, scr, s);
+  *L_out = Lmin - 1;
+  *s_out = s_acc / qn;
+  return check_launch("fa_cheb_eval");
+}
+
+int fa_sign_iter(fa_ctx* const* levels, int n_levels, const void* v, int L_v, double s_v, int64_t m, int iters,
+                 void* out, int* L_out, double* s_out, int64_t* m_out, void* ws, size_t ws_bytes, void* stream) {
+  if (!v || !out || !L_out || !s_out || !m_out) return fail(FA_E_INVAL, "fa_sign_iter: null argument");
+  if (iters < 1 || iters > 8) return fail(FA_E_INVAL, "iters %d out of [1, 8]", iters);
+  Chain ch;
+  int rc = make_chain(levels, n_levels, ch);
+  if (rc) return rc;
+  fa_ctx* top = levels[0];
+  if (!ch.at(L_v)) return fail(FA_E_SHAPE, "no level %d in the chain", L_v);
+  const size_t need = fa_chain_workspace_bytes(top, 3);
+  if (!ws || ws_bytes < need) return fail(FA_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
+  for (int64_t mm = m, it = 0; it < iters; ++it, mm = 2 * mm * mm * mm)
+    if (mm < 1 || mm > (INT64_C(1) << 20)) return fail(FA_E_INVAL, "multiplier out of range at iteration %d", (int)it);
+  Arena ar{(char*)ws, ws_bytes, 0};
+  hipStream_t s = (hipStream_t)stream;
+  const size_t ctw = 2 * (size_t)top->L * top->n;
+  double* zb = ar.take(ctw);
+  double* vb[2] = {ar.take(ctw), ar.take(ctw)};
+  if (!zb || !vb[0] || !vb[1]) return fail(FA_E_NOMEM, "workspace too small for the sign iteration");
+  CtRef V{(double*)v, L_v, s_v};
+  for (int it = 0; it < iters; ++it) {
+    const double mm = (double)m;
+    CtRef z;
+    if ((rc = chain_mul_rescale(ch, V, V, zb, z, ar, s))) return rc;
+    fa_ctx* c = ch.at(z.L);
+    const auto m1 = const_residues(c, (int64_t)-1);
+    const auto k3 = const_residues(c, std::nearbyint(3.0 * mm * mm * z.s));
+    fa::ct_elem(c, z.p, nullptr, z.p, 2, m1.data(), 0, s);
+    fa::ct_elem(c, z.p, nullptr, z.p, 2, k3.data(), 1, s);
+    CtRef nv;
+    double* dst = it == iters - 1 ? (double*)out : vb[it & 1];
+    if ((rc = chain_mul_rescale(ch, V, z, dst, nv, ar, s))) return rc;
+    V = nv;
+    m = 2 * m * m * m;
+  }
+  *L_out = V.L;
+  *s_out = V.s;
+  *m_out = m;
+  return check_launch("fa_sign_iter");
+}
+
 int fa_rotate(fa_ctx* c, const void* ct, int step, void* out, void* ws, size_t ws_bytes, void* stream) {
   if (!c || !ct || !out) return fail(FA_E_INVAL, "fa_rotate: null argument");
   if (step < 1 || step >= c->n / 2) return fail(FA_E_INVAL, "step %d out of [1, N/2)", step);

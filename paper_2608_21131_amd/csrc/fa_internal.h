@@ -172,6 +172,16 @@ void mac_diag(const fa_ctx* c, const double* const* q, const double* const* qrot
 void mac_diag_ct(const fa_ctx* c, const double* q, const double* qrot, const double* const* blocks, int n_blocks,
                  int B, int G, double* acc, hipStream_t s);
 
+// Rescale n_polys polynomials [n_polys][L][N] (NTT form) by the last prime:
+// out [n_polys][L-1][N] = round(x / q_last); scratch: n_polys * L * N words.
+void rescale(const fa_ctx* c, const double* ct, int n_polys, double* out, double* scratch, hipStream_t s);
+// out [3][L][N] = tensor of the ciphertexts x, y (NTT form)
+void tensor(const fa_ctx* c, const double* x, const double* y, double* out, hipStream_t s);
+// element-wise over n_polys polynomials: mode 0 out = x * cst, 1 out = x with cst added to
+// polynomial 0, 2 out = x + y, 3 out = x - y  (cst given by its residues cres[L], or null)
+void ct_elem(const fa_ctx* c, const double* x, const double* y, double* out, int n_polys, const uint64_t* cres,
+             int mode, hipStream_t s);
+
 // out[w] = ct * pt[w] (both polys), w < count
 void mul_plain(const fa_ctx* c, const double* ct, const double* const* pts, int count, double* out, hipStream_t s);
 // dst[r] += src[r] for n_limbs limbs of N words, limb r over prime r % period

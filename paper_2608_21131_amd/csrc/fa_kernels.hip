@@ -974,6 +974,68 @@ __global__ __launch_bounds__(256) void k_add_limbs(double* __restrict__ dst, con
   dst[o] = canon(dst[o] + src[o], q);
 }
 
+// --- the membership path: rescale, ct x ct tensor, constants -------------
+// Rescale, lift: lift[h][t][k] = the centred value of last[h][k] (residues of
+// the last prime, coefficient form, canonical) reduced mod q_t, t < L-1.
+#define FA_MAXLIMB 16
+struct ResArgs {
+  double c[FA_MAXLIMB];   // per limb: q_last^-1 mod q_t (rescale) or a constant mod q_t
+  double cp[FA_MAXLIMB];  // c * (1/q_t)
+};
+__global__ __launch_bounds__(256) void k_rescale_lift(const double* __restrict__ last, double* __restrict__ lift,
+                                                      const DevPrime* __restrict__ pr, int logn, int Lm1,
+                                                      double ql) {
+  const int n = 1 << logn;
+  const int k = blockIdx.x * 256 + threadIdx.x;
+  const int t = blockIdx.y, h = blockIdx.z;
+  const double q = pr[t].q, qinv = pr[t].qinv;
+  double v = last[(size_t)h * n + k];
+  if (v > 0.5 * (ql - 1.0)) v -= ql;  // centred, |v| < q_last / 2, exact
+  lift[((size_t)h * Lm1 + t) * n + k] = canon_full(v, q, qinv);
+}
+// out[h][t] = (c[h][t] - lift^[h][t]) * q_last^-1  (NTT form), t < L-1; c has L limbs per poly
+__global__ __launch_bounds__(256) void k_rescale_combine(const double* __restrict__ ct, const double* __restrict__ lift,
+                                                         double* __restrict__ out, ResArgs a,
+                                                         const DevPrime* __restrict__ pr, int logn, int L) {
+  const int n = 1 << logn;
+  const int k = blockIdx.x * 256 + threadIdx.x;
+  const int t = blockIdx.y, h = blockIdx.z;
+  const double q = pr[t].q, qinv = pr[t].qinv;
+  const double x = ct[((size_t)h * L + t) * n + k] - lift[((size_t)h * (L - 1) + t) * n + k];
+  out[((size_t)h * (L - 1) + t) * n + k] = canon_full(mulc(x, a.c[t], a.cp[t], q), q, qinv);
+}
+// out = (x0 y0, x0 y1 + x1 y0, x1 y1) over the L primes (NTT form)
+__global__ __launch_bounds__(256) void k_tensor(const double* __restrict__ x, const double* __restrict__ y,
+                                                double* __restrict__ out, const DevPrime* __restrict__ pr, int logn,
+                                                int L) {
+  const int n = 1 << logn;
+  const int k = blockIdx.x * 256 + threadIdx.x;
+  const int t = blockIdx.y;
+  const double q = pr[t].q, qinv = pr[t].qinv;
+  const size_t o = (size_t)t * n + k, ln = (size_t)L * n;
+  const double x0 = x[o], x1 = x[ln + o], y0 = y[o], y1 = y[ln + o];
+  out[o] = canon_full(mul(x0, y0, q, qinv), q, qinv);
+  out[ln + o] = canon_full(mul(x0, y1, q, qinv) + mul(x1, y0, q, qinv), q, qinv);
+  out[2 * ln + o] = canon_full(mul(x1, y1, q, qinv), q, qinv);
+}
+// out[h][t] = x[h][t] * c_t (mode 0), or out = x with c_t added to polynomial 0 (mode 1),
+// or out[h][t] = x[h][t] +/- y[h][t] (mode 2 add, mode 3 subtract)
+__global__ __launch_bounds__(256) void k_ct_elem(const double* __restrict__ x, const double* __restrict__ y,
+                                                 double* __restrict__ out, ResArgs a,
+                                                 const DevPrime* __restrict__ pr, int logn, int L, int mode) {
+  const int n = 1 << logn;
+  const int k = blockIdx.x * 256 + threadIdx.x;
+  const int t = blockIdx.y, h = blockIdx.z;
+  const double q = pr[t].q, qinv = pr[t].qinv;
+  const size_t o = ((size_t)h * L + t) * n + k;
+  double v = x[o];
+  if (mode == 0) v = mulc(v, a.c[t], a.cp[t], q);
+  else if (mode == 1) v = h == 0 ? v + a.c[t] : v;
+  else if (mode == 2) v = v + y[o];
+  else v = v - y[o];
+  out[o] = canon_full(v, q, qinv);
+}
+
 __global__ __launch_bounds__(256) void k_int_to_res(const int64_t* __restrict__ src, double* __restrict__ dst,
                                                     const DevPrime* __restrict__ pr, int logn, int nprimes) {
   const int n = 1 << logn;
@@ -1431,6 +1493,55 @@ void mul_plain(const fa_ctx* c, const double* ct, const double* const* pts, int 
 void add_automorph(const fa_ctx* c, double* dst, const double* src, int n_polys, uint32_t gal, hipStream_t s) {
   dim3 g(c->n / 256, n_polys * c->L);
   hipLaunchKernelGGL(k_add_automorph, g, dim3(256), 0, s, dst, src, c->d_pr, c->logn, c->L, gal);
+}
+
+static ResArgs res_args(const fa_ctx* c, const uint64_t* cres, int L) {
+  ResArgs a;
+  for (int t = 0; t < FA_MAXLIMB; ++t) {
+    a.c[t] = t < L ? (double)cres[t] : 0.0;
+    a.cp[t] = t < L ? a.c[t] / (double)c->primes[t] : 0.0;
+  }
+  return a;
+}
+
+void rescale(const fa_ctx* c, const double* ct, int n_polys, double* out, double* scratch, hipStream_t s) {
+  const size_t n = c->n;
+  const int L = c->L;
+  double* last = scratch;                        // [n_polys][N]
+  double* lift = scratch + (size_t)n_polys * n;  // [n_polys][L-1][N]
+  {
+    LimbBatch inv(c, s, false);
+    for (int h = 0; h < n_polys; ++h) inv.add(last + (size_t)h * n, L - 1, ct + ((size_t)h * L + L - 1) * n);
+  }
+  const double ql = (double)c->primes[L - 1];
+  hipLaunchKernelGGL(k_rescale_lift, dim3(c->n / 256, L - 1, n_polys), dim3(256), 0, s, last, lift, c->d_pr, c->logn,
+                     L - 1, ql);
+  ntt_fwd_strided(c, lift, n, n_polys * (L - 1), L - 1, 0, s);
+  std::vector<uint64_t> inv(L - 1);
+  const uint64_t qlast = c->primes[L - 1];
+  for (int t = 0; t < L - 1; ++t) {
+    const uint64_t q = c->primes[t];
+    // (q_last mod q)^(q-2) mod q
+    unsigned __int128 b = qlast % q, r = 1;
+    for (uint64_t e = q - 2; e; e >>= 1) {
+      if (e & 1) r = r * b % q;
+      b = b * b % q;
+    }
+    inv[t] = (uint64_t)r;
+  }
+  hipLaunchKernelGGL(k_rescale_combine, dim3(c->n / 256, L - 1, n_polys), dim3(256), 0, s, ct, lift, out,
+                     res_args(c, inv.data(), L - 1), c->d_pr, c->logn, L);
+}
+
+void tensor(const fa_ctx* c, const double* x, const double* y, double* out, hipStream_t s) {
+  hipLaunchKernelGGL(k_tensor, dim3(c->n / 256, c->L), dim3(256), 0, s, x, y, out, c->d_pr, c->logn, c->L);
+}
+
+void ct_elem(const fa_ctx* c, const double* x, const double* y, double* out, int n_polys, const uint64_t* cres,
+             int mode, hipStream_t s) {
+  std::vector<uint64_t> zero(c->L, 0);
+  hipLaunchKernelGGL(k_ct_elem, dim3(c->n / 256, c->L, n_polys), dim3(256), 0, s, x, y, out,
+                     res_args(c, cres ? cres : zero.data(), c->L), c->d_pr, c->logn, c->L, mode);
 }
 
 void add_limbs(const fa_ctx* c, double* dst, const double* src, int n_limbs, int period, hipStream_t s) {

@@ -81,6 +81,19 @@ SIGNATURES = {
     "fa_keygen_relin": (ctypes.c_int, [_vp, _i64p, _u64p, _i64p]),
     "fa_has_relin_key": (ctypes.c_int, [_vp]),
     "fa_encrypt_pts": (ctypes.c_int, [_vp, _vp, ctypes.c_int, _u64p, _i64p, _vp, _vp]),
+    "fa_rescale": (ctypes.c_int, [_vp, _vp, _vp, ctypes.c_int, _vp, _vp, ctypes.c_size_t, _vp]),
+    "fa_mul_ct": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
+    "fa_ct_add": (ctypes.c_int, [_vp, _vp, _vp, _vp, ctypes.c_int, _vp]),
+    "fa_ct_mul_const": (ctypes.c_int, [_vp, _vp, ctypes.c_int64, _vp, _vp]),
+    "fa_ct_add_const": (ctypes.c_int, [_vp, _vp, ctypes.c_double, _vp, _vp]),
+    "fa_chain_workspace_bytes": (ctypes.c_size_t, [_vp, ctypes.c_int]),
+    "fa_cheb_eval": (ctypes.c_int, [ctypes.POINTER(_vp), ctypes.c_int, _vp, ctypes.c_int, ctypes.c_double, _f64p,
+                                    ctypes.c_int, _vp, ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_double),
+                                    _vp, ctypes.c_size_t, _vp]),
+    "fa_sign_iter": (ctypes.c_int, [ctypes.POINTER(_vp), ctypes.c_int, _vp, ctypes.c_int, ctypes.c_double,
+                                    ctypes.c_int64, ctypes.c_int, _vp, ctypes.POINTER(ctypes.c_int),
+                                    ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64), _vp,
+                                    ctypes.c_size_t, _vp]),
     "fa_batch_workspace_bytes": (ctypes.c_size_t, [_vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int]),
     "fa_score_batch": (ctypes.c_int, [_vp, ctypes.POINTER(_vp), ctypes.POINTER(_vp), ctypes.c_int,
                                       ctypes.POINTER(_vp), ctypes.c_int, ctypes.c_int, ctypes.c_int,
@@ -346,6 +359,41 @@ class Context:
                                        _stream(stream)))
         return outs
 
+    # ---- the membership path ----
+    def chain_workspace(self, degree: int) -> torch.Tensor:
+        nbytes = int(self.lib.fa_chain_workspace_bytes(self.h, degree))
+        return torch.empty(max(1, nbytes // 8 + 32), dtype=torch.float64, device="cuda")
+
+    def rescale(self, lo: "Context", ct: torch.Tensor, n_polys: int = 2, out: torch.Tensor | None = None,
+                stream=None) -> torch.Tensor:
+        """round(ct / last prime) at the next level down (lo = this context minus that prime)."""
+        out = torch.empty(n_polys * lo.L * lo.n, dtype=torch.float64, device="cuda") if out is None else out
+        ws = torch.empty(n_polys * self.L * self.n + 32, dtype=torch.float64, device="cuda")
+        _check(self.lib.fa_rescale(self.h, lo.h, _dev(ct), n_polys, _dev(out), _dev(ws), ws.numel() * 8,
+                                   _stream(stream)))
+        return out
+
+    def mul_ct(self, x: torch.Tensor, y: torch.Tensor, out: torch.Tensor | None = None, stream=None):
+        out = self.new_ct() if out is None else out
+        ws = self.chain_workspace(1)
+        _check(self.lib.fa_mul_ct(self.h, _dev(x), _dev(y), _dev(out), _dev(ws), ws.numel() * 8, _stream(stream)))
+        return out
+
+    def ct_add(self, x, y, out=None, subtract: bool = False, stream=None):
+        out = self.new_ct() if out is None else out
+        _check(self.lib.fa_ct_add(self.h, _dev(x), _dev(y), _dev(out), 1 if subtract else 0, _stream(stream)))
+        return out
+
+    def ct_mul_const(self, x, k: int, out=None, stream=None):
+        out = self.new_ct() if out is None else out
+        _check(self.lib.fa_ct_mul_const(self.h, _dev(x), int(k), _dev(out), _stream(stream)))
+        return out
+
+    def ct_add_const(self, x, k: int, out=None, stream=None):
+        out = self.new_ct() if out is None else out
+        _check(self.lib.fa_ct_add_const(self.h, _dev(x), float(k), _dev(out), _stream(stream)))
+        return out
+
     def project_ct(self, q: torch.Tensor, w_pts: torch.Tensor, d_in: int, r: int, baby_step: int,
                    out: torch.Tensor | None = None, ws: torch.Tensor | None = None, stream=None) -> torch.Tensor:
         out = self.new_ct() if out is None else out
@@ -375,3 +423,38 @@ class Context:
         ws = self.workspace(OP_ROTATE, 1) if ws is None else ws
         _check(self.lib.fa_rotate(self.h, _dev(ct), step, _dev(out), _dev(ws), ws.numel() * 8, _stream(stream)))
         return out
+
+
+def _levels_arg(levels):
+    levels = list(levels)
+    return (_vp * len(levels))(*[c.h for c in levels]), len(levels)
+
+
+def cheb_eval(levels, u: torch.Tensor, L_u: int, s_u: float, coeffs, out: torch.Tensor | None = None,
+              ws: torch.Tensor | None = None, stream=None):
+    """sum_k coeffs[k] T_k(u) on a chain of contexts (levels[0] the top); returns
+    (out, level, scale) with out[:2*level*N] the result."""
+    top = levels[0]
+    arr, nl = _levels_arg(levels)
+    c = _np(coeffs, np.float64)
+    out = top.new_ct() if out is None else out
+    ws = top.chain_workspace(len(c) - 1) if ws is None else ws
+    L_out, s_out = ctypes.c_int(0), ctypes.c_double(0.0)
+    _check(top.lib.fa_cheb_eval(arr, nl, _dev(u), L_u, s_u, _ptr(c, _f64p), len(c) - 1, _dev(out),
+                                ctypes.byref(L_out), ctypes.byref(s_out), _dev(ws), ws.numel() * 8,
+                                _stream(stream)))
+    return out, L_out.value, s_out.value
+
+
+def sign_iter(levels, v: torch.Tensor, L_v: int, s_v: float, m: int, iters: int, out: torch.Tensor | None = None,
+              ws: torch.Tensor | None = None, stream=None):
+    """iters steps of f(x) = (3x - x^3)/2 on x = v/m; returns (out, level, scale, multiplier)."""
+    top = levels[0]
+    arr, nl = _levels_arg(levels)
+    out = top.new_ct() if out is None else out
+    ws = top.chain_workspace(3) if ws is None else ws
+    L_out, s_out, m_out = ctypes.c_int(0), ctypes.c_double(0.0), ctypes.c_int64(0)
+    _check(top.lib.fa_sign_iter(arr, nl, _dev(v), L_v, s_v, int(m), iters, _dev(out), ctypes.byref(L_out),
+                                ctypes.byref(s_out), ctypes.byref(m_out), _dev(ws), ws.numel() * 8,
+                                _stream(stream)))
+    return out, L_out.value, s_out.value, m_out.value

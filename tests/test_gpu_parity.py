@@ -400,3 +400,84 @@ def test_encrypted_block_needs_relin_key():
     with pytest.raises(fa.FaError) as ei:
         p.ctx.score_block(ct, [cts], d, fa.LAYOUT_DIAG_ENC, B)
     assert ei.value.code == fa.FA_E_NOKEY
+
+
+# ----------------------------------------------------------------------------
+# membership path: rescale, ct x ct product, Chebyshev evaluator, sign iteration
+# ----------------------------------------------------------------------------
+def _gpu_chain(logn, L, K, wid):
+    from paper_2608_21131_amd import fa
+    top = ckks.Params(logn=logn, L=L, K=K, log_scale=50)
+    s = gen.ternary_secret(gen.rng(wid, gen.STREAM_SECRET), top.n)
+    ra = gen.uniform_residues(gen.rng(wid, gen.STREAM_KEY_A, 0), top.primes, top.dnum, top.n)
+    re_ = gen.rounded_gaussian(gen.rng(wid, gen.STREAM_KEY_E, 0), (top.dnum, top.n))
+    ctx = fa.Context(logn, L, K, 50)
+    assert ctx.primes == top.primes
+    ctx.keygen_relin(s, ra, re_)
+    levels = [ctx] + [ctx.at_level(l) for l in range(L - 1, 1, -1)]
+    och = ckks.LevelChain(top, s, (ra, re_), {}, rot_levels=[])
+    return top, s, levels, och
+
+
+def _enc_both(top, levels, och, s, v, wid, tag):
+    m = ckks.encode(v, top.n, 50)
+    a = gen.uniform_residues(gen.rng(wid, gen.STREAM_ENC_A, tag), top.q, 1, top.n)[0]
+    e = gen.rounded_gaussian(gen.rng(wid, gen.STREAM_ENC_E, tag), top.n)
+    return levels[0].encrypt(m, a, e), och.orc[top.L].encrypt(m, a, e, s)
+
+
+def _export_at(levels, ct, L):
+    c = levels[levels[0].L - L]
+    return c.export(ct[:2 * L * c.n], 2).reshape(2, L, c.n)
+
+
+def test_rescale_and_product_parity():
+    top, s, levels, och = _gpu_chain(11, 6, 2, 50)
+    v1 = gen.gaussian_unit_rows(gen.rng(50, gen.STREAM_QUERY), 1, top.slots)[0]
+    v2 = gen.gaussian_unit_rows(gen.rng(50, gen.STREAM_DB), 1, top.slots)[0]
+    x, xo = _enc_both(top, levels, och, s, v1, 50, 1)
+    y, yo = _enc_both(top, levels, och, s, v2, 50, 2)
+    say("[chain] rescale / product")
+    r = levels[0].rescale(levels[1], x)
+    assert np.array_equal(_export_at(levels, r, top.L - 1), och.orc[top.L].rescale(xo))
+    p = levels[0].mul_ct(x, y)
+    po = och.orc[top.L].mul(xo, yo, och.rlk[top.L])
+    assert np.array_equal(_export_at(levels, p, top.L), po)
+    pr = levels[0].rescale(levels[1], p)
+    z = levels[1].decode(levels[1].decrypt(pr), 50) * (2.0 ** 50 / (2.0 ** 100 / top.q[-1]))
+    assert np.max(np.abs(z - v1 * v2)) < 1e-6
+    # constants and sums
+    a = levels[0].ct_add_const(levels[0].ct_mul_const(x, -3), 12345)
+    ao = och.orc[top.L].add_const(och.orc[top.L].mul_const(xo, -3), 12345)
+    assert np.array_equal(_export_at(levels, a, top.L), ao)
+    d = levels[0].ct_add(x, y, subtract=True)
+    assert np.array_equal(_export_at(levels, d, top.L), och.orc[top.L].add(xo, yo, sub=True))
+
+
+def test_chebyshev_and_sign_parity():
+    """The GPU chain evaluates the degree-7 Chebyshev series and two sign steps exactly as
+    the oracle chain does (word for word), and the values match numpy."""
+    from paper_2608_21131_amd import fa
+    top, s, levels, och = _gpu_chain(11, 9, 2, 51)
+    u = np.random.default_rng(51).uniform(-1, 1, top.slots)
+    coeffs = np.random.default_rng(52).uniform(-1, 1, 8)
+    x, xo = _enc_both(top, levels, och, s, u, 51, 1)
+    say("[chain] Chebyshev degree 7")
+    out, L, sc = fa.cheb_eval(levels, x, top.L, 2.0 ** 50, coeffs)
+    oo, Lo, so = ckks.cheb_eval(och, xo, top.L, 2.0 ** 50, coeffs)
+    assert (L, sc) == (Lo, so)
+    assert np.array_equal(_export_at(levels, out, L), oo)
+    c = levels[top.L - L]
+    z = c.decode(c.decrypt(out[:2 * L * c.n]), 50) * (2.0 ** 50 / sc)
+    assert np.max(np.abs(z - np.polynomial.chebyshev.chebval(u, coeffs))) < 1e-6
+    say("[chain] two sign steps")
+    v = np.random.default_rng(53).uniform(-0.5, 0.5, top.slots)
+    w, wo = _enc_both(top, levels, och, s, 4 * v, 51, 2)
+    out, L, sc, m = fa.sign_iter(levels, w, top.L, 2.0 ** 50, 4, 2)
+    oo, Lo, so, mo = ckks.sign_iter(och, wo, top.L, 2.0 ** 50, 4, 2)
+    assert (L, sc, m) == (Lo, so, mo)
+    assert np.array_equal(_export_at(levels, out, L), oo)
+    c = levels[top.L - L]
+    z = c.decode(c.decrypt(out[:2 * L * c.n]), 50) * (2.0 ** 50 / sc) / m
+    f = lambda t: (3 * t - t ** 3) / 2
+    assert np.max(np.abs(z - f(f(v)))) < 1e-6
