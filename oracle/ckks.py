@@ -679,28 +679,34 @@ class LevelChain:
 def cheb_eval(ch: LevelChain, u: np.ndarray, Lu: int, su: float, coeffs) -> tuple:
     """sum_k c_k T_k(u) for a ciphertext u (slots in [-1, 1]) by the direct evaluator:
     T_{a+b} = 2 T_a T_b - T_{a-b} with a = b = k/2 (then T_0 = 1) for even k and
-    a = b + 1 for odd k (then T_1), T_2..T_d in order; then every T_k is brought to the
-    lowest level, multiplied by round(c_k * q) for the prime q the final rescale divides
-    out, summed with round(c_0 * s) and rescaled.  Returns (ct, level, scale)."""
+    a = b + 1 for odd k (then T_1), T_2..T_d in order.  Ciphertexts are added at a common
+    scale, so T_{a-b} is brought to the product's scale s_a s_b before the rescale: T_0 as
+    the constant round(s_a s_b), T_1 times the integer round(s_a s_b / s_1) (no level spent).
+    Then every T_k is brought to the lowest level and multiplied by round(c_k q s_u / s_k)
+    -- q the prime the final rescale divides out, s_k the scale T_k carries -- so that every
+    term sits at the one scale s_u q, summed with round(c_0 s_u q) and rescaled.
+    Returns (ct, level, scale s_u)."""
     d = len(coeffs) - 1
     assert d >= 1
     T = {1: (u, Lu, su)}
     for k in range(2, d + 1):
         a, b = (k // 2, k // 2) if k % 2 == 0 else (k // 2 + 1, k // 2)
-        p, L, sp = ch.mul_rescale(*T[a], *T[b])
+        L = min(T[a][1], T[b][1])
         orc = ch.orc[L]
+        p = orc.mul(ch.drop(T[a][0], L), ch.drop(T[b][0], L), ch.rlk[L])
+        sp = T[a][2] * T[b][2]
         p = orc.add(p, p)
         if k % 2 == 0:
-            p = orc.add_const(p, -int(np.rint(1.0 * sp)))
+            p = orc.add_const(p, -int(np.rint(sp)))
         else:
-            p = orc.add(p, ch.drop(T[1][0], L), sub=True)
-        T[k] = (p, L, sp)
+            p = orc.add(p, orc.mul_const(ch.drop(T[1][0], L), int(np.rint(sp / T[1][2]))), sub=True)
+        T[k] = (orc.rescale(p), L - 1, sp / float(ch.q(L)))
     Lmin = min(v[1] for v in T.values())
     qn = ch.q(Lmin)
     orc = ch.orc[Lmin]
     acc = None
     for k in range(1, d + 1):
-        term = orc.mul_const(ch.drop(T[k][0], Lmin), int(np.rint(coeffs[k] * float(qn))))
+        term = orc.mul_const(ch.drop(T[k][0], Lmin), int(np.rint(coeffs[k] * float(qn) * (su / T[k][2]))))
         acc = term if acc is None else orc.add(acc, term)
     s_acc = su * float(qn)
     acc = orc.add_const(acc, int(np.rint(coeffs[0] * s_acc)))
@@ -718,3 +724,43 @@ def sign_iter(ch: LevelChain, V: np.ndarray, L: int, s: float, m: int, iters: in
         V, L, s = ch.mul_rescale(V, L, s, w, Lz, sz)
         m = 2 * m ** 3
     return V, L, s, m
+
+
+def membership(ch: LevelChain, qr: np.ndarray, Lq: int, sq: float, blocks, d: int, B: int, y_lo: float,
+               y_hi: float, coeffs, m: int, iters: int) -> tuple:
+    """Membership scan (paper section 3.1, "Membership search"): whether cos(q, x_i) >= tau is
+    decided under encryption as the sign of <q_R, x_i> - tau |q_R|, with |q_R| from a
+    low-degree Chebyshev series of the square root and the difference pre-scaled into [-1, 1].
+
+    qr: the projected query at level Lq, scale sq, slot s = q_R[s mod d]; blocks: each the
+    [G][B][Lq][N] pre-rotated diagonal plaintexts of up to N/2 candidates at scale
+    2^log_scale; coeffs: the series of tau * sqrt(y) in u = (2y - y_lo - y_hi)/(y_hi - y_lo).
+      1. score_i = Rescale(diagonal product), scale s_sc = sq * 2^log_scale / q;
+      2. y = |q_R|^2 in every slot: Rescale(qr * qr), then y += Rotate(y, 2^k) for 2^k < d;
+      3. u = alpha (y - mid): alpha = 2/(y_hi - y_lo) changes only the scale the
+         ciphertext is read at (s_y / alpha), the shift is the constant round(-mid * s_y);
+      4. t = sum_k c_k T_k(u) by cheb_eval with every c_k multiplied by s_sc / s_u, so t
+         holds tau |q_R| at the scores' scale s_sc;
+      5. out_i = sign_iter(score_i - t (score dropped to t's level), multiplier m).
+    Returns (list of per-block ciphertexts, level, scale, multiplier)."""
+    orc, keys = ch.orc[Lq], ch.keys[Lq]
+    G = d // B
+    qrot = orc.baby_rotations(qr, B, keys)
+    scores = [orc.rescale(orc.bsgs_block(qrot, _c(pts).reshape(G, B, Lq, -1), B, G, keys)) for pts in blocks]
+    s_sc = sq * 2.0 ** ch.top.log_scale / float(ch.q(Lq))
+    y, Ly, sy = ch.mul_rescale(qr, Lq, sq, qr, Lq, sq)
+    k = 1
+    while k < d:
+        y = ch.orc[Ly].add(y, ch.orc[Ly].rotate(y, k, ch.keys[Ly][k]))
+        k <<= 1
+    alpha, mid = 2.0 / (y_hi - y_lo), 0.5 * (y_hi + y_lo)
+    u = ch.orc[Ly].add_const(y, int(np.rint(-mid * sy)))
+    su = sy / alpha
+    ratio = s_sc / su
+    t, Lt, _ = cheb_eval(ch, u, Ly, su, [c * ratio for c in coeffs])
+    outs, res = [], None
+    for sc in scores:
+        diff = ch.orc[Lt].add(ch.drop(sc, Lt), t, sub=True)
+        res = sign_iter(ch, diff, Lt, s_sc, m, iters)
+        outs.append(res[0])
+    return outs, res[1], res[2], res[3]

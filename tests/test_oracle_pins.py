@@ -753,3 +753,56 @@ def test_sign_iteration_matches_the_odd_polynomial():
     assert np.max(np.abs(z - f(f(x)))) < 1e-6
     big = np.abs(x) > 1e-3
     assert np.all(np.sign(z[big]) == np.sign(x[big]))
+
+
+def _membership_setup(logn, L, K, wid, d, B, rot_levels):
+    top = ckks.Params(logn=logn, L=L, K=K, log_scale=50)
+    s = gen.ternary_secret(gen.rng(wid, gen.STREAM_SECRET), top.n)
+    ra = gen.uniform_residues(gen.rng(wid, gen.STREAM_KEY_A, 0), top.primes, top.dnum, top.n)
+    re_ = gen.rounded_gaussian(gen.rng(wid, gen.STREAM_KEY_E, 0), (top.dnum, top.n))
+    steps = sorted(set(ckks.steps_for_bsgs(d, B) + [1 << k for k in range(int(np.log2(d)))]))
+    rot = {r: (gen.uniform_residues(gen.rng(wid, gen.STREAM_KEY_A, r), top.primes, top.dnum, top.n),
+               gen.rounded_gaussian(gen.rng(wid, gen.STREAM_KEY_E, r), (top.dnum, top.n))) for r in steps}
+    return ckks.LevelChain(top, s, (ra, re_), rot, rot_levels=rot_levels), s
+
+
+def _membership_model(X, qR, tau, y_lo, y_hi, coeffs, m, iters):
+    """float64 model of the scan: f^iters((<q_R, x> - chebval(u(|q_R|^2)))/m)."""
+    y = float(qR @ qR)
+    u = (2 * y - y_lo - y_hi) / (y_hi - y_lo)
+    t = np.polynomial.chebyshev.chebval(u, coeffs)
+    x = (X @ qR - t) / m
+    for _ in range(iters):
+        x = (3 * x - x ** 3) / 2
+    return x, t
+
+
+@pytest.mark.parametrize("y_lo,y_hi", [(0.5, 2.5), (0.6, 1.6)])
+def test_membership_scan_decides_the_threshold(y_lo, y_hi):
+    """Membership scan on levels 11 -> 2 (N = 2^11, d = 16, two blocks): every output / m
+    equals the float64 model f(f((<q_R, x_i> - t)/m)) within 1e-5, where t is the
+    degree-7 Chebyshev interpolant of tau sqrt(y) at y = |q_R|^2 (itself within 1e-4 of
+    tau |q_R|), and the output's sign is the decision cos(q_R, x_i) >= tau wherever the
+    margin exceeds the interpolation error.  The second domain has width 1, so the map
+    onto [-1, 1] doubles y (carried by the scale) and the series must be rescaled to the
+    scores' scale by a factor near 2."""
+    d, B, tau, m, iters = 16, 4, 0.6, 4, 2
+    ch, s = _membership_setup(11, 11, 3, 45, d, B, rot_levels=[11, 10])
+    top = ch.top
+    g = np.random.default_rng(45)
+    X = gen.normalize_rows(g.standard_normal((1024 + 500, d)))
+    qR = 1.1 * gen.normalize_rows((X[3] + 0.4 * g.standard_normal(d))[None])[0]
+    half, mid = (y_hi - y_lo) / 2, (y_hi + y_lo) / 2
+    coeffs = np.polynomial.chebyshev.chebinterpolate(lambda u: tau * np.sqrt(mid + half * u), 7)
+    ct = _enc_at(ch, ckks.replicate(qR, top.slots), s, 45, 1)
+    blocks = [ckks.layout_b_pts(X[:1024], top, d, B), ckks.layout_b_pts(X[1024:], top, d, B)]
+    outs, L, sc, mo = ckks.membership(ch, ct, top.L, 2.0 ** 50, blocks, d, B, y_lo, y_hi, coeffs, m, iters)
+    assert (L, mo) == (top.L - 9, 2 * 128 ** 3)
+    want, t = _membership_model(np.vstack([X, np.zeros((2 * top.slots - len(X), d))]), qR, tau, y_lo, y_hi, coeffs, m, iters)
+    assert abs(t - tau * np.linalg.norm(qR)) < 1e-4
+    z = np.concatenate([_dec_at(ch, o, L, sc, s) for o in outs]) / mo
+    assert np.max(np.abs(z - want)) < 1e-5
+    margin = (X @ qR - tau * np.linalg.norm(qR))
+    ok = np.abs(margin) > 2e-4
+    assert np.all(np.sign(z[:len(X)][ok]) == np.sign(margin[ok]))
+    assert 0 < np.count_nonzero(margin > 0) < len(X) // 4
