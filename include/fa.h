@@ -314,6 +314,45 @@ int fa_cheb_eval(fa_ctx* const* levels, int n_levels, const void* u, int L_u, do
 int fa_sign_iter(fa_ctx* const* levels, int n_levels, const void* v, int L_v, double s_v, int64_t m, int iters,
                  void* out, int* L_out, double* s_out, int64_t* m_out, void* ws, size_t ws_bytes, void* stream);
 
+/* Chebyshev interpolation coefficients (coeffs[0..degree]) of
+ * g(u) = tau * sqrt(y(u)), y(u) = (y_lo + y_hi)/2 + u (y_hi - y_lo)/2, on
+ * u in [-1, 1], at the degree + 1 Chebyshev points of the first kind: the
+ * low-degree square-root approximation of the threshold tau |q_R| (Section
+ * 3.1 "Membership search").  Host only.  FA_E_INVAL unless 0 < y_lo < y_hi
+ * and 1 <= degree <= 64. */
+int fa_cheb_fit_sqrt(double tau, double y_lo, double y_hi, int degree, double* coeffs);
+
+/* Membership scan of one projected query against resident candidate blocks
+ * (Section 3.1 "Membership search": the server decides under encryption
+ * whether cos(q, x_i) >= tau, as the sign of <q_R, x_i> - tau |q_R|, with
+ * |q_R| = sqrt(|q_R|^2) by a low-degree Chebyshev series, pre-scaled into
+ * [-1, 1]).  levels: the chain as for fa_cheb_eval; q_r a ciphertext at level
+ * L_q (scale s_q) holding the d-periodic projected query (slot s =
+ * q_R[s mod d], as fa_project_ct writes it, rescaled or not); blocks[i]
+ * diagonal blocks (fa_encode_db_block, FA_LAYOUT_DIAG, baby_step) encoded on
+ * the chain's level-L_q context.  Steps:
+ *   score_i = Rescale(diagonal product of q_r with block i)  (level L_q - 1);
+ *   y = |q_R|^2 in every slot: Rescale(q_r * q_r) folded by y += Rotate(y, 2^k),
+ *       2^k < d (needs level L_q - 1 keys for those steps);
+ *   u = (2y - y_lo - y_hi)/(y_hi - y_lo): the factor taken into the scale,
+ *       the shift an added constant;
+ *   t = sum_k coeffs[k] T_k(u) (fa_cheb_eval's evaluator; coeffs from
+ *       fa_cheb_fit_sqrt or any series of tau |q_R| in u), produced at the
+ *       scores' scale;
+ *   out_i = fa_sign_iter((score_i - t) at t's level, m, iters): with
+ *       x = (score_i - t)/m in [-1, 1], out_i / *m_out approximates
+ *       f^iters(x), f(x) = (3x - x^3)/2, whose sign is the decision.
+ * out: n_blocks ciphertexts at a stride of 2*L_q*N words, each valid in its
+ * first 2*(*L_out)*N words (level *L_out, scale *s_out).  Levels used:
+ * 1 (scores) + ceil(log2 degree) + 1 (series) + 2*iters; FA_E_SHAPE if the
+ * chain is too short.  ws: fa_membership_workspace_bytes(level-L_q context,
+ * n_blocks, d, baby_step, degree) bytes. */
+size_t fa_membership_workspace_bytes(const fa_ctx* ctx_q, int n_blocks, int d, int baby_step, int degree);
+int fa_membership(fa_ctx* const* levels, int n_levels, const void* q_r, int L_q, double s_q,
+                  const void* const* blocks, int n_blocks, int d, int baby_step, double y_lo, double y_hi,
+                  const double* coeffs, int degree, int64_t m, int iters, void* out, int* L_out, double* s_out,
+                  int64_t* m_out, void* ws, size_t ws_bytes, void* stream);
+
 /* ---- measurement -------------------------------------------------------- */
 
 /* Phase timing of subsequent diagonal-layout fa_score_block calls with HIP

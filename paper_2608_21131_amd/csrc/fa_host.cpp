@@ -1668,43 +1668,50 @@ static int chain_mul_rescale(const Chain& ch, const CtRef& a, const CtRef& b, do
   return FA_OK;
 }
 
-int fa_cheb_eval(fa_ctx* const* levels, int n_levels, const void* u, int L_u, double s_u, const double* coeffs,
-                 int degree, void* out, int* L_out, double* s_out, void* ws, size_t ws_bytes, void* stream) {
-  if (!u || !coeffs || !out || !L_out || !s_out) return fail(FA_E_INVAL, "fa_cheb_eval: null argument");
-  if (degree < 1 || degree > 64) return fail(FA_E_INVAL, "degree %d out of [1, 64]", degree);
-  Chain ch;
-  int rc = make_chain(levels, n_levels, ch);
-  if (rc) return rc;
-  fa_ctx* top = levels[0];
-  if (!ch.at(L_u)) return fail(FA_E_SHAPE, "no level %d in the chain", L_u);
-  const size_t need = fa_chain_workspace_bytes(top, degree);
-  if (!ws || ws_bytes < need) return fail(FA_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
-  Arena ar{(char*)ws, ws_bytes, 0};
-  hipStream_t s = (hipStream_t)stream;
-  const size_t ctw = 2 * (size_t)top->L * top->n;
+// sum_k coeffs[k] T_k(u) by the direct evaluator into out (scale u.s); the
+// terms and their scratch come from ar and are released on return
+static int cheb_core(const Chain& ch, const CtRef& u, const double* coeffs, int degree, double* out, CtRef& res,
+                     Arena& ar, hipStream_t s) {
+  const size_t mark = ar.used;
+  const size_t ctw = 2 * (size_t)u.L * ch.at(u.L)->n;
   std::vector<CtRef> T(degree + 1);
-  T[1] = {(double*)u, L_u, s_u};
+  T[1] = u;
+  int rc;
+  // T_k = Rescale(2 T_a T_b - T_{a-b}), with T_{a-b} brought to the product's
+  // scale s_a s_b before the rescale: T_0 = 1 as the constant round(s_a s_b),
+  // T_1 times the integer round(s_a s_b / s_1)
   for (int k = 2; k <= degree; ++k) {
     const int a = k % 2 == 0 ? k / 2 : k / 2 + 1, b = k / 2;
+    const int L = std::min(T[a].L, T[b].L);
+    fa_ctx* c = ch.at(L);
+    if (!c || !ch.at(L - 1)) return fail(FA_E_SHAPE, "the chain has no level %d", L - 1);
     double* dst = ar.take(ctw);
     if (!dst) return fail(FA_E_NOMEM, "workspace too small for the Chebyshev terms");
-    CtRef p;
-    if ((rc = chain_mul_rescale(ch, T[a], T[b], dst, p, ar, s))) return rc;
-    fa_ctx* c = ch.at(p.L);
-    fa::ct_elem(c, p.p, p.p, p.p, 2, nullptr, 2, s);  // 2 T_a T_b
+    const size_t mark_k = ar.used, cw = 2 * (size_t)L * c->n;
+    double* xa = ar.take(cw);
+    double* xb = ar.take(cw);
+    double* prod = ar.take(cw);
+    double* t1 = ar.take(cw);
+    double* scr = ar.take(cw);
+    if (!xa || !xb || !prod || !t1 || !scr) return fail(FA_E_NOMEM, "workspace too small for the Chebyshev terms");
+    if ((rc = drop_to(ch, T[a], L, xa, s)) || (rc = drop_to(ch, T[b], L, xb, s))) return rc;
+    if ((rc = mul_relin(c, xa, xb, prod, ar, s))) return rc;
+    fa::ct_elem(c, prod, prod, prod, 2, nullptr, 2, s);  // 2 T_a T_b
+    const double sp = T[a].s * T[b].s;
     if (k % 2 == 0) {
-      const auto r = const_residues(c, -std::nearbyint(1.0 * p.s));
-      fa::ct_elem(c, p.p, nullptr, p.p, 2, r.data(), 1, s);
+      const auto r = const_residues(c, -std::nearbyint(sp));
+      fa::ct_elem(c, prod, nullptr, prod, 2, r.data(), 1, s);
     } else {
-      double* t1 = ar.take(ctw);
-      if (!t1) return fail(FA_E_NOMEM, "workspace too small for the Chebyshev terms");
-      if ((rc = drop_to(ch, T[1], p.L, t1, s))) return rc;
-      fa::ct_elem(c, p.p, t1, p.p, 2, nullptr, 3, s);
-      ar.used -= rup(ctw);  // t1 released
+      if ((rc = drop_to(ch, T[1], L, t1, s))) return rc;
+      const auto r = const_residues(c, std::nearbyint(sp / T[1].s));
+      fa::ct_elem(c, t1, nullptr, t1, 2, r.data(), 0, s);
+      fa::ct_elem(c, prod, t1, prod, 2, nullptr, 3, s);
     }
-    T[k] = p;
+    fa::rescale(c, prod, 2, dst, scr, s);
+    T[k] = {dst, L - 1, sp / (double)c->primes[L - 1]};
+    ar.used = mark_k;
   }
-  int Lmin = L_u;
+  int Lmin = u.L;
   for (int k = 1; k <= degree; ++k) Lmin = std::min(Lmin, T[k].L);
   fa_ctx* c = ch.at(Lmin);
   if (!ch.at(Lmin - 1)) return fail(FA_E_SHAPE, "the chain has no level %d", Lmin - 1);
@@ -1714,9 +1721,10 @@ int fa_cheb_eval(fa_ctx* const* levels, int n_levels, const void* u, int L_u, do
   double* term = ar.take(cw);
   double* scr = ar.take(2 * (size_t)Lmin * c->n);
   if (!acc || !term || !scr) return fail(FA_E_NOMEM, "workspace too small for the Chebyshev sum");
+  // every term is brought to the one scale u.s * qn: its constant carries u.s / T_k.s
   for (int k = 1; k <= degree; ++k) {
     if ((rc = drop_to(ch, T[k], Lmin, term, s))) return rc;
-    const auto ck = const_residues(c, std::nearbyint(coeffs[k] * qn));
+    const auto ck = const_residues(c, std::nearbyint(coeffs[k] * qn * (u.s / T[k].s)));
     if (k == 1) {
       fa::ct_elem(c, term, nullptr, acc, 2, ck.data(), 0, s);
     } else {
@@ -1724,35 +1732,24 @@ int fa_cheb_eval(fa_ctx* const* levels, int n_levels, const void* u, int L_u, do
       fa::ct_elem(c, acc, term, acc, 2, nullptr, 2, s);
     }
   }
-  const double s_acc = s_u * qn;
+  const double s_acc = u.s * qn;
   const auto c0 = const_residues(c, std::nearbyint(coeffs[0] * s_acc));
   fa::ct_elem(c, acc, nullptr, acc, 2, c0.data(), 1, s);
-  fa::rescale(c, acc, 2, (double*)out, scr, s);
-  *L_out = Lmin - 1;
-  *s_out = s_acc / qn;
-  return check_launch("fa_cheb_eval");
+  fa::rescale(c, acc, 2, out, scr, s);
+  res = {out, Lmin - 1, s_acc / qn};
+  ar.used = mark;
+  return FA_OK;
 }
 
-int fa_sign_iter(fa_ctx* const* levels, int n_levels, const void* v, int L_v, double s_v, int64_t m, int iters,
-                 void* out, int* L_out, double* s_out, int64_t* m_out, void* ws, size_t ws_bytes, void* stream) {
-  if (!v || !out || !L_out || !s_out || !m_out) return fail(FA_E_INVAL, "fa_sign_iter: null argument");
-  if (iters < 1 || iters > 8) return fail(FA_E_INVAL, "iters %d out of [1, 8]", iters);
-  Chain ch;
-  int rc = make_chain(levels, n_levels, ch);
-  if (rc) return rc;
-  fa_ctx* top = levels[0];
-  if (!ch.at(L_v)) return fail(FA_E_SHAPE, "no level %d in the chain", L_v);
-  const size_t need = fa_chain_workspace_bytes(top, 3);
-  if (!ws || ws_bytes < need) return fail(FA_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
-  for (int64_t mm = m, it = 0; it < iters; ++it, mm = 2 * mm * mm * mm)
-    if (mm < 1 || mm > (INT64_C(1) << 20)) return fail(FA_E_INVAL, "multiplier out of range at iteration %d", (int)it);
-  Arena ar{(char*)ws, ws_bytes, 0};
-  hipStream_t s = (hipStream_t)stream;
-  const size_t ctw = 2 * (size_t)top->L * top->n;
+// iters sign steps from V (multiplier m) into out; V is not written
+static int sign_core(const Chain& ch, CtRef V, int64_t m, int iters, double* out, CtRef& res, int64_t& m_out,
+                     Arena& ar, hipStream_t s) {
+  const size_t mark = ar.used;
+  const size_t ctw = 2 * (size_t)V.L * ch.at(V.L)->n;
   double* zb = ar.take(ctw);
   double* vb[2] = {ar.take(ctw), ar.take(ctw)};
   if (!zb || !vb[0] || !vb[1]) return fail(FA_E_NOMEM, "workspace too small for the sign iteration");
-  CtRef V{(double*)v, L_v, s_v};
+  int rc;
   for (int it = 0; it < iters; ++it) {
     const double mm = (double)m;
     CtRef z;
@@ -1763,15 +1760,179 @@ int fa_sign_iter(fa_ctx* const* levels, int n_levels, const void* v, int L_v, do
     fa::ct_elem(c, z.p, nullptr, z.p, 2, m1.data(), 0, s);
     fa::ct_elem(c, z.p, nullptr, z.p, 2, k3.data(), 1, s);
     CtRef nv;
-    double* dst = it == iters - 1 ? (double*)out : vb[it & 1];
+    double* dst = it == iters - 1 ? out : vb[it & 1];
     if ((rc = chain_mul_rescale(ch, V, z, dst, nv, ar, s))) return rc;
     V = nv;
     m = 2 * m * m * m;
   }
-  *L_out = V.L;
-  *s_out = V.s;
-  *m_out = m;
+  res = V;
+  m_out = m;
+  ar.used = mark;
+  return FA_OK;
+}
+
+static int sign_args_ok(int64_t m, int iters) {
+  if (iters < 1 || iters > 8) return fail(FA_E_INVAL, "iters %d out of [1, 8]", iters);
+  for (int64_t mm = m, it = 0; it < iters; ++it, mm = 2 * mm * mm * mm)
+    if (mm < 1 || mm > (INT64_C(1) << 20)) return fail(FA_E_INVAL, "multiplier out of range at iteration %d", (int)it);
+  return FA_OK;
+}
+
+int fa_cheb_eval(fa_ctx* const* levels, int n_levels, const void* u, int L_u, double s_u, const double* coeffs,
+                 int degree, void* out, int* L_out, double* s_out, void* ws, size_t ws_bytes, void* stream) {
+  if (!u || !coeffs || !out || !L_out || !s_out) return fail(FA_E_INVAL, "fa_cheb_eval: null argument");
+  if (degree < 1 || degree > 64) return fail(FA_E_INVAL, "degree %d out of [1, 64]", degree);
+  Chain ch;
+  int rc = make_chain(levels, n_levels, ch);
+  if (rc) return rc;
+  if (!ch.at(L_u)) return fail(FA_E_SHAPE, "no level %d in the chain", L_u);
+  const size_t need = fa_chain_workspace_bytes(levels[0], degree);
+  if (!ws || ws_bytes < need) return fail(FA_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
+  Arena ar{(char*)ws, ws_bytes, 0};
+  CtRef res;
+  if ((rc = cheb_core(ch, {(double*)u, L_u, s_u}, coeffs, degree, (double*)out, res, ar, (hipStream_t)stream)))
+    return rc;
+  *L_out = res.L;
+  *s_out = res.s;
+  return check_launch("fa_cheb_eval");
+}
+
+int fa_sign_iter(fa_ctx* const* levels, int n_levels, const void* v, int L_v, double s_v, int64_t m, int iters,
+                 void* out, int* L_out, double* s_out, int64_t* m_out, void* ws, size_t ws_bytes, void* stream) {
+  if (!v || !out || !L_out || !s_out || !m_out) return fail(FA_E_INVAL, "fa_sign_iter: null argument");
+  int rc = sign_args_ok(m, iters);
+  if (rc) return rc;
+  Chain ch;
+  if ((rc = make_chain(levels, n_levels, ch))) return rc;
+  if (!ch.at(L_v)) return fail(FA_E_SHAPE, "no level %d in the chain", L_v);
+  const size_t need = fa_chain_workspace_bytes(levels[0], 3);
+  if (!ws || ws_bytes < need) return fail(FA_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
+  Arena ar{(char*)ws, ws_bytes, 0};
+  CtRef res;
+  if ((rc = sign_core(ch, {(double*)v, L_v, s_v}, m, iters, (double*)out, res, *m_out, ar, (hipStream_t)stream)))
+    return rc;
+  *L_out = res.L;
+  *s_out = res.s;
   return check_launch("fa_sign_iter");
+}
+
+int fa_cheb_fit_sqrt(double tau, double y_lo, double y_hi, int degree, double* coeffs) {
+  if (!coeffs) return fail(FA_E_INVAL, "fa_cheb_fit_sqrt: null argument");
+  if (degree < 1 || degree > 64) return fail(FA_E_INVAL, "degree %d out of [1, 64]", degree);
+  if (!(y_lo > 0) || !(y_hi > y_lo)) return fail(FA_E_INVAL, "need 0 < y_lo < y_hi");
+  // interpolation at the n = degree + 1 Chebyshev points of the first kind,
+  // u_j = cos(pi (j + 1/2) / n):  c_k = (2/n) sum_j g(u_j) cos(k pi (j + 1/2) / n), c_0 halved
+  const int n = degree + 1;
+  const double pi = 3.14159265358979323846;
+  const double half = 0.5 * (y_hi - y_lo), mid = 0.5 * (y_hi + y_lo);
+  std::vector<double> g(n);
+  for (int j = 0; j < n; ++j) g[j] = tau * std::sqrt(mid + half * std::cos(pi * (j + 0.5) / n));
+  for (int k = 0; k < n; ++k) {
+    double acc = 0;
+    for (int j = 0; j < n; ++j) acc += g[j] * std::cos(pi * k * (j + 0.5) / n);
+    coeffs[k] = (k ? 2.0 : 1.0) * acc / n;
+  }
+  return FA_OK;
+}
+
+static bool has_rotations(const fa_ctx* c, const std::vector<int>& steps) {
+  for (int r : steps)
+    if (!c->keys.count(r)) return false;
+  return true;
+}
+
+size_t fa_membership_workspace_bytes(const fa_ctx* cq, int n_blocks, int d, int baby_step, int degree) {
+  if (!cq || n_blocks < 1 || d < 1 || baby_step < 1 || d % baby_step || degree < 1) return 0;
+  const size_t ctw = 2 * (size_t)cq->L * cq->n;
+  const size_t nb = (size_t)n_blocks;
+  const size_t scoring = nb * rup(ctw) + std::max(score_ws(cq, n_blocks, d, baby_step), rup(nb * ctw));
+  const size_t chain = 4 * rup(ctw) + rotate_ws(cq, 1) + fa_chain_workspace_bytes(cq, std::max(degree, 3));
+  return nb * rup(ctw) + std::max(scoring, chain);
+}
+
+int fa_membership(fa_ctx* const* levels, int n_levels, const void* q_r, int L_q, double s_q,
+                  const void* const* blocks, int n_blocks, int d, int baby_step, double y_lo, double y_hi,
+                  const double* coeffs, int degree, int64_t m, int iters, void* out, int* L_out, double* s_out,
+                  int64_t* m_out, void* ws, size_t ws_bytes, void* stream) {
+  if (!q_r || !blocks || !coeffs || !out || !L_out || !s_out || !m_out)
+    return fail(FA_E_INVAL, "fa_membership: null argument");
+  if (n_blocks < 1) return fail(FA_E_SHAPE, "n_blocks must be positive");
+  for (int i = 0; i < n_blocks; ++i)
+    if (!blocks[i]) return fail(FA_E_INVAL, "block %d is null", i);
+  if (degree < 1 || degree > 64) return fail(FA_E_INVAL, "degree %d out of [1, 64]", degree);
+  if (!(y_hi > y_lo)) return fail(FA_E_INVAL, "need y_lo < y_hi");
+  int rc = sign_args_ok(m, iters);
+  if (rc) return rc;
+  Chain ch;
+  if ((rc = make_chain(levels, n_levels, ch))) return rc;
+  fa_ctx* cq = ch.at(L_q);
+  fa_ctx* cy = ch.at(L_q - 1);
+  if (!cq || !cy) return fail(FA_E_SHAPE, "the chain has no level %d or %d", L_q, L_q - 1);
+  const int S = cq->n / 2;
+  if (d < 2 || (d & (d - 1)) || d > S) return fail(FA_E_SHAPE, "d=%d must be a power of two in [2, N/2]", d);
+  if (baby_step < 1 || d % baby_step) return fail(FA_E_INVAL, "baby_step %d must divide d=%d", baby_step, d);
+  std::vector<int> fold;
+  for (int k = 1; k < d; k <<= 1) fold.push_back(k);
+  if (!has_rotations(cy, fold)) return fail(FA_E_NOKEY, "level %d lacks a rotation key for the norm's fold", L_q - 1);
+  const size_t need = fa_membership_workspace_bytes(cq, n_blocks, d, baby_step, degree);
+  if (!ws || ws_bytes < need) return fail(FA_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
+  Arena ar{(char*)ws, ws_bytes, 0};
+  hipStream_t s = (hipStream_t)stream;
+  const size_t n = cq->n, ctw_q = 2 * (size_t)L_q * n, ctw_y = 2 * (size_t)(L_q - 1) * n;
+
+  // scores <q_R, x_i> of every block, rescaled: level L_q - 1, scale s_sc
+  double* scores = ar.take((size_t)n_blocks * ctw_y);
+  const size_t base = ar.used;
+  double* raw = ar.take((size_t)n_blocks * ctw_q);
+  if (!scores || !raw) return fail(FA_E_NOMEM, "workspace too small for the scores");
+  if ((rc = score_diag(cq, (const double*)q_r, (const double* const*)blocks, n_blocks, d, baby_step, raw, ar, s)))
+    return rc;
+  ar.used = base + rup((size_t)n_blocks * ctw_q);
+  double* scr = ar.take((size_t)n_blocks * ctw_q);
+  if (!scr) return fail(FA_E_NOMEM, "workspace too small for the scores' rescale");
+  fa::rescale(cq, raw, 2 * n_blocks, scores, scr, s);
+  const double s_sc = s_q * std::ldexp(1.0, cq->log_scale) / (double)cq->primes[L_q - 1];
+  ar.used = base;
+
+  // y = |q_R|^2 in every slot: the rescaled square folded over d slots
+  double* yb = ar.take(ctw_q);
+  double* tb = ar.take(ctw_q);
+  double* db = ar.take(ctw_q);
+  double* rb = ar.take(ctw_q);
+  if (!yb || !tb || !db || !rb) return fail(FA_E_NOMEM, "workspace too small for the threshold");
+  CtRef q{(double*)q_r, L_q, s_q}, y;
+  if ((rc = chain_mul_rescale(ch, q, q, yb, y, ar, s))) return rc;
+  for (int r : fold) {
+    if ((rc = rotate_batch(cy, yb, 1, r, rb, ar, s))) return rc;
+    fa::add_automorph(cy, yb, rb, 2, 1u, s);
+  }
+  // u = alpha (y - mid) in [-1, 1]: the factor alpha costs nothing, it is taken
+  // into the scale (u at scale y.s / alpha); the shift is an added constant
+  const double alpha = 2.0 / (y_hi - y_lo), mid = 0.5 * (y_hi + y_lo);
+  const auto cm = const_residues(cy, std::nearbyint(-mid * y.s));
+  fa::ct_elem(cy, yb, nullptr, yb, 2, cm.data(), 1, s);
+  const CtRef u{yb, y.L, y.s / alpha};
+  // t = tau |q_R| at the scores' scale: the coefficients carry s_sc / s_u
+  std::vector<double> cf(degree + 1);
+  const double ratio = s_sc / u.s;
+  for (int k = 0; k <= degree; ++k) cf[k] = coeffs[k] * ratio;
+  CtRef t;
+  if ((rc = cheb_core(ch, u, cf.data(), degree, tb, t, ar, s))) return rc;
+
+  // per block: sign of (score - t) / m
+  CtRef res{};
+  int64_t mo = m;
+  for (int i = 0; i < n_blocks; ++i) {
+    fa_ctx* ct = ch.at(t.L);
+    if ((rc = drop_to(ch, {scores + (size_t)i * ctw_y, L_q - 1, s_sc}, t.L, db, s))) return rc;
+    fa::ct_elem(ct, db, tb, db, 2, nullptr, 3, s);
+    if ((rc = sign_core(ch, {db, t.L, s_sc}, m, iters, (double*)out + (size_t)i * ctw_q, res, mo, ar, s)))
+      return rc;
+  }
+  *L_out = res.L;
+  *s_out = res.s;
+  *m_out = mo;
+  return check_launch("fa_membership");
 }
 
 int fa_rotate(fa_ctx* c, const void* ct, int step, void* out, void* ws, size_t ws_bytes, void* stream) {

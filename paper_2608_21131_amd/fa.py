@@ -94,6 +94,15 @@ SIGNATURES = {
                                     ctypes.c_int64, ctypes.c_int, _vp, ctypes.POINTER(ctypes.c_int),
                                     ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64), _vp,
                                     ctypes.c_size_t, _vp]),
+    "fa_cheb_fit_sqrt": (ctypes.c_int, [ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.c_int, _f64p]),
+    "fa_membership_workspace_bytes": (ctypes.c_size_t, [_vp, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                                        ctypes.c_int]),
+    "fa_membership": (ctypes.c_int, [ctypes.POINTER(_vp), ctypes.c_int, _vp, ctypes.c_int, ctypes.c_double,
+                                     ctypes.POINTER(_vp), ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                     ctypes.c_double, ctypes.c_double, _f64p, ctypes.c_int, ctypes.c_int64,
+                                     ctypes.c_int, _vp, ctypes.POINTER(ctypes.c_int),
+                                     ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64), _vp,
+                                     ctypes.c_size_t, _vp]),
     "fa_batch_workspace_bytes": (ctypes.c_size_t, [_vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int]),
     "fa_score_batch": (ctypes.c_int, [_vp, ctypes.POINTER(_vp), ctypes.POINTER(_vp), ctypes.c_int,
                                       ctypes.POINTER(_vp), ctypes.c_int, ctypes.c_int, ctypes.c_int,
@@ -457,4 +466,40 @@ def sign_iter(levels, v: torch.Tensor, L_v: int, s_v: float, m: int, iters: int,
     _check(top.lib.fa_sign_iter(arr, nl, _dev(v), L_v, s_v, int(m), iters, _dev(out), ctypes.byref(L_out),
                                 ctypes.byref(s_out), ctypes.byref(m_out), _dev(ws), ws.numel() * 8,
                                 _stream(stream)))
+    return out, L_out.value, s_out.value, m_out.value
+
+
+def cheb_fit_sqrt(tau: float, y_lo: float, y_hi: float, degree: int) -> np.ndarray:
+    """Chebyshev coefficients of tau * sqrt(y) for y in [y_lo, y_hi] mapped onto [-1, 1]."""
+    lib = load_library()
+    out = np.zeros(degree + 1, dtype=np.float64)
+    _check(lib.fa_cheb_fit_sqrt(float(tau), float(y_lo), float(y_hi), int(degree), _ptr(out, _f64p)))
+    return out
+
+
+def membership_workspace(ctx_q, n_blocks: int, d: int, baby_step: int, degree: int) -> torch.Tensor:
+    nbytes = int(ctx_q.lib.fa_membership_workspace_bytes(ctx_q.h, n_blocks, d, baby_step, degree))
+    return torch.empty(max(1, nbytes // 8 + 32), dtype=torch.float64, device="cuda")
+
+
+def membership(levels, q_r: torch.Tensor, L_q: int, s_q: float, blocks, d: int, baby_step: int, y_lo: float,
+               y_hi: float, coeffs, m: int, iters: int, out: torch.Tensor | None = None,
+               ws: torch.Tensor | None = None, stream=None):
+    """Membership scan of a projected query against diagonal blocks encoded at level L_q;
+    returns (out, level, scale, multiplier): out holds one ciphertext per block at a
+    stride of the level-L_q ciphertext size."""
+    top = levels[0]
+    arr, nl = _levels_arg(levels)
+    cq = levels[top.L - L_q]
+    blocks = list(blocks)
+    nb = len(blocks)
+    c = _np(coeffs, np.float64)
+    out = cq.new_ct(nb) if out is None else out
+    ws = membership_workspace(cq, nb, d, baby_step, len(c) - 1) if ws is None else ws
+    barr = (_vp * nb)(*[ctypes.c_void_p(b.data_ptr()) for b in blocks])
+    L_out, s_out, m_out = ctypes.c_int(0), ctypes.c_double(0.0), ctypes.c_int64(0)
+    _check(top.lib.fa_membership(arr, nl, _dev(q_r), L_q, s_q, barr, nb, d, baby_step, float(y_lo), float(y_hi),
+                                 _ptr(c, _f64p), len(c) - 1, int(m), iters, _dev(out), ctypes.byref(L_out),
+                                 ctypes.byref(s_out), ctypes.byref(m_out), _dev(ws), ws.numel() * 8,
+                                 _stream(stream)))
     return out, L_out.value, s_out.value, m_out.value

@@ -6,6 +6,7 @@ import os
 import re
 import shutil
 
+import numpy as np
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -49,3 +50,16 @@ def test_binding_matches_header(lib):
 def test_last_error_is_callable_without_gpu(lib):
     lib.fa_last_error.restype = ctypes.c_char_p
     assert isinstance(lib.fa_last_error(), bytes)
+
+
+def test_chebyshev_square_root_fit_matches_numpy(lib):
+    """fa_cheb_fit_sqrt (host only) is Chebyshev interpolation at the first-kind points:
+    numpy's chebinterpolate of the same function agrees to rounding."""
+    from paper_2608_21131_amd import fa
+    for tau, lo, hi, deg in [(0.6, 0.5, 2.5, 7), (1.0, 0.1, 1.0, 12), (0.3, 1.0, 9.0, 3)]:
+        got = fa.cheb_fit_sqrt(tau, lo, hi, deg)
+        half, mid = (hi - lo) / 2, (hi + lo) / 2
+        ref = np.polynomial.chebyshev.chebinterpolate(lambda u: tau * np.sqrt(mid + half * u), deg)
+        assert np.max(np.abs(got - ref)) < 1e-14
+    with pytest.raises(fa.FaError):
+        fa.cheb_fit_sqrt(0.6, 0.0, 2.5, 7)

@@ -481,3 +481,56 @@ def test_chebyshev_and_sign_parity():
     z = c.decode(c.decrypt(out[:2 * L * c.n]), 50) * (2.0 ** 50 / sc) / m
     f = lambda t: (3 * t - t ** 3) / 2
     assert np.max(np.abs(z - f(f(v)))) < 1e-6
+
+
+def _gpu_membership_chain(logn, L, K, wid, d, B):
+    from paper_2608_21131_amd import fa
+    top = ckks.Params(logn=logn, L=L, K=K, log_scale=50)
+    s = gen.ternary_secret(gen.rng(wid, gen.STREAM_SECRET), top.n)
+    ra = gen.uniform_residues(gen.rng(wid, gen.STREAM_KEY_A, 0), top.primes, top.dnum, top.n)
+    re_ = gen.rounded_gaussian(gen.rng(wid, gen.STREAM_KEY_E, 0), (top.dnum, top.n))
+    steps = sorted(set(ckks.steps_for_bsgs(d, B) + [1 << k for k in range(int(np.log2(d)))]))
+    rot = {r: (gen.uniform_residues(gen.rng(wid, gen.STREAM_KEY_A, r), top.primes, top.dnum, top.n),
+               gen.rounded_gaussian(gen.rng(wid, gen.STREAM_KEY_E, r), (top.dnum, top.n))) for r in steps}
+    ctx = fa.Context(logn, L, K, 50)
+    assert ctx.primes == top.primes
+    ctx.keygen_relin(s, ra, re_)
+    ctx.keygen(s, steps, np.stack([rot[r][0] for r in steps]), np.stack([rot[r][1] for r in steps]))
+    levels = [ctx] + [ctx.at_level(l) for l in range(L - 1, 1, -1)]
+    och = ckks.LevelChain(top, s, (ra, re_), rot, rot_levels=[L, L - 1])
+    return top, s, levels, och
+
+
+@pytest.mark.parametrize("y_lo,y_hi", [(0.5, 2.5), (0.6, 1.6)])
+def test_membership_scan_parity(y_lo, y_hi):
+    """The membership scan (scores, |q_R|^2 by square and fold, Chebyshev tau |q_R|, two
+    sign steps; levels 11 -> 2 at N = 2^11, d = 16, a full and a ragged block) writes the
+    oracle's ciphertexts word for word, and its decrypted signs are the decisions
+    cos(q_R, x_i) >= tau wherever the margin exceeds the series' error."""
+    from paper_2608_21131_amd import fa
+    d, B, tau, m, iters = 16, 4, 0.6, 4, 2
+    top, s, levels, och = _gpu_membership_chain(11, 11, 3, 46, d, B)
+    g = np.random.default_rng(46)
+    X = gen.normalize_rows(g.standard_normal((top.slots + 500, d)))
+    qR = 1.1 * gen.normalize_rows((X[3] + 0.4 * g.standard_normal(d))[None])[0]
+    coeffs = fa.cheb_fit_sqrt(tau, y_lo, y_hi, 7)
+    x, xo = _enc_both(top, levels, och, s, ckks.replicate(qR, top.slots), 46, 1)
+    parts = [X[:top.slots], X[top.slots:]]
+    blocks = [levels[0].encode_db_block_int(ckks.layout_b_coeffs(b, top, d, B)) for b in parts]
+    oblocks = [ckks.layout_b_pts(b, top, d, B) for b in parts]
+    say(f"[membership] N=2^11 L=11 d={d} domain [{y_lo}, {y_hi}]")
+    out, L, sc, mo = fa.membership(levels, x, top.L, 2.0 ** 50, blocks, d, B, y_lo, y_hi, coeffs, m, iters)
+    oo, Lo, so, mo2 = ckks.membership(och, xo, top.L, 2.0 ** 50, oblocks, d, B, y_lo, y_hi, coeffs, m, iters)
+    assert (L, sc, mo) == (Lo, so, mo2) and L == 2
+    ctw = levels[0].ct_words
+    c = levels[top.L - L]
+    z = []
+    for i in range(2):
+        blk = out[i * ctw:i * ctw + 2 * L * c.n]
+        assert np.array_equal(_export_at(levels, blk, L), oo[i]), i
+        z.append(c.decode(c.decrypt(blk), 50) * (2.0 ** 50 / sc) / mo)
+    z = np.concatenate(z)[:len(X)]
+    margin = X @ qR - tau * np.linalg.norm(qR)
+    ok = np.abs(margin) > 2e-4
+    assert np.all(np.sign(z[ok]) == np.sign(margin[ok]))
+    assert 0 < np.count_nonzero(margin > 0) < len(X) // 4
