@@ -59,6 +59,9 @@ def parse():
                     help="rerank: also time the encrypted-database variant (ct x ct, database diagonals encrypted "
                          "and enrolled at this many primes, lazy relinearisation) and report it under enc_db "
                          "(0: skip; 12: all primes)")
+    ap.add_argument("--membership", type=int, default=1,
+                    help="rerank: also time the face membership scan (222,049 centroids, encrypted threshold) "
+                         "and report it under membership (0: skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-check", action="store_true", help="skip the decrypt-and-compare check")
     ap.add_argument("--copy-calib", action="store_true",
@@ -227,6 +230,94 @@ def run_enc_level(bn, args, level):
            "database_bytes": stream_bytes, "level_hbm_floor_ms": round(stream_bytes / (HBM_PEAK_GBS * 1e9) * 1e3, 4),
            "mac_achieved_GBs": round(mac_bytes / (ph["mac_ms"] * 1e-3) / 1e9, 1), "max_abs_score_err": err}
     del blocks
+    torch.cuda.empty_cache()
+    return res
+
+
+def run_membership(bn, args):
+    """The face membership scan (section 3.1, "Membership search"): per step one encrypted 512-d
+    query (scale 2^50, 12 primes) is projected to R = 128 under encryption, rescaled, scored
+    against all 222,049 centroids enrolled at 11 primes, and every candidate's decision
+    cos >= tau is evaluated under encryption (|q_R|^2 by square and fold, tau |q_R| by the
+    degree-7 Chebyshev series, two sign steps; levels 12 -> 2).  Its own context and keys."""
+    fa, torch, wl = bn.fa, bn.torch, bn.wl
+    w = wl.WORKLOADS["face"]
+    x = w.extra
+    ls = x["log_scale"]
+    t = time.time()
+    ctx = fa.Context(w.log_n, w.L, w.K, ls)
+    s = wl.secret(w)
+    ctx.set_secret(s)
+    steps = wl.rotation_steps(w)
+    ctx.keygen_relin(s, *wl.relin_randomness(w, ctx.primes, ctx.dnum))
+    for i in range(0, len(steps), 8):
+        chunk = steps[i:i + 8]
+        rand = [wl.key_randomness(w, r, ctx.primes, ctx.dnum) for r in chunk]
+        ctx.keygen(s, chunk, np.stack([v[0] for v in rand]), np.stack([v[1] for v in rand]))
+    levels = [ctx] + [ctx.at_level(l) for l in range(w.L - 1, 1, -1)]
+    c11 = levels[1]
+    W = wl.projection(w)
+    R, B, Bp, S, nb = w.d, w.B, w.B_proj, w.slots, w.n_blocks
+    wpts = ctx.encode_projection(W.astype(np.float32), Bp)
+    Xr = wl.projected_rows(w, W)
+    blocks = [c11.encode_db_block(Xr[i * S:(i + 1) * S].astype(np.float32), R, fa.LAYOUT_DIAG, B)
+              for i in range(nb)]
+    qs, ids = wl.face_queries(w, 1)
+    q = qs[0]
+    a, e = wl.enc_randomness(w, ctx.primes[:w.L])
+    ct = ctx.encrypt(ctx.encode(np.tile(q, S // w.d_in), ls), a, e)
+    coeffs = fa.cheb_fit_sqrt(x["tau"], x["y_lo"], x["y_hi"], x["degree"])
+    s_q = 2.0 ** (2 * ls) / ctx.primes[w.L - 1]
+    qr, q11, out = ctx.new_ct(), c11.new_ct(), c11.new_ct(nb)
+    ws_p = ctx.workspace(fa.OP_PROJECT, 1, R, Bp)
+    ws_r = torch.empty(2 * w.L * w.n + 32, dtype=torch.float64, device="cuda")
+    ws_m = fa.membership_workspace(c11, nb, R, B, x["degree"])
+    torch.cuda.synchronize()
+    log(f"[bench] face: keys, {len(levels)} levels, {nb} blocks of {R} diagonals at {c11.L} primes "
+        f"({time.time() - t:.1f}s)")
+    res_m = {}
+
+    def project():
+        ctx.project_ct(ct, wpts, w.d_in, R, Bp, out=qr, ws=ws_p)
+        ctx.rescale(c11, qr, out=q11, ws=ws_r)
+
+    def scan():
+        res_m["r"] = fa.membership(levels, q11, c11.L, s_q, blocks, R, B, x["y_lo"], x["y_hi"], coeffs, x["m"],
+                                   x["iters"], out=out, ws=ws_m)
+
+    def step():
+        project()
+        scan()
+
+    ms = bn.timed(step, args.steps, args.warmup)
+    ms_proj = bn.timed(project, args.steps, 1)
+    ms_scan = bn.timed(scan, args.steps, 1)
+    _, L, sc, mo = res_m["r"]
+    res = {"workload": w.desc, "ms_per_query": round(ms, 4), "value": round(w.rows / (ms * 1e-3), 1),
+           "unit": "decisions/s", "phases_ms": {"project_and_rescale_ms": round(ms_proj, 4),
+                                                "scan_ms": round(ms_scan, 4)},
+           "levels": f"{w.L} -> {L}", "tau": x["tau"], "chebyshev_degree": x["degree"],
+           "sign_steps": x["iters"], "database_bytes": 8 * nb * R * c11.L * w.n,
+           "paper_warm_latency_s_context": 7.0}
+    if not args.no_check:
+        ctw = c11.ct_words
+        c2 = levels[w.L - L]
+        z = np.concatenate([c2.decode(c2.decrypt(out[i * ctw:i * ctw + 2 * L * c2.n]), ls) for i in range(nb)])
+        z = z[:w.rows] * (2.0 ** ls / sc) / mo
+        qR = W.astype(np.float32).astype(np.float64).T @ q
+        Xm = Xr.astype(np.float32).astype(np.float64)
+        y = float(qR @ qR)
+        u = (2 * y - x["y_lo"] - x["y_hi"]) / (x["y_hi"] - x["y_lo"])
+        tq = float(np.polynomial.chebyshev.chebval(u, coeffs))
+        v = (Xm @ qR - tq) / x["m"]
+        for _ in range(x["iters"]):
+            v = (3 * v - v ** 3) / 2
+        margin = Xm @ qR - x["tau"] * np.sqrt(y)
+        ok = np.abs(margin) > abs(tq - x["tau"] * np.sqrt(y)) + 1e-4
+        res.update({"max_abs_err_vs_float64": float(np.max(np.abs(z - v))),
+                    "decision_mismatches": int(np.count_nonzero(np.sign(z[ok]) != np.sign(margin[ok]))),
+                    "matches": np.flatnonzero(z > 0).tolist(), "query_identity": int(ids[0])})
+    del blocks, levels
     torch.cuda.empty_cache()
     return res
 
@@ -656,6 +747,9 @@ def main():
         for qb in res["query_batch"]:
             log(f"[bench] batch of {qb['queries']} at {qb['scoring_level_primes']} primes: "
                 f"{qb['ms_per_query_level']:.3f} ms per query level, {qb['value'] / 1e6:.1f} M scores/s")
+    if extra and args.membership:
+        res["membership"] = run_membership(bn, args)
+        log(f"[bench] face membership scan: {res['membership']['ms_per_query']:.3f} ms per query")
     print(json.dumps(res), flush=True)
 
 

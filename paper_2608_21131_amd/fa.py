@@ -374,10 +374,11 @@ class Context:
         return torch.empty(max(1, nbytes // 8 + 32), dtype=torch.float64, device="cuda")
 
     def rescale(self, lo: "Context", ct: torch.Tensor, n_polys: int = 2, out: torch.Tensor | None = None,
-                stream=None) -> torch.Tensor:
+                ws: torch.Tensor | None = None, stream=None) -> torch.Tensor:
         """round(ct / last prime) at the next level down (lo = this context minus that prime)."""
         out = torch.empty(n_polys * lo.L * lo.n, dtype=torch.float64, device="cuda") if out is None else out
-        ws = torch.empty(n_polys * self.L * self.n + 32, dtype=torch.float64, device="cuda")
+        if ws is None:
+            ws = torch.empty(n_polys * self.L * self.n + 32, dtype=torch.float64, device="cuda")
         _check(self.lib.fa_rescale(self.h, lo.h, _dev(ct), n_polys, _dev(out), _dev(ws), ws.numel() * 8,
                                    _stream(stream)))
         return out

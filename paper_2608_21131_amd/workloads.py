@@ -75,6 +75,12 @@ WORKLOADS = {
              "32 encrypted queries back to back, CKKS N=2^16, 12+3 primes",
         extra=dict(coarse=222_049, fine_pool_blocks=4, fine_blocks=2, rerank_pool_blocks=8, rerank_blocks=4,
                    rerank_last=11_696, queries=32, top_coarse=16, top_fine=64)),
+    "face": Workload(
+        "face", 16, 12, 3, rows=222_049, dim=128, d=128, B=16, wid=7, d_in=512, B_proj=16,
+        desc="face membership scan: 222,049 identity centroids (unit 512-d rows, projected to R=128 and "
+             "re-normalised) against one encrypted 512-d query, cos >= tau decided under encryption; "
+             "CKKS N=2^16, 12+3 primes of 50 bits, scale 2^50 with rescaling, levels 12 -> 2",
+        extra=dict(log_scale=50, tau=0.5, y_lo=0.5, y_hi=2.5, degree=7, m=4, iters=2, query_noise=1.0)),
 }
 
 
@@ -91,11 +97,26 @@ def candidate_rows(w: Workload, n_rows: int | None = None, stream_extra: int = 0
     return gen.gaussian_unit_rows(g, n_rows, w.dim).astype(np.float32), None
 
 
+def raw_rows(w: Workload) -> np.ndarray:
+    """The d_in-dimensional unit N(0, I) rows behind a projected workload (float64)."""
+    return gen.gaussian_unit_rows(gen.rng(w.wid, gen.STREAM_DB), w.rows, w.d_in)
+
+
 def projected_rows(w: Workload, W: np.ndarray) -> np.ndarray:
-    """Candidates of the rank-reduction workload: normalise(W^T x) for unit N(0, I) rows x
-    of dimension d_in, re-normalised at enrollment as the paper's client does (float64)."""
-    g = gen.rng(w.wid, gen.STREAM_DB)
-    return gen.normalize_rows(gen.gaussian_unit_rows(g, w.rows, w.d_in) @ W)
+    """Candidates of a projected workload: normalise(W^T x) for its raw rows x, re-normalised
+    at enrollment as the paper's client does (float64)."""
+    return gen.normalize_rows(raw_rows(w) @ W)
+
+
+def face_queries(w: Workload, count: int = 1):
+    """Queries of the membership workload: each a noisy view of one enrolled identity,
+    q = normalise(c_j + rho z/|z|) with z ~ N(0, I) and rho = query_noise, so that
+    cos(q, c_j) is about 1/sqrt(1 + rho^2).  Returns (queries [count][d_in], identities j)."""
+    g = gen.rng(w.wid, gen.STREAM_QUERY)
+    C = raw_rows(w)
+    j = g.integers(0, w.rows, count)
+    z = gen.normalize_rows(g.standard_normal((count, w.d_in)))
+    return gen.normalize_rows(C[j] + w.extra["query_noise"] * z), j
 
 
 def query_vectors(w: Workload, count: int = 1, centers=None) -> np.ndarray:

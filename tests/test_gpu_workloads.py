@@ -331,3 +331,91 @@ def test_rerank_encrypted_database_at_three_primes_fullsize():
         err = max(err, float(np.max(np.abs(z[:len(rows)] - rows @ q))))
     say(f"[enc] max |score - float64| = {err:.2e}")
     assert err < 1e-4
+
+
+def test_membership_face_scan_fullsize():
+    """The face membership scan at full size, as bench.py times it: an encrypted 512-d query
+    (scale 2^50, 12 primes) projected to R = 128 and rescaled, then 222,049 centroids in 7
+    blocks at 11 primes, tau |q_R| by the degree-7 Chebyshev series and two sign steps
+    (levels 12 -> 2).  The projected query and the ragged last block's output are bit-exact
+    against the oracle; every output is within 1e-4 of the float64 model, every decision
+    whose margin exceeds the series' error is cos >= tau, and the query's own identity is
+    the one match."""
+    from paper_2608_21131_amd import fa
+    w = wl.WORKLOADS["face"]
+    x = w.extra
+    top = ckks.Params(logn=w.log_n, L=w.L, K=w.K, log_scale=x["log_scale"])
+    S, R, B, Bp = top.slots, w.d, w.B, w.B_proj
+    ctx = fa.Context(w.log_n, w.L, w.K, x["log_scale"])
+    assert ctx.primes == top.primes
+    s = wl.secret(w)
+    steps = wl.rotation_steps(w)
+    rlk = wl.relin_randomness(w, top.primes, top.dnum)
+    rot = {r: wl.key_randomness(w, r, top.primes, top.dnum) for r in steps}
+    say(f"[face] keys: relinearisation + {len(steps)} rotations, then levels 11..2")
+    ctx.keygen_relin(s, *rlk)
+    for i in range(0, len(steps), 8):
+        chunk = steps[i:i + 8]
+        ctx.keygen(s, chunk, np.stack([rot[r][0] for r in chunk]), np.stack([rot[r][1] for r in chunk]))
+    levels = [ctx] + [ctx.at_level(l) for l in range(w.L - 1, 1, -1)]
+    W = wl.projection(w)
+    qs, ids = wl.face_queries(w)
+    q, ident = qs[0], int(ids[0])
+    m = ckks.encode(ckks.replicate(q, S), top.n, x["log_scale"])
+    a, e = wl.enc_randomness(w, top.q)
+    ct = ctx.encrypt(m, a, e)
+    pre = ckks.prerotate(ckks.projection_diagonals(W, S), Bp)
+    wco = np.stack([ckks.encode(pre[g, b], top.n, x["log_scale"]) for g in range(R // Bp) for b in range(Bp)])
+    say("[face] projection and rescale on the GPU")
+    qr = ctx.project_ct(ct, ctx.encode_db_block_int(wco), w.d_in, R, Bp)
+    q11 = ctx.rescale(levels[1], qr)
+    s_q = 2.0 ** (2 * x["log_scale"]) / top.q[-1]
+    Xr = wl.projected_rows(w, W)
+    nb = w.n_blocks
+    lp = ckks.Params(logn=w.log_n, L=w.L - 1, K=w.K, log_scale=x["log_scale"], primes=top.q[:w.L - 1] + top.p)
+    last = Xr[(nb - 1) * S:]
+    blocks = [levels[1].encode_db_block(Xr[i * S:(i + 1) * S].astype(np.float32), R, fa.LAYOUT_DIAG, B)
+              for i in range(nb - 1)]
+    blocks.append(levels[1].encode_db_block_int(ckks.layout_b_coeffs(last, lp, R, B)))
+    coeffs = fa.cheb_fit_sqrt(x["tau"], x["y_lo"], x["y_hi"], x["degree"])
+    say(f"[face] membership scan over {nb} blocks")
+    out, L, sc, mo = fa.membership(levels, q11, w.L - 1, s_q, blocks, R, B, x["y_lo"], x["y_hi"], coeffs,
+                                   x["m"], x["iters"])
+    assert L == 2
+    # float64 model and decisions over all 222,049 centroids
+    ctw = levels[1].ct_words
+    c2 = levels[w.L - L]
+    z = np.concatenate([c2.decode(c2.decrypt(out[i * ctw:i * ctw + 2 * L * c2.n]), 50) for i in range(nb)])
+    z = z[:w.rows] * (2.0 ** 50 / sc) / mo
+    qR = W.T @ q
+    Xm = np.vstack([Xr[:(nb - 1) * S].astype(np.float32).astype(np.float64), last])
+    y = float(qR @ qR)
+    assert x["y_lo"] < y < x["y_hi"]
+    u = (2 * y - x["y_lo"] - x["y_hi"]) / (x["y_hi"] - x["y_lo"])
+    t = np.polynomial.chebyshev.chebval(u, coeffs)
+    err = abs(t - x["tau"] * np.sqrt(y))
+    v = (Xm @ qR - t) / x["m"]
+    for _ in range(x["iters"]):
+        v = (3 * v - v ** 3) / 2
+    assert np.max(np.abs(z - v)) < 1e-4
+    margin = Xm @ qR - x["tau"] * np.sqrt(y)
+    ok = np.abs(margin) > err + 1e-4
+    assert np.all(np.sign(z[ok]) == np.sign(margin[ok]))
+    assert np.flatnonzero(z > 0).tolist() == [ident]
+    say(f"[face] y={y:.4f} series error {err:.2e}; identity {ident} matched; oracle chain")
+    # oracle: the projection, its rescale, and the last block's scan
+    ch = ckks.LevelChain(top, s, rlk, rot, rot_levels=[w.L, w.L - 1, w.L - 2])
+    ct_o = ch.orc[w.L].encrypt(m, a, e, s)
+    keys = ch.keys[w.L]
+    wres = np.stack([ckks.to_residues(v_, top.q) for v_ in wco]).reshape(R // Bp, Bp, w.L, top.n)
+    zo = ch.orc[w.L].bsgs_block(ch.orc[w.L].baby_rotations(ct_o, Bp, keys), wres, Bp, R // Bp, keys)
+    zo = ch.orc[w.L].rotate_sum(zo, R, int(np.log2(w.d_in // R)), keys)
+    assert np.array_equal(ctx.export(qr, 2).reshape(2, w.L, top.n), zo)
+    q11o = ch.orc[w.L].rescale(zo)
+    assert np.array_equal(levels[1].export(q11, 2).reshape(2, w.L - 1, top.n), q11o)
+    say("[face] oracle scan of the last block")
+    oo, Lo, so, mo2 = ckks.membership(ch, q11o, w.L - 1, s_q, [ckks.layout_b_pts(last, lp, R, B)], R, B,
+                                      x["y_lo"], x["y_hi"], coeffs, x["m"], x["iters"])
+    assert (Lo, so, mo2) == (L, sc, mo)
+    blk = out[(nb - 1) * ctw:(nb - 1) * ctw + 2 * L * c2.n]
+    assert np.array_equal(c2.export(blk, 2).reshape(2, L, top.n), oo[0])
