@@ -1538,15 +1538,21 @@ int fa_rescale(const fa_ctx* hi, const fa_ctx* lo, const void* ct, int n_polys, 
   return check_launch("fa_rescale");
 }
 
-// relinearised product at one level: out = Relin(x (x) y)
-static int mul_relin(fa_ctx* c, const double* x, const double* y, double* out, Arena& ar, hipStream_t s) {
+// relinearised products at one level, out_j = Relin(x_j (x) y_j) for count pairs:
+// x_j = x + j*sx with xL limbs per polynomial (read as its drop to this level), likewise y;
+// out [count][2][L][N]
+static int mul_relin_n(fa_ctx* c, const double* x, int xL, size_t sx, const double* y, int yL, size_t sy, int count,
+                       double* out, Arena& ar, hipStream_t s) {
   const size_t mark = ar.used;
-  double* t3 = ar.take(3 * (size_t)c->L * c->n);
+  double* t3 = ar.take((size_t)count * 3 * c->L * c->n);
   if (!t3) return fail(FA_E_NOMEM, "workspace too small for a ciphertext product");
-  fa::tensor(c, x, y, t3, s);
-  const int rc = relin_batch(c, t3, 1, out, ar, s);
+  fa::tensor(c, x, xL, sx, y, yL, sy, count, t3, s);
+  const int rc = relin_batch(c, t3, count, out, ar, s);
   ar.used = mark;
   return rc;
+}
+static int mul_relin(fa_ctx* c, const double* x, const double* y, double* out, Arena& ar, hipStream_t s) {
+  return mul_relin_n(c, x, c->L, 0, y, c->L, 0, 1, out, ar, s);
 }
 
 int fa_mul_ct(fa_ctx* c, const void* x, const void* y, void* out, void* ws, size_t ws_bytes, void* stream) {
@@ -1636,35 +1642,37 @@ int make_chain(fa_ctx* const* levels, int n_levels, Chain& ch) {
   }
   return FA_OK;
 }
-// copy x ([2][Lx][N]) dropped to L primes into dst ([2][L][N])
-int drop_to(const Chain& ch, const CtRef& x, int L, double* dst, hipStream_t s) {
-  const size_t n = ch.at(L)->n;
-  for (int h = 0; h < 2; ++h)
-    HIPCHK(hipMemcpyAsync(dst + (size_t)h * L * n, x.p + (size_t)h * x.L * n, (size_t)L * n * 8,
-                          hipMemcpyDeviceToDevice, s));
-  return FA_OK;
-}
 }  // namespace
 
-// product of two chain ciphertexts at the lower of their levels, rescaled into
-// dst (level L-1, scale sa*sb/q_{L-1}); tmp: two [2][L][N] + scratch from ar
+// count products x_j * y_j of chain ciphertexts (x_j = x + j*sx at level Lx, y_j = y + j*sy
+// at level Ly) at L = min(Lx, Ly), relinearised and rescaled into dst ([count][2][L-1][N]);
+// scratch from ar
+static int chain_mul_rescale_n(const Chain& ch, const double* x, int Lx, size_t sx, const double* y, int Ly,
+                               size_t sy, int count, double* dst, Arena& ar, hipStream_t s) {
+  const int L = std::min(Lx, Ly);
+  fa_ctx* c = ch.at(L);
+  if (!c || !ch.at(L - 1)) return fail(FA_E_SHAPE, "the chain has no level %d", L - 1);
+  const size_t mark = ar.used, cw = (size_t)count * 2 * L * c->n;
+  double* prod = ar.take(cw);
+  double* scr = ar.take(cw);
+  if (!prod || !scr) return fail(FA_E_NOMEM, "workspace too small for a chain product");
+  int rc;
+  if ((rc = mul_relin_n(c, x, Lx, sx, y, Ly, sy, count, prod, ar, s))) return rc;
+  fa::rescale(c, prod, 2 * count, dst, scr, s);
+  ar.used = mark;
+  return FA_OK;
+}
+// workspace of chain_mul_rescale_n at level L (count pairs)
+static size_t mul_rescale_ws(const fa_ctx* c, int count) {
+  const size_t cw = (size_t)count * 2 * c->L * c->n;
+  return 2 * rup(cw) + rup((size_t)count * 3 * c->L * c->n) + relin_ws(c);
+}
 static int chain_mul_rescale(const Chain& ch, const CtRef& a, const CtRef& b, double* dst, CtRef& out, Arena& ar,
                              hipStream_t s) {
   const int L = std::min(a.L, b.L);
-  fa_ctx* c = ch.at(L);
-  if (!c || !ch.at(L - 1)) return fail(FA_E_SHAPE, "the chain has no level %d", L - 1);
-  const size_t mark = ar.used, ctw = 2 * (size_t)L * c->n;
-  double* xa = ar.take(ctw);
-  double* xb = ar.take(ctw);
-  double* prod = ar.take(ctw);
-  double* scr = ar.take(2 * (size_t)L * c->n);
-  if (!xa || !xb || !prod || !scr) return fail(FA_E_NOMEM, "workspace too small for a chain product");
-  int rc;
-  if ((rc = drop_to(ch, a, L, xa, s)) || (rc = drop_to(ch, b, L, xb, s))) return rc;
-  if ((rc = mul_relin(c, xa, xb, prod, ar, s))) return rc;
-  fa::rescale(c, prod, 2, dst, scr, s);
-  out = {dst, L - 1, a.s * b.s / (double)c->primes[L - 1]};
-  ar.used = mark;
+  int rc = chain_mul_rescale_n(ch, a.p, a.L, 0, b.p, b.L, 0, 1, dst, ar, s);
+  if (rc) return rc;
+  out = {dst, L - 1, a.s * b.s / (double)ch.at(L)->primes[L - 1]};
   return FA_OK;
 }
 
@@ -1688,23 +1696,19 @@ static int cheb_core(const Chain& ch, const CtRef& u, const double* coeffs, int 
     double* dst = ar.take(ctw);
     if (!dst) return fail(FA_E_NOMEM, "workspace too small for the Chebyshev terms");
     const size_t mark_k = ar.used, cw = 2 * (size_t)L * c->n;
-    double* xa = ar.take(cw);
-    double* xb = ar.take(cw);
     double* prod = ar.take(cw);
     double* t1 = ar.take(cw);
     double* scr = ar.take(cw);
-    if (!xa || !xb || !prod || !t1 || !scr) return fail(FA_E_NOMEM, "workspace too small for the Chebyshev terms");
-    if ((rc = drop_to(ch, T[a], L, xa, s)) || (rc = drop_to(ch, T[b], L, xb, s))) return rc;
-    if ((rc = mul_relin(c, xa, xb, prod, ar, s))) return rc;
+    if (!prod || !t1 || !scr) return fail(FA_E_NOMEM, "workspace too small for the Chebyshev terms");
+    if ((rc = mul_relin_n(c, T[a].p, T[a].L, 0, T[b].p, T[b].L, 0, 1, prod, ar, s))) return rc;
     fa::ct_elem(c, prod, prod, prod, 2, nullptr, 2, s);  // 2 T_a T_b
     const double sp = T[a].s * T[b].s;
     if (k % 2 == 0) {
       const auto r = const_residues(c, -std::nearbyint(sp));
       fa::ct_elem(c, prod, nullptr, prod, 2, r.data(), 1, s);
     } else {
-      if ((rc = drop_to(ch, T[1], L, t1, s))) return rc;
       const auto r = const_residues(c, std::nearbyint(sp / T[1].s));
-      fa::ct_elem(c, t1, nullptr, t1, 2, r.data(), 0, s);
+      fa::ct_elem(c, T[1].p, nullptr, t1, 2, r.data(), 0, s, T[1].L);  // T_1 dropped to L, scaled
       fa::ct_elem(c, prod, t1, prod, 2, nullptr, 3, s);
     }
     fa::rescale(c, prod, 2, dst, scr, s);
@@ -1723,12 +1727,11 @@ static int cheb_core(const Chain& ch, const CtRef& u, const double* coeffs, int 
   if (!acc || !term || !scr) return fail(FA_E_NOMEM, "workspace too small for the Chebyshev sum");
   // every term is brought to the one scale u.s * qn: its constant carries u.s / T_k.s
   for (int k = 1; k <= degree; ++k) {
-    if ((rc = drop_to(ch, T[k], Lmin, term, s))) return rc;
     const auto ck = const_residues(c, std::nearbyint(coeffs[k] * qn * (u.s / T[k].s)));
     if (k == 1) {
-      fa::ct_elem(c, term, nullptr, acc, 2, ck.data(), 0, s);
+      fa::ct_elem(c, T[k].p, nullptr, acc, 2, ck.data(), 0, s, T[k].L);
     } else {
-      fa::ct_elem(c, term, nullptr, term, 2, ck.data(), 0, s);
+      fa::ct_elem(c, T[k].p, nullptr, term, 2, ck.data(), 0, s, T[k].L);
       fa::ct_elem(c, acc, term, acc, 2, nullptr, 2, s);
     }
   }
@@ -1741,34 +1744,53 @@ static int cheb_core(const Chain& ch, const CtRef& u, const double* coeffs, int 
   return FA_OK;
 }
 
-// iters sign steps from V (multiplier m) into out; V is not written
-static int sign_core(const Chain& ch, CtRef V, int64_t m, int iters, double* out, CtRef& res, int64_t& m_out,
-                     Arena& ar, hipStream_t s) {
+// iters sign steps on count ciphertexts at once: V_j = v + j*sv at level L (scale s_v,
+// multiplier m), results at out + j*so; v is not written.  Returns the final level,
+// scale and multiplier.
+static int sign_core_n(const Chain& ch, const double* v, int L, size_t sv, int count, double s_v, int64_t m,
+                       int iters, double* out, size_t so, CtRef& res, int64_t& m_out, Arena& ar, hipStream_t s) {
   const size_t mark = ar.used;
-  const size_t ctw = 2 * (size_t)V.L * ch.at(V.L)->n;
-  double* zb = ar.take(ctw);
-  double* vb[2] = {ar.take(ctw), ar.take(ctw)};
+  const size_t cw = (size_t)count * 2 * L * ch.at(L)->n;
+  double* zb = ar.take(cw);
+  double* vb[2] = {ar.take(cw), ar.take(cw)};
   if (!zb || !vb[0] || !vb[1]) return fail(FA_E_NOMEM, "workspace too small for the sign iteration");
   int rc;
+  const double* V = v;
+  size_t stride = sv;
   for (int it = 0; it < iters; ++it) {
     const double mm = (double)m;
-    CtRef z;
-    if ((rc = chain_mul_rescale(ch, V, V, zb, z, ar, s))) return rc;
-    fa_ctx* c = ch.at(z.L);
-    const auto m1 = const_residues(c, (int64_t)-1);
-    const auto k3 = const_residues(c, std::nearbyint(3.0 * mm * mm * z.s));
-    fa::ct_elem(c, z.p, nullptr, z.p, 2, m1.data(), 0, s);
-    fa::ct_elem(c, z.p, nullptr, z.p, 2, k3.data(), 1, s);
-    CtRef nv;
-    double* dst = it == iters - 1 ? out : vb[it & 1];
-    if ((rc = chain_mul_rescale(ch, V, z, dst, nv, ar, s))) return rc;
-    V = nv;
+    // z = V^2, then 3 m^2 - z (at z's scale)
+    if ((rc = chain_mul_rescale_n(ch, V, L, stride, V, L, stride, count, zb, ar, s))) return rc;
+    fa_ctx* c = ch.at(L);
+    const int Lz = L - 1;
+    fa_ctx* cz = ch.at(Lz);
+    const double sz = s_v * s_v / (double)c->primes[L - 1];
+    const auto m1 = const_residues(cz, (int64_t)-1);
+    const auto k3 = const_residues(cz, std::nearbyint(3.0 * mm * mm * sz));
+    fa::ct_elem(cz, zb, nullptr, zb, 2 * count, m1.data(), 0, s);
+    fa::ct_elem(cz, zb, nullptr, zb, 2 * count, k3.data(), 1, s);
+    // V <- V (3 m^2 - V^2) at level Lz - 1
+    const bool last = it == iters - 1;
+    double* dst = last && (count == 1 || so == 2 * (size_t)(Lz - 1) * cz->n) ? out : vb[it & 1];
+    if ((rc = chain_mul_rescale_n(ch, V, L, stride, zb, Lz, 2 * (size_t)Lz * cz->n, count, dst, ar, s))) return rc;
+    s_v = s_v * sz / (double)cz->primes[Lz - 1];
+    L = Lz - 1;
+    V = dst;
+    stride = 2 * (size_t)L * cz->n;
     m = 2 * m * m * m;
   }
-  res = V;
+  if (V != out) {
+    const size_t words = 2 * (size_t)L * ch.at(L)->n;
+    for (int j = 0; j < count; ++j)
+      HIPCHK(hipMemcpyAsync(out + j * so, V + j * stride, words * 8, hipMemcpyDeviceToDevice, s));
+  }
+  res = {out, L, s_v};
   m_out = m;
   ar.used = mark;
   return FA_OK;
+}
+static size_t sign_ws(const fa_ctx* c, int count) {
+  return 3 * rup((size_t)count * 2 * c->L * c->n) + mul_rescale_ws(c, count);
 }
 
 static int sign_args_ok(int64_t m, int iters) {
@@ -1809,7 +1831,8 @@ int fa_sign_iter(fa_ctx* const* levels, int n_levels, const void* v, int L_v, do
   if (!ws || ws_bytes < need) return fail(FA_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
   Arena ar{(char*)ws, ws_bytes, 0};
   CtRef res;
-  if ((rc = sign_core(ch, {(double*)v, L_v, s_v}, m, iters, (double*)out, res, *m_out, ar, (hipStream_t)stream)))
+  if ((rc = sign_core_n(ch, (const double*)v, L_v, 0, 1, s_v, m, iters, (double*)out, 0, res, *m_out, ar,
+                       (hipStream_t)stream)))
     return rc;
   *L_out = res.L;
   *s_out = res.s;
@@ -1845,9 +1868,10 @@ size_t fa_membership_workspace_bytes(const fa_ctx* cq, int n_blocks, int d, int 
   if (!cq || n_blocks < 1 || d < 1 || baby_step < 1 || d % baby_step || degree < 1) return 0;
   const size_t ctw = 2 * (size_t)cq->L * cq->n;
   const size_t nb = (size_t)n_blocks;
-  const size_t scoring = nb * rup(ctw) + std::max(score_ws(cq, n_blocks, d, baby_step), rup(nb * ctw));
-  const size_t chain = 4 * rup(ctw) + rotate_ws(cq, 1) + fa_chain_workspace_bytes(cq, std::max(degree, 3));
-  return nb * rup(ctw) + std::max(scoring, chain);
+  const size_t scoring = rup(nb * ctw) + std::max(score_ws(cq, n_blocks, d, baby_step), rup(nb * ctw));
+  const size_t per_query = std::max(rotate_ws(cq, 1), fa_chain_workspace_bytes(cq, std::max(degree, 3)));
+  const size_t per_block = rup(nb * ctw) + sign_ws(cq, n_blocks);
+  return rup(nb * ctw) + std::max(scoring, 3 * rup(ctw) + std::max(per_query, per_block));
 }
 
 int fa_membership(fa_ctx* const* levels, int n_levels, const void* q_r, int L_q, double s_q,
@@ -1897,9 +1921,8 @@ int fa_membership(fa_ctx* const* levels, int n_levels, const void* q_r, int L_q,
   // y = |q_R|^2 in every slot: the rescaled square folded over d slots
   double* yb = ar.take(ctw_q);
   double* tb = ar.take(ctw_q);
-  double* db = ar.take(ctw_q);
   double* rb = ar.take(ctw_q);
-  if (!yb || !tb || !db || !rb) return fail(FA_E_NOMEM, "workspace too small for the threshold");
+  if (!yb || !tb || !rb) return fail(FA_E_NOMEM, "workspace too small for the threshold");
   CtRef q{(double*)q_r, L_q, s_q}, y;
   if ((rc = chain_mul_rescale(ch, q, q, yb, y, ar, s))) return rc;
   for (int r : fold) {
@@ -1919,16 +1942,17 @@ int fa_membership(fa_ctx* const* levels, int n_levels, const void* q_r, int L_q,
   CtRef t;
   if ((rc = cheb_core(ch, u, cf.data(), degree, tb, t, ar, s))) return rc;
 
-  // per block: sign of (score - t) / m
+  // every block at once: (score - t) at t's level, then the sign steps on all of them
+  fa_ctx* ct = ch.at(t.L);
+  const size_t ctw_t = 2 * (size_t)t.L * n;
+  double* db = ar.take((size_t)n_blocks * ctw_t);
+  if (!db) return fail(FA_E_NOMEM, "workspace too small for the differences");
+  for (int i = 0; i < n_blocks; ++i)
+    fa::ct_elem(ct, scores + (size_t)i * ctw_y, tb, db + (size_t)i * ctw_t, 2, nullptr, 3, s, L_q - 1);
   CtRef res{};
   int64_t mo = m;
-  for (int i = 0; i < n_blocks; ++i) {
-    fa_ctx* ct = ch.at(t.L);
-    if ((rc = drop_to(ch, {scores + (size_t)i * ctw_y, L_q - 1, s_sc}, t.L, db, s))) return rc;
-    fa::ct_elem(ct, db, tb, db, 2, nullptr, 3, s);
-    if ((rc = sign_core(ch, {db, t.L, s_sc}, m, iters, (double*)out + (size_t)i * ctw_q, res, mo, ar, s)))
-      return rc;
-  }
+  if ((rc = sign_core_n(ch, db, t.L, ctw_t, n_blocks, s_sc, m, iters, (double*)out, ctw_q, res, mo, ar, s)))
+    return rc;
   *L_out = res.L;
   *s_out = res.s;
   *m_out = mo;

@@ -175,12 +175,17 @@ void mac_diag_ct(const fa_ctx* c, const double* q, const double* qrot, const dou
 // Rescale n_polys polynomials [n_polys][L][N] (NTT form) by the last prime:
 // out [n_polys][L-1][N] = round(x / q_last); scratch: n_polys * L * N words.
 void rescale(const fa_ctx* c, const double* ct, int n_polys, double* out, double* scratch, hipStream_t s);
-// out [3][L][N] = tensor of the ciphertexts x, y (NTT form)
-void tensor(const fa_ctx* c, const double* x, const double* y, double* out, hipStream_t s);
+// out [count][3][L][N]: tensors of count ciphertext pairs (NTT form); pair j reads
+// x + j*sx and y + j*sy (words), each with xL / yL limbs per polynomial of which the
+// first L are used (a ciphertext above this level is read as its drop)
+void tensor(const fa_ctx* c, const double* x, int xL, size_t sx, const double* y, int yL, size_t sy, int count,
+            double* out, hipStream_t s);
 // element-wise over n_polys polynomials: mode 0 out = x * cst, 1 out = x with cst added to
-// polynomial 0, 2 out = x + y, 3 out = x - y  (cst given by its residues cres[L], or null)
+// the even polynomials (the first of each ciphertext), 2 out = x + y, 3 out = x - y (cst
+// given by its residues cres[L], or null); x has xL limbs per polynomial (0: L), its
+// first L read
 void ct_elem(const fa_ctx* c, const double* x, const double* y, double* out, int n_polys, const uint64_t* cres,
-             int mode, hipStream_t s);
+             int mode, hipStream_t s, int xL = 0);
 
 // out[w] = ct * pt[w] (both polys), w < count
 void mul_plain(const fa_ctx* c, const double* ct, const double* const* pts, int count, double* out, hipStream_t s);

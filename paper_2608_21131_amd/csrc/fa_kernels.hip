@@ -1005,32 +1005,39 @@ __global__ __launch_bounds__(256) void k_rescale_combine(const double* __restric
   out[((size_t)h * (L - 1) + t) * n + k] = canon_full(mulc(x, a.c[t], a.cp[t], q), q, qinv);
 }
 // out = (x0 y0, x0 y1 + x1 y0, x1 y1) over the L primes (NTT form)
+// ciphertext j = blockIdx.z: x_j = x + j*sx with xL limbs per polynomial (its first L
+// limbs read: the drop to L is free), likewise y; out_j = out + j*3LN
 __global__ __launch_bounds__(256) void k_tensor(const double* __restrict__ x, const double* __restrict__ y,
                                                 double* __restrict__ out, const DevPrime* __restrict__ pr, int logn,
-                                                int L) {
+                                                int L, int xL, int yL, size_t sx, size_t sy) {
   const int n = 1 << logn;
   const int k = blockIdx.x * 256 + threadIdx.x;
   const int t = blockIdx.y;
+  const size_t j = blockIdx.z;
   const double q = pr[t].q, qinv = pr[t].qinv;
   const size_t o = (size_t)t * n + k, ln = (size_t)L * n;
-  const double x0 = x[o], x1 = x[ln + o], y0 = y[o], y1 = y[ln + o];
+  x += j * sx;
+  y += j * sy;
+  out += j * 3 * ln;
+  const double x0 = x[o], x1 = x[(size_t)xL * n + o], y0 = y[o], y1 = y[(size_t)yL * n + o];
   out[o] = canon_full(mul(x0, y0, q, qinv), q, qinv);
   out[ln + o] = canon_full(mul(x0, y1, q, qinv) + mul(x1, y0, q, qinv), q, qinv);
   out[2 * ln + o] = canon_full(mul(x1, y1, q, qinv), q, qinv);
 }
-// out[h][t] = x[h][t] * c_t (mode 0), or out = x with c_t added to polynomial 0 (mode 1),
-// or out[h][t] = x[h][t] +/- y[h][t] (mode 2 add, mode 3 subtract)
+// out[h][t] = x[h][t] * c_t (mode 0), or out = x with c_t added to the first polynomial of
+// every ciphertext (even h, mode 1), or out[h][t] = x[h][t] +/- y[h][t] (mode 2 add, mode 3
+// subtract); x has xL limbs per polynomial (its first L read), y and out L
 __global__ __launch_bounds__(256) void k_ct_elem(const double* __restrict__ x, const double* __restrict__ y,
                                                  double* __restrict__ out, ResArgs a,
-                                                 const DevPrime* __restrict__ pr, int logn, int L, int mode) {
+                                                 const DevPrime* __restrict__ pr, int logn, int L, int xL, int mode) {
   const int n = 1 << logn;
   const int k = blockIdx.x * 256 + threadIdx.x;
   const int t = blockIdx.y, h = blockIdx.z;
   const double q = pr[t].q, qinv = pr[t].qinv;
   const size_t o = ((size_t)h * L + t) * n + k;
-  double v = x[o];
+  double v = x[((size_t)h * xL + t) * n + k];
   if (mode == 0) v = mulc(v, a.c[t], a.cp[t], q);
-  else if (mode == 1) v = h == 0 ? v + a.c[t] : v;
+  else if (mode == 1) v = (h & 1) == 0 ? v + a.c[t] : v;
   else if (mode == 2) v = v + y[o];
   else v = v - y[o];
   out[o] = canon_full(v, q, qinv);
@@ -1533,15 +1540,17 @@ void rescale(const fa_ctx* c, const double* ct, int n_polys, double* out, double
                      res_args(c, inv.data(), L - 1), c->d_pr, c->logn, L);
 }
 
-void tensor(const fa_ctx* c, const double* x, const double* y, double* out, hipStream_t s) {
-  hipLaunchKernelGGL(k_tensor, dim3(c->n / 256, c->L), dim3(256), 0, s, x, y, out, c->d_pr, c->logn, c->L);
+void tensor(const fa_ctx* c, const double* x, int xL, size_t sx, const double* y, int yL, size_t sy, int count,
+            double* out, hipStream_t s) {
+  hipLaunchKernelGGL(k_tensor, dim3(c->n / 256, c->L, count), dim3(256), 0, s, x, y, out, c->d_pr, c->logn, c->L,
+                     xL, yL, sx, sy);
 }
 
 void ct_elem(const fa_ctx* c, const double* x, const double* y, double* out, int n_polys, const uint64_t* cres,
-             int mode, hipStream_t s) {
+             int mode, hipStream_t s, int xL) {
   std::vector<uint64_t> zero(c->L, 0);
   hipLaunchKernelGGL(k_ct_elem, dim3(c->n / 256, c->L, n_polys), dim3(256), 0, s, x, y, out,
-                     res_args(c, cres ? cres : zero.data(), c->L), c->d_pr, c->logn, c->L, mode);
+                     res_args(c, cres ? cres : zero.data(), c->L), c->d_pr, c->logn, c->L, xL ? xL : c->L, mode);
 }
 
 void add_limbs(const fa_ctx* c, double* dst, const double* src, int n_limbs, int period, hipStream_t s) {
