@@ -296,10 +296,19 @@ def run_membership(bn, args):
     ms = bn.timed(step, args.steps, args.warmup)
     ms_proj = bn.timed(project, args.steps, 1)
     ms_scan = bn.timed(scan, args.steps, 1)
+    c11.profile(True)  # events around the scoring inside the scan (baby, MAC, giant phases)
+    scan()
+    ph = c11.profile_read()
+    sb, sm, sg, st = (ph[k] for k in ("baby_ms", "mac_ms", "giant_ms", "total_ms"))
+    c11.profile(False)
     _, L, sc, mo = res_m["r"]
     res = {"workload": w.desc, "ms_per_query": round(ms, 4), "value": round(w.rows / (ms * 1e-3), 1),
            "unit": "decisions/s", "phases_ms": {"project_and_rescale_ms": round(ms_proj, 4),
-                                                "scan_ms": round(ms_scan, 4)},
+                                                "scan_ms": round(ms_scan, 4),
+                                                "scan_profiled_once": {"score_baby_ms": round(sb, 4),
+                                                                       "score_mac_ms": round(sm, 4),
+                                                                       "score_giant_ms": round(sg, 4),
+                                                                       "score_total_ms": round(st, 4)}},
            "levels": f"{w.L} -> {L}", "tau": x["tau"], "chebyshev_degree": x["degree"],
            "sign_steps": x["iters"], "database_bytes": 8 * nb * R * c11.L * w.n,
            "paper_warm_latency_s_context": 7.0}

@@ -76,7 +76,7 @@ WORKLOADS = {
         extra=dict(coarse=222_049, fine_pool_blocks=4, fine_blocks=2, rerank_pool_blocks=8, rerank_blocks=4,
                    rerank_last=11_696, queries=32, top_coarse=16, top_fine=64)),
     "face": Workload(
-        "face", 16, 12, 3, rows=222_049, dim=128, d=128, B=16, wid=7, d_in=512, B_proj=16,
+        "face", 16, 12, 3, rows=222_049, dim=128, d=128, B=32, wid=7, d_in=512, B_proj=16,
         desc="face membership scan: 222,049 identity centroids (unit 512-d rows, projected to R=128 and "
              "re-normalised) against one encrypted 512-d query, cos >= tau decided under encryption; "
              "CKKS N=2^16, 12+3 primes of 50 bits, scale 2^50 with rescaling, levels 12 -> 2",
