@@ -275,6 +275,9 @@ void fa_ctx_destroy(fa_ctx* c) {
     (void)hipEventDestroy(c->join_ev[i]);
   }
   if (c->fork_ev) (void)hipEventDestroy(c->fork_ev);
+  if (c->side) (void)hipStreamDestroy(c->side);
+  if (c->side_fork) (void)hipEventDestroy(c->side_fork);
+  if (c->side_join) (void)hipEventDestroy(c->side_join);
   (void)hipFree(c->d_export);
   delete c;
 }
@@ -1864,14 +1867,32 @@ static bool has_rotations(const fa_ctx* c, const std::vector<int>& steps) {
   return true;
 }
 
-size_t fa_membership_workspace_bytes(const fa_ctx* cq, int n_blocks, int d, int baby_step, int degree) {
-  if (!cq || n_blocks < 1 || d < 1 || baby_step < 1 || d % baby_step || degree < 1) return 0;
+// Workspace of the membership scan, in three regions: the rescaled scores;
+// the threshold chain (y, t, fold scratch and the chain's products), which
+// runs on the side stream while the scores are formed; the scoring (raw
+// scores, the diagonal product, the rescale scratch), reused after both have
+// joined for the differences and the batched sign steps.
+static void membership_regions(const fa_ctx* cq, int n_blocks, int d, int baby_step, int degree, size_t r[3]) {
   const size_t ctw = 2 * (size_t)cq->L * cq->n;
   const size_t nb = (size_t)n_blocks;
-  const size_t scoring = rup(nb * ctw) + std::max(score_ws(cq, n_blocks, d, baby_step), rup(nb * ctw));
-  const size_t per_query = std::max(rotate_ws(cq, 1), fa_chain_workspace_bytes(cq, std::max(degree, 3)));
-  const size_t per_block = rup(nb * ctw) + sign_ws(cq, n_blocks);
-  return rup(nb * ctw) + std::max(scoring, 3 * rup(ctw) + std::max(per_query, per_block));
+  r[0] = rup(nb * ctw);
+  r[1] = 3 * rup(ctw) + std::max(rotate_ws(cq, 1), fa_chain_workspace_bytes(cq, std::max(degree, 3)));
+  r[1] = (r[1] + 255) & ~(size_t)255;  // the next region starts aligned
+  r[2] = std::max(rup(nb * ctw) + std::max(score_ws(cq, n_blocks, d, baby_step), rup(nb * ctw)),
+                  rup(nb * ctw) + sign_ws(cq, n_blocks));
+}
+size_t fa_membership_workspace_bytes(const fa_ctx* cq, int n_blocks, int d, int baby_step, int degree) {
+  if (!cq || n_blocks < 1 || d < 1 || baby_step < 1 || d % baby_step || degree < 1) return 0;
+  size_t r[3];
+  membership_regions(cq, n_blocks, d, baby_step, degree, r);
+  return r[0] + r[1] + r[2];
+}
+
+static int ensure_side(fa_ctx* c) {
+  if (!c->side) HIPCHK(hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking));
+  if (!c->side_fork) HIPCHK(hipEventCreateWithFlags(&c->side_fork, hipEventDisableTiming));
+  if (!c->side_join) HIPCHK(hipEventCreateWithFlags(&c->side_join, hipEventDisableTiming));
+  return FA_OK;
 }
 
 int fa_membership(fa_ctx* const* levels, int n_levels, const void* q_r, int L_q, double s_q,
@@ -1898,49 +1919,66 @@ int fa_membership(fa_ctx* const* levels, int n_levels, const void* q_r, int L_q,
   std::vector<int> fold;
   for (int k = 1; k < d; k <<= 1) fold.push_back(k);
   if (!has_rotations(cy, fold)) return fail(FA_E_NOKEY, "level %d lacks a rotation key for the norm's fold", L_q - 1);
-  const size_t need = fa_membership_workspace_bytes(cq, n_blocks, d, baby_step, degree);
+  size_t reg[3];
+  membership_regions(cq, n_blocks, d, baby_step, degree, reg);
+  const size_t need = reg[0] + reg[1] + reg[2];
   if (!ws || ws_bytes < need) return fail(FA_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
-  Arena ar{(char*)ws, ws_bytes, 0};
-  hipStream_t s = (hipStream_t)stream;
+  if ((rc = ensure_side(cq))) return rc;
+  hipStream_t s = (hipStream_t)stream, s2 = cq->side;
+  char* base = (char*)ws;
+  Arena ar_th{base + reg[0], reg[1], 0};           // threshold chain (side stream)
+  Arena ar{base + reg[0] + reg[1], reg[2], 0};     // scoring, then differences and signs
   const size_t n = cq->n, ctw_q = 2 * (size_t)L_q * n, ctw_y = 2 * (size_t)(L_q - 1) * n;
+  double* scores = (double*)base;
 
-  // scores <q_R, x_i> of every block, rescaled: level L_q - 1, scale s_sc
-  double* scores = ar.take((size_t)n_blocks * ctw_y);
-  const size_t base = ar.used;
-  double* raw = ar.take((size_t)n_blocks * ctw_q);
-  if (!scores || !raw) return fail(FA_E_NOMEM, "workspace too small for the scores");
-  if ((rc = score_diag(cq, (const double*)q_r, (const double* const*)blocks, n_blocks, d, baby_step, raw, ar, s)))
-    return rc;
-  ar.used = base + rup((size_t)n_blocks * ctw_q);
-  double* scr = ar.take((size_t)n_blocks * ctw_q);
-  if (!scr) return fail(FA_E_NOMEM, "workspace too small for the scores' rescale");
-  fa::rescale(cq, raw, 2 * n_blocks, scores, scr, s);
+  // the threshold chain depends only on q_r: fork it onto the side stream
   const double s_sc = s_q * std::ldexp(1.0, cq->log_scale) / (double)cq->primes[L_q - 1];
-  ar.used = base;
-
-  // y = |q_R|^2 in every slot: the rescaled square folded over d slots
-  double* yb = ar.take(ctw_q);
-  double* tb = ar.take(ctw_q);
-  double* rb = ar.take(ctw_q);
-  if (!yb || !tb || !rb) return fail(FA_E_NOMEM, "workspace too small for the threshold");
-  CtRef q{(double*)q_r, L_q, s_q}, y;
-  if ((rc = chain_mul_rescale(ch, q, q, yb, y, ar, s))) return rc;
-  for (int r : fold) {
-    if ((rc = rotate_batch(cy, yb, 1, r, rb, ar, s))) return rc;
-    fa::add_automorph(cy, yb, rb, 2, 1u, s);
-  }
-  // u = alpha (y - mid) in [-1, 1]: the factor alpha costs nothing, it is taken
-  // into the scale (u at scale y.s / alpha); the shift is an added constant
-  const double alpha = 2.0 / (y_hi - y_lo), mid = 0.5 * (y_hi + y_lo);
-  const auto cm = const_residues(cy, std::nearbyint(-mid * y.s));
-  fa::ct_elem(cy, yb, nullptr, yb, 2, cm.data(), 1, s);
-  const CtRef u{yb, y.L, y.s / alpha};
-  // t = tau |q_R| at the scores' scale: the coefficients carry s_sc / s_u
-  std::vector<double> cf(degree + 1);
-  const double ratio = s_sc / u.s;
-  for (int k = 0; k <= degree; ++k) cf[k] = coeffs[k] * ratio;
+  double* tb = ar_th.take(ctw_q);
   CtRef t;
-  if ((rc = cheb_core(ch, u, cf.data(), degree, tb, t, ar, s))) return rc;
+  HIPCHK(hipEventRecord(cq->side_fork, s));
+  HIPCHK(hipStreamWaitEvent(s2, cq->side_fork, 0));
+  auto threshold = [&]() -> int {
+    // y = |q_R|^2 in every slot: the rescaled square folded over d slots
+    double* yb = ar_th.take(ctw_q);
+    double* rb = ar_th.take(ctw_q);
+    if (!yb || !tb || !rb) return fail(FA_E_NOMEM, "workspace too small for the threshold");
+    CtRef q{(double*)q_r, L_q, s_q}, y;
+    int e;
+    if ((e = chain_mul_rescale(ch, q, q, yb, y, ar_th, s2))) return e;
+    for (int r : fold) {
+      if ((e = rotate_batch(cy, yb, 1, r, rb, ar_th, s2))) return e;
+      fa::add_automorph(cy, yb, rb, 2, 1u, s2);
+    }
+    // u = alpha (y - mid) in [-1, 1]: the factor alpha costs nothing, it is taken
+    // into the scale (u at scale y.s / alpha); the shift is an added constant
+    const double alpha = 2.0 / (y_hi - y_lo), mid = 0.5 * (y_hi + y_lo);
+    const auto cm = const_residues(cy, std::nearbyint(-mid * y.s));
+    fa::ct_elem(cy, yb, nullptr, yb, 2, cm.data(), 1, s2);
+    const CtRef u{yb, y.L, y.s / alpha};
+    // t = tau |q_R| at the scores' scale: the coefficients carry s_sc / s_u
+    std::vector<double> cf(degree + 1);
+    const double ratio = s_sc / u.s;
+    for (int k = 0; k <= degree; ++k) cf[k] = coeffs[k] * ratio;
+    return cheb_core(ch, u, cf.data(), degree, tb, t, ar_th, s2);
+  };
+  // the scores <q_R, x_i> of every block on the caller's stream, rescaled
+  // (level L_q - 1, scale s_sc), enqueued first: the threshold chain's many
+  // small launches are enqueued after them and run beside them
+  double* raw = ar.take((size_t)n_blocks * ctw_q);
+  rc = raw ? score_diag(cq, (const double*)q_r, (const double* const*)blocks, n_blocks, d, baby_step, raw, ar, s)
+           : fail(FA_E_NOMEM, "workspace too small for the scores");
+  if (!rc) {
+    ar.used = rup((size_t)n_blocks * ctw_q);
+    double* scr = ar.take((size_t)n_blocks * ctw_q);
+    if (scr) fa::rescale(cq, raw, 2 * n_blocks, scores, scr, s);
+    else rc = fail(FA_E_NOMEM, "workspace too small for the scores' rescale");
+  }
+  if (!rc) rc = threshold();
+  // joined back on every path, so that no side-stream work outlives the call's stream order
+  HIPCHK(hipEventRecord(cq->side_join, s2));
+  HIPCHK(hipStreamWaitEvent(s, cq->side_join, 0));
+  if (rc) return rc;
+  ar.used = 0;
 
   // every block at once: (score - t) at t's level, then the sign steps on all of them
   fa_ctx* ct = ch.at(t.L);

@@ -73,6 +73,10 @@ struct fa_ctx {
   hipStream_t aux[FA_MAXAUX] = {};
   hipEvent_t fork_ev = nullptr;
   hipEvent_t join_ev[FA_MAXAUX] = {};
+  // side stream (default priority) of the membership scan: the threshold chain
+  // runs there while the scores run on the caller's stream
+  hipStream_t side = nullptr;
+  hipEvent_t side_fork = nullptr, side_join = nullptr;
   // device staging of fa_decrypt / fa_export_coeffs (client and test side),
   // grown on demand and reused; the mutex serialises callers on other threads
   std::mutex export_mu;
