@@ -215,7 +215,11 @@ size_t fa_workspace_bytes(const fa_ctx* ctx, int op, int n_blocks, int d, int ba
  *   Needs keys for steps 1..B-1 and g*B, 1 <= g < G.
  *   FA_LAYOUT_ROW: n_blocks row-packed plaintexts; out[w] = q * pt_w (no
  *   rotation; follow with fa_rotate_sum(first_shift=1, n_steps=log2 d)).
- * ws: device workspace of ws_bytes >= fa_workspace_bytes(...). */
+ * ws: device workspace of ws_bytes >= fa_workspace_bytes(...).
+ * Errors: FA_E_SHAPE if n_blocks < 1 (checked first: an empty list of blocks
+ * is a shape error, whatever the pointer) or d is not a power of two <= N/2;
+ * FA_E_INVAL for a null pointer or a baby step not dividing d; FA_E_NOKEY /
+ * FA_E_NOMEM for a missing key or a short workspace. */
 int fa_score_block(fa_ctx* ctx, const void* q, const void* const* blocks, int n_blocks, int d, int layout,
                    int baby_step, void* out, void* ws, size_t ws_bytes, void* stream);
 

@@ -1490,8 +1490,8 @@ int fa_score_batch(fa_ctx* c, const void* const* qs, const void* const* preps, i
 
 int fa_score_block(fa_ctx* c, const void* q, const void* const* blocks, int n_blocks, int d, int layout,
                    int baby_step, void* out, void* ws, size_t ws_bytes, void* stream) {
-  if (!c || !q || !blocks || !out) return fail(FA_E_INVAL, "fa_score_block: null argument");
   if (n_blocks < 1) return fail(FA_E_SHAPE, "n_blocks must be positive");
+  if (!c || !q || !blocks || !out) return fail(FA_E_INVAL, "fa_score_block: null argument");
   for (int i = 0; i < n_blocks; ++i)
     if (!blocks[i]) return fail(FA_E_INVAL, "block %d is null", i);
   hipStream_t s = (hipStream_t)stream;

@@ -248,6 +248,43 @@ def test_deterministic_repeat():
     assert np.array_equal(a[0], a[1])
 
 
+def test_more_blocks_than_one_launch_holds_and_a_zero_block():
+    """35 blocks in one call (the multiply-accumulate launch addresses at most 32 blocks, so
+    the library splits them): blocks 0, 31, 32 and 33 bit-exact against the oracle, every
+    decrypted score within 1e-4; an all-zero block scores to the zero ciphertext exactly,
+    on both sides; and no block, or a block of no rows, is an error."""
+    from paper_2608_21131_amd import fa
+    p = pair("tiny", wid=11)
+    S, d, B = p.par.slots, 16, 4
+    G = d // B
+    g = gen.rng(11, gen.STREAM_DB)
+    rows = [S if i % 3 == 0 else 1 + (37 * i) % S for i in range(34)]
+    Xs = [gen.gaussian_unit_rows(g, r, d) for r in rows]
+    q = gen.gaussian_unit_rows(gen.rng(11, gen.STREAM_QUERY), 1, d)[0]
+    ct_dev, ct_orc = p.encrypt_both(ckks.encode(ckks.replicate(q, S), p.n, 40), tag=11)
+    keys = p.keys(ckks.steps_for_bsgs(d, B))
+    coeffs = [ckks.layout_b_coeffs(X, p.par, d, B) for X in Xs] + [np.zeros((d, p.n), dtype=np.int64)]
+    blocks = [p.ctx.encode_db_block_int(c) for c in coeffs]
+    say(f"[blocks] tiny d={d} B={B}: {len(blocks)} blocks in one call")
+    out = p.ctx.score_block(ct_dev, blocks, d, 1, B)
+    got = p.export_ct(out, len(blocks))
+    qrot = p.orc.baby_rotations(ct_orc, B, keys)
+    for i in (0, 31, 32, 33, 34):
+        pts = np.stack([ckks.to_residues(ci, p.par.q) for ci in coeffs[i]]).reshape(G, B, p.par.L, p.n)
+        assert np.array_equal(got[i], p.orc.bsgs_block(qrot, pts, B, G, keys)), i
+    assert not got[34].any()
+    W_ = p.ctx.ct_words
+    for i, X in enumerate(Xs):
+        z = p.ctx.decode(p.ctx.decrypt(out[i * W_:(i + 1) * W_]), 80)
+        assert np.max(np.abs(z[:len(X)] - X @ q)) < 1e-4, i
+    with pytest.raises(fa.FaError) as ei:
+        p.ctx.score_block(ct_dev, [], d, 1, B)
+    assert ei.value.code == fa.FA_E_SHAPE
+    with pytest.raises(fa.FaError) as ei:
+        p.ctx.encode_db_block(np.zeros((0, d), np.float32), d, 1, B)
+    assert ei.value.code == fa.FA_E_SHAPE
+
+
 def test_encode_projection_vs_oracle():
     """fa_encode_projection packs W's hybrid diagonals, pre-rotated, like the oracle (|dm| <= 1)."""
     p = pair("small", wid=11)
@@ -501,36 +538,43 @@ def _gpu_membership_chain(logn, L, K, wid, d, B):
     return top, s, levels, och
 
 
-@pytest.mark.parametrize("y_lo,y_hi", [(0.5, 2.5), (0.6, 1.6)])
-def test_membership_scan_parity(y_lo, y_hi):
-    """The membership scan (scores, |q_R|^2 by square and fold, Chebyshev tau |q_R|, two
-    sign steps; levels 11 -> 2 at N = 2^11, d = 16, a full and a ragged block) writes the
-    oracle's ciphertexts word for word, and its decrypted signs are the decisions
-    cos(q_R, x_i) >= tau wherever the margin exceeds the series' error."""
+@pytest.mark.parametrize("y_lo,y_hi,degree,iters,nblk", [(0.5, 2.5, 7, 2, 2), (0.6, 1.6, 7, 2, 2),
+                                                       (0.5, 2.5, 1, 1, 1), (0.5, 2.5, 3, 2, 1)])
+def test_membership_scan_parity(y_lo, y_hi, degree, iters, nblk):
+    """The membership scan (scores, |q_R|^2 by square and fold, Chebyshev tau |q_R|, sign
+    steps; from level 11 at N = 2^11, d = 16, a full and a ragged block) writes the oracle's
+    ciphertexts word for word, and its decrypted signs are the decisions cos(q_R, x_i) >= tau
+    wherever the margin exceeds the series' error.  Also the degenerate settings: a series
+    of degree 1, one sign step, one block."""
     from paper_2608_21131_amd import fa
-    d, B, tau, m, iters = 16, 4, 0.6, 4, 2
+    d, B, tau, m = 16, 4, 0.6, 4
     top, s, levels, och = _gpu_membership_chain(11, 11, 3, 46, d, B)
     g = np.random.default_rng(46)
     X = gen.normalize_rows(g.standard_normal((top.slots + 500, d)))
     qR = 1.1 * gen.normalize_rows((X[3] + 0.4 * g.standard_normal(d))[None])[0]
-    coeffs = fa.cheb_fit_sqrt(tau, y_lo, y_hi, 7)
+    coeffs = fa.cheb_fit_sqrt(tau, y_lo, y_hi, degree)
     x, xo = _enc_both(top, levels, och, s, ckks.replicate(qR, top.slots), 46, 1)
-    parts = [X[:top.slots], X[top.slots:]]
+    parts = [X[:top.slots], X[top.slots:]][:nblk]
+    X = np.vstack(parts)
     blocks = [levels[0].encode_db_block_int(ckks.layout_b_coeffs(b, top, d, B)) for b in parts]
     oblocks = [ckks.layout_b_pts(b, top, d, B) for b in parts]
-    say(f"[membership] N=2^11 L=11 d={d} domain [{y_lo}, {y_hi}]")
+    say(f"[membership] N=2^11 L=11 d={d} domain [{y_lo}, {y_hi}] degree {degree}, {iters} sign steps, "
+        f"{nblk} block(s)")
     out, L, sc, mo = fa.membership(levels, x, top.L, 2.0 ** 50, blocks, d, B, y_lo, y_hi, coeffs, m, iters)
     oo, Lo, so, mo2 = ckks.membership(och, xo, top.L, 2.0 ** 50, oblocks, d, B, y_lo, y_hi, coeffs, m, iters)
-    assert (L, sc, mo) == (Lo, so, mo2) and L == 2
+    depth = 1 + (int(np.ceil(np.log2(degree))) + 1) + 2 * iters
+    assert (L, sc, mo) == (Lo, so, mo2) and L == top.L - depth
     ctw = levels[0].ct_words
     c = levels[top.L - L]
     z = []
-    for i in range(2):
+    for i in range(nblk):
         blk = out[i * ctw:i * ctw + 2 * L * c.n]
         assert np.array_equal(_export_at(levels, blk, L), oo[i]), i
         z.append(c.decode(c.decrypt(blk), 50) * (2.0 ** 50 / sc) / mo)
     z = np.concatenate(z)[:len(X)]
-    margin = X @ qR - tau * np.linalg.norm(qR)
-    ok = np.abs(margin) > 2e-4
+    y = float(qR @ qR)
+    t = np.polynomial.chebyshev.chebval((2 * y - y_lo - y_hi) / (y_hi - y_lo), coeffs)
+    margin = X @ qR - tau * np.sqrt(y)
+    ok = np.abs(margin) > abs(t - tau * np.sqrt(y)) + 2e-4
     assert np.all(np.sign(z[ok]) == np.sign(margin[ok]))
     assert 0 < np.count_nonzero(margin > 0) < len(X) // 4
