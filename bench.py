@@ -175,7 +175,62 @@ def run_diag_level(bn, args):
     mac_bytes = 8 * (w.n_blocks * w.d * ptw + (w.B - 1) * 2 * ptw + 2 * ptw + w.n_blocks * w.G * 2 * ptw)
     stream_bytes = 8 * w.n_blocks * w.d * ptw
     return dict(ms=ms, scores=w.rows, phases=ph, err=err, mac_bytes=mac_bytes, stream_bytes=stream_bytes,
-                X=X, cpu=(lambda: cpu_baseline_diag(bn, X, qv)), ctx=ctx, blocks=blocks, centers=centers)
+                X=X, cpu=(lambda: cpu_baseline_diag(bn, X, qv)), ctx=ctx, blocks=blocks, centers=centers,
+                io=transfer_ms(bn, q, out))
+
+
+def transfer_ms(bn, q, out):
+    """Outside the timed level: the PCIe legs a client adds around it, timed with events on
+    the stream: the query ciphertext host -> device and the output ciphertexts device -> host,
+    both from / to pinned host memory."""
+    torch = bn.torch
+    hq = torch.empty(q.numel(), dtype=torch.float64, pin_memory=True)
+    ho = torch.empty(out.numel(), dtype=torch.float64, pin_memory=True)
+    dq = torch.empty_like(q)
+    stream = torch.cuda.current_stream()
+    res = {}
+    for name, dst, src in (("query_h2d_ms", dq, hq), ("scores_d2h_ms", ho, out)):
+        dst.copy_(src, non_blocking=True)
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ev0.record(stream)
+        for _ in range(5):
+            dst.copy_(src, non_blocking=True)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        res[name] = round(ev0.elapsed_time(ev1) / 5, 4)
+    res["query_bytes"] = 8 * q.numel()
+    res["scores_bytes"] = 8 * out.numel()
+    return res
+
+
+def copy_peak_GBs(bn):
+    """Measured HBM stream-copy rate: a 1 GiB device-to-device copy, read + write bytes over
+    its event-timed duration (mean of 5 after one warm-up)."""
+    torch = bn.torch
+    src = torch.empty(1 << 27, dtype=torch.float64, device="cuda")
+    dst = torch.empty_like(src)
+    src.fill_(1.0)
+    dst.copy_(src)
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    for _ in range(5):
+        dst.copy_(src)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / 5
+    del src, dst
+    return round(2 * 8 * (1 << 27) / (ms * 1e-3) / 1e9, 1)
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def run_enc_level(bn, args, level):
@@ -707,10 +762,12 @@ def main():
         traffic = measured_traffic(args.traffic) if (w.name == "rerank" and w.B == 64 and not args.level) else None
         roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic, "kernel": "k_mac_diag",
-                    "algorithmic_bytes": r["mac_bytes"], "avg_ms": round(mac_ms, 4)}
+                    "algorithmic_bytes": r["mac_bytes"], "avg_ms": round(mac_ms, 4),
+                    "measured_copy_GBs": copy_peak_GBs(bn)}
     cpu = None
     if not args.no_cpu_baseline and r.get("cpu"):
         cpu = r["cpu"]()
+        cpu["cpu_model"] = cpu_model()
     floor_ms = r["stream_bytes"] / (HBM_PEAK_GBS * 1e9) * 1e3
     cfg = {"workload": w.desc, "rows_scored_per_step": r["scores"], "d": w.d, "baby_step": w.B,
            "giant_steps": w.G, "log_n": w.log_n, "L": w.L, "K": w.K, "log_scale": 40}
@@ -741,6 +798,7 @@ def main():
         "level_hbm_floor_ms": round(floor_ms, 4),
         "level_frac_of_hbm_roofline": round(floor_ms / ms, 4),
         "max_abs_score_err": r["err"],
+        "transfers_outside_timing": r.get("io"),
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
