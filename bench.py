@@ -67,7 +67,7 @@ def parse():
     ap.add_argument("--no-check", action="store_true", help="skip the decrypt-and-compare check")
     ap.add_argument("--copy-calib", action="store_true",
                     help="run one plain 1 GiB device copy before the timed region (HBM counter calibration)")
-    ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "k_mac_diag_rerank110k_traffic.md"),
+    ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "k_mac_diag3_rerank110k_traffic.md"),
                     help="rocprofv3 counter summary with the measured per-launch HBM bytes of the "
                          "multiply-accumulate kernel (used only while that kernel's source is unchanged)")
     return ap.parse_args()
@@ -654,7 +654,7 @@ def run_three_level(bn, args):
 
 
 def measured_traffic(path):
-    """HBM bytes per launch of k_mac_diag from the committed counter summary, or None
+    """HBM bytes per launch of the multiply-accumulate kernel from the committed counter summary, or None
     when the summary is missing or the kernel source changed since it was taken."""
     import hashlib
     import re
@@ -670,11 +670,14 @@ def measured_traffic(path):
     return int(mb.group(1))
 
 
-def mac_source_sha256():
+MAC_KERNEL = "k_mac_diag3"  # the single-query launches of the rerank level (three steps in flight)
+
+
+def mac_source_sha256(kernel=MAC_KERNEL):
     """sha256 of the multiply-accumulate kernel's source text (template line to closing brace)."""
     import hashlib
     src = open(os.path.join(ROOT, "paper_2608_21131_amd", "csrc", "fa_kernels.hip")).read()
-    a = src.index("void k_mac_diag(")
+    a = src.index(f"void {kernel}(")
     a = src.rindex("template <", 0, a)
     b = src.index("\n}\n", a) + 3
     return hashlib.sha256(src[a:b].encode()).hexdigest()
@@ -761,7 +764,7 @@ def main():
         achieved = r["mac_bytes"] / (mac_ms * 1e-3) / 1e9
         traffic = measured_traffic(args.traffic) if (w.name == "rerank" and w.B == 64 and not args.level) else None
         roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic, "kernel": "k_mac_diag",
+                    "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic, "kernel": MAC_KERNEL,
                     "algorithmic_bytes": r["mac_bytes"], "avg_ms": round(mac_ms, 4),
                     "measured_copy_GBs": copy_peak_GBs(bn)}
     cpu = None

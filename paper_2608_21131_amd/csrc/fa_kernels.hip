@@ -848,6 +848,157 @@ __global__ __launch_bounds__(256) void k_mac_diag(MacArgs args, const DevPrime* 
     }
 }
 
+// One query, NACC pairs: the same product with three steps in flight per wave.
+// Steps cycle through two LDS slots (direct-to-LDS loads of the NACC plaintext
+// rows, the rotated query in registers) and one register stage (the NACC
+// plaintext words and the rotated query loaded straight into registers), so a
+// wave holds the loads of three steps while it multiplies one.  The LDS
+// slots are synchronised by the vector-memory counter as in k_mac_diag (a
+// slot's wait counts the loads issued after it); the register stage is waited
+// on by the compiler.  Reductions every 6 steps (lazy sums below 6q + q/2).
+template <int NACC>
+__global__ __launch_bounds__(256) void k_mac_diag3(MacArgs args, const DevPrime* __restrict__ pr, int logn) {
+  constexpr int ROWS = NACC + 2;    // an LDS step: the plaintext rows, then the rotated query's x0 / x1
+  constexpr int GL = NACC / 2 + 1;  // vector-memory operations of an LDS step
+  constexpr int GR = NACC + 2;      // of a register step
+  static_assert(GL + GR <= 63, "vector-memory counter range");
+  __shared__ double slab[4][2][ROWS][64];
+  unsigned tile = blockIdx.x, chunk = 0;
+  if (args.nchunk > 1) {
+    const unsigned j = blockIdx.x >> 3;
+    chunk = j % (unsigned)args.nchunk;
+    tile = (j / (unsigned)args.nchunk) * 8u + (blockIdx.x & 7u);
+    if (tile >= (unsigned)args.ntile) return;
+  }
+  const int n = 1 << logn;
+  const size_t ln = (size_t)args.L * n;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const size_t c0 = (size_t)tile * 256 + (size_t)w * 64;
+  const size_t f = c0 + lane;
+  const int t = (int)(c0 >> logn);
+  const double q = pr[t].q, qinv = pr[t].qinv;
+  const int pair0 = args.pair0 + (int)chunk * NACC;
+  const int last = args.n_pairs - 1;
+  const int G = 1 << args.logG;
+  const int B = args.B;
+  const int hp = lane >> 5;
+  const size_t lo = c0 + 2 * (size_t)(lane & 31);
+  // plaintext row of pair i at step 0 (pairs past the end re-read the last pair)
+  auto row = [&](int i) -> const double* {
+    const int pa = min(pair0 + i, last);
+    return args.blk[pa >> args.logG] + (size_t)((pa & (G - 1)) * B) * ln;
+  };
+  const double* src[NACC / 2];  // direct-to-LDS source of load i (pairs 2i, 2i+1)
+#pragma unroll
+  for (int i = 0; i < NACC / 2; ++i) src[i] = (hp ? row(2 * i + 1) : row(2 * i)) + lo;
+  const double* qd0 = args.q0[0] + (size_t)hp * ln + lo;    // direct-to-LDS: x0 row (lanes 0-31), x1 row
+  const double* qdr = args.qrot[0] + (size_t)hp * ln + lo;
+  const double* qv0 = args.q0[0] + f;                       // into registers
+  const double* qvr = args.qrot[0] + f;
+  double a0[NACC], a1[NACC];
+#pragma unroll
+  for (int i = 0; i < NACC; ++i) {
+    a0[i] = 0.0;
+    a1[i] = 0.0;
+  }
+  auto dma = [&](auto slc, int b) {
+    constexpr int SL = decltype(slc)::value;
+#pragma unroll
+    for (int i = 0; i < NACC / 2; ++i)
+      __builtin_amdgcn_global_load_lds((gbl_void_t*)(src[i] + (size_t)b * ln), (lds_void_t*)&slab[w][SL][2 * i][0],
+                                       16, 0, 0);
+    __builtin_amdgcn_global_load_lds((gbl_void_t*)(b == 0 ? qd0 : qdr + (size_t)(b - 1) * 2 * ln),
+                                     (lds_void_t*)&slab[w][SL][NACC][0], 16, 0, 0);
+  };
+  double pv[NACC], xr0, xr1;
+  auto rld = [&](int b) {
+#pragma unroll
+    for (int i = 0; i < NACC; ++i) pv[i] = __builtin_nontemporal_load(row(i) + (size_t)b * ln + f);
+    const double* x = b == 0 ? qv0 : qvr + (size_t)(b - 1) * 2 * ln;
+    xr0 = x[0];
+    xr1 = x[ln];
+  };
+  auto mac_lds = [&](auto slc) {
+    constexpr int SL = decltype(slc)::value;
+    const double x0 = slab[w][SL][NACC][lane], x1 = slab[w][SL][NACC + 1][lane];
+    const double x0p = x0 * qinv, x1p = x1 * qinv;
+#pragma unroll
+    for (int c = 0; c < NACC; c += 8) {
+      double pc[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) pc[i] = slab[w][SL][c + i][lane];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        a0[c + i] += mulc(pc[i], x0, x0p, q);
+        a1[c + i] += mulc(pc[i], x1, x1p, q);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, 1>;
+  dma(S0{}, 0);
+  if (B > 1) dma(S1{}, 1);
+  if (B > 2) rld(2);
+  int red = 0;
+  for (int b = 0; b < B; b += 3) {
+    // step b out of slot 0: issued after its loads are slot 1's step (if any)
+    // and the register step (if any), in that order
+    __builtin_amdgcn_sched_barrier(0);
+    if (b + 2 < B) __builtin_amdgcn_s_waitcnt(FA_VMCNT(GL + GR));
+    else if (b + 1 < B) __builtin_amdgcn_s_waitcnt(FA_VMCNT(GL));
+    else __builtin_amdgcn_s_waitcnt(FA_VMCNT(0));
+    __builtin_amdgcn_sched_barrier(0);
+    mac_lds(S0{});
+    __builtin_amdgcn_s_waitcnt(FA_LGKMCNT0);
+    __builtin_amdgcn_sched_barrier(0);
+    const bool n0 = b + 3 < B, n1 = b + 4 < B, n2 = b + 5 < B;
+    if (n0) dma(S0{}, b + 3);
+    if (b + 1 < B) {
+      // step b+1 out of slot 1: issued after it are the register step (when
+      // b+2 < B) and slot 0's refill (when b+3 < B)
+      __builtin_amdgcn_sched_barrier(0);
+      if (n0) __builtin_amdgcn_s_waitcnt(FA_VMCNT(GR + GL));
+      else if (b + 2 < B) __builtin_amdgcn_s_waitcnt(FA_VMCNT(GR));
+      else __builtin_amdgcn_s_waitcnt(FA_VMCNT(0));
+      __builtin_amdgcn_sched_barrier(0);
+      mac_lds(S1{});
+      __builtin_amdgcn_s_waitcnt(FA_LGKMCNT0);
+      __builtin_amdgcn_sched_barrier(0);
+      if (n1) dma(S1{}, b + 4);
+    }
+    if (b + 2 < B) {
+      // step b+2 out of registers (the compiler waits for them)
+      const double x0p = xr0 * qinv, x1p = xr1 * qinv;
+#pragma unroll
+      for (int i = 0; i < NACC; ++i) {
+        a0[i] += mulc(pv[i], xr0, x0p, q);
+        a1[i] += mulc(pv[i], xr1, x1p, q);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      if (n2) rld(b + 5);
+    }
+    if (++red == 2) {
+      red = 0;
+#pragma unroll
+      for (int i = 0; i < NACC; ++i) {
+        a0[i] = reduce(a0[i], q, qinv);
+        a1[i] = reduce(a1[i], q, qinv);
+      }
+    }
+  }
+  const int cnt = min(NACC, args.n_pairs - pair0);
+  double* accp = args.acc[0];
+#pragma unroll
+  for (int i = 0; i < NACC; ++i) {
+    if (i < cnt) {
+      double* o = accp + (size_t)(pair0 + i) * 2 * ln + f;
+      o[0] = canon_full(a0[i], q, qinv);
+      o[ln] = canon_full(a1[i], q, qinv);
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // multiply-accumulate against an encrypted block (ct x ct, three components)
 //   acc[pair][0] += c0 q0,  acc[pair][1] += c0 q1 + c1 q0,  acc[pair][2] += c1 q1
@@ -1370,6 +1521,16 @@ void giant_ks(const fa_ctx* c, const double* ext, const double* acc, size_t astr
 // Most (block, giant) accumulator pairs one pass keeps in registers for one
 // query: 32 (default), 16 or 8; FA_MAC_PAIRS overrides it for tuning.  With
 // NQ queries per pass the pairs per pass drop to 32 / NQ.
+// the three-stage single-query kernel (FA_MAC_STAGES=2 selects the two-slot one)
+static bool mac_three_stages() {
+  static int v = -1;
+  if (v < 0) {
+    const char* e = getenv("FA_MAC_STAGES");
+    v = e && atoi(e) == 2 ? 2 : 3;
+  }
+  return v == 3;
+}
+
 static int mac_pairs_max() {
   static int v = -1;
   if (v < 0) {
@@ -1393,8 +1554,16 @@ static void launch_mac(MacArgs a, int nchunk, const fa_ctx* c, hipStream_t s) {
   a.ntile = (int)((size_t)c->L * c->n / 256);
   a.nchunk = nchunk;
   const unsigned grid = nchunk == 1 ? (unsigned)a.ntile : 8u * nchunk * ((a.ntile + 7) / 8);
-  hipLaunchKernelGGL((k_mac_diag<NQ, NACC, MacStages<NQ, NACC>::S>), dim3(grid), dim3(256), 0, s, a, c->d_pr,
-                     c->logn);
+  if constexpr (NQ == 1 && NACC == 32) {
+    if (mac_three_stages())
+      hipLaunchKernelGGL((k_mac_diag3<NACC>), dim3(grid), dim3(256), 0, s, a, c->d_pr, c->logn);
+    else
+      hipLaunchKernelGGL((k_mac_diag<NQ, NACC, MacStages<NQ, NACC>::S>), dim3(grid), dim3(256), 0, s, a, c->d_pr,
+                         c->logn);
+  } else {
+    hipLaunchKernelGGL((k_mac_diag<NQ, NACC, MacStages<NQ, NACC>::S>), dim3(grid), dim3(256), 0, s, a, c->d_pr,
+                       c->logn);
+  }
 }
 
 // pairs p0.. of the current query group: all full chunks of the group's widest
