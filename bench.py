@@ -175,7 +175,7 @@ def run_diag_level(bn, args):
     mac_bytes = 8 * (w.n_blocks * w.d * ptw + (w.B - 1) * 2 * ptw + 2 * ptw + w.n_blocks * w.G * 2 * ptw)
     stream_bytes = 8 * w.n_blocks * w.d * ptw
     return dict(ms=ms, scores=w.rows, phases=ph, err=err, mac_bytes=mac_bytes, stream_bytes=stream_bytes,
-                X=X, cpu=(lambda: cpu_baseline_diag(bn, X, qv)), ctx=ctx, blocks=blocks, centers=centers,
+                X=X, cpu=(lambda: cpu_baseline_diag(bn, X, qv, L=ctx.L)), ctx=ctx, blocks=blocks, centers=centers,
                 io=transfer_ms(bn, q, out))
 
 
@@ -287,7 +287,9 @@ def run_enc_level(bn, args, level):
                                              "mac_ct_ms": round(ph["mac_ms"], 4),
                                              "relin_and_giant_ms": round(ph["giant_ms"], 4)},
            "database_bytes": stream_bytes, "level_hbm_floor_ms": round(stream_bytes / (HBM_PEAK_GBS * 1e9) * 1e3, 4),
-           "mac_achieved_GBs": round(mac_bytes / (ph["mac_ms"] * 1e-3) / 1e9, 1), "max_abs_score_err": err}
+           "mac_achieved_GBs": round(mac_bytes / (ph["mac_ms"] * 1e-3) / 1e9, 1), "max_abs_score_err": err,
+           "roofline": roofline_of("k_mac_diag_ct", mac_bytes, ph["mac_ms"]),
+           "cpu_baseline": None if args.no_cpu_baseline else cpu_baseline_diag(bn, X, qv, L=ctx.L, enc=True)}
     del blocks
     torch.cuda.empty_cache()
     return res
@@ -366,7 +368,9 @@ def run_membership(bn, args):
                                                                        "score_total_ms": round(st, 4)}},
            "levels": f"{w.L} -> {L}", "tau": x["tau"], "chebyshev_degree": x["degree"],
            "sign_steps": x["iters"], "database_bytes": 8 * nb * R * c11.L * w.n,
-           "paper_warm_latency_s_context": 7.0}
+           "paper_warm_latency_s_context": 7.0,
+           "roofline": roofline_of("k_mac_diag", mac_batch_bytes(1, nb * (R // B), B, c11.L * w.n), sm),
+           "cpu_baseline": None if args.no_cpu_baseline else cpu_baseline_membership(bn, w, s, q, Xr)}
     if not args.no_check:
         ctw = c11.ct_words
         c2 = levels[w.L - L]
@@ -388,6 +392,87 @@ def run_membership(bn, args):
     del blocks, levels
     torch.cuda.empty_cache()
     return res
+
+
+def cpu_baseline_membership(bn, w, s, q, Xr):
+    """The oracle timed on a bounded sample of the face scan, extrapolated to one query:
+    one rotation at 12 and at 11 primes, the block product with 1 and 2 giant groups on
+    block 0 at 11 primes, a relinearised product and rescale at 10 and at 5 primes; then
+    (B_proj-1) + (G_proj-1) + 2 rotations for the projection, B-1 baby rotations, the blocks'
+    products, log2(d) fold rotations, degree-1 Chebyshev products and 2 * iters sign products
+    per block."""
+    from oracle import ckks
+    x = w.extra
+    t_start = time.time()
+    top = ckks.Params(logn=w.log_n, L=w.L, K=w.K, log_scale=x["log_scale"])
+
+    def level(L):
+        par = top if L == w.L else ckks.Params(logn=w.log_n, L=L, K=w.K, log_scale=x["log_scale"],
+                                               primes=top.q[:L] + top.p)
+        idx = list(range(L)) + list(range(w.L, w.L + w.K))
+        orc = ckks.Oracle(par)
+
+        def key(r):
+            a, e = bn.wl.key_randomness(w, r, top.primes, top.dnum)
+            return a[:par.dnum][:, idx], e[:par.dnum]
+        return par, orc, key
+
+    def enc(par, orc):
+        a, e = bn.wl.enc_randomness(w, top.q)
+        m = ckks.encode(ckks.replicate(q, par.slots), par.n, x["log_scale"])
+        return orc.encrypt(m, np.ascontiguousarray(a[:par.L]), e, s)
+
+    def t_rot(L):
+        par, orc, key = level(L)
+        k1 = orc.keygen(s, 1, *key(1))
+        ct = enc(par, orc)
+        t = time.time()
+        orc.rotate(ct, 1, k1)
+        return time.time() - t, par, orc, key, ct
+
+    def t_mul(L):
+        par, orc, key = level(L)
+        rlk = orc.keygen_relin(s, *key(0))
+        ct = enc(par, orc)
+        t = time.time()
+        orc.rescale(orc.mul(ct, ct, rlk))
+        return time.time() - t
+
+    r12 = t_rot(w.L)[0]
+    r11, par, orc, key, ct = t_rot(w.L - 1)
+    B, G, nb = w.B, w.d // w.B, w.n_blocks
+    keys = {gB: orc.keygen(s, gB, *key(gB)) for gB in (B,)}
+    diags = ckks.diagonals(Xr[:par.slots], par.slots, w.d)
+    pts = np.stack([ckks.encode_residues(np.roll(diags[gg * B + b], gg * B), par)
+                    for gg in range(2) for b in range(B)]).reshape(2, B, par.L, par.n)
+    qrot = np.repeat(ct[None], B, axis=0)
+    t = time.time()
+    orc.bsgs_block(qrot, pts[:1], B, 1, keys)
+    g1 = time.time() - t
+    t = time.time()
+    orc.bsgs_block(qrot, pts, B, 2, keys)
+    g2 = time.time() - t
+    m10, m5 = t_mul(w.L - 2), t_mul(5)
+    Gp = w.d // w.B_proj
+    est = ((w.B_proj - 1) + (Gp - 1) + 2) * r12 + (B - 1) * r11 + nb * (g1 + (G - 1) * max(g2 - g1, 0.0)) \
+        + int(np.log2(w.d)) * r11 + (1 + x["degree"] - 1) * m10 + nb * 2 * x["iters"] * m5
+    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    log(f"[bench] oracle sample (face scan): rot {r12:.2f}/{r11:.2f}s, G1 {g1:.2f}s, G2 {g2:.2f}s, "
+        f"mul {m10:.2f}/{m5:.2f}s -> query {est:.1f}s ({time.time() - t_start:.1f}s wall)")
+    return {"value": round(w.rows / est, 2), "unit": "decisions/s", "cores": cores, "kind": "oracle",
+            "sample": "rotations at 12 and 11 primes, the block product with 1 and 2 giant groups on block 0, "
+                      "products at 10 and 5 primes; extrapolated to the projection, the scan's scoring, the "
+                      "norm's fold, the Chebyshev series and the sign steps of one query",
+            "query_s_est": round(est, 2), "cpu_model": cpu_model()}
+
+
+def roofline_of(kernel, nbytes, ms):
+    """The roofline object of a multiply-accumulate kernel: algorithmic bytes over its
+    event-timed duration against the 8 TB/s HBM peak (no counter run behind it: traffic null)."""
+    achieved = nbytes / (ms * 1e-3) / 1e9
+    return {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None, "kernel": kernel,
+            "algorithmic_bytes": int(nbytes), "avg_ms": round(ms, 4)}
 
 
 def mac_batch_bytes(nq, n_pairs, B, ptw):
@@ -463,7 +548,7 @@ def run_batch_level(bn, args, r, nq):
             "unit": "scores/s", "phases_ms": {"prepare_ms": round(prep_ms, 4), "score_batch_ms": round(score_ms, 4),
                                               "mac_ms": round(mac_ms, 4), "giant_ms": round(giant_ms, 4)},
             "mac_achieved_GBs": round(mac_bytes / (mac_ms * 1e-3) / 1e9, 1), "mac_algorithmic_bytes": mac_bytes,
-            "max_abs_score_err": err}
+            "roofline": roofline_of("k_mac_diag", mac_bytes, mac_ms), "max_abs_score_err": err}
 
 
 def run_tiny(bn, args):
@@ -683,23 +768,37 @@ def mac_source_sha256(kernel=MAC_KERNEL):
     return hashlib.sha256(src[a:b].encode()).hexdigest()
 
 
-def cpu_baseline_diag(bn, X, qv):
+def oracle_at_level(bn, w, L):
+    """The oracle's parameters at L ciphertext primes of the workload's chain, and a key
+    generator with the workload's key randomness restricted to those primes."""
+    from oracle import ckks
+    top = ckks.Params(logn=w.log_n, L=w.L, K=w.K)
+    par = top if L == w.L else ckks.Params(logn=w.log_n, L=L, K=w.K, primes=top.q[:L] + top.p)
+    idx = list(range(L)) + list(range(w.L, w.L + w.K))
+    orc = ckks.Oracle(par)
+
+    def rand(r):
+        a, e = bn.wl.key_randomness(w, r, top.primes, top.dnum)
+        return a[:par.dnum][:, idx], e[:par.dnum]
+    return par, orc, rand
+
+
+def cpu_baseline_diag(bn, X, qv, L=None, enc=False):
     """Time the oracle on a sample of the same level and scale to scores/s.
 
     Sample: two rotations of the query, and the oracle's block product with
-    G = 1 and G = 2 on the first B diagonals of block 0.  Level estimate =
-    (B-1) t_rot + n_blocks (t_G1 + (G-1)(t_G2 - t_G1)).
+    G = 1 and G = 2 on the first B diagonals of block 0 (with enc, the diagonals
+    encrypted and the ct x ct product with its relinearisations).  Level
+    estimate = (B-1) t_rot + n_blocks (t_G1 + (G-1)(t_G2 - t_G1)).
     """
     from oracle import ckks
     w = bn.w
     B, G = w.B, w.G
+    L = w.L if L is None else L
     t_start = time.time()
-    par = ckks.Params(logn=w.log_n, L=w.L, K=w.K)
-    orc = ckks.Oracle(par)
-    keys = {}
-    for r in (1, 2, B):
-        a, e = bn.wl.key_randomness(w, r, par.primes, par.dnum)
-        keys[r] = orc.keygen(bn.s, r, a, e)
+    par, orc, rand = oracle_at_level(bn, w, L)
+    keys = {r: orc.keygen(bn.s, r, *rand(r)) for r in (1, 2, B)}
+    rlk = orc.keygen_relin(bn.s, *rand(0)) if enc else None
     ea, ee = bn.wl.enc_randomness(w, par.q)
     m = ckks.encode(ckks.replicate(pad(qv, w.d), par.slots), par.n, 40)
     ct = orc.encrypt(m, ea, ee, bn.s)
@@ -711,25 +810,34 @@ def cpu_baseline_diag(bn, X, qv):
     rows = np.zeros((min(S, X.shape[0]), w.d))
     rows[:, :w.dim] = X[:S]
     diags = ckks.diagonals(rows, S, w.d)
-    pts = np.empty((2, B, par.L, par.n), dtype=np.uint64)
-    for gg in range(2):
-        for b in range(B):
-            pts[gg, b] = ckks.encode_residues(np.roll(diags[gg * B + b], gg * B), par)
+    coeffs = [ckks.encode(np.roll(diags[gg * B + b], gg * B), par.n, 40) for gg in range(2) for b in range(B)]
+    pts = np.stack([ckks.to_residues(c, par.q) for c in coeffs]).reshape(2, B, par.L, par.n)
+    if enc:
+        da, de = bn.wl.db_enc_randomness(w, par.q, 0, 2 * B)
+        cts = np.stack([orc.encrypt(c, da[j], de[j], bn.s) for j, c in enumerate(coeffs)])
+        cts = cts.reshape(2, B, 2, par.L, par.n)
     qrot = np.repeat(ct[None], B, axis=0)
     t = time.time()
-    orc.bsgs_block(qrot, pts[:1], B, 1, keys)
+    if enc:
+        orc.bsgs_block_ct(qrot, cts[:1], B, 1, keys, rlk)
+    else:
+        orc.bsgs_block(qrot, pts[:1], B, 1, keys)
     t_g1 = time.time() - t
     t = time.time()
-    orc.bsgs_block(qrot, pts, B, 2, keys)
+    if enc:
+        orc.bsgs_block_ct(qrot, cts, B, 2, keys, rlk)
+    else:
+        orc.bsgs_block(qrot, pts, B, 2, keys)
     t_g2 = time.time() - t
     est = (B - 1) * t_rot + w.n_blocks * (t_g1 + (G - 1) * max(t_g2 - t_g1, 0.0))
     cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    log(f"[bench] oracle sample: rot {t_rot:.2f}s, G1 {t_g1:.2f}s, G2 {t_g2:.2f}s -> level {est:.1f}s "
-        f"({time.time() - t_start:.1f}s wall)")
+    log(f"[bench] oracle sample at {L} primes{' (encrypted blocks)' if enc else ''}: rot {t_rot:.2f}s, "
+        f"G1 {t_g1:.2f}s, G2 {t_g2:.2f}s -> level {est:.1f}s ({time.time() - t_start:.1f}s wall)")
     return {"value": round(w.rows / est, 2), "unit": "scores/s", "cores": cores, "kind": "oracle",
-            "sample": f"2 rotations + block product with 1 and 2 giant groups (B={B}) on block 0 of the same "
-                      f"level; extrapolated to {B - 1} baby rotations and {w.n_blocks} blocks x {G} groups",
-            "level_s_est": round(est, 2)}
+            "sample": f"2 rotations + {'encrypted ' if enc else ''}block product with 1 and 2 giant groups "
+                      f"(B={B}) on block 0 of the same level at {L} primes; extrapolated to {B - 1} baby "
+                      f"rotations and {w.n_blocks} blocks x {G} groups",
+            "level_s_est": round(est, 2), "cpu_model": cpu_model()}
 
 
 def main():
@@ -820,7 +928,9 @@ def main():
                              "phases_ms": {k: round(v, 4) for k, v in r2["phases"].items()},
                              "max_abs_score_err": r2["err"],
                              "level_hbm_floor_ms": round(r2["stream_bytes"] / (HBM_PEAK_GBS * 1e9) * 1e3, 4),
-                             "mac_achieved_GBs": round(r2["mac_bytes"] / (r2["phases"]["mac_ms"] * 1e-3) / 1e9, 1)}
+                             "mac_achieved_GBs": round(r2["mac_bytes"] / (r2["phases"]["mac_ms"] * 1e-3) / 1e9, 1),
+                             "roofline": roofline_of(MAC_KERNEL, r2["mac_bytes"], r2["phases"]["mac_ms"]),
+                             "cpu_baseline": None if args.no_cpu_baseline else r2["cpu"]()}
         log(f"[bench] level drop to {args.also_level} primes: {r2['ms']:.3f} ms/level")
     if extra and args.enc_level:
         res["enc_db"] = run_enc_level(bn, args, min(args.enc_level, w.L))
@@ -831,6 +941,9 @@ def main():
         if r2 is not None:
             res["query_batch"].append(run_batch_level(bn, a2, r2, args.batch))
         for qb in res["query_batch"]:
+            ref = cpu if qb["scoring_level_primes"] == w.L else res.get("level_drop", {}).get("cpu_baseline")
+            qb["cpu_baseline"] = None if ref is None else dict(
+                ref, sample="the oracle scores a batch's queries one by one: " + ref["sample"])
             log(f"[bench] batch of {qb['queries']} at {qb['scoring_level_primes']} primes: "
                 f"{qb['ms_per_query_level']:.3f} ms per query level, {qb['value'] / 1e6:.1f} M scores/s")
     if extra and args.membership:
