@@ -4,7 +4,21 @@
 // Paper: Section 2 ("Measured prototype vs. deployment", "Reproducing this")
 // for the block-of-n/2-rows-as-d-diagonals scorer; Section 3.1 ("How",
 // "Detail") for the diagonal matrix-vector method, baby-step/giant-step with
-// plaintext pre-rotation of the database, and the single final fold.
+// plaintext pre-rotation of the database, and the single final fold;
+// Section 3.1 ("Membership search") for the threshold path.
+//
+// In order:
+//   errors, modular arithmetic and prime selection;
+//   encoding (FFT tables) and the context (tables, level contexts);
+//   keys, encryption, decryption and export (test and client side);
+//   decoding and enrollment of database blocks and projections;
+//   workspace arena, key switching (ModUp, key products, ModDown), rotations,
+//     relinearisation, lanes;
+//   scoring: baby phase, multiply-accumulate, giant phase, the encrypted-
+//     database variant, prepared queries and query batches;
+//   the membership path: rescale, ct x ct products, constants, the chain of
+//     levels, Chebyshev evaluator, sign iteration, the one-call scan;
+//   rotations, rotate-and-sum, phase profiling and the projection.
 
 #include <hip/hip_runtime.h>
 
