@@ -1541,7 +1541,12 @@ static bool chain_ok(const fa_ctx* hi, const fa_ctx* lo) {
 size_t fa_chain_workspace_bytes(const fa_ctx* top, int degree) {
   if (!top || degree < 1) return 0;
   const size_t ctw = 2 * (size_t)top->L * top->n;
-  return (size_t)(degree + 4) * rup(ctw) + 2 * rup(3 * (size_t)top->L * top->n) + relin_ws(top);
+  const size_t gen = (size_t)std::max(1, degree / 2);  // the widest generation of Chebyshev terms
+  // the terms, the sum and its rescale scratch; one generation's products (or a
+  // sign step's: three ciphertexts and one product)
+  return (size_t)(degree + 3) * rup(ctw) +
+         std::max(gen * (2 * rup(ctw) + rup(3 * (size_t)top->L * top->n)), 4 * rup(ctw) + rup(3 * (size_t)top->L * top->n)) +
+         relin_ws(top);
 }
 
 int fa_rescale(const fa_ctx* hi, const fa_ctx* lo, const void* ct, int n_polys, void* out, void* ws, size_t ws_bytes,
@@ -1694,43 +1699,58 @@ static int chain_mul_rescale(const Chain& ch, const CtRef& a, const CtRef& b, do
 }
 
 // sum_k coeffs[k] T_k(u) by the direct evaluator into out (scale u.s); the
-// terms and their scratch come from ar and are released on return
+// terms and their scratch come from ar and are released on return.  The terms
+// are formed generation by generation (T_2; T_3, T_4; T_5 .. T_8; ...): every
+// product of a generation reads terms of earlier generations only and sits at
+// one level, so a generation is one batched product, one fix-up and one rescale.
 static int cheb_core(const Chain& ch, const CtRef& u, const double* coeffs, int degree, double* out, CtRef& res,
                      Arena& ar, hipStream_t s) {
   const size_t mark = ar.used;
-  const size_t ctw = 2 * (size_t)u.L * ch.at(u.L)->n;
   std::vector<CtRef> T(degree + 1);
   T[1] = u;
   int rc;
   // T_k = Rescale(2 T_a T_b - T_{a-b}), with T_{a-b} brought to the product's
   // scale s_a s_b before the rescale: T_0 = 1 as the constant round(s_a s_b),
   // T_1 times the integer round(s_a s_b / s_1)
-  for (int k = 2; k <= degree; ++k) {
-    const int a = k % 2 == 0 ? k / 2 : k / 2 + 1, b = k / 2;
-    const int L = std::min(T[a].L, T[b].L);
+  for (int k0 = 2; k0 <= degree; k0 = 2 * k0 - 1) {
+    const int k1 = std::min(degree, 2 * (k0 - 1));  // generation k0 .. k1
+    const int count = k1 - k0 + 1;
+    std::vector<const double*> xs(count), ys(count);
+    std::vector<int> xLs(count), yLs(count), odd(count);
+    std::vector<double> sp(count);
+    int L = u.L;
+    for (int j = 0; j < count; ++j) {
+      const int k = k0 + j, a = (k + 1) / 2, b = k / 2;
+      xs[j] = T[a].p;
+      ys[j] = T[b].p;
+      xLs[j] = T[a].L;
+      yLs[j] = T[b].L;
+      odd[j] = k & 1;
+      sp[j] = T[a].s * T[b].s;
+      L = std::min(L, std::min(T[a].L, T[b].L));
+    }
     fa_ctx* c = ch.at(L);
     if (!c || !ch.at(L - 1)) return fail(FA_E_SHAPE, "the chain has no level %d", L - 1);
-    double* dst = ar.take(ctw);
-    if (!dst) return fail(FA_E_NOMEM, "workspace too small for the Chebyshev terms");
-    const size_t mark_k = ar.used, cw = 2 * (size_t)L * c->n;
-    double* prod = ar.take(cw);
-    double* t1 = ar.take(cw);
-    double* scr = ar.take(cw);
-    if (!prod || !t1 || !scr) return fail(FA_E_NOMEM, "workspace too small for the Chebyshev terms");
-    if ((rc = mul_relin_n(c, T[a].p, T[a].L, 0, T[b].p, T[b].L, 0, 1, prod, ar, s))) return rc;
-    fa::ct_elem(c, prod, prod, prod, 2, nullptr, 2, s);  // 2 T_a T_b
-    const double sp = T[a].s * T[b].s;
-    if (k % 2 == 0) {
-      const auto r = const_residues(c, -std::nearbyint(sp));
-      fa::ct_elem(c, prod, nullptr, prod, 2, r.data(), 1, s);
-    } else {
-      const auto r = const_residues(c, std::nearbyint(sp / T[1].s));
-      fa::ct_elem(c, T[1].p, nullptr, t1, 2, r.data(), 0, s, T[1].L);  // T_1 dropped to L, scaled
-      fa::ct_elem(c, prod, t1, prod, 2, nullptr, 3, s);
+    const size_t cw = 2 * (size_t)L * c->n, cwo = 2 * (size_t)(L - 1) * c->n;
+    double* gen = ar.take((size_t)count * cwo);
+    if (!gen) return fail(FA_E_NOMEM, "workspace too small for the Chebyshev terms");
+    const size_t mark_g = ar.used;
+    double* prod = ar.take((size_t)count * cw);
+    double* scr = ar.take((size_t)count * cw);
+    double* t3 = ar.take((size_t)count * 3 * L * c->n);
+    if (!prod || !scr || !t3) return fail(FA_E_NOMEM, "workspace too small for the Chebyshev terms");
+    fa::tensor_list(c, xs.data(), xLs.data(), ys.data(), yLs.data(), count, t3, s);
+    if ((rc = relin_batch(c, t3, count, prod, ar, s))) return rc;
+    std::vector<std::vector<uint64_t>> cres(count);
+    std::vector<const uint64_t*> cptr(count);
+    for (int j = 0; j < count; ++j) {
+      cres[j] = odd[j] ? const_residues(c, std::nearbyint(sp[j] / T[1].s)) : const_residues(c, -std::nearbyint(sp[j]));
+      cptr[j] = cres[j].data();
     }
-    fa::rescale(c, prod, 2, dst, scr, s);
-    T[k] = {dst, L - 1, sp / (double)c->primes[L - 1]};
-    ar.used = mark_k;
+    fa::cheb_fix(c, prod, count, T[1].p, T[1].L, cptr.data(), odd.data(), s);
+    fa::rescale(c, prod, 2 * count, gen, scr, s);
+    for (int j = 0; j < count; ++j) T[k0 + j] = {gen + (size_t)j * cwo, L - 1, sp[j] / (double)c->primes[L - 1]};
+    ar.used = mark_g;
   }
   int Lmin = u.L;
   for (int k = 1; k <= degree; ++k) Lmin = std::min(Lmin, T[k].L);
@@ -1739,22 +1759,22 @@ static int cheb_core(const Chain& ch, const CtRef& u, const double* coeffs, int 
   const double qn = (double)c->primes[Lmin - 1];
   const size_t cw = 2 * (size_t)Lmin * c->n;
   double* acc = ar.take(cw);
-  double* term = ar.take(cw);
-  double* scr = ar.take(2 * (size_t)Lmin * c->n);
-  if (!acc || !term || !scr) return fail(FA_E_NOMEM, "workspace too small for the Chebyshev sum");
+  double* scr = ar.take(cw);
+  if (!acc || !scr) return fail(FA_E_NOMEM, "workspace too small for the Chebyshev sum");
   // every term is brought to the one scale u.s * qn: its constant carries u.s / T_k.s
+  std::vector<std::vector<uint64_t>> ck(degree);
+  std::vector<const uint64_t*> cptr(degree);
+  std::vector<const double*> xs(degree);
+  std::vector<int> xLs(degree);
   for (int k = 1; k <= degree; ++k) {
-    const auto ck = const_residues(c, std::nearbyint(coeffs[k] * qn * (u.s / T[k].s)));
-    if (k == 1) {
-      fa::ct_elem(c, T[k].p, nullptr, acc, 2, ck.data(), 0, s, T[k].L);
-    } else {
-      fa::ct_elem(c, T[k].p, nullptr, term, 2, ck.data(), 0, s, T[k].L);
-      fa::ct_elem(c, acc, term, acc, 2, nullptr, 2, s);
-    }
+    ck[k - 1] = const_residues(c, std::nearbyint(coeffs[k] * qn * (u.s / T[k].s)));
+    cptr[k - 1] = ck[k - 1].data();
+    xs[k - 1] = T[k].p;
+    xLs[k - 1] = T[k].L;
   }
   const double s_acc = u.s * qn;
   const auto c0 = const_residues(c, std::nearbyint(coeffs[0] * s_acc));
-  fa::ct_elem(c, acc, nullptr, acc, 2, c0.data(), 1, s);
+  fa::lincomb(c, acc, xs.data(), xLs.data(), cptr.data(), degree, c0.data(), s);
   fa::rescale(c, acc, 2, out, scr, s);
   res = {out, Lmin - 1, s_acc / qn};
   ar.used = mark;
@@ -1999,8 +2019,7 @@ int fa_membership(fa_ctx* const* levels, int n_levels, const void* q_r, int L_q,
   const size_t ctw_t = 2 * (size_t)t.L * n;
   double* db = ar.take((size_t)n_blocks * ctw_t);
   if (!db) return fail(FA_E_NOMEM, "workspace too small for the differences");
-  for (int i = 0; i < n_blocks; ++i)
-    fa::ct_elem(ct, scores + (size_t)i * ctw_y, tb, db + (size_t)i * ctw_t, 2, nullptr, 3, s, L_q - 1);
+  fa::ct_elem(ct, scores, tb, db, 2 * n_blocks, nullptr, 3, s, L_q - 1, ctw_y, 0, ctw_t);
   CtRef res{};
   int64_t mo = m;
   if ((rc = sign_core_n(ch, db, t.L, ctw_t, n_blocks, s_sc, m, iters, (double*)out, ctw_q, res, mo, ar, s)))

@@ -188,8 +188,24 @@ void tensor(const fa_ctx* c, const double* x, int xL, size_t sx, const double* y
 // the even polynomials (the first of each ciphertext), 2 out = x + y, 3 out = x - y (cst
 // given by its residues cres[L], or null); x has xL limbs per polynomial (0: L), its
 // first L read
+// (ciphertext j of a batch at x + j*sx, y + j*sy, out + j*so words; by default
+// consecutive ciphertexts)
 void ct_elem(const fa_ctx* c, const double* x, const double* y, double* out, int n_polys, const uint64_t* cres,
-             int mode, hipStream_t s, int xL = 0);
+             int mode, hipStream_t s, int xL = 0, size_t sx = (size_t)-1, size_t sy = (size_t)-1,
+             size_t so = (size_t)-1);
+// tensors of count ciphertext pairs (x_j, y_j) given by pointer, each with its own
+// limbs per polynomial (xL[j], yL[j]; the first L read); out [count][3][L][N]
+void tensor_list(const fa_ctx* c, const double* const* xs, const int* xLs, const double* const* ys, const int* yLs,
+                 int count, double* out, hipStream_t s);
+// in place over count ciphertexts prod [count][2][L][N]: p_j <- 2 p_j - c_j T1 when
+// odd[j], else 2 p_j + c_j on polynomial 0 (c_j given by its residues cres[j][L];
+// T1 with t1L limbs per polynomial)
+void cheb_fix(const fa_ctx* c, double* prod, int count, const double* t1, int t1L, const uint64_t* const* cres,
+              const int* odd, hipStream_t s);
+// out [2][L][N] = sum_i x_i * c_i + c0 on polynomial 0 (x_i canonical, xL[i] limbs per
+// polynomial; c_i by residues cres[i][L]; c0 by residues or null)
+void lincomb(const fa_ctx* c, double* out, const double* const* xs, const int* xLs, const uint64_t* const* cres,
+             int nterm, const uint64_t* c0res, hipStream_t s);
 
 // out[w] = ct * pt[w] (both polys), w < count
 void mul_plain(const fa_ctx* c, const double* ct, const double* const* pts, int count, double* out, hipStream_t s);

@@ -1133,6 +1133,25 @@ struct ResArgs {
   double c[FA_MAXLIMB];   // per limb: q_last^-1 mod q_t (rescale) or a constant mod q_t
   double cp[FA_MAXLIMB];  // c * (1/q_t)
 };
+#define FA_MAXTERM 8
+struct TensorList {
+  const double* x[FA_MAXTERM];
+  const double* y[FA_MAXTERM];
+  int xL[FA_MAXTERM], yL[FA_MAXTERM];
+};
+struct ChebFixArgs {
+  double c[FA_MAXTERM][FA_MAXLIMB];
+  double cp[FA_MAXTERM][FA_MAXLIMB];
+  int odd[FA_MAXTERM];
+};
+struct LinArgs {
+  const double* x[FA_MAXTERM];
+  int xL[FA_MAXTERM];
+  double c[FA_MAXTERM][FA_MAXLIMB];
+  double cp[FA_MAXTERM][FA_MAXLIMB];
+  double c0[FA_MAXLIMB];
+  int nterm, accumulate;
+};
 __global__ __launch_bounds__(256) void k_rescale_lift(const double* __restrict__ last, double* __restrict__ lift,
                                                       const DevPrime* __restrict__ pr, int logn, int Lm1,
                                                       double ql) {
@@ -1175,22 +1194,76 @@ __global__ __launch_bounds__(256) void k_tensor(const double* __restrict__ x, co
   out[ln + o] = canon_full(mul(x0, y1, q, qinv) + mul(x1, y0, q, qinv), q, qinv);
   out[2 * ln + o] = canon_full(mul(x1, y1, q, qinv), q, qinv);
 }
-// out[h][t] = x[h][t] * c_t (mode 0), or out = x with c_t added to the first polynomial of
-// every ciphertext (even h, mode 1), or out[h][t] = x[h][t] +/- y[h][t] (mode 2 add, mode 3
-// subtract); x has xL limbs per polynomial (its first L read), y and out L
-__global__ __launch_bounds__(256) void k_ct_elem(const double* __restrict__ x, const double* __restrict__ y,
-                                                 double* __restrict__ out, ResArgs a,
-                                                 const DevPrime* __restrict__ pr, int logn, int L, int xL, int mode) {
+// tensors of count ciphertext pairs given by pointer (pair j = blockIdx.z): x_j with
+// xL[j] limbs per polynomial (its first L read), likewise y_j; out_j = out + j*3LN
+__global__ __launch_bounds__(256) void k_tensor_list(TensorList a, double* __restrict__ out,
+                                                     const DevPrime* __restrict__ pr, int logn, int L) {
+  const int n = 1 << logn;
+  const int k = blockIdx.x * 256 + threadIdx.x;
+  const int t = blockIdx.y, j = blockIdx.z;
+  const double q = pr[t].q, qinv = pr[t].qinv;
+  const size_t o = (size_t)t * n + k, ln = (size_t)L * n;
+  const double* __restrict__ x = a.x[j];
+  const double* __restrict__ y = a.y[j];
+  const double x0 = x[o], x1 = x[(size_t)a.xL[j] * n + o], y0 = y[o], y1 = y[(size_t)a.yL[j] * n + o];
+  out += (size_t)j * 3 * ln;
+  out[o] = canon_full(mul(x0, y0, q, qinv), q, qinv);
+  out[ln + o] = canon_full(mul(x0, y1, q, qinv) + mul(x1, y0, q, qinv), q, qinv);
+  out[2 * ln + o] = canon_full(mul(x1, y1, q, qinv), q, qinv);
+}
+// Chebyshev products, in place over count ciphertexts (pair j = blockIdx.z >> 1,
+// polynomial h = blockIdx.z & 1): p_j <- 2 p_j - c_j T1 (odd[j]; T1 with t1L limbs per
+// polynomial, its first L read) or 2 p_j + c_j on polynomial 0 (even)
+__global__ __launch_bounds__(256) void k_cheb_fix(double* __restrict__ prod, const double* __restrict__ t1,
+                                                  ChebFixArgs a, const DevPrime* __restrict__ pr, int logn, int L,
+                                                  int t1L) {
+  const int n = 1 << logn;
+  const int k = blockIdx.x * 256 + threadIdx.x;
+  const int t = blockIdx.y, j = blockIdx.z >> 1, h = blockIdx.z & 1;
+  const double q = pr[t].q, qinv = pr[t].qinv;
+  const size_t o = ((size_t)(2 * j + h) * L + t) * n + k;
+  double v = prod[o];
+  v = v + v;
+  if (a.odd[j]) v -= mulc(t1[((size_t)h * t1L + t) * n + k], a.c[j][t], a.cp[j][t], q);
+  else if (h == 0) v += a.c[j][t];
+  prod[o] = canon_full(v, q, qinv);
+}
+// out = (accumulate ? out : 0) + sum_i x_i * c_i (+ c0 on polynomial 0), one ciphertext;
+// x_i canonical with xL[i] limbs per polynomial (its first L read); a reduction after
+// every four terms keeps the lazy sum below 5q
+__global__ __launch_bounds__(256) void k_lincomb(double* __restrict__ out, LinArgs a, const DevPrime* __restrict__ pr,
+                                                 int logn, int L) {
   const int n = 1 << logn;
   const int k = blockIdx.x * 256 + threadIdx.x;
   const int t = blockIdx.y, h = blockIdx.z;
   const double q = pr[t].q, qinv = pr[t].qinv;
   const size_t o = ((size_t)h * L + t) * n + k;
-  double v = x[((size_t)h * xL + t) * n + k];
+  double v = a.accumulate ? out[o] : 0.0;
+  for (int i = 0; i < a.nterm; ++i) {
+    v += mulc(a.x[i][((size_t)h * a.xL[i] + t) * n + k], a.c[i][t], a.cp[i][t], q);
+    if ((i & 3) == 3) v = reduce(v, q, qinv);
+  }
+  if (h == 0) v += a.c0[t];
+  out[o] = canon_full(v, q, qinv);
+}
+// out[h][t] = x[h][t] * c_t (mode 0), or out = x with c_t added to the first polynomial of
+// every ciphertext (even h, mode 1), or out[h][t] = x[h][t] +/- y[h][t] (mode 2 add, mode 3
+// subtract); x has xL limbs per polynomial (its first L read), y and out L
+__global__ __launch_bounds__(256) void k_ct_elem(const double* __restrict__ x, const double* __restrict__ y,
+                                                 double* __restrict__ out, ResArgs a,
+                                                 const DevPrime* __restrict__ pr, int logn, int L, int xL, int mode,
+                                                 size_t sx, size_t sy, size_t so) {
+  const int n = 1 << logn;
+  const int k = blockIdx.x * 256 + threadIdx.x;
+  const int t = blockIdx.y, h = blockIdx.z;
+  const size_t ct = (size_t)(h >> 1), p = (size_t)(h & 1);
+  const double q = pr[t].q, qinv = pr[t].qinv;
+  const size_t o = ct * so + (p * L + t) * n + k;
+  double v = x[ct * sx + (p * xL + t) * n + k];
   if (mode == 0) v = mulc(v, a.c[t], a.cp[t], q);
-  else if (mode == 1) v = (h & 1) == 0 ? v + a.c[t] : v;
-  else if (mode == 2) v = v + y[o];
-  else v = v - y[o];
+  else if (mode == 1) v = p == 0 ? v + a.c[t] : v;
+  else if (mode == 2) v = v + y[ct * sy + (p * L + t) * n + k];
+  else v = v - y[ct * sy + (p * L + t) * n + k];
   out[o] = canon_full(v, q, qinv);
 }
 
@@ -1715,11 +1788,75 @@ void tensor(const fa_ctx* c, const double* x, int xL, size_t sx, const double* y
                      xL, yL, sx, sy);
 }
 
+void tensor_list(const fa_ctx* c, const double* const* xs, const int* xLs, const double* const* ys, const int* yLs,
+                 int count, double* out, hipStream_t s) {
+  const size_t step = (size_t)3 * c->L * c->n;
+  for (int j0 = 0; j0 < count; j0 += FA_MAXTERM) {
+    const int m = std::min(FA_MAXTERM, count - j0);
+    TensorList a{};
+    for (int j = 0; j < m; ++j) {
+      a.x[j] = xs[j0 + j];
+      a.y[j] = ys[j0 + j];
+      a.xL[j] = xLs[j0 + j];
+      a.yL[j] = yLs[j0 + j];
+    }
+    hipLaunchKernelGGL(k_tensor_list, dim3(c->n / 256, c->L, m), dim3(256), 0, s, a, out + (size_t)j0 * step,
+                       c->d_pr, c->logn, c->L);
+  }
+}
+
+void cheb_fix(const fa_ctx* c, double* prod, int count, const double* t1, int t1L, const uint64_t* const* cres,
+              const int* odd, hipStream_t s) {
+  const size_t step = (size_t)2 * c->L * c->n;
+  for (int j0 = 0; j0 < count; j0 += FA_MAXTERM) {
+    const int m = std::min(FA_MAXTERM, count - j0);
+    ChebFixArgs a{};
+    for (int j = 0; j < m; ++j) {
+      const ResArgs r = res_args(c, cres[j0 + j], c->L);
+      for (int t = 0; t < FA_MAXLIMB; ++t) {
+        a.c[j][t] = r.c[t];
+        a.cp[j][t] = r.cp[t];
+      }
+      a.odd[j] = odd[j0 + j];
+    }
+    hipLaunchKernelGGL(k_cheb_fix, dim3(c->n / 256, c->L, 2 * m), dim3(256), 0, s, prod + (size_t)j0 * step,
+                       t1, a, c->d_pr, c->logn, c->L, t1L);
+  }
+}
+
+void lincomb(const fa_ctx* c, double* out, const double* const* xs, const int* xLs, const uint64_t* const* cres,
+             int nterm, const uint64_t* c0res, hipStream_t s) {
+  for (int i0 = 0; i0 < nterm; i0 += FA_MAXTERM) {
+    const int m = std::min(FA_MAXTERM, nterm - i0);
+    LinArgs a{};
+    for (int i = 0; i < m; ++i) {
+      const ResArgs r = res_args(c, cres[i0 + i], c->L);
+      a.x[i] = xs[i0 + i];
+      a.xL[i] = xLs[i0 + i];
+      for (int t = 0; t < FA_MAXLIMB; ++t) {
+        a.c[i][t] = r.c[t];
+        a.cp[i][t] = r.cp[t];
+      }
+    }
+    if (i0 == 0 && c0res)
+      for (int t = 0; t < c->L; ++t) a.c0[t] = (double)c0res[t];
+    a.nterm = m;
+    a.accumulate = i0 > 0;
+    hipLaunchKernelGGL(k_lincomb, dim3(c->n / 256, c->L, 2), dim3(256), 0, s, out, a, c->d_pr, c->logn, c->L);
+  }
+}
+
 void ct_elem(const fa_ctx* c, const double* x, const double* y, double* out, int n_polys, const uint64_t* cres,
-             int mode, hipStream_t s, int xL) {
+             int mode, hipStream_t s, int xL, size_t sx, size_t sy, size_t so) {
   std::vector<uint64_t> zero(c->L, 0);
+  const int xl = xL ? xL : c->L;
+  const size_t n = c->n, ctw = 2 * (size_t)c->L * n;
+  // the defaults: consecutive ciphertexts (x with xl limbs per polynomial)
+  if (sx == (size_t)-1) sx = 2 * (size_t)xl * n;
+  if (sy == (size_t)-1) sy = ctw;
+  if (so == (size_t)-1) so = ctw;
   hipLaunchKernelGGL(k_ct_elem, dim3(c->n / 256, c->L, n_polys), dim3(256), 0, s, x, y, out,
-                     res_args(c, cres ? cres : zero.data(), c->L), c->d_pr, c->logn, c->L, xL ? xL : c->L, mode);
+                     res_args(c, cres ? cres : zero.data(), c->L), c->d_pr, c->logn, c->L, xl, mode, sx, sy, so);
 }
 
 void add_limbs(const fa_ctx* c, double* dst, const double* src, int n_limbs, int period, hipStream_t s) {
