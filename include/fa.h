@@ -11,6 +11,11 @@
  *   - the encrypted rank reduction Enc(W^T q) by the diagonal method with one
  *     final fold (Section 3.1, "How" and "Detail");
  *   - the rotate-and-sum fold and the row-packed variant;
+ *   - scoring at a dropped level, batches of queries per pass over the
+ *     blocks, and blocks of encrypted candidates (ct x ct);
+ *   - the membership path: rescaling, ciphertext products, a Chebyshev series
+ *     of the threshold and the sign iteration (Section 3.1, "Membership
+ *     search");
  *   - client-side helpers for tests and benchmarks: key generation, secret-key
  *     encryption, decryption, encoding and decoding (Section 2, "Setting").
  *
@@ -20,8 +25,10 @@
  *   below 2^50, in descending order.  Hybrid key switching uses alpha = K
  *   primes per digit and dnum = ceil(L/K) digits.  Slot j is the evaluation
  *   at zeta^(5^j mod 2N), zeta = exp(i*pi/N); rotating by r rolls the slots
- *   left by r (automorphism X -> X^(5^r)).  There is no rescaling: the scale
- *   of a product is the product of the scales.
+ *   left by r (automorphism X -> X^(5^r)).  The scoring calls do not
+ *   rescale: the scale of a product is the product of the scales.  The
+ *   membership calls (fa_rescale onwards) rescale after every ciphertext
+ *   product and track the scale as a double.
  *
  * Memory.  Ciphertext, plaintext and workspace buffers are caller-owned
  * DEVICE memory (for example torch tensors), 8-byte words, 256-byte aligned:
@@ -36,7 +43,10 @@
  *
  * Streams.  Calls that take `stream` (a hipStream_t) only enqueue work on it
  * and return; the caller synchronises.  Calls without `stream` are
- * synchronous.
+ * synchronous.  Some calls also use auxiliary streams of the context (default
+ * priority), forked from and joined back to `stream` with events, so their
+ * work is ordered on `stream` as a whole.  A context is used by one host
+ * thread at a time: its auxiliary streams and events are shared.
  *
  * Errors.  Every call returns FA_OK (0) or a negative FA_E_* code; all
  * argument checks happen on the host before any launch, so a failed call has

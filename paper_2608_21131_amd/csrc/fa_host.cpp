@@ -1830,6 +1830,20 @@ static size_t sign_ws(const fa_ctx* c, int count) {
   return 3 * rup((size_t)count * 2 * c->L * c->n) + mul_rescale_ws(c, count);
 }
 
+// levels the direct evaluator of this degree spends: ceil(log2 degree) product
+// generations and the final rescale
+static int cheb_depth(int degree) {
+  int g = 0;
+  while ((1 << g) < degree) ++g;
+  return g + 1;
+}
+// every level from L down to L - depth is in the chain (checked before any launch)
+static int chain_spans(const Chain& ch, int L, int depth) {
+  for (int l = L; l >= L - depth; --l)
+    if (!ch.at(l)) return fail(FA_E_SHAPE, "the chain has no level %d (%d levels needed below %d)", l, depth, L);
+  return FA_OK;
+}
+
 static int sign_args_ok(int64_t m, int iters) {
   if (iters < 1 || iters > 8) return fail(FA_E_INVAL, "iters %d out of [1, 8]", iters);
   for (int64_t mm = m, it = 0; it < iters; ++it, mm = 2 * mm * mm * mm)
@@ -1844,7 +1858,7 @@ int fa_cheb_eval(fa_ctx* const* levels, int n_levels, const void* u, int L_u, do
   Chain ch;
   int rc = make_chain(levels, n_levels, ch);
   if (rc) return rc;
-  if (!ch.at(L_u)) return fail(FA_E_SHAPE, "no level %d in the chain", L_u);
+  if ((rc = chain_spans(ch, L_u, cheb_depth(degree)))) return rc;
   const size_t need = fa_chain_workspace_bytes(levels[0], degree);
   if (!ws || ws_bytes < need) return fail(FA_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
   Arena ar{(char*)ws, ws_bytes, 0};
@@ -1863,7 +1877,7 @@ int fa_sign_iter(fa_ctx* const* levels, int n_levels, const void* v, int L_v, do
   if (rc) return rc;
   Chain ch;
   if ((rc = make_chain(levels, n_levels, ch))) return rc;
-  if (!ch.at(L_v)) return fail(FA_E_SHAPE, "no level %d in the chain", L_v);
+  if ((rc = chain_spans(ch, L_v, 2 * iters))) return rc;
   const size_t need = fa_chain_workspace_bytes(levels[0], 3);
   if (!ws || ws_bytes < need) return fail(FA_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
   Arena ar{(char*)ws, ws_bytes, 0};
@@ -1953,6 +1967,11 @@ int fa_membership(fa_ctx* const* levels, int n_levels, const void* q_r, int L_q,
   std::vector<int> fold;
   for (int k = 1; k < d; k <<= 1) fold.push_back(k);
   if (!has_rotations(cy, fold)) return fail(FA_E_NOKEY, "level %d lacks a rotation key for the norm's fold", L_q - 1);
+  if ((rc = chain_spans(ch, L_q, 1 + cheb_depth(degree) + 2 * iters))) return rc;
+  for (int g = 1; g < d / baby_step; ++g)
+    if (!cq->keys.count(g * baby_step)) return fail(FA_E_NOKEY, "no rotation key for giant step %d", g * baby_step);
+  for (int b = 1; b < baby_step; ++b)
+    if (!cq->keys.count(b)) return fail(FA_E_NOKEY, "no rotation key for baby step %d", b);
   size_t reg[3];
   membership_regions(cq, n_blocks, d, baby_step, degree, reg);
   const size_t need = reg[0] + reg[1] + reg[2];

@@ -578,3 +578,26 @@ def test_membership_scan_parity(y_lo, y_hi, degree, iters, nblk):
     ok = np.abs(margin) > abs(t - tau * np.sqrt(y)) + 2e-4
     assert np.all(np.sign(z[ok]) == np.sign(margin[ok]))
     assert 0 < np.count_nonzero(margin > 0) < len(X) // 4
+
+
+def test_chain_calls_reject_short_chains_and_bad_arguments():
+    """The chain calls check depth, multipliers and keys before any launch: a degree-7
+    series needs 4 levels below its input, two sign steps 4, and a multiplier that would
+    overflow is refused; the membership scan needs its fold keys."""
+    from paper_2608_21131_amd import fa
+    top, s, levels, och = _gpu_chain(10, 5, 2, 52)
+    x, _ = _enc_both(top, levels, och, s, np.full(top.slots, 0.5), 52, 1)
+    with pytest.raises(fa.FaError) as ei:
+        fa.cheb_eval(levels, x, top.L, 2.0 ** 50, np.ones(8))
+    assert ei.value.code == fa.FA_E_SHAPE
+    fa.cheb_eval(levels, x, top.L, 2.0 ** 50, np.ones(4))  # degree 3: 3 levels, 5 -> 2
+    with pytest.raises(fa.FaError) as ei:
+        fa.sign_iter(levels, x, top.L, 2.0 ** 50, 4, 3)
+    assert ei.value.code in (fa.FA_E_SHAPE, fa.FA_E_INVAL)
+    with pytest.raises(fa.FaError) as ei:
+        fa.sign_iter(levels, x, top.L, 2.0 ** 50, 1 << 21, 1)
+    assert ei.value.code == fa.FA_E_INVAL
+    blk = levels[0].new_pt(16)
+    with pytest.raises(fa.FaError) as ei:
+        fa.membership(levels, x, top.L, 2.0 ** 50, [blk], 16, 4, 0.5, 2.5, np.ones(2), 4, 1)
+    assert ei.value.code == fa.FA_E_NOKEY
