@@ -762,101 +762,137 @@ int fa_encode(const fa_ctx* c, const double* slots, int n_slots, int log_scale, 
 
 }  // extern "C"
 
-// centred CRT of L residues -> double, multi-word arithmetic (little endian)
+// Centred CRT of nl residues -> double by balanced mixed radix (Garner):
+// x = a_0 + q_0 (a_1 + q_1 (a_2 + ...)) with every digit a_i in
+// [-(q_i-1)/2, (q_i-1)/2].  For odd moduli these representations cover exactly
+// the centred range [-(Q-1)/2, (Q-1)/2], so the digits are those of the centred
+// residue.  Digit j: v = x mod q_j, then v <- (v - a_i) q_i^-1 mod q_j for
+// i < j.  Every prime lies in (2^49, 2^50), so |a_i| < q_i / 2 < q_j and
+// a_i mod q_j is a_i or a_i + q_j.  Horner in double from the top digit then
+// rounds once per step.
 namespace {
-struct Crt {
-  int L, W;
-  std::vector<u64> Q, halfQ;             // [W]
-  std::vector<std::vector<u64>> qhat;    // [L][W]
-  std::vector<u64> qhat_inv;             // [L]
-  std::vector<u64> q;
+constexpr int kMaxGarner = 16;
+struct Garner {
+  int nl = 0;
+  u64 q[kMaxGarner];
+  u64 inv[kMaxGarner][kMaxGarner], inv_sh[kMaxGarner][kMaxGarner];  // q_i^-1 mod q_j (i < j), Shoup companion
 };
-int cmp(const u64* a, const u64* b, int W) {
-  for (int i = W - 1; i >= 0; --i)
-    if (a[i] != b[i]) return a[i] < b[i] ? -1 : 1;
-  return 0;
+// Shoup companion of a constant w < q: floor(w 2^64 / q)
+u64 shoup(u64 w, u64 q) { return (u64)(((u128)w << 64) / q); }
+// a * w mod q for a < 2^64 and w < q < 2^63, with wsh = shoup(w, q)
+inline u64 mul_shoup(u64 a, u64 w, u64 wsh, u64 q) {
+  const u64 hq = (u64)(((u128)a * wsh) >> 64);
+  const u64 r = a * w - hq * q;  // in [0, 2q)
+  return r >= q ? r - q : r;
 }
-void sub_inplace(u64* a, const u64* b, int W) {
-  u64 borrow = 0;
-  for (int i = 0; i < W; ++i) {
-    const u128 d = (u128)a[i] - b[i] - borrow;
-    a[i] = (u64)d;
-    borrow = (u64)(d >> 64) ? 1 : 0;
-  }
+Garner make_garner(const fa_ctx* c, int nl) {
+  Garner g;
+  g.nl = nl;
+  for (int i = 0; i < nl; ++i) g.q[i] = c->primes[i];
+  for (int i = 0; i < nl; ++i)
+    for (int j = i + 1; j < nl; ++j) {
+      g.inv[i][j] = invmod(g.q[i] % g.q[j], g.q[j]);
+      g.inv_sh[i][j] = shoup(g.inv[i][j], g.q[j]);
+    }
+  return g;
 }
-void mul_small(std::vector<u64>& a, u64 m) {
-  u64 carry = 0;
-  for (auto& w : a) {
-    const u128 p = (u128)w * m + carry;
-    w = (u64)p;
-    carry = (u64)(p >> 64);
+// the centred integer with residues res[t * stride] (t < nl), as a double
+inline double garner_to_double(const Garner& g, const uint64_t* res, size_t stride) {
+  const int nl = g.nl;
+  int64_t a[kMaxGarner];
+  for (int j = 0; j < nl; ++j) {
+    const u64 qj = g.q[j];
+    u64 v = res[(size_t)j * stride];
+    if (v >= qj) v %= qj;  // fa_decrypt hands out canonical residues; others are reduced here
+    for (int i = 0; i < j; ++i) {
+      const u64 ai = a[i] < 0 ? (u64)(a[i] + (int64_t)qj) : (u64)a[i];
+      v = v >= ai ? v - ai : v + qj - ai;
+      v = mul_shoup(v, g.inv[i][j], g.inv_sh[i][j], qj);
+    }
+    a[j] = v > (qj - 1) / 2 ? (int64_t)v - (int64_t)qj : (int64_t)v;
   }
-  if (carry) a.push_back(carry);
+  double x = (double)a[nl - 1];
+  for (int i = nl - 2; i >= 0; --i) x = (double)a[i] + (double)g.q[i] * x;
+  return x;
 }
-Crt make_crt(const fa_ctx* c, int nl) {
-  Crt r;
-  r.L = nl;
-  r.q.assign(c->primes.begin(), c->primes.begin() + nl);
-  std::vector<u64> Q{1};
-  for (int t = 0; t < nl; ++t) mul_small(Q, r.q[t]);
-  r.W = (int)Q.size() + 1;
-  Q.resize(r.W, 0);
-  r.Q = Q;
-  r.halfQ = Q;
-  u64 carry = 0;
-  for (int i = r.W - 1; i >= 0; --i) {
-    const u64 w = r.halfQ[i];
-    r.halfQ[i] = (w >> 1) | (carry << 63);
-    carry = w & 1;
+
+// A_t = sum_k x_k e^{+2 pi i k t / n} over split real / imaginary arrays that
+// already hold x in bit-reversed order (x_k at index brev(k)); n a power of
+// two, radix-2 stages in place, A_t at index t.  twr / twi hold the stages'
+// twiddles one after the other: for the stage of span len (len = 4, 8, ...,
+// n), e^{+2 pi i j / len} for j < len/2 at offset len/2 - 2 (see dec_tables);
+// the span-2 stage needs none.
+void fft_pos_brev_in(double* re, double* im, int n, const double* twr, const double* twi) {
+  for (int s0 = 0; s0 < n; s0 += 2) {
+    const double ur = re[s0], ui = im[s0], vr = re[s0 + 1], vi = im[s0 + 1];
+    re[s0] = ur + vr;
+    im[s0] = ui + vi;
+    re[s0 + 1] = ur - vr;
+    im[s0 + 1] = ui - vi;
   }
-  r.qhat.resize(nl);
-  r.qhat_inv.resize(nl);
-  for (int t = 0; t < nl; ++t) {
-    std::vector<u64> h{1};
-    u64 hm = 1;
-    for (int j = 0; j < nl; ++j)
-      if (j != t) {
-        mul_small(h, r.q[j]);
-        hm = mulmod(hm, r.q[j] % r.q[t], r.q[t]);
+  for (int len = 4; len <= n; len <<= 1) {
+    const int h = len / 2;
+    const double* wr = twr + (h - 2);  // stage offsets: 0, 2, 6, 14, ... = h - 2
+    const double* wi = twi + (h - 2);
+    for (int s0 = 0; s0 < n; s0 += len) {
+      double* ar = re + s0;
+      double* ai = im + s0;
+      double* br = re + s0 + h;
+      double* bi = im + s0 + h;
+      for (int j = 0; j < h; ++j) {
+        const double vr = br[j] * wr[j] - bi[j] * wi[j];
+        const double vi = br[j] * wi[j] + bi[j] * wr[j];
+        const double ur = ar[j], ui = ai[j];
+        ar[j] = ur + vr;
+        ai[j] = ui + vi;
+        br[j] = ur - vr;
+        bi[j] = ui - vi;
       }
-    h.resize(r.W, 0);
-    r.qhat[t] = h;
-    r.qhat_inv[t] = invmod(hm, r.q[t]);
+    }
   }
-  return r;
 }
-double crt_to_double(const Crt& r, const uint64_t* res, size_t stride) {
-  std::vector<u64> acc(r.W + 1, 0);
-  for (int t = 0; t < r.L; ++t) {
-    const u64 y = mulmod(res[t * stride] % r.q[t], r.qhat_inv[t], r.q[t]);
-    u64 carry = 0;
-    for (int i = 0; i < r.W; ++i) {
-      const u128 p = (u128)r.qhat[t][i] * y + acc[i] + carry;
-      acc[i] = (u64)p;
-      carry = (u64)(p >> 64);
+
+// decode tables of ring degree n: e^{+2 pi i k / (n/2)} for k < n/4 (split),
+// and the slot -> transform index map t_j = (5^j mod 2n - 1) / 4
+struct DecTables {
+  std::vector<double> twr, twi;  // per-stage twiddles of fft_pos_brev_in for length n/2
+  std::vector<uint32_t> brev;    // bit reversal over log2(n/2) bits
+  std::vector<uint32_t> slot_t;
+};
+const DecTables& dec_tables(int n) {
+  static std::mutex mu;
+  static std::map<int, std::unique_ptr<DecTables>> cache;
+  std::lock_guard<std::mutex> lock(mu);
+  auto& slot = cache[n];
+  if (!slot) {
+    auto t = std::make_unique<DecTables>();
+    const int h = n / 2;
+    // stage of span len: e^{+2 pi i j / len}, j < len/2, at offset len/2 - 2;
+    // taken from the length-h table (index j h / len) so every stage uses the
+    // same rounded values as a single table would
+    std::vector<double> cr(h / 2), ci(h / 2);
+    for (int k = 0; k < h / 2; ++k) {
+      const double ang = 2.0 * M_PI * (double)k / (double)h;
+      cr[k] = std::cos(ang);
+      ci[k] = std::sin(ang);
     }
-    acc[r.W] += carry;
+    t->twr.assign(h > 2 ? h - 2 : 0, 0.0);
+    t->twi.assign(h > 2 ? h - 2 : 0, 0.0);
+    for (int len = 4; len <= h; len <<= 1)
+      for (int j = 0; j < len / 2; ++j) {
+        t->twr[len / 2 - 2 + j] = cr[(size_t)j * (h / len)];
+        t->twi[len / 2 - 2 + j] = ci[(size_t)j * (h / len)];
+      }
+    int bits = 0;
+    while ((1 << bits) < h) ++bits;
+    t->brev.resize(h);
+    for (int k = 0; k < h; ++k) t->brev[k] = bitrev((uint32_t)k, bits);
+    const std::vector<u64>& e = fft_tables(n).e;
+    t->slot_t.resize(h);
+    for (int j = 0; j < h; ++j) t->slot_t[j] = (uint32_t)((e[j] - 1) / 4);
+    slot = std::move(t);
   }
-  // reduce mod Q: acc < L * Q
-  while (acc[r.W] != 0 || cmp(acc.data(), r.Q.data(), r.W) >= 0) {
-    u64 borrow = 0;
-    for (int i = 0; i < r.W; ++i) {
-      const u128 d = (u128)acc[i] - r.Q[i] - borrow;
-      acc[i] = (u64)d;
-      borrow = (u64)(d >> 64) ? 1 : 0;
-    }
-    acc[r.W] -= borrow;
-  }
-  double sign = 1.0;
-  if (cmp(acc.data(), r.halfQ.data(), r.W) > 0) {
-    std::vector<u64> t = r.Q;
-    sub_inplace(t.data(), acc.data(), r.W);
-    std::copy(t.begin(), t.end(), acc.begin());
-    sign = -1.0;
-  }
-  double v = 0.0;
-  for (int i = r.W - 1; i >= 0; --i) v = v * 18446744073709551616.0 + (double)acc[i];
-  return sign * v;
+  return *slot;
 }
 }  // namespace
 
@@ -865,26 +901,36 @@ extern "C" {
 int fa_decode(const fa_ctx* c, const uint64_t* res, int log_scale, double* out, int n_slots) {
   if (!c || !res || !out) return fail(FA_E_INVAL, "fa_decode: null argument");
   if (n_slots < 0 || n_slots > c->n / 2) return fail(FA_E_SHAPE, "fa_decode: n_slots %d > N/2", n_slots);
-  const int n = c->n;
+  const int n = c->n, h = n / 2;
   // The decrypted value m' = m + e is far below the product of the first few
   // primes: |m'| < 2^(log_scale + 20) for slot values below 2^12 in magnitude,
   // so the centred CRT over just enough primes already returns it exactly.
   int nl = 0;
   double bits = 0.0;
   while (nl < c->L && bits < log_scale + 22.0) bits += std::log2((double)c->primes[nl++]);
-  Crt r = make_crt(c, nl);
-  std::vector<double> m(n);
-  parallel_for(16, [&](int w) {
-    for (int k = w; k < n; k += 16) m[k] = crt_to_double(r, res + k, (size_t)n);
-  });
-  // z(2t+1) = sum_k m_k w^k e^{+2 pi i k t / N}
+  if (nl > kMaxGarner) return fail(FA_E_SHAPE, "fa_decode: %d primes needed (at most %d)", nl, kMaxGarner);
+  const Garner g = make_garner(c, nl);
+  // Every slot exponent e_j = 5^j mod 2N is 1 mod 4, and X^(N/2) = i at such a
+  // root: m(zeta^e) = w(zeta^e) with w_k = m_k + i m_{k+N/2} (k < N/2).  With
+  // e = 4t + 1, w(zeta^e) = sum_k (w_k zeta^k) e^{+2 pi i k t / (N/2)}, one
+  // transform of length N/2.
   const FftTables& tb = fft_tables(n);
-  std::vector<cplx> y(n);
-  for (int k = 0; k < n; ++k) y[k] = cplx(m[k] * tb.twist[k].real(), m[k] * tb.twist[k].imag());
-  fft(y, tb.root_inv);
-  const std::vector<u64>& e = tb.e;
+  const DecTables& dt = dec_tables(n);
+  std::vector<double> re(h), im(h);
+  const int nw = std::max(1, std::min(8, h / 4096));
+  parallel_for(nw, [&](int w) {
+    for (int k = w; k < h; k += nw) {
+      const double lo = garner_to_double(g, res + k, (size_t)n);
+      const double hi = garner_to_double(g, res + k + h, (size_t)n);
+      const double cr = tb.twist[k].real(), ci = tb.twist[k].imag();
+      const uint32_t kb = dt.brev[k];
+      re[kb] = lo * cr - hi * ci;
+      im[kb] = lo * ci + hi * cr;
+    }
+  });
+  fft_pos_brev_in(re.data(), im.data(), h, dt.twr.data(), dt.twi.data());
   const double inv_scale = std::ldexp(1.0, -log_scale);
-  for (int j = 0; j < n_slots; ++j) out[j] = y[(e[j] - 1) / 2].real() * inv_scale;
+  for (int j = 0; j < n_slots; ++j) out[j] = re[dt.slot_t[j]] * inv_scale;
   return FA_OK;
 }
 

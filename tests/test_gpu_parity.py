@@ -169,6 +169,27 @@ def test_projection_parity(name, d_in, R, B, rows):
     assert np.max(np.abs(cos - ref)) < 1e-4
 
 
+@pytest.mark.parametrize("name,extra", [("p1", 0), ("p1", 40), ("p2", 40), ("p4", 40), ("p4", 80)])
+def test_decode_matches_oracle_decode(name, extra):
+    """The client decode (centred CRT over just enough primes, then the slot
+    transform) against the oracle's big-integer CRT and numpy FFT, on the
+    residues of m * 2^extra + noise for a slot vector encoded at 2^40: two
+    primes at scale 2^40, three at 2^80 and 2^120; also a short n_slots."""
+    p = pair(name)
+    g = np.random.default_rng(11 + extra)
+    v = g.uniform(-1, 1, p.par.slots)
+    m = [int(x) * (1 << extra) + int(e) for x, e in zip(ckks.encode(v, p.n, 40), g.integers(-999, 999, p.n))]
+    res = np.stack([np.array([x % q for x in m], dtype=np.uint64) for q in p.par.q])
+    ls = 40 + extra
+    say(f"[decode] {name} at 2^{ls}")
+    got = p.ctx.decode(res, ls)
+    ref = ckks.decode_residues(res, p.par, ls)
+    assert np.max(np.abs(got - ref)) < 1e-12
+    assert np.max(np.abs(got - v)) < 1e-6
+    short = p.ctx.decode(res, ls, n_slots=37)
+    assert short.shape == (37,) and np.array_equal(short, got[:37])
+
+
 @pytest.mark.parametrize("name", ["tiny", "p4"])
 def test_float_encode_matches_oracle(name):
     p = pair(name)
