@@ -55,7 +55,7 @@ def parse():
     ap.add_argument("--batch", type=int, default=4,
                     help="rerank: also time cross-query batching (this many queries per plaintext pass, each "
                          "prepared once, all scored against the same blocks) and report it under query_batch "
-                         "(0: skip)")
+                         "(0: skip); three_level: queries per coarse-level pass (at most 4)")
     ap.add_argument("--enc-level", type=int, default=3,
                     help="rerank: also time the encrypted-database variant (ct x ct, database diagonals encrypted "
                          "and enrolled at this many primes, lazy relinearisation) and report it under enc_db "
@@ -633,7 +633,13 @@ def run_three_level(bn, args):
     blocks, the last truncated to 11,696 rows) -> top-10.  Pool blocks are chosen by
     hashing the kept ids (id mod pool size), deterministic and data-oblivious in cost.
     Each query is dropped to --level primes (default 3) and its baby rotations are
-    computed once and reused by the three levels."""
+    computed once and reused by the three levels.
+
+    Queries run in groups of --batch (default 4): every query scores all coarse blocks,
+    so a group's coarse level is one cross-query batch (one pass over the coarse
+    plaintexts per group).  The fine and rerank blocks differ per query and are scored
+    one query at a time.  The client's decrypts run on a second stream, so its decode
+    and top-k of one query overlap the server's next level on the first."""
     w, fa, torch = bn.w, bn.fa, bn.torch
     top_ctx = bn.ctx
     level = args.level if args.level else 3
@@ -641,6 +647,7 @@ def run_three_level(bn, args):
     ex = w.extra
     S = w.slots
     nq = args.queries or ex["queries"]
+    gq = max(1, min(4, args.batch if args.batch else 1, nq))
     g_coarse, centers = bn.wl.candidate_rows(w, ex["coarse"], stream_extra=1)
     pools = {"coarse": [], "fine": [], "rerank": []}
     rows_of = {"coarse": [], "fine": [], "rerank": []}
@@ -657,26 +664,39 @@ def run_three_level(bn, args):
             pools[name].append(ctx.encode_db_block(r, w.d, fa.LAYOUT_DIAG, w.B))
     torch.cuda.synchronize()
     nblk = sum(len(v) for v in pools.values())
+    n_coarse = len(pools["coarse"])
     log(f"[bench] three_level: {nblk} resident blocks at {ctx.L} primes "
-        f"({nblk * w.d * ctx.L * w.n * 8 / 1e9:.1f} GB), {time.time() - bn.t0:.1f}s")
+        f"({nblk * w.d * ctx.L * w.n * 8 / 1e9:.1f} GB), {gq} queries per coarse pass, {time.time() - bn.t0:.1f}s")
     queries = bn.wl.query_vectors(w, nq, centers)
     qcts = [bn.encrypt(qv, tag=i) for i, qv in enumerate(queries)]
-    q = ctx.new_ct()
-    prep = ctx.prepare_query(qcts[0] if ctx is top_ctx else top_ctx.drop_level(ctx, qcts[0]), w.B)
-    out = ctx.new_ct(7)
+    qs = [ctx.new_ct() for _ in range(gq)] if ctx is not top_ctx else None
+    preps = [torch.empty(int(ctx.lib.fa_prepared_words(ctx.h, w.B)), dtype=torch.float64, device="cuda")
+             for _ in range(gq)]
+    outs_c = [ctx.new_ct(n_coarse) for _ in range(gq)]
+    outs_f = [ctx.new_ct(ex["fine_blocks"]) for _ in range(gq)]
+    outs_r = [ctx.new_ct(ex["rerank_blocks"]) for _ in range(gq)]
     ws_p = ctx.workspace(fa.OP_PREPARE, 1, w.B, w.B)
-    ws = ctx.workspace(fa.OP_SCORE_PREPARED, 7, w.d, w.B)
-    stream = torch.cuda.current_stream()
-    level_ms = []
+    ws_b = ctx.batch_workspace(gq, n_coarse, w.d, w.B)
+    ws_s = ctx.workspace(fa.OP_SCORE_PREPARED, max(ex["fine_blocks"], ex["rerank_blocks"]), w.d, w.B)
+    sa = torch.cuda.current_stream()
+    sb = torch.cuda.Stream()  # the client's decrypts (default priority)
+    gpu_ms = []  # per query: [prepare, coarse, fine, rerank]
     errs = []
 
     from concurrent.futures import ThreadPoolExecutor
     pool = ThreadPoolExecutor(max_workers=8)
 
-    def top(ct, nb, k, rows_list, qv, n_rows_last=None):
-        # client side: decrypt every block (device), then decode them on host threads
+    def ev():
+        e = torch.cuda.Event(enable_timing=True)
+        e.record(sa)
+        return e
+
+    def top(ct, nb, k, rows_list, qv, done, n_rows_last=None):
+        # client side: wait for the level on the second stream, decrypt every block
+        # there, then decode the blocks on host threads and keep the top k
+        sb.wait_event(done)
         W_ = ctx.ct_words
-        res = [ctx.decrypt(ct[b * W_:(b + 1) * W_]) for b in range(nb)]
+        res = [ctx.decrypt(ct[b * W_:(b + 1) * W_], stream=sb) for b in range(nb)]
         zs = list(pool.map(lambda r: ctx.decode(r, 80), res))
         scores = []
         for b in range(nb):
@@ -688,54 +708,65 @@ def run_three_level(bn, args):
                 errs.append(float(np.max(np.abs(z[:n_valid] - ref))))
         return topk(np.concatenate(scores), k)
 
-    def one_query(i, check):
-        qv = queries[i] if check else None
-        evs = [torch.cuda.Event(enable_timing=True) for _ in range(7)]
-        evs[0].record(stream)
-        if ctx is not top_ctx:
-            top_ctx.drop_level(ctx, qcts[i], out=q)
-            qi = q
-        else:
-            qi = qcts[i]
-        ctx.prepare_query(qi, w.B, out=prep, ws=ws_p)
-        evs[1].record(stream)
-        ctx.score_prepared(qi, prep, pools["coarse"], w.d, w.B, out=out, ws=ws)
-        evs[2].record(stream)
-        ids = top(out, len(pools["coarse"]), ex["top_coarse"], rows_of["coarse"], qv)
-        fsel = sorted(set(int(x) % ex["fine_pool_blocks"] for x in ids))
-        fsel = (fsel + [b for b in range(ex["fine_pool_blocks"]) if b not in fsel])[:ex["fine_blocks"]]
-        evs[3].record(stream)
-        ctx.score_prepared(qi, prep, [pools["fine"][b] for b in fsel], w.d, w.B, out=out, ws=ws)
-        evs[4].record(stream)
-        ids = top(out, len(fsel), ex["top_fine"], [rows_of["fine"][b] for b in fsel], qv)
-        rsel = sorted(set(int(x) % ex["rerank_pool_blocks"] for x in ids))
-        rsel = (rsel + [b for b in range(ex["rerank_pool_blocks"]) if b not in rsel])[:ex["rerank_blocks"]]
-        evs[5].record(stream)
-        ctx.score_prepared(qi, prep, [pools["rerank"][b] for b in rsel], w.d, w.B, out=out, ws=ws)
-        evs[6].record(stream)
-        top(out, len(rsel), 10, [rows_of["rerank"][b] for b in rsel], qv, n_rows_last=ex["rerank_last"])
+    def group(i0, check):
+        m = min(gq, nq - i0)
+        qv = [queries[i0 + j] if check else None for j in range(m)]
+        qi = []
+        e0 = ev()
+        for j in range(m):
+            if qs is not None:
+                top_ctx.drop_level(ctx, qcts[i0 + j], out=qs[j])
+                qi.append(qs[j])
+            else:
+                qi.append(qcts[i0 + j])
+            ctx.prepare_query(qi[j], w.B, out=preps[j], ws=ws_p)
+        e1 = ev()
+        ctx.score_batch(qi, preps[:m], pools["coarse"], w.d, w.B, outs=outs_c[:m], ws=ws_b)
+        e2 = ev()
+        fine, rer = [], []
+        for j in range(m):
+            ids = top(outs_c[j], n_coarse, ex["top_coarse"], rows_of["coarse"], qv[j], e2)
+            fsel = sorted(set(int(x) % ex["fine_pool_blocks"] for x in ids))
+            fsel = (fsel + [b for b in range(ex["fine_pool_blocks"]) if b not in fsel])[:ex["fine_blocks"]]
+            a = ev()
+            ctx.score_prepared(qi[j], preps[j], [pools["fine"][b] for b in fsel], w.d, w.B, out=outs_f[j], ws=ws_s)
+            fine.append((a, ev(), fsel))
+        for j in range(m):
+            fsel = fine[j][2]
+            ids = top(outs_f[j], len(fsel), ex["top_fine"], [rows_of["fine"][b] for b in fsel], qv[j], fine[j][1])
+            rsel = sorted(set(int(x) % ex["rerank_pool_blocks"] for x in ids))
+            rsel = (rsel + [b for b in range(ex["rerank_pool_blocks"]) if b not in rsel])[:ex["rerank_blocks"]]
+            a = ev()
+            ctx.score_prepared(qi[j], preps[j], [pools["rerank"][b] for b in rsel], w.d, w.B, out=outs_r[j],
+                               ws=ws_s)
+            rer.append((a, ev(), rsel))
+        for j in range(m):
+            rsel = rer[j][2]
+            top(outs_r[j], len(rsel), 10, [rows_of["rerank"][b] for b in rsel], qv[j], rer[j][1],
+                n_rows_last=ex["rerank_last"])
         torch.cuda.synchronize()
-        level_ms.append([evs[0].elapsed_time(evs[1]), evs[1].elapsed_time(evs[2]), evs[3].elapsed_time(evs[4]),
-                         evs[5].elapsed_time(evs[6])])
+        for j in range(m):
+            gpu_ms.append([e0.elapsed_time(e1) / m, e1.elapsed_time(e2) / m, fine[j][0].elapsed_time(fine[j][1]),
+                           rer[j][0].elapsed_time(rer[j][1])])
 
-    for i in range(min(2, nq)):  # warm-up queries (the first one checked against float64)
-        one_query(i, check=(i == 0))
-    level_ms.clear()
+    group(0, check=True)  # warm-up group, checked against float64
+    gpu_ms.clear()
     t = time.time()
     steps = max(1, args.steps)
     for _ in range(steps):
-        for i in range(nq):
-            one_query(i, check=False)
+        for i0 in range(0, nq, gq):
+            group(i0, check=False)
     wall = (time.time() - t) / (steps * nq)
-    lm = np.array(level_ms)
+    lm = np.array(gpu_ms)
     gpu_q = float(lm.sum(axis=1).mean())
     n_scores = ex["coarse"] + ex["fine_blocks"] * S + (ex["rerank_blocks"] - 1) * S + ex["rerank_last"]
     ph = {"prepare_ms": float(lm[:, 0].mean()), "coarse_ms": float(lm[:, 1].mean()),
           "fine_ms": float(lm[:, 2].mean()), "rerank_ms": float(lm[:, 3].mean()), "query_gpu_ms": gpu_q,
           "query_wall_ms": wall * 1e3}
-    blocks_q = len(pools["coarse"]) + ex["fine_blocks"] + ex["rerank_blocks"]
+    blocks_q = n_coarse + ex["fine_blocks"] + ex["rerank_blocks"]
     return dict(ms=gpu_q, scores=n_scores, phases=ph, err=max(errs) if errs else None, mac_bytes=None,
-                stream_bytes=8 * blocks_q * w.d * ctx.L * w.n, cpu=None, queries=nq, level=ctx.L)
+                stream_bytes=8 * blocks_q * w.d * ctx.L * w.n, cpu=None, queries=nq, level=ctx.L,
+                coarse_group=gq)
 
 
 def measured_traffic(path):
@@ -888,6 +919,8 @@ def main():
                             "level before scoring")
     if r.get("queries"):
         cfg["queries_per_step"] = r["queries"]
+    if r.get("coarse_group"):
+        cfg["queries_per_coarse_pass"] = r["coarse_group"]
     if r.get("level") and r["level"] < w.L:
         cfg["scoring_level_primes"] = r["level"]
     res = {
