@@ -497,8 +497,9 @@ def mac_batch_bytes(nq, n_pairs, B, ptw):
 
 def run_batch_level(bn, args, r, nq):
     """Cross-query batching on the level r was timed on (same context and resident blocks):
-    per step, nq fresh queries are (dropped and) prepared -- their baby rotations -- and then
-    scored together, every plaintext pass serving up to four of them."""
+    per step, nq fresh queries are (dropped and) prepared together -- their baby rotations,
+    each step's key switches issued for all of them at once -- and then scored together,
+    every plaintext pass serving up to four of them."""
     w, fa, torch = bn.w, bn.fa, bn.torch
     top, ctx, blocks = bn.ctx, r["ctx"], r["blocks"]
     X, S = r["X"], w.slots
@@ -508,7 +509,7 @@ def run_batch_level(bn, args, r, nq):
     preps = [torch.empty(int(ctx.lib.fa_prepared_words(ctx.h, w.B)), dtype=torch.float64, device="cuda")
              for _ in range(nq)]
     outs = [ctx.new_ct(w.n_blocks) for _ in range(nq)]
-    ws_p = ctx.workspace(fa.OP_PREPARE, 1, w.B, w.B)
+    ws_p = ctx.prepare_batch_workspace(nq, w.B)
     ws_b = ctx.batch_workspace(nq, w.n_blocks, w.d, w.B)
     stream = torch.cuda.current_stream()
     marks, phases = [], []
@@ -516,10 +517,10 @@ def run_batch_level(bn, args, r, nq):
     def step():
         e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
         e0.record(stream)
-        for j in range(nq):
-            if ctx is not top:
+        if ctx is not top:
+            for j in range(nq):
                 top.drop_level(ctx, q_tops[j], out=qs[j])
-            ctx.prepare_query(qs[j], w.B, out=preps[j], ws=ws_p)
+        ctx.prepare_batch(qs, w.B, outs=preps, ws=ws_p)
         e1.record(stream)
         ctx.score_batch(qs, preps, blocks, w.d, w.B, outs=outs, ws=ws_b)
         e2.record(stream)
@@ -637,8 +638,8 @@ def run_three_level(bn, args):
 
     Queries run in groups of --batch (default 4): every query scores all coarse blocks,
     so a group's coarse level is one cross-query batch (one pass over the coarse
-    plaintexts per group).  The fine and rerank blocks differ per query and are scored
-    one query at a time.  The client's decrypts run on a second stream, so its decode
+    plaintexts per group), and the group's queries are prepared together.  The fine and
+    rerank blocks differ per query and are scored one query at a time.  The client's decrypts run on a second stream, so its decode
     and top-k of one query overlap the server's next level on the first."""
     w, fa, torch = bn.w, bn.fa, bn.torch
     top_ctx = bn.ctx
@@ -675,7 +676,7 @@ def run_three_level(bn, args):
     outs_c = [ctx.new_ct(n_coarse) for _ in range(gq)]
     outs_f = [ctx.new_ct(ex["fine_blocks"]) for _ in range(gq)]
     outs_r = [ctx.new_ct(ex["rerank_blocks"]) for _ in range(gq)]
-    ws_p = ctx.workspace(fa.OP_PREPARE, 1, w.B, w.B)
+    ws_p = ctx.prepare_batch_workspace(gq, w.B)
     ws_b = ctx.batch_workspace(gq, n_coarse, w.d, w.B)
     ws_s = ctx.workspace(fa.OP_SCORE_PREPARED, max(ex["fine_blocks"], ex["rerank_blocks"]), w.d, w.B)
     sa = torch.cuda.current_stream()
@@ -719,7 +720,7 @@ def run_three_level(bn, args):
                 qi.append(qs[j])
             else:
                 qi.append(qcts[i0 + j])
-            ctx.prepare_query(qi[j], w.B, out=preps[j], ws=ws_p)
+        ctx.prepare_batch(qi, w.B, outs=preps[:m], ws=ws_p)
         e1 = ev()
         ctx.score_batch(qi, preps[:m], pools["coarse"], w.d, w.B, outs=outs_c[:m], ws=ws_b)
         e2 = ev()

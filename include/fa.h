@@ -248,6 +248,21 @@ int fa_prepare_query(fa_ctx* ctx, const void* q, int baby_step, void* prep, void
 int fa_score_prepared(fa_ctx* ctx, const void* q, const void* prep, const void* const* blocks, int n_blocks, int d,
                       int baby_step, void* out, void* ws, size_t ws_bytes, void* stream);
 
+/* Several queries prepared together (the same cross-query batching applied
+ * to the baby rotations): preps[j] receives exactly what
+ * fa_prepare_query(qs[j], baby_step) writes, for j < n_q.  The key switches
+ * of one baby step are issued for all n_q queries together, so a rotation
+ * key read from HBM for one query is found in the caches by the others.
+ * qs[j] device ciphertexts, preps[j] device, fa_prepared_words(ctx,
+ * baby_step) words each; workspace fa_prepare_batch_workspace_bytes(n_q,
+ * baby_step) bytes (it grows with n_q: every query's extended digits).
+ * Errors: FA_E_INVAL (null pointer, baby_step out of range), FA_E_SHAPE
+ * (n_q < 1), FA_E_NOKEY (a baby-step key is missing), FA_E_NOMEM (workspace
+ * too small). */
+size_t fa_prepare_batch_workspace_bytes(const fa_ctx* ctx, int n_q, int baby_step);
+int fa_prepare_batch(fa_ctx* ctx, const void* const* qs, int n_q, int baby_step, void* const* preps, void* ws,
+                     size_t ws_bytes, void* stream);
+
 /* Cross-query batching against resident blocks (section "Conclusion and
  * Future Work": score a batch of queries per loaded region so that the load
  * is paid once per batch): n_q queries,

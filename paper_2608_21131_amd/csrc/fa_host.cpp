@@ -1087,6 +1087,17 @@ size_t baby_ws(const fa_ctx* c, int B) {
   const size_t lanes = lanes_wanted();
   return rup(L * n) + rup(dn * np * n) + lanes * rup(rb * 2 * np * n) + lanes * rup(rb * 2 * L * n);
 }
+// workspace of the baby rotations of n_q queries prepared together (the
+// rotated queries themselves are separate): one query's coefficient-form c1,
+// every query's extended digits, and per lane the key-switch products and
+// conversions of one launch group (about as many rotations as baby_ws's group)
+int batch_steps(int nq) { return std::max(1, rot_batch() / std::max(1, nq)); }
+size_t baby_batch_ws(const fa_ctx* c, int nq, int B) {
+  const size_t n = c->n, L = c->L, np = c->np, dn = c->dnum;
+  const size_t items = (size_t)std::max(1, std::min(batch_steps(nq), B - 1)) * nq;
+  const size_t lanes = lanes_wanted();
+  return rup(L * n) + (size_t)nq * rup(dn * np * n) + lanes * rup(items * 2 * np * n) + lanes * rup(items * 2 * L * n);
+}
 // blocks whose giant steps are processed together
 constexpr int kGiantChunk = 8;
 // scratch of the giant steps of one query (accumulators not included)
@@ -1155,15 +1166,15 @@ static void moddown_polys(fa_ctx* c, double* u, int count, double* conv, const d
 // goes through u (per rotation [2][np][N]); the ciphertext-prime part is formed
 // inside the finishing kernel.  conv: per rotation [2][L][N] scratch.
 static void ks_moddown(fa_ctx* c, const fa::KsItem* ks, int count, const double* const* c0s, double* const* outs,
-                       double* u, double* conv, hipStream_t s, const double* const* b1s = nullptr) {
+                       double* u, double* conv, hipStream_t s, const double* const* b1s = nullptr, int nq = 1) {
   const size_t n = c->n, L = c->L;
-  fa::ks_inner(c, ks, count, false, s, c->L);
+  fa::ks_inner(c, ks, count, false, s, c->L, nq);
   moddown_polys(c, u, 2 * count, conv, nullptr, nullptr, nullptr, s, false);
   std::vector<fa::MdKsItem> it(count);
   for (int j = 0; j < count; ++j)
     it[j] = {conv + (size_t)2 * j * L * n, ks[j].ext, ks[j].c1, ks[j].key, c0s[j], b1s ? b1s[j] : nullptr, outs[j],
              ks[j].gal};
-  fa::moddown_ks(c, it.data(), count, s);
+  fa::moddown_ks(c, it.data(), count, s, nq);
 }
 
 // Auxiliary streams for `lanes` lanes (lane 0 is the caller's stream).
@@ -1319,6 +1330,60 @@ static int baby_phase(fa_ctx* c, const double* q, int B, double* qrot, Arena& ar
   if ((rc = join_lanes(c, s, bl))) return rc;
   ar.used = mark;
   return FA_OK;
+}
+
+// Baby rotations of n_q queries, qrots[j][b-1] = Rotate(qs[j], b), b = 1..B-1:
+// one ModUp per query, then launch groups of a few steps each holding the key
+// switches of every query for those steps (step-major), so that a step's key,
+// read from HBM for the first query, is found in the caches by the others.
+// Each rotation runs the same kernels on the same inputs as in baby_phase, so
+// the results are identical to preparing the queries one by one.
+static int baby_phase_batch(fa_ctx* c, const double* const* qs, int nq, int B, double* const* qrots, Arena& ar,
+                            hipStream_t s) {
+  const size_t n = c->n, L = c->L, np = c->np, dn = c->dnum;
+  const size_t ctw = 2 * L * n, ext_w = dn * np * n;
+  if (B < 2) return FA_OK;
+  for (int b = 1; b < B; ++b)
+    if (!c->keys.count(b)) return fail(FA_E_NOKEY, "no rotation key for baby step %d", b);
+  const int rbq = std::max(1, std::min(batch_steps(nq), B - 1));
+  const size_t items = (size_t)rbq * nq;
+  const int lanes = lanes_wanted();
+  const size_t u_lane = rup(items * 2 * np * n) / 8, c_lane = rup(items * 2 * L * n) / 8;
+  const size_t mark = ar.used;
+  double* y = ar.take(L * n);
+  double* ext = ar.take((size_t)nq * (rup(ext_w) / 8));
+  double* u = ar.take((size_t)lanes * u_lane);
+  double* conv = ar.take((size_t)lanes * c_lane);
+  if (!y || !ext || !u || !conv) return fail(FA_E_NOMEM, "workspace too small for the baby rotations");
+  int rc = ensure_lanes(c, lanes);
+  if (rc) return rc;
+  for (int j = 0; j < nq; ++j) modup(c, qs[j], ctw, 1, y, L * n, ext + (size_t)j * (rup(ext_w) / 8), ext_w, s);
+  const int ngroup = (B - 1 + rbq - 1) / rbq;
+  const int bl = std::min(lanes, ngroup);
+  if ((rc = fork_lanes(c, s, bl))) return rc;
+  std::vector<fa::KsItem> ks(items);
+  std::vector<const double*> c0s(items);
+  std::vector<double*> outs(items);
+  for (int r0 = 1, j0 = 0; r0 < B; r0 += rbq, ++j0) {
+    const int lane = j0 % bl;
+    hipStream_t ls = lane_stream(c, s, lane);
+    double* ul = u + lane * u_lane;
+    double* cl = conv + lane * c_lane;
+    int m = 0;
+    for (int b = r0; b < std::min(B, r0 + rbq); ++b) {
+      const double* key = c->keys[b];
+      const uint32_t gal = galois(c->n, b);
+      for (int j = 0; j < nq; ++j, ++m) {
+        ks[m] = {ext + (size_t)j * (rup(ext_w) / 8), qs[j] + L * n, key, ul + (size_t)m * 2 * np * n, nullptr, gal};
+        c0s[m] = qs[j];
+        outs[m] = qrots[j] + (size_t)(b - 1) * ctw;
+      }
+    }
+    ks_moddown(c, ks.data(), m, c0s.data(), outs.data(), ul, cl, ls, nullptr, nq);
+  }
+  if ((rc = join_lanes(c, s, bl))) return rc;
+  ar.used = mark;
+  return check_launch("prepare_batch");
 }
 
 // Giant steps of one query from its accumulators acc ([nb][G][2][L][N]):
@@ -1500,6 +1565,25 @@ int fa_prepare_query(fa_ctx* c, const void* q, int baby_step, void* prep, void* 
   Arena ar{(char*)ws, ws_bytes, 0};
   int rc = baby_phase(c, (const double*)q, baby_step, (double*)prep, ar, (hipStream_t)stream);
   return rc ? rc : check_launch("fa_prepare_query");
+}
+
+size_t fa_prepare_batch_workspace_bytes(const fa_ctx* c, int n_q, int baby_step) {
+  if (!c || n_q < 1 || baby_step < 1) return 0;
+  return baby_batch_ws(c, n_q, baby_step);
+}
+
+int fa_prepare_batch(fa_ctx* c, const void* const* qs, int n_q, int baby_step, void* const* preps, void* ws,
+                     size_t ws_bytes, void* stream) {
+  if (!c || !qs || !preps) return fail(FA_E_INVAL, "fa_prepare_batch: null argument");
+  if (n_q < 1) return fail(FA_E_SHAPE, "n_q must be positive");
+  for (int j = 0; j < n_q; ++j)
+    if (!qs[j] || !preps[j]) return fail(FA_E_INVAL, "query %d or its prepared buffer is null", j);
+  if (baby_step < 1 || baby_step > c->n / 2) return fail(FA_E_INVAL, "baby_step %d out of range", baby_step);
+  const size_t need = baby_batch_ws(c, n_q, baby_step);
+  if (baby_step > 1 && (!ws || ws_bytes < need)) return fail(FA_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
+  Arena ar{(char*)ws, ws_bytes, 0};
+  return baby_phase_batch(c, (const double* const*)qs, n_q, baby_step, (double* const*)preps, ar,
+                          (hipStream_t)stream);
 }
 
 int fa_score_prepared(fa_ctx* c, const void* q, const void* prep, const void* const* blocks, int n_blocks, int d,

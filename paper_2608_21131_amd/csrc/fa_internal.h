@@ -142,7 +142,10 @@ struct MdKsItem {
   double* out;         // [2][L][N]
   uint32_t gal;
 };
-void moddown_ks(const fa_ctx* c, const MdKsItem* items, int count, hipStream_t s);
+// nq > 1: the items come in groups of nq (g*nq .. g*nq+nq-1) sharing one key
+// (the same rotation of nq queries); their workgroups run back to back on one
+// XCD so the key words are read from HBM once per group.  count % nq == 0.
+void moddown_ks(const fa_ctx* c, const MdKsItem* items, int count, hipStream_t s, int nq = 1);
 
 // Key-switch inner product with the automorphism folded in:
 // u[j] (+)= sum_i sigma_{g_j}(ext[j or 0]_i) * key_j[i]  over all np primes.
@@ -155,7 +158,9 @@ struct KsItem {
   uint32_t gal;       // Galois element
 };
 // t0 > 0: only primes t0..np-1 (the special primes when t0 = L)
-void ks_inner(const fa_ctx* c, const KsItem* items, int count, bool accumulate, hipStream_t s, int t0 = 0);
+// nq > 1: items grouped by key as for moddown_ks (count % nq == 0)
+void ks_inner(const fa_ctx* c, const KsItem* items, int count, bool accumulate, hipStream_t s, int t0 = 0,
+              int nq = 1);
 
 // Fused giant steps of nb blocks: u[blk] = sum_{g=1..ng} sum_i sigma_g(NTT(ext)_i) key_g[i]
 // + P sigma_g(acc_g.c0), with ext = [nb][ng][dnum][np][N] holding only the first

@@ -411,15 +411,36 @@ struct MdKsArgs {
   fa::MdKsItem it[FA_MAXMD];
 };
 
+// Work item decode shared by the key-switch kernels: `rest` runs over (x, y,
+// key group) with x fastest; the nq items of a key group (the same rotation
+// for nq queries, items g*nq .. g*nq+nq-1) use the same key words.  With
+// nq > 1 the ids are decoded so that those nq workgroups run one after the
+// other on one XCD (ids 8 apart) and share the key words in its L2.  Returns
+// false for the padding ids of the last group of eight.
+__device__ __forceinline__ bool ks_decode(unsigned W, int nx, int ny, int nq, int ngroup, int& x, int& y, int& item) {
+  unsigned rest = W, qi = 0;
+  if (nq > 1) {
+    const unsigned j8 = W >> 3;
+    qi = j8 % (unsigned)nq;
+    rest = (j8 / (unsigned)nq) * 8u + (W & 7u);
+  }
+  if (rest >= (unsigned)(nx * ny * ngroup)) return false;
+  x = (int)(rest % (unsigned)nx);
+  y = (int)((rest / (unsigned)nx) % (unsigned)ny);
+  item = (int)(rest / (unsigned)(nx * ny)) * nq + (int)qi;
+  return true;
+}
+
 template <int DNUM, int ROWS>
 __global__ __launch_bounds__(256) void k_moddown_ks_b(MdKsArgs args, const DevPrime* __restrict__ pr,
                                                       const double* __restrict__ twt, const double* __restrict__ twr,
-                                                      int logn, int L, int np, int alpha) {
+                                                      int logn, int L, int np, int alpha, int nq, int ngroup) {
   __shared__ double sm[ROWS * ROWW];
-  const int t = blockIdx.y;
-  const fa::MdKsItem& it = args.it[blockIdx.z];
   const int n = 1 << logn;
-  const int row0 = blockIdx.x * ROWS;
+  int tile, t, item;
+  if (!ks_decode(blockIdx.x, (n >> 8) / ROWS, L, nq, ngroup, tile, t, item)) return;
+  const fa::MdKsItem& it = args.it[item];
+  const int row0 = tile * ROWS;
   const uint32_t k0 = (uint32_t)row0 * 256u + threadIdx.x;  // this thread's words: k0 + 256 j, j < ROWS
   const double q = pr[t].q, qinv = pr[t].qinv, pv = pr[t].pinv, pvp = pv * qinv;
   const int own = t / alpha;
@@ -532,11 +553,13 @@ struct KsArgs {
 
 template <int DNUM>
 __global__ __launch_bounds__(256) void k_ks_inner(KsArgs args, const DevPrime* __restrict__ pr, int logn, int L,
-                                                  int np, int alpha, int accumulate, int t0) {
+                                                  int np, int alpha, int accumulate, int t0, int nq, int ngroup) {
   const int n = 1 << logn;
-  const int k = blockIdx.x * 256 + threadIdx.x;
-  const int t = t0 + blockIdx.y;
-  const fa::KsItem& it = args.it[blockIdx.z];
+  int kx, tr, item;
+  if (!ks_decode(blockIdx.x, n / 256, np - t0, nq, ngroup, kx, tr, item)) return;
+  const int k = kx * 256 + threadIdx.x;
+  const int t = t0 + tr;
+  const fa::KsItem& it = args.it[item];
   const double q = pr[t].q, qinv = pr[t].qinv;
   const uint32_t kk = perm((uint32_t)k, it.gal, logn);
   const int own = t < L ? t / alpha : -1;
@@ -1480,61 +1503,72 @@ void moddown(const fa_ctx* c, const MdItem* items, int count, hipStream_t s, boo
   }
 }
 
-template <int DNUM>
-static void launch_moddown_ks(const fa_ctx* c, const MdKsArgs& a, int m, hipStream_t s) {
-  const int rows = (c->n >> 8) < 16 ? (c->n >> 8) : 16;
-  dim3 gb((c->n >> 8) / rows, c->L, m);
-  if (rows == 16)
-    hipLaunchKernelGGL((k_moddown_ks_b<DNUM, 16>), gb, dim3(256), 0, s, a, c->d_pr, c->d_twt_fwd, c->d_twr_fwd,
-                       c->logn, c->L, c->np, c->alpha);
-  else if (rows == 8)
-    hipLaunchKernelGGL((k_moddown_ks_b<DNUM, 8>), gb, dim3(256), 0, s, a, c->d_pr, c->d_twt_fwd, c->d_twr_fwd,
-                       c->logn, c->L, c->np, c->alpha);
-  else
-    hipLaunchKernelGGL((k_moddown_ks_b<DNUM, 4>), gb, dim3(256), 0, s, a, c->d_pr, c->d_twt_fwd, c->d_twr_fwd,
-                       c->logn, c->L, c->np, c->alpha);
+// 1-D grid of the key-switch kernels: nx * ny * ngroup work units, padded to
+// whole groups of eight per query when nq > 1 (see ks_decode)
+static unsigned ks_grid(int nx, int ny, int nq, int ngroup) {
+  const unsigned units = (unsigned)nx * ny * ngroup;
+  return nq > 1 ? 8u * nq * ((units + 7) / 8) : units;
 }
 
-void moddown_ks(const fa_ctx* c, const MdKsItem* items, int count, hipStream_t s) {
-  for (int off = 0; off < count; off += FA_MAXMD) {
-    const int m = count - off < FA_MAXMD ? count - off : FA_MAXMD;
+template <int DNUM>
+static void launch_moddown_ks(const fa_ctx* c, const MdKsArgs& a, int m, int nq, hipStream_t s) {
+  const int rows = (c->n >> 8) < 16 ? (c->n >> 8) : 16;
+  const int ngroup = m / nq;
+  dim3 gb(ks_grid((c->n >> 8) / rows, c->L, nq, ngroup));
+  if (rows == 16)
+    hipLaunchKernelGGL((k_moddown_ks_b<DNUM, 16>), gb, dim3(256), 0, s, a, c->d_pr, c->d_twt_fwd, c->d_twr_fwd,
+                       c->logn, c->L, c->np, c->alpha, nq, ngroup);
+  else if (rows == 8)
+    hipLaunchKernelGGL((k_moddown_ks_b<DNUM, 8>), gb, dim3(256), 0, s, a, c->d_pr, c->d_twt_fwd, c->d_twr_fwd,
+                       c->logn, c->L, c->np, c->alpha, nq, ngroup);
+  else
+    hipLaunchKernelGGL((k_moddown_ks_b<DNUM, 4>), gb, dim3(256), 0, s, a, c->d_pr, c->d_twt_fwd, c->d_twr_fwd,
+                       c->logn, c->L, c->np, c->alpha, nq, ngroup);
+}
+
+void moddown_ks(const fa_ctx* c, const MdKsItem* items, int count, hipStream_t s, int nq) {
+  const int chunk = (FA_MAXMD / nq) * nq;
+  for (int off = 0; off < count; off += chunk) {
+    const int m = count - off < chunk ? count - off : chunk;
     MdKsArgs a;
     for (int i = 0; i < m; ++i) a.it[i] = items[off + i];
     switch (c->dnum) {
-      case 1: launch_moddown_ks<1>(c, a, m, s); break;
-      case 2: launch_moddown_ks<2>(c, a, m, s); break;
-      case 3: launch_moddown_ks<3>(c, a, m, s); break;
-      case 4: launch_moddown_ks<4>(c, a, m, s); break;
-      case 5: launch_moddown_ks<5>(c, a, m, s); break;
-      case 6: launch_moddown_ks<6>(c, a, m, s); break;
-      case 7: launch_moddown_ks<7>(c, a, m, s); break;
-      case 8: launch_moddown_ks<8>(c, a, m, s); break;
+      case 1: launch_moddown_ks<1>(c, a, m, nq, s); break;
+      case 2: launch_moddown_ks<2>(c, a, m, nq, s); break;
+      case 3: launch_moddown_ks<3>(c, a, m, nq, s); break;
+      case 4: launch_moddown_ks<4>(c, a, m, nq, s); break;
+      case 5: launch_moddown_ks<5>(c, a, m, nq, s); break;
+      case 6: launch_moddown_ks<6>(c, a, m, nq, s); break;
+      case 7: launch_moddown_ks<7>(c, a, m, nq, s); break;
+      case 8: launch_moddown_ks<8>(c, a, m, nq, s); break;
       default: break;
     }
   }
 }
 
 template <int DNUM>
-static void launch_ks(const fa_ctx* c, const KsArgs& a, int m, bool accumulate, hipStream_t s, int t0) {
-  dim3 g(c->n / 256, c->np - t0, m);
+static void launch_ks(const fa_ctx* c, const KsArgs& a, int m, bool accumulate, hipStream_t s, int t0, int nq) {
+  const int ngroup = m / nq;
+  dim3 g(ks_grid(c->n / 256, c->np - t0, nq, ngroup));
   hipLaunchKernelGGL(k_ks_inner<DNUM>, g, dim3(256), 0, s, a, c->d_pr, c->logn, c->L, c->np, c->alpha,
-                     accumulate ? 1 : 0, t0);
+                     accumulate ? 1 : 0, t0, nq, ngroup);
 }
 
-void ks_inner(const fa_ctx* c, const KsItem* items, int count, bool accumulate, hipStream_t s, int t0) {
-  for (int off = 0; off < count; off += FA_MAXKS) {
+void ks_inner(const fa_ctx* c, const KsItem* items, int count, bool accumulate, hipStream_t s, int t0, int nq) {
+  const int chunk = (FA_MAXKS / nq) * nq;
+  for (int off = 0; off < count; off += chunk) {
     KsArgs a;
-    const int m = count - off < FA_MAXKS ? count - off : FA_MAXKS;
+    const int m = count - off < chunk ? count - off : chunk;
     for (int i = 0; i < m; ++i) a.it[i] = items[off + i];
     switch (c->dnum) {
-      case 1: launch_ks<1>(c, a, m, accumulate, s, t0); break;
-      case 2: launch_ks<2>(c, a, m, accumulate, s, t0); break;
-      case 3: launch_ks<3>(c, a, m, accumulate, s, t0); break;
-      case 4: launch_ks<4>(c, a, m, accumulate, s, t0); break;
-      case 5: launch_ks<5>(c, a, m, accumulate, s, t0); break;
-      case 6: launch_ks<6>(c, a, m, accumulate, s, t0); break;
-      case 7: launch_ks<7>(c, a, m, accumulate, s, t0); break;
-      case 8: launch_ks<8>(c, a, m, accumulate, s, t0); break;
+      case 1: launch_ks<1>(c, a, m, accumulate, s, t0, nq); break;
+      case 2: launch_ks<2>(c, a, m, accumulate, s, t0, nq); break;
+      case 3: launch_ks<3>(c, a, m, accumulate, s, t0, nq); break;
+      case 4: launch_ks<4>(c, a, m, accumulate, s, t0, nq); break;
+      case 5: launch_ks<5>(c, a, m, accumulate, s, t0, nq); break;
+      case 6: launch_ks<6>(c, a, m, accumulate, s, t0, nq); break;
+      case 7: launch_ks<7>(c, a, m, accumulate, s, t0, nq); break;
+      case 8: launch_ks<8>(c, a, m, accumulate, s, t0, nq); break;
       default: break;
     }
   }

@@ -103,6 +103,9 @@ SIGNATURES = {
                                      ctypes.c_int, _vp, ctypes.POINTER(ctypes.c_int),
                                      ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64), _vp,
                                      ctypes.c_size_t, _vp]),
+    "fa_prepare_batch_workspace_bytes": (ctypes.c_size_t, [_vp, ctypes.c_int, ctypes.c_int]),
+    "fa_prepare_batch": (ctypes.c_int, [_vp, ctypes.POINTER(_vp), ctypes.c_int, ctypes.c_int, ctypes.POINTER(_vp),
+                                        _vp, ctypes.c_size_t, _vp]),
     "fa_batch_workspace_bytes": (ctypes.c_size_t, [_vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int]),
     "fa_score_batch": (ctypes.c_int, [_vp, ctypes.POINTER(_vp), ctypes.POINTER(_vp), ctypes.c_int,
                                       ctypes.POINTER(_vp), ctypes.c_int, ctypes.c_int, ctypes.c_int,
@@ -334,6 +337,25 @@ class Context:
         _check(self.lib.fa_prepare_query(self.h, _dev(q), baby_step, _dev(out), _dev(ws), ws.numel() * 8,
                                          _stream(stream)))
         return out
+
+    def prepare_batch_workspace(self, n_q: int, baby_step: int) -> torch.Tensor:
+        nbytes = int(self.lib.fa_prepare_batch_workspace_bytes(self.h, n_q, baby_step))
+        return torch.empty(max(1, nbytes // 8 + 32), dtype=torch.float64, device="cuda")
+
+    def prepare_batch(self, qs, baby_step: int, outs=None, ws: torch.Tensor | None = None, stream=None) -> list:
+        """Prepare several queries together; outs[j] equals prepare_query(qs[j], baby_step)."""
+        qs = list(qs)
+        nq = len(qs)
+        words = int(self.lib.fa_prepared_words(self.h, baby_step))
+        outs = [torch.empty(words, dtype=torch.float64, device="cuda") for _ in range(nq)] if outs is None \
+            else list(outs)
+        if len(outs) != nq:
+            raise ValueError("one prepared buffer per query")
+        ws = self.prepare_batch_workspace(nq, baby_step) if ws is None else ws
+        qa = (_vp * nq)(*[ctypes.c_void_p(x.data_ptr()) for x in qs])
+        oa = (_vp * nq)(*[ctypes.c_void_p(x.data_ptr()) for x in outs])
+        _check(self.lib.fa_prepare_batch(self.h, qa, nq, baby_step, oa, _dev(ws), ws.numel() * 8, _stream(stream)))
+        return outs
 
     def score_prepared(self, q: torch.Tensor, prep: torch.Tensor, blocks, d: int, baby_step: int,
                        out: torch.Tensor | None = None, ws: torch.Tensor | None = None, stream=None) -> torch.Tensor:

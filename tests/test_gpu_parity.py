@@ -379,6 +379,55 @@ def test_batch_scores_match_oracle_and_single(name, d, B, nq, rows_list, oracle)
             assert np.max(np.abs(z[:len(X)] - X @ Q[j])) < 1e-4
 
 
+@pytest.mark.parametrize("name,B,nq", [("tiny", 4, 1), ("tiny", 16, 3), ("p1", 16, 5), ("p4", 16, 4)])
+def test_prepare_batch_matches_single(name, B, nq):
+    """fa_prepare_batch: every query's baby rotations equal fa_prepare_query's word for word
+    (launch groups of 16 // nq steps x nq queries, the last group short), and the batch
+    prepared at the small size scores to the oracle's BSGS block."""
+    import torch
+    p = pair(name, wid=17)
+    S = p.par.slots
+    d = 4 * B if name == "tiny" else 128
+    keys = p.keys(ckks.steps_for_bsgs(d, B), oracle=(name == "tiny"))
+    Q = gen.gaussian_unit_rows(gen.rng(17, gen.STREAM_QUERY, nq), nq, d)
+    cts = [p.encrypt_both(ckks.encode(ckks.replicate(Q[j], S), p.n, 40), tag=170 + j) for j in range(nq)]
+    say(f"[prepare_batch] {name} B={B} nq={nq}")
+    preps = p.ctx.prepare_batch([ct[0] for ct in cts], B)
+    torch.cuda.synchronize()
+    words = (B - 1) * p.ctx.ct_words  # the B-1 rotated ciphertexts (the buffer holds one spare word)
+    for j in range(nq):
+        single = p.ctx.prepare_query(cts[j][0], B)
+        assert torch.equal(preps[j][:words], single[:words]), j
+    if name == "tiny":
+        G = d // B
+        X = gen.gaussian_unit_rows(gen.rng(17, gen.STREAM_DB), 200, d)
+        c = ckks.layout_b_coeffs(X, p.par, d, B)
+        blk = p.ctx.encode_db_block_int(c)
+        pts = np.stack([ckks.to_residues(ci, p.par.q) for ci in c]).reshape(G, B, p.par.L, p.n)
+        for j in range(nq):
+            got = p.export_ct(p.ctx.score_prepared(cts[j][0], preps[j], [blk], d, B))[0]
+            ref = p.orc.bsgs_block(p.orc.baby_rotations(cts[j][1], B, keys), pts, B, G, keys)
+            assert np.array_equal(got, ref), j
+
+
+def test_prepare_batch_rejects_bad_arguments():
+    from paper_2608_21131_amd import fa
+    p = pair("tiny", wid=18)
+    S = p.par.slots
+    q = gen.gaussian_unit_rows(gen.rng(18, gen.STREAM_QUERY), 1, 16)[0]
+    ct, _ = p.encrypt_both(ckks.encode(ckks.replicate(q, S), p.n, 40), tag=18)
+    p.keys([1, 2, 3], oracle=False)
+    with pytest.raises(fa.FaError, match="FA_E_SHAPE"):
+        p.ctx.prepare_batch([], 4)                                         # no query
+    with pytest.raises(ValueError):
+        p.ctx.prepare_batch([ct, ct], 4, outs=[p.ctx.prepare_query(ct, 4)])  # one buffer missing
+    small = p.ctx.prepare_batch_workspace(2, 4)[:16]
+    with pytest.raises(fa.FaError, match="FA_E_NOMEM"):
+        p.ctx.prepare_batch([ct, ct], 4, ws=small)                         # workspace too small
+    with pytest.raises(fa.FaError, match="FA_E_NOKEY"):
+        p.ctx.prepare_batch([ct, ct], 8)                                   # no key for steps 4..7
+
+
 def test_batch_rejects_bad_arguments():
     from paper_2608_21131_amd import fa
     p = pair("tiny", wid=16)
