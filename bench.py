@@ -576,7 +576,7 @@ def run_tiny(bn, args):
         sc = np.concatenate([bn.decode(out, i, 80)[::w.d] for i in range(n_pts)])[:w.rows]
         err = float(np.max(np.abs(sc - X.astype(np.float64) @ qv)))
     return dict(ms=ms, scores=w.rows, phases={}, err=err, mac_bytes=None, stream_bytes=8 * n_pts * w.L * w.n,
-                cpu=None)
+                cpu=(lambda: cpu_baseline_rows(bn, X, qv, n_pts, steps)))
 
 
 def run_rank(bn, args):
@@ -614,8 +614,11 @@ def run_rank(bn, args):
         qR = W.T @ qv
         raw = bn.decode(out, 0, 120)[:w.rows]
         err = float(np.max(np.abs(raw / np.linalg.norm(qR) - Xr @ qR / np.linalg.norm(qR))))
+    n_fold = int(np.log2(w.d_in // w.d))
     return dict(ms=ms, scores=w.rows, phases={"projection_ms": pj, "scoring_ms": sc}, err=err, mac_bytes=None,
-                stream_bytes=8 * 2 * w.d * w.L * w.n, cpu=None)
+                stream_bytes=8 * 2 * w.d * w.L * w.n,
+                cpu=(lambda: cpu_baseline_diag(bn, Xr, W.T @ qv, n_blocks=2, n_scores=w.rows,
+                                               n_rot=2 * (w.B - 1) + n_fold)))
 
 
 def topk(sc, k):
@@ -766,8 +769,9 @@ def run_three_level(bn, args):
           "query_wall_ms": wall * 1e3}
     blocks_q = n_coarse + ex["fine_blocks"] + ex["rerank_blocks"]
     return dict(ms=gpu_q, scores=n_scores, phases=ph, err=max(errs) if errs else None, mac_bytes=None,
-                stream_bytes=8 * blocks_q * w.d * ctx.L * w.n, cpu=None, queries=nq, level=ctx.L,
-                coarse_group=gq)
+                stream_bytes=8 * blocks_q * w.d * ctx.L * w.n, queries=nq, level=ctx.L, coarse_group=gq,
+                cpu=(lambda: cpu_baseline_diag(bn, g_coarse, queries[0], L=ctx.L, n_blocks=blocks_q,
+                                               n_scores=n_scores)))
 
 
 def measured_traffic(path):
@@ -815,13 +819,46 @@ def oracle_at_level(bn, w, L):
     return par, orc, rand
 
 
-def cpu_baseline_diag(bn, X, qv, L=None, enc=False):
+def cpu_baseline_rows(bn, X, qv, n_pts, steps):
+    """The row layout on the oracle: time one plaintext product and two rotations of the same
+    parameters and extrapolate to n_pts products, each followed by `steps` rotate-and-sum steps."""
+    from oracle import ckks
+    w = bn.w
+    t_start = time.time()
+    par, orc, rand = oracle_at_level(bn, w, w.L)
+    keys = {r: orc.keygen(bn.s, r, *rand(r)) for r in (1, 2)}
+    ea, ee = bn.wl.enc_randomness(w, par.q)
+    ct = orc.encrypt(ckks.encode(ckks.replicate(qv, par.slots), par.n, 40), ea, ee, bn.s)
+    pt = ckks.to_residues(ckks.encode(ckks.pack_rows(X.astype(np.float64), par.slots, w.d)[0], par.n, 40), par.q)
+    t = time.time()
+    orc.mul_plain(ct, pt)
+    t_mul = time.time() - t
+    t = time.time()
+    orc.rotate(ct, 1, keys[1])
+    orc.rotate(ct, 2, keys[2])
+    t_rot = (time.time() - t) / 2
+    est = n_pts * (t_mul + steps * t_rot)
+    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    log(f"[bench] oracle sample (rows): mul {t_mul:.3f}s, rot {t_rot:.3f}s -> {est:.2f}s "
+        f"({time.time() - t_start:.1f}s wall)")
+    return {"value": round(w.rows / est, 2), "unit": "scores/s", "cores": cores, "kind": "oracle",
+            "sample": f"1 plaintext product + 2 rotations at {w.L} primes; extrapolated to {n_pts} products "
+                      f"x (1 + {steps} rotate-and-sum steps)",
+            "level_s_est": round(est, 3), "cpu_model": cpu_model()}
+
+
+def cpu_baseline_diag(bn, X, qv, L=None, enc=False, n_blocks=None, n_scores=None, n_rot=None):
     """Time the oracle on a sample of the same level and scale to scores/s.
 
     Sample: two rotations of the query, and the oracle's block product with
     G = 1 and G = 2 on the first B diagonals of block 0 (with enc, the diagonals
     encrypted and the ct x ct product with its relinearisations).  Level
-    estimate = (B-1) t_rot + n_blocks (t_G1 + (G-1)(t_G2 - t_G1)).
+    estimate = (B-1) t_rot + n_blocks (t_G1 + (G-1)(t_G2 - t_G1)).  n_blocks,
+    n_scores and n_rot (the rotations outside the block products, B-1 by default) override
+    the workload's: the three-level query has its baby rotations once, then the
+    blocks of all three levels; the rank reduction has two baby-step sets, the
+    projection's two fold rotations, and two block products (W's and the
+    candidates').
     """
     from oracle import ckks
     w = bn.w
@@ -861,14 +898,17 @@ def cpu_baseline_diag(bn, X, qv, L=None, enc=False):
     else:
         orc.bsgs_block(qrot, pts, B, 2, keys)
     t_g2 = time.time() - t
-    est = (B - 1) * t_rot + w.n_blocks * (t_g1 + (G - 1) * max(t_g2 - t_g1, 0.0))
+    nb = w.n_blocks if n_blocks is None else n_blocks
+    nr = B - 1 if n_rot is None else n_rot
+    est = nr * t_rot + nb * (t_g1 + (G - 1) * max(t_g2 - t_g1, 0.0))
     cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
     log(f"[bench] oracle sample at {L} primes{' (encrypted blocks)' if enc else ''}: rot {t_rot:.2f}s, "
-        f"G1 {t_g1:.2f}s, G2 {t_g2:.2f}s -> level {est:.1f}s ({time.time() - t_start:.1f}s wall)")
-    return {"value": round(w.rows / est, 2), "unit": "scores/s", "cores": cores, "kind": "oracle",
+        f"G1 {t_g1:.2f}s, G2 {t_g2:.2f}s -> {nb} blocks {est:.1f}s ({time.time() - t_start:.1f}s wall)")
+    return {"value": round((w.rows if n_scores is None else n_scores) / est, 2), "unit": "scores/s", "cores": cores,
+            "kind": "oracle",
             "sample": f"2 rotations + {'encrypted ' if enc else ''}block product with 1 and 2 giant groups "
-                      f"(B={B}) on block 0 of the same level at {L} primes; extrapolated to {B - 1} baby "
-                      f"rotations and {w.n_blocks} blocks x {G} groups",
+                      f"(B={B}) on block 0 at {L} primes; extrapolated to {nr} rotations and {nb} blocks x "
+                      f"{G} groups",
             "level_s_est": round(est, 2), "cpu_model": cpu_model()}
 
 
