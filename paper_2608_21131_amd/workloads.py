@@ -58,7 +58,7 @@ WORKLOADS = {
         desc="tiny scoring: 1,024 x 128-d N(0,1) unit rows, CKKS N=2^13, 3+1 primes, row layout, "
              "ct x pt then 7 rotate-and-sum steps"),
     "fine": Workload(
-        "fine", 15, 8, 2, rows=65_536, dim=96, d=128, B=16, wid=2, n_comp=1024,
+        "fine", 15, 8, 2, rows=65_536, dim=96, d=128, B=32, wid=2, n_comp=1024,
         desc="fine level: 65,536 x 96-d (zero-padded to 128) mixture rows, CKKS N=2^15, 8+2 primes, "
              "diagonal blocks"),
     "rank": Workload(
