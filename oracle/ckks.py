@@ -45,7 +45,9 @@ from dataclasses import dataclass, field
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "liboracle.so")
+# FA_ORACLE_LIB names another build of the same C core (the sanitizer test
+# loads one built with AddressSanitizer and UndefinedBehaviorSanitizer)
+LIB_PATH = os.environ.get("FA_ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
 
 PRIME_BITS = 50
 
