@@ -167,6 +167,15 @@ int fa_decrypt(fa_ctx* ctx, const void* ct, uint64_t* out, void* stream);
 /* Canonical form of n_polys consecutive [L][N] polynomials of a device
  * buffer (2 for a ciphertext, 1 for a plaintext): host out [n_polys][L][N]. */
 int fa_export_coeffs(fa_ctx* ctx, const void* buf, int n_polys, uint64_t* out, void* stream);
+/* The inverse of fa_export_coeffs: n_polys polynomials in canonical form
+ * (host [n_polys][L][N], limb t of every polynomial below prime t) into the
+ * device buffer buf in the library's private form.  Enrolled blocks can so
+ * be saved and loaded again without re-encoding them (the paper keeps its
+ * encrypted database on disk and reloads it warm, section 2 "Measured
+ * prototype vs. deployment").  Allocates a staging buffer; synchronous on
+ * the stream.  Errors: FA_E_INVAL (null pointer, n_polys < 1, a residue not
+ * below its prime), FA_E_NOMEM, FA_E_HIP. */
+int fa_import_coeffs(fa_ctx* ctx, const uint64_t* coeffs, int n_polys, void* buf, void* stream);
 /* Encode a real slot vector (host, n_slots <= S values, rest zero) to integer
  * coefficients m_k = rint(2^log_scale * (2/N) * sum_j v_j cos(pi k 5^j / N))
  * (round half to even, float64): host out [N]. */

@@ -743,6 +743,42 @@ int fa_decrypt(fa_ctx* c, const void* ct, uint64_t* out, void* stream) {
   return export_polys(c, (const double*)ct, 1, out, (hipStream_t)stream, true);
 }
 
+int fa_import_coeffs(fa_ctx* c, const uint64_t* coeffs, int n_polys, void* buf, void* stream) {
+  if (!c || !coeffs || !buf || n_polys < 1) return fail(FA_E_INVAL, "fa_import_coeffs: bad argument");
+  const size_t n = c->n, L = c->L;
+  for (size_t p = 0; p < (size_t)n_polys; ++p)
+    for (size_t t = 0; t < L; ++t) {
+      const uint64_t* r = coeffs + (p * L + t) * n;
+      for (size_t k = 0; k < n; ++k)
+        if (r[k] >= c->primes[t])
+          return fail(FA_E_INVAL, "fa_import_coeffs: residue %zu of polynomial %zu, limb %zu is not below its prime",
+                      k, p, t);
+    }
+  hipStream_t s = (hipStream_t)stream;
+  const int chunk = 16;  // polynomials staged per copy
+  uint64_t* du = nullptr;
+  int rc = dev_alloc(&du, (size_t)std::min(chunk, n_polys) * L * n);
+  if (rc) return rc;
+  double* dst = (double*)buf;
+  for (int p0 = 0; p0 < n_polys && !rc; p0 += chunk) {
+    const int m = std::min(chunk, n_polys - p0);
+    const size_t words = (size_t)m * L * n;
+    hipError_t he = hipMemcpyAsync(du, coeffs + (size_t)p0 * L * n, words * 8, hipMemcpyHostToDevice, s);
+    if (he != hipSuccess) {
+      rc = fail(FA_E_HIP, "fa_import_coeffs: %s", hipGetErrorString(he));
+      break;
+    }
+    double* d = dst + (size_t)p0 * L * n;
+    fa::u64_to_res(du, words, d, s);
+    fa::ntt_fwd_strided(c, d, n, m * (int)L, (int)L, 0, s);
+    rc = check_launch("fa_import_coeffs");
+    he = hipStreamSynchronize(s);  // the staging buffer is reused by the next chunk
+    if (!rc && he != hipSuccess) rc = fail(FA_E_HIP, "fa_import_coeffs: %s", hipGetErrorString(he));
+  }
+  (void)hipFree(du);
+  return rc;
+}
+
 int fa_export_coeffs(fa_ctx* c, const void* buf, int n_polys, uint64_t* out, void* stream) {
   if (!c || !buf || !out || n_polys < 1) return fail(FA_E_INVAL, "fa_export_coeffs: bad argument");
   return export_polys(c, (const double*)buf, n_polys, out, (hipStream_t)stream, false);

@@ -60,6 +60,7 @@ SIGNATURES = {
     "fa_encrypt": (ctypes.c_int, [_vp, _i64p, _u64p, _i64p, _vp, _vp]),
     "fa_decrypt": (ctypes.c_int, [_vp, _vp, _u64p, _vp]),
     "fa_export_coeffs": (ctypes.c_int, [_vp, _vp, ctypes.c_int, _u64p, _vp]),
+    "fa_import_coeffs": (ctypes.c_int, [_vp, _u64p, ctypes.c_int, _vp, _vp]),
     "fa_encode": (ctypes.c_int, [_vp, _f64p, ctypes.c_int, ctypes.c_int, _i64p]),
     "fa_decode": (ctypes.c_int, [_vp, _u64p, ctypes.c_int, _f64p, ctypes.c_int]),
     "fa_encode_db_block": (ctypes.c_int, [_vp, _f32p, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
@@ -274,6 +275,38 @@ class Context:
         out = np.empty((n_polys, self.L, self.n), dtype=np.uint64)
         _check(self.lib.fa_export_coeffs(self.h, _dev(buf), n_polys, _ptr(out, _u64p), _stream(stream)))
         return out
+
+    def import_coeffs(self, coeffs, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+        """The inverse of export: canonical [n_polys][L][N] residues into a device buffer."""
+        c = _np(coeffs, np.uint64)
+        if c.ndim != 3 or c.shape[1:] != (self.L, self.n):
+            raise ValueError(f"coefficients must be [n_polys][{self.L}][{self.n}]")
+        out = torch.empty(c.size, dtype=torch.float64, device="cuda") if out is None else out
+        _check(self.lib.fa_import_coeffs(self.h, _ptr(c, _u64p), c.shape[0], _dev(out), _stream(stream)))
+        return out
+
+    def save_buffers(self, path: str, buffers: dict) -> None:
+        """Save device buffers {name: (tensor, n_polys)} (enrolled blocks, ciphertexts) in canonical
+        coefficient form with a header naming this context's ring, primes and each buffer's size."""
+        import json
+        header = {"format": "fa-coeffs-1", "log_n": self.log_n, "L": self.L, "K": self.K,
+                  "primes": [int(p) for p in self.primes], "buffers": {k: int(v[1]) for k, v in buffers.items()}}
+        arrays = {"header": np.frombuffer(json.dumps(header).encode(), dtype=np.uint8)}
+        for name, (buf, n_polys) in buffers.items():
+            arrays["buf_" + name] = self.export(buf, n_polys)
+        np.savez(path, **arrays)
+
+    def load_buffers(self, path: str) -> dict:
+        """Load what save_buffers wrote into new device buffers {name: tensor}; the file must come
+        from a context with the same ring degree and primes."""
+        import json
+        with np.load(path, allow_pickle=False) as z:
+            header = json.loads(bytes(z["header"]).decode())
+            mine = {"log_n": self.log_n, "L": self.L, "K": self.K, "primes": [int(p) for p in self.primes]}
+            if header.get("format") != "fa-coeffs-1" or any(header.get(k) != v for k, v in mine.items()):
+                raise ValueError(f"{path}: saved for another context ({header.get('log_n')}, {header.get('L')}, "
+                                 f"{header.get('K')})")
+            return {name: self.import_coeffs(z["buf_" + name]) for name in header["buffers"]}
 
     def encode(self, slots, log_scale: int | None = None) -> np.ndarray:
         v = _np(slots, np.float64)

@@ -190,6 +190,34 @@ def test_decode_matches_oracle_decode(name, extra):
     assert short.shape == (37,) and np.array_equal(short, got[:37])
 
 
+def test_save_and_load_enrolled_blocks(tmp_path):
+    """save_buffers / load_buffers (fa_export_coeffs, then fa_import_coeffs): an enrolled block
+    and a ciphertext come back word for word and score identically; a file saved for another
+    ring is refused, and so is a residue that is not below its prime."""
+    import torch
+    from paper_2608_21131_amd import fa
+    p = pair("p1", wid=19)
+    S, d, B = p.par.slots, 128, 16
+    p.keys(ckks.steps_for_bsgs(d, B), oracle=False)
+    X = gen.gaussian_unit_rows(gen.rng(19, gen.STREAM_DB), 1000, d)
+    q = gen.gaussian_unit_rows(gen.rng(19, gen.STREAM_QUERY), 1, d)[0]
+    ct, _ = p.encrypt_both(ckks.encode(ckks.replicate(q, S), p.n, 40), tag=19)
+    blk = p.ctx.encode_db_block(X.astype(np.float32), d, 1, B)
+    path = str(tmp_path / "enrolled.npz")
+    say("[save/load] p1")
+    p.ctx.save_buffers(path, {"block": (blk, d), "query": (ct, 2)})
+    got = p.ctx.load_buffers(path)
+    assert torch.equal(got["block"], blk) and torch.equal(got["query"], ct)
+    ref = p.export_ct(p.ctx.score_block(ct, [blk], d, 1, B))
+    assert np.array_equal(p.export_ct(p.ctx.score_block(got["query"], [got["block"]], d, 1, B)), ref)
+    with pytest.raises(ValueError):
+        pair("tiny").ctx.load_buffers(path)
+    bad = p.ctx.export(blk, 1)
+    bad[0, 1, 5] = p.par.q[1]
+    with pytest.raises(fa.FaError, match="FA_E_INVAL"):
+        p.ctx.import_coeffs(bad)
+
+
 @pytest.mark.parametrize("name", ["tiny", "p4"])
 def test_float_encode_matches_oracle(name):
     p = pair(name)
