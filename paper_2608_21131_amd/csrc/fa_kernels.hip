@@ -1629,6 +1629,15 @@ void giant_ks(const fa_ctx* c, const double* ext, const double* acc, size_t astr
 // query: 32 (default), 16 or 8; FA_MAC_PAIRS overrides it for tuning.  With
 // NQ queries per pass the pairs per pass drop to 32 / NQ.
 // the three-stage single-query kernel (FA_MAC_STAGES=2 selects the two-slot one)
+// 17..31 pairs left: one padded 32-pair launch (FA_MAC_PAD=0: 16 + 16 / 8)
+static bool mac_pad_wide() {
+  static int v = -1;
+  if (v < 0) {
+    const char* e = getenv("FA_MAC_PAD");
+    v = e ? atoi(e) : 1;
+  }
+  return v != 0;
+}
 static bool mac_three_stages() {
   static int v = -1;
   if (v < 0) {
@@ -1661,7 +1670,7 @@ static void launch_mac(MacArgs a, int nchunk, const fa_ctx* c, hipStream_t s) {
   a.ntile = (int)((size_t)c->L * c->n / 256);
   a.nchunk = nchunk;
   const unsigned grid = nchunk == 1 ? (unsigned)a.ntile : 8u * nchunk * ((a.ntile + 7) / 8);
-  if constexpr (NQ == 1 && NACC == 32) {
+  if constexpr (NQ == 1) {
     if (mac_three_stages())
       hipLaunchKernelGGL((k_mac_diag3<NACC>), dim3(grid), dim3(256), 0, s, a, c->d_pr, c->logn);
     else
@@ -1682,6 +1691,12 @@ static int mac_chunks(MacArgs& a, int p0, const fa_ctx* c, hipStream_t s) {
   if (left >= WIDE) {
     launch_mac<NQ, WIDE>(a, left / WIDE, c, s);
     return p0 + (left / WIDE) * WIDE;
+  }
+  if (NQ == 1 && WIDE == 32 && left > 16 && mac_pad_wide()) {
+    // one padded launch: the missing pairs re-read the last pair's rows (cache
+    // hits) instead of a second launch re-reading every rotated query
+    launch_mac<NQ, WIDE>(a, 1, c, s);
+    return p0 + WIDE;
   }
   if (WIDE > 16 && left > 8) {
     launch_mac<NQ, (WIDE > 16 ? 16 : WIDE)>(a, 1, c, s);
