@@ -14,7 +14,10 @@
 //     0.375c, so |result| <= (0.5 + 0.375c) q; exact for |a| <= 8q.
 //   mul(a, b):        |a|, |b| <= q  ->  |result| <= 0.75 q.
 //   reduce(x):        |x| < 2^52    ->  |result| <= q/2 (+ rounding slack).
-// Forward NTT values stay within 1.6 q, inverse NTT values within 2 q.
+// Forward NTT values stay within 5.82 q (stages alternate lazy and reduced
+// butterflies, see ct_bfly), inverse NTT values within 2 q; every transform
+// output that leaves a kernel is either canonicalised or feeds a mulc / mul
+// whose operand stays within 8 q.
 
 #include <hip/hip_runtime.h>
 
@@ -60,9 +63,16 @@ __device__ __forceinline__ uint32_t perm(uint32_t i, uint32_t gal, int logn) {
   return __brev((e2 - 1u) >> 1) >> (32 - logn);
 }
 
-// Cooley-Tukey butterfly (forward): (x, y) -> (x + w y, x - w y)
+// Cooley-Tukey butterfly (forward): (x, y) -> (x + w y, x - w y).  With R
+// false x is not reduced first: the passes below reduce on odd stages only.
+// With c the bound (in units of q) of the stage's inputs, a reduced stage
+// leaves 1 + 0.375c and a lazy one 1.375c + 0.5; alternating from c <= 1 the
+// bound settles at 2.45 after reduced and 3.87 after lazy stages, and two lazy
+// stages in a row (an odd first pass meeting the next pass's stage 0) reach
+// 5.82: always inside the 8q of mulc's exactness and below 2^53.
+template <bool R = true>
 __device__ __forceinline__ void ct_bfly(double& x, double& y, double w, double q, double qinv) {
-  const double u = reduce(x, q, qinv);
+  const double u = R ? reduce(x, q, qinv) : x;
   const double t = mulc(y, w, w * qinv, q);
   x = u + t;
   y = u - t;
@@ -134,7 +144,8 @@ __device__ __forceinline__ void fwd_a_body(const Ld& ld, double* a, const double
 #pragma unroll
       for (int m = 0; m < P::E1; ++m) {
         if (m & half) continue;
-        ct_bfly(x[m], x[m + half], w[(1 << s) + (m >> (P::S1 - s))], q, qinv);
+        if (s & 1) ct_bfly<true>(x[m], x[m + half], w[(1 << s) + (m >> (P::S1 - s))], q, qinv);
+        else ct_bfly<false>(x[m], x[m + half], w[(1 << s) + (m >> (P::S1 - s))], q, qinv);
       }
     }
 #pragma unroll
@@ -152,7 +163,8 @@ __device__ __forceinline__ void fwd_a_body(const Ld& ld, double* a, const double
 #pragma unroll
       for (int m = 0; m < P::E2; ++m) {
         if (m & half) continue;
-        ct_bfly(x[m], x[m + half], w[(1 << s) + (hh << s2) + (m >> (P::S2 - s2))], q, qinv);
+        if (s & 1) ct_bfly<true>(x[m], x[m + half], w[(1 << s) + (hh << s2) + (m >> (P::S2 - s2))], q, qinv);
+        else ct_bfly<false>(x[m], x[m + half], w[(1 << s) + (hh << s2) + (m >> (P::S2 - s2))], q, qinv);
       }
     }
 #pragma unroll
@@ -334,7 +346,8 @@ __device__ __forceinline__ void fwd_b_lds(const double* __restrict__ a, int row0
 #pragma unroll
       for (int m = 0; m < 16; ++m) {
         if (m & half) continue;
-        ct_bfly(x[m], x[m + half], twb(T, f, s1, m >> (4 - s1), q, qinv), q, qinv);
+        if (s1 & 1) ct_bfly<true>(x[m], x[m + half], twb(T, f, s1, m >> (4 - s1), q, qinv), q, qinv);
+        else ct_bfly<false>(x[m], x[m + half], twb(T, f, s1, m >> (4 - s1), q, qinv), q, qinv);
       }
     }
 #pragma unroll
@@ -353,7 +366,9 @@ __device__ __forceinline__ void fwd_b_lds(const double* __restrict__ a, int row0
 #pragma unroll
       for (int m = 0; m < 16; ++m) {
         if (m & half) continue;
-        ct_bfly(x[m], x[m + half], twb(T, f, s1, (lh << (s1 - 4)) + (m >> (8 - s1)), q, qinv), q, qinv);
+        const double w = twb(T, f, s1, (lh << (s1 - 4)) + (m >> (8 - s1)), q, qinv);
+        if (s1 & 1) ct_bfly<true>(x[m], x[m + half], w, q, qinv);
+        else ct_bfly<false>(x[m], x[m + half], w, q, qinv);
       }
     }
     // back to LDS: each thread rewrites the words it read
