@@ -60,6 +60,9 @@ def parse():
                     help="rerank: also time the encrypted-database variant (ct x ct, database diagonals encrypted "
                          "and enrolled at this many primes, lazy relinearisation) and report it under enc_db "
                          "(0: skip; 12: all primes)")
+    ap.add_argument("--enc-w", type=int, default=1,
+                    help="rank: also time the projection with W's diagonals encrypted and report it under "
+                         "enc_projection (0: skip)")
     ap.add_argument("--membership", type=int, default=1,
                     help="rerank: also time the face membership scan (222,049 centroids, encrypted threshold) "
                          "and report it under membership (0: skip)")
@@ -615,10 +618,37 @@ def run_rank(bn, args):
         raw = bn.decode(out, 0, 120)[:w.rows]
         err = float(np.max(np.abs(raw / np.linalg.norm(qR) - Xr @ qR / np.linalg.norm(qR))))
     n_fold = int(np.log2(w.d_in // w.d))
+    enc_proj = run_enc_projection(bn, args, wpts, q, W.T @ qv) if args.enc_w else None
     return dict(ms=ms, scores=w.rows, phases={"projection_ms": pj, "scoring_ms": sc}, err=err, mac_bytes=None,
+                enc_projection=enc_proj,
                 stream_bytes=8 * 2 * w.d * w.L * w.n,
                 cpu=(lambda: cpu_baseline_diag(bn, Xr, W.T @ qv, n_blocks=2, n_scores=w.rows,
                                                n_rot=2 * (w.B - 1) + n_fold)))
+
+
+def run_enc_projection(bn, args, wpts, q, qR):
+    """The projection with W's R diagonals encrypted (the paper keeps the projection encrypted on
+    the server): R ciphertexts, scored ct x ct with one relinearisation per giant step, then the
+    fold.  Timed on its own, after the plaintext-projection step."""
+    w, ctx, fa, torch = bn.w, bn.ctx, bn.fa, bn.torch
+    a, e = bn.wl.db_enc_randomness(w, ctx.primes[:w.L], 0, w.d, block=99)
+    w_cts = ctx.encrypt_pts(wpts, w.d, a, e)
+    del a, e
+    out = ctx.new_ct()
+    ws = ctx.workspace(fa.OP_PROJECT_ENC, 1, w.d, w.B_proj)
+    ms = bn.timed(lambda: ctx.project_ct_enc(q, w_cts, w.d_in, w.d, w.B_proj, out=out, ws=ws), args.steps,
+                  args.warmup)
+    err = None
+    if not args.no_check:
+        z = bn.decode(out, 0, 80)
+        err = float(np.max(np.abs(z - np.tile(qR, w.slots // w.d))))
+    res = {"ms_per_projection": round(ms, 4), "max_abs_err_vs_WTq": err,
+           "encrypted_diagonals_bytes": 8 * w.d * 2 * w.L * w.n,
+           "note": f"Enc(W^T q) with the {w.d} hybrid diagonals of W encrypted ({w.d_in}->{w.d}, baby step "
+                   f"{w.B_proj}), ct x ct, one relinearisation per giant step, then the fold"}
+    del w_cts
+    torch.cuda.empty_cache()
+    return res
 
 
 def topk(sc, k):
@@ -987,6 +1017,8 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
+    if r.get("enc_projection"):
+        res["enc_projection"] = r["enc_projection"]
     if w.name == "three_level":
         res["metric"] = ("server GPU time per query (3 levels) + aggregate server scores/s, 32 encrypted queries "
                          "back-to-back, one MI355X")

@@ -80,7 +80,8 @@ enum {
   FA_OP_ROTATE = 3,
   FA_OP_PREPARE = 4,
   FA_OP_SCORE_PREPARED = 5,
-  FA_OP_SCORE_ENC = 6
+  FA_OP_SCORE_ENC = 6,
+  FA_OP_PROJECT_ENC = 7
 };
 
 typedef struct fa_ctx fa_ctx;
@@ -213,7 +214,8 @@ int fa_encode_db_block_int(fa_ctx* ctx, const int64_t* coeffs, int n_pts, void* 
 /* Device workspace needed by an operation (bytes).  op = FA_OP_SCORE with
  * layout FA_LAYOUT_DIAG (FA_OP_SCORE_ENC with FA_LAYOUT_DIAG_ENC): n_blocks,
  * d, baby_step as passed to fa_score_block;
- * FA_OP_PROJECT: n_blocks = 1, d = r; FA_OP_ROTATE_SUM / FA_OP_ROTATE: n_blocks
+ * FA_OP_PROJECT (FA_OP_PROJECT_ENC for fa_project_ct_enc): n_blocks = 1,
+ * d = r; FA_OP_ROTATE_SUM / FA_OP_ROTATE: n_blocks
  * = number of ciphertexts. */
 size_t fa_workspace_bytes(const fa_ctx* ctx, int op, int n_blocks, int d, int baby_step);
 
@@ -297,6 +299,18 @@ int fa_score_batch(fa_ctx* ctx, const void* const* qs, const void* const* preps,
  * g*B, and r*2^k. */
 int fa_project_ct(fa_ctx* ctx, const void* q, const void* w_pts, int d_in, int r, int baby_step, void* q_r,
                   void* ws, size_t ws_bytes, void* stream);
+
+/* The projection with W itself encrypted (Section 3.1: the server holds the
+ * projection's diagonals as ciphertexts).  w_cts holds r ciphertexts
+ * ([r][2][L][N], fa_encrypt_pts of the plaintexts fa_project_ct takes);
+ * each giant step's three-component tensor sum is relinearised once, as for
+ * FA_LAYOUT_DIAG_ENC blocks, before the same giant steps and fold.  Output
+ * slot s = (W^T q)[s mod r] at the product of the two scales.  Needs the keys
+ * fa_project_ct needs and the relinearisation key (FA_E_NOKEY otherwise).
+ * Workspace: fa_workspace_bytes(FA_OP_PROJECT_ENC, 1, r, baby_step).  Other
+ * errors as fa_project_ct. */
+int fa_project_ct_enc(fa_ctx* ctx, const void* q, const void* w_cts, int d_in, int r, int baby_step, void* q_r,
+                      void* ws, size_t ws_bytes, void* stream);
 
 /* In place, for each of n_cts consecutive ciphertexts in cts:
  * ct <- ct + Rotate(ct, first_shift * 2^k) for k = 0..n_steps-1. */

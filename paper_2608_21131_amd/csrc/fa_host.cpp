@@ -1584,6 +1584,9 @@ size_t fa_workspace_bytes(const fa_ctx* c, int op, int n_blocks, int d, int baby
     case FA_OP_SCORE_ENC:
       if (baby_step < 1 || d < baby_step) return 0;
       return score_enc_ws(c, std::max(1, n_blocks), d, baby_step);
+    case FA_OP_PROJECT_ENC:
+      if (baby_step < 1 || d < baby_step) return 0;
+      return std::max(score_enc_ws(c, 1, d, baby_step), rotate_ws(c, 1));
     default:
       return 0;
   }
@@ -2273,13 +2276,17 @@ int fa_profile_read(fa_ctx* c, double* ms) {
   return FA_OK;
 }
 
-int fa_project_ct(fa_ctx* c, const void* q, const void* w_pts, int d_in, int r, int baby_step, void* q_r, void* ws,
-                  size_t ws_bytes, void* stream) {
-  if (!c || !q || !w_pts || !q_r) return fail(FA_E_INVAL, "fa_project_ct: null argument");
+// The projection q_R = W^T q: the diagonal product of q with the r hybrid
+// diagonals of W (plaintexts, or ciphertexts when enc), then the fold
+// z += Rotate(z, r * 2^k) while r * 2^k < d_in.
+static int project(fa_ctx* c, const void* q, const void* w, bool enc, int d_in, int r, int baby_step, void* q_r,
+                   void* ws, size_t ws_bytes, void* stream) {
+  const char* fn = enc ? "fa_project_ct_enc" : "fa_project_ct";
+  if (!c || !q || !w || !q_r) return fail(FA_E_INVAL, "%s: null argument", fn);
   if (r < 1 || (r & (r - 1)) || d_in < r || d_in % r || ((d_in / r) & (d_in / r - 1)) || d_in > c->n / 2)
     return fail(FA_E_SHAPE, "d_in=%d, r=%d: both powers of two with r <= d_in <= N/2", d_in, r);
   if (baby_step < 1 || r % baby_step) return fail(FA_E_INVAL, "baby_step %d must divide r=%d", baby_step, r);
-  const size_t need = fa_workspace_bytes(c, FA_OP_PROJECT, 1, r, baby_step);
+  const size_t need = fa_workspace_bytes(c, enc ? FA_OP_PROJECT_ENC : FA_OP_PROJECT, 1, r, baby_step);
   if (!ws || ws_bytes < need) return fail(FA_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
   int steps = 0;
   while ((r << steps) < d_in) ++steps;
@@ -2287,8 +2294,9 @@ int fa_project_ct(fa_ctx* c, const void* q, const void* w_pts, int d_in, int r, 
     if (!c->keys.count(r << k)) return fail(FA_E_NOKEY, "no rotation key for fold step %d", r << k);
   hipStream_t s = (hipStream_t)stream;
   Arena ar{(char*)ws, ws_bytes, 0};
-  const void* blocks[1] = {w_pts};
-  int rc = score_diag(c, (const double*)q, (const double* const*)blocks, 1, r, baby_step, (double*)q_r, ar, s);
+  const void* blocks[1] = {w};
+  int rc = enc ? score_diag_enc(c, (const double*)q, (const double* const*)blocks, 1, r, baby_step, (double*)q_r, ar, s)
+               : score_diag(c, (const double*)q, (const double* const*)blocks, 1, r, baby_step, (double*)q_r, ar, s);
   if (rc) return rc;
   for (int k = 0; k < steps; ++k) {
     Arena ar2{(char*)ws, ws_bytes, 0};
@@ -2297,7 +2305,17 @@ int fa_project_ct(fa_ctx* c, const void* q, const void* w_pts, int d_in, int r, 
     if (rc) return rc;
     fa::add_automorph(c, (double*)q_r, tmp, 2, 1u, s);
   }
-  return check_launch("fa_project_ct");
+  return check_launch(fn);
+}
+
+int fa_project_ct(fa_ctx* c, const void* q, const void* w_pts, int d_in, int r, int baby_step, void* q_r, void* ws,
+                  size_t ws_bytes, void* stream) {
+  return project(c, q, w_pts, false, d_in, r, baby_step, q_r, ws, ws_bytes, stream);
+}
+
+int fa_project_ct_enc(fa_ctx* c, const void* q, const void* w_cts, int d_in, int r, int baby_step, void* q_r,
+                      void* ws, size_t ws_bytes, void* stream) {
+  return project(c, q, w_cts, true, d_in, r, baby_step, q_r, ws, ws_bytes, stream);
 }
 
 }  // extern "C"

@@ -19,7 +19,8 @@ LIB_PATH = os.path.join(_HERE, "libfa.so")
 
 FA_OK, FA_E_INVAL, FA_E_SHAPE, FA_E_NOKEY, FA_E_NOMEM, FA_E_HIP = 0, -1, -2, -3, -4, -5
 LAYOUT_ROW, LAYOUT_DIAG, LAYOUT_DIAG_ENC = 0, 1, 2
-OP_SCORE, OP_PROJECT, OP_ROTATE_SUM, OP_ROTATE, OP_PREPARE, OP_SCORE_PREPARED, OP_SCORE_ENC = 0, 1, 2, 3, 4, 5, 6
+(OP_SCORE, OP_PROJECT, OP_ROTATE_SUM, OP_ROTATE, OP_PREPARE, OP_SCORE_PREPARED, OP_SCORE_ENC,
+ OP_PROJECT_ENC) = 0, 1, 2, 3, 4, 5, 6, 7
 
 _ERR_NAMES = {FA_E_INVAL: "FA_E_INVAL", FA_E_SHAPE: "FA_E_SHAPE", FA_E_NOKEY: "FA_E_NOKEY",
               FA_E_NOMEM: "FA_E_NOMEM", FA_E_HIP: "FA_E_HIP"}
@@ -72,6 +73,8 @@ SIGNATURES = {
                                       ctypes.c_int, _vp, _vp, ctypes.c_size_t, _vp]),
     "fa_project_ct": (ctypes.c_int, [_vp, _vp, _vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, _vp, _vp,
                                      ctypes.c_size_t, _vp]),
+    "fa_project_ct_enc": (ctypes.c_int, [_vp, _vp, _vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, _vp, _vp,
+                                         ctypes.c_size_t, _vp]),
     "fa_rotate_sum": (ctypes.c_int, [_vp, _vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, _vp, ctypes.c_size_t,
                                      _vp]),
     "fa_rotate": (ctypes.c_int, [_vp, _vp, ctypes.c_int, _vp, _vp, ctypes.c_size_t, _vp]),
@@ -465,6 +468,15 @@ class Context:
         ws = self.workspace(OP_PROJECT, 1, r, baby_step) if ws is None else ws
         _check(self.lib.fa_project_ct(self.h, _dev(q), _dev(w_pts), d_in, r, baby_step, _dev(out), _dev(ws),
                                       ws.numel() * 8, _stream(stream)))
+        return out
+
+    def project_ct_enc(self, q: torch.Tensor, w_cts: torch.Tensor, d_in: int, r: int, baby_step: int,
+                       out: torch.Tensor | None = None, ws: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+        """The projection with W's r diagonals encrypted (fa_encrypt_pts of project_ct's plaintexts)."""
+        out = self.new_ct() if out is None else out
+        ws = self.workspace(OP_PROJECT_ENC, 1, r, baby_step) if ws is None else ws
+        _check(self.lib.fa_project_ct_enc(self.h, _dev(q), _dev(w_cts), d_in, r, baby_step, _dev(out), _dev(ws),
+                                          ws.numel() * 8, _stream(stream)))
         return out
 
     def rotate_sum(self, cts: torch.Tensor, n_cts: int, first_shift: int, n_steps: int,

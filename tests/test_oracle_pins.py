@@ -670,6 +670,36 @@ def test_encrypted_block_scores_match_float64(small, B):
     assert np.max(np.abs(z[rows:])) < 1e-4
 
 
+def test_encrypted_projection_matches_float64(small4):
+    """W's pre-rotated hybrid diagonals encrypted: the ct x ct diagonal product (one
+    relinearisation per giant index) and the fold decrypt to W^T q, periodic in R, and the
+    projected query then scores projected rows to their float64 inner products."""
+    par, orc = small4
+    d_in, R, B, rows = 64, 16, 4, 100
+    G, c = R // B, d_in // R
+    s = gen.ternary_secret(gen.rng(35, gen.STREAM_SECRET), par.n)
+    W = gen.projection_matrix(gen.rng(35, gen.STREAM_W), d_in, R, var=1.0 / R)
+    q = gen.gaussian_unit_rows(gen.rng(35, gen.STREAM_QUERY), 1, d_in)[0]
+    ct = enc(orc, ckks.replicate(q, par.slots), s, wid=35)
+    steps = sorted(set(ckks.steps_for_bsgs(R, B) + [R << k for k in range(int(np.log2(c)))]))
+    keys = keyset(orc, s, steps, wid=35)
+    rlk, _ = relin_key(orc, s, 35)
+    pre = ckks.prerotate(ckks.projection_diagonals(W, par.slots), B)
+    wct = np.empty((G, B, 2, par.L, par.n), dtype=np.uint64)
+    for g in range(G):
+        for b in range(B):
+            a = gen.uniform_residues(gen.rng(35, gen.STREAM_ENC_A, 1 + g * B + b), par.q, 1, par.n)[0]
+            e = gen.rounded_gaussian(gen.rng(35, gen.STREAM_ENC_E, 1 + g * B + b), par.n)
+            wct[g, b] = orc.encrypt(ckks.encode(pre[g, b], par.n, 40), a, e, s)
+    z = orc.bsgs_block_ct(orc.baby_rotations(ct, B, keys), wct, B, G, keys, rlk)
+    z = orc.rotate_sum(z, R, int(np.log2(c)), keys)
+    qR = W.T @ q
+    assert np.max(np.abs(dec(orc, z, s, 80) - np.tile(qR, par.slots // R))) < 1e-4
+    Xr = gen.normalize_rows(gen.gaussian_unit_rows(gen.rng(35, gen.STREAM_DB), rows, d_in) @ W)
+    out = orc.bsgs_block(orc.baby_rotations(z, B, keys), ckks.layout_b_pts(Xr, par, R, B), B, G, keys)
+    assert np.max(np.abs(dec(orc, out, s, 120)[:rows] - Xr @ qR)) < 1e-4
+
+
 # ----------------------------------------------------------------------------
 # membership path: rescale, Chebyshev direct evaluator, sign iteration
 # ----------------------------------------------------------------------------
