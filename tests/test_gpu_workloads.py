@@ -171,6 +171,14 @@ def test_rank_reduction_fullsize():
     raw = st.decode(out, 0, 120)[:w.rows]
     cos = raw / np.linalg.norm(qR)
     assert np.max(np.abs(cos - Xr @ qR / np.linalg.norm(qR))) < 1e-4
+    # W's diagonals encrypted (as bench.py times it): the projection decrypts to W^T q
+    say("[rank] projection with W encrypted")
+    ra, re_ = wl.relin_randomness(w, st.par.primes, st.par.dnum)
+    st.ctx.keygen_relin(st.s, ra, re_)
+    a, e = wl.db_enc_randomness(w, st.par.q, 0, R, block=99)
+    wct = st.ctx.encrypt_pts(wpts, R, a, e)
+    qr_e = st.ctx.project_ct_enc(ct, wct, w.d_in, R, Bp)
+    assert np.max(np.abs(st.decode(qr_e, 0, 80) - np.tile(qR, S // R))) < 1e-4
 
 
 def test_rerank_level_at_three_primes_fullsize():
