@@ -1527,13 +1527,13 @@ static unsigned ks_grid(int nx, int ny, int nq, int ngroup) {
 
 template <int DNUM>
 static void launch_moddown_ks(const fa_ctx* c, const MdKsArgs& a, int m, int nq, hipStream_t s) {
-  const int rows = (c->n >> 8) < 16 ? (c->n >> 8) : 16;
+  // eight 256-word rows per workgroup (four on a ring of 2^10, the smallest
+  // accepted): twice the workgroups of sixteen-row tiles, measured faster at
+  // 8 and 12 primes and even at 3
+  const int rows = (c->n >> 8) < 8 ? (c->n >> 8) : 8;
   const int ngroup = m / nq;
   dim3 gb(ks_grid((c->n >> 8) / rows, c->L, nq, ngroup));
-  if (rows == 16)
-    hipLaunchKernelGGL((k_moddown_ks_b<DNUM, 16>), gb, dim3(256), 0, s, a, c->d_pr, c->d_twt_fwd, c->d_twr_fwd,
-                       c->logn, c->L, c->np, c->alpha, nq, ngroup);
-  else if (rows == 8)
+  if (rows == 8)
     hipLaunchKernelGGL((k_moddown_ks_b<DNUM, 8>), gb, dim3(256), 0, s, a, c->d_pr, c->d_twt_fwd, c->d_twr_fwd,
                        c->logn, c->L, c->np, c->alpha, nq, ngroup);
   else
