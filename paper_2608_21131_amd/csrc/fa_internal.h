@@ -23,8 +23,11 @@ struct DevPrime {
   double pmod;   // P mod q     (ciphertext primes only; 0 for special primes)
 };
 
-// Up to FA_MAXL limbs (polynomials over one prime) processed by one launch.
-#define FA_MAXL 64
+// Up to FA_MAXL limbs (polynomials over one prime) processed by one launch:
+// 128 covers one batch of 16 rotations' special-prime products (96 limbs) or
+// one block's giant accumulators at 12 primes in a single launch, and keeps
+// the list (passed by value) inside the 4 KiB of kernel arguments.
+#define FA_MAXL 128
 // Each limb is transformed from src[i] into ptr[i] (src[i] == ptr[i]: in place);
 // the inverse transform ends with a multiply by scale[i] (N^-1, possibly times a
 // basis-conversion constant).
@@ -35,6 +38,7 @@ struct LimbList {
   const double* src[FA_MAXL];
   double scale[FA_MAXL];
 };
+static_assert(sizeof(LimbList) <= 4096, "LimbList is a kernel argument");
 
 #define FA_MAXAUX 3
 
