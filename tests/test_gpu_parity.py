@@ -106,6 +106,8 @@ def test_row_layout_then_rotate_sum(name, d, rows):
     ("tiny", 16, 16, [100]),
     ("tiny", 512, 8, [300]),    # d = N/2 (the widest block), G = 64 > 32 giants per giant-kernel launch
     ("tiny", 512, 64, [512]),   # d = N/2 with a full block of rows
+    ("tiny", 16, 4, [512] * 9 + [5]),   # 10 blocks: the giant steps in two chunks of blocks
+    ("tiny", 16, 4, [64] * 33),          # 33 blocks: more than one multiply-accumulate launch holds
     ("p1", 128, 16, [4096, 1000]),
     ("p2", 128, 16, [3000]),
 ])
