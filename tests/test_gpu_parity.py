@@ -377,6 +377,7 @@ def test_prepared_query_scores_identically(name, d, B):
 @pytest.mark.parametrize("name,d,B,nq,rows_list,oracle", [
     ("tiny", 16, 4, 5, [300, 512], True),   # groups of 4 + 1 queries per plaintext pass
     ("tiny", 16, 16, 3, [100], True),        # 2 + 1, G = 1 (no giant steps)
+    ("tiny", 16, 4, 4, [64] * 33, True),     # 33 blocks: two plaintext passes of 4 queries
     ("p1", 128, 16, 2, [4096, 1000], False),
     ("p2", 128, 16, 4, [3000], False),
 ])
