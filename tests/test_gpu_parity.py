@@ -483,6 +483,7 @@ def test_batch_rejects_bad_arguments():
 @pytest.mark.parametrize("name,d,B,rows_list", [
     ("tiny", 16, 4, [300, 512]),
     ("tiny", 16, 16, [100]),
+    ("tiny", 16, 4, [32] * 33),  # 33 encrypted blocks: two ct x ct launches
     ("p1", 128, 16, [4096, 1000]),
 ])
 def test_encrypted_block_score_parity(name, d, B, rows_list):
