@@ -1143,7 +1143,8 @@ size_t giant_scratch_ws(const fa_ctx* c, int nb, int d, int B) {
   if (G <= 1) return 0;
   const size_t lanes = lanes_wanted();
   const size_t cb = std::min(nb, kGiantChunk);
-  return lanes * rup(cb * L * n) + rup(cb * (G - 1) * dn * np * n) + rup(cb * 2 * np * n) + rup(cb * 2 * L * n);
+  return lanes * rup(std::max(cb, G - 1) * L * n) + rup(cb * (G - 1) * dn * np * n) + rup(cb * 2 * np * n) +
+         rup(cb * 2 * L * n);
 }
 // workspace of the multiply-accumulate and the giant steps of nq queries
 size_t giant_ws(const fa_ctx* c, int nb, int d, int B, int nq = 1) {
@@ -1439,7 +1440,7 @@ static int giant_phase(fa_ctx* c, const double* acc, int nb, int G, int B, doubl
   }
   const int lanes = lanes_wanted();
   const int cbm = std::min(nb, kGiantChunk);
-  const size_t gy_l = rup((size_t)cbm * L * n) / 8;
+  const size_t gy_l = rup((size_t)std::max(cbm, G - 1) * L * n) / 8;
   const size_t ext_w = dn * np * n;
   const size_t mark = ar.used;
   double* gy = ar.take(lanes * gy_l);
@@ -1458,12 +1459,24 @@ static int giant_phase(fa_ctx* c, const double* acc, int nb, int G, int B, doubl
   for (int b0 = 0; b0 < nb; b0 += cbm) {
     const int cb = std::min(cbm, nb - b0);
     const double* accb = acc + (size_t)b0 * astride;
-    const int gl = std::min(lanes, G - 1);
+    // the ModUps of the giant accumulators in as few launch groups as the
+    // lanes allow: one per block (over its G-1 giants) when there are fewer
+    // blocks than giants, else one per giant (over the blocks)
+    const bool per_block = cb < G - 1;
+    const int gl = std::min(lanes, per_block ? cb : G - 1);
     if ((rc = fork_lanes(c, s, gl))) return rc;
-    for (int g = 1; g < G; ++g) {
-      const int lane = (g - 1) % gl;
-      modup(c, accb + (size_t)g * ctw, astride, cb, gy + lane * gy_l, L * n, gext + (size_t)(g - 1) * ext_w,
-            (size_t)(G - 1) * ext_w, lane_stream(c, s, lane), false);
+    if (per_block) {
+      for (int blk = 0; blk < cb; ++blk) {
+        const int lane = blk % gl;
+        modup(c, accb + (size_t)blk * astride + ctw, ctw, G - 1, gy + lane * gy_l, L * n,
+              gext + (size_t)blk * (G - 1) * ext_w, ext_w, lane_stream(c, s, lane), false);
+      }
+    } else {
+      for (int g = 1; g < G; ++g) {
+        const int lane = (g - 1) % gl;
+        modup(c, accb + (size_t)g * ctw, astride, cb, gy + lane * gy_l, L * n, gext + (size_t)(g - 1) * ext_w,
+              (size_t)(G - 1) * ext_w, lane_stream(c, s, lane), false);
+      }
     }
     if ((rc = join_lanes(c, s, gl))) return rc;
     fa::giant_ks(c, gext, accb, astride, keys.data(), ggal.data(), cb, G - 1, usum, s);
