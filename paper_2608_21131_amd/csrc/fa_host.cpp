@@ -1181,10 +1181,11 @@ static void modup(fa_ctx* c, const double* cts, size_t ct_stride, int batch, dou
 // With pass_b false only the special-prime inverse and the conversion's first
 // pass run (bases, outs and gals unused): moddown_ks finishes.
 static void moddown_polys(fa_ctx* c, double* u, int count, double* conv, const double* const* bases,
-                          double* const* outs, const uint32_t* gals, hipStream_t s, bool pass_b = true) {
+                          double* const* outs, const uint32_t* gals, hipStream_t s, bool pass_b = true,
+                          bool inv_b_done = false) {
   const size_t n = c->n, L = c->L, np = c->np;
   {
-    fa::LimbBatch inv(c, s, false);
+    fa::LimbBatch inv(c, s, false, inv_b_done);
     for (int i = 0; i < count; ++i)
       for (int k = 0; k < c->K; ++k)
         inv.add(u + (size_t)i * np * n + (L + k) * n, (int)L + k, nullptr, c->h_md_scale[k]);
@@ -1205,8 +1206,16 @@ static void moddown_polys(fa_ctx* c, double* u, int count, double* conv, const d
 static void ks_moddown(fa_ctx* c, const fa::KsItem* ks, int count, const double* const* c0s, double* const* outs,
                        double* u, double* conv, hipStream_t s, const double* const* b1s = nullptr, int nq = 1) {
   const size_t n = c->n, L = c->L;
-  fa::ks_inner(c, ks, count, false, s, c->L, nq);
-  moddown_polys(c, u, 2 * count, conv, nullptr, nullptr, nullptr, s, false);
+  if (c->dnum == 1) {
+    // one digit: the special-prime sum and the first inverse pass in one
+    // kernel (measured faster at 2 and 3 primes; with more digits the fused
+    // kernel's longer load phase made it slower)
+    fa::ks_inv_b(c, ks, count, s, nq);
+    moddown_polys(c, u, 2 * count, conv, nullptr, nullptr, nullptr, s, false, true);
+  } else {
+    fa::ks_inner(c, ks, count, false, s, c->L, nq);
+    moddown_polys(c, u, 2 * count, conv, nullptr, nullptr, nullptr, s, false);
+  }
   std::vector<fa::MdKsItem> it(count);
   for (int j = 0; j < count; ++j)
     it[j] = {conv + (size_t)2 * j * L * n, ks[j].ext, ks[j].c1, ks[j].key, c0s[j], b1s ? b1s[j] : nullptr, outs[j],

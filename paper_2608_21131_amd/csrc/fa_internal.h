@@ -95,6 +95,8 @@ namespace fa {
 
 void ntt_fwd(const fa_ctx* c, const LimbList& l, hipStream_t s);
 void ntt_inv(const fa_ctx* c, const LimbList& l, hipStream_t s);
+// the second (column) pass of the inverse transform alone, ptr in place
+void ntt_inv_a(const fa_ctx* c, const LimbList& l, hipStream_t s);
 
 // Batched forward / inverse over `count` polynomials laid out as
 // base + i * stride (words) whose prime index is prime_of(i) = i % period
@@ -165,6 +167,11 @@ struct KsItem {
 // nq > 1: items grouped by key as for moddown_ks (count % nq == 0)
 void ks_inner(const fa_ctx* c, const KsItem* items, int count, bool accumulate, hipStream_t s, int t0 = 0,
               int nq = 1);
+// The special-prime part of ks_inner (no c0 term, not accumulated) fused with
+// the first pass of its inverse transform: it.u's special limbs leave holding
+// what k_ntt_inv_b would produce from ks_inner's output (ntt_inv_a finishes).
+// One-digit contexts (dnum == 1) only; does nothing otherwise.
+void ks_inv_b(const fa_ctx* c, const KsItem* items, int count, hipStream_t s, int nq = 1);
 
 // Fused giant steps of nb blocks: u[blk] = sum_{g=1..ng} sum_i sigma_g(NTT(ext)_i) key_g[i]
 // + P sigma_g(acc_g.c0), with ext = [nb][ng][dnum][np][N] holding only the first
@@ -240,9 +247,12 @@ void dec_combine(const fa_ctx* c, const double* ct, double* out, hipStream_t s);
 struct LimbBatch {
   const fa_ctx* c;
   hipStream_t s;
-  bool fwd;
+  bool fwd, a_only;  // a_only (inverse): the second pass alone, in place
   LimbList l;
-  LimbBatch(const fa_ctx* c_, hipStream_t s_, bool fwd_) : c(c_), s(s_), fwd(fwd_) { l.n = 0; }
+  LimbBatch(const fa_ctx* c_, hipStream_t s_, bool fwd_, bool a_only_ = false)
+      : c(c_), s(s_), fwd(fwd_), a_only(a_only_) {
+    l.n = 0;
+  }
   // scale < 0: N^-1 of the prime
   void add(double* dst, int prime, const double* src = nullptr, double scale = -1.0) {
     l.ptr[l.n] = dst;
@@ -254,6 +264,7 @@ struct LimbBatch {
   void flush() {
     if (l.n) {
       if (fwd) ntt_fwd(c, l, s);
+      else if (a_only) ntt_inv_a(c, l, s);
       else ntt_inv(c, l, s);
       l.n = 0;
     }

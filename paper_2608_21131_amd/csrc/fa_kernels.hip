@@ -605,6 +605,96 @@ __global__ __launch_bounds__(256) void k_ks_inner(KsArgs args, const DevPrime* _
   *u1 = canon_full(acc1, q, qinv);
 }
 
+// Key-switch sum on the special primes fused with the first pass of its
+// inverse transform: for special prime t and the workgroup's rows,
+//   u_h = sum_i sigma(ext_i) * key_i[h]   (h = 0, 1; canonical residues)
+// formed word by word, then the eight stages of inverse pass B in registers
+// and LDS, written to it.u in place of k_ks_inner's output after
+// k_ntt_inv_b.  Sixteen threads per row, sixteen consecutive words each.
+template <int DNUM>
+__global__ __launch_bounds__(256) void k_ks_inv_b(KsArgs args, const DevPrime* __restrict__ pr,
+                                                  const double* __restrict__ twt, const double* __restrict__ twr,
+                                                  int logn, int L, int np, int nq, int ngroup) {
+  __shared__ double sm[16 * ROWW];
+  const int n = 1 << logn;
+  const int rows = (n >> 8) < 16 ? (n >> 8) : 16;
+  int tile, tr, item;
+  if (!ks_decode(blockIdx.x, (n >> 8) / rows, np - L, nq, ngroup, tile, tr, item)) return;
+  const int t = L + tr;
+  const fa::KsItem& it = args.it[item];
+  const double q = pr[t].q, qinv = pr[t].qinv;
+  const double* __restrict__ T = twt + (size_t)t * 256;
+  const double* __restrict__ F = twr + (size_t)t * (n >> 8) * 8;
+  const int u = threadIdx.x, lh = u & 15, rl = u >> 4, r = tile * rows + rl;
+  const bool active = u < rows * 16;
+  double y0[16], y1[16];
+  if (active) {
+    const uint32_t k0 = (uint32_t)r * 256u + 16u * lh;
+#pragma unroll
+    for (int m = 0; m < 16; ++m) y0[m] = y1[m] = 0.0;
+#pragma unroll 1
+    for (int i = 0; i < DNUM; ++i) {
+      const double* __restrict__ src = it.ext + ((size_t)i * np + t) * n;
+      const double2* kb = reinterpret_cast<const double2*>(it.key + (((size_t)i * 2 + 0) * np + t) * n + k0);
+      const double2* ka = reinterpret_cast<const double2*>(it.key + (((size_t)i * 2 + 1) * np + t) * n + k0);
+#pragma unroll
+      for (int m2 = 0; m2 < 8; ++m2) {
+        const double2 b = kb[m2], a = ka[m2];
+        const double x0 = src[perm(k0 + 2u * m2, it.gal, logn)];
+        const double x1 = src[perm(k0 + 2u * m2 + 1u, it.gal, logn)];
+        y0[2 * m2] += mul(x0, b.x, q, qinv);
+        y1[2 * m2] += mul(x0, a.x, q, qinv);
+        y0[2 * m2 + 1] += mul(x1, b.y, q, qinv);
+        y1[2 * m2 + 1] += mul(x1, a.y, q, qinv);
+      }
+    }
+#pragma unroll
+    for (int m = 0; m < 16; ++m) {
+      y0[m] = canon_full(y0[m], q, qinv);
+      y1[m] = canon_full(y1[m], q, qinv);
+    }
+  }
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    double x[16];
+    if (active) {
+#pragma unroll
+      for (int m = 0; m < 16; ++m) x[m] = h == 0 ? y0[m] : y1[m];
+#pragma unroll
+      for (int s1 = 7; s1 >= 4; --s1) {
+        const int half = 8 >> (s1 - 4);
+        const double f = F[r * 8 + s1];
+#pragma unroll
+        for (int m = 0; m < 16; ++m) {
+          if (m & half) continue;
+          gs_bfly(x[m], x[m + half], twb(T, f, s1, (lh << (s1 - 4)) + (m >> (8 - s1)), q, qinv), q, qinv);
+        }
+      }
+#pragma unroll
+      for (int m = 0; m < 16; ++m) sm[lds_row(rl, 16 * lh + m)] = x[m];
+    }
+    __syncthreads();
+    if (active) {
+#pragma unroll
+      for (int m = 0; m < 16; ++m) x[m] = sm[lds_row(rl, lh + 16 * m)];
+#pragma unroll
+      for (int s1 = 3; s1 >= 0; --s1) {
+        const int half = 8 >> s1;
+        const double f = F[r * 8 + s1];
+#pragma unroll
+        for (int m = 0; m < 16; ++m) {
+          if (m & half) continue;
+          gs_bfly(x[m], x[m + half], twb(T, f, s1, m >> (4 - s1), q, qinv), q, qinv);
+        }
+      }
+      double* out = it.u + ((size_t)h * np + t) * n + (size_t)r * 256;
+#pragma unroll
+      for (int m = 0; m < 16; ++m) out[lh + 16 * m] = x[m];
+    }
+    __syncthreads();  // the second polynomial reuses the LDS rows
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Giant steps of the diagonal scoring, fused: for every block and every
 // ciphertext/special prime t,
@@ -1420,6 +1510,17 @@ void ntt_inv(const fa_ctx* c, const LimbList& l, hipStream_t s) {
   FA_SA_SWITCH(launch_inv, c, l, s)
 }
 
+template <int SA>
+static void launch_inv_a(const fa_ctx* c, const LimbList& l, hipStream_t s) {
+  using P = PassA<SA>;
+  dim3 ga(c->n / P::TILE, l.n);
+  hipLaunchKernelGGL(k_ntt_inv_a<SA>, ga, dim3(256), 0, s, l, c->d_pr, c->d_twa_inv);
+}
+void ntt_inv_a(const fa_ctx* c, const LimbList& l, hipStream_t s) {
+  if (l.n == 0) return;
+  FA_SA_SWITCH(launch_inv_a, c, l, s)
+}
+
 static void strided(const fa_ctx* c, double* base, size_t stride, int count, int period, int prime_off,
                     hipStream_t s, bool fwd) {
   LimbBatch b(c, s, fwd);
@@ -1586,6 +1687,26 @@ void ks_inner(const fa_ctx* c, const KsItem* items, int count, bool accumulate, 
       case 8: launch_ks<8>(c, a, m, accumulate, s, t0, nq); break;
       default: break;
     }
+  }
+}
+
+template <int DNUM>
+static void launch_ks_inv_b(const fa_ctx* c, const KsArgs& a, int m, hipStream_t s, int nq) {
+  const int rows = (c->n >> 8) < 16 ? (c->n >> 8) : 16;
+  const int ngroup = m / nq;
+  dim3 g(ks_grid((c->n >> 8) / rows, c->K, nq, ngroup));
+  hipLaunchKernelGGL(k_ks_inv_b<DNUM>, g, dim3(256), 0, s, a, c->d_pr, c->d_twt_inv, c->d_twr_inv, c->logn, c->L,
+                     c->np, nq, ngroup);
+}
+
+void ks_inv_b(const fa_ctx* c, const KsItem* items, int count, hipStream_t s, int nq) {
+  if (c->dnum != 1) return;  // the host calls it for one-digit contexts only
+  const int chunk = (FA_MAXKS / nq) * nq;
+  for (int off = 0; off < count; off += chunk) {
+    KsArgs a;
+    const int m = count - off < chunk ? count - off : chunk;
+    for (int i = 0; i < m; ++i) a.it[i] = items[off + i];
+    launch_ks_inv_b<1>(c, a, m, s, nq);
   }
 }
 

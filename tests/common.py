@@ -12,6 +12,7 @@ from paper_2608_21131_amd import gen
 # parameter sets: (log2 N, L, K)
 PARAMS = {
     "tiny": (10, 3, 1),
+    "tiny1": (10, 3, 3),   # one digit (alpha = K = L)
     "small": (11, 4, 2),
     "p1": (13, 3, 1),
     "p2": (15, 8, 2),

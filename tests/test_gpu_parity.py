@@ -53,8 +53,8 @@ def test_encrypt_decrypt_parity(name):
     assert np.max(np.abs(z - v)) < 1e-6
 
 
-@pytest.mark.parametrize("name,steps", [("tiny", [1, 3, 100]), ("small", [1, 7]), ("p1", [1, 64]),
-                                        ("p2", [5]), ("p4", [1])])
+@pytest.mark.parametrize("name,steps", [("tiny", [1, 3, 100]), ("tiny1", [1, 5]), ("small", [1, 7]),
+                                        ("p1", [1, 64]), ("p2", [5]), ("p4", [1])])
 def test_rotation_parity(name, steps):
     p = pair(name)
     v = np.random.default_rng(3).uniform(-1, 1, p.par.slots)
@@ -108,6 +108,8 @@ def test_row_layout_then_rotate_sum(name, d, rows):
     ("tiny", 512, 64, [512]),   # d = N/2 with a full block of rows
     ("tiny", 16, 4, [512] * 9 + [5]),   # 10 blocks: the giant steps in two chunks of blocks
     ("tiny", 16, 4, [64] * 33),          # 33 blocks: more than one multiply-accumulate launch holds
+    ("tiny1", 16, 4, [300, 512]),        # one digit: the fused special-prime kernel
+    ("tiny1", 64, 8, [512]),
     ("p1", 128, 16, [4096, 1000]),
     ("p2", 128, 16, [3000]),
 ])
@@ -378,6 +380,7 @@ def test_prepared_query_scores_identically(name, d, B):
     ("tiny", 16, 4, 5, [300, 512], True),   # groups of 4 + 1 queries per plaintext pass
     ("tiny", 16, 16, 3, [100], True),        # 2 + 1, G = 1 (no giant steps)
     ("tiny", 16, 4, 4, [64] * 33, True),     # 33 blocks: two plaintext passes of 4 queries
+    ("tiny1", 16, 4, 4, [300], True),        # one digit, batched preparation
     ("p1", 128, 16, 2, [4096, 1000], False),
     ("p2", 128, 16, 4, [3000], False),
 ])
@@ -412,7 +415,8 @@ def test_batch_scores_match_oracle_and_single(name, d, B, nq, rows_list, oracle)
             assert np.max(np.abs(z[:len(X)] - X @ Q[j])) < 1e-4
 
 
-@pytest.mark.parametrize("name,B,nq", [("tiny", 4, 1), ("tiny", 16, 3), ("p1", 16, 5), ("p4", 16, 4)])
+@pytest.mark.parametrize("name,B,nq", [("tiny", 4, 1), ("tiny", 16, 3), ("tiny1", 16, 3), ("p1", 16, 5),
+                                       ("p4", 16, 4)])
 def test_prepare_batch_matches_single(name, B, nq):
     """fa_prepare_batch: every query's baby rotations equal fa_prepare_query's word for word
     (launch groups of 16 // nq steps x nq queries, the last group short), and the batch
