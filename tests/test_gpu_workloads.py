@@ -274,6 +274,73 @@ def test_rerank_query_batch_fullsize():
     assert err < 1e-4
 
 
+def test_three_level_coarse_batch_at_three_primes_fullsize():
+    """The full three-level query's coarse level as bench.py runs it: 222,049 x 512-d centroids
+    in 7 blocks enrolled at 3 primes, four queries dropped to 3 primes, prepared together
+    (fa_prepare_batch) and scored in one plaintext pass (fa_score_batch).  The first query's
+    last, partial block bit-exact against the oracle at the lower level; every score of the
+    four queries within 1e-4 of float64."""
+    from paper_2608_21131_amd import fa
+    w = wl.WORKLOADS["three_level"]
+    ex = w.extra
+    L_low = 3
+    par = ckks.Params(logn=w.log_n, L=w.L, K=w.K)
+    lp = ckks.Params(logn=w.log_n, L=L_low, K=w.K, primes=par.q[:L_low] + par.p)
+    ctx = fa.Context(w.log_n, w.L, w.K, 40)
+    s = wl.secret(w)
+    steps = wl.rotation_steps(w)
+    say(f"[3lvl] keys for {len(steps)} rotations")
+    for i in range(0, len(steps), 8):
+        chunk = steps[i:i + 8]
+        rand = [wl.key_randomness(w, r, par.primes, par.dnum) for r in chunk]
+        ctx.keygen(s, chunk, np.stack([x[0] for x in rand]), np.stack([x[1] for x in rand]))
+    low = ctx.at_level(L_low)
+    lo = ckks.Oracle(lp)
+    idx = list(range(L_low)) + list(range(par.L, par.L + par.K))
+    keys = {}
+    for r in ckks.steps_for_bsgs(w.d, w.B):
+        a, e = wl.key_randomness(w, r, par.primes, par.dnum)
+        keys[r] = lo.keygen(s, r, a[:lp.dnum][:, idx], e[:lp.dnum])
+    X, centers = wl.candidate_rows(w, ex["coarse"], stream_extra=1)
+    S = par.slots
+    nb = -(-ex["coarse"] // S)
+    blocks, ref_coeffs = [], None
+    for b in range(nb):
+        rows = X[b * S:(b + 1) * S]
+        if b == nb - 1:
+            ref_coeffs = ckks.layout_b_coeffs(rows.astype(np.float64), lp, w.d, w.B)
+            blocks.append(low.encode_db_block_int(ref_coeffs))
+        else:
+            blocks.append(low.encode_db_block(rows, w.d, 1, w.B))
+    Q = wl.query_vectors(w, 4, centers)
+    full_o = ckks.Oracle(par)
+    qs, q0_o = [], None
+    for j, v in enumerate(Q):
+        a, e = wl.enc_randomness(w, par.q, tag=j)
+        m = ckks.encode(ckks.replicate(v, S), par.n, 40)
+        qs.append(ctx.drop_level(low, ctx.encrypt(m, a, e)))
+        if j == 0:
+            q0_o = np.ascontiguousarray(full_o.encrypt(m, a, e, s)[:, :L_low])
+    say(f"[3lvl] 4 queries x {nb} coarse blocks at {L_low} primes, prepared and scored together")
+    preps = low.prepare_batch(qs, w.B)
+    outs = low.score_batch(qs, preps, blocks, w.d, w.B)
+    got = low.export(outs[0], 2 * nb).reshape(nb, 2, L_low, par.n)[-1]
+    say("[3lvl] oracle: baby rotations + the last block for the first query")
+    pts_o = np.stack([ckks.to_residues(x, lp.q) for x in ref_coeffs]).reshape(w.G, w.B, L_low, par.n)
+    assert np.array_equal(got, lo.bsgs_block(lo.baby_rotations(q0_o, w.B, keys), pts_o, w.B, w.G, keys))
+    err = 0.0
+    W_ = low.ct_words
+    for j in range(len(Q)):
+        for b in range(nb):
+            rows = X[b * S:(b + 1) * S].astype(np.float64)
+            z = low.decode(low.decrypt(outs[j][b * W_:(b + 1) * W_]), 80)
+            err = max(err, float(np.max(np.abs(z[:len(rows)] - rows @ Q[j]))))
+            if len(rows) < S:
+                err = max(err, float(np.max(np.abs(z[len(rows):]))))
+    say(f"[3lvl] max |score - float64| = {err:.2e}")
+    assert err < 1e-4
+
+
 def test_rerank_encrypted_database_at_three_primes_fullsize():
     """The rerank level against an encrypted database (every diagonal a ciphertext, enrolled at
     3 primes), ct x ct with one relinearisation per (block, giant): the last block's output
