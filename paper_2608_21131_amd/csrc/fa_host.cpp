@@ -1071,15 +1071,14 @@ int fa_encode_projection(fa_ctx* c, const float* W, int d_in, int r, int baby_st
 namespace {
 constexpr int kRotBatch = 16;  // most rotations key-switched per launch group
 
-// Rotations per launch group actually used (<= kRotBatch; FA_ROT_BATCH tunes it):
-// smaller groups keep the key-switch products resident in the last-level cache.
+// Rotations per launch group actually used (1..kRotBatch; FA_ROT_BATCH tunes
+// it).  The environment is read once, by a thread-safe static initialiser.
 int rot_batch() {
-  static int v = -1;
-  if (v < 0) {
+  static const int v = [] {
     const char* e = getenv("FA_ROT_BATCH");
-    v = e ? atoi(e) : kRotBatch;
-    if (v < 1 || v > kRotBatch) v = kRotBatch;
-  }
+    const int r = e ? atoi(e) : kRotBatch;
+    return (r < 1 || r > kRotBatch) ? kRotBatch : r;
+  }();
   return v;
 }
 
@@ -1106,13 +1105,11 @@ size_t rotate_ws(const fa_ctx* c, int nb) {
 // Lanes (the caller's stream plus auxiliary streams) that independent
 // key-switch batches of one scoring call are spread over; FA_STREAMS tunes it.
 int lanes_wanted() {
-  static int v = -1;
-  if (v < 0) {
+  static const int v = [] {
     const char* e = getenv("FA_STREAMS");
-    v = e ? atoi(e) : 2;
-    if (v < 1) v = 1;
-    if (v > FA_MAXAUX + 1) v = FA_MAXAUX + 1;
-  }
+    const int r = e ? atoi(e) : 2;
+    return r < 1 ? 1 : (r > FA_MAXAUX + 1 ? FA_MAXAUX + 1 : r);
+  }();
   return v;
 }
 

@@ -1767,29 +1767,26 @@ void giant_ks(const fa_ctx* c, const double* ext, const double* acc, size_t astr
 // the three-stage single-query kernel (FA_MAC_STAGES=2 selects the two-slot one)
 // 17..31 pairs left: one padded 32-pair launch (FA_MAC_PAD=0: 16 + 16 / 8)
 static bool mac_pad_wide() {
-  static int v = -1;
-  if (v < 0) {
+  static const bool v = [] {
     const char* e = getenv("FA_MAC_PAD");
-    v = e ? atoi(e) : 1;
-  }
-  return v != 0;
+    return !e || atoi(e) != 0;
+  }();
+  return v;
 }
 static bool mac_three_stages() {
-  static int v = -1;
-  if (v < 0) {
+  static const bool v = [] {
     const char* e = getenv("FA_MAC_STAGES");
-    v = e && atoi(e) == 2 ? 2 : 3;
-  }
-  return v == 3;
+    return !(e && atoi(e) == 2);
+  }();
+  return v;
 }
 
 static int mac_pairs_max() {
-  static int v = -1;
-  if (v < 0) {
+  static const int v = [] {
     const char* e = getenv("FA_MAC_PAIRS");
-    v = e ? atoi(e) : 32;
-    if (v != 8 && v != 16) v = 32;
-  }
+    const int r = e ? atoi(e) : 32;
+    return (r == 8 || r == 16) ? r : 32;
+  }();
   return v;
 }
 
