@@ -547,7 +547,12 @@ def test_encrypted_block_needs_relin_key():
     assert ei.value.code == fa.FA_E_NOKEY
 
 
-@pytest.mark.parametrize("name,d_in,R,B", [("small", 64, 16, 4), ("p2", 512, 128, 16)])
+@pytest.mark.parametrize("name,d_in,R,B", [
+    ("small", 64, 16, 4),
+    ("small", 16, 16, 4),   # R = d_in: no fold
+    ("small", 64, 16, 1),   # B = 1: no baby rotations
+    ("p2", 512, 128, 16),
+])
 def test_encrypted_projection_parity(name, d_in, R, B):
     """fa_project_ct_enc (W's diagonals encrypted): the output ciphertext equals the oracle's
     ct x ct diagonal product and fold word for word and decrypts to W^T q."""
