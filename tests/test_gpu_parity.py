@@ -142,7 +142,12 @@ def test_diag_score_parity(name, d, B, rows_list):
             assert np.max(np.abs(z[len(X):])) < 1e-4
 
 
-@pytest.mark.parametrize("name,d_in,R,B,rows", [("small", 64, 16, 4, 100), ("p2", 512, 128, 16, 2000)])
+@pytest.mark.parametrize("name,d_in,R,B,rows", [
+    ("small", 64, 16, 4, 100),
+    ("small", 16, 16, 4, 100),   # R = d_in: no fold
+    ("small", 64, 16, 1, 100),   # B = 1: no baby rotations
+    ("p2", 512, 128, 16, 2000),
+])
 def test_projection_parity(name, d_in, R, B, rows):
     p = pair(name, wid=6)
     S = p.par.slots
