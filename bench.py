@@ -187,6 +187,7 @@ def transfer_ms(bn, q, out):
     the stream: the query ciphertext host -> device and the output ciphertexts device -> host,
     both from / to pinned host memory."""
     torch = bn.torch
+    q, out = q.t, out.t
     hq = torch.empty(q.numel(), dtype=torch.float64, pin_memory=True)
     ho = torch.empty(out.numel(), dtype=torch.float64, pin_memory=True)
     dq = torch.empty_like(q)
@@ -377,7 +378,8 @@ def run_membership(bn, args):
     if not args.no_check:
         ctw = c11.ct_words
         c2 = levels[w.L - L]
-        z = np.concatenate([c2.decode(c2.decrypt(out[i * ctw:i * ctw + 2 * L * c2.n]), ls) for i in range(nb)])
+        z = np.concatenate([c2.decode(c2.decrypt(c2.wrap(out.t[i * ctw:i * ctw + 2 * L * c2.n], 2, 1, 0)), ls)
+                            for i in range(nb)])
         z = z[:w.rows] * (2.0 ** ls / sc) / mo
         qR = W.astype(np.float32).astype(np.float64).T @ q
         Xm = Xr.astype(np.float32).astype(np.float64)
@@ -509,8 +511,7 @@ def run_batch_level(bn, args, r, nq):
     qvs = bn.wl.query_vectors(w, nq + 1, r["centers"])[1:]
     q_tops = [bn.encrypt(pad(v, w.d), tag=100 + j) for j, v in enumerate(qvs)]
     qs = [ctx.new_ct() for _ in range(nq)] if ctx is not top else q_tops
-    preps = [torch.empty(int(ctx.lib.fa_prepared_words(ctx.h, w.B)), dtype=torch.float64, device="cuda")
-             for _ in range(nq)]
+    preps = [ctx.new_prep(w.B) for _ in range(nq)]
     outs = [ctx.new_ct(w.n_blocks) for _ in range(nq)]
     ws_p = ctx.prepare_batch_workspace(nq, w.B)
     ws_b = ctx.batch_workspace(nq, w.n_blocks, w.d, w.B)
@@ -704,8 +705,7 @@ def run_three_level(bn, args):
     queries = bn.wl.query_vectors(w, nq, centers)
     qcts = [bn.encrypt(qv, tag=i) for i, qv in enumerate(queries)]
     qs = [ctx.new_ct() for _ in range(gq)] if ctx is not top_ctx else None
-    preps = [torch.empty(int(ctx.lib.fa_prepared_words(ctx.h, w.B)), dtype=torch.float64, device="cuda")
-             for _ in range(gq)]
+    preps = [ctx.new_prep(w.B) for _ in range(gq)]
     outs_c = [ctx.new_ct(n_coarse) for _ in range(gq)]
     outs_f = [ctx.new_ct(ex["fine_blocks"]) for _ in range(gq)]
     outs_r = [ctx.new_ct(ex["rerank_blocks"]) for _ in range(gq)]
@@ -763,7 +763,7 @@ def run_three_level(bn, args):
             fsel = sorted(set(int(x) % ex["fine_pool_blocks"] for x in ids))
             fsel = (fsel + [b for b in range(ex["fine_pool_blocks"]) if b not in fsel])[:ex["fine_blocks"]]
             a = ev()
-            ctx.score_prepared(qi[j], preps[j], [pools["fine"][b] for b in fsel], w.d, w.B, out=outs_f[j], ws=ws_s)
+            ctx.score_prepared(qi[j], preps[j], pools["fine"], w.d, w.B, out=outs_f[j], ws=ws_s, block_ids=fsel)
             fine.append((a, ev(), fsel))
         for j in range(m):
             fsel = fine[j][2]
@@ -771,8 +771,8 @@ def run_three_level(bn, args):
             rsel = sorted(set(int(x) % ex["rerank_pool_blocks"] for x in ids))
             rsel = (rsel + [b for b in range(ex["rerank_pool_blocks"]) if b not in rsel])[:ex["rerank_blocks"]]
             a = ev()
-            ctx.score_prepared(qi[j], preps[j], [pools["rerank"][b] for b in rsel], w.d, w.B, out=outs_r[j],
-                               ws=ws_s)
+            ctx.score_prepared(qi[j], preps[j], pools["rerank"], w.d, w.B, out=outs_r[j], ws=ws_s,
+                               block_ids=rsel)
             rer.append((a, ev(), rsel))
         for j in range(m):
             rsel = rer[j][2]

@@ -17,29 +17,40 @@
  *     of the threshold and the sign iteration (Section 3.1, "Membership
  *     search");
  *   - client-side helpers for tests and benchmarks: key generation, secret-key
- *     encryption, decryption, encoding and decoding (Section 2, "Setting").
+ *     encryption, decryption, encoding and decoding (Section 2, "Setting" and
+ *     "The round trip").
  *
  * Scheme and conventions (shared with the documentation of every call):
  *   N = 2^log_n ring degree, S = N/2 slots, L ciphertext primes, K special
- *   primes, all 50-bit and congruent to 1 mod 2N: the L+K largest such primes
- *   below 2^50, in descending order.  Hybrid key switching uses alpha = K
- *   primes per digit and dnum = ceil(L/K) digits.  Slot j is the evaluation
- *   at zeta^(5^j mod 2N), zeta = exp(i*pi/N); rotating by r rolls the slots
- *   left by r (automorphism X -> X^(5^r)).  The scoring calls do not
- *   rescale: the scale of a product is the product of the scales.  The
+ *   primes, all in (2^49, 2^50) and congruent to 1 mod 2N: by default the L+K
+ *   largest such primes below 2^50, in descending order.  Hybrid key switching
+ *   uses alpha = K primes per digit and dnum = ceil(L/K) digits.  Slot j is
+ *   the evaluation at zeta^(5^j mod 2N), zeta = exp(i*pi/N); rotating by r
+ *   rolls the slots left by r (automorphism X -> X^(5^r)).  The scoring calls
+ *   do not rescale: the scale of a product is the product of the scales.  The
  *   membership calls (fa_rescale onwards) rescale after every ciphertext
  *   product and track the scale as a double.
  *
- * Memory.  Ciphertext, plaintext and workspace buffers are caller-owned
- * DEVICE memory (for example torch tensors), 8-byte words, 256-byte aligned:
- *   ciphertext  2*L*N words  [c0 | c1], each [L][N]
- *   plaintext     L*N words  [L][N]
- * The word format and coefficient order inside the device buffers are private
- * to the library (NTT form); fa_export_coeffs() returns the canonical form:
- * coefficient order, residues in [0, q_i) as uint64.  Host arrays are marked
- * "host".  The context owns its tables and rotation keys (device memory it
- * allocates at fa_ctx_create / fa_keygen and frees at fa_ctx_destroy); the
- * scoring calls allocate nothing.
+ * Buffers.  Ciphertexts, plaintexts and workspaces are caller-owned DEVICE
+ * memory (for example torch tensors), 8-byte words, 256-byte aligned.  Every
+ * scoring-path call takes its ciphertexts and plaintexts as fa_buf
+ * descriptors: the device pointer and its capacity, plus what the buffer
+ * holds -- polynomials per object (2 ciphertext, 1 plaintext, 3 a product
+ * before relinearisation), the number of objects stored back to back, the
+ * number of primes per polynomial (its level) and the scale exponent.  One
+ * object occupies n_polys * limbs * N words: a ciphertext [c0 | c1], each
+ * [limbs][N]; a plaintext [limbs][N].  Calls check the descriptors of their
+ * inputs on the host before any launch and return FA_E_SHAPE when a buffer is
+ * at another level than the context, holds the wrong kind of object, holds too
+ * few objects for the call, is smaller than its contents, or carries a scale
+ * the call cannot combine (see each call).  An output descriptor must bring
+ * `dev` and `bytes`; the call fills in its n_polys, count, limbs and
+ * log_scale.  The word format and coefficient order inside device buffers are
+ * private to the library (NTT form); fa_export_coeffs() returns the canonical
+ * form: coefficient order, residues in [0, q_i) as uint64.  Host arrays are
+ * marked "host".  The context owns its tables and rotation keys (device
+ * memory it allocates at fa_ctx_create / fa_keygen and frees at
+ * fa_ctx_destroy); the scoring calls allocate nothing.
  *
  * Streams.  Calls that take `stream` (a hipStream_t) only enqueue work on it
  * and return; the caller synchronises.  Calls without `stream` are
@@ -66,7 +77,8 @@ extern "C" {
 enum {
   FA_OK = 0,
   FA_E_INVAL = -1, /* bad argument value (null pointer, out-of-range size)   */
-  FA_E_SHAPE = -2, /* sizes inconsistent with the context or with each other */
+  FA_E_SHAPE = -2, /* sizes, levels, kinds or scales inconsistent with the
+                      context or with each other                             */
   FA_E_NOKEY = -3, /* a rotation key the operation needs was never generated */
   FA_E_NOMEM = -4, /* workspace too small, or a setup-time allocation failed */
   FA_E_HIP = -5    /* HIP runtime / launch error                             */
@@ -87,18 +99,34 @@ enum {
 typedef struct fa_ctx fa_ctx;
 
 typedef struct {
-  uint32_t log_n;     /* 10..16 */
-  uint32_t L;         /* ciphertext primes, 1..16 */
-  uint32_t K;         /* special primes, 1..4 (= primes per key-switch digit) */
-  uint32_t log_scale; /* default scale 2^log_scale used by fa_encode_db_block */
+  uint32_t log_n;         /* 10..16 */
+  uint32_t L;             /* ciphertext primes, 1..16 */
+  uint32_t K;             /* special primes, 1..4 (= primes per key-switch digit); ceil(L/K) <= 8 */
+  uint32_t log_scale;     /* default scale 2^log_scale of fa_encode_db_block / fa_encode_projection */
+  const uint64_t* primes; /* host [L+K]: q_0..q_{L-1}, then p_0..p_{K-1}, distinct primes in
+                             (2^49, 2^50), each 1 mod 2N; or NULL for the default choice */
 } fa_params;
+
+/* A caller-owned device buffer and its contents (see "Buffers" above). */
+typedef struct {
+  void* dev;         /* device memory, 256-byte aligned                        */
+  size_t bytes;      /* its capacity in bytes                                  */
+  uint32_t n_polys;  /* polynomials per object: 2 ciphertext, 1 plaintext      */
+  uint32_t count;    /* objects stored back to back                            */
+  uint32_t limbs;    /* primes per polynomial: the level                       */
+  int32_t log_scale; /* the objects are at scale 2^log_scale                   */
+} fa_buf;
 
 /* ---- context ------------------------------------------------------------ */
 
-/* Create a context on the current HIP device: selects the primes, builds
- * twiddle and basis-conversion tables on the device.  Returns FA_E_INVAL for
- * parameters outside the ranges above, FA_E_NOMEM / FA_E_HIP on device
- * failure.  *out is set only on success. */
+/* Create a context on the current HIP device for the scheme parameters of
+ * Section 2 "Security parameters" (ring degree, RNS primes, scale): selects
+ * or checks the primes, builds twiddle and basis-conversion tables on the
+ * device.  Returns FA_E_INVAL for parameters outside the ranges of fa_params
+ * (including more than 8 key-switch digits, and explicit primes that are not
+ * distinct primes in (2^49, 2^50) congruent to 1 mod 2N) before touching the
+ * device, FA_E_NOMEM / FA_E_HIP on device failure.  *out is set only on
+ * success. */
 int fa_ctx_create(const fa_params* params, fa_ctx** out);
 void fa_ctx_destroy(fa_ctx* ctx);
 
@@ -111,29 +139,35 @@ void fa_ctx_destroy(fa_ctx* ctx);
  * level its ranked product needs, Section 2 "Measured prototype vs.
  * deployment").  Keys generated later on either context are not shared. */
 int fa_ctx_create_level(const fa_ctx* parent, uint32_t L_low, fa_ctx** out);
-/* Level drop of a ciphertext from `parent` to `child` (fa_ctx_create_level):
- * keeps the first child->L limbs of c0 and c1.  Exact while the message plus
- * noise stays below half the product of the kept primes. */
-int fa_drop_level(const fa_ctx* parent, const fa_ctx* child, const void* ct, void* out, void* stream);
+/* Level drop of `ct` (ciphertexts of `parent`, at parent->L primes) to the
+ * level of `child` (fa_ctx_create_level): keeps the first child L limbs of c0
+ * and c1 of every ciphertext, scale unchanged.  Exact while the message plus
+ * noise stays below half the product of the kept primes.  FA_E_SHAPE if
+ * `child` is not a lower level of `parent` or ct is not at the parent's
+ * level. */
+int fa_drop_level(const fa_ctx* parent, const fa_ctx* child, const fa_buf* ct, fa_buf* out, void* stream);
 
 /* The L+K primes (host out[L+K]): q_0..q_{L-1}, then p_0..p_{K-1}. */
 int fa_ctx_primes(const fa_ctx* ctx, uint64_t* out);
-size_t fa_ct_words(const fa_ctx* ctx); /* 2*L*N */
-size_t fa_pt_words(const fa_ctx* ctx); /* L*N   */
+size_t fa_ct_bytes(const fa_ctx* ctx);  /* one ciphertext: 2*L*N*8 */
+size_t fa_pt_bytes(const fa_ctx* ctx);  /* one plaintext:    L*N*8 */
 size_t fa_key_bytes(const fa_ctx* ctx); /* device bytes per rotation key */
 const char* fa_last_error(void);
 
 /* ---- keys and client-side operations (tests, benchmark set-up) ---------- */
 
-/* Rotation keys for left rotations by steps[0..n_steps-1] (1 <= step < S),
- * switching from the automorphed secret sigma_{5^r}(s) back to s, with all
- * randomness supplied by the caller (host arrays):
+/* Rotation keys (the keys a rotation of the packed vector needs, Section 2
+ * "What CKKS gives us"; the server keeps them resident, Section 3.4
+ * "Warm-query kernel path") for left rotations by steps[0..n_steps-1]
+ * (1 <= step < S), switching from the automorphed secret sigma_{5^r}(s) back
+ * to s, with all randomness supplied by the caller (host arrays):
  *   s  [N]                        ternary secret, entries in {-1, 0, 1}
  *   a  [n_steps][dnum][L+K][N]    uniform residues, a[..][t][..] < prime t
  *   e  [n_steps][dnum][N]         small noise integers
  * Key digit i of step r: b_i = -a_i*s + e_i + (P*Qhat_i*[Qhat_i^-1]_{Q_i})*sigma(s)
  * over every prime of Q u P.  Keys already present for a step are replaced.
- * Synchronous; allocates the keys' device memory. */
+ * Synchronous; allocates the keys' device memory.  Errors: FA_E_INVAL (null
+ * array, a step out of range, a non-ternary secret), FA_E_NOMEM, FA_E_HIP. */
 int fa_keygen(fa_ctx* ctx, const int64_t* s, const int32_t* steps, int n_steps, const uint64_t* a,
               const int64_t* e);
 /* 1 if a key for left rotation by `step` exists, else 0. */
@@ -149,65 +183,94 @@ int fa_keygen_relin(fa_ctx* ctx, const int64_t* s, const uint64_t* a, const int6
 /* 1 if the relinearisation key exists, else 0. */
 int fa_has_relin_key(const fa_ctx* ctx);
 
-/* Secret-key encryption (the query is encrypted by its owner): host inputs
- *   m [N] integer plaintext coefficients (|m| < 2^62), a [L][N] uniform
- *   residues, e [N] noise; s is the secret given to fa_keygen (or set by
- *   fa_set_secret).  Writes c1 = a, c0 = -a*s + e + m  into ct (device). */
+/* Secret-key encryption of the query by its owner (Section 2 "The round
+ * trip", step 1; the single-key setting of "Setting"): host inputs
+ *   m [N] integer plaintext coefficients (|m| < 2^62) at scale 2^log_scale,
+ *   a [L][N] uniform residues, e [N] noise (|e| <= 1024); s is the secret
+ *   given to fa_keygen (or set by fa_set_secret).
+ * Writes one ciphertext c1 = a, c0 = -a*s + e + m into ct (device; its
+ * descriptor gets n_polys 2, count 1, limbs L, log_scale).  Synchronous on
+ * the stream.  Errors: FA_E_INVAL (null pointer, a coefficient out of range),
+ * FA_E_SHAPE (ct->bytes below one ciphertext), FA_E_NOMEM / FA_E_HIP. */
 int fa_set_secret(fa_ctx* ctx, const int64_t* s);
-int fa_encrypt(fa_ctx* ctx, const int64_t* m, const uint64_t* a, const int64_t* e, void* ct, void* stream);
-/* Encrypts n_pts device plaintexts (as written by fa_encode_db_block /
- * fa_encode_db_block_int, [n_pts][L][N]) into cts (device, [n_pts][2][L][N]):
- * ct_j = (-a_j*s + e_j + pt_j, a_j) with host a [n_pts][L][N] residues and
- * e [n_pts][N] noise (|e| <= 1024).  This is how a data owner enrolls an
- * encrypted block (FA_LAYOUT_DIAG_ENC).  Synchronous on the stream. */
-int fa_encrypt_pts(fa_ctx* ctx, const void* pts, int n_pts, const uint64_t* a, const int64_t* e, void* cts,
-                   void* stream);
-/* m' = c0 + c1*s, coefficient form, host out [L][N] residues in [0, q_i).
- * Synchronous with respect to `stream`. */
-int fa_decrypt(fa_ctx* ctx, const void* ct, uint64_t* out, void* stream);
-/* Canonical form of n_polys consecutive [L][N] polynomials of a device
- * buffer (2 for a ciphertext, 1 for a plaintext): host out [n_polys][L][N]. */
-int fa_export_coeffs(fa_ctx* ctx, const void* buf, int n_polys, uint64_t* out, void* stream);
-/* The inverse of fa_export_coeffs: n_polys polynomials in canonical form
- * (host [n_polys][L][N], limb t of every polynomial below prime t) into the
- * device buffer buf in the library's private form.  Enrolled blocks can so
- * be saved and loaded again without re-encoding them (the paper keeps its
- * encrypted database on disk and reloads it warm, section 2 "Measured
- * prototype vs. deployment").  Allocates a staging buffer; synchronous on
- * the stream.  Errors: FA_E_INVAL (null pointer, n_polys < 1, a residue not
- * below its prime), FA_E_NOMEM, FA_E_HIP. */
-int fa_import_coeffs(fa_ctx* ctx, const uint64_t* coeffs, int n_polys, void* buf, void* stream);
+int fa_encrypt(fa_ctx* ctx, const int64_t* m, int32_t log_scale, const uint64_t* a, const int64_t* e, fa_buf* ct,
+               void* stream);
+/* Encrypts the pts->count device plaintexts of `pts` (as written by
+ * fa_encode_db_block / fa_encode_db_block_int) into cts (device, that many
+ * ciphertexts, same scale): ct_j = (-a_j*s + e_j + pt_j, a_j) with host
+ * a [count][L][N] residues and e [count][N] noise (|e| <= 1024).  This is how
+ * a data owner enrolls an encrypted block (FA_LAYOUT_DIAG_ENC; Section 2
+ * "Measured prototype vs. deployment": a deployment stores the database as
+ * ciphertexts).  Synchronous on the stream. */
+int fa_encrypt_pts(fa_ctx* ctx, const fa_buf* pts, const uint64_t* a, const int64_t* e, fa_buf* cts, void* stream);
+/* The client's decryption of a score ciphertext (Section 2 "The round trip",
+ * steps 3, 5 and 7): m' = c0 + c1*s of the first ciphertext of ct,
+ * coefficient form, host out [L][N] residues in [0, q_i).  Synchronous with
+ * respect to `stream`.  FA_E_SHAPE unless ct holds a ciphertext at the
+ * context's level. */
+int fa_decrypt(fa_ctx* ctx, const fa_buf* ct, uint64_t* out, void* stream);
+/* Canonical form of every polynomial of a device buffer: host out
+ * [count][n_polys][L][N], coefficient order, residues in [0, q_i) -- the
+ * representation in which ciphertexts are compared word for word with an
+ * independent implementation of the scheme (Section 2 "What CKKS gives us").
+ * Synchronous on the stream.  FA_E_SHAPE unless buf is at the context's
+ * level. */
+int fa_export_coeffs(fa_ctx* ctx, const fa_buf* buf, uint64_t* out, void* stream);
+/* The inverse of fa_export_coeffs: buf->count objects of buf->n_polys
+ * polynomials in canonical form (host [count][n_polys][L][N], limb t of
+ * every polynomial below prime t) into buf (device) in the library's
+ * private form; buf->limbs must be L and buf->log_scale is kept.  Enrolled
+ * blocks can so be saved and loaded again without re-encoding them (the
+ * paper keeps its encrypted database on disk and reloads it warm, Section 2
+ * "Measured prototype vs. deployment").  Allocates a staging buffer;
+ * synchronous on the stream.  Errors: FA_E_INVAL (null pointer, a residue
+ * not below its prime), FA_E_SHAPE (limbs, n_polys or capacity), FA_E_NOMEM,
+ * FA_E_HIP. */
+int fa_import_coeffs(fa_ctx* ctx, const uint64_t* coeffs, fa_buf* buf, void* stream);
 /* Encode a real slot vector (host, n_slots <= S values, rest zero) to integer
  * coefficients m_k = rint(2^log_scale * (2/N) * sum_j v_j cos(pi k 5^j / N))
- * (round half to even, float64): host out [N]. */
+ * (round half to even, float64): host out [N] (the client's packing of its
+ * query into slots, Section 2 "What CKKS gives us"). */
 int fa_encode(const fa_ctx* ctx, const double* slots, int n_slots, int log_scale, int64_t* out);
 /* Decode decrypted residues (host [L][N], e.g. from fa_decrypt) at scale
- * 2^log_scale into n_slots real slot values (host).  The centred CRT uses
- * the first primes whose product exceeds 2^(log_scale + 22), which is exact
- * for slot values of magnitude below 2^12 (scores are cosines). */
+ * 2^log_scale into n_slots real slot values (host): the client's reading of
+ * its scores (Section 2 "The round trip").  The centred CRT uses the first
+ * primes whose product exceeds 2^(log_scale + 22), which is exact for slot
+ * values of magnitude below 2^12 (scores are cosines). */
 int fa_decode(const fa_ctx* ctx, const uint64_t* res, int log_scale, double* out, int n_slots);
 
 /* ---- server: enrollment ------------------------------------------------- */
 
 /* Encode a block of candidate rows (host float32 [n_rows][dim], dim <= d,
- * zero-padded to d) into device plaintexts at scale 2^log_scale:
- *   FA_LAYOUT_DIAG: n_rows <= S; d diagonals diag_j[i] = X[i][(i+j) mod d],
- *     diagonal gB+b pre-rotated right by gB, stored g-major: pts[g*B+b];
- *     d % baby_step == 0, d | S.  Writes d plaintexts.
+ * zero-padded to d) into device plaintexts at scale 2^(ctx log_scale):
+ *   FA_LAYOUT_DIAG (Section 2 "Measured prototype vs. deployment": a block of
+ *     n/2 vectors stored as its diagonals; Section 3.1 "Detail": each
+ *     diagonal pre-rotated in plaintext by its giant-step amount): n_rows <= S;
+ *     d diagonals diag_j[i] = X[i][(i+j) mod d], diagonal gB+b pre-rotated
+ *     right by gB, stored g-major: pts[g*B+b]; d % baby_step == 0, d | S.
+ *     Writes d plaintexts.
  *   FA_LAYOUT_ROW: rows packed S/d per plaintext, slot t*d+u = X[w*S/d+t][u];
  *     writes ceil(n_rows / (S/d)) plaintexts (baby_step ignored).
- * pts must hold that many plaintexts (L*N words each). */
+ * pts->bytes must hold that many plaintexts; its descriptor is filled in
+ * (n_polys 1, count, limbs L, log_scale).  Errors: FA_E_SHAPE (d not a power
+ * of two <= S, dim outside [1, d], no rows or more than S rows in a diagonal
+ * block, pts too small), FA_E_INVAL (null pointer, unknown layout, baby step
+ * not dividing d). */
 int fa_encode_db_block(fa_ctx* ctx, const float* rows, int n_rows, int dim, int d, int layout, int baby_step,
-                       void* pts, void* stream);
+                       fa_buf* pts, void* stream);
 /* Plaintexts of a projection W (host float32 [d_in][r], row-major) for
  * fa_project_ct (Section 3.1 "How", "Detail"): the r hybrid diagonals
  * e_j[s] = W[(s+j) mod d_in][s mod r] over all S slots, diagonal gB+b
- * pre-rotated right by gB, stored g-major (pts[g*B+b]), at scale 2^log_scale.
- * d_in and r powers of two, r | d_in, d_in | S, baby_step | r.  Writes r
- * plaintexts. */
-int fa_encode_projection(fa_ctx* ctx, const float* W, int d_in, int r, int baby_step, void* pts, void* stream);
-/* Plaintexts from integer coefficients (host [n_pts][N], |c| < 2^62). */
-int fa_encode_db_block_int(fa_ctx* ctx, const int64_t* coeffs, int n_pts, void* pts, void* stream);
+ * pre-rotated right by gB, stored g-major (pts[g*B+b]), at scale
+ * 2^(ctx log_scale).  d_in and r powers of two, r | d_in, d_in | S,
+ * baby_step | r.  Writes r plaintexts. */
+int fa_encode_projection(fa_ctx* ctx, const float* W, int d_in, int r, int baby_step, fa_buf* pts, void* stream);
+/* Plaintexts from integer coefficients (host [n_pts][N], |c| < 2^62, the
+ * caller's encoding at scale 2^log_scale): the enrollment of the same
+ * diagonal or row layouts from coefficients computed elsewhere (for example
+ * by an independent encoder).  Writes n_pts plaintexts. */
+int fa_encode_db_block_int(fa_ctx* ctx, const int64_t* coeffs, int n_pts, int32_t log_scale, fa_buf* pts,
+                           void* stream);
 
 /* ---- server: scoring ---------------------------------------------------- */
 
@@ -219,106 +282,136 @@ int fa_encode_db_block_int(fa_ctx* ctx, const int64_t* coeffs, int n_pts, void* 
  * = number of ciphertexts. */
 size_t fa_workspace_bytes(const fa_ctx* ctx, int op, int n_blocks, int d, int baby_step);
 
-/* Score one encrypted query q (device ciphertext, slot s = query[s mod d])
- * against n_blocks resident blocks (device pointers blocks[0..n_blocks-1]).
- *   FA_LAYOUT_DIAG_ENC: as FA_LAYOUT_DIAG with every block holding d
- *   ciphertexts ([d][2][L][N], fa_encrypt_pts of a diagonal block): acc_g is
- *   the three-component tensor sum over b, relinearised once per (block, g)
- *   (lazy relinearisation), before the same giant steps.  Needs the
- *   relinearisation key as well.
+/* The stateless scorer of Section 2 "Reproducing this": per request it takes
+ * the encrypted query and a list of group ids, gathers those groups' rows --
+ * here blocks resident in HBM -- and returns their encrypted scores.
+ *   q: one ciphertext (slot s = query[s mod d]) at the context's level;
+ *   blocks[0..n_resident-1]: the resident blocks of this level;
+ *   block_ids[0..n_blocks-1]: the blocks to score, each in [0, n_resident),
+ *     repeats allowed; NULL scores blocks 0..n_blocks-1;
+ *   out: n_blocks ciphertexts, out[j] the scores of block block_ids[j], at
+ *     scale 2^(q log_scale + block log_scale).
+ * Layouts:
  *   FA_LAYOUT_DIAG (Section 3.1 diagonal method, baby step B = baby_step,
  *   G = d/B giant steps): each block holds d pre-rotated plaintexts from
- *   fa_encode_db_block; out receives n_blocks ciphertexts; slot i of output
- *   b is <X_i, q> at the product scale.  Sequence: qrot_b = Rotate(q, b)
- *   (b < B, one shared decomposition); acc_g = sum_b pt[g*B+b] * qrot_b;
- *   out = acc_0 + sum_{g>=1} Rotate(acc_g, gB) with the key-switch products
- *   of all g >= 1 summed over Q u P before one division by P per block.
- *   Needs keys for steps 1..B-1 and g*B, 1 <= g < G.
- *   FA_LAYOUT_ROW: n_blocks row-packed plaintexts; out[w] = q * pt_w (no
- *   rotation; follow with fa_rotate_sum(first_shift=1, n_steps=log2 d)).
+ *   fa_encode_db_block; slot i of out[j] is <X_i, q>.  Sequence:
+ *   qrot_b = Rotate(q, b) (b < B, one shared decomposition);
+ *   acc_g = sum_b pt[g*B+b] * qrot_b; out = acc_0 + sum_{g>=1} Rotate(acc_g, gB)
+ *   with the key-switch products of all g >= 1 summed over Q u P before one
+ *   division by P per block.  Needs keys for steps 1..B-1 and g*B, 1 <= g < G.
+ *   FA_LAYOUT_DIAG_ENC: as FA_LAYOUT_DIAG with every block holding d
+ *   ciphertexts (fa_encrypt_pts of a diagonal block): acc_g is the
+ *   three-component tensor sum over b, relinearised once per (block, g)
+ *   (lazy relinearisation), before the same giant steps.  Needs the
+ *   relinearisation key as well.
+ *   FA_LAYOUT_ROW: each block holds row-packed plaintexts, of which the first
+ *   is used; out[j] = q * pt (no rotation; follow with
+ *   fa_rotate_sum(first_shift=1, n_steps=log2 d)).
  * ws: device workspace of ws_bytes >= fa_workspace_bytes(...).
- * Errors: FA_E_SHAPE if n_blocks < 1 (checked first: an empty list of blocks
- * is a shape error, whatever the pointer) or d is not a power of two <= N/2;
- * FA_E_INVAL for a null pointer or a baby step not dividing d; FA_E_NOKEY /
- * FA_E_NOMEM for a missing key or a short workspace. */
-int fa_score_block(fa_ctx* ctx, const void* q, const void* const* blocks, int n_blocks, int d, int layout,
-                   int baby_step, void* out, void* ws, size_t ws_bytes, void* stream);
+ * Errors: FA_E_SHAPE if n_blocks < 1 (checked first: an empty request is a
+ * shape error, whatever the pointers), if d is not a power of two <= N/2, if
+ * q is not one ciphertext at the context's level, if a scored block is at
+ * another level, holds the wrong kind or fewer than d objects, if the scored
+ * blocks are not all at one scale, if the product scale exceeds
+ * 2^(log2 Q - 8) (the scores would wrap modulo Q), or if out cannot hold
+ * n_blocks ciphertexts; FA_E_INVAL for a null pointer, an unknown layout, a
+ * block id outside [0, n_resident) or a baby step not dividing d;
+ * FA_E_NOKEY / FA_E_NOMEM for a missing key or a short workspace. */
+int fa_score_block(fa_ctx* ctx, const fa_buf* q, const fa_buf* blocks, int n_resident, const int32_t* block_ids,
+                   int n_blocks, int d, int layout, int baby_step, fa_buf* out, void* ws, size_t ws_bytes,
+                   void* stream);
 
 /* The same diagonal-layout scoring split in two, so that one query's baby
  * rotations serve several levels or batches (the paper projects the query
  * once and reuses it across batches, Section 3.4):
  *   fa_prepare_query writes Rotate(q, b), b = 1..baby_step-1, into prep
- *     (device, fa_prepared_words(ctx, baby_step) words);
- *   fa_score_prepared then scores q against n_blocks blocks exactly as
- *     fa_score_block with FA_LAYOUT_DIAG does (bit-identical output).
+ *     (device, fa_prepared_bytes(ctx, baby_step) bytes; its descriptor gets
+ *     n_polys 2, count baby_step-1, the query's level and scale);
+ *   fa_score_prepared then scores q against blocks exactly as fa_score_block
+ *     with FA_LAYOUT_DIAG does (bit-identical output); FA_E_SHAPE if prep
+ *     does not hold baby_step-1 rotations at q's level and scale.
  * Workspace: FA_OP_PREPARE (baby_step) and FA_OP_SCORE_PREPARED (n_blocks,
  * d, baby_step). */
-size_t fa_prepared_words(const fa_ctx* ctx, int baby_step);
-int fa_prepare_query(fa_ctx* ctx, const void* q, int baby_step, void* prep, void* ws, size_t ws_bytes,
+size_t fa_prepared_bytes(const fa_ctx* ctx, int baby_step);
+int fa_prepare_query(fa_ctx* ctx, const fa_buf* q, int baby_step, fa_buf* prep, void* ws, size_t ws_bytes,
                      void* stream);
-int fa_score_prepared(fa_ctx* ctx, const void* q, const void* prep, const void* const* blocks, int n_blocks, int d,
-                      int baby_step, void* out, void* ws, size_t ws_bytes, void* stream);
+int fa_score_prepared(fa_ctx* ctx, const fa_buf* q, const fa_buf* prep, const fa_buf* blocks, int n_resident,
+                      const int32_t* block_ids, int n_blocks, int d, int baby_step, fa_buf* out, void* ws,
+                      size_t ws_bytes, void* stream);
 
-/* Several queries prepared together (the same cross-query batching applied
- * to the baby rotations): preps[j] receives exactly what
- * fa_prepare_query(qs[j], baby_step) writes, for j < n_q.  The key switches
- * of one baby step are issued for all n_q queries together, so a rotation
- * key read from HBM for one query is found in the caches by the others.
- * qs[j] device ciphertexts, preps[j] device, fa_prepared_words(ctx,
- * baby_step) words each; workspace fa_prepare_batch_workspace_bytes(n_q,
- * baby_step) bytes (it grows with n_q: every query's extended digits).
- * Errors: FA_E_INVAL (null pointer, baby_step out of range), FA_E_SHAPE
- * (n_q < 1), FA_E_NOKEY (a baby-step key is missing), FA_E_NOMEM (workspace
- * too small). */
+/* Several queries prepared together (the cross-query batching of "Conclusion
+ * and Future Work" applied to the baby rotations): preps[j] receives exactly
+ * what fa_prepare_query(qs[j], baby_step) writes, for j < n_q.  The key
+ * switches of one baby step are issued for the queries of a group together
+ * (groups of at most 16 queries), so a rotation key read from HBM for one
+ * query is found in the caches by the others.  qs[j] device ciphertexts,
+ * preps[j] device, fa_prepared_bytes(ctx, baby_step) bytes each; workspace
+ * fa_prepare_batch_workspace_bytes(n_q, baby_step) bytes (it grows with the
+ * group size: every query's extended digits).  Errors: FA_E_INVAL (null
+ * pointer, baby_step out of range), FA_E_SHAPE (n_q < 1, a query not one
+ * ciphertext at the context's level, a prepared buffer too small),
+ * FA_E_NOKEY (a baby-step key is missing), FA_E_NOMEM (workspace too
+ * small). */
 size_t fa_prepare_batch_workspace_bytes(const fa_ctx* ctx, int n_q, int baby_step);
-int fa_prepare_batch(fa_ctx* ctx, const void* const* qs, int n_q, int baby_step, void* const* preps, void* ws,
+int fa_prepare_batch(fa_ctx* ctx, const fa_buf* qs, int n_q, int baby_step, fa_buf* preps, void* ws,
                      size_t ws_bytes, void* stream);
 
-/* Cross-query batching against resident blocks (section "Conclusion and
- * Future Work": score a batch of queries per loaded region so that the load
- * is paid once per batch): n_q queries,
- * each prepared with fa_prepare_query (qs[j] the query ciphertext, preps[j]
- * its baby rotations), scored against the same n_blocks blocks.  Each pass
- * over the plaintexts serves up to four queries, so the plaintext stream is
- * read once per four queries instead of once per query.  outs[j] (device,
+/* Cross-query batching against resident blocks ("Conclusion and Future
+ * Work": score a batch of queries per loaded region so that the load is paid
+ * once per batch): n_q queries, each prepared with fa_prepare_query (qs[j]
+ * the query ciphertext, preps[j] its baby rotations), scored against the
+ * same blocks (blocks / n_resident / block_ids as in fa_score_block).  Each
+ * pass over the plaintexts serves up to four queries, so the plaintext stream
+ * is read once per four queries instead of once per query.  outs[j] (device,
  * n_blocks ciphertexts) is bit-identical to fa_score_prepared(qs[j],
  * preps[j], ...).  Workspace: fa_batch_workspace_bytes(n_q, n_blocks, d,
  * baby_step) bytes (the accumulators of all n_q queries plus one query's
  * giant-step scratch).  Errors as fa_score_prepared; FA_E_SHAPE if n_q < 1. */
 size_t fa_batch_workspace_bytes(const fa_ctx* ctx, int n_q, int n_blocks, int d, int baby_step);
-int fa_score_batch(fa_ctx* ctx, const void* const* qs, const void* const* preps, int n_q,
-                   const void* const* blocks, int n_blocks, int d, int baby_step, void* const* outs, void* ws,
-                   size_t ws_bytes, void* stream);
+int fa_score_batch(fa_ctx* ctx, const fa_buf* qs, const fa_buf* preps, int n_q, const fa_buf* blocks,
+                   int n_resident, const int32_t* block_ids, int n_blocks, int d, int baby_step, fa_buf* outs,
+                   void* ws, size_t ws_bytes, void* stream);
 
-/* Encrypted projection q_R = W^T q (Section 3.1): q holds a d_in-periodic
- * query, w_pts the r plaintexts of W's hybrid diagonals
- * e_j[s] = W[(s+j) mod d_in][s mod r] (j < r), encoded by the caller as a
- * FA_LAYOUT_DIAG block (pre-rotated, g-major, baby step B).  Runs the same
- * baby-step/giant-step product, then folds: z += Rotate(z, r*2^k) for
- * k < log2(d_in/r).  Output slot s = (W^T q)[s mod r].  Needs keys 1..B-1,
- * g*B, and r*2^k. */
-int fa_project_ct(fa_ctx* ctx, const void* q, const void* w_pts, int d_in, int r, int baby_step, void* q_r,
+/* Encrypted projection q_R = W^T q (Section 3.1 "How"): q holds one
+ * d_in-periodic query ciphertext, w_pts the r plaintexts of W's hybrid
+ * diagonals e_j[s] = W[(s+j) mod d_in][s mod r] (j < r), encoded as a
+ * FA_LAYOUT_DIAG block (pre-rotated, g-major, baby step B; Section 3.1
+ * "Detail").  Runs the same baby-step/giant-step product, then one final
+ * fold: z += Rotate(z, r*2^k) for k < log2(d_in/r).  Output slot
+ * s = (W^T q)[s mod r], at scale 2^(q log_scale + w log_scale).  Needs keys
+ * 1..B-1, g*B, and r*2^k.  Errors: FA_E_SHAPE (d_in, r not powers of two
+ * with r <= d_in <= N/2; q or w_pts at another level, of the wrong kind, w_pts
+ * holding fewer than r plaintexts; the product scale above 2^(log2 Q - 8);
+ * q_r too small), FA_E_INVAL (null pointer, baby step not dividing r),
+ * FA_E_NOKEY, FA_E_NOMEM. */
+int fa_project_ct(fa_ctx* ctx, const fa_buf* q, const fa_buf* w_pts, int d_in, int r, int baby_step, fa_buf* q_r,
                   void* ws, size_t ws_bytes, void* stream);
 
-/* The projection with W itself encrypted (Section 3.1: the server holds the
- * projection's diagonals as ciphertexts).  w_cts holds r ciphertexts
- * ([r][2][L][N], fa_encrypt_pts of the plaintexts fa_project_ct takes);
- * each giant step's three-component tensor sum is relinearised once, as for
- * FA_LAYOUT_DIAG_ENC blocks, before the same giant steps and fold.  Output
- * slot s = (W^T q)[s mod r] at the product of the two scales.  Needs the keys
+/* The projection with W itself encrypted (Section 3.1 "How": the server holds
+ * the projection's diagonals as ciphertexts).  w_cts holds r ciphertexts
+ * (fa_encrypt_pts of the plaintexts fa_project_ct takes); each giant step's
+ * three-component tensor sum is relinearised once, as for FA_LAYOUT_DIAG_ENC
+ * blocks, before the same giant steps and fold.  Output slot
+ * s = (W^T q)[s mod r] at the product of the two scales.  Needs the keys
  * fa_project_ct needs and the relinearisation key (FA_E_NOKEY otherwise).
  * Workspace: fa_workspace_bytes(FA_OP_PROJECT_ENC, 1, r, baby_step).  Other
  * errors as fa_project_ct. */
-int fa_project_ct_enc(fa_ctx* ctx, const void* q, const void* w_cts, int d_in, int r, int baby_step, void* q_r,
-                      void* ws, size_t ws_bytes, void* stream);
+int fa_project_ct_enc(fa_ctx* ctx, const fa_buf* q, const fa_buf* w_cts, int d_in, int r, int baby_step,
+                      fa_buf* q_r, void* ws, size_t ws_bytes, void* stream);
 
-/* In place, for each of n_cts consecutive ciphertexts in cts:
- * ct <- ct + Rotate(ct, first_shift * 2^k) for k = 0..n_steps-1. */
-int fa_rotate_sum(fa_ctx* ctx, void* cts, int n_cts, int first_shift, int n_steps, void* ws, size_t ws_bytes,
-                  void* stream);
+/* The rotate-and-sum fold (Section 3.1 "Detail": one final fold after the
+ * diagonal product; the row-packed scoring sums a row's slots the same way):
+ * in place, for each of the cts->count ciphertexts of cts,
+ * ct <- ct + Rotate(ct, first_shift * 2^k) for k = 0..n_steps-1.  Errors:
+ * FA_E_SHAPE (cts not ciphertexts at the context's level), FA_E_INVAL (null
+ * pointer, a shift out of [1, N/2)), FA_E_NOKEY, FA_E_NOMEM. */
+int fa_rotate_sum(fa_ctx* ctx, fa_buf* cts, int first_shift, int n_steps, void* ws, size_t ws_bytes, void* stream);
 
-/* out = Rotate(ct, step) (one full key switch). */
-int fa_rotate(fa_ctx* ctx, const void* ct, int step, void* out, void* ws, size_t ws_bytes, void* stream);
+/* out = Rotate(ct, step): one full key switch of the first ciphertext of ct
+ * (Section 2 "What CKKS gives us": rotating the packed vector).  out must not
+ * overlap ct (FA_E_INVAL): the key-switch finish reads ct through the
+ * automorphism while it writes out. */
+int fa_rotate(fa_ctx* ctx, const fa_buf* ct, int step, fa_buf* out, void* ws, size_t ws_bytes, void* stream);
 
 /* ---- the membership (threshold) path ------------------------------------
  * Section 3.1 ("Membership search"): the server returns an encrypted yes/no
@@ -328,9 +421,10 @@ int fa_rotate(fa_ctx* ctx, const void* ct, int step, void* out, void* ws, size_t
  * on a chain of contexts, levels[0] with L primes and each next one the
  * previous minus its last ciphertext prime (fa_ctx_create_level), every one
  * holding the relinearisation key.  A ciphertext's level is its number of
- * primes; its scale (a double) is tracked by the caller and returned by the
- * polynomial calls.  Products are relinearised and rescaled by the last prime
- * of their level (scale sa*sb/q); constants are integers. */
+ * primes and its scale is a double (after rescaling it is no power of two),
+ * both passed explicitly, so these calls take plain device pointers instead
+ * of fa_buf descriptors.  Products are relinearised and rescaled by the last
+ * prime of their level (scale sa*sb/q); constants are integers. */
 
 /* Rescale n_polys polynomials of ct ([n_polys][L][N] at hi) by hi's last
  * prime: out ([n_polys][L-1][N], lo's layout) = round(ct / q_last), the

@@ -264,6 +264,99 @@ static int dev_alloc(T** p, size_t count) {
   return FA_OK;
 }
 
+// ---------------------------------------------------------------------------
+// buffer descriptors: every check runs on the host before anything is enqueued
+// ---------------------------------------------------------------------------
+static size_t obj_bytes(const fa_ctx* c, uint32_t n_polys) { return (size_t)n_polys * c->L * c->n * 8; }
+
+static const char* kind_name(uint32_t n_polys) {
+  return n_polys == 1 ? "plaintexts" : n_polys == 2 ? "ciphertexts" : "objects";
+}
+
+// An input buffer: at least min_count objects of n_polys polynomials at the
+// context's level, its capacity covering its contents.
+static int in_check(const fa_ctx* c, const fa_buf* b, const char* fn, const char* what, uint32_t n_polys,
+                    uint32_t min_count) {
+  if (!b || !b->dev) return fail(FA_E_INVAL, "%s: %s is null", fn, what);
+  if (b->n_polys != n_polys)
+    return fail(FA_E_SHAPE, "%s: %s holds %u polynomials per object, the call takes %s (%u)", fn, what, b->n_polys,
+                kind_name(n_polys), n_polys);
+  if ((int)b->limbs != c->L)
+    return fail(FA_E_SHAPE, "%s: %s is at %u primes, the context at %d", fn, what, b->limbs, c->L);
+  if (b->count < min_count) return fail(FA_E_SHAPE, "%s: %s holds %u %s, at least %u needed", fn, what, b->count,
+                                        kind_name(n_polys), min_count);
+  if (b->bytes < (size_t)b->count * obj_bytes(c, n_polys))
+    return fail(FA_E_SHAPE, "%s: %s claims %u objects in %zu bytes", fn, what, b->count, b->bytes);
+  return FA_OK;
+}
+
+// An output buffer: room for `objects` objects of n_polys polynomials.
+static int out_check(const fa_ctx* c, const fa_buf* b, const char* fn, const char* what, size_t objects,
+                     uint32_t n_polys) {
+  if (!b || !b->dev) return fail(FA_E_INVAL, "%s: %s is null", fn, what);
+  if (b->bytes < objects * obj_bytes(c, n_polys))
+    return fail(FA_E_SHAPE, "%s: %s has %zu bytes, %zu %s need %zu", fn, what, b->bytes, objects,
+                kind_name(n_polys), objects * obj_bytes(c, n_polys));
+  return FA_OK;
+}
+
+static void out_set(const fa_ctx* c, fa_buf* b, uint32_t n_polys, size_t count, int32_t log_scale) {
+  b->n_polys = n_polys;
+  b->count = (uint32_t)count;
+  b->limbs = (uint32_t)c->L;
+  b->log_scale = log_scale;
+}
+
+// log2 of the ciphertext modulus Q
+static double log2_q(const fa_ctx* c) {
+  double v = 0.0;
+  for (int t = 0; t < c->L; ++t) v += std::log2((double)c->primes[t]);
+  return v;
+}
+
+// A product's scale must leave room below Q/2 for values of magnitude up to
+// 2^7 (sums of d products of unit entries, plus noise), else it wraps mod Q.
+static int scale_check(const fa_ctx* c, const char* fn, long log_scale) {
+  if (log_scale < 0 || (double)log_scale > log2_q(c) - 8.0)
+    return fail(FA_E_SHAPE, "%s: the product scale 2^%ld does not fit below Q = 2^%.1f with 8 bits to spare", fn,
+                log_scale, log2_q(c));
+  return FA_OK;
+}
+
+static bool overlap(const fa_buf* a, const fa_buf* b) {
+  const char* a0 = (const char*)a->dev;
+  const char* b0 = (const char*)b->dev;
+  return a0 < b0 + b->bytes && b0 < a0 + a->bytes;
+}
+
+// The blocks a scoring request names: ids[j] (or j when ids is null) among the
+// n_resident resident blocks, each holding at least min_count objects of
+// n_polys polynomials at the context's level, all at one scale.
+static int gather_blocks(const fa_ctx* c, const char* fn, const fa_buf* blocks, int n_resident, const int32_t* ids,
+                         int n_blocks, uint32_t n_polys, uint32_t min_count, std::vector<const double*>& ptrs,
+                         int32_t* log_scale) {
+  if (n_blocks < 1) return fail(FA_E_SHAPE, "%s: n_blocks must be positive", fn);
+  if (!blocks) return fail(FA_E_INVAL, "%s: null block list", fn);
+  if (n_resident < 1) return fail(FA_E_SHAPE, "%s: n_resident must be positive", fn);
+  if (!ids && n_blocks > n_resident)
+    return fail(FA_E_SHAPE, "%s: %d blocks requested without ids from %d resident", fn, n_blocks, n_resident);
+  ptrs.resize(n_blocks);
+  for (int j = 0; j < n_blocks; ++j) {
+    const int id = ids ? ids[j] : j;
+    if (id < 0 || id >= n_resident) return fail(FA_E_INVAL, "%s: block id %d outside [0, %d)", fn, id, n_resident);
+    char what[48];
+    snprintf(what, sizeof what, "block %d", id);
+    int rc = in_check(c, &blocks[id], fn, what, n_polys, min_count);
+    if (rc) return rc;
+    if (j == 0) *log_scale = blocks[id].log_scale;
+    else if (blocks[id].log_scale != *log_scale)
+      return fail(FA_E_SHAPE, "%s: block %d is at scale 2^%d, block %d at 2^%d", fn, id, blocks[id].log_scale,
+                  ids ? ids[0] : 0, *log_scale);
+    ptrs[j] = (const double*)blocks[id].dev;
+  }
+  return FA_OK;
+}
+
 extern "C" {
 
 const char* fa_last_error(void) { return g_err.c_str(); }
@@ -441,16 +534,37 @@ int fa_ctx_create(const fa_params* prm, fa_ctx** out) {
   if (prm->log_n < 10 || prm->log_n > 16) return fail(FA_E_INVAL, "log_n must be in [10, 16], got %u", prm->log_n);
   if (prm->L < 1 || prm->L > 16) return fail(FA_E_INVAL, "L must be in [1, 16], got %u", prm->L);
   if (prm->K < 1 || prm->K > 4) return fail(FA_E_INVAL, "K must be in [1, 4], got %u", prm->K);
+  // the key-switch kernels are instantiated for 1..8 digits
+  if ((prm->L + prm->K - 1) / prm->K > 8)
+    return fail(FA_E_INVAL, "L=%u, K=%u gives %u key-switch digits; at most 8 are supported", prm->L, prm->K,
+                (prm->L + prm->K - 1) / prm->K);
   if (prm->log_scale < 1 || prm->log_scale > 60) return fail(FA_E_INVAL, "log_scale must be in [1, 60]");
-  std::vector<u64> primes = select_primes((int)prm->log_n, (int)(prm->L + prm->K));
-  if (primes.size() != prm->L + prm->K) return fail(FA_E_INVAL, "not enough 50-bit NTT primes");
+  const int np = (int)(prm->L + prm->K);
+  std::vector<u64> primes;
+  if (prm->primes) {
+    // explicit primes: the residue arithmetic needs them in (2^49, 2^50), the
+    // negacyclic transform needs 2N | q - 1, and the CRT needs them distinct
+    const u64 m = 2ull << prm->log_n;
+    for (int t = 0; t < np; ++t) {
+      const u64 q = prm->primes[t];
+      if (q <= (1ull << 49) || q >= (1ull << 50)) return fail(FA_E_INVAL, "prime %d = %llu is not in (2^49, 2^50)", t, (unsigned long long)q);
+      if (q % m != 1) return fail(FA_E_INVAL, "prime %d = %llu is not 1 mod 2N", t, (unsigned long long)q);
+      if (!is_prime(q)) return fail(FA_E_INVAL, "%llu (entry %d) is not prime", (unsigned long long)q, t);
+      for (int u = 0; u < t; ++u)
+        if (prm->primes[u] == q) return fail(FA_E_INVAL, "prime %llu is listed twice", (unsigned long long)q);
+      primes.push_back(q);
+    }
+  } else {
+    primes = select_primes((int)prm->log_n, np);
+    if ((int)primes.size() != np) return fail(FA_E_INVAL, "not enough 50-bit NTT primes");
+  }
   return ctx_build(prm, primes, out);
 }
 
 int fa_ctx_create_level(const fa_ctx* parent, uint32_t L_low, fa_ctx** out) {
   if (!parent || !out) return fail(FA_E_INVAL, "fa_ctx_create_level: null argument");
   if (L_low < 1 || (int)L_low > parent->L) return fail(FA_E_INVAL, "L_low=%u must be in [1, %d]", L_low, parent->L);
-  const fa_params prm{(uint32_t)parent->logn, L_low, (uint32_t)parent->K, (uint32_t)parent->log_scale};
+  const fa_params prm{(uint32_t)parent->logn, L_low, (uint32_t)parent->K, (uint32_t)parent->log_scale, nullptr};
   std::vector<u64> primes(parent->primes.begin(), parent->primes.begin() + L_low);
   primes.insert(primes.end(), parent->primes.begin() + parent->L, parent->primes.end());
   fa_ctx* c = nullptr;
@@ -490,16 +604,21 @@ int fa_ctx_create_level(const fa_ctx* parent, uint32_t L_low, fa_ctx** out) {
   return FA_OK;
 }
 
-int fa_drop_level(const fa_ctx* parent, const fa_ctx* child, const void* ct, void* out, void* stream) {
-  if (!parent || !child || !ct || !out) return fail(FA_E_INVAL, "fa_drop_level: null argument");
+int fa_drop_level(const fa_ctx* parent, const fa_ctx* child, const fa_buf* ct, fa_buf* out, void* stream) {
+  if (!parent || !child) return fail(FA_E_INVAL, "fa_drop_level: null context");
   if (child->n != parent->n || child->L > parent->L) return fail(FA_E_SHAPE, "fa_drop_level: not a lower level");
   for (int t = 0; t < child->L; ++t)
     if (child->primes[t] != parent->primes[t]) return fail(FA_E_SHAPE, "fa_drop_level: prime %d differs", t);
+  int rc = in_check(parent, ct, "fa_drop_level", "ct", 2, 1);
+  if (rc || (rc = out_check(child, out, "fa_drop_level", "out", ct->count, 2))) return rc;
   const size_t n = parent->n;
   hipStream_t s = (hipStream_t)stream;
-  for (int h = 0; h < 2; ++h)
-    HIPCHK(hipMemcpyAsync((double*)out + (size_t)h * child->L * n, (const double*)ct + (size_t)h * parent->L * n,
-                          (size_t)child->L * n * 8, hipMemcpyDeviceToDevice, s));
+  for (uint32_t j = 0; j < ct->count; ++j)
+    for (int h = 0; h < 2; ++h)
+      HIPCHK(hipMemcpyAsync((double*)out->dev + ((size_t)2 * j + h) * child->L * n,
+                            (const double*)ct->dev + ((size_t)2 * j + h) * parent->L * n, (size_t)child->L * n * 8,
+                            hipMemcpyDeviceToDevice, s));
+  out_set(child, out, 2, ct->count, ct->log_scale);
   return FA_OK;
 }
 
@@ -508,8 +627,8 @@ int fa_ctx_primes(const fa_ctx* c, uint64_t* out) {
   std::copy(c->primes.begin(), c->primes.end(), out);
   return FA_OK;
 }
-size_t fa_ct_words(const fa_ctx* c) { return c ? (size_t)2 * c->L * c->n : 0; }
-size_t fa_pt_words(const fa_ctx* c) { return c ? (size_t)c->L * c->n : 0; }
+size_t fa_ct_bytes(const fa_ctx* c) { return c ? obj_bytes(c, 2) : 0; }
+size_t fa_pt_bytes(const fa_ctx* c) { return c ? obj_bytes(c, 1) : 0; }
 size_t fa_key_bytes(const fa_ctx* c) { return c ? (size_t)c->dnum * 2 * c->np * c->n * 8 : 0; }
 
 // ---------------------------------------------------------------------------
@@ -626,8 +745,12 @@ int fa_keygen_relin(fa_ctx* c, const int64_t* s, const uint64_t* a, const int64_
 int fa_has_relin_key(const fa_ctx* c) { return c && c->d_rlk ? 1 : 0; }
 
 
-int fa_encrypt(fa_ctx* c, const int64_t* m, const uint64_t* a, const int64_t* e, void* ct, void* stream) {
-  if (!c || !m || !a || !e || !ct) return fail(FA_E_INVAL, "fa_encrypt: null argument");
+int fa_encrypt(fa_ctx* c, const int64_t* m, int32_t log_scale, const uint64_t* a, const int64_t* e, fa_buf* ct,
+               void* stream) {
+  if (!c || !m || !a || !e) return fail(FA_E_INVAL, "fa_encrypt: null argument");
+  int rc0 = out_check(c, ct, "fa_encrypt", "ct", 1, 2);
+  if (rc0) return rc0;
+  if (log_scale < 0 || log_scale > 1000) return fail(FA_E_INVAL, "fa_encrypt: log_scale %d out of range", log_scale);
   hipStream_t s = (hipStream_t)stream;
   const size_t n = c->n, L = c->L;
   for (size_t k = 0; k < n; ++k)
@@ -644,7 +767,7 @@ int fa_encrypt(fa_ctx* c, const int64_t* m, const uint64_t* a, const int64_t* e,
     (void)hipFree(dm);
     return rc;
   }
-  double* dct = (double*)ct;
+  double* dct = (double*)ct->dev;
   HIPCHK(hipMemcpyAsync(du, a, L * n * 8, hipMemcpyHostToDevice, s));
   HIPCHK(hipMemcpyAsync(dm, me.data(), n * 8, hipMemcpyHostToDevice, s));
   fa::u64_to_res(du, L * n, dct + L * n, s);
@@ -657,13 +780,18 @@ int fa_encrypt(fa_ctx* c, const int64_t* m, const uint64_t* a, const int64_t* e,
   (void)hipFree(du);
   (void)hipFree(dm);
   (void)hipFree(dv);
+  out_set(c, ct, 2, 1, log_scale);
   return FA_OK;
 }
 
-int fa_encrypt_pts(fa_ctx* c, const void* pts, int n_pts, const uint64_t* a, const int64_t* e, void* cts,
+int fa_encrypt_pts(fa_ctx* c, const fa_buf* pts_b, const uint64_t* a, const int64_t* e, fa_buf* cts_b,
                    void* stream) {
-  if (!c || !pts || !a || !e || !cts) return fail(FA_E_INVAL, "fa_encrypt_pts: null argument");
-  if (n_pts < 1) return fail(FA_E_SHAPE, "n_pts must be positive");
+  if (!c || !a || !e) return fail(FA_E_INVAL, "fa_encrypt_pts: null argument");
+  int rc0 = in_check(c, pts_b, "fa_encrypt_pts", "pts", 1, 1);
+  if (rc0 || (rc0 = out_check(c, cts_b, "fa_encrypt_pts", "cts", pts_b->count, 2))) return rc0;
+  const int n_pts = (int)pts_b->count;
+  const void* pts = pts_b->dev;
+  void* cts = cts_b->dev;
   hipStream_t s = (hipStream_t)stream;
   const size_t n = c->n, L = c->L;
   for (size_t k = 0; k < (size_t)n_pts * n; ++k)
@@ -704,6 +832,7 @@ int fa_encrypt_pts(fa_ctx* c, const void* pts, int n_pts, const uint64_t* a, con
   (void)hipFree(de);
   (void)hipFree(dv);
   if (!rc && he != hipSuccess) rc = fail(FA_E_HIP, "fa_encrypt_pts: %s", hipGetErrorString(he));
+  if (!rc) out_set(c, cts_b, 2, n_pts, pts_b->log_scale);
   return rc;
 }
 
@@ -738,13 +867,20 @@ static int export_polys(fa_ctx* c, const double* src, int n_polys, uint64_t* out
   return FA_OK;
 }
 
-int fa_decrypt(fa_ctx* c, const void* ct, uint64_t* out, void* stream) {
-  if (!c || !ct || !out) return fail(FA_E_INVAL, "fa_decrypt: null argument");
-  return export_polys(c, (const double*)ct, 1, out, (hipStream_t)stream, true);
+int fa_decrypt(fa_ctx* c, const fa_buf* ct, uint64_t* out, void* stream) {
+  if (!c || !out) return fail(FA_E_INVAL, "fa_decrypt: null argument");
+  int rc = in_check(c, ct, "fa_decrypt", "ct", 2, 1);
+  if (rc) return rc;
+  return export_polys(c, (const double*)ct->dev, 1, out, (hipStream_t)stream, true);
 }
 
-int fa_import_coeffs(fa_ctx* c, const uint64_t* coeffs, int n_polys, void* buf, void* stream) {
-  if (!c || !coeffs || !buf || n_polys < 1) return fail(FA_E_INVAL, "fa_import_coeffs: bad argument");
+int fa_import_coeffs(fa_ctx* c, const uint64_t* coeffs, fa_buf* buf, void* stream) {
+  if (!c || !coeffs || !buf || !buf->dev) return fail(FA_E_INVAL, "fa_import_coeffs: null argument");
+  if (buf->n_polys < 1 || buf->n_polys > 3 || buf->count < 1)
+    return fail(FA_E_SHAPE, "fa_import_coeffs: %u objects of %u polynomials", buf->count, buf->n_polys);
+  int rc0 = in_check(c, buf, "fa_import_coeffs", "buf", buf->n_polys, 1);
+  if (rc0) return rc0;
+  const int n_polys = (int)(buf->n_polys * buf->count);
   const size_t n = c->n, L = c->L;
   for (size_t p = 0; p < (size_t)n_polys; ++p)
     for (size_t t = 0; t < L; ++t) {
@@ -759,7 +895,7 @@ int fa_import_coeffs(fa_ctx* c, const uint64_t* coeffs, int n_polys, void* buf, 
   uint64_t* du = nullptr;
   int rc = dev_alloc(&du, (size_t)std::min(chunk, n_polys) * L * n);
   if (rc) return rc;
-  double* dst = (double*)buf;
+  double* dst = (double*)buf->dev;
   for (int p0 = 0; p0 < n_polys && !rc; p0 += chunk) {
     const int m = std::min(chunk, n_polys - p0);
     const size_t words = (size_t)m * L * n;
@@ -779,9 +915,13 @@ int fa_import_coeffs(fa_ctx* c, const uint64_t* coeffs, int n_polys, void* buf, 
   return rc;
 }
 
-int fa_export_coeffs(fa_ctx* c, const void* buf, int n_polys, uint64_t* out, void* stream) {
-  if (!c || !buf || !out || n_polys < 1) return fail(FA_E_INVAL, "fa_export_coeffs: bad argument");
-  return export_polys(c, (const double*)buf, n_polys, out, (hipStream_t)stream, false);
+int fa_export_coeffs(fa_ctx* c, const fa_buf* buf, uint64_t* out, void* stream) {
+  if (!c || !buf || !out) return fail(FA_E_INVAL, "fa_export_coeffs: null argument");
+  if (buf->n_polys < 1 || buf->n_polys > 3 || buf->count < 1)
+    return fail(FA_E_SHAPE, "fa_export_coeffs: %u objects of %u polynomials", buf->count, buf->n_polys);
+  int rc = in_check(c, buf, "fa_export_coeffs", "buf", buf->n_polys, 1);
+  if (rc) return rc;
+  return export_polys(c, (const double*)buf->dev, (int)(buf->n_polys * buf->count), out, (hipStream_t)stream, false);
 }
 
 // ---------------------------------------------------------------------------
@@ -990,17 +1130,24 @@ static int upload_int_pts(fa_ctx* c, const int64_t* coeffs, int n_pts, double* p
   return rc;
 }
 
-int fa_encode_db_block_int(fa_ctx* c, const int64_t* coeffs, int n_pts, void* pts, void* stream) {
-  if (!c || !coeffs || !pts || n_pts < 1) return fail(FA_E_INVAL, "fa_encode_db_block_int: bad argument");
+int fa_encode_db_block_int(fa_ctx* c, const int64_t* coeffs, int n_pts, int32_t log_scale, fa_buf* pts,
+                           void* stream) {
+  if (!c || !coeffs) return fail(FA_E_INVAL, "fa_encode_db_block_int: null argument");
+  if (n_pts < 1) return fail(FA_E_SHAPE, "fa_encode_db_block_int: n_pts must be positive");
+  if (log_scale < 0 || log_scale > 1000) return fail(FA_E_INVAL, "fa_encode_db_block_int: log_scale out of range");
+  int rc = out_check(c, pts, "fa_encode_db_block_int", "pts", n_pts, 1);
+  if (rc) return rc;
   for (size_t i = 0; i < (size_t)n_pts * c->n; ++i)
     if (coeffs[i] > (INT64_C(1) << 62) || coeffs[i] < -(INT64_C(1) << 62))
       return fail(FA_E_INVAL, "fa_encode_db_block_int: coefficient out of range");
-  return upload_int_pts(c, coeffs, n_pts, (double*)pts, (hipStream_t)stream);
+  rc = upload_int_pts(c, coeffs, n_pts, (double*)pts->dev, (hipStream_t)stream);
+  if (!rc) out_set(c, pts, 1, n_pts, log_scale);
+  return rc;
 }
 
 int fa_encode_db_block(fa_ctx* c, const float* rows, int n_rows, int dim, int d, int layout, int baby_step,
-                       void* pts, void* stream) {
-  if (!c || !rows || !pts) return fail(FA_E_INVAL, "fa_encode_db_block: null argument");
+                       fa_buf* pts_b, void* stream) {
+  if (!c || !rows || !pts_b || !pts_b->dev) return fail(FA_E_INVAL, "fa_encode_db_block: null argument");
   const int S = c->n / 2;
   if (d < 1 || (d & (d - 1)) || d > S) return fail(FA_E_SHAPE, "d=%d must be a power of two <= N/2", d);
   if (dim < 1 || dim > d) return fail(FA_E_SHAPE, "dim=%d must be in [1, d=%d]", dim, d);
@@ -1013,6 +1160,7 @@ int fa_encode_db_block(fa_ctx* c, const float* rows, int n_rows, int dim, int d,
     if (n_rows > S) return fail(FA_E_SHAPE, "a diagonal block holds at most N/2=%d rows, got %d", S, n_rows);
     if (baby_step < 1 || d % baby_step) return fail(FA_E_INVAL, "baby_step %d must divide d=%d", baby_step, d);
     n_pts = d;
+    if (int rc = out_check(c, pts_b, "fa_encode_db_block", "pts", n_pts, 1)) return rc;
     coeffs.assign((size_t)n_pts * c->n, 0);
     parallel_for(n_pts, [&](int j) {
       const int g = j / baby_step;
@@ -1028,6 +1176,7 @@ int fa_encode_db_block(fa_ctx* c, const float* rows, int n_rows, int dim, int d,
   } else if (layout == FA_LAYOUT_ROW) {
     const int per = S / d;
     n_pts = (n_rows + per - 1) / per;
+    if (int rc = out_check(c, pts_b, "fa_encode_db_block", "pts", n_pts, 1)) return rc;
     coeffs.assign((size_t)n_pts * c->n, 0);
     parallel_for(n_pts, [&](int w) {
       std::vector<double> v(S, 0.0);
@@ -1041,15 +1190,18 @@ int fa_encode_db_block(fa_ctx* c, const float* rows, int n_rows, int dim, int d,
   } else {
     return fail(FA_E_INVAL, "unknown layout %d", layout);
   }
-  return upload_int_pts(c, coeffs.data(), n_pts, (double*)pts, (hipStream_t)stream);
+  const int rc = upload_int_pts(c, coeffs.data(), n_pts, (double*)pts_b->dev, (hipStream_t)stream);
+  if (!rc) out_set(c, pts_b, 1, n_pts, c->log_scale);
+  return rc;
 }
 
-int fa_encode_projection(fa_ctx* c, const float* W, int d_in, int r, int baby_step, void* pts, void* stream) {
-  if (!c || !W || !pts) return fail(FA_E_INVAL, "fa_encode_projection: null argument");
+int fa_encode_projection(fa_ctx* c, const float* W, int d_in, int r, int baby_step, fa_buf* pts, void* stream) {
+  if (!c || !W || !pts || !pts->dev) return fail(FA_E_INVAL, "fa_encode_projection: null argument");
   const int S = c->n / 2;
   if (r < 1 || (r & (r - 1)) || d_in < r || d_in % r || (d_in & (d_in - 1)) || d_in > S)
     return fail(FA_E_SHAPE, "d_in=%d, r=%d: powers of two with r | d_in and d_in <= N/2", d_in, r);
   if (baby_step < 1 || r % baby_step) return fail(FA_E_INVAL, "baby_step %d must divide r=%d", baby_step, r);
+  if (int rc = out_check(c, pts, "fa_encode_projection", "pts", r, 1)) return rc;
   const std::vector<u64>& e = slot_exps(c->n);
   const double scale = std::ldexp(1.0, c->log_scale);
   std::vector<int64_t> coeffs((size_t)r * c->n);
@@ -1060,7 +1212,9 @@ int fa_encode_projection(fa_ctx* c, const float* W, int d_in, int r, int baby_st
       v[(s + shift) % S] = (double)W[(size_t)((s + j) % d_in) * r + (s % r)];
     encode_one(c->n, e, v.data(), S, scale, coeffs.data() + (size_t)j * c->n);
   });
-  return upload_int_pts(c, coeffs.data(), r, (double*)pts, (hipStream_t)stream);
+  const int rc = upload_int_pts(c, coeffs.data(), r, (double*)pts->dev, (hipStream_t)stream);
+  if (!rc) out_set(c, pts, 1, r, c->log_scale);
+  return rc;
 }
 
 // ---------------------------------------------------------------------------
@@ -1593,7 +1747,7 @@ size_t fa_workspace_bytes(const fa_ctx* c, int op, int n_blocks, int d, int baby
       return std::max(score_ws(c, 1, d, baby_step), rotate_ws(c, 1));
     case FA_OP_ROTATE_SUM:
     case FA_OP_ROTATE:
-      return rotate_ws(c, std::min(std::max(1, n_blocks), kRotBatch)) + rup(fa_ct_words(c) * kRotBatch);
+      return rotate_ws(c, std::min(std::max(1, n_blocks), kRotBatch)) + rup((fa_ct_bytes(c) / 8) * kRotBatch);
     case FA_OP_PREPARE:
       if (baby_step < 1) return 0;
       return baby_ws(c, baby_step);
@@ -1611,57 +1765,106 @@ size_t fa_workspace_bytes(const fa_ctx* c, int op, int n_blocks, int d, int baby
   }
 }
 
-size_t fa_prepared_words(const fa_ctx* c, int baby_step) {
-  return (c && baby_step >= 1) ? qrot_words(c, baby_step) : 0;
+size_t fa_prepared_bytes(const fa_ctx* c, int baby_step) {
+  return (c && baby_step >= 1) ? qrot_words(c, baby_step) * 8 : 0;
 }
 
-int fa_prepare_query(fa_ctx* c, const void* q, int baby_step, void* prep, void* ws, size_t ws_bytes, void* stream) {
-  if (!c || !q || !prep) return fail(FA_E_INVAL, "fa_prepare_query: null argument");
+// The query ciphertext and its prepared baby rotations: prep must hold the
+// baby_step - 1 rotations of q, at q's level and scale.
+static int prep_check(const fa_ctx* c, const char* fn, const fa_buf* q, const fa_buf* prep, int baby_step) {
+  int rc = in_check(c, q, fn, "q", 2, 1);
+  if (rc) return rc;
+  if (baby_step < 2) return prep && prep->dev ? FA_OK : fail(FA_E_INVAL, "%s: prep is null", fn);
+  if ((rc = in_check(c, prep, fn, "prep", 2, (uint32_t)(baby_step - 1)))) return rc;
+  if (prep->log_scale != q->log_scale)
+    return fail(FA_E_SHAPE, "%s: prep is at scale 2^%d, the query at 2^%d", fn, prep->log_scale, q->log_scale);
+  return FA_OK;
+}
+
+int fa_prepare_query(fa_ctx* c, const fa_buf* q, int baby_step, fa_buf* prep, void* ws, size_t ws_bytes,
+                     void* stream) {
+  if (!c) return fail(FA_E_INVAL, "fa_prepare_query: null context");
   if (baby_step < 1 || baby_step > c->n / 2) return fail(FA_E_INVAL, "baby_step %d out of range", baby_step);
+  int rc = in_check(c, q, "fa_prepare_query", "q", 2, 1);
+  if (rc || (rc = out_check(c, prep, "fa_prepare_query", "prep", (size_t)(baby_step - 1), 2))) return rc;
   const size_t need = baby_ws(c, baby_step);
   if (baby_step > 1 && (!ws || ws_bytes < need)) return fail(FA_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
   Arena ar{(char*)ws, ws_bytes, 0};
-  int rc = baby_phase(c, (const double*)q, baby_step, (double*)prep, ar, (hipStream_t)stream);
-  return rc ? rc : check_launch("fa_prepare_query");
+  rc = baby_phase(c, (const double*)q->dev, baby_step, (double*)prep->dev, ar, (hipStream_t)stream);
+  if (rc || (rc = check_launch("fa_prepare_query"))) return rc;
+  out_set(c, prep, 2, (size_t)(baby_step - 1), q->log_scale);
+  return FA_OK;
 }
+
+// queries whose baby steps are key-switched together: the per-launch item
+// lists hold up to 32 key switches, so a group's steps per launch stay >= 2
+constexpr int kBatchGroup = 16;
 
 size_t fa_prepare_batch_workspace_bytes(const fa_ctx* c, int n_q, int baby_step) {
   if (!c || n_q < 1 || baby_step < 1) return 0;
-  return baby_batch_ws(c, n_q, baby_step);
+  return baby_batch_ws(c, std::min(n_q, kBatchGroup), baby_step);
 }
 
-int fa_prepare_batch(fa_ctx* c, const void* const* qs, int n_q, int baby_step, void* const* preps, void* ws,
+int fa_prepare_batch(fa_ctx* c, const fa_buf* qs, int n_q, int baby_step, fa_buf* preps, void* ws,
                      size_t ws_bytes, void* stream) {
   if (!c || !qs || !preps) return fail(FA_E_INVAL, "fa_prepare_batch: null argument");
   if (n_q < 1) return fail(FA_E_SHAPE, "n_q must be positive");
-  for (int j = 0; j < n_q; ++j)
-    if (!qs[j] || !preps[j]) return fail(FA_E_INVAL, "query %d or its prepared buffer is null", j);
   if (baby_step < 1 || baby_step > c->n / 2) return fail(FA_E_INVAL, "baby_step %d out of range", baby_step);
-  const size_t need = baby_batch_ws(c, n_q, baby_step);
+  for (int j = 0; j < n_q; ++j) {
+    int rc = in_check(c, &qs[j], "fa_prepare_batch", "a query", 2, 1);
+    if (rc || (rc = out_check(c, &preps[j], "fa_prepare_batch", "a prepared buffer", (size_t)(baby_step - 1), 2)))
+      return rc;
+  }
+  const size_t need = baby_batch_ws(c, std::min(n_q, kBatchGroup), baby_step);
   if (baby_step > 1 && (!ws || ws_bytes < need)) return fail(FA_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
-  Arena ar{(char*)ws, ws_bytes, 0};
-  return baby_phase_batch(c, (const double* const*)qs, n_q, baby_step, (double* const*)preps, ar,
-                          (hipStream_t)stream);
+  for (int j0 = 0; j0 < n_q; j0 += kBatchGroup) {
+    const int m = std::min(kBatchGroup, n_q - j0);
+    std::vector<const double*> qp(m);
+    std::vector<double*> pp(m);
+    for (int j = 0; j < m; ++j) {
+      qp[j] = (const double*)qs[j0 + j].dev;
+      pp[j] = (double*)preps[j0 + j].dev;
+    }
+    Arena ar{(char*)ws, ws_bytes, 0};
+    int rc = baby_phase_batch(c, qp.data(), m, baby_step, pp.data(), ar, (hipStream_t)stream);
+    if (rc) return rc;
+  }
+  for (int j = 0; j < n_q; ++j) out_set(c, &preps[j], 2, (size_t)(baby_step - 1), qs[j].log_scale);
+  return FA_OK;
 }
 
-int fa_score_prepared(fa_ctx* c, const void* q, const void* prep, const void* const* blocks, int n_blocks, int d,
-                      int baby_step, void* out, void* ws, size_t ws_bytes, void* stream) {
-  if (!c || !q || !prep || !blocks || !out) return fail(FA_E_INVAL, "fa_score_prepared: null argument");
-  if (n_blocks < 1) return fail(FA_E_SHAPE, "n_blocks must be positive");
-  for (int i = 0; i < n_blocks; ++i)
-    if (!blocks[i]) return fail(FA_E_INVAL, "block %d is null", i);
+// Shape of a diagonal request (d a power of two <= S, baby step dividing d).
+static int diag_shape(const fa_ctx* c, int d, int baby_step) {
   const int S = c->n / 2;
   if (d < 1 || (d & (d - 1)) || d > S) return fail(FA_E_SHAPE, "d=%d must be a power of two <= N/2", d);
   if (baby_step < 1 || d % baby_step) return fail(FA_E_INVAL, "baby_step %d must divide d=%d", baby_step, d);
+  return FA_OK;
+}
+
+int fa_score_prepared(fa_ctx* c, const fa_buf* q, const fa_buf* prep, const fa_buf* blocks, int n_resident,
+                      const int32_t* block_ids, int n_blocks, int d, int baby_step, fa_buf* out, void* ws,
+                      size_t ws_bytes, void* stream) {
+  const char* fn = "fa_score_prepared";
+  if (!c) return fail(FA_E_INVAL, "%s: null context", fn);
+  std::vector<const double*> bp;
+  int32_t bls = 0;
+  int rc = gather_blocks(c, fn, blocks, n_resident, block_ids, n_blocks, 1, 1, bp, &bls);
+  if (rc || (rc = diag_shape(c, d, baby_step))) return rc;
+  if ((rc = gather_blocks(c, fn, blocks, n_resident, block_ids, n_blocks, 1, (uint32_t)d, bp, &bls))) return rc;
+  if ((rc = prep_check(c, fn, q, prep, baby_step))) return rc;
+  if ((rc = scale_check(c, fn, (long)q->log_scale + bls))) return rc;
+  if ((rc = out_check(c, out, fn, "out", n_blocks, 2))) return rc;
   const size_t need = giant_ws(c, n_blocks, d, baby_step);
   if (!ws || ws_bytes < need) return fail(FA_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
   Arena ar{(char*)ws, ws_bytes, 0};
   hipStream_t s = (hipStream_t)stream;
   if (c->prof) HIPCHK(hipEventRecord(c->ev[0], s));
-  const double* qp = (const double*)q;
-  const double* pp = (const double*)prep;
-  double* op = (double*)out;
-  return mac_giant_phase(c, &qp, &pp, 1, (const double* const*)blocks, n_blocks, d, baby_step, &op, ar, s);
+  const double* qp = (const double*)q->dev;
+  const double* pp = (const double*)prep->dev;
+  double* op = (double*)out->dev;
+  rc = mac_giant_phase(c, &qp, &pp, 1, bp.data(), n_blocks, d, baby_step, &op, ar, s);
+  if (!rc) out_set(c, out, 2, n_blocks, q->log_scale + bls);
+  return rc;
 }
 
 size_t fa_batch_workspace_bytes(const fa_ctx* c, int n_q, int n_blocks, int d, int baby_step) {
@@ -1669,50 +1872,73 @@ size_t fa_batch_workspace_bytes(const fa_ctx* c, int n_q, int n_blocks, int d, i
   return giant_ws(c, std::max(1, n_blocks), d, baby_step, n_q);
 }
 
-int fa_score_batch(fa_ctx* c, const void* const* qs, const void* const* preps, int n_q, const void* const* blocks,
-                   int n_blocks, int d, int baby_step, void* const* outs, void* ws, size_t ws_bytes, void* stream) {
-  if (!c || !qs || !preps || !blocks || !outs) return fail(FA_E_INVAL, "fa_score_batch: null argument");
+int fa_score_batch(fa_ctx* c, const fa_buf* qs, const fa_buf* preps, int n_q, const fa_buf* blocks, int n_resident,
+                   const int32_t* block_ids, int n_blocks, int d, int baby_step, fa_buf* outs, void* ws,
+                   size_t ws_bytes, void* stream) {
+  const char* fn = "fa_score_batch";
+  if (!c || !qs || !preps || !outs) return fail(FA_E_INVAL, "%s: null argument", fn);
   if (n_q < 1) return fail(FA_E_SHAPE, "n_q must be positive");
-  for (int j = 0; j < n_q; ++j)
-    if (!qs[j] || !preps[j] || !outs[j]) return fail(FA_E_INVAL, "query %d: null argument", j);
-  if (n_blocks < 1) return fail(FA_E_SHAPE, "n_blocks must be positive");
-  for (int i = 0; i < n_blocks; ++i)
-    if (!blocks[i]) return fail(FA_E_INVAL, "block %d is null", i);
-  const int S = c->n / 2;
-  if (d < 1 || (d & (d - 1)) || d > S) return fail(FA_E_SHAPE, "d=%d must be a power of two <= N/2", d);
-  if (baby_step < 1 || d % baby_step) return fail(FA_E_INVAL, "baby_step %d must divide d=%d", baby_step, d);
+  std::vector<const double*> bp;
+  int32_t bls = 0;
+  int rc = gather_blocks(c, fn, blocks, n_resident, block_ids, n_blocks, 1, 1, bp, &bls);
+  if (rc || (rc = diag_shape(c, d, baby_step))) return rc;
+  if ((rc = gather_blocks(c, fn, blocks, n_resident, block_ids, n_blocks, 1, (uint32_t)d, bp, &bls))) return rc;
+  std::vector<const double*> qp(n_q), pp(n_q);
+  std::vector<double*> op(n_q);
+  for (int j = 0; j < n_q; ++j) {
+    if ((rc = prep_check(c, fn, &qs[j], &preps[j], baby_step))) return rc;
+    if ((rc = scale_check(c, fn, (long)qs[j].log_scale + bls))) return rc;
+    if ((rc = out_check(c, &outs[j], fn, "an output", n_blocks, 2))) return rc;
+    qp[j] = (const double*)qs[j].dev;
+    pp[j] = (const double*)preps[j].dev;
+    op[j] = (double*)outs[j].dev;
+  }
   const size_t need = giant_ws(c, n_blocks, d, baby_step, n_q);
   if (!ws || ws_bytes < need) return fail(FA_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
   Arena ar{(char*)ws, ws_bytes, 0};
   hipStream_t s = (hipStream_t)stream;
   if (c->prof) HIPCHK(hipEventRecord(c->ev[0], s));
-  return mac_giant_phase(c, (const double* const*)qs, (const double* const*)preps, n_q, (const double* const*)blocks,
-                         n_blocks, d, baby_step, (double* const*)outs, ar, s);
+  rc = mac_giant_phase(c, qp.data(), pp.data(), n_q, bp.data(), n_blocks, d, baby_step, op.data(), ar, s);
+  if (!rc)
+    for (int j = 0; j < n_q; ++j) out_set(c, &outs[j], 2, n_blocks, qs[j].log_scale + bls);
+  return rc;
 }
 
-int fa_score_block(fa_ctx* c, const void* q, const void* const* blocks, int n_blocks, int d, int layout,
-                   int baby_step, void* out, void* ws, size_t ws_bytes, void* stream) {
+int fa_score_block(fa_ctx* c, const fa_buf* q, const fa_buf* blocks, int n_resident, const int32_t* block_ids,
+                   int n_blocks, int d, int layout, int baby_step, fa_buf* out, void* ws, size_t ws_bytes,
+                   void* stream) {
+  const char* fn = "fa_score_block";
   if (n_blocks < 1) return fail(FA_E_SHAPE, "n_blocks must be positive");
-  if (!c || !q || !blocks || !out) return fail(FA_E_INVAL, "fa_score_block: null argument");
-  for (int i = 0; i < n_blocks; ++i)
-    if (!blocks[i]) return fail(FA_E_INVAL, "block %d is null", i);
-  hipStream_t s = (hipStream_t)stream;
-  if (layout == FA_LAYOUT_ROW) {
-    fa::mul_plain(c, (const double*)q, (const double* const*)blocks, n_blocks, (double*)out, s);
-    return check_launch("fa_score_block(row)");
-  }
-  if (layout != FA_LAYOUT_DIAG && layout != FA_LAYOUT_DIAG_ENC) return fail(FA_E_INVAL, "unknown layout %d", layout);
-  const int S = c->n / 2;
-  if (d < 1 || (d & (d - 1)) || d > S) return fail(FA_E_SHAPE, "d=%d must be a power of two <= N/2", d);
-  if (baby_step < 1 || d % baby_step) return fail(FA_E_INVAL, "baby_step %d must divide d=%d", baby_step, d);
+  if (!c) return fail(FA_E_INVAL, "%s: null context", fn);
+  if (layout != FA_LAYOUT_ROW && layout != FA_LAYOUT_DIAG && layout != FA_LAYOUT_DIAG_ENC)
+    return fail(FA_E_INVAL, "unknown layout %d", layout);
   const bool enc = layout == FA_LAYOUT_DIAG_ENC;
+  const uint32_t kind = enc ? 2 : 1;
+  std::vector<const double*> bp;
+  int32_t bls = 0;
+  int rc = gather_blocks(c, fn, blocks, n_resident, block_ids, n_blocks, kind, 1, bp, &bls);
+  if (rc || (rc = in_check(c, q, fn, "q", 2, 1))) return rc;
+  if (layout != FA_LAYOUT_ROW) {
+    if ((rc = diag_shape(c, d, baby_step))) return rc;
+    if ((rc = gather_blocks(c, fn, blocks, n_resident, block_ids, n_blocks, kind, (uint32_t)d, bp, &bls))) return rc;
+  }
+  if ((rc = scale_check(c, fn, (long)q->log_scale + bls))) return rc;
+  if ((rc = out_check(c, out, fn, "out", n_blocks, 2))) return rc;
+  hipStream_t s = (hipStream_t)stream;
+  const double* qd = (const double*)q->dev;
+  if (layout == FA_LAYOUT_ROW) {
+    fa::mul_plain(c, qd, bp.data(), n_blocks, (double*)out->dev, s);
+    if ((rc = check_launch("fa_score_block(row)"))) return rc;
+    out_set(c, out, 2, n_blocks, q->log_scale + bls);
+    return FA_OK;
+  }
   const size_t need = enc ? score_enc_ws(c, n_blocks, d, baby_step) : score_ws(c, n_blocks, d, baby_step);
   if (!ws || ws_bytes < need) return fail(FA_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
   Arena ar{(char*)ws, ws_bytes, 0};
-  if (enc)
-    return score_diag_enc(c, (const double*)q, (const double* const*)blocks, n_blocks, d, baby_step, (double*)out, ar,
-                          s);
-  return score_diag(c, (const double*)q, (const double* const*)blocks, n_blocks, d, baby_step, (double*)out, ar, s);
+  rc = enc ? score_diag_enc(c, qd, bp.data(), n_blocks, d, baby_step, (double*)out->dev, ar, s)
+           : score_diag(c, qd, bp.data(), n_blocks, d, baby_step, (double*)out->dev, ar, s);
+  if (!rc) out_set(c, out, 2, n_blocks, q->log_scale + bls);
+  return rc;
 }
 
 // ---- the membership path: rescale, ct x ct products, constants, polynomials ----
@@ -2237,19 +2463,26 @@ int fa_membership(fa_ctx* const* levels, int n_levels, const void* q_r, int L_q,
   return check_launch("fa_membership");
 }
 
-int fa_rotate(fa_ctx* c, const void* ct, int step, void* out, void* ws, size_t ws_bytes, void* stream) {
-  if (!c || !ct || !out) return fail(FA_E_INVAL, "fa_rotate: null argument");
+int fa_rotate(fa_ctx* c, const fa_buf* ct, int step, fa_buf* out, void* ws, size_t ws_bytes, void* stream) {
+  if (!c) return fail(FA_E_INVAL, "fa_rotate: null context");
+  int rc = in_check(c, ct, "fa_rotate", "ct", 2, 1);
+  if (rc || (rc = out_check(c, out, "fa_rotate", "out", 1, 2))) return rc;
+  if (overlap(ct, out)) return fail(FA_E_INVAL, "fa_rotate: out overlaps ct (the rotation cannot run in place)");
   if (step < 1 || step >= c->n / 2) return fail(FA_E_INVAL, "step %d out of [1, N/2)", step);
   if (!c->keys.count(step)) return fail(FA_E_NOKEY, "no rotation key for step %d", step);
   if (!ws || ws_bytes < rotate_ws(c, 1)) return fail(FA_E_NOMEM, "workspace too small for rotation");
   Arena ar{(char*)ws, ws_bytes, 0};
-  return rotate_batch(c, (const double*)ct, 1, step, (double*)out, ar, (hipStream_t)stream);
+  rc = rotate_batch(c, (const double*)ct->dev, 1, step, (double*)out->dev, ar, (hipStream_t)stream);
+  if (!rc) out_set(c, out, 2, 1, ct->log_scale);
+  return rc;
 }
 
-int fa_rotate_sum(fa_ctx* c, void* cts, int n_cts, int first_shift, int n_steps, void* ws, size_t ws_bytes,
-                  void* stream) {
-  if (!c || !cts) return fail(FA_E_INVAL, "fa_rotate_sum: null argument");
-  if (n_cts < 1 || n_steps < 0 || first_shift < 1) return fail(FA_E_INVAL, "fa_rotate_sum: bad sizes");
+int fa_rotate_sum(fa_ctx* c, fa_buf* cts_b, int first_shift, int n_steps, void* ws, size_t ws_bytes, void* stream) {
+  if (!c) return fail(FA_E_INVAL, "fa_rotate_sum: null context");
+  if (int rc = in_check(c, cts_b, "fa_rotate_sum", "cts", 2, 1)) return rc;
+  const int n_cts = (int)cts_b->count;
+  void* cts = cts_b->dev;
+  if (n_steps < 0 || first_shift < 1) return fail(FA_E_INVAL, "fa_rotate_sum: bad sizes");
   for (int k = 0; k < n_steps; ++k) {
     const long r = (long)first_shift << k;
     if (r >= c->n / 2) return fail(FA_E_INVAL, "rotation %ld out of [1, N/2)", r);
@@ -2258,7 +2491,7 @@ int fa_rotate_sum(fa_ctx* c, void* cts, int n_cts, int first_shift, int n_steps,
   const size_t need = fa_workspace_bytes(c, FA_OP_ROTATE_SUM, n_cts, 0, 1);
   if (!ws || ws_bytes < need) return fail(FA_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
   hipStream_t s = (hipStream_t)stream;
-  const size_t ctw = fa_ct_words(c);
+  const size_t ctw = (fa_ct_bytes(c) / 8);
   Arena ar{(char*)ws, ws_bytes, 0};
   double* tmp = ar.take(ctw * kRotBatch);
   double* base = (double*)cts;
@@ -2298,12 +2531,20 @@ int fa_profile_read(fa_ctx* c, double* ms) {
 // The projection q_R = W^T q: the diagonal product of q with the r hybrid
 // diagonals of W (plaintexts, or ciphertexts when enc), then the fold
 // z += Rotate(z, r * 2^k) while r * 2^k < d_in.
-static int project(fa_ctx* c, const void* q, const void* w, bool enc, int d_in, int r, int baby_step, void* q_r,
-                   void* ws, size_t ws_bytes, void* stream) {
+static int project(fa_ctx* c, const fa_buf* qb, const fa_buf* wb, bool enc, int d_in, int r, int baby_step,
+                   fa_buf* qrb, void* ws, size_t ws_bytes, void* stream) {
   const char* fn = enc ? "fa_project_ct_enc" : "fa_project_ct";
-  if (!c || !q || !w || !q_r) return fail(FA_E_INVAL, "%s: null argument", fn);
+  if (!c) return fail(FA_E_INVAL, "%s: null context", fn);
   if (r < 1 || (r & (r - 1)) || d_in < r || d_in % r || ((d_in / r) & (d_in / r - 1)) || d_in > c->n / 2)
     return fail(FA_E_SHAPE, "d_in=%d, r=%d: both powers of two with r <= d_in <= N/2", d_in, r);
+  int rc0 = in_check(c, qb, fn, "q", 2, 1);
+  if (rc0 || (rc0 = in_check(c, wb, fn, enc ? "w_cts" : "w_pts", enc ? 2 : 1, (uint32_t)r))) return rc0;
+  if ((rc0 = scale_check(c, fn, (long)qb->log_scale + wb->log_scale))) return rc0;
+  if ((rc0 = out_check(c, qrb, fn, "q_r", 1, 2))) return rc0;
+  if (overlap(qb, qrb)) return fail(FA_E_INVAL, "%s: q_r overlaps q", fn);
+  const void* q = qb->dev;
+  const void* w = wb->dev;
+  void* q_r = qrb->dev;
   if (baby_step < 1 || r % baby_step) return fail(FA_E_INVAL, "baby_step %d must divide r=%d", baby_step, r);
   const size_t need = fa_workspace_bytes(c, enc ? FA_OP_PROJECT_ENC : FA_OP_PROJECT, 1, r, baby_step);
   if (!ws || ws_bytes < need) return fail(FA_E_NOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
@@ -2319,20 +2560,22 @@ static int project(fa_ctx* c, const void* q, const void* w, bool enc, int d_in, 
   if (rc) return rc;
   for (int k = 0; k < steps; ++k) {
     Arena ar2{(char*)ws, ws_bytes, 0};
-    double* tmp = ar2.take(fa_ct_words(c));
+    double* tmp = ar2.take((fa_ct_bytes(c) / 8));
     rc = rotate_batch(c, (const double*)q_r, 1, r << k, tmp, ar2, s);
     if (rc) return rc;
     fa::add_automorph(c, (double*)q_r, tmp, 2, 1u, s);
   }
-  return check_launch(fn);
+  if ((rc = check_launch(fn))) return rc;
+  out_set(c, qrb, 2, 1, qb->log_scale + wb->log_scale);
+  return FA_OK;
 }
 
-int fa_project_ct(fa_ctx* c, const void* q, const void* w_pts, int d_in, int r, int baby_step, void* q_r, void* ws,
-                  size_t ws_bytes, void* stream) {
+int fa_project_ct(fa_ctx* c, const fa_buf* q, const fa_buf* w_pts, int d_in, int r, int baby_step, fa_buf* q_r,
+                  void* ws, size_t ws_bytes, void* stream) {
   return project(c, q, w_pts, false, d_in, r, baby_step, q_r, ws, ws_bytes, stream);
 }
 
-int fa_project_ct_enc(fa_ctx* c, const void* q, const void* w_cts, int d_in, int r, int baby_step, void* q_r,
+int fa_project_ct_enc(fa_ctx* c, const fa_buf* q, const fa_buf* w_cts, int d_in, int r, int baby_step, fa_buf* q_r,
                       void* ws, size_t ws_bytes, void* stream) {
   return project(c, q, w_cts, true, d_in, r, baby_step, q_r, ws, ws_bytes, stream);
 }

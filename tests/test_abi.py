@@ -63,3 +63,34 @@ def test_chebyshev_square_root_fit_matches_numpy(lib):
         assert np.max(np.abs(got - ref)) < 1e-14
     with pytest.raises(fa.FaError):
         fa.cheb_fit_sqrt(0.6, 0.0, 2.5, 7)
+
+
+def test_context_parameters_rejected_before_the_device(lib):
+    """fa_ctx_create refuses, before touching the device, more key-switch digits than the
+    kernels are built for and explicit primes the arithmetic cannot use: outside (2^49, 2^50),
+    not 1 mod 2N, composite, or listed twice."""
+    from oracle import ckks
+    from paper_2608_21131_amd import fa
+    fa.load_library()
+    h = ctypes.c_void_p()
+
+    def create(logn, L, K, primes=None):
+        arr = None if primes is None else np.ascontiguousarray(primes, dtype=np.uint64)
+        prm = fa._Params(logn, L, K, 40, None if arr is None else arr.ctypes.data_as(fa._u64p))
+        rc = fa._LIB.fa_ctx_create(ctypes.byref(prm), ctypes.byref(h))
+        return rc, fa._LIB.fa_last_error().decode()
+
+    rc, msg = create(16, 12, 1)          # twelve digits
+    assert rc == fa.FA_E_INVAL and "digits" in msg
+    rc, msg = create(12, 16, 1)          # sixteen digits
+    assert rc == fa.FA_E_INVAL and "digits" in msg
+    logn = 12
+    m = 2 << logn
+    good = ckks.find_primes(logn, 4)
+    composite = next(c for c in range(good[0] - m, good[0] - 200 * m, -m) if not ckks.is_probable_prime(c))
+    for bad, what in [([good[0], good[1], 1 << 50, good[3]], "not in"),
+                      ([good[0], good[1], good[2] + 2, good[3]], "1 mod 2N"),
+                      ([good[0], composite, good[2], good[3]], "not prime"),
+                      ([good[0], good[1], good[0], good[3]], "twice")]:
+        rc, msg = create(logn, 3, 1, bad)
+        assert rc == fa.FA_E_INVAL and what in msg, (bad, msg)

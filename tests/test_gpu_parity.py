@@ -216,14 +216,16 @@ def test_save_and_load_enrolled_blocks(tmp_path):
     blk = p.ctx.encode_db_block(X.astype(np.float32), d, 1, B)
     path = str(tmp_path / "enrolled.npz")
     say("[save/load] p1")
-    p.ctx.save_buffers(path, {"block": (blk, d), "query": (ct, 2)})
+    p.ctx.save_buffers(path, {"block": blk, "query": ct})
     got = p.ctx.load_buffers(path)
-    assert torch.equal(got["block"], blk) and torch.equal(got["query"], ct)
+    assert torch.equal(got["block"].t, blk.t) and torch.equal(got["query"].t, ct.t)
+    assert (got["block"].count, got["block"].n_polys, got["block"].log_scale) == (d, 1, 40)
+    assert (got["query"].count, got["query"].n_polys, got["query"].log_scale) == (1, 2, 40)
     ref = p.export_ct(p.ctx.score_block(ct, [blk], d, 1, B))
     assert np.array_equal(p.export_ct(p.ctx.score_block(got["query"], [got["block"]], d, 1, B)), ref)
     with pytest.raises(ValueError):
         pair("tiny").ctx.load_buffers(path)
-    bad = p.ctx.export(blk, 1)
+    bad = p.ctx.export(blk.item(0))
     bad[0, 1, 5] = p.par.q[1]
     with pytest.raises(fa.FaError, match="FA_E_INVAL"):
         p.ctx.import_coeffs(bad)
@@ -439,7 +441,7 @@ def test_prepare_batch_matches_single(name, B, nq):
     words = (B - 1) * p.ctx.ct_words  # the B-1 rotated ciphertexts (the buffer holds one spare word)
     for j in range(nq):
         single = p.ctx.prepare_query(cts[j][0], B)
-        assert torch.equal(preps[j][:words], single[:words]), j
+        assert torch.equal(preps[j].t[:words], single.t[:words]), j
     if name == "tiny":
         G = d // B
         X = gen.gaussian_unit_rows(gen.rng(17, gen.STREAM_DB), 200, d)
@@ -638,9 +640,17 @@ def _enc_both(top, levels, och, s, v, wid, tag):
     return levels[0].encrypt(m, a, e), och.orc[top.L].encrypt(m, a, e, s)
 
 
+def _at(levels, ct, L, offset_words=0):
+    """The ciphertext at level L held in the first words of ct (from offset_words), described
+    at that level."""
+    c = levels[levels[0].L - L]
+    t = ct.t if hasattr(ct, "t") else ct
+    return c.wrap(t[offset_words:offset_words + 2 * L * c.n], 2, 1, 0)
+
+
 def _export_at(levels, ct, L):
     c = levels[levels[0].L - L]
-    return c.export(ct[:2 * L * c.n], 2).reshape(2, L, c.n)
+    return c.export(_at(levels, ct, L)).reshape(2, L, c.n)
 
 
 def test_rescale_and_product_parity():
@@ -656,7 +666,7 @@ def test_rescale_and_product_parity():
     po = och.orc[top.L].mul(xo, yo, och.rlk[top.L])
     assert np.array_equal(_export_at(levels, p, top.L), po)
     pr = levels[0].rescale(levels[1], p)
-    z = levels[1].decode(levels[1].decrypt(pr), 50) * (2.0 ** 50 / (2.0 ** 100 / top.q[-1]))
+    z = levels[1].decode(levels[1].decrypt(_at(levels, pr, top.L - 1)), 50) * (2.0 ** 50 / (2.0 ** 100 / top.q[-1]))
     assert np.max(np.abs(z - v1 * v2)) < 1e-6
     # constants and sums
     a = levels[0].ct_add_const(levels[0].ct_mul_const(x, -3), 12345)
@@ -680,7 +690,7 @@ def test_chebyshev_and_sign_parity():
     assert (L, sc) == (Lo, so)
     assert np.array_equal(_export_at(levels, out, L), oo)
     c = levels[top.L - L]
-    z = c.decode(c.decrypt(out[:2 * L * c.n]), 50) * (2.0 ** 50 / sc)
+    z = c.decode(c.decrypt(_at(levels, out, L)), 50) * (2.0 ** 50 / sc)
     assert np.max(np.abs(z - np.polynomial.chebyshev.chebval(u, coeffs))) < 1e-6
     say("[chain] two sign steps")
     v = np.random.default_rng(53).uniform(-0.5, 0.5, top.slots)
@@ -690,7 +700,7 @@ def test_chebyshev_and_sign_parity():
     assert (L, sc, m) == (Lo, so, mo)
     assert np.array_equal(_export_at(levels, out, L), oo)
     c = levels[top.L - L]
-    z = c.decode(c.decrypt(out[:2 * L * c.n]), 50) * (2.0 ** 50 / sc) / m
+    z = c.decode(c.decrypt(_at(levels, out, L)), 50) * (2.0 ** 50 / sc) / m
     f = lambda t: (3 * t - t ** 3) / 2
     assert np.max(np.abs(z - f(f(v)))) < 1e-6
 
@@ -743,7 +753,7 @@ def test_membership_scan_parity(y_lo, y_hi, degree, iters, nblk):
     c = levels[top.L - L]
     z = []
     for i in range(nblk):
-        blk = out[i * ctw:i * ctw + 2 * L * c.n]
+        blk = _at(levels, out, L, i * ctw)
         assert np.array_equal(_export_at(levels, blk, L), oo[i]), i
         z.append(c.decode(c.decrypt(blk), 50) * (2.0 ** 50 / sc) / mo)
     z = np.concatenate(z)[:len(X)]
@@ -776,3 +786,148 @@ def test_chain_calls_reject_short_chains_and_bad_arguments():
     with pytest.raises(fa.FaError) as ei:
         fa.membership(levels, x, top.L, 2.0 ** 50, [blk], 16, 4, 0.5, 2.5, np.ones(2), 4, 1)
     assert ei.value.code == fa.FA_E_NOKEY
+
+
+# ----------------------------------------------------------------------------
+# the buffer descriptors, block ids and explicit primes of the C ABI
+# ----------------------------------------------------------------------------
+def test_descriptor_checks_refuse_mismatched_buffers():
+    """Every scoring-path call checks its fa_buf descriptors on the host before any launch: a
+    ciphertext at another level, a plaintext passed as a ciphertext, blocks at two scales, a
+    block with too few diagonals, a product scale the modulus cannot hold, an output too small,
+    a block id out of range and an in-place rotation are refused with FA_E_SHAPE / FA_E_INVAL,
+    and the output buffers are left untouched."""
+    import torch
+    from paper_2608_21131_amd import fa
+    p = pair("tiny", wid=30)
+    S, d, B = p.par.slots, 16, 4
+    p.keys(ckks.steps_for_bsgs(d, B) + [16, 32], oracle=False)
+    q = gen.gaussian_unit_rows(gen.rng(30, gen.STREAM_QUERY), 1, d)[0]
+    ct, _ = p.encrypt_both(ckks.encode(ckks.replicate(q, S), p.n, 40), tag=30)
+    X = gen.gaussian_unit_rows(gen.rng(30, gen.STREAM_DB), 100, d).astype(np.float32)
+    blk = p.ctx.encode_db_block(X, d, fa.LAYOUT_DIAG, B)
+    assert (blk.n_polys, blk.count, blk.limbs, blk.log_scale) == (1, d, p.par.L, 40)
+    low = p.ctx.at_level(2)
+    ct_low = p.ctx.drop_level(low, ct)
+    assert (ct_low.limbs, ct_low.log_scale) == (2, 40)
+    out = p.ctx.new_ct(2)
+    out.t.fill_(7.0)
+
+    def code(fn, *a, **k):
+        with pytest.raises(fa.FaError) as ei:
+            fn(*a, **k)
+        return ei.value.code
+
+    say("[descriptors] tiny")
+    # a ciphertext of the 2-prime level given to the 3-prime context (same tensor, its descriptor)
+    wrong_level = p.ctx.wrap(ct_low.t, fa.CT, 1, 40)
+    wrong_level.limbs = 2
+    assert code(p.ctx.score_block, wrong_level, [blk], d, fa.LAYOUT_DIAG, B, out=out) == fa.FA_E_SHAPE
+    assert code(p.ctx.rotate_sum, wrong_level, 1, 1, 1) == fa.FA_E_SHAPE
+    assert code(p.ctx.project_ct, wrong_level, blk, 64, d, B) == fa.FA_E_SHAPE
+    # a plaintext passed as the query, a ciphertext passed as a block
+    assert code(p.ctx.score_block, blk.item(0), [blk], d, fa.LAYOUT_DIAG, B, out=out) == fa.FA_E_SHAPE
+    assert code(p.ctx.score_block, ct, [ct], d, fa.LAYOUT_DIAG, B, out=out) == fa.FA_E_SHAPE
+    assert code(p.ctx.rotate_sum, blk, 1, 1, 1) == fa.FA_E_SHAPE
+    assert code(p.ctx.decrypt, blk.item(0)) == fa.FA_E_SHAPE
+    # W's plaintexts at another level, or too few of them
+    w_low = low.encode_db_block(X, d, fa.LAYOUT_DIAG, B)
+    assert code(p.ctx.project_ct, ct, w_low, 64, d, B) == fa.FA_E_SHAPE
+    assert code(p.ctx.project_ct, ct, blk.items(0, d - 1), 64, d, B) == fa.FA_E_SHAPE
+    # blocks at two scales; a block with fewer than d diagonals
+    blk80 = p.ctx.encode_db_block_int(np.zeros((d, p.n), np.int64), log_scale=80)
+    assert code(p.ctx.score_block, ct, [blk, blk80], d, fa.LAYOUT_DIAG, B, out=out) == fa.FA_E_SHAPE
+    assert code(p.ctx.score_block, ct, [blk.items(0, d - 1)], d, fa.LAYOUT_DIAG, B, out=out) == fa.FA_E_SHAPE
+    # a product scale above Q / 2^8 (Q ~ 2^150 here): 2^(110 + 40)
+    hi = p.ctx.wrap(ct.t, fa.CT, 1, 110)
+    assert code(p.ctx.score_block, hi, [blk], d, fa.LAYOUT_DIAG, B, out=out) == fa.FA_E_SHAPE
+    assert code(p.ctx.project_ct, hi, blk, 64, d, B) == fa.FA_E_SHAPE
+    # an output too small for two blocks; block ids out of range
+    assert code(p.ctx.score_block, ct, [blk, blk], d, fa.LAYOUT_DIAG, B, out=out.item(0)) == fa.FA_E_SHAPE
+    assert code(p.ctx.score_block, ct, [blk], d, fa.LAYOUT_DIAG, B, out=out, block_ids=[1]) == fa.FA_E_INVAL
+    assert code(p.ctx.score_block, ct, [blk], d, fa.LAYOUT_DIAG, B, out=out, block_ids=[-1]) == fa.FA_E_INVAL
+    # a rotation into its own input
+    assert code(p.ctx.rotate, ct, 1, out=ct) == fa.FA_E_INVAL
+    torch.cuda.synchronize()
+    assert bool((out.t == 7.0).all()), "a refused call wrote its output"
+
+
+def test_block_ids_select_resident_blocks():
+    """block_ids: the scorer takes the ids of the groups to score among the resident blocks
+    (repeats allowed) and writes output j for block ids[j], word for word what scoring that
+    list of blocks directly gives; the oracle agrees on one of them."""
+    p = pair("tiny", wid=31)
+    S, d, B = p.par.slots, 16, 4
+    G = d // B
+    keys = p.keys(ckks.steps_for_bsgs(d, B))
+    q = gen.gaussian_unit_rows(gen.rng(31, gen.STREAM_QUERY), 1, d)[0]
+    ct, ct_o = p.encrypt_both(ckks.encode(ckks.replicate(q, S), p.n, 40), tag=31)
+    g = gen.rng(31, gen.STREAM_DB)
+    Xs = [gen.gaussian_unit_rows(g, r, d) for r in (300, 512, 77)]
+    coeffs = [ckks.layout_b_coeffs(X, p.par, d, B) for X in Xs]
+    resident = [p.ctx.encode_db_block_int(c) for c in coeffs]
+    ids = [2, 0, 2, 1]
+    say("[block_ids] tiny")
+    got = p.export_ct(p.ctx.score_block(ct, resident, d, 1, B, block_ids=ids), len(ids))
+    ref = p.export_ct(p.ctx.score_block(ct, [resident[i] for i in ids], d, 1, B), len(ids))
+    assert np.array_equal(got, ref)
+    pts = np.stack([ckks.to_residues(ci, p.par.q) for ci in coeffs[2]]).reshape(G, B, p.par.L, p.n)
+    assert np.array_equal(got[0], p.orc.bsgs_block(p.orc.baby_rotations(ct_o, B, keys), pts, B, G, keys))
+    prep = p.ctx.prepare_query(ct, B)
+    got2 = p.export_ct(p.ctx.score_prepared(ct, prep, resident, d, B, block_ids=ids), len(ids))
+    assert np.array_equal(got2, ref)
+    got3 = p.ctx.score_batch([ct, ct], [prep, prep], resident, d, B, block_ids=ids)
+    assert all(np.array_equal(p.export_ct(o, len(ids)), ref) for o in got3)
+
+
+def test_explicit_primes_match_the_oracle():
+    """fa_params.primes: a context over an explicit prime list (not the default choice: every
+    other NTT prime below 2^50, ciphertext and special primes interleaved) rotates and scores
+    exactly as the oracle over the same primes."""
+    from paper_2608_21131_amd import fa
+    logn, L, K = 10, 3, 1
+    primes = ckks.find_primes(logn, 2 * (L + K))[1::2]
+    par = ckks.Params(logn=logn, L=L, K=K, primes=primes)
+    orc = ckks.Oracle(par)
+    ctx = fa.Context(logn, L, K, 40, primes=primes)
+    assert ctx.primes == primes
+    s = gen.ternary_secret(gen.rng(32, gen.STREAM_SECRET), par.n)
+    d, B = 16, 4
+    steps = ckks.steps_for_bsgs(d, B)
+    rand = [(gen.uniform_residues(gen.rng(32, gen.STREAM_KEY_A, r), par.primes, par.dnum, par.n),
+             gen.rounded_gaussian(gen.rng(32, gen.STREAM_KEY_E, r), (par.dnum, par.n))) for r in steps]
+    ctx.keygen(s, steps, np.stack([x[0] for x in rand]), np.stack([x[1] for x in rand]))
+    keys = {r: orc.keygen(s, r, *rand[i]) for i, r in enumerate(steps)}
+    q = gen.gaussian_unit_rows(gen.rng(32, gen.STREAM_QUERY), 1, d)[0]
+    m = ckks.encode(ckks.replicate(q, par.slots), par.n, 40)
+    a = gen.uniform_residues(gen.rng(32, gen.STREAM_ENC_A), par.q, 1, par.n)[0]
+    e = gen.rounded_gaussian(gen.rng(32, gen.STREAM_ENC_E), par.n)
+    ct, ct_o = ctx.encrypt(m, a, e), orc.encrypt(m, a, e, s)
+    say("[primes] explicit list, N=2^10")
+    assert np.array_equal(ctx.export(ctx.rotate(ct, 3)).reshape(2, L, par.n), orc.rotate(ct_o, 3, keys[3]))
+    X = gen.gaussian_unit_rows(gen.rng(32, gen.STREAM_DB), 400, d)
+    c = ckks.layout_b_coeffs(X, par, d, B)
+    out = ctx.score_block(ct, [ctx.encode_db_block_int(c)], d, fa.LAYOUT_DIAG, B)
+    pts = np.stack([ckks.to_residues(ci, par.q) for ci in c]).reshape(d // B, B, L, par.n)
+    ref = orc.bsgs_block(orc.baby_rotations(ct_o, B, keys), pts, B, d // B, keys)
+    assert np.array_equal(ctx.export(out).reshape(2, L, par.n), ref)
+    z = ctx.decode(ctx.decrypt(out), 80)
+    assert np.max(np.abs(z[:400] - X @ q)) < 1e-4
+
+
+@pytest.mark.parametrize("nq", [17, 33])
+def test_prepare_batch_beyond_one_group(nq):
+    """fa_prepare_batch with more queries than one key-switch group holds (groups of 16):
+    every query's baby rotations equal fa_prepare_query's word for word."""
+    import torch
+    p = pair("tiny", wid=33)
+    S, B = p.par.slots, 4
+    p.keys(ckks.steps_for_bsgs(16, B), oracle=False)
+    Q = gen.gaussian_unit_rows(gen.rng(33, gen.STREAM_QUERY, nq), nq, 16)
+    cts = [p.encrypt_both(ckks.encode(ckks.replicate(Q[j], S), p.n, 40), tag=330 + j)[0] for j in range(nq)]
+    say(f"[prepare_batch] tiny B={B} nq={nq}")
+    preps = p.ctx.prepare_batch(cts, B)
+    torch.cuda.synchronize()
+    words = (B - 1) * p.ctx.ct_words  # the rotations (the buffer holds one spare word)
+    for j in range(nq):
+        assert torch.equal(preps[j].t[:words], p.ctx.prepare_query(cts[j], B).t[:words]), j

@@ -460,7 +460,8 @@ def test_membership_face_scan_fullsize():
     # float64 model and decisions over all 222,049 centroids
     ctw = levels[1].ct_words
     c2 = levels[w.L - L]
-    z = np.concatenate([c2.decode(c2.decrypt(out[i * ctw:i * ctw + 2 * L * c2.n]), 50) for i in range(nb)])
+    at_L = [c2.wrap(out.t[i * ctw:i * ctw + 2 * L * c2.n], 2, 1, 0) for i in range(nb)]
+    z = np.concatenate([c2.decode(c2.decrypt(b_), 50) for b_ in at_L])
     z = z[:w.rows] * (2.0 ** 50 / sc) / mo
     qR = W.T @ q
     Xm = np.vstack([Xr[:(nb - 1) * S].astype(np.float32).astype(np.float64), last])
@@ -492,5 +493,4 @@ def test_membership_face_scan_fullsize():
     oo, Lo, so, mo2 = ckks.membership(ch, q11o, w.L - 1, s_q, [ckks.layout_b_pts(last, lp, R, B)], R, B,
                                       x["y_lo"], x["y_hi"], coeffs, x["m"], x["iters"])
     assert (Lo, so, mo2) == (L, sc, mo)
-    blk = out[(nb - 1) * ctw:(nb - 1) * ctw + 2 * L * c2.n]
-    assert np.array_equal(c2.export(blk, 2).reshape(2, L, top.n), oo[0])
+    assert np.array_equal(c2.export(at_L[nb - 1], 2).reshape(2, L, top.n), oo[0])
