@@ -46,8 +46,8 @@ def parse():
                     choices=["tiny", "fine", "rank", "rerank", "three_level", "face"])
     ap.add_argument("--baby-step", type=int, default=0)
     ap.add_argument("--level", type=int, default=0,
-                    help="fine/rerank: drop the query to this many ciphertext primes and score there, with the "
-                         "database enrolled at that level (0: score at all primes)")
+                    help="fine/rerank/three_level: drop the query to this many ciphertext primes and score there, "
+                         "with the database enrolled at that level (0: score at all primes)")
     ap.add_argument("--queries", type=int, default=0, help="three_level: queries per step (default 32)")
     ap.add_argument("--also-level", type=int, default=3,
                     help="rerank: also time the level with the query dropped to this many primes and report it "
@@ -63,6 +63,10 @@ def parse():
     ap.add_argument("--enc-w", type=int, default=1,
                     help="rank: also time the projection with W's diagonals encrypted and report it under "
                          "enc_projection (0: skip)")
+    ap.add_argument("--three-level", type=int, default=1,
+                    help="rerank: also run the full three-level query (32 queries back to back at all 12 primes, "
+                         "coarse, fine and rerank levels with the client's decrypt and top-k between them) and "
+                         "report it under three_level (0: skip)")
     ap.add_argument("--membership", type=int, default=1,
                     help="rerank: also time the face membership scan (222,049 centroids, encrypted threshold) "
                          "and report it under membership (0: skip)")
@@ -178,7 +182,7 @@ def run_diag_level(bn, args):
     mac_bytes = 8 * (w.n_blocks * w.d * ptw + (w.B - 1) * 2 * ptw + 2 * ptw + w.n_blocks * w.G * 2 * ptw)
     stream_bytes = 8 * w.n_blocks * w.d * ptw
     return dict(ms=ms, scores=w.rows, phases=ph, err=err, mac_bytes=mac_bytes, stream_bytes=stream_bytes,
-                X=X, cpu=(lambda: cpu_baseline_diag(bn, X, qv, L=ctx.L)), ctx=ctx, blocks=blocks, centers=centers,
+                X=X, cpu=(lambda: cpu_level_diag(bn, X, qv, L=ctx.L)), ctx=ctx, blocks=blocks, centers=centers,
                 io=transfer_ms(bn, q, out))
 
 
@@ -666,9 +670,10 @@ def run_three_level(bn, args):
     """32 queries, each: coarse level (222,049 rows, 7 blocks) -> client decrypt, top-16 ->
     fine level (2 of 4 fine-pool blocks) -> top-64 -> rerank level (4 of 8 rerank-pool
     blocks, the last truncated to 11,696 rows) -> top-10.  Pool blocks are chosen by
-    hashing the kept ids (id mod pool size), deterministic and data-oblivious in cost.
-    Each query is dropped to --level primes (default 3) and its baby rotations are
-    computed once and reused by the three levels.
+    hashing the kept ids (id mod pool size), deterministic and data-oblivious in cost,
+    and passed to the scorer as block ids among the level's resident blocks.  Each
+    query is scored at all primes (or dropped to --level primes first) and its baby
+    rotations are computed once and reused by the three levels.
 
     Queries run in groups of --batch (default 4): every query scores all coarse blocks,
     so a group's coarse level is one cross-query batch (one pass over the coarse
@@ -677,7 +682,7 @@ def run_three_level(bn, args):
     and top-k of one query overlap the server's next level on the first."""
     w, fa, torch = bn.w, bn.fa, bn.torch
     top_ctx = bn.ctx
-    level = args.level if args.level else 3
+    level = args.level if args.level else w.L
     ctx = top_ctx.at_level(level) if level < w.L else top_ctx
     ex = w.extra
     S = w.slots
@@ -793,6 +798,23 @@ def run_three_level(bn, args):
     wall = (time.time() - t) / (steps * nq)
     lm = np.array(gpu_ms)
     gpu_q = float(lm.sum(axis=1).mean())
+    # the multiply-accumulate launches of one group, timed with the library's phase events
+    # (outside the timed queries): the coarse level's batched pass and one rerank level
+    ctx.profile(True)
+    m = min(gq, nq)
+    qi = [qcts[j] for j in range(m)] if qs is None else qs[:m]
+    ctx.prepare_batch(qi, w.B, outs=preps[:m], ws=ws_p)
+    ctx.score_batch(qi, preps[:m], pools["coarse"], w.d, w.B, outs=outs_c[:m], ws=ws_b)
+    ph_c = ctx.profile_read()
+    ctx.score_prepared(qi[0], preps[0], pools["rerank"], w.d, w.B, out=outs_r[0], ws=ws_s,
+                       block_ids=list(range(ex["rerank_blocks"])))
+    ph_r = ctx.profile_read()
+    ctx.profile(False)
+    ptw = ctx.L * w.n
+    mac_rooflines = {
+        "coarse_batch": roofline_of("k_mac_diag", mac_batch_bytes(m, n_coarse * w.G, w.B, ptw), ph_c["mac_ms"]),
+        "rerank": roofline_of(MAC_KERNEL, mac_batch_bytes(1, ex["rerank_blocks"] * w.G, w.B, ptw), ph_r["mac_ms"])}
+    mac_rooflines["coarse_batch"]["queries_per_pass"] = m
     n_scores = ex["coarse"] + ex["fine_blocks"] * S + (ex["rerank_blocks"] - 1) * S + ex["rerank_last"]
     ph = {"prepare_ms": float(lm[:, 0].mean()), "coarse_ms": float(lm[:, 1].mean()),
           "fine_ms": float(lm[:, 2].mean()), "rerank_ms": float(lm[:, 3].mean()), "query_gpu_ms": gpu_q,
@@ -800,6 +822,7 @@ def run_three_level(bn, args):
     blocks_q = n_coarse + ex["fine_blocks"] + ex["rerank_blocks"]
     return dict(ms=gpu_q, scores=n_scores, phases=ph, err=max(errs) if errs else None, mac_bytes=None,
                 stream_bytes=8 * blocks_q * w.d * ctx.L * w.n, queries=nq, level=ctx.L, coarse_group=gq,
+                mac_rooflines=mac_rooflines,
                 cpu=(lambda: cpu_baseline_diag(bn, g_coarse, queries[0], L=ctx.L, n_blocks=blocks_q,
                                                n_scores=n_scores)))
 
@@ -847,6 +870,78 @@ def oracle_at_level(bn, w, L):
         a, e = bn.wl.key_randomness(w, r, top.primes, top.dnum)
         return a[:par.dnum][:, idx], e[:par.dnum]
     return par, orc, rand
+
+
+def cpu_level_diag(bn, X, qv, L=None):
+    """The oracle timed over one whole level of the workload, on the host cores: the B-1
+    baby rotations of the query, then every block's product (its d diagonals'
+    multiply-accumulate, the giant steps and one ModDown per block), on the workload's
+    seeded rows, query and keys.  The keys and each block's integer encoding are prepared
+    outside the timed parts; the level time is the sum of the timed parts."""
+    from oracle import ckks
+    w = bn.w
+    B, G, S = w.B, w.G, w.slots
+    L = w.L if L is None else L
+    t_start = time.time()
+    par, orc, rand = oracle_at_level(bn, w, L)
+    keys = {r: orc.keygen(bn.s, r, *rand(r)) for r in ckks.steps_for_bsgs(w.d, B)}
+    ea, ee = bn.wl.enc_randomness(w, par.q)
+    ct = orc.encrypt(ckks.encode(ckks.replicate(pad(qv, w.d), par.slots), par.n, 40), ea, ee, bn.s)
+    log(f"[bench] oracle level at {L} primes: {len(keys)} keys ready ({time.time() - t_start:.1f}s)")
+    t = time.time()
+    qrot = orc.baby_rotations(ct, B, keys)
+    t_baby = time.time() - t
+    log(f"[bench] oracle level: {B - 1} baby rotations {t_baby:.2f}s")
+    t_blocks = []
+    for b in range(w.n_blocks):
+        rows = np.zeros((min(S, X.shape[0] - b * S), w.d))
+        rows[:, :w.dim] = X[b * S:(b + 1) * S]
+        c = ckks.layout_b_coeffs(rows, par, w.d, B)
+        pts = np.stack([ckks.to_residues(x, par.q) for x in c]).reshape(G, B, par.L, par.n)
+        del c
+        t = time.time()
+        orc.bsgs_block(qrot, pts, B, G, keys)
+        t_blocks.append(time.time() - t)
+        del pts
+        log(f"[bench] oracle level: block {b} ({len(rows)} rows) {t_blocks[-1]:.2f}s")
+    level_s = t_baby + sum(t_blocks)
+    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    log(f"[bench] oracle level at {L} primes: {level_s:.2f}s timed ({time.time() - t_start:.1f}s wall)")
+    return {"value": round(w.rows / level_s, 2), "unit": "scores/s", "cores": cores, "kind": "oracle",
+            "sample": f"one whole level timed: {B - 1} baby rotations + the products of all {w.n_blocks} blocks "
+                      f"({w.rows} rows, {w.n_blocks * w.d} diagonals, B={B}, G={G}) at {L} primes, the same "
+                      f"seeded rows, query and keys as the GPU level",
+            "level_s": round(level_s, 3), "phases_s": {"baby_rotations": round(t_baby, 3),
+                                                        "blocks": [round(x, 3) for x in t_blocks]},
+            "cpu_model": cpu_model()}
+
+
+def run_three_level_field(args):
+    """The full three-level query as a field of the default line: its own context (the
+    three_level workload's keys), 32 queries back to back at all 12 primes."""
+    import copy
+    a3 = copy.copy(args)
+    a3.workload, a3.baby_step, a3.level, a3.queries = "three_level", 0, 0, 0
+    a3.steps = 1
+    bn3 = Bench(a3)
+    r = run_three_level(bn3, a3)
+    w = bn3.w
+    ph = r["phases"]
+    res = {"workload": w.desc, "queries": r["queries"], "scoring_level_primes": r["level"],
+           "queries_per_coarse_pass": r["coarse_group"], "ms_per_query_gpu": round(r["ms"], 4),
+           "value": round(r["scores"] / (r["ms"] * 1e-3), 1), "unit": "scores/s",
+           "scores_per_query": r["scores"], "phases_ms": {k: round(v, 4) for k, v in ph.items()},
+           "with_client": {"query_wall_ms": round(ph["query_wall_ms"], 3),
+                           "scores_per_s": round(r["scores"] / (ph["query_wall_ms"] * 1e-3), 1)},
+           "query_hbm_floor_ms": round(r["stream_bytes"] / (HBM_PEAK_GBS * 1e9) * 1e3, 4),
+           "frac_of_hbm_roofline": round(r["stream_bytes"] / (HBM_PEAK_GBS * 1e9) * 1e3 / r["ms"], 4),
+           "max_abs_score_err": r["err"],
+           "roofline": r["mac_rooflines"]["coarse_batch"], "mac_rooflines": r["mac_rooflines"],
+           "cpu_baseline": None if args.no_cpu_baseline else r["cpu"]()}
+    del bn3, r
+    import torch
+    torch.cuda.empty_cache()
+    return res
 
 
 def cpu_baseline_rows(bn, X, qv, n_pts, steps):
@@ -977,6 +1072,8 @@ def main():
                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic, "kernel": MAC_KERNEL,
                     "algorithmic_bytes": r["mac_bytes"], "avg_ms": round(mac_ms, 4),
                     "measured_copy_GBs": copy_peak_GBs(bn)}
+    elif r.get("mac_rooflines"):
+        roofline = r["mac_rooflines"]["coarse_batch"]
     cpu = None
     if not args.no_cpu_baseline and r.get("cpu"):
         cpu = r["cpu"]()
@@ -1023,6 +1120,7 @@ def main():
         res["metric"] = ("server GPU time per query (3 levels) + aggregate server scores/s, 32 encrypted queries "
                          "back-to-back, one MI355X")
         res["ms_per_level"] = None
+        res["mac_rooflines"] = r["mac_rooflines"]
         # the client's part (decrypt, decode, top-k between levels) runs on the host between the
         # levels; the wall clock around whole queries, client included, is reported beside
         ph = r["phases"]
@@ -1063,6 +1161,10 @@ def main():
     if extra and args.membership:
         res["membership"] = run_membership(bn, args)
         log(f"[bench] face membership scan: {res['membership']['ms_per_query']:.3f} ms per query")
+    if extra and args.three_level:
+        res["three_level"] = run_three_level_field(args)
+        log(f"[bench] three-level query at {res['three_level']['scoring_level_primes']} primes: "
+            f"{res['three_level']['ms_per_query_gpu']:.3f} GPU ms per query")
     print(json.dumps(res), flush=True)
 
 

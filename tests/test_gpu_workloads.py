@@ -93,7 +93,11 @@ def test_tiny_rows_fullsize():
     assert np.max(np.abs(st.decode(o2, 0, 80)[:w.rows] - Xd @ q)) < 1e-4
 
 
-def _multi_block(w, check_block):
+def _multi_block(w):
+    """Every block of the level bit-exact against the oracle: all blocks enrolled from the
+    oracle's integer encoding (the same plaintexts on both sides), scored in one call as
+    bench.py launches it; then the same rows enrolled by the library's float encoder score
+    within 1e-4 of float64 as well."""
     st = Setup(w)
     X, centers = wl.candidate_rows(w)
     q = wl.query_vectors(w, 1, centers)[0]
@@ -101,43 +105,47 @@ def _multi_block(w, check_block):
     qp[:len(q)] = q
     ct, ct_o = st.encrypt_query(qp)
     S = st.par.slots
-    blocks, ref_coeffs = [], None
+    blocks, coeffs = [], []
     for b in range(w.n_blocks):
         rows = X[b * S:(b + 1) * S]
-        if b == check_block:
-            ref_coeffs = ckks.layout_b_coeffs(padded(rows.astype(np.float64), w.d), st.par, w.d, w.B)
-            blocks.append(st.ctx.encode_db_block_int(ref_coeffs))
-        else:
-            blocks.append(st.ctx.encode_db_block(rows, w.d, 1, w.B))
+        coeffs.append(ckks.layout_b_coeffs(padded(rows.astype(np.float64), w.d), st.par, w.d, w.B))
+        blocks.append(st.ctx.encode_db_block_int(coeffs[-1]))
+        say(f"[{w.name}] block {b}: {len(rows)} rows encoded by the oracle")
     say(f"[{w.name}] scoring {w.n_blocks} blocks (B={w.B}, G={w.G}) on the GPU")
     out = st.ctx.score_block(ct, blocks, w.d, 1, w.B)
-    got = st.export(out, w.n_blocks)[check_block]
-    say(f"[{w.name}] oracle: {w.B - 1} baby rotations + block {check_block}")
+    got = st.export(out, w.n_blocks)
+    say(f"[{w.name}] oracle: {w.B - 1} baby rotations")
     qrot = st.orc.baby_rotations(ct_o, w.B, st.keys)
-    pts_o = np.stack([ckks.to_residues(x, st.par.q) for x in ref_coeffs]).reshape(w.G, w.B, st.par.L, st.par.n)
-    ref = st.orc.bsgs_block(qrot, pts_o, w.B, w.G, st.keys)
-    assert np.array_equal(got, ref)
-    err = 0.0
     for b in range(w.n_blocks):
-        rows = X[b * S:(b + 1) * S].astype(np.float64)
-        z = st.decode(out, b, 80)
-        err = max(err, float(np.max(np.abs(z[:len(rows)] - rows @ q))))
-        if len(rows) < S:
-            err = max(err, float(np.max(np.abs(z[len(rows):]))))
-    say(f"[{w.name}] max |score - float64| = {err:.2e}")
-    assert err < 1e-4
+        pts_o = np.stack([ckks.to_residues(x, st.par.q) for x in coeffs[b]]).reshape(w.G, w.B, st.par.L,
+                                                                                    st.par.n)
+        assert np.array_equal(got[b], st.orc.bsgs_block(qrot, pts_o, w.B, w.G, st.keys)), b
+        say(f"[{w.name}] block {b} bit-exact")
+    del blocks, coeffs
+    fblocks = [st.ctx.encode_db_block(X[b * S:(b + 1) * S], w.d, 1, w.B) for b in range(w.n_blocks)]
+    outs = {"oracle-encoded": out, "float-encoded": st.ctx.score_block(ct, fblocks, w.d, 1, w.B)}
+    for name, o in outs.items():
+        err = 0.0
+        for b in range(w.n_blocks):
+            rows = X[b * S:(b + 1) * S].astype(np.float64)
+            z = st.decode(o, b, 80)
+            err = max(err, float(np.max(np.abs(z[:len(rows)] - rows @ q))))
+            if len(rows) < S:
+                err = max(err, float(np.max(np.abs(z[len(rows):]))))
+        say(f"[{w.name}] {name} blocks: max |score - float64| = {err:.2e}")
+        assert err < 1e-4
 
 
 def test_fine_level_fullsize():
-    """65,536 x 96-d (zero-padded to 128) at N=2^15: 4 diagonal blocks; block 3 bit-exact;
+    """65,536 x 96-d (zero-padded to 128) at N=2^15: 4 diagonal blocks, all bit-exact;
     every score is the exact 96-d cosine."""
-    _multi_block(wl.WORKLOADS["fine"], check_block=3)
+    _multi_block(wl.WORKLOADS["fine"])
 
 
 def test_rerank_level_fullsize():
-    """110,000 x 512-d at N=2^16, B=64: 4 blocks as bench.py times them; the partial last
-    block (11,696 rows) bit-exact; all 110,000 scores within 1e-4 of float64."""
-    _multi_block(wl.WORKLOADS["rerank"], check_block=3)
+    """110,000 x 512-d at N=2^16, B=64: 4 blocks as bench.py times them, all bit-exact (the
+    last one partial, 11,696 rows); all 110,000 scores within 1e-4 of float64."""
+    _multi_block(wl.WORKLOADS["rerank"])
 
 
 def test_rank_reduction_fullsize():
@@ -245,33 +253,132 @@ def test_rerank_level_at_three_primes_fullsize():
 
 
 def test_rerank_query_batch_fullsize():
-    """Cross-query batching at the rerank level's full size: 5 queries (one plaintext pass for
-    the first four, one for the fifth) against the 4 resident blocks.  Every output ciphertext
-    equals the single-query path word for word (that path is checked against the oracle above)
-    and every decrypted score is within 1e-4 of float64."""
+    """Cross-query batching at the rerank level's full size: 5 queries prepared together
+    (fa_prepare_batch: a step's key switches issued for all five) and scored in two plaintext
+    passes (four queries, then one) against the 4 resident blocks.  Every output ciphertext
+    equals the single-query path word for word; the second query's last block (scored in the
+    four-query pass) is bit-exact against the oracle; every decrypted score is within 1e-4 of
+    float64."""
     w = wl.WORKLOADS["rerank"]
-    st = Setup(w, oracle_steps=[])
+    st = Setup(w)
     X, centers = wl.candidate_rows(w)
     Q = wl.query_vectors(w, 5, centers)
     S = st.par.slots
-    blocks = [st.ctx.encode_db_block(X[b * S:(b + 1) * S], w.d, 1, w.B) for b in range(w.n_blocks)]
-    cts, preps = [], []
+    last = X[(w.n_blocks - 1) * S:]
+    c_last = ckks.layout_b_coeffs(last.astype(np.float64), st.par, w.d, w.B)
+    blocks = [st.ctx.encode_db_block(X[b * S:(b + 1) * S], w.d, 1, w.B) for b in range(w.n_blocks - 1)]
+    blocks.append(st.ctx.encode_db_block_int(c_last))
+    cts, cts_o = [], []
     for j, v in enumerate(Q):
         a, e = wl.enc_randomness(w, st.par.q, tag=j)
-        cts.append(st.ctx.encrypt(ckks.encode(ckks.replicate(v, S), st.par.n, 40), a, e))
-        preps.append(st.ctx.prepare_query(cts[-1], w.B))
+        m = ckks.encode(ckks.replicate(v, S), st.par.n, 40)
+        cts.append(st.ctx.encrypt(m, a, e))
+        cts_o.append(st.orc.encrypt(m, a, e, st.s) if j == 1 else None)
+    say(f"[batch] {len(Q)} queries prepared together")
+    preps = st.ctx.prepare_batch(cts, w.B)
     say(f"[batch] {len(Q)} queries x {w.n_blocks} blocks")
     outs = st.ctx.score_batch(cts, preps, blocks, w.d, w.B)
     err = 0.0
     for j in range(len(Q)):
-        single = st.ctx.score_prepared(cts[j], preps[j], blocks, w.d, w.B)
+        single = st.ctx.score_block(cts[j], blocks, w.d, 1, w.B)
         assert np.array_equal(st.export(outs[j], w.n_blocks), st.export(single, w.n_blocks)), j
         for b in range(w.n_blocks):
             rows = X[b * S:(b + 1) * S].astype(np.float64)
             z = st.decode(outs[j], b, 80)
             err = max(err, float(np.max(np.abs(z[:len(rows)] - rows @ Q[j]))))
-    say(f"[batch] max |score - float64| = {err:.2e}")
+    say(f"[batch] max |score - float64| = {err:.2e}; oracle: query 1's rotations and last block")
     assert err < 1e-4
+    pts_o = np.stack([ckks.to_residues(x, st.par.q) for x in c_last]).reshape(w.G, w.B, st.par.L, st.par.n)
+    ref = st.orc.bsgs_block(st.orc.baby_rotations(cts_o[1], w.B, st.keys), pts_o, w.B, w.G, st.keys)
+    assert np.array_equal(st.export(outs[1], w.n_blocks)[-1], ref)
+
+
+def test_three_level_fullsize_at_all_primes():
+    """The full three-level query at its own parameters (N=2^16, 12+3 primes), as bench.py runs
+    it: four queries prepared together and scored in one pass over the 7 coarse blocks
+    (222,049 centroids); the client decrypts, keeps the top 16 and names 2 of the 4 fine-pool
+    blocks by id; then the top 64 name 4 of the 8 rerank-pool blocks.  For the first query the
+    last coarse block, the second fine block and the last rerank block are bit-exact against
+    the oracle; every score of every level is within 1e-4 of float64."""
+    w = wl.WORKLOADS["three_level"]
+    ex = w.extra
+    st = Setup(w)
+    S = st.par.slots
+    coarse, centers = wl.candidate_rows(w, ex["coarse"], stream_extra=1)
+    pools, rows_of, ref_coeffs = {}, {}, {}
+    n_coarse = -(-ex["coarse"] // S)
+    rows_of["coarse"] = [coarse[b * S:(b + 1) * S] for b in range(n_coarse)]
+    for name, nb, extra in (("fine", ex["fine_pool_blocks"], 2), ("rerank", ex["rerank_pool_blocks"], 3)):
+        X, _ = wl.candidate_rows(w, nb * S, stream_extra=extra, centers=centers)
+        rows_of[name] = [X[b * S:(b + 1) * S] for b in range(nb)]
+    # the rerank level's last block is truncated like bench.py's (11,696 rows)
+    Q = wl.query_vectors(w, 4, centers)
+    # blocks a check may select are enrolled from the oracle's integer encoding (the same
+    # plaintexts on both sides); the other coarse blocks by the library's float encoder
+    for name in ("coarse", "fine", "rerank"):
+        pools[name] = []
+        for b, r in enumerate(rows_of[name]):
+            if name == "coarse" and b < n_coarse - 1:
+                pools[name].append(st.ctx.encode_db_block(r, w.d, 1, w.B))
+                continue
+            ref_coeffs[(name, b)] = ckks.layout_b_coeffs(r.astype(np.float64), st.par, w.d, w.B)
+            pools[name].append(st.ctx.encode_db_block_int(ref_coeffs[(name, b)]))
+        say(f"[3lvl-12] {name}: {len(pools[name])} resident blocks at 12 primes")
+    cts, q0_o = [], None
+    for j, v in enumerate(Q):
+        a, e = wl.enc_randomness(w, st.par.q, tag=j)
+        m = ckks.encode(ckks.replicate(v, S), st.par.n, 40)
+        cts.append(st.ctx.encrypt(m, a, e))
+        if j == 0:
+            q0_o = st.orc.encrypt(m, a, e, st.s)
+
+    def scores(out, nb, rows_list, qv, n_last=None):
+        zs, err = [], 0.0
+        for b in range(nb):
+            n_valid = len(rows_list[b]) if (b < nb - 1 or n_last is None) else n_last
+            z = st.decode(out, b, 80)[:n_valid]
+            err = max(err, float(np.max(np.abs(z - rows_list[b][:n_valid].astype(np.float64) @ qv))))
+            zs.append(z)
+        return np.concatenate(zs), err
+
+    def top(sc, k):
+        return np.lexsort((np.arange(len(sc)), -sc))[:k]
+
+    say("[3lvl-12] coarse: 4 queries prepared and scored in one pass")
+    preps = st.ctx.prepare_batch(cts, w.B)
+    outs_c = st.ctx.score_batch(cts, preps, pools["coarse"], w.d, w.B)
+    checks = {}
+    errs = []
+    for j in range(len(Q)):
+        sc, err = scores(outs_c[j], n_coarse, rows_of["coarse"], Q[j])
+        errs.append(err)
+        fsel = sorted(set(int(x) % ex["fine_pool_blocks"] for x in top(sc, ex["top_coarse"])))
+        fsel = (fsel + [b for b in range(ex["fine_pool_blocks"]) if b not in fsel])[:ex["fine_blocks"]]
+        out_f = st.ctx.score_prepared(cts[j], preps[j], pools["fine"], w.d, w.B, block_ids=fsel)
+        fr = [rows_of["fine"][b] for b in fsel]
+        sc, err = scores(out_f, len(fsel), fr, Q[j])
+        errs.append(err)
+        rsel = sorted(set(int(x) % ex["rerank_pool_blocks"] for x in top(sc, ex["top_fine"])))
+        rsel = (rsel + [b for b in range(ex["rerank_pool_blocks"]) if b not in rsel])[:ex["rerank_blocks"]]
+        out_r = st.ctx.score_prepared(cts[j], preps[j], pools["rerank"], w.d, w.B, block_ids=rsel)
+        rr = [rows_of["rerank"][b] for b in rsel]
+        _, err = scores(out_r, len(rsel), rr, Q[j], n_last=ex["rerank_last"])
+        errs.append(err)
+        if j == 0:
+            checks = {"coarse": (outs_c[0], n_coarse - 1, ("coarse", n_coarse - 1)),
+                      "fine": (out_f, len(fsel) - 1, ("fine", fsel[-1])),
+                      "rerank": (out_r, len(rsel) - 1, ("rerank", rsel[-1]))}
+        say(f"[3lvl-12] query {j}: fine blocks {fsel}, rerank blocks {rsel}")
+    say(f"[3lvl-12] max |score - float64| = {max(errs):.2e}")
+    assert max(errs) < 1e-4
+    say("[3lvl-12] oracle: the first query's baby rotations")
+    qrot = st.orc.baby_rotations(q0_o, w.B, st.keys)
+    for name, (out, b, key) in checks.items():
+        c = ref_coeffs[key]
+        pts_o = np.stack([ckks.to_residues(x, st.par.q) for x in c]).reshape(w.G, w.B, st.par.L, st.par.n)
+        got = st.export(out, b + 1)[b]
+        say(f"[3lvl-12] oracle: {name} block {b}")
+        assert np.array_equal(got, st.orc.bsgs_block(qrot, pts_o, w.B, w.G, st.keys)), name
 
 
 def test_three_level_coarse_batch_at_three_primes_fullsize():
