@@ -413,6 +413,23 @@ int fa_rotate_sum(fa_ctx* ctx, fa_buf* cts, int first_shift, int n_steps, void* 
  * automorphism while it writes out. */
 int fa_rotate(fa_ctx* ctx, const fa_buf* ct, int step, fa_buf* out, void* ws, size_t ws_bytes, void* stream);
 
+/* For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  The same
+ * rotation as fa_rotate, with its key-switch scratch (the decomposed and
+ * extended digits, the special-prime sums, the conversions) in a fixed device
+ * array of the library instead of a caller workspace: FA_STATIC_SCRATCH_BYTES
+ * per GPU, reserved on each GPU the library runs on until the process ends.
+ * The call allocates nothing.  FA_E_NOMEM if the context's rotation needs more
+ * scratch than that (fa_workspace_bytes(ctx, FA_OP_ROTATE, 1, 0, 1) >
+ * FA_STATIC_SCRATCH_BYTES; N=2^16 with 12+3 primes needs 63 MiB); FA_E_HIP if
+ * the array could not be located on this GPU when the context was created.
+ * Every call on one GPU uses that GPU's one array and leaves its contents
+ * behind (nothing in it has to start at zero): calls that overlap on one GPU
+ * (other streams, other host threads, other contexts) race.  Other errors as
+ * fa_rotate. */
+#define FA_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+int fa_rotate_static(fa_ctx* ctx, const fa_buf* ct, int step, fa_buf* out, void* stream);
+
 /* ---- the membership (threshold) path ------------------------------------
  * Section 3.1 ("Membership search"): the server returns an encrypted yes/no
  * for score >= tau |q_R| by approximating tau |q_R| = sqrt(tau^2 |q_R|^2)

@@ -404,6 +404,8 @@ static int ctx_build(const fa_params* prm, const std::vector<u64>& primes, fa_ct
   c->dnum = (c->L + c->K - 1) / c->K;
   c->log_scale = (int)prm->log_scale;
   (void)hipGetDevice(&c->device);
+  // set-up of fa_rotate_static: the fixed scratch array's address on this device
+  c->static_scratch = fa::static_scratch(c->device, &c->static_scratch_err);
   c->primes = primes;
   const int n = c->n, np = c->np, L = c->L, K = c->K;
   // P mod q_t, P^-1 mod q_t
@@ -2475,6 +2477,18 @@ int fa_rotate(fa_ctx* c, const fa_buf* ct, int step, fa_buf* out, void* ws, size
   rc = rotate_batch(c, (const double*)ct->dev, 1, step, (double*)out->dev, ar, (hipStream_t)stream);
   if (!rc) out_set(c, out, 2, 1, ct->log_scale);
   return rc;
+}
+
+int fa_rotate_static(fa_ctx* c, const fa_buf* ct, int step, fa_buf* out, void* stream) {
+  if (!c) return fail(FA_E_INVAL, "fa_rotate_static: null context");
+  const size_t need = rotate_ws(c, 1);
+  if (need > FA_STATIC_SCRATCH_BYTES)
+    return fail(FA_E_NOMEM, "fa_rotate_static: this context's rotation needs %zu bytes of scratch, the fixed array "
+                "holds %zu", need, (size_t)FA_STATIC_SCRATCH_BYTES);
+  if (!c->static_scratch)
+    return fail(FA_E_HIP, "fa_rotate_static: the fixed scratch array is not available on device %d: %s", c->device,
+                hipGetErrorString(c->static_scratch_err));
+  return fa_rotate(c, ct, step, out, c->static_scratch, FA_STATIC_SCRATCH_BYTES, stream);
 }
 
 int fa_rotate_sum(fa_ctx* c, fa_buf* cts_b, int first_shift, int n_steps, void* ws, size_t ws_bytes, void* stream) {

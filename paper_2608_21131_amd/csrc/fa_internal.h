@@ -44,6 +44,9 @@ static_assert(sizeof(LimbList) <= 4096, "LimbList is a kernel argument");
 
 struct fa_ctx {
   int logn, n, L, K, np, alpha, dnum, log_scale, device;
+  // the fixed scratch array's address on this context's device (fa_rotate_static)
+  void* static_scratch = nullptr;
+  hipError_t static_scratch_err = hipSuccess;
   std::vector<uint64_t> primes;   // [np] q_0..q_{L-1}, p_0..p_{K-1}
   std::vector<uint64_t> psi;      // chosen primitive 2N-th roots
   // device tables
@@ -93,6 +96,8 @@ struct fa_ctx {
 // --------------------------------------------------------------------------
 namespace fa {
 
+// device address of the library's fixed scratch array on `device` (current)
+void* static_scratch(int device, hipError_t* err);
 void ntt_fwd(const fa_ctx* c, const LimbList& l, hipStream_t s);
 void ntt_inv(const fa_ctx* c, const LimbList& l, hipStream_t s);
 // the second (column) pass of the inverse transform alone, ptr in place

@@ -22,6 +22,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdlib>
+#include <mutex>
 #include <type_traits>
 
 #include "fa_internal.h"
@@ -1466,7 +1467,35 @@ __global__ __launch_bounds__(256) void k_dec_combine(const double* __restrict__ 
 // ===========================================================================
 // launchers
 // ===========================================================================
+// The library's fixed scratch array (fa_rotate_static): every GPU that loads
+// the library holds its own copy.  The host refers to it only through the
+// device address hipGetSymbolAddress returns on that GPU.
+static __device__ __align__(256) double scratch[FA_STATIC_SCRATCH_BYTES / 8];
+
 namespace fa {
+
+// The address of `scratch` on `device` (which must be current), looked up once
+// per device and kept; nullptr (with the HIP error in *err) if the lookup fails.
+void* static_scratch(int device, hipError_t* err) {
+  constexpr int kMaxDev = 64;
+  static std::mutex mu;
+  static void* ptr[kMaxDev] = {};
+  static hipError_t res[kMaxDev] = {};
+  static bool done[kMaxDev] = {};
+  if (device < 0 || device >= kMaxDev) {
+    *err = hipErrorInvalidDevice;
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(mu);
+  if (!done[device]) {
+    void* p = nullptr;
+    res[device] = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    ptr[device] = res[device] == hipSuccess ? p : nullptr;
+    done[device] = true;
+  }
+  *err = res[device];
+  return ptr[device];
+}
 
 template <int SA>
 static void launch_fwd(const fa_ctx* c, const LimbList& l, hipStream_t s) {

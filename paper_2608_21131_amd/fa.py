@@ -111,6 +111,7 @@ SIGNATURES = {
     "fa_prepare_batch": (ctypes.c_int, [_vp, _bp, ctypes.c_int, ctypes.c_int, _bp, _vp, ctypes.c_size_t, _vp]),
     "fa_batch_workspace_bytes": (ctypes.c_size_t, [_vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int]),
     "fa_score_batch": (ctypes.c_int, [_vp, _bp, _bp, ctypes.c_int, _bp, ctypes.c_int, _i32p, ctypes.c_int, ctypes.c_int, ctypes.c_int, _bp, _vp, ctypes.c_size_t, _vp]),
+    "fa_rotate_static": (ctypes.c_int, [_vp, _bp, ctypes.c_int, _bp, _vp]),
     "fa_profile": (ctypes.c_int, [_vp, ctypes.c_int]),
     "fa_profile_read": (ctypes.c_int, [_vp, _f64p]),
 }
@@ -619,6 +620,13 @@ class Context:
         ms = np.zeros(4, dtype=np.float64)
         _check(self.lib.fa_profile_read(self.h, _ptr(ms, _f64p)))
         return {"baby_ms": ms[0], "mac_ms": ms[1], "giant_ms": ms[2], "total_ms": ms[3]}
+
+    def rotate_static(self, ct: Buf, step: int, out: Buf | None = None, stream=None) -> Buf:
+        """fa_rotate with the library's fixed scratch array: no workspace, no allocation in the call."""
+        out = self.new_ct() if out is None else out
+        fo = out.c()
+        _check(self.lib.fa_rotate_static(self.h, ctypes.byref(ct.c()), step, ctypes.byref(fo), _stream(stream)))
+        return out.take(fo)
 
     def rotate(self, ct: Buf, step: int, out: Buf | None = None, ws: torch.Tensor | None = None,
                stream=None) -> Buf:
