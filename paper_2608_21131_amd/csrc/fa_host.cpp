@@ -1227,15 +1227,18 @@ int fa_encode_projection(fa_ctx* c, const float* W, int d_in, int r, int baby_st
 namespace {
 constexpr int kRotBatch = 16;  // most rotations key-switched per launch group
 
-// Rotations per launch group actually used (1..kRotBatch; FA_ROT_BATCH tunes
-// it).  The environment is read once, by a thread-safe static initialiser.
-int rot_batch() {
+// Rotations per launch group of one query's baby steps (1..kRotBatch;
+// FA_ROT_BATCH overrides it): 8 with several key-switch digits (measured
+// 0.05 ms faster than 16 on the 12-prime rerank level), 16 with one digit (the
+// fused special-prime kernel's launches stay large).  The environment is read
+// once, by a thread-safe static initialiser.
+int rot_batch(const fa_ctx* c) {
   static const int v = [] {
     const char* e = getenv("FA_ROT_BATCH");
-    const int r = e ? atoi(e) : kRotBatch;
-    return (r < 1 || r > kRotBatch) ? kRotBatch : r;
+    const int r = e ? atoi(e) : 0;
+    return (r < 1 || r > kRotBatch) ? 0 : r;
   }();
-  return v;
+  return v ? v : (c->dnum > 1 ? 8 : kRotBatch);
 }
 
 struct Arena {
@@ -1272,7 +1275,7 @@ int lanes_wanted() {
 // workspace of the baby rotations (qrot itself is separate)
 size_t baby_ws(const fa_ctx* c, int B) {
   const size_t n = c->n, L = c->L, np = c->np, dn = c->dnum;
-  const size_t rb = std::max(1, std::min(rot_batch(), B - 1));
+  const size_t rb = std::max(1, std::min(rot_batch(c), B - 1));
   const size_t lanes = lanes_wanted();
   return rup(L * n) + rup(dn * np * n) + lanes * rup(rb * 2 * np * n) + lanes * rup(rb * 2 * L * n);
 }
@@ -1280,7 +1283,7 @@ size_t baby_ws(const fa_ctx* c, int B) {
 // rotated queries themselves are separate): one query's coefficient-form c1,
 // every query's extended digits, and per lane the key-switch products and
 // conversions of one launch group (about as many rotations as baby_ws's group)
-int batch_steps(int nq) { return std::max(1, rot_batch() / std::max(1, nq)); }
+int batch_steps(int nq) { return std::max(1, kRotBatch / std::max(1, nq)); }
 size_t baby_batch_ws(const fa_ctx* c, int nq, int B) {
   const size_t n = c->n, L = c->L, np = c->np, dn = c->dnum;
   const size_t items = (size_t)std::max(1, std::min(batch_steps(nq), B - 1)) * nq;
@@ -1503,7 +1506,7 @@ static int baby_phase(fa_ctx* c, const double* q, int B, double* qrot, Arena& ar
   if (B < 2) return FA_OK;
   for (int b = 1; b < B; ++b)
     if (!c->keys.count(b)) return fail(FA_E_NOKEY, "no rotation key for baby step %d", b);
-  const int rb = std::max(1, std::min(rot_batch(), B - 1));
+  const int rb = std::max(1, std::min(rot_batch(c), B - 1));
   const int lanes = lanes_wanted();
   const size_t mark = ar.used;
   double* y = ar.take(L * n);

@@ -152,6 +152,7 @@ struct MdKsItem {
   const double* b1;    // [L][N] or null: added to the second output polynomial
   double* out;         // [2][L][N]
   uint32_t gal;
+  uint32_t inv_gal;    // gal^-1 mod 2N (set by the launcher)
 };
 // nq > 1: the items come in groups of nq (g*nq .. g*nq+nq-1) sharing one key
 // (the same rotation of nq queries); their workgroups run back to back on one
@@ -167,6 +168,7 @@ struct KsItem {
   double* u;          // [2][np][N]
   const double* c0;   // [L][N] or null: adds P * sigma(c0) to u0 on the ciphertext primes
   uint32_t gal;       // Galois element
+  uint32_t inv_gal;   // gal^-1 mod 2N (set by the launcher)
 };
 // t0 > 0: only primes t0..np-1 (the special primes when t0 = L)
 // nq > 1: items grouped by key as for moddown_ks (count % nq == 0)

@@ -447,14 +447,37 @@ __device__ __forceinline__ bool ks_decode(unsigned W, int nx, int ny, int nq, in
   return true;
 }
 
-template <int DNUM, int ROWS>
+// One query's key switches (nq == 1): ids decoded source-tile-major with the
+// items fastest within an XCD, so the workgroups one XCD runs back to back (ids
+// 8 apart) take the same source tile x of prime y for every rotation of the
+// launch; the digits and c0 words of that tile, which every rotation gathers
+// (through its own automorphism, into its own output tile), are read from HBM
+// once and from that XCD's L2 after.  Returns false for the padding ids.
+__device__ __forceinline__ bool ks_decode_src(unsigned W, int nx, int ny, int m, int& x, int& y, int& item) {
+  const unsigned j8 = W >> 3;
+  item = (int)(j8 % (unsigned)m);
+  const unsigned rest = (j8 / (unsigned)m) * 8u + (W & 7u);
+  if (rest >= (unsigned)(nx * ny)) return false;
+  x = (int)(rest % (unsigned)nx);
+  y = (int)(rest / (unsigned)nx);
+  return true;
+}
+
+template <int DNUM, int ROWS, bool NT>
 __global__ __launch_bounds__(256) void k_moddown_ks_b(MdKsArgs args, const DevPrime* __restrict__ pr,
                                                       const double* __restrict__ twt, const double* __restrict__ twr,
                                                       int logn, int L, int np, int alpha, int nq, int ngroup) {
   __shared__ double sm[ROWS * ROWW];
   const int n = 1 << logn;
   int tile, t, item;
-  if (!ks_decode(blockIdx.x, (n >> 8) / ROWS, L, nq, ngroup, tile, t, item)) return;
+  if (nq == 1) {
+    int src;
+    if (!ks_decode_src(blockIdx.x, (n >> 8) / ROWS, L, ngroup, src, t, item)) return;
+    // the output tile whose automorphism image is the source tile
+    tile = (int)(perm((uint32_t)src * (ROWS * 256u), args.it[item].inv_gal, logn) / (ROWS * 256u));
+  } else if (!ks_decode(blockIdx.x, (n >> 8) / ROWS, L, nq, ngroup, tile, t, item)) {
+    return;
+  }
   const fa::MdKsItem& it = args.it[item];
   const int row0 = tile * ROWS;
   const uint32_t k0 = (uint32_t)row0 * 256u + threadIdx.x;  // this thread's words: k0 + 256 j, j < ROWS
@@ -474,8 +497,12 @@ __global__ __launch_bounds__(256) void k_moddown_ks_b(MdKsArgs args, const DevPr
 #pragma unroll
     for (int j = 0; j < ROWS; ++j) {
       const double x = src[perm(k0 + 256u * j, it.gal, logn)];
-      u0[j] += mul(x, kb[256 * j], q, qinv);
-      u1[j] += mul(x, ka[256 * j], q, qinv);
+      // NT (one query): each key word is used once, so it streams past the
+      // caches; several queries share it through L2 (see ks_decode)
+      const double b = NT ? __builtin_nontemporal_load(kb + 256 * j) : kb[256 * j];
+      const double a = NT ? __builtin_nontemporal_load(ka + 256 * j) : ka[256 * j];
+      u0[j] += mul(x, b, q, qinv);
+      u1[j] += mul(x, a, q, qinv);
     }
   }
 #pragma unroll
@@ -488,7 +515,7 @@ __global__ __launch_bounds__(256) void k_moddown_ks_b(MdKsArgs args, const DevPr
   for (int j = 0; j < ROWS; ++j) {
     const int e = threadIdx.x + 256 * j;
     const double r = mulc(u0[j] - sm[lds_row(e >> 8, e & 255)], pv, pvp, q) + it.c0[o + perm(k0 + 256u * j, it.gal, logn)];
-    it.out[o + k0 + 256 * j] = canon_full(r, q, qinv);
+    __builtin_nontemporal_store(canon_full(r, q, qinv), it.out + o + k0 + 256 * j);
   }
   __syncthreads();
   fwd_b_lds(it.conv + (size_t)L * n + o, row0, ROWS, T, F, q, qinv, sm);
@@ -497,7 +524,7 @@ __global__ __launch_bounds__(256) void k_moddown_ks_b(MdKsArgs args, const DevPr
     const int e = threadIdx.x + 256 * j;
     double r = mulc(u1[j] - sm[lds_row(e >> 8, e & 255)], pv, pvp, q);
     if (it.b1) r += it.b1[o + k0 + 256 * j];
-    it.out[(size_t)L * n + o + k0 + 256 * j] = canon_full(r, q, qinv);
+    __builtin_nontemporal_store(canon_full(r, q, qinv), it.out + (size_t)L * n + o + k0 + 256 * j);
   }
 }
 
@@ -572,7 +599,13 @@ __global__ __launch_bounds__(256) void k_ks_inner(KsArgs args, const DevPrime* _
                                                   int np, int alpha, int accumulate, int t0, int nq, int ngroup) {
   const int n = 1 << logn;
   int kx, tr, item;
-  if (!ks_decode(blockIdx.x, n / 256, np - t0, nq, ngroup, kx, tr, item)) return;
+  if (nq == 1) {
+    int src;
+    if (!ks_decode_src(blockIdx.x, n / 256, np - t0, ngroup, src, tr, item)) return;
+    kx = (int)(perm((uint32_t)src * 256u, args.it[item].inv_gal, logn) / 256u);  // see k_moddown_ks_b
+  } else if (!ks_decode(blockIdx.x, n / 256, np - t0, nq, ngroup, kx, tr, item)) {
+    return;
+  }
   const int k = kx * 256 + threadIdx.x;
   const int t = t0 + tr;
   const fa::KsItem& it = args.it[item];
@@ -620,7 +653,13 @@ __global__ __launch_bounds__(256) void k_ks_inv_b(KsArgs args, const DevPrime* _
   const int n = 1 << logn;
   const int rows = (n >> 8) < 16 ? (n >> 8) : 16;
   int tile, tr, item;
-  if (!ks_decode(blockIdx.x, (n >> 8) / rows, np - L, nq, ngroup, tile, tr, item)) return;
+  if (nq == 1) {
+    int src;
+    if (!ks_decode_src(blockIdx.x, (n >> 8) / rows, np - L, ngroup, src, tr, item)) return;
+    tile = (int)(perm((uint32_t)src * (uint32_t)(rows * 256), args.it[item].inv_gal, logn) / (uint32_t)(rows * 256));
+  } else if (!ks_decode(blockIdx.x, (n >> 8) / rows, np - L, nq, ngroup, tile, tr, item)) {
+    return;
+  }
   const int t = L + tr;
   const fa::KsItem& it = args.it[item];
   const double q = pr[t].q, qinv = pr[t].qinv;
@@ -1651,8 +1690,16 @@ void moddown(const fa_ctx* c, const MdItem* items, int count, hipStream_t s, boo
 // 1-D grid of the key-switch kernels: nx * ny * ngroup work units, padded to
 // whole groups of eight per query when nq > 1 (see ks_decode)
 static unsigned ks_grid(int nx, int ny, int nq, int ngroup) {
+  if (nq == 1) return 8u * ngroup * (((unsigned)nx * ny + 7) / 8);  // ks_decode_src
   const unsigned units = (unsigned)nx * ny * ngroup;
-  return nq > 1 ? 8u * nq * ((units + 7) / 8) : units;
+  return 8u * nq * ((units + 7) / 8);
+}
+
+// inverse of an odd Galois element modulo 2N (Newton's iteration modulo 2^32)
+static uint32_t inv_galois(uint32_t g, int logn) {
+  uint32_t x = g;
+  for (int i = 0; i < 5; ++i) x *= 2u - g * x;
+  return x & ((2u << logn) - 1u);
 }
 
 template <int DNUM>
@@ -1663,12 +1710,15 @@ static void launch_moddown_ks(const fa_ctx* c, const MdKsArgs& a, int m, int nq,
   const int rows = (c->n >> 8) < 8 ? (c->n >> 8) : 8;
   const int ngroup = m / nq;
   dim3 gb(ks_grid((c->n >> 8) / rows, c->L, nq, ngroup));
-  if (rows == 8)
-    hipLaunchKernelGGL((k_moddown_ks_b<DNUM, 8>), gb, dim3(256), 0, s, a, c->d_pr, c->d_twt_fwd, c->d_twr_fwd,
+  if (rows == 8 && nq == 1)
+    hipLaunchKernelGGL((k_moddown_ks_b<DNUM, 8, true>), gb, dim3(256), 0, s, a, c->d_pr, c->d_twt_fwd, c->d_twr_fwd,
                        c->logn, c->L, c->np, c->alpha, nq, ngroup);
+  else if (rows == 8)
+    hipLaunchKernelGGL((k_moddown_ks_b<DNUM, 8, false>), gb, dim3(256), 0, s, a, c->d_pr, c->d_twt_fwd,
+                       c->d_twr_fwd, c->logn, c->L, c->np, c->alpha, nq, ngroup);
   else
-    hipLaunchKernelGGL((k_moddown_ks_b<DNUM, 4>), gb, dim3(256), 0, s, a, c->d_pr, c->d_twt_fwd, c->d_twr_fwd,
-                       c->logn, c->L, c->np, c->alpha, nq, ngroup);
+    hipLaunchKernelGGL((k_moddown_ks_b<DNUM, 4, false>), gb, dim3(256), 0, s, a, c->d_pr, c->d_twt_fwd,
+                       c->d_twr_fwd, c->logn, c->L, c->np, c->alpha, nq, ngroup);
 }
 
 void moddown_ks(const fa_ctx* c, const MdKsItem* items, int count, hipStream_t s, int nq) {
@@ -1676,7 +1726,10 @@ void moddown_ks(const fa_ctx* c, const MdKsItem* items, int count, hipStream_t s
   for (int off = 0; off < count; off += chunk) {
     const int m = count - off < chunk ? count - off : chunk;
     MdKsArgs a;
-    for (int i = 0; i < m; ++i) a.it[i] = items[off + i];
+    for (int i = 0; i < m; ++i) {
+      a.it[i] = items[off + i];
+      a.it[i].inv_gal = inv_galois(a.it[i].gal, c->logn);
+    }
     switch (c->dnum) {
       case 1: launch_moddown_ks<1>(c, a, m, nq, s); break;
       case 2: launch_moddown_ks<2>(c, a, m, nq, s); break;
@@ -1704,7 +1757,10 @@ void ks_inner(const fa_ctx* c, const KsItem* items, int count, bool accumulate, 
   for (int off = 0; off < count; off += chunk) {
     KsArgs a;
     const int m = count - off < chunk ? count - off : chunk;
-    for (int i = 0; i < m; ++i) a.it[i] = items[off + i];
+    for (int i = 0; i < m; ++i) {
+      a.it[i] = items[off + i];
+      a.it[i].inv_gal = inv_galois(a.it[i].gal, c->logn);
+    }
     switch (c->dnum) {
       case 1: launch_ks<1>(c, a, m, accumulate, s, t0, nq); break;
       case 2: launch_ks<2>(c, a, m, accumulate, s, t0, nq); break;
@@ -1734,7 +1790,10 @@ void ks_inv_b(const fa_ctx* c, const KsItem* items, int count, hipStream_t s, in
   for (int off = 0; off < count; off += chunk) {
     KsArgs a;
     const int m = count - off < chunk ? count - off : chunk;
-    for (int i = 0; i < m; ++i) a.it[i] = items[off + i];
+    for (int i = 0; i < m; ++i) {
+      a.it[i] = items[off + i];
+      a.it[i].inv_gal = inv_galois(a.it[i].gal, c->logn);
+    }
     launch_ks_inv_b<1>(c, a, m, s, nq);
   }
 }

@@ -119,11 +119,13 @@ SIGNATURES = {
 _LIB = None
 
 
-def load_library(path: str = LIB_PATH):
-    """Load libfa.so and declare its signatures (raises if it was never built)."""
+def load_library(path: str | None = None):
+    """Load libfa.so (the in-tree build, or the file FA_LIBRARY names) and declare its
+    signatures; raises if it was never built."""
     global _LIB
     if _LIB is not None:
         return _LIB
+    path = path or os.environ.get("FA_LIBRARY") or LIB_PATH
     if not os.path.exists(path):
         raise RuntimeError(f"libfa.so not built ({path}); run __graft_entry__.build()")
     lib = ctypes.CDLL(path)
