@@ -73,7 +73,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-check", action="store_true", help="skip the decrypt-and-compare check")
     ap.add_argument("--copy-calib", action="store_true",
-                    help="run one plain 1 GiB device copy before the timed region (HBM counter calibration)")
+                    help="before the timed region, fill, copy and sum one plain 1 GiB buffer (HBM counter "
+                         "calibration: known writes, reads and writes, reads)")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "k_mac_diag3_rerank110k_traffic.md"),
                     help="rocprofv3 counter summary with the measured per-launch HBM bytes of the "
                          "multiply-accumulate kernel (used only while that kernel's source is unchanged)")
@@ -155,10 +156,11 @@ def run_diag_level(bn, args):
     if args.copy_calib:
         src = bn.torch.empty(1 << 27, dtype=bn.torch.float64, device="cuda")
         dst = bn.torch.empty_like(src)
-        src.fill_(1.0)
-        dst.copy_(src)
+        src.fill_(1.0)  # 1 GiB written
+        dst.copy_(src)  # 1 GiB read, 1 GiB written
+        tot = src.sum()  # 1 GiB read, nothing but the scalar written
         bn.torch.cuda.synchronize()
-        del src, dst
+        del src, dst, tot
     ctx.profile(True)
     phases = []
 

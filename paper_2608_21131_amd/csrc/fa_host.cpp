@@ -372,6 +372,7 @@ void fa_ctx_destroy(fa_ctx* c) {
   (void)hipFree(c->d_twr_inv);
   (void)hipFree(c->d_mu_hat);
   (void)hipFree(c->d_md_hat);
+  (void)hipFree(c->d_mu_scale);
   (void)hipFree(c->d_s);
   for (auto& kv : c->keys) (void)hipFree(kv.second);
   (void)hipFree(c->d_rlk);
@@ -503,7 +504,8 @@ static int ctx_build(const fa_params* prm, const std::vector<u64>& primes, fa_ct
       (rc = dev_alloc(&c->d_twa_inv, twa_i.size())) || (rc = dev_alloc(&c->d_twt_fwd, twt_f.size())) ||
       (rc = dev_alloc(&c->d_twt_inv, twt_i.size())) || (rc = dev_alloc(&c->d_twr_fwd, twr_f.size())) ||
       (rc = dev_alloc(&c->d_twr_inv, twr_i.size())) || (rc = dev_alloc(&c->d_mu_hat, mu_hat.size())) ||
-      (rc = dev_alloc(&c->d_md_hat, md_hat.size())) || (rc = dev_alloc(&c->d_s, (size_t)np * n))) {
+      (rc = dev_alloc(&c->d_md_hat, md_hat.size())) || (rc = dev_alloc(&c->d_mu_scale, (size_t)L)) ||
+      (rc = dev_alloc(&c->d_s, (size_t)np * n))) {
     fa_ctx_destroy(c);
     return rc;
   }
@@ -520,6 +522,7 @@ static int ctx_build(const fa_params* prm, const std::vector<u64>& primes, fa_ct
   up(c->d_twr_inv, twr_i);
   up(c->d_mu_hat, mu_hat);
   up(c->d_md_hat, md_hat);
+  up(c->d_mu_scale, c->h_mu_scale);
   if (e == hipSuccess) e = hipMemset(c->d_s, 0, (size_t)np * n * 8);
   if (e != hipSuccess) {
     fa_ctx_destroy(c);
@@ -1303,9 +1306,10 @@ size_t giant_scratch_ws(const fa_ctx* c, int nb, int d, int B) {
          rup(cb * 2 * L * n);
 }
 // workspace of the multiply-accumulate and the giant steps of nq queries
+// (the giant steps of all nq queries run together, over nq * nb blocks)
 size_t giant_ws(const fa_ctx* c, int nb, int d, int B, int nq = 1) {
   const size_t G = d / B;
-  return (size_t)nq * rup((size_t)nb * G * 2 * c->L * c->n) + giant_scratch_ws(c, nb, d, B);
+  return rup((size_t)nq * nb * G * 2 * c->L * c->n) + giant_scratch_ws(c, nq * nb, d, B);
 }
 size_t qrot_words(const fa_ctx* c, int B) { return (size_t)(B - 1) * 2 * c->L * c->n + 1; }
 size_t score_ws(const fa_ctx* c, int nb, int d, int B) {
@@ -1320,15 +1324,15 @@ static void modup(fa_ctx* c, const double* cts, size_t ct_stride, int batch, dou
                   double* ext, size_t ext_stride, hipStream_t s, bool pass_b = true) {
   const size_t n = c->n, L = c->L;
   {
-    fa::LimbBatch inv(c, s, false);
+    // the row pass of the inverse transform; the fused ModUp kernel finishes it
+    fa::LimbBatch inv(c, s, false, false, true);
     for (int b = 0; b < batch; ++b)
       for (size_t t = 0; t < L; ++t)
-        inv.add(y + (size_t)b * y_stride + t * n, (int)t, cts + (size_t)b * ct_stride + (L + t) * n,
-                c->h_mu_scale[t]);
+        inv.add(y + (size_t)b * y_stride + t * n, (int)t, cts + (size_t)b * ct_stride + (L + t) * n);
   }
   std::vector<fa::MuItem> it(batch);
   for (int b = 0; b < batch; ++b) it[b] = {y + (size_t)b * y_stride, ext + (size_t)b * ext_stride};
-  fa::modup_ntt(c, it.data(), batch, s, pass_b);
+  fa::modup_fused(c, it.data(), batch, s, pass_b);
 }
 
 // ModDown of `count` polynomials u_i = u + i * np * N over Q u P (NTT form):
@@ -1594,13 +1598,14 @@ static int baby_phase_batch(fa_ctx* c, const double* const* qs, int nq, int B, d
 // P.  The first pass of every giant's ModUp runs on the lanes (round-robin over
 // g); one fused kernel then finishes the transforms and forms the key-switch
 // sums.  Scratch comes from ar (giant_ws minus the accumulators).
-static int giant_phase(fa_ctx* c, const double* acc, int nb, int G, int B, double* out, Arena& ar, hipStream_t s) {
+static int giant_phase(fa_ctx* c, const double* acc, int nb, int G, int B, double* const* outs, Arena& ar,
+                       hipStream_t s) {
   const size_t n = c->n, L = c->L, np = c->np, dn = c->dnum;
   const size_t ctw = 2 * L * n;
   const size_t astride = (size_t)G * ctw;
   if (G == 1) {
     for (int blk = 0; blk < nb; ++blk)
-      HIPCHK(hipMemcpyAsync(out + (size_t)blk * ctw, acc + (size_t)blk * ctw, ctw * 8, hipMemcpyDeviceToDevice, s));
+      HIPCHK(hipMemcpyAsync(outs[blk], acc + (size_t)blk * ctw, ctw * 8, hipMemcpyDeviceToDevice, s));
     return FA_OK;
   }
   const int lanes = lanes_wanted();
@@ -1652,8 +1657,8 @@ static int giant_phase(fa_ctx* c, const double* acc, int nb, int G, int B, doubl
       const double* acc0 = accb + (size_t)blk * astride;
       bases[2 * blk] = acc0;
       bases[2 * blk + 1] = acc0 + L * n;
-      douts[2 * blk] = out + (size_t)(b0 + blk) * ctw;
-      douts[2 * blk + 1] = out + (size_t)(b0 + blk) * ctw + L * n;
+      douts[2 * blk] = outs[b0 + blk];
+      douts[2 * blk + 1] = outs[b0 + blk] + L * n;
     }
     moddown_polys(c, usum, 2 * cb, gconv, bases.data(), douts.data(), gals.data(), s);
   }
@@ -1677,14 +1682,20 @@ static int mac_giant_phase(fa_ctx* c, const double* const* q, const double* cons
   const int G = d / B;
   int rc = check_giant_keys(c, d, B);
   if (rc) return rc;
+  // the queries' accumulators one after the other: their giant steps then run
+  // as those of nq * nb blocks (larger launches, keys shared across queries)
+  double* acc_all = ar.take((size_t)nq * nb * G * ctw);
+  if (!acc_all) return fail(FA_E_NOMEM, "workspace too small for score_block");
   std::vector<double*> acc(nq);
-  for (int j = 0; j < nq; ++j)
-    if (!(acc[j] = ar.take((size_t)nb * G * ctw))) return fail(FA_E_NOMEM, "workspace too small for score_block");
+  std::vector<double*> bouts((size_t)nq * nb);
+  for (int j = 0; j < nq; ++j) {
+    acc[j] = acc_all + (size_t)j * nb * G * ctw;
+    for (int blk = 0; blk < nb; ++blk) bouts[(size_t)j * nb + blk] = outs[j] + (size_t)blk * ctw;
+  }
   if (c->prof) HIPCHK(hipEventRecord(c->ev[1], s));
   fa::mac_diag(c, q, qrot, nq, blocks, nb, B, G, acc.data(), s);
   if (c->prof) HIPCHK(hipEventRecord(c->ev[2], s));
-  for (int j = 0; j < nq; ++j)
-    if ((rc = giant_phase(c, acc[j], nb, G, B, outs[j], ar, s))) return rc;
+  if ((rc = giant_phase(c, acc_all, nq * nb, G, B, bouts.data(), ar, s))) return rc;
   if (c->prof) {
     HIPCHK(hipEventRecord(c->ev[3], s));
     c->prof_done = true;
@@ -1731,7 +1742,9 @@ static int score_diag_enc(fa_ctx* c, const double* q, const double* const* block
   fa::mac_diag_ct(c, q, qrot, blocks, nb, B, G, acc3, s);
   if (c->prof) HIPCHK(hipEventRecord(c->ev[2], s));
   if ((rc = relin_batch(c, acc3, nb * G, acc, ar, s))) return rc;
-  if ((rc = giant_phase(c, acc, nb, G, B, out, ar, s))) return rc;
+  std::vector<double*> bouts(nb);
+  for (int blk = 0; blk < nb; ++blk) bouts[blk] = out + (size_t)blk * 2 * ln;
+  if ((rc = giant_phase(c, acc, nb, G, B, bouts.data(), ar, s))) return rc;
   if (c->prof) {
     HIPCHK(hipEventRecord(c->ev[3], s));
     c->prof_done = true;

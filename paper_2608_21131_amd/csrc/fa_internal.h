@@ -62,6 +62,7 @@ struct fa_ctx {
   double* d_twr_inv = nullptr;
   double* d_mu_hat = nullptr;     // [dnum][alpha][np]   (D_i/d_j) mod prime t
   double* d_md_hat = nullptr;     // [K][L]              (P/p_k) mod q_t
+  double* d_mu_scale = nullptr;   // [L] device copy of h_mu_scale
   // host copies used to build per-limb constants
   std::vector<double> h_ninv;     // [np] N^-1 mod prime
   std::vector<double> h_mu_scale; // [L] N^-1 (D_i/q_t)^-1 mod q_t, t in digit i
@@ -102,6 +103,8 @@ void ntt_fwd(const fa_ctx* c, const LimbList& l, hipStream_t s);
 void ntt_inv(const fa_ctx* c, const LimbList& l, hipStream_t s);
 // the second (column) pass of the inverse transform alone, ptr in place
 void ntt_inv_a(const fa_ctx* c, const LimbList& l, hipStream_t s);
+// the first (row) pass of the inverse transform alone, src -> ptr
+void ntt_inv_b(const fa_ctx* c, const LimbList& l, hipStream_t s);
 
 // Batched forward / inverse over `count` polynomials laid out as
 // base + i * stride (words) whose prime index is prime_of(i) = i % period
@@ -112,16 +115,19 @@ void ntt_inv_strided(const fa_ctx* c, double* base, size_t stride, int count, in
                      hipStream_t s);
 
 // ModUp: for each item, ext[i][t] = NTT(Conv_{digit i -> t}(y)) for every digit
-// i and prime t outside the digit, where y ([L][N]) holds the coefficients of
-// c1 already multiplied by (D_i/q_t)^-1 (canonical).  Own-digit limbs of ext
-// are not written: the key-switch kernel reads them from c1.
+// i and prime t outside the digit, where y ([L][N]) is c1 after the first
+// (row) pass of its inverse transform.  One kernel finishes the inverse
+// (column pass and the scaling by N^-1 (D_i/q_t)^-1, canonical), converts and
+// runs the first forward pass of every converted limb, so the coefficients
+// never reach HBM.  Own-digit limbs of ext are not written: the key-switch
+// kernels read them from c1.
 #define FA_MAXMU 16
 struct MuItem {
-  const double* y;  // [L][N]
+  const double* y;  // [L][N], row pass of the inverse transform done
   double* ext;      // [dnum][np][N]
 };
 // pass_b false: only the first forward pass (the giant-step kernel finishes it)
-void modup_ntt(const fa_ctx* c, const MuItem* items, int count, hipStream_t s, bool pass_b = true);
+void modup_fused(const fa_ctx* c, const MuItem* items, int count, hipStream_t s, bool pass_b = true);
 
 // ModDown with its finish: out = base[pi_gal] + (uQ - NTT(Conv_{P->Q}(yP))) * P^-1,
 // where yP ([K][N]) holds the special-prime coefficients of the key-switch
@@ -254,10 +260,10 @@ void dec_combine(const fa_ctx* c, const double* ct, double* out, hipStream_t s);
 struct LimbBatch {
   const fa_ctx* c;
   hipStream_t s;
-  bool fwd, a_only;  // a_only (inverse): the second pass alone, in place
+  bool fwd, a_only, b_only;  // inverse: a_only the second pass alone (in place), b_only the first alone
   LimbList l;
-  LimbBatch(const fa_ctx* c_, hipStream_t s_, bool fwd_, bool a_only_ = false)
-      : c(c_), s(s_), fwd(fwd_), a_only(a_only_) {
+  LimbBatch(const fa_ctx* c_, hipStream_t s_, bool fwd_, bool a_only_ = false, bool b_only_ = false)
+      : c(c_), s(s_), fwd(fwd_), a_only(a_only_), b_only(b_only_) {
     l.n = 0;
   }
   // scale < 0: N^-1 of the prime
@@ -272,6 +278,7 @@ struct LimbBatch {
     if (l.n) {
       if (fwd) ntt_fwd(c, l, s);
       else if (a_only) ntt_inv_a(c, l, s);
+      else if (b_only) ntt_inv_b(c, l, s);
       else ntt_inv(c, l, s);
       l.n = 0;
     }

@@ -185,36 +185,157 @@ __global__ __launch_bounds__(256) void k_ntt_fwd_a(LimbList ll, const DevPrime* 
 }
 
 // ModUp, first pass: ext[i][t] = pass A of Conv_{digit i -> t}(y), for every
-// digit i and prime t outside the digit; y holds the digit-scaled
-// coefficients of c1 (inverse transform with the conversion constant folded
-// into its final scaling).
+// digit i and prime t outside the digit.
 struct MuArgs {
   fa::MuItem it[FA_MAXMU];
 };
 
+// ModUp from the row-passed c1, fused: a workgroup owns one column tile of
+// one digit i.  It finishes the inverse transform of the digit's limbs on
+// that tile (column pass, then the scaling by N^-1 (D_i/d_j)^-1, leaving
+// canonical residues, exactly as k_ntt_inv_a does) and keeps the results in
+// registers; then for every prime t outside the digit it forms the fast basis
+// conversion of the tile (as ConvLd does) and runs the first forward pass on
+// it (as fwd_a_body does), writing ext[i][t].  Each source word is read once
+// and the coefficients never leave the chip.  With ngrp > 1 the targets of a
+// digit are split into ngrp contiguous groups, one per workgroup (each group
+// repeats the inverse pass): small launches get more workgroups.
 template <int SA, int ALPHA>
-__global__ __launch_bounds__(256) void k_modup_a(MuArgs args, const DevPrime* __restrict__ pr,
-                                                 const double* __restrict__ twa, const double* __restrict__ hat,
-                                                 int logn, int L, int np) {
+__global__ __launch_bounds__(256) void k_modup_fused(MuArgs args, const DevPrime* __restrict__ pr,
+                                                     const double* __restrict__ twa_f,
+                                                     const double* __restrict__ twa_i,
+                                                     const double* __restrict__ hat,
+                                                     const double* __restrict__ scale, int logn, int L, int np,
+                                                     int ngrp) {
   using P = PassA<SA>;
+  constexpr int NU = P::TILE / P::E1 / 256;   // tile units per thread in the E1 layout
+  constexpr int NU2 = P::TILE / P::E2 / 256;  // ... in the E2 layout
+  static_assert(NU * P::E1 * 256 == P::TILE && NU2 * P::E2 * 256 == P::TILE, "whole units per thread");
   __shared__ double sm[P::TILE];
-  const int i = blockIdx.y / np, t = blockIdx.y % np;
-  const int lo = i * ALPHA;
-  if (t >= lo && t < lo + ALPHA && t < L) return;  // own limbs: read from c1 directly
+  const int i = blockIdx.y / ngrp, grp = blockIdx.y % ngrp;
   const fa::MuItem& it = args.it[blockIdx.z];
   const int n = 1 << logn;
-  ConvLd<ALPHA> ld;
-  ld.q = pr[t].q;
-  ld.qinv = pr[t].qinv;
+  const int lo = i * ALPHA;
+  const int nl = L - lo < ALPHA ? L - lo : ALPHA;  // a short last digit has fewer limbs
+  const int per = (np - nl + ngrp - 1) / ngrp;      // targets of this group: k0 <= k < k0 + per
+  const int k0 = grp * per;
+  const int col0 = blockIdx.x * P::COLS;
+  double y[ALPHA][NU][P::E1];
 #pragma unroll
   for (int j = 0; j < ALPHA; ++j) {
-    const bool ok = lo + j < L;  // a short last digit converts fewer primes
-    ld.y[j] = it.y + (size_t)(ok ? lo + j : lo) * n;
-    ld.h[j] = ok ? hat[((size_t)i * ALPHA + j) * np + t] : 0.0;
-    ld.hp[j] = ld.h[j] * ld.qinv;
+    if (j < nl) {
+      const int pj = lo + j;
+      const double q = pr[pj].q, qinv = pr[pj].qinv;
+      const double* __restrict__ w = twa_i + (size_t)pj * 256;
+      const double* __restrict__ a = it.y + (size_t)pj * n;
+#pragma unroll
+      for (int v = 0; v < NU2; ++v) {
+        const int u = threadIdx.x + 256 * v;
+        const int c = u % P::COLS, hh = u / P::COLS;
+        double x[P::E2];
+#pragma unroll
+        for (int m = 0; m < P::E2; ++m) x[m] = a[((size_t)((hh << P::S2) + m) << 8) + col0 + c];
+#pragma unroll
+        for (int s2 = P::S2 - 1; s2 >= 0; --s2) {
+          const int st = P::S1 + s2, half = P::E2 >> (s2 + 1);
+#pragma unroll
+          for (int m = 0; m < P::E2; ++m) {
+            if (m & half) continue;
+            gs_bfly(x[m], x[m + half], w[(1 << st) + (hh << s2) + (m >> (P::S2 - s2))], q, qinv);
+          }
+        }
+#pragma unroll
+        for (int m = 0; m < P::E2; ++m) sm[((hh << P::S2) + m) * P::COLS + c] = x[m];
+      }
+      __syncthreads();
+      const double sc = scale[pj], scp = sc * qinv;
+#pragma unroll
+      for (int v = 0; v < NU; ++v) {
+        const int u = threadIdx.x + 256 * v;
+        const int c = u % P::COLS, hl = u / P::COLS;
+        double x[P::E1];
+#pragma unroll
+        for (int m = 0; m < P::E1; ++m) x[m] = sm[(hl + (m << P::S2)) * P::COLS + c];
+#pragma unroll
+        for (int st = P::S1 - 1; st >= 0; --st) {
+          const int half = P::E1 >> (st + 1);
+#pragma unroll
+          for (int m = 0; m < P::E1; ++m) {
+            if (m & half) continue;
+            gs_bfly(x[m], x[m + half], w[(1 << st) + (m >> (P::S1 - st))], q, qinv);
+          }
+        }
+#pragma unroll
+        for (int m = 0; m < P::E1; ++m) y[j][v][m] = canon_full(mulc(x[m], sc, scp, q), q, qinv);
+      }
+      __syncthreads();  // the next limb reuses the LDS tile
+    } else {
+#pragma unroll
+      for (int v = 0; v < NU; ++v)
+#pragma unroll
+        for (int m = 0; m < P::E1; ++m) y[j][v][m] = 0.0;
+    }
   }
-  fwd_a_body<SA>(ld, it.ext + ((size_t)i * np + t) * n, twa + (size_t)t * 256, ld.q, ld.qinv, blockIdx.x * P::COLS,
-                 sm);
+#pragma unroll 1
+  for (int k = k0; k < k0 + per && k < np - nl; ++k) {
+    const int t = k < lo ? k : k + nl;  // the k-th prime outside the digit (own limbs: read from c1 directly)
+    const double q = pr[t].q, qinv = pr[t].qinv;
+    double h[ALPHA], hp[ALPHA];
+#pragma unroll
+    for (int j = 0; j < ALPHA; ++j) {
+      h[j] = j < nl ? hat[((size_t)i * ALPHA + j) * np + t] : 0.0;
+      hp[j] = h[j] * qinv;
+    }
+    const double* __restrict__ w = twa_f + (size_t)t * 256;
+    double* __restrict__ a = it.ext + ((size_t)i * np + t) * n;
+#pragma unroll
+    for (int v = 0; v < NU; ++v) {
+      const int u = threadIdx.x + 256 * v;
+      const int c = u % P::COLS, hl = u / P::COLS;
+      double x[P::E1];
+#pragma unroll
+      for (int m = 0; m < P::E1; ++m) {
+        double acc = 0.0;
+#pragma unroll
+        for (int j = 0; j < ALPHA; ++j) acc += mulc(y[j][v][m], h[j], hp[j], q);
+        x[m] = reduce(acc, q, qinv);
+      }
+#pragma unroll
+      for (int st = 0; st < P::S1; ++st) {
+        const int half = P::E1 >> (st + 1);
+#pragma unroll
+        for (int m = 0; m < P::E1; ++m) {
+          if (m & half) continue;
+          if (st & 1) ct_bfly<true>(x[m], x[m + half], w[(1 << st) + (m >> (P::S1 - st))], q, qinv);
+          else ct_bfly<false>(x[m], x[m + half], w[(1 << st) + (m >> (P::S1 - st))], q, qinv);
+        }
+      }
+#pragma unroll
+      for (int m = 0; m < P::E1; ++m) sm[(hl + (m << P::S2)) * P::COLS + c] = x[m];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int v = 0; v < NU2; ++v) {
+      const int u = threadIdx.x + 256 * v;
+      const int c = u % P::COLS, hh = u / P::COLS;
+      double x[P::E2];
+#pragma unroll
+      for (int m = 0; m < P::E2; ++m) x[m] = sm[((hh << P::S2) + m) * P::COLS + c];
+#pragma unroll
+      for (int s2 = 0; s2 < P::S2; ++s2) {
+        const int st = P::S1 + s2, half = P::E2 >> (s2 + 1);
+#pragma unroll
+        for (int m = 0; m < P::E2; ++m) {
+          if (m & half) continue;
+          if (st & 1) ct_bfly<true>(x[m], x[m + half], w[(1 << st) + (hh << s2) + (m >> (P::S2 - s2))], q, qinv);
+          else ct_bfly<false>(x[m], x[m + half], w[(1 << st) + (hh << s2) + (m >> (P::S2 - s2))], q, qinv);
+        }
+      }
+#pragma unroll
+      for (int m = 0; m < P::E2; ++m) a[((size_t)((hh << P::S2) + m) << 8) + col0 + c] = x[m];
+    }
+    __syncthreads();  // the next prime reuses the LDS tile
+  }
 }
 
 // ModDown, first pass: conv[t] = pass A of Conv_{P -> q_t}(y_P), where y_P
@@ -1588,6 +1709,12 @@ void ntt_inv_a(const fa_ctx* c, const LimbList& l, hipStream_t s) {
   if (l.n == 0) return;
   FA_SA_SWITCH(launch_inv_a, c, l, s)
 }
+void ntt_inv_b(const fa_ctx* c, const LimbList& l, hipStream_t s) {
+  if (l.n == 0) return;
+  const int rows = (c->n >> 8) < 16 ? (c->n >> 8) : 16;
+  dim3 gb((c->n >> 8) / rows, l.n);
+  hipLaunchKernelGGL(k_ntt_inv_b, gb, dim3(256), 0, s, l, c->d_pr, c->d_twt_inv, c->d_twr_inv, c->logn);
+}
 
 static void strided(const fa_ctx* c, double* base, size_t stride, int count, int period, int prime_off,
                     hipStream_t s, bool fwd) {
@@ -1604,32 +1731,51 @@ void ntt_inv_strided(const fa_ctx* c, double* base, size_t stride, int count, in
   strided(c, base, stride, count, period, prime_off, s, false);
 }
 
+// target groups of a fused ModUp launch: a launch of at least 256 workgroups
+// keeps one group per digit (the repeated inverse passes of more groups cost
+// more than they gain there); a smaller one (one ciphertext) is split to about
+// FA_MU_WGS (default 512) workgroups, at most one group per target
+static int modup_groups(int wgs, int targets) {
+  static const int want = [] {
+    const char* e = getenv("FA_MU_WGS");
+    return e && atoi(e) > 0 ? atoi(e) : 512;
+  }();
+  if (wgs >= 256) return 1;
+  const int g = (want + wgs - 1) / wgs;
+  return g < 1 ? 1 : g > targets ? targets : g;
+}
 template <int SA, int ALPHA>
-static void launch_modup_a(const fa_ctx* c, const MuArgs& a, int count, hipStream_t s) {
+static void launch_modup_fused(const fa_ctx* c, const MuArgs& a, int count, hipStream_t s) {
   using P = PassA<SA>;
-  dim3 g(c->n / P::TILE, c->dnum * c->np, count);
-  hipLaunchKernelGGL((k_modup_a<SA, ALPHA>), g, dim3(256), 0, s, a, c->d_pr, c->d_twa_fwd, c->d_mu_hat, c->logn,
-                     c->L, c->np);
+  const int ngrp = modup_groups(c->n / P::TILE * c->dnum * count, c->np - ALPHA);
+  dim3 g(c->n / P::TILE, c->dnum * ngrp, count);
+  hipLaunchKernelGGL((k_modup_fused<SA, ALPHA>), g, dim3(256), 0, s, a, c->d_pr, c->d_twa_fwd, c->d_twa_inv,
+                     c->d_mu_hat, c->d_mu_scale, c->logn, c->L, c->np, ngrp);
 }
 template <int SA>
-static void launch_modup_a_sa(const fa_ctx* c, const MuArgs& a, int count, hipStream_t s) {
+static void launch_modup_fused_sa(const fa_ctx* c, const MuArgs& a, int count, hipStream_t s) {
   switch (c->alpha) {
-    case 1: launch_modup_a<SA, 1>(c, a, count, s); break;
-    case 2: launch_modup_a<SA, 2>(c, a, count, s); break;
-    case 3: launch_modup_a<SA, 3>(c, a, count, s); break;
-    case 4: launch_modup_a<SA, 4>(c, a, count, s); break;
+    case 1: launch_modup_fused<SA, 1>(c, a, count, s); break;
+    case 2: launch_modup_fused<SA, 2>(c, a, count, s); break;
+    case 3: launch_modup_fused<SA, 3>(c, a, count, s); break;
+    case 4: launch_modup_fused<SA, 4>(c, a, count, s); break;
     default: break;
   }
 }
 
-void modup_ntt(const fa_ctx* c, const MuItem* items, int count, hipStream_t s, bool pass_b) {
+static void modup_pass_b(const fa_ctx* c, const MuItem* items, int count, hipStream_t s);
+
+void modup_fused(const fa_ctx* c, const MuItem* items, int count, hipStream_t s, bool pass_b) {
   for (int off = 0; off < count; off += FA_MAXMU) {
     const int m = count - off < FA_MAXMU ? count - off : FA_MAXMU;
     MuArgs a;
     for (int i = 0; i < m; ++i) a.it[i] = items[off + i];
-    FA_SA_SWITCH(launch_modup_a_sa, c, a, m, s)
+    FA_SA_SWITCH(launch_modup_fused_sa, c, a, m, s)
   }
-  if (!pass_b) return;
+  if (pass_b) modup_pass_b(c, items, count, s);
+}
+
+static void modup_pass_b(const fa_ctx* c, const MuItem* items, int count, hipStream_t s) {
   // second pass over every converted limb
   LimbList l;
   l.n = 0;
@@ -1869,6 +2015,15 @@ static bool mac_three_stages() {
   return v;
 }
 
+// pairs per pass of a four-query group: 8 (default) or 16 (FA_MAC_Q4_PAIRS)
+static int mac_q4_pairs() {
+  static const int v = [] {
+    const char* e = getenv("FA_MAC_Q4_PAIRS");
+    return e && atoi(e) == 16 ? 16 : 8;
+  }();
+  return v;
+}
+
 static int mac_pairs_max() {
   static const int v = [] {
     const char* e = getenv("FA_MAC_PAIRS");
@@ -1949,7 +2104,7 @@ void mac_diag(const fa_ctx* c, const double* const* q, const double* const* qrot
       a.logG = logG;
       a.L = c->L;
       for (int p0 = 0; p0 < a.n_pairs;) {
-        if (m == 4) p0 = mac_chunks<4, 8>(a, p0, c, s);
+        if (m == 4) p0 = mac_q4_pairs() == 16 ? mac_chunks<4, 16>(a, p0, c, s) : mac_chunks<4, 8>(a, p0, c, s);
         else if (m == 2) p0 = pmax >= 32 ? mac_chunks<2, 16>(a, p0, c, s) : mac_chunks<2, 8>(a, p0, c, s);
         else if (pmax >= 32) p0 = mac_chunks<1, 32>(a, p0, c, s);
         else if (pmax >= 16) p0 = mac_chunks<1, 16>(a, p0, c, s);
