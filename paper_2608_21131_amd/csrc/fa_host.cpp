@@ -373,6 +373,7 @@ void fa_ctx_destroy(fa_ctx* c) {
   (void)hipFree(c->d_mu_hat);
   (void)hipFree(c->d_md_hat);
   (void)hipFree(c->d_mu_scale);
+  (void)hipFree(c->d_md_scale);
   (void)hipFree(c->d_s);
   for (auto& kv : c->keys) (void)hipFree(kv.second);
   (void)hipFree(c->d_rlk);
@@ -505,6 +506,7 @@ static int ctx_build(const fa_params* prm, const std::vector<u64>& primes, fa_ct
       (rc = dev_alloc(&c->d_twt_inv, twt_i.size())) || (rc = dev_alloc(&c->d_twr_fwd, twr_f.size())) ||
       (rc = dev_alloc(&c->d_twr_inv, twr_i.size())) || (rc = dev_alloc(&c->d_mu_hat, mu_hat.size())) ||
       (rc = dev_alloc(&c->d_md_hat, md_hat.size())) || (rc = dev_alloc(&c->d_mu_scale, (size_t)L)) ||
+      (rc = dev_alloc(&c->d_md_scale, (size_t)K)) ||
       (rc = dev_alloc(&c->d_s, (size_t)np * n))) {
     fa_ctx_destroy(c);
     return rc;
@@ -523,6 +525,7 @@ static int ctx_build(const fa_params* prm, const std::vector<u64>& primes, fa_ct
   up(c->d_mu_hat, mu_hat);
   up(c->d_md_hat, md_hat);
   up(c->d_mu_scale, c->h_mu_scale);
+  up(c->d_md_scale, c->h_md_scale);
   if (e == hipSuccess) e = hipMemset(c->d_s, 0, (size_t)np * n * 8);
   if (e != hipSuccess) {
     fa_ctx_destroy(c);
@@ -1337,18 +1340,20 @@ static void modup(fa_ctx* c, const double* cts, size_t ct_stride, int batch, dou
 
 // ModDown of `count` polynomials u_i = u + i * np * N over Q u P (NTT form):
 // out_i = bases_i[pi_gal_i] + (u_i,Q - Conv_{P->Q}(u_i,P)) * P^-1.  The special-
-// prime limbs of u are overwritten (scaled coefficients); conv is scratch.
-// With pass_b false only the special-prime inverse and the conversion's first
-// pass run (bases, outs and gals unused): moddown_ks finishes.
+// prime limbs of u are overwritten (the row pass of their inverse transform;
+// inv_b_done: already done by the caller); conv is scratch.  With pass_b
+// false only the special-prime inverse and the conversion's first pass run
+// (bases, outs and gals unused): moddown_ks finishes.
 static void moddown_polys(fa_ctx* c, double* u, int count, double* conv, const double* const* bases,
                           double* const* outs, const uint32_t* gals, hipStream_t s, bool pass_b = true,
                           bool inv_b_done = false) {
   const size_t n = c->n, L = c->L, np = c->np;
-  {
-    fa::LimbBatch inv(c, s, false, inv_b_done);
+  if (!inv_b_done) {
+    // the row pass of the inverse transform, in place; the fused ModDown
+    // kernel finishes it
+    fa::LimbBatch inv(c, s, false, false, true);
     for (int i = 0; i < count; ++i)
-      for (int k = 0; k < c->K; ++k)
-        inv.add(u + (size_t)i * np * n + (L + k) * n, (int)L + k, nullptr, c->h_md_scale[k]);
+      for (int k = 0; k < c->K; ++k) inv.add(u + (size_t)i * np * n + (L + k) * n, (int)L + k);
   }
   std::vector<fa::MdItem> it(count);
   for (int i = 0; i < count; ++i) {
@@ -1356,7 +1361,7 @@ static void moddown_polys(fa_ctx* c, double* u, int count, double* conv, const d
     it[i] = {ui + L * n, conv + (size_t)i * L * n, ui, pass_b ? bases[i] : nullptr, pass_b ? outs[i] : nullptr,
              pass_b ? gals[i] : 1u};
   }
-  fa::moddown(c, it.data(), count, s, pass_b);
+  fa::moddown_fused(c, it.data(), count, s, pass_b);
 }
 
 // Key switch and ModDown of `count` rotations: outs[j] = (c0s[j][pi] + ModDown(u_0),

@@ -63,6 +63,7 @@ struct fa_ctx {
   double* d_mu_hat = nullptr;     // [dnum][alpha][np]   (D_i/d_j) mod prime t
   double* d_md_hat = nullptr;     // [K][L]              (P/p_k) mod q_t
   double* d_mu_scale = nullptr;   // [L] device copy of h_mu_scale
+  double* d_md_scale = nullptr;   // [K] device copy of h_md_scale
   // host copies used to build per-limb constants
   std::vector<double> h_ninv;     // [np] N^-1 mod prime
   std::vector<double> h_mu_scale; // [L] N^-1 (D_i/q_t)^-1 mod q_t, t in digit i
@@ -143,6 +144,10 @@ struct MdItem {
 };
 // pass_b false: conversion and first forward pass only (conv is left for moddown_ks)
 void moddown(const fa_ctx* c, const MdItem* items, int count, hipStream_t s, bool pass_b = true);
+// The same from yP after the first (row) pass of its inverse transform only:
+// one kernel finishes the inverse (column pass and the (P/p_k)^-1 N^-1
+// scaling), converts and runs the first forward pass of every target limb.
+void moddown_fused(const fa_ctx* c, const MdItem* items, int count, hipStream_t s, bool pass_b = true);
 
 // ModDown finish of rotations whose key-switch sum on the ciphertext primes is
 // formed in the same kernel (ks_inner then only covers the special primes):

@@ -190,44 +190,39 @@ struct MuArgs {
   fa::MuItem it[FA_MAXMU];
 };
 
-// ModUp from the row-passed c1, fused: a workgroup owns one column tile of
-// one digit i.  It finishes the inverse transform of the digit's limbs on
-// that tile (column pass, then the scaling by N^-1 (D_i/d_j)^-1, leaving
-// canonical residues, exactly as k_ntt_inv_a does) and keeps the results in
-// registers; then for every prime t outside the digit it forms the fast basis
+// Fused basis conversion from row-passed sources: a workgroup owns one column
+// tile of one source group (a digit of c1 for ModUp, the special primes for
+// ModDown).  It finishes the inverse transform of the group's limbs on that
+// tile (column pass, then the scaling by N^-1 times the conversion factor,
+// leaving canonical residues, exactly as k_ntt_inv_a does) and keeps the
+// results in registers; then for every target prime it forms the fast basis
 // conversion of the tile (as ConvLd does) and runs the first forward pass on
-// it (as fwd_a_body does), writing ext[i][t].  Each source word is read once
-// and the coefficients never leave the chip.  With ngrp > 1 the targets of a
-// digit are split into ngrp contiguous groups, one per workgroup (each group
-// repeats the inverse pass): small launches get more workgroups.
-template <int SA, int ALPHA>
-__global__ __launch_bounds__(256) void k_modup_fused(MuArgs args, const DevPrime* __restrict__ pr,
-                                                     const double* __restrict__ twa_f,
-                                                     const double* __restrict__ twa_i,
-                                                     const double* __restrict__ hat,
-                                                     const double* __restrict__ scale, int logn, int L, int np,
-                                                     int ngrp) {
+// it (as fwd_a_body does).  Each source word is read once and the
+// coefficients never leave the chip.  With ngrp > 1 the targets are split
+// into ngrp contiguous groups, one per workgroup (each group repeats the
+// inverse pass): small launches get more workgroups.
+//
+// Src describes the group: nl source limbs src(j) over primes sprime(j) with
+// scales scale(j); ntarget targets, the k-th over prime target(k), with
+// conversion factors hat(j, t), written to out(t).
+template <int SA, int NS, class Src>
+__device__ __forceinline__ void conv_fused_body(const Src& sr, const DevPrime* __restrict__ pr,
+                                                const double* __restrict__ twa_f, const double* __restrict__ twa_i,
+                                                int grp, int ngrp, double* sm) {
   using P = PassA<SA>;
   constexpr int NU = P::TILE / P::E1 / 256;   // tile units per thread in the E1 layout
   constexpr int NU2 = P::TILE / P::E2 / 256;  // ... in the E2 layout
   static_assert(NU * P::E1 * 256 == P::TILE && NU2 * P::E2 * 256 == P::TILE, "whole units per thread");
-  __shared__ double sm[P::TILE];
-  const int i = blockIdx.y / ngrp, grp = blockIdx.y % ngrp;
-  const fa::MuItem& it = args.it[blockIdx.z];
-  const int n = 1 << logn;
-  const int lo = i * ALPHA;
-  const int nl = L - lo < ALPHA ? L - lo : ALPHA;  // a short last digit has fewer limbs
-  const int per = (np - nl + ngrp - 1) / ngrp;      // targets of this group: k0 <= k < k0 + per
-  const int k0 = grp * per;
+  const int nl = sr.nl;
   const int col0 = blockIdx.x * P::COLS;
-  double y[ALPHA][NU][P::E1];
+  double y[NS][NU][P::E1];
 #pragma unroll
-  for (int j = 0; j < ALPHA; ++j) {
+  for (int j = 0; j < NS; ++j) {
     if (j < nl) {
-      const int pj = lo + j;
+      const int pj = sr.sprime(j);
       const double q = pr[pj].q, qinv = pr[pj].qinv;
       const double* __restrict__ w = twa_i + (size_t)pj * 256;
-      const double* __restrict__ a = it.y + (size_t)pj * n;
+      const double* __restrict__ a = sr.src(j);
 #pragma unroll
       for (int v = 0; v < NU2; ++v) {
         const int u = threadIdx.x + 256 * v;
@@ -248,7 +243,7 @@ __global__ __launch_bounds__(256) void k_modup_fused(MuArgs args, const DevPrime
         for (int m = 0; m < P::E2; ++m) sm[((hh << P::S2) + m) * P::COLS + c] = x[m];
       }
       __syncthreads();
-      const double sc = scale[pj], scp = sc * qinv;
+      const double sc = sr.scale(j), scp = sc * qinv;
 #pragma unroll
       for (int v = 0; v < NU; ++v) {
         const int u = threadIdx.x + 256 * v;
@@ -276,18 +271,20 @@ __global__ __launch_bounds__(256) void k_modup_fused(MuArgs args, const DevPrime
         for (int m = 0; m < P::E1; ++m) y[j][v][m] = 0.0;
     }
   }
+  const int per = (sr.ntarget + ngrp - 1) / ngrp;  // targets of this group: k0 <= k < k0 + per
+  const int k0 = grp * per;
 #pragma unroll 1
-  for (int k = k0; k < k0 + per && k < np - nl; ++k) {
-    const int t = k < lo ? k : k + nl;  // the k-th prime outside the digit (own limbs: read from c1 directly)
+  for (int k = k0; k < k0 + per && k < sr.ntarget; ++k) {
+    const int t = sr.target(k);
     const double q = pr[t].q, qinv = pr[t].qinv;
-    double h[ALPHA], hp[ALPHA];
+    double h[NS], hp[NS];
 #pragma unroll
-    for (int j = 0; j < ALPHA; ++j) {
-      h[j] = j < nl ? hat[((size_t)i * ALPHA + j) * np + t] : 0.0;
+    for (int j = 0; j < NS; ++j) {
+      h[j] = j < nl ? sr.hat(j, t) : 0.0;
       hp[j] = h[j] * qinv;
     }
     const double* __restrict__ w = twa_f + (size_t)t * 256;
-    double* __restrict__ a = it.ext + ((size_t)i * np + t) * n;
+    double* __restrict__ a = sr.out(t);
 #pragma unroll
     for (int v = 0; v < NU; ++v) {
       const int u = threadIdx.x + 256 * v;
@@ -297,7 +294,7 @@ __global__ __launch_bounds__(256) void k_modup_fused(MuArgs args, const DevPrime
       for (int m = 0; m < P::E1; ++m) {
         double acc = 0.0;
 #pragma unroll
-        for (int j = 0; j < ALPHA; ++j) acc += mulc(y[j][v][m], h[j], hp[j], q);
+        for (int j = 0; j < NS; ++j) acc += mulc(y[j][v][m], h[j], hp[j], q);
         x[m] = reduce(acc, q, qinv);
       }
 #pragma unroll
@@ -334,8 +331,62 @@ __global__ __launch_bounds__(256) void k_modup_fused(MuArgs args, const DevPrime
 #pragma unroll
       for (int m = 0; m < P::E2; ++m) a[((size_t)((hh << P::S2) + m) << 8) + col0 + c] = x[m];
     }
-    __syncthreads();  // the next prime reuses the LDS tile
+    __syncthreads();  // the next target reuses the LDS tile
   }
+}
+
+// ModUp sources: digit i of c1, converted to every prime outside the digit
+// (own limbs are read from c1 directly by the key-switch kernels)
+struct MuSrc {
+  const double* y;     // [L][N], row pass of the inverse done
+  double* ext;         // [dnum][np][N]
+  const double* hatt;  // [dnum][alpha][np]
+  const double* sct;   // [L]
+  int i, alpha, lo, nl, n, np, ntarget;
+  __device__ const double* src(int j) const { return y + (size_t)(lo + j) * n; }
+  __device__ int sprime(int j) const { return lo + j; }
+  __device__ double scale(int j) const { return sct[lo + j]; }
+  __device__ int target(int k) const { return k < lo ? k : k + nl; }
+  __device__ double hat(int j, int t) const { return hatt[((size_t)i * alpha + j) * np + t]; }
+  __device__ double* out(int t) const { return ext + ((size_t)i * np + t) * n; }
+};
+// ModDown sources: the K special-prime limbs, converted to the L ciphertext primes
+struct MdSrc {
+  const double* yP;    // [K][N], row pass of the inverse done
+  double* conv;        // [L][N]
+  const double* hatt;  // [K][L]
+  const double* sct;   // [K]
+  int L, nl, n, ntarget;
+  __device__ const double* src(int j) const { return yP + (size_t)j * n; }
+  __device__ int sprime(int j) const { return L + j; }
+  __device__ double scale(int j) const { return sct[j]; }
+  __device__ int target(int k) const { return k; }
+  __device__ double hat(int j, int t) const { return hatt[(size_t)j * L + t]; }
+  __device__ double* out(int t) const { return conv + (size_t)t * n; }
+};
+
+template <int SA, int ALPHA>
+__global__ __launch_bounds__(256) void k_modup_fused(MuArgs args, const DevPrime* __restrict__ pr,
+                                                     const double* __restrict__ twa_f,
+                                                     const double* __restrict__ twa_i,
+                                                     const double* __restrict__ hat,
+                                                     const double* __restrict__ scale, int logn, int L, int np,
+                                                     int ngrp) {
+  __shared__ double sm[PassA<SA>::TILE];
+  const fa::MuItem& it = args.it[blockIdx.z];
+  MuSrc sr;
+  sr.y = it.y;
+  sr.ext = it.ext;
+  sr.hatt = hat;
+  sr.sct = scale;
+  sr.i = blockIdx.y / ngrp;
+  sr.alpha = ALPHA;
+  sr.lo = sr.i * ALPHA;
+  sr.nl = L - sr.lo < ALPHA ? L - sr.lo : ALPHA;  // a short last digit has fewer limbs
+  sr.n = 1 << logn;
+  sr.np = np;
+  sr.ntarget = np - sr.nl;
+  conv_fused_body<SA, ALPHA>(sr, pr, twa_f, twa_i, blockIdx.y % ngrp, ngrp, sm);
 }
 
 // ModDown, first pass: conv[t] = pass A of Conv_{P -> q_t}(y_P), where y_P
@@ -363,6 +414,27 @@ __global__ __launch_bounds__(256) void k_moddown_a(MdArgs args, const DevPrime* 
     ld.hp[k] = ld.h[k] * ld.qinv;
   }
   fwd_a_body<SA>(ld, it.conv + (size_t)t * n, twa + (size_t)t * 256, ld.q, ld.qinv, blockIdx.x * P::COLS, sm);
+}
+
+template <int SA, int KP>
+__global__ __launch_bounds__(256, 2) void k_moddown_fused(MdArgs args, const DevPrime* __restrict__ pr,
+                                                       const double* __restrict__ twa_f,
+                                                       const double* __restrict__ twa_i,
+                                                       const double* __restrict__ hat,
+                                                       const double* __restrict__ scale, int logn, int L,
+                                                       int ngrp) {
+  __shared__ double sm[PassA<SA>::TILE];
+  const fa::MdItem& it = args.it[blockIdx.z];
+  MdSrc sr;
+  sr.yP = it.yP;
+  sr.conv = it.conv;
+  sr.hatt = hat;
+  sr.sct = scale;
+  sr.L = L;
+  sr.nl = KP;
+  sr.n = 1 << logn;
+  sr.ntarget = L;
+  conv_fused_body<SA, KP>(sr, pr, twa_f, twa_i, blockIdx.y, ngrp, sm);
 }
 
 // inverse pass A (the last pass of the inverse transform): columns; the final
@@ -1817,6 +1889,38 @@ static void launch_moddown_a_sa(const fa_ctx* c, const MdArgs& a, int count, hip
     case 3: launch_moddown_a<SA, 3>(c, a, count, s); break;
     case 4: launch_moddown_a<SA, 4>(c, a, count, s); break;
     default: break;
+  }
+}
+
+template <int SA, int KP>
+static void launch_moddown_fused(const fa_ctx* c, const MdArgs& a, int count, hipStream_t s) {
+  using P = PassA<SA>;
+  const int ngrp = modup_groups(c->n / P::TILE * count, c->L);
+  dim3 g(c->n / P::TILE, ngrp, count);
+  hipLaunchKernelGGL((k_moddown_fused<SA, KP>), g, dim3(256), 0, s, a, c->d_pr, c->d_twa_fwd, c->d_twa_inv,
+                     c->d_md_hat, c->d_md_scale, c->logn, c->L, ngrp);
+}
+template <int SA>
+static void launch_moddown_fused_sa(const fa_ctx* c, const MdArgs& a, int count, hipStream_t s) {
+  switch (c->K) {
+    case 1: launch_moddown_fused<SA, 1>(c, a, count, s); break;
+    case 2: launch_moddown_fused<SA, 2>(c, a, count, s); break;
+    case 3: launch_moddown_fused<SA, 3>(c, a, count, s); break;
+    case 4: launch_moddown_fused<SA, 4>(c, a, count, s); break;
+    default: break;
+  }
+}
+
+void moddown_fused(const fa_ctx* c, const MdItem* items, int count, hipStream_t s, bool pass_b) {
+  const int rows = (c->n >> 8) < 16 ? (c->n >> 8) : 16;
+  for (int off = 0; off < count; off += FA_MAXMD) {
+    const int m = count - off < FA_MAXMD ? count - off : FA_MAXMD;
+    MdArgs a;
+    for (int i = 0; i < m; ++i) a.it[i] = items[off + i];
+    FA_SA_SWITCH(launch_moddown_fused_sa, c, a, m, s)
+    if (!pass_b) continue;
+    dim3 gb((c->n >> 8) / rows, c->L, m);
+    hipLaunchKernelGGL(k_moddown_b, gb, dim3(256), 0, s, a, c->d_pr, c->d_twt_fwd, c->d_twr_fwd, c->logn);
   }
 }
 
