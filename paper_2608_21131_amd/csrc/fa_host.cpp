@@ -1328,7 +1328,7 @@ static void modup(fa_ctx* c, const double* cts, size_t ct_stride, int batch, dou
   const size_t n = c->n, L = c->L;
   {
     // the row pass of the inverse transform; the fused ModUp kernel finishes it
-    fa::LimbBatch inv(c, s, false, false, true);
+    fa::LimbBatch inv(c, s, false, true);
     for (int b = 0; b < batch; ++b)
       for (size_t t = 0; t < L; ++t)
         inv.add(y + (size_t)b * y_stride + t * n, (int)t, cts + (size_t)b * ct_stride + (L + t) * n);
@@ -1351,7 +1351,7 @@ static void moddown_polys(fa_ctx* c, double* u, int count, double* conv, const d
   if (!inv_b_done) {
     // the row pass of the inverse transform, in place; the fused ModDown
     // kernel finishes it
-    fa::LimbBatch inv(c, s, false, false, true);
+    fa::LimbBatch inv(c, s, false, true);
     for (int i = 0; i < count; ++i)
       for (int k = 0; k < c->K; ++k) inv.add(u + (size_t)i * np * n + (L + k) * n, (int)L + k);
   }

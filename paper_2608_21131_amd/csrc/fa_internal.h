@@ -102,8 +102,6 @@ namespace fa {
 void* static_scratch(int device, hipError_t* err);
 void ntt_fwd(const fa_ctx* c, const LimbList& l, hipStream_t s);
 void ntt_inv(const fa_ctx* c, const LimbList& l, hipStream_t s);
-// the second (column) pass of the inverse transform alone, ptr in place
-void ntt_inv_a(const fa_ctx* c, const LimbList& l, hipStream_t s);
 // the first (row) pass of the inverse transform alone, src -> ptr
 void ntt_inv_b(const fa_ctx* c, const LimbList& l, hipStream_t s);
 
@@ -131,11 +129,14 @@ struct MuItem {
 void modup_fused(const fa_ctx* c, const MuItem* items, int count, hipStream_t s, bool pass_b = true);
 
 // ModDown with its finish: out = base[pi_gal] + (uQ - NTT(Conv_{P->Q}(yP))) * P^-1,
-// where yP ([K][N]) holds the special-prime coefficients of the key-switch
-// product already multiplied by (P/p_k)^-1 (canonical); conv is scratch.
+// where yP ([K][N]) holds the special-prime limbs of the key-switch product
+// after the first (row) pass of their inverse transform.  One kernel finishes
+// the inverse (column pass and the scaling by N^-1 (P/p_k)^-1, canonical),
+// converts and runs the first forward pass of every target limb into conv
+// (scratch); a second finishes the forward transform and the formula.
 #define FA_MAXMD 32
 struct MdItem {
-  const double* yP;    // [K][N]
+  const double* yP;    // [K][N], row pass of the inverse done
   double* conv;        // [L][N] scratch
   const double* uQ;    // [L][N] NTT form
   const double* base;  // [L][N] or null
@@ -143,10 +144,6 @@ struct MdItem {
   uint32_t gal;        // permutation of base (1 = none)
 };
 // pass_b false: conversion and first forward pass only (conv is left for moddown_ks)
-void moddown(const fa_ctx* c, const MdItem* items, int count, hipStream_t s, bool pass_b = true);
-// The same from yP after the first (row) pass of its inverse transform only:
-// one kernel finishes the inverse (column pass and the (P/p_k)^-1 N^-1
-// scaling), converts and runs the first forward pass of every target limb.
 void moddown_fused(const fa_ctx* c, const MdItem* items, int count, hipStream_t s, bool pass_b = true);
 
 // ModDown finish of rotations whose key-switch sum on the ciphertext primes is
@@ -265,10 +262,10 @@ void dec_combine(const fa_ctx* c, const double* ct, double* out, hipStream_t s);
 struct LimbBatch {
   const fa_ctx* c;
   hipStream_t s;
-  bool fwd, a_only, b_only;  // inverse: a_only the second pass alone (in place), b_only the first alone
+  bool fwd, b_only;  // inverse: b_only the first (row) pass alone, src -> ptr
   LimbList l;
-  LimbBatch(const fa_ctx* c_, hipStream_t s_, bool fwd_, bool a_only_ = false, bool b_only_ = false)
-      : c(c_), s(s_), fwd(fwd_), a_only(a_only_), b_only(b_only_) {
+  LimbBatch(const fa_ctx* c_, hipStream_t s_, bool fwd_, bool b_only_ = false)
+      : c(c_), s(s_), fwd(fwd_), b_only(b_only_) {
     l.n = 0;
   }
   // scale < 0: N^-1 of the prime
@@ -282,7 +279,6 @@ struct LimbBatch {
   void flush() {
     if (l.n) {
       if (fwd) ntt_fwd(c, l, s);
-      else if (a_only) ntt_inv_a(c, l, s);
       else if (b_only) ntt_inv_b(c, l, s);
       else ntt_inv(c, l, s);
       l.n = 0;

@@ -115,21 +115,6 @@ struct PlainLd {
   const double* src;
   __device__ double operator()(size_t i) const { return src[i]; }
 };
-// fast basis conversion of NS canonical inputs y_j = [x_j (S/s_j)^-1]_{s_j}
-// into the target prime: sum_j y_j * ((S/s_j) mod q)   (lazily reduced)
-template <int NS>
-struct ConvLd {
-  const double* y[NS];
-  double h[NS], hp[NS];
-  double q, qinv;
-  __device__ double operator()(size_t i) const {
-    double acc = 0.0;
-#pragma unroll
-    for (int j = 0; j < NS; ++j) acc += mulc(y[j][i], h[j], hp[j], q);
-    return reduce(acc, q, qinv);
-  }
-};
-
 template <int SA, class Ld>
 __device__ __forceinline__ void fwd_a_body(const Ld& ld, double* a, const double* __restrict__ w, double q,
                                            double qinv, int col0, double* sm) {
@@ -389,32 +374,10 @@ __global__ __launch_bounds__(256) void k_modup_fused(MuArgs args, const DevPrime
   conv_fused_body<SA, ALPHA>(sr, pr, twa_f, twa_i, blockIdx.y % ngrp, ngrp, sm);
 }
 
-// ModDown, first pass: conv[t] = pass A of Conv_{P -> q_t}(y_P), where y_P
-// holds the scaled special-prime coefficients of the key-switch product.
+// ModDown, first pass: conv[t] = pass A of Conv_{P -> q_t}(y_P).
 struct MdArgs {
   fa::MdItem it[FA_MAXMD];
 };
-
-template <int SA, int KP>
-__global__ __launch_bounds__(256) void k_moddown_a(MdArgs args, const DevPrime* __restrict__ pr,
-                                                   const double* __restrict__ twa, const double* __restrict__ hat,
-                                                   int logn, int L) {
-  using P = PassA<SA>;
-  __shared__ double sm[P::TILE];
-  const int t = blockIdx.y;
-  const fa::MdItem& it = args.it[blockIdx.z];
-  const int n = 1 << logn;
-  ConvLd<KP> ld;
-  ld.q = pr[t].q;
-  ld.qinv = pr[t].qinv;
-#pragma unroll
-  for (int k = 0; k < KP; ++k) {
-    ld.y[k] = it.yP + (size_t)k * n;
-    ld.h[k] = hat[(size_t)k * L + t];
-    ld.hp[k] = ld.h[k] * ld.qinv;
-  }
-  fwd_a_body<SA>(ld, it.conv + (size_t)t * n, twa + (size_t)t * 256, ld.q, ld.qinv, blockIdx.x * P::COLS, sm);
-}
 
 template <int SA, int KP>
 __global__ __launch_bounds__(256, 2) void k_moddown_fused(MdArgs args, const DevPrime* __restrict__ pr,
@@ -1771,16 +1734,6 @@ void ntt_inv(const fa_ctx* c, const LimbList& l, hipStream_t s) {
   FA_SA_SWITCH(launch_inv, c, l, s)
 }
 
-template <int SA>
-static void launch_inv_a(const fa_ctx* c, const LimbList& l, hipStream_t s) {
-  using P = PassA<SA>;
-  dim3 ga(c->n / P::TILE, l.n);
-  hipLaunchKernelGGL(k_ntt_inv_a<SA>, ga, dim3(256), 0, s, l, c->d_pr, c->d_twa_inv);
-}
-void ntt_inv_a(const fa_ctx* c, const LimbList& l, hipStream_t s) {
-  if (l.n == 0) return;
-  FA_SA_SWITCH(launch_inv_a, c, l, s)
-}
 void ntt_inv_b(const fa_ctx* c, const LimbList& l, hipStream_t s) {
   if (l.n == 0) return;
   const int rows = (c->n >> 8) < 16 ? (c->n >> 8) : 16;
@@ -1875,24 +1828,6 @@ static void modup_pass_b(const fa_ctx* c, const MuItem* items, int count, hipStr
 }
 
 template <int SA, int KP>
-static void launch_moddown_a(const fa_ctx* c, const MdArgs& a, int count, hipStream_t s) {
-  using P = PassA<SA>;
-  dim3 g(c->n / P::TILE, c->L, count);
-  hipLaunchKernelGGL((k_moddown_a<SA, KP>), g, dim3(256), 0, s, a, c->d_pr, c->d_twa_fwd, c->d_md_hat, c->logn,
-                     c->L);
-}
-template <int SA>
-static void launch_moddown_a_sa(const fa_ctx* c, const MdArgs& a, int count, hipStream_t s) {
-  switch (c->K) {
-    case 1: launch_moddown_a<SA, 1>(c, a, count, s); break;
-    case 2: launch_moddown_a<SA, 2>(c, a, count, s); break;
-    case 3: launch_moddown_a<SA, 3>(c, a, count, s); break;
-    case 4: launch_moddown_a<SA, 4>(c, a, count, s); break;
-    default: break;
-  }
-}
-
-template <int SA, int KP>
 static void launch_moddown_fused(const fa_ctx* c, const MdArgs& a, int count, hipStream_t s) {
   using P = PassA<SA>;
   const int ngrp = modup_groups(c->n / P::TILE * count, c->L);
@@ -1924,18 +1859,6 @@ void moddown_fused(const fa_ctx* c, const MdItem* items, int count, hipStream_t 
   }
 }
 
-void moddown(const fa_ctx* c, const MdItem* items, int count, hipStream_t s, bool pass_b) {
-  const int rows = (c->n >> 8) < 16 ? (c->n >> 8) : 16;
-  for (int off = 0; off < count; off += FA_MAXMD) {
-    const int m = count - off < FA_MAXMD ? count - off : FA_MAXMD;
-    MdArgs a;
-    for (int i = 0; i < m; ++i) a.it[i] = items[off + i];
-    FA_SA_SWITCH(launch_moddown_a_sa, c, a, m, s)
-    if (!pass_b) continue;
-    dim3 gb((c->n >> 8) / rows, c->L, m);
-    hipLaunchKernelGGL(k_moddown_b, gb, dim3(256), 0, s, a, c->d_pr, c->d_twt_fwd, c->d_twr_fwd, c->logn);
-  }
-}
 
 // 1-D grid of the key-switch kernels: nx * ny * ngroup work units, padded to
 // whole groups of eight per query when nq > 1 (see ks_decode)
