@@ -29,6 +29,12 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+# fp64 vector rate of the MI355X: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz = 39.3e12 lane-operations
+# per second (78.6 TFLOP/s counting an FMA as two).  A modular product of two residues in this
+# library's exact fp64 arithmetic is 6 of them (product, its FMA error term, quotient estimate,
+# rounding, FMA correction, sum), so the ALU roofline of the key-switch phases is 6.55e12 products/s.
+FP64_LANE_OPS = 256 * 4 * 16 * 2.4e9
+MODMUL_PEAK = FP64_LANE_OPS / 6
 METRIC = "encrypted candidate scores/sec + ms/level at 110k x 512-dim, one MI355X"
 
 
@@ -829,6 +835,34 @@ def run_three_level(bn, args):
                                                n_scores=n_scores)))
 
 
+def keyswitch_modmuls(n, L, K, dnum, alpha, B, G, nb):
+    """Modular products of the baby and giant phases of one query's level, counted from the
+    algorithm (not from the kernels): an NTT or inverse NTT of one limb is (N/2) log2 N butterflies,
+    one product each, plus N scalings for an inverse; a fast basis conversion is one product per
+    source limb per target word; a key-switch inner product is two per digit per word."""
+    import math
+    lg = int(math.log2(n))
+    ntt = n // 2 * lg            # one forward transform of a limb
+    intt = ntt + n               # one inverse transform with its final scaling
+    np_ = L + K
+    conv_up = dnum * (np_ - alpha)           # converted limbs of one ModUp (alpha sources each)
+    modup = L * intt + conv_up * (alpha * n + ntt)
+    moddown = 2 * (K * intt + L * (K * n + ntt) + L * n)   # both polynomials, with the P^-1 finish
+    # baby: one ModUp of the query, then per rotation the key products over all primes and a ModDown
+    baby = modup + (B - 1) * (dnum * np_ * n * 2 + moddown)
+    # giant: per (block, giant) pair a ModUp and the key products (plus P c0); one ModDown per block
+    pairs = nb * (G - 1)
+    giant = pairs * (modup + dnum * np_ * n * 2 + L * n) + nb * moddown
+    return baby, giant
+
+
+def alu_roofline(modmuls, ms, label):
+    achieved = modmuls / (ms * 1e-3)
+    return {"bound": "alu", "achieved": round(achieved / 1e9, 1), "peak": round(MODMUL_PEAK / 1e9, 1),
+            "unit": "Gmodmul/s", "frac": round(achieved / MODMUL_PEAK, 4), "modmuls": int(modmuls),
+            "phase": label, "avg_ms": round(ms, 4)}
+
+
 def measured_traffic(path):
     """HBM bytes per launch of the multiply-accumulate kernel from the committed counter summary, or None
     when the summary is missing or the kernel source changed since it was taken."""
@@ -844,6 +878,24 @@ def measured_traffic(path):
     if mac_source_sha256() != mh.group(1):
         return None
     return int(mb.group(1))
+
+
+LEVEL_TRAFFIC = os.path.join(ROOT, "profiles", "rerank110k_level_traffic.md")
+
+
+def measured_level_traffic(path=LEVEL_TRAFFIC):
+    """Calibrated HBM bytes (FETCH_SIZE + WRITE_SIZE) of every dispatch of one rerank level from the
+    committed counter summary, or None when it is missing or the library sources changed since."""
+    import re
+    from paper_2608_21131_amd.rocprof_summary import sources_sha256
+    if not os.path.exists(path):
+        return None
+    txt = open(path).read()
+    got = {k: re.search(rf"{k}: ([0-9a-f]+)", txt) for k in
+           ("level_read_bytes", "level_write_bytes", "level_traffic_bytes", "sources_sha256")}
+    if not all(got.values()) or got["sources_sha256"].group(1) != sources_sha256():
+        return None
+    return {k: int(got[k].group(1)) for k in ("level_read_bytes", "level_write_bytes", "level_traffic_bytes")}
 
 
 MAC_KERNEL = "k_mac_diag3"  # the single-query launches of the rerank level (three steps in flight)
@@ -1111,11 +1163,29 @@ def main():
         "phases_ms": {k: round(v, 4) for k, v in r["phases"].items()},
         "level_hbm_floor_ms": round(floor_ms, 4),
         "level_frac_of_hbm_roofline": round(floor_ms / ms, 4),
+        "level_traffic": None,
         "max_abs_score_err": r["err"],
         "transfers_outside_timing": r.get("io"),
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
+    if (w.name in ("rerank", "fine") and not args.level and r["phases"].get("baby_ms")
+            and r["phases"].get("giant_ms")):
+        # the key-switch phases against the fp64 ALU roofline (modular products per second); the
+        # digits hold K primes each (alpha = K), dnum = ceil(L / K)
+        dnum = -(-w.L // w.K)
+        bmm, gmm = keyswitch_modmuls(w.n, w.L, w.K, dnum, w.K, w.B, w.G, w.n_blocks)
+        res["keyswitch_alu"] = {"baby": alu_roofline(bmm, r["phases"]["baby_ms"], "baby rotations"),
+                                "giant": alu_roofline(gmm, r["phases"]["giant_ms"], "giant steps")}
+    if w.name == "rerank" and w.B == 64 and not args.level:
+        lt = measured_level_traffic()
+        if lt:
+            # every dispatch of one level, counted by rocprofv3 (profiles/rerank110k_level_traffic.md)
+            fl = lt["level_traffic_bytes"] / (HBM_PEAK_GBS * 1e9) * 1e3
+            res["level_traffic"] = {"bytes": lt["level_traffic_bytes"], "read_bytes": lt["level_read_bytes"],
+                                    "write_bytes": lt["level_write_bytes"], "floor_ms": round(fl, 4),
+                                    "frac_of_floor": round(fl / ms, 4),
+                                    "source": "profiles/rerank110k_level_traffic.md"}
     if r.get("enc_projection"):
         res["enc_projection"] = r["enc_projection"]
     if w.name == "three_level":
