@@ -17,6 +17,9 @@ PARAMS = {
     "p1": (13, 3, 1),
     "p2": (15, 8, 2),
     "p4": (16, 12, 3),
+    # short last digits (fewer limbs than alpha) and the remaining transform splits
+    "s12": (12, 5, 2),     # digits of 2, 2, 1 primes
+    "s14": (14, 7, 4),     # digits of 4, 3 primes
 }
 
 
