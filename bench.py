@@ -385,7 +385,7 @@ def run_membership(bn, args):
            "levels": f"{w.L} -> {L}", "tau": x["tau"], "chebyshev_degree": x["degree"],
            "sign_steps": x["iters"], "database_bytes": 8 * nb * R * c11.L * w.n,
            "paper_warm_latency_s_context": 7.0,
-           "roofline": roofline_of("k_mac_diag", mac_batch_bytes(1, nb * (R // B), B, c11.L * w.n), sm),
+           "roofline": roofline_of(MAC_KERNEL, mac_batch_bytes(1, nb * (R // B), B, c11.L * w.n), sm),
            "cpu_baseline": None if args.no_cpu_baseline else cpu_baseline_membership(bn, w, s, q, Xr)}
     if not args.no_check:
         ctw = c11.ct_words
