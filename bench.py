@@ -137,6 +137,18 @@ class Bench:
         torch.cuda.synchronize()
         return ev0.elapsed_time(ev1) / steps
 
+    def phases(self, step_fn, ctx, n=3):
+        """The library's phase split (baby / MAC / giant), from n further steps each followed by its
+        (synchronising) read.  The timed steps run back to back without it: a read after every step
+        would hold the host until the GPU drains, and the next step's first launches would start late."""
+        ctx.profile(True)
+        out = []
+        for _ in range(n):
+            step_fn()
+            out.append(ctx.profile_read())
+        ctx.profile(False)
+        return {k: float(np.mean([p[k] for p in out])) for k in out[0]}
+
 
 def pad(v, d):
     out = np.zeros(d)
@@ -167,17 +179,14 @@ def run_diag_level(bn, args):
         tot = src.sum()  # 1 GiB read, nothing but the scalar written
         bn.torch.cuda.synchronize()
         del src, dst, tot
-    ctx.profile(True)
-    phases = []
 
     def step():
         if ctx is not top:
             top.drop_level(ctx, q_top, out=q)
         ctx.score_block(q, blocks, w.d, fa.LAYOUT_DIAG, w.B, out=out, ws=ws)
-        phases.append(ctx.profile_read())
 
     ms = bn.timed(step, args.steps, args.warmup)
-    ph = {k: float(np.mean([p[k] for p in phases[args.warmup:]])) for k in phases[0]}
+    ph = bn.phases(step, ctx)
     err = None
     if not args.no_check:
         err = 0.0
@@ -274,17 +283,14 @@ def run_enc_level(bn, args, level):
     q = ctx.new_ct() if ctx is not top else q_top
     out = ctx.new_ct(w.n_blocks)
     ws = ctx.workspace(fa.OP_SCORE_ENC, w.n_blocks, w.d, w.B)
-    ctx.profile(True)
-    phases = []
 
     def step():
         if ctx is not top:
             top.drop_level(ctx, q_top, out=q)
         ctx.score_block(q, blocks, w.d, fa.LAYOUT_DIAG_ENC, w.B, out=out, ws=ws)
-        phases.append(ctx.profile_read())
 
     ms = bn.timed(step, args.steps, args.warmup)
-    ph = {k: float(np.mean([p[k] for p in phases[args.warmup:]])) for k in phases[0]}
+    ph = bn.phases(step, ctx)
     err = None
     if not args.no_check:
         err = 0.0
@@ -528,7 +534,7 @@ def run_batch_level(bn, args, r, nq):
     ws_p = ctx.prepare_batch_workspace(nq, w.B)
     ws_b = ctx.batch_workspace(nq, w.n_blocks, w.d, w.B)
     stream = torch.cuda.current_stream()
-    marks, phases = [], []
+    marks = []
 
     def step():
         e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
@@ -541,14 +547,14 @@ def run_batch_level(bn, args, r, nq):
         ctx.score_batch(qs, preps, blocks, w.d, w.B, outs=outs, ws=ws_b)
         e2.record(stream)
         marks.append((e0, e1, e2))
-        phases.append(ctx.profile_read())
 
     ms = bn.timed(step, args.steps, args.warmup)
     torch.cuda.synchronize()
     prep_ms = float(np.mean([a.elapsed_time(b) for a, b, _ in marks[args.warmup:]]))
     score_ms = float(np.mean([b.elapsed_time(c) for _, b, c in marks[args.warmup:]]))
-    mac_ms = float(np.mean([p["mac_ms"] for p in phases[args.warmup:]]))
-    giant_ms = float(np.mean([p["giant_ms"] for p in phases[args.warmup:]]))
+    ph = bn.phases(step, ctx)
+    mac_ms = ph["mac_ms"]
+    giant_ms = ph["giant_ms"]
     err = None
     if not args.no_check:
         err = 0.0
