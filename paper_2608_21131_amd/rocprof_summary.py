@@ -2,6 +2,7 @@
 
     python -m paper_2608_21131_amd.rocprof_summary traffic FETCH.csv WRITE.csv
     python -m paper_2608_21131_amd.rocprof_summary trace KERNEL_TRACE.csv
+    python -m paper_2608_21131_amd.rocprof_summary valu VALUBUSY.csv
 
 `traffic` takes the counter_collection.csv of two `rocprofv3 --pmc FETCH_SIZE` /
 `--pmc WRITE_SIZE` runs of `bench.py --copy-calib ...`.  The run's calibration
@@ -10,7 +11,8 @@ each counter: the fill writes 1 GiB, the copy reads and writes 1 GiB, the sum
 reads 1 GiB.  The level is the span of dispatches after the second-to-last
 multiply-accumulate launch up to and including the last one: one giant-step
 phase, one baby-step phase and one multiply-accumulate, the same work as one
-timed step.  `trace` lists the kernels of the same span with their durations.
+timed step.  `trace` lists the kernels of the same span with their durations,
+`valu` their duration-weighted VALUBusy from a `--pmc VALUBusy` run.
 """
 import csv
 import hashlib
@@ -124,10 +126,27 @@ def trace(trace_csv):
     return "\n".join(out)
 
 
+def valu(valu_csv):
+    rows = _span(_rows(valu_csv))
+    agg = OrderedDict()
+    for r in rows:
+        us = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+        a = agg.setdefault(_name(r["Kernel_Name"]), [0, 0.0, 0.0])
+        a[0] += 1
+        a[1] += us
+        a[2] += us * float(r["Counter_Value"])
+    out = ["| kernel | launches | us (counter run) | VALUBusy |", "|---|---:|---:|---:|"]
+    for k, (cnt, us, w) in sorted(agg.items(), key=lambda kv: -kv[1][1]):
+        out.append(f"| {k} | {cnt} | {us:.1f} | {w / us:.1f}% |")
+    return "\n".join(out)
+
+
 if __name__ == "__main__":
     if len(sys.argv) == 4 and sys.argv[1] == "traffic":
         print(traffic(sys.argv[2], sys.argv[3]))
     elif len(sys.argv) == 3 and sys.argv[1] == "trace":
         print(trace(sys.argv[2]))
+    elif len(sys.argv) == 3 and sys.argv[1] == "valu":
+        print(valu(sys.argv[2]))
     else:
         raise SystemExit(__doc__)
