@@ -1286,7 +1286,7 @@ size_t baby_ws(const fa_ctx* c, int B) {
   return rup(L * n) + rup(dn * np * n) + lanes * rup(rb * 2 * np * n) + lanes * rup(rb * 2 * L * n);
 }
 // workspace of the baby rotations of n_q queries prepared together (the
-// rotated queries themselves are separate): one query's coefficient-form c1,
+// rotated queries themselves are separate): one query's row-passed c1,
 // every query's extended digits, and per lane the key-switch products and
 // conversions of one launch group (about as many rotations as baby_ws's group)
 int batch_steps(int nq) { return std::max(1, kRotBatch / std::max(1, nq)); }
@@ -1321,8 +1321,9 @@ size_t score_ws(const fa_ctx* c, int nb, int d, int B) {
 }  // namespace
 
 // Extended digits (NTT form) of the c1 of `batch` ciphertexts cts + b * ct_stride.
-// y (per item [L][N]) receives c1's coefficients times (D_i/q_t)^-1; ext receives
-// every converted limb.  The ciphertexts are only read.
+// y (per item [L][N]) receives c1 after the row pass of its inverse transform
+// (scratch); ext receives every converted limb (pass_b false: the first
+// forward pass only).  The ciphertexts are only read.
 static void modup(fa_ctx* c, const double* cts, size_t ct_stride, int batch, double* y, size_t y_stride,
                   double* ext, size_t ext_stride, hipStream_t s, bool pass_b = true) {
   const size_t n = c->n, L = c->L;
