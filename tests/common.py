@@ -20,6 +20,7 @@ PARAMS = {
     # short last digits (fewer limbs than alpha) and the remaining transform splits
     "s12": (12, 5, 2),     # digits of 2, 2, 1 primes
     "s14": (14, 7, 4),     # digits of 4, 3 primes
+    "d8": (13, 16, 2),     # eight digits, the most the key-switch kernels take
 }
 
 

@@ -55,7 +55,7 @@ def test_encrypt_decrypt_parity(name):
 
 @pytest.mark.parametrize("name,steps", [("tiny", [1, 3, 100]), ("tiny1", [1, 5]), ("small", [1, 7]),
                                         ("p1", [1, 64]), ("p2", [5]), ("p4", [1]), ("s12", [1, 9]),
-                                        ("s14", [1, 33])])
+                                        ("s14", [1, 33]), ("d8", [1, 17])])
 def test_rotation_parity(name, steps):
     p = pair(name)
     v = np.random.default_rng(3).uniform(-1, 1, p.par.slots)
@@ -115,6 +115,7 @@ def test_row_layout_then_rotate_sum(name, d, rows):
     ("p2", 128, 16, [3000]),
     ("s12", 64, 8, [700, 2048]),         # short last digit, N = 2^12
     ("s14", 128, 16, [5000]),            # short last digit with four-prime digits, N = 2^14
+    ("d8", 64, 8, [1500]),               # eight key-switch digits
 ])
 def test_diag_score_parity(name, d, B, rows_list):
     p = pair(name, wid=5)
