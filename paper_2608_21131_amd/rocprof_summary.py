@@ -3,6 +3,7 @@
     python -m paper_2608_21131_amd.rocprof_summary traffic FETCH.csv WRITE.csv
     python -m paper_2608_21131_amd.rocprof_summary trace KERNEL_TRACE.csv
     python -m paper_2608_21131_amd.rocprof_summary valu VALUBUSY.csv
+    python -m paper_2608_21131_amd.rocprof_summary waves SQ1.csv [SQ2.csv ...]
 
 `traffic` takes the counter_collection.csv of two `rocprofv3 --pmc FETCH_SIZE` /
 `--pmc WRITE_SIZE` runs of `bench.py --copy-calib ...`.  The run's calibration
@@ -13,6 +14,9 @@ multiply-accumulate launch up to and including the last one: one giant-step
 phase, one baby-step phase and one multiply-accumulate, the same work as one
 timed step.  `trace` lists the kernels of the same span with their durations,
 `valu` their duration-weighted VALUBusy from a `--pmc VALUBusy` run.
+`waves` sums SQ counters (one or more `--pmc SQ_...` runs, SQ_WAVE_CYCLES
+among them) over the same span and gives each as a fraction of the kernel's
+wave-cycles.
 """
 import csv
 import hashlib
@@ -52,10 +56,13 @@ def _name(k):
 
 
 def _span(rows):
-    mac = [i for i, r in enumerate(rows) if MAC in r["Kernel_Name"]]
+    """Rows of the dispatches after the second-to-last multiply-accumulate launch up to the last one
+    (a counter file holds one row per counter per dispatch)."""
+    key = "Dispatch_Id" if "Dispatch_Id" in rows[0] else "Start_Timestamp"
+    mac = sorted({int(r[key]) for r in rows if MAC in r["Kernel_Name"]})
     if len(mac) < 2:
         raise SystemExit("need at least two multiply-accumulate launches (a warm-up and a timed step)")
-    return rows[mac[-2] + 1:mac[-1] + 1]
+    return [r for r in rows if mac[-2] < int(r[key]) <= mac[-1]]
 
 
 def _calib(rows, counter):
@@ -141,6 +148,27 @@ def valu(valu_csv):
     return "\n".join(out)
 
 
+def waves(*csvs):
+    agg = OrderedDict()
+    names = []
+    for path in csvs:
+        for r in _span(_rows(path)):
+            c = r["Counter_Name"]
+            if c not in names:
+                names.append(c)
+            agg.setdefault(_name(r["Kernel_Name"]), {}).setdefault(c, 0.0)
+            agg[_name(r["Kernel_Name"])][c] += float(r["Counter_Value"])
+    if "SQ_WAVE_CYCLES" not in names:
+        raise SystemExit("SQ_WAVE_CYCLES is needed as the denominator")
+    cols = [c for c in names if c != "SQ_WAVE_CYCLES"]
+    out = ["| kernel | " + " | ".join(c.replace("SQ_", "") for c in cols) + " |",
+           "|---|" + "---:|" * len(cols)]
+    for k, v in sorted(agg.items(), key=lambda kv: -kv[1].get("SQ_WAVE_CYCLES", 0.0)):
+        wc = v.get("SQ_WAVE_CYCLES", 0.0) or 1.0
+        out.append(f"| {k} | " + " | ".join(f"{v.get(c, 0.0) / wc:.2f}" for c in cols) + " |")
+    return "\n".join(out)
+
+
 if __name__ == "__main__":
     if len(sys.argv) == 4 and sys.argv[1] == "traffic":
         print(traffic(sys.argv[2], sys.argv[3]))
@@ -148,5 +176,7 @@ if __name__ == "__main__":
         print(trace(sys.argv[2]))
     elif len(sys.argv) == 3 and sys.argv[1] == "valu":
         print(valu(sys.argv[2]))
+    elif len(sys.argv) >= 3 and sys.argv[1] == "waves":
+        print(waves(*sys.argv[2:]))
     else:
         raise SystemExit(__doc__)

@@ -66,3 +66,17 @@ def test_trace_lists_the_level_span(tmp_path):
     txt = rs.trace(str(tmp_path / "t.csv"))
     assert "| k_ntt_inv_b | 1 |" in txt and "| k_giant_ks | 1 |" in txt and "| k_mac_diag3 | 1 |" in txt
     assert "k_warm" not in txt
+
+
+def test_waves_normalises_by_wave_cycles_over_the_level(tmp_path):
+    # two counters per dispatch, as rocprofv3 writes them: one row per counter
+    path = tmp_path / "sq.csv"
+    with open(path, "w", newline="") as f:
+        w = csv.writer(f)
+        w.writerow(HEAD)
+        disp = [("k_mac_diag3<32>", 8.0, 100.0), ("k_giant_ks<4, 16>", 30.0, 100.0), ("k_mac_diag3<32>", 40.0, 100.0)]
+        for i, (name, wait, cyc) in enumerate(disp):
+            for c, v in (("SQ_WAIT_ANY", wait), ("SQ_WAVE_CYCLES", cyc)):
+                w.writerow([i + 1, i + 1, 64, name, c, v, 1000 * i, 1000 * i + 500])
+    txt = rs.waves(str(path))
+    assert "| k_giant_ks | 0.30 |" in txt and "| k_mac_diag3 | 0.40 |" in txt
