@@ -107,7 +107,7 @@ def test_row_layout_then_rotate_sum(name, d, rows):
     ("tiny", 16, 16, [100]),
     ("tiny", 512, 8, [300]),    # d = N/2 (the widest block), G = 64 > 32 giants per giant-kernel launch
     ("tiny", 512, 64, [512]),   # d = N/2 with a full block of rows
-    ("tiny", 16, 4, [512] * 9 + [5]),   # 10 blocks: the giant steps in two chunks of blocks
+    ("tiny", 16, 4, [512] * 16 + [5]),  # 17 blocks: the giant steps in two chunks of blocks
     ("tiny", 16, 4, [64] * 33),          # 33 blocks: more than one multiply-accumulate launch holds
     ("tiny1", 16, 4, [300, 512]),        # one digit: the fused special-prime kernel
     ("tiny1", 64, 8, [512]),
