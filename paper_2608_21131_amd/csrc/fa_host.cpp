@@ -1285,11 +1285,18 @@ size_t baby_ws(const fa_ctx* c, int B) {
   const size_t lanes = lanes_wanted();
   return rup(L * n) + rup(dn * np * n) + lanes * rup(rb * 2 * np * n) + lanes * rup(rb * 2 * L * n);
 }
+// baby steps per launch group of a query batch: 64 rotations per group from
+// four queries on (16, 32, 64, 128 measured; 64 keeps the workspace near
+// 2 GB per lane), kRotBatch for fewer queries so that one or two still fill
+// both lanes
+int batch_steps(int nq) {
+  nq = std::max(1, nq);
+  return std::max(1, (nq >= 4 ? 64 : kRotBatch) / nq);
+}
 // workspace of the baby rotations of n_q queries prepared together (the
 // rotated queries themselves are separate): one query's row-passed c1,
 // every query's extended digits, and per lane the key-switch products and
-// conversions of one launch group (about as many rotations as baby_ws's group)
-int batch_steps(int nq) { return std::max(1, kRotBatch / std::max(1, nq)); }
+// conversions of one launch group (batch_steps(n_q) x n_q rotations)
 size_t baby_batch_ws(const fa_ctx* c, int nq, int B) {
   const size_t n = c->n, L = c->L, np = c->np, dn = c->dnum;
   const size_t items = (size_t)std::max(1, std::min(batch_steps(nq), B - 1)) * nq;
