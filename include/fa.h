@@ -343,8 +343,9 @@ int fa_score_prepared(fa_ctx* ctx, const fa_buf* q, const fa_buf* prep, const fa
  * and Future Work" applied to the baby rotations): preps[j] receives exactly
  * what fa_prepare_query(qs[j], baby_step) writes, for j < n_q.  The key
  * switches of one baby step are issued for the queries of a group together
- * (groups of at most 16 queries), so a rotation key read from HBM for one
- * query is found in the caches by the others.  qs[j] device ciphertexts,
+ * (groups of at most 16 queries; from four queries on a launch group holds
+ * 64 rotations), so a rotation key read from HBM for one query is found in
+ * the caches by the others.  qs[j] device ciphertexts,
  * preps[j] device, fa_prepared_bytes(ctx, baby_step) bytes each; workspace
  * fa_prepare_batch_workspace_bytes(n_q, baby_step) bytes (it grows with the
  * group size: every query's extended digits).  Errors: FA_E_INVAL (null
@@ -364,9 +365,11 @@ int fa_prepare_batch(fa_ctx* ctx, const fa_buf* qs, int n_q, int baby_step, fa_b
  * pass over the plaintexts serves up to four queries, so the plaintext stream
  * is read once per four queries instead of once per query.  outs[j] (device,
  * n_blocks ciphertexts) is bit-identical to fa_score_prepared(qs[j],
- * preps[j], ...).  Workspace: fa_batch_workspace_bytes(n_q, n_blocks, d,
- * baby_step) bytes (the accumulators of all n_q queries plus one query's
- * giant-step scratch).  Errors as fa_score_prepared; FA_E_SHAPE if n_q < 1. */
+ * preps[j], ...).  The giant steps of all n_q queries then run together, over
+ * n_q * n_blocks blocks in chunks of up to 16.  Workspace:
+ * fa_batch_workspace_bytes(n_q, n_blocks, d, baby_step) bytes (the
+ * accumulators of all n_q queries plus the giant-step scratch of one chunk).
+ * Errors as fa_score_prepared; FA_E_SHAPE if n_q < 1. */
 size_t fa_batch_workspace_bytes(const fa_ctx* ctx, int n_q, int n_blocks, int d, int baby_step);
 int fa_score_batch(fa_ctx* ctx, const fa_buf* qs, const fa_buf* preps, int n_q, const fa_buf* blocks,
                    int n_resident, const int32_t* block_ids, int n_blocks, int d, int baby_step, fa_buf* outs,
