@@ -67,3 +67,28 @@ def test_random_parameter_sets(cfg):
         assert np.array_equal(got[i], p.orc.bsgs_block(qrot, pts, B, G, keys)), i
         z = p.ctx.decode(p.ctx.decrypt(out[i * p.ctx.ct_words:(i + 1) * p.ctx.ct_words]), 80)
         assert np.max(np.abs(z[:len(X)] - X @ q)) < 1e-4
+
+
+@pytest.mark.parametrize("cfg", SETS[:3], ids=[f"n{c[0]}-L{c[1]}-K{c[2]}-d{c[3]}-B{c[4]}" for c in SETS[:3]])
+def test_random_sets_query_batch(cfg):
+    """Five queries prepared together and scored in one batch against four blocks: 20 blocks of
+    giant steps (a 16-block chunk and a 4-block one), a four-query and a one-query plaintext pass.
+    Every output equals the single-query path word for word (that path is checked against the
+    oracle above)."""
+    logn, L, K, d, B, _, _ = cfg
+    name = f"sweep_{logn}_{L}_{K}"
+    PARAMS[name] = (logn, L, K)
+    p = Pair(name, wid=23)
+    S = p.par.slots
+    g = gen.rng(23, gen.STREAM_DB, d, B)
+    blocks = [p.ctx.encode_db_block_int(ckks.layout_b_coeffs(gen.gaussian_unit_rows(g, r, d), p.par, d, B))
+              for r in (S, S // 2, 7, S)]
+    p.keys(ckks.steps_for_bsgs(d, B), oracle=False)
+    qv = gen.gaussian_unit_rows(gen.rng(23, gen.STREAM_QUERY), 5, d)
+    cts = [p.encrypt_both(ckks.encode(ckks.replicate(v, S), p.n, 40), tag=30 + j)[0] for j, v in enumerate(qv)]
+    say(f"[sweep batch] N=2^{logn} L={L} K={K} d={d} B={B}: 5 queries x 4 blocks")
+    preps = p.ctx.prepare_batch(cts, B)
+    outs = p.ctx.score_batch(cts, preps, blocks, d, B)
+    for j in range(5):
+        single = p.ctx.score_block(cts[j], blocks, d, 1, B)
+        assert np.array_equal(p.export_ct(outs[j], 4), p.export_ct(single, 4)), j
