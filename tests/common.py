@@ -21,6 +21,9 @@ PARAMS = {
     "s12": (12, 5, 2),     # digits of 2, 2, 1 primes
     "s14": (14, 7, 4),     # digits of 4, 3 primes
     "d8": (13, 16, 2),     # eight digits, the most the key-switch kernels take
+    # the largest parameters the library takes, at the full ring size
+    "max8": (16, 16, 2),   # 16 ciphertext primes in eight digits
+    "max20": (16, 16, 4),  # 16 + 4: the most primes
 }
 
 

@@ -55,7 +55,8 @@ def test_encrypt_decrypt_parity(name):
 
 @pytest.mark.parametrize("name,steps", [("tiny", [1, 3, 100]), ("tiny1", [1, 5]), ("small", [1, 7]),
                                         ("p1", [1, 64]), ("p2", [5]), ("p4", [1]), ("s12", [1, 9]),
-                                        ("s14", [1, 33]), ("d8", [1, 17])])
+                                        ("s14", [1, 33]), ("d8", [1, 17]), ("max8", [1, 12345]),
+                                        ("max20", [3])])
 def test_rotation_parity(name, steps):
     p = pair(name)
     v = np.random.default_rng(3).uniform(-1, 1, p.par.slots)
@@ -116,6 +117,7 @@ def test_row_layout_then_rotate_sum(name, d, rows):
     ("s12", 64, 8, [700, 2048]),         # short last digit, N = 2^12
     ("s14", 128, 16, [5000]),            # short last digit with four-prime digits, N = 2^14
     ("d8", 64, 8, [1500]),               # eight key-switch digits
+    ("max8", 16, 4, [32768, 3000]),      # eight digits of 16 primes at N = 2^16
 ])
 def test_diag_score_parity(name, d, B, rows_list):
     p = pair(name, wid=5)
