@@ -19,6 +19,7 @@ from __future__ import annotations
 
 import argparse
 import json
+import math
 import os
 import sys
 import time
@@ -692,8 +693,11 @@ def run_three_level(bn, args):
     Queries run in groups of --batch (default 4): every query scores all coarse blocks,
     so a group's coarse level is one cross-query batch (one pass over the coarse
     plaintexts per group), and the group's queries are prepared together.  The fine and
-    rerank blocks differ per query and are scored one query at a time.  The client's decrypts run on a second stream, so its decode
-    and top-k of one query overlap the server's next level on the first."""
+    rerank blocks differ per query and are scored one query at a time.  The client's decrypts
+    run on a second stream, at the lowest level that holds the scores, so its decode and
+    top-k of one query overlap the server's next level on the first; the next group's
+    preparation and coarse pass are enqueued before the client takes this group's rerank
+    results."""
     w, fa, torch = bn.w, bn.fa, bn.torch
     top_ctx = bn.ctx
     level = args.level if args.level else w.L
@@ -733,6 +737,17 @@ def run_three_level(bn, args):
     ws_s = ctx.workspace(fa.OP_SCORE_PREPARED, max(ex["fine_blocks"], ex["rerank_blocks"]), w.d, w.B)
     sa = torch.cuda.current_stream()
     sb = torch.cuda.Stream()  # the client's decrypts (default priority)
+    # The client decrypts at the lowest level that still holds the scores: the decoder reads
+    # only the first primes that cover the scale (2^80) plus 22 bits, and a ciphertext reduced
+    # modulo a divisor of Q encrypts the same m + e, so the returned blocks are cut to those
+    # primes on the GPU first (fewer limbs to decrypt, transform and copy back; the decoded
+    # scores are identical).
+    bits, n_dec = 0.0, 0
+    while n_dec < ctx.L and bits < 80 + 22:
+        bits += math.log2(ctx.primes[n_dec])
+        n_dec += 1
+    dctx = ctx.at_level(n_dec) if n_dec < ctx.L else ctx
+    dbuf = dctx.new_ct(max(n_coarse, ex["fine_blocks"], ex["rerank_blocks"]))
     gpu_ms = []  # per query: [prepare, coarse, fine, rerank]
     errs = []
 
@@ -745,12 +760,13 @@ def run_three_level(bn, args):
         return e
 
     def top(ct, nb, k, rows_list, qv, done, n_rows_last=None):
-        # client side: wait for the level on the second stream, decrypt every block
-        # there, then decode the blocks on host threads and keep the top k
+        # client side: wait for the level on the second stream, cut the blocks to the
+        # decoder's primes and decrypt them there, then decode the blocks on host threads
+        # and keep the top k
         sb.wait_event(done)
-        W_ = ctx.ct_words
-        res = [ctx.decrypt(ct[b * W_:(b + 1) * W_], stream=sb) for b in range(nb)]
-        zs = list(pool.map(lambda r: ctx.decode(r, 80), res))
+        low = ct if dctx is ctx else ctx.drop_level(dctx, ct, out=dbuf.items(0, nb), stream=sb)
+        futs = [pool.submit(dctx.decode, dctx.decrypt(low.item(b), stream=sb), 80) for b in range(nb)]
+        zs = [f.result() for f in futs]
         scores = []
         for b in range(nb):
             z = zs[b]
@@ -761,24 +777,29 @@ def run_three_level(bn, args):
                 errs.append(float(np.max(np.abs(z[:n_valid] - ref))))
         return topk(np.concatenate(scores), k)
 
-    def group(i0, check):
+    def head(i0, check):
+        # server: the group's preparation and its coarse level (one cross-query pass)
         m = min(gq, nq - i0)
-        qv = [queries[i0 + j] if check else None for j in range(m)]
-        qi = []
+        g = {"m": m, "qv": [queries[i0 + j] if check else None for j in range(m)], "qi": []}
         e0 = ev()
         for j in range(m):
             if qs is not None:
                 top_ctx.drop_level(ctx, qcts[i0 + j], out=qs[j])
-                qi.append(qs[j])
+                g["qi"].append(qs[j])
             else:
-                qi.append(qcts[i0 + j])
-        ctx.prepare_batch(qi, w.B, outs=preps[:m], ws=ws_p)
+                g["qi"].append(qcts[i0 + j])
+        ctx.prepare_batch(g["qi"], w.B, outs=preps[:m], ws=ws_p)
         e1 = ev()
-        ctx.score_batch(qi, preps[:m], pools["coarse"], w.d, w.B, outs=outs_c[:m], ws=ws_b)
-        e2 = ev()
+        ctx.score_batch(g["qi"], preps[:m], pools["coarse"], w.d, w.B, outs=outs_c[:m], ws=ws_b)
+        g["e"] = (e0, e1, ev())
+        return g
+
+    def body(g):
+        # client top-k of the coarse and fine levels, each followed by the server's next level
+        m, qi, qv = g["m"], g["qi"], g["qv"]
         fine, rer = [], []
         for j in range(m):
-            ids = top(outs_c[j], n_coarse, ex["top_coarse"], rows_of["coarse"], qv[j], e2)
+            ids = top(outs_c[j], n_coarse, ex["top_coarse"], rows_of["coarse"], qv[j], g["e"][2])
             fsel = sorted(set(int(x) % ex["fine_pool_blocks"] for x in ids))
             fsel = (fsel + [b for b in range(ex["fine_pool_blocks"]) if b not in fsel])[:ex["fine_blocks"]]
             a = ev()
@@ -793,22 +814,36 @@ def run_three_level(bn, args):
             ctx.score_prepared(qi[j], preps[j], pools["rerank"], w.d, w.B, out=outs_r[j], ws=ws_s,
                                block_ids=rsel)
             rer.append((a, ev(), rsel))
+        g["fine"], g["rer"] = fine, rer
+
+    def tail(g):
+        # client top-k of the rerank level; then the group's server time from its events
+        m, fine, rer = g["m"], g["fine"], g["rer"]
         for j in range(m):
             rsel = rer[j][2]
-            top(outs_r[j], len(rsel), 10, [rows_of["rerank"][b] for b in rsel], qv[j], rer[j][1],
+            top(outs_r[j], len(rsel), 10, [rows_of["rerank"][b] for b in rsel], g["qv"][j], rer[j][1],
                 n_rows_last=ex["rerank_last"])
-        torch.cuda.synchronize()
+        rer[-1][1].synchronize()
+        e0, e1, e2 = g["e"]
         for j in range(m):
             gpu_ms.append([e0.elapsed_time(e1) / m, e1.elapsed_time(e2) / m, fine[j][0].elapsed_time(fine[j][1]),
                            rer[j][0].elapsed_time(rer[j][1])])
 
-    group(0, check=True)  # warm-up group, checked against float64
+    g0 = head(0, check=True)  # warm-up group, checked against float64
+    body(g0)
+    tail(g0)
     gpu_ms.clear()
     t = time.time()
     steps = max(1, args.steps)
-    for _ in range(steps):
-        for i0 in range(0, nq, gq):
-            group(i0, check=False)
+    starts = [i0 for _ in range(steps) for i0 in range(0, nq, gq)]
+    # groups back to back: the next group's preparation and coarse pass are enqueued before
+    # the client finishes this group's rerank results, so the GPU works while it does
+    g = head(starts[0], check=False)
+    for k in range(len(starts)):
+        body(g)
+        nxt = head(starts[k + 1], check=False) if k + 1 < len(starts) else None
+        tail(g)
+        g = nxt
     wall = (time.time() - t) / (steps * nq)
     lm = np.array(gpu_ms)
     gpu_q = float(lm.sum(axis=1).mean())
