@@ -727,8 +727,9 @@ def run_three_level(bn, args):
         f"({nblk * w.d * ctx.L * w.n * 8 / 1e9:.1f} GB), {gq} queries per coarse pass, {time.time() - bn.t0:.1f}s")
     queries = bn.wl.query_vectors(w, nq, centers)
     qcts = [bn.encrypt(qv, tag=i) for i, qv in enumerate(queries)]
-    qs = [ctx.new_ct() for _ in range(gq)] if ctx is not top_ctx else None
-    preps = [ctx.new_prep(w.B) for _ in range(gq)]
+    # two sets of per-query buffers: consecutive groups overlap on the GPU (see below)
+    qss = [[ctx.new_ct() for _ in range(gq)] for _ in range(2)] if ctx is not top_ctx else None
+    prepss = [[ctx.new_prep(w.B) for _ in range(gq)] for _ in range(2)]
     outs_c = [ctx.new_ct(n_coarse) for _ in range(gq)]
     outs_f = [ctx.new_ct(ex["fine_blocks"]) for _ in range(gq)]
     outs_r = [ctx.new_ct(ex["rerank_blocks"]) for _ in range(gq)]
@@ -777,15 +778,16 @@ def run_three_level(bn, args):
                 errs.append(float(np.max(np.abs(z[:n_valid] - ref))))
         return topk(np.concatenate(scores), k)
 
-    def head(i0, check):
+    def head(i0, check, slot):
         # server: the group's preparation and its coarse level (one cross-query pass)
         m = min(gq, nq - i0)
-        g = {"m": m, "qv": [queries[i0 + j] if check else None for j in range(m)], "qi": []}
+        preps = prepss[slot]
+        g = {"m": m, "qv": [queries[i0 + j] if check else None for j in range(m)], "qi": [], "preps": preps}
         e0 = ev()
         for j in range(m):
-            if qs is not None:
-                top_ctx.drop_level(ctx, qcts[i0 + j], out=qs[j])
-                g["qi"].append(qs[j])
+            if qss is not None:
+                top_ctx.drop_level(ctx, qcts[i0 + j], out=qss[slot][j])
+                g["qi"].append(qss[slot][j])
             else:
                 g["qi"].append(qcts[i0 + j])
         ctx.prepare_batch(g["qi"], w.B, outs=preps[:m], ws=ws_p)
@@ -794,10 +796,10 @@ def run_three_level(bn, args):
         g["e"] = (e0, e1, ev())
         return g
 
-    def body(g):
-        # client top-k of the coarse and fine levels, each followed by the server's next level
-        m, qi, qv = g["m"], g["qi"], g["qv"]
-        fine, rer = [], []
+    def body_fine(g):
+        # client top-k of the coarse level, each followed by the server's fine level
+        m, qi, qv, preps = g["m"], g["qi"], g["qv"], g["preps"]
+        fine = []
         for j in range(m):
             ids = top(outs_c[j], n_coarse, ex["top_coarse"], rows_of["coarse"], qv[j], g["e"][2])
             fsel = sorted(set(int(x) % ex["fine_pool_blocks"] for x in ids))
@@ -805,6 +807,12 @@ def run_three_level(bn, args):
             a = ev()
             ctx.score_prepared(qi[j], preps[j], pools["fine"], w.d, w.B, out=outs_f[j], ws=ws_s, block_ids=fsel)
             fine.append((a, ev(), fsel))
+        g["fine"] = fine
+
+    def body_rerank(g):
+        # client top-k of the fine level, each followed by the server's rerank level
+        m, qi, qv, preps, fine = g["m"], g["qi"], g["qv"], g["preps"], g["fine"]
+        rer = []
         for j in range(m):
             fsel = fine[j][2]
             ids = top(outs_f[j], len(fsel), ex["top_fine"], [rows_of["fine"][b] for b in fsel], qv[j], fine[j][1])
@@ -814,7 +822,7 @@ def run_three_level(bn, args):
             ctx.score_prepared(qi[j], preps[j], pools["rerank"], w.d, w.B, out=outs_r[j], ws=ws_s,
                                block_ids=rsel)
             rer.append((a, ev(), rsel))
-        g["fine"], g["rer"] = fine, rer
+        g["rer"] = rer
 
     def tail(g):
         # client top-k of the rerank level; then the group's server time from its events
@@ -829,19 +837,27 @@ def run_three_level(bn, args):
             gpu_ms.append([e0.elapsed_time(e1) / m, e1.elapsed_time(e2) / m, fine[j][0].elapsed_time(fine[j][1]),
                            rer[j][0].elapsed_time(rer[j][1])])
 
-    g0 = head(0, check=True)  # warm-up group, checked against float64
-    body(g0)
+    g0 = head(0, True, 0)  # warm-up group, checked against float64
+    body_fine(g0)
+    body_rerank(g0)
     tail(g0)
     gpu_ms.clear()
     t = time.time()
     steps = max(1, args.steps)
     starts = [i0 for _ in range(steps) for i0 in range(0, nq, gq)]
-    # groups back to back: the next group's preparation and coarse pass are enqueued before
-    # the client finishes this group's rerank results, so the GPU works while it does
-    g = head(starts[0], check=False)
+    # Groups overlap on the GPU, two deep.  Host order per group k: enqueue group k+1's
+    # preparation and coarse pass, take group k's fine results (enqueuing its rerank levels),
+    # take group k+1's coarse results (enqueuing its fine levels), take group k's rerank
+    # results.  The stream then runs ... fine(k), coarse(k+1), rerank(k), fine(k+1), ... while
+    # the client works on earlier results; the two groups in flight use separate query and
+    # preparation buffers.
+    g = head(starts[0], False, 0)
+    body_fine(g)
     for k in range(len(starts)):
-        body(g)
-        nxt = head(starts[k + 1], check=False) if k + 1 < len(starts) else None
+        nxt = head(starts[k + 1], False, (k + 1) % 2) if k + 1 < len(starts) else None
+        body_rerank(g)
+        if nxt is not None:
+            body_fine(nxt)
         tail(g)
         g = nxt
     wall = (time.time() - t) / (steps * nq)
@@ -851,7 +867,8 @@ def run_three_level(bn, args):
     # (outside the timed queries): the coarse level's batched pass and one rerank level
     ctx.profile(True)
     m = min(gq, nq)
-    qi = [qcts[j] for j in range(m)] if qs is None else qs[:m]
+    preps = prepss[0]
+    qi = [qcts[j] for j in range(m)] if qss is None else qss[0][:m]
     ctx.prepare_batch(qi, w.B, outs=preps[:m], ws=ws_p)
     ctx.score_batch(qi, preps[:m], pools["coarse"], w.d, w.B, outs=outs_c[:m], ws=ws_b)
     ph_c = ctx.profile_read()
