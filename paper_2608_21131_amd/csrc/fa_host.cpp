@@ -980,9 +980,11 @@ Garner make_garner(const fa_ctx* c, int nl) {
     }
   return g;
 }
-// the centred integer with residues res[t * stride] (t < nl), as a double
+// the centred integer with residues res[t * stride] (t < nl), as a double;
+// NL > 0 fixes the prime count at compile time (the loops unroll), NL = 0 reads it from g
+template <int NL = 0>
 inline double garner_to_double(const Garner& g, const uint64_t* res, size_t stride) {
-  const int nl = g.nl;
+  const int nl = NL > 0 ? NL : g.nl;
   int64_t a[kMaxGarner];
   for (int j = 0; j < nl; ++j) {
     const u64 qj = g.q[j];
@@ -1101,17 +1103,27 @@ int fa_decode(const fa_ctx* c, const uint64_t* res, int log_scale, double* out, 
   const FftTables& tb = fft_tables(n);
   const DecTables& dt = dec_tables(n);
   std::vector<double> re(h), im(h);
-  const int nw = std::max(1, std::min(8, h / 4096));
-  parallel_for(nw, [&](int w) {
-    for (int k = w; k < h; k += nw) {
-      const double lo = garner_to_double(g, res + k, (size_t)n);
-      const double hi = garner_to_double(g, res + k + h, (size_t)n);
+  // One host thread: a client decodes its result blocks several at a time, and
+  // threads started inside each decode made those concurrent calls several
+  // times slower than serial ones.
+  auto crt = [&](auto nlc) {
+    constexpr int NL = decltype(nlc)::value;
+    for (int k = 0; k < h; ++k) {
+      const double lo = garner_to_double<NL>(g, res + k, (size_t)n);
+      const double hi = garner_to_double<NL>(g, res + k + h, (size_t)n);
       const double cr = tb.twist[k].real(), ci = tb.twist[k].imag();
       const uint32_t kb = dt.brev[k];
       re[kb] = lo * cr - hi * ci;
       im[kb] = lo * ci + hi * cr;
     }
-  });
+  };
+  switch (nl) {
+    case 1: crt(std::integral_constant<int, 1>{}); break;
+    case 2: crt(std::integral_constant<int, 2>{}); break;
+    case 3: crt(std::integral_constant<int, 3>{}); break;
+    case 4: crt(std::integral_constant<int, 4>{}); break;
+    default: crt(std::integral_constant<int, 0>{}); break;
+  }
   fft_pos_brev_in(re.data(), im.data(), h, dt.twr.data(), dt.twi.data());
   const double inv_scale = std::ldexp(1.0, -log_scale);
   for (int j = 0; j < n_slots; ++j) out[j] = re[dt.slot_t[j]] * inv_scale;
