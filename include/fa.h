@@ -236,7 +236,9 @@ int fa_encode(const fa_ctx* ctx, const double* slots, int n_slots, int log_scale
  * 2^log_scale into n_slots real slot values (host): the client's reading of
  * its scores (Section 2 "The round trip").  The centred CRT uses the first
  * primes whose product exceeds 2^(log_scale + 22), which is exact for slot
- * values of magnitude below 2^12 (scores are cosines). */
+ * values of magnitude below 2^12 (scores are cosines).  Runs on the calling
+ * thread only and touches no device state: a client may decode several
+ * blocks at once from threads of its own. */
 int fa_decode(const fa_ctx* ctx, const uint64_t* res, int log_scale, double* out, int n_slots);
 
 /* ---- server: enrollment ------------------------------------------------- */
