@@ -502,6 +502,8 @@ def test_batch_rejects_bad_arguments():
     ("tiny", 16, 16, [100]),
     ("tiny", 16, 4, [32] * 33),  # 33 encrypted blocks: two ct x ct launches
     ("p1", 128, 16, [4096, 1000]),
+    ("p2", 128, 16, [3000]),     # four key-switch digits in the relinearisation and giant steps
+    ("s12", 64, 8, [700, 2048]),  # a short last digit
 ])
 def test_encrypted_block_score_parity(name, d, B, rows_list):
     """Encrypted database blocks (ct x ct, lazy relinearisation): the encrypted diagonals, and
